@@ -1,0 +1,198 @@
+/*
+ * scadles.h -- C ABI of the ScaDLES data-parallel hot path on MI355X (gfx950).
+ *
+ * The hot path of one training step of ScaDLES (Tyagi & Swany, "ScaDLES:
+ * Scalable Deep Learning over Streaming data at the Edge", arXiv 2301.08897):
+ * K simulated edge devices each hold a flat fp32 gradient of n elements in the
+ * HBM of one GPU. For every device the library
+ *   1. keeps the Top-k entries by magnitude (Top-k sparsification, §III-C and
+ *      §IV "High communication cost"), ties broken towards the lower index,
+ *      with k = clamp(floor(ratio * n), 1, n) (compression ratio CR, §V-G);
+ *   2. measures the energies ||g||^2 and ||Top-k(g)||^2 that drive the
+ *      adaptive compression rule of §IV (send Top-k(g) when the relative
+ *      energy loss is at most delta, else send g);
+ * then
+ *   3. aggregates all devices' (sparse or dense) gradients weighted by each
+ *      device's streaming rate, g~ = sum_j r_j g_j (Eqn 4b, weights of Eqn 4a);
+ *   4. applies the SGD update w <- w - eta_scaled * g~ (Eqn 4c).
+ *
+ * Conventions for every entry point:
+ *   - Pointers marked (dev) are device pointers owned by the caller; the
+ *     library never frees or retains them. Pointers marked (host) are host
+ *     memory read during the call only.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Every device-side effect is asynchronous on that stream; outputs are
+ *     valid once the stream has been synchronised.
+ *   - No entry point allocates device memory. Scratch space is the
+ *     caller-provided workspace `ws` of `ws_bytes` bytes (dev, 256-byte
+ *     aligned), sized by the matching *_workspace_bytes() query. A workspace
+ *     must not be shared by calls that may run concurrently.
+ *   - All arguments are validated on the host before anything is launched; an
+ *     invalid call returns a non-zero scadles_status, launches nothing, and
+ *     scadles_last_error() describes the problem.
+ *   - Gradients must be finite (NaN/Inf give unspecified results, never a
+ *     memory fault). Magnitude ranking uses the 31-bit key bits(g) & 0x7FFFFFFF,
+ *     so -0 and +0 rank equal and denormals are ranked exactly (no flushing).
+ *   - Results are deterministic: re-running a call on the same inputs gives
+ *     bit-identical outputs.
+ */
+#ifndef SCADLES_H
+#define SCADLES_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SCADLES_OK = 0,
+  SCADLES_EINVAL = 1,      /* invalid argument (NULL pointer, size, ratio, weight ...) */
+  SCADLES_EWORKSPACE = 2,  /* workspace NULL, misaligned or smaller than required     */
+  SCADLES_EHIP = 3,        /* the HIP runtime reported an error while launching        */
+  SCADLES_EUNSORTED = 4,   /* validation mode only: a sparse set's idx is not strictly
+                              ascending or holds an entry >= n                          */
+  SCADLES_EINTERNAL = 5    /* internal consistency check failed                        */
+} scadles_status;
+
+/* Largest number of devices one call accepts. */
+#define SCADLES_MAX_DEVICES 64
+
+/* One device's contribution to the weighted aggregation (Eqn 4b).
+ * Sparse: idx (dev, k entries, strictly ascending, each < n) and val (dev, k
+ * entries) hold the kept gradient entries; every other position is zero.
+ * Dense: idx == NULL and k == n; val (dev, n entries) is the full gradient.
+ * val must be 4-byte aligned; a dense val must be 16-byte aligned.          */
+typedef struct {
+  const uint32_t* idx;
+  const float* val;
+  uint64_t k;
+} scadles_sparse;
+
+/* Number of entries Top-k keeps for a vector of n elements at compression
+ * ratio `ratio` (§V-G: CR 0.1 keeps a tenth of the entries):
+ * k = clamp(floor(ratio * n), 1, n), computed in IEEE double.
+ * Returns 0 when n == 0, n > 2^32 - 1 or ratio is not in (0, 1].            */
+uint64_t scadles_topk_k(uint64_t n, double ratio);
+
+/* Workspace bytes needed by scadles_step_fused for K devices of n elements at
+ * the given per-device compression ratios (host[K]); scadles_topk_select uses
+ * K = 1. Returns 0 for arguments the calls would reject.                    */
+size_t scadles_workspace_bytes(uint32_t K, uint64_t n, const double* ratios);
+
+/* Workspace bytes needed by scadles_weighted_aggregate for K sets over n
+ * positions. Returns 0 for arguments the call would reject.                 */
+size_t scadles_aggregate_workspace_bytes(uint32_t K, uint64_t n);
+
+/* Top-k sparsification of one gradient (§IV "High communication cost";
+ * Top-k as in §III-C), with the energies of the adaptive rule.
+ *   grad      (dev, n floats, 16-byte aligned) the gradient; not modified.
+ *   n         1 <= n <= 2^32 - 1.
+ *   ratio     compression ratio in (0, 1]; k = scadles_topk_k(n, ratio).
+ *   idx, val  (dev, k entries each) receive the kept positions in strictly
+ *             ascending order and their signed values (bit copies of grad).
+ *             The kept set holds the k largest |grad|; among equal magnitudes
+ *             the lower index is kept.
+ *   energies  (dev, 2 doubles) or NULL: receives sum grad^2 and the sum over
+ *             the kept entries, both accumulated in double.
+ * Returns SCADLES_EINVAL for a NULL or misaligned pointer, n out of range or
+ * a ratio outside (0, 1]; SCADLES_EWORKSPACE for an undersized workspace.   */
+scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio,
+                                   uint32_t* idx, float* val, double* energies,
+                                   void* ws, size_t ws_bytes, void* stream);
+
+/* Weighted aggregation of K devices' contributions (Eqn 4b):
+ *   dense[i] = sum over j = 0..K-1, in that order, of w_j * v_j(i)
+ * where v_j(i) is device j's value at i (zero when i is not in a sparse set).
+ * The sum is accumulated in double with one fused multiply-add per term and
+ * rounded to float once, so the result does not depend on the launch shape.
+ *   sets     (host[K]) the contributions, see scadles_sparse.
+ *   weights  (host[K]) r_j of Eqn 4a: finite, >= 0, summing to 1 within
+ *            K * 2^-23.
+ *   dense    (dev, n floats, 16-byte aligned) overwritten; +0 where no device
+ *            contributes.
+ * Returns SCADLES_EINVAL for bad arguments; with the "validate" option set it
+ * also synchronises `stream` and returns SCADLES_EUNSORTED if a set's idx is
+ * not strictly ascending or reaches n. Without it such input gives
+ * unspecified values (never an out-of-bounds access).                       */
+scadles_status scadles_weighted_aggregate(const scadles_sparse* sets, const float* weights,
+                                          uint32_t K, uint64_t n, float* dense,
+                                          void* ws, size_t ws_bytes, void* stream);
+
+/* SGD update (Eqn 4c): params[i] <- params[i] - lr * grad[i], evaluated as
+ * one fused multiply-add in double and rounded to float once.
+ *   params (dev, n floats) updated in place; grad (dev, n floats), may not
+ *   alias params. Both 16-byte aligned. lr finite.                          */
+scadles_status scadles_apply_sgd(float* params, const float* grad, uint64_t n, float lr,
+                                 void* stream);
+
+/* One whole hot-path step for K devices in one call (the training step of
+ * §IV): Top-k + energies for every device, the adaptive decision, weighted
+ * aggregation and, optionally, the SGD update.
+ *   grads      (host[K] of dev pointers, n floats each, 16-byte aligned).
+ *   ratios     (host[K]) per-device compression ratio in (0, 1].
+ *   delta      compression threshold of §IV: device j sends Top-k(g_j) when
+ *              |E_all - E_kept| / E_all <= delta (E_all == 0 counts as 0) and
+ *              its dense gradient otherwise. +INFINITY always compresses.
+ *   weights    (host[K]) as for scadles_weighted_aggregate.
+ *   idx, val   (host[K] of dev pointers) per-device outputs of k_j entries,
+ *              exactly as scadles_topk_select writes them (always written,
+ *              whatever the decision).
+ *   dense      (dev, n floats, 16-byte aligned) receives g~ of Eqn 4b.
+ *   energies   (dev, 2K doubles) or NULL: E_all and E_kept per device.
+ *   compressed (dev, K bytes) or NULL: 1 if the device sent Top-k, else 0.
+ *   params     (dev, n floats, 16-byte aligned) or NULL: when non-NULL the
+ *              SGD update of Eqn 4c with learning rate lr is applied to it
+ *              using the float g~ written to dense.
+ * K <= SCADLES_MAX_DEVICES. Same error convention as above.                 */
+scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_t n,
+                                  const double* ratios, double delta, const float* weights,
+                                  uint32_t* const* idx, float* const* val, float* dense,
+                                  double* energies, uint8_t* compressed,
+                                  float* params, float lr,
+                                  void* ws, size_t ws_bytes, void* stream);
+
+/* Aggregation weights and learning-rate scale from streaming rates
+ * (§IV "Heterogeneous streams", Eqn 4a and the linear scaling rule):
+ *   b_j = clamp(S_j, b_min, b_max)   (batch bounded to [b_min, b_max]),
+ *   r_j = b_j / sum_i b_i            (computed in double, stored as float),
+ *   gamma = sum_i b_i / base_batch   (eta_scaled = gamma * eta).
+ *   rates   (host[K]) S_j, finite and >= 0, not all zero after clamping.
+ *   b_min <= b_max; pass 0 and +INFINITY for no bounds.
+ *   weights (host[K]) receives r_j. gamma (host) may be NULL; if not,
+ *   base_batch must be > 0.
+ * Host-only; touches no GPU state.                                          */
+scadles_status scadles_stream_weights(const double* rates, uint32_t K, double b_min,
+                                      double b_max, double base_batch, float* weights,
+                                      double* gamma);
+
+/* Message for the last non-OK status returned on the calling thread.        */
+const char* scadles_last_error(void);
+
+/* Process-wide options, for testing and diagnosis:
+ *   "validate"       1: scadles_weighted_aggregate checks its sets (syncs).
+ *   "force_exact"    1: Top-k skips the sampled single-read path and always
+ *                       runs the exact multi-pass radix select.
+ *   "force_fallback" 1: the sampled path runs but its result is discarded as
+ *                       if the bracket had missed, exercising the fallback.
+ * Returns SCADLES_EINVAL for an unknown name.                               */
+scadles_status scadles_set_option(const char* name, int64_t value);
+
+/* Stage timing. While enabled, every scadles_topk_select / scadles_step_fused
+ * call records HIP events on its stream at the boundaries of its stages.
+ * scadles_profile_read synchronises those events, writes the summed
+ * milliseconds of each stage to stage_ms (host[SCADLES_PROFILE_STAGES]) and
+ * the number of calls recorded to *calls, and clears the record.
+ * Stages: 0 bracket (sampling), 1 main select pass (one read of every
+ * gradient), 2 exact threshold from candidates, 3 ordered compaction,
+ * 4 exact fallback, 5 aggregation (+SGD).                                   */
+#define SCADLES_PROFILE_STAGES 6
+scadles_status scadles_profile_enable(int on);
+scadles_status scadles_profile_read(double* stage_ms, uint32_t* calls);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCADLES_H */

@@ -1,0 +1,196 @@
+"""CPU oracle of the ScaDLES hot path -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package. The product path
+(``paper_2301_08897_amd``) never imports it, and the two share no code.
+
+The arithmetic lives in ``scadles_oracle.c`` (plain C, double precision,
+full sort, serial sums); this module compiles it with gcc and wraps it for
+numpy arrays. ``topk_by_threshold`` is a second, O(n) statement of the same
+Top-k definition for vectors too long to sort in a test: the k-th largest
+magnitude from a library selection routine (``numpy.partition``), then the
+definition of the kept set written out.
+
+Paper: Tyagi & Swany, "ScaDLES: Scalable Deep Learning over Streaming data at
+the Edge", arXiv 2301.08897. Section, equation and table numbers below refer
+to it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "scadles_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+_lock = threading.Lock()
+
+_u32p = ctypes.POINTER(ctypes.c_uint32)
+_f32p = ctypes.POINTER(ctypes.c_float)
+_f64p = ctypes.POINTER(ctypes.c_double)
+_u64p = ctypes.POINTER(ctypes.c_uint64)
+
+
+def build() -> str:
+    """Compile the oracle with gcc (no -ffast-math: IEEE semantics, denormals kept)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fno-fast-math",
+           "-ffp-contract=off", _SRC, "-o", _LIB_PATH, "-lm"]
+    subprocess.run(cmd, check=True)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(_LIB_PATH):
+            build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        lib.oracle_topk_k.restype = ctypes.c_uint64
+        lib.oracle_topk_k.argtypes = [ctypes.c_uint64, ctypes.c_double]
+        lib.oracle_topk.restype = ctypes.c_int
+        lib.oracle_topk.argtypes = [_f32p, ctypes.c_uint64, ctypes.c_uint64, _u32p, _f32p,
+                                    _f64p, _f64p]
+        lib.oracle_compress_decision.restype = ctypes.c_int
+        lib.oracle_compress_decision.argtypes = [ctypes.c_double, ctypes.c_double,
+                                                 ctypes.c_double, _f64p]
+        lib.oracle_aggregate.restype = ctypes.c_int
+        lib.oracle_aggregate.argtypes = [ctypes.c_uint32, ctypes.c_uint64,
+                                         ctypes.POINTER(_u32p), ctypes.POINTER(_f32p),
+                                         _u64p, _f32p, _f32p]
+        lib.oracle_sgd.restype = None
+        lib.oracle_sgd.argtypes = [_f32p, _f32p, ctypes.c_uint64, ctypes.c_float]
+        lib.oracle_stream_weights.restype = ctypes.c_int
+        lib.oracle_stream_weights.argtypes = [_f64p, ctypes.c_uint32, ctypes.c_double,
+                                              ctypes.c_double, ctypes.c_double, _f32p, _f64p]
+        _lib = lib
+        return lib
+
+
+def _ptr(a: np.ndarray, ctype):
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+def topk_k(n: int, ratio: float) -> int:
+    """k = clamp(floor(ratio * n), 1, n) in double (§V-G); 0 for invalid input."""
+    return int(_load().oracle_topk_k(int(n), float(ratio)))
+
+
+def topk(g: np.ndarray, k: int):
+    """Top-k of one gradient by full sort (§III-C, §IV).
+
+    Returns (idx uint32 ascending, val float32, e_all, e_kept)."""
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    n = g.size
+    idx = np.empty(k, dtype=np.uint32)
+    val = np.empty(k, dtype=np.float32)
+    e_all = ctypes.c_double()
+    e_kept = ctypes.c_double()
+    rc = _load().oracle_topk(_ptr(g, ctypes.c_float), n, int(k), _ptr(idx, ctypes.c_uint32),
+                             _ptr(val, ctypes.c_float), ctypes.byref(e_all),
+                             ctypes.byref(e_kept))
+    if rc != 0:
+        raise ValueError(f"oracle_topk rejected n={n} k={k}")
+    return idx, val, e_all.value, e_kept.value
+
+
+def topk_by_threshold(g: np.ndarray, k: int):
+    """Top-k of one gradient in O(n), for full-size vectors (§III-C, §IV).
+
+    The k-th largest magnitude T comes from ``numpy.partition``. Kept set, by
+    definition: every entry with |g| > T, plus the lowest-indexed entries with
+    |g| == T until k are kept. Returns (idx uint32 ascending, T as float32
+    magnitude, count above T, number of ties kept)."""
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    n = g.size
+    if not 1 <= k <= n:
+        raise ValueError("k out of range")
+    mag = np.abs(g)
+    t = np.partition(mag, n - k)[n - k]
+    above = mag > t
+    c_gt = int(np.count_nonzero(above))
+    need = k - c_gt
+    ties = np.flatnonzero(mag == t)[:need]
+    keep = above
+    keep[ties] = True
+    idx = np.flatnonzero(keep).astype(np.uint32)
+    return idx, np.float32(t), c_gt, need
+
+
+def compress_decision(e_all: float, e_kept: float, delta: float):
+    """Adaptive rule of §IV. Returns (send_topk: bool, energy-loss ratio)."""
+    rho = ctypes.c_double()
+    r = _load().oracle_compress_decision(float(e_all), float(e_kept), float(delta),
+                                         ctypes.byref(rho))
+    return bool(r), rho.value
+
+
+def aggregate(sets, weights, n: int) -> np.ndarray:
+    """Eqn 4b. ``sets`` is a list of (idx uint32 or None for dense, val float32)."""
+    K = len(sets)
+    w = np.ascontiguousarray(weights, dtype=np.float32)
+    idx_arrs, val_arrs = [], []
+    idx_ptrs = (_u32p * K)()
+    val_ptrs = (_f32p * K)()
+    ks = np.empty(K, dtype=np.uint64)
+    for j, (idx, val) in enumerate(sets):
+        v = np.ascontiguousarray(val, dtype=np.float32)
+        val_arrs.append(v)
+        val_ptrs[j] = _ptr(v, ctypes.c_float)
+        if idx is None:
+            idx_ptrs[j] = _u32p()
+            ks[j] = n
+        else:
+            i = np.ascontiguousarray(idx, dtype=np.uint32)
+            idx_arrs.append(i)
+            idx_ptrs[j] = _ptr(i, ctypes.c_uint32)
+            ks[j] = i.size
+    out = np.empty(n, dtype=np.float32)
+    rc = _load().oracle_aggregate(K, n, idx_ptrs, val_ptrs, _ptr(ks, ctypes.c_uint64),
+                                  _ptr(w, ctypes.c_float), _ptr(out, ctypes.c_float))
+    if rc != 0:
+        raise ValueError("oracle_aggregate rejected its input")
+    return out
+
+
+def aggregate_at(contrib: np.ndarray, weights) -> np.ndarray:
+    """Eqn 4b at selected positions only: ``contrib`` is float32[K, m], device
+    j's value at each position (0 where it keeps nothing). Sums in double in
+    device order, one rounding to float -- the same arithmetic as
+    ``aggregate`` restricted to m positions."""
+    contrib = np.asarray(contrib, dtype=np.float32)
+    w = np.asarray(weights, dtype=np.float32)
+    acc = np.zeros(contrib.shape[1], dtype=np.float64)
+    for j in range(contrib.shape[0]):
+        acc += np.float64(w[j]) * contrib[j].astype(np.float64)
+    return acc.astype(np.float32)
+
+
+def sgd(params: np.ndarray, grad: np.ndarray, lr: float) -> np.ndarray:
+    """Eqn 4c on a copy of ``params``."""
+    p = np.array(params, dtype=np.float32, copy=True)
+    g = np.ascontiguousarray(grad, dtype=np.float32)
+    _load().oracle_sgd(_ptr(p, ctypes.c_float), _ptr(g, ctypes.c_float), p.size,
+                       ctypes.c_float(lr))
+    return p
+
+
+def stream_weights(rates, b_min: float = 0.0, b_max: float = float("inf"),
+                   base_batch: float = 1.0):
+    """Eqn 4a weights and the linear-scaling factor gamma (§IV)."""
+    r = np.ascontiguousarray(rates, dtype=np.float64)
+    K = r.size
+    w = np.empty(K, dtype=np.float32)
+    gamma = ctypes.c_double()
+    rc = _load().oracle_stream_weights(_ptr(r, ctypes.c_double), K, float(b_min), float(b_max),
+                                       float(base_batch), _ptr(w, ctypes.c_float),
+                                       ctypes.byref(gamma))
+    if rc != 0:
+        raise ValueError("oracle_stream_weights rejected its input")
+    return w, gamma.value

@@ -1,0 +1,185 @@
+/*
+ * scadles_oracle.c -- the CPU oracle of the ScaDLES hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY. Only the test suite, the smoke check and the CPU
+ * baseline leg of the benchmark may load this library. The product path
+ * (paper_2301_08897_amd) never calls it, and the two share no code.
+ *
+ * Everything here is the plain definition of what the hot path computes,
+ * written for a reader to check against the paper by eye: a full sort for
+ * Top-k, serial sums in double in index / device order, no blocking, no
+ * fusion, no reordering. Slow on purpose.
+ *
+ * Paper: Tyagi & Swany, "ScaDLES: Scalable Deep Learning over Streaming data
+ * at the Edge", arXiv 2301.08897.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* Number of entries kept at compression ratio `ratio` (§V-G: a CR of 0.1 keeps
+ * a tenth of the tensor; Top-k "top k%" in §IV). Reading: k = floor(ratio*n)
+ * evaluated in double, at least 1 and at most n. 0 flags invalid input.     */
+uint64_t oracle_topk_k(uint64_t n, double ratio)
+{
+  if (n == 0 || n > 0xFFFFFFFFull) return 0;
+  if (!(ratio > 0.0) || !(ratio <= 1.0)) return 0; /* also rejects NaN */
+  double f = floor(ratio * (double)n);
+  uint64_t k = (uint64_t)f;
+  if (k < 1) k = 1;
+  if (k > n) k = n;
+  return k;
+}
+
+typedef struct {
+  float mag; /* |g_i| */
+  uint32_t i;
+} mag_index;
+
+/* Order of Top-k: larger magnitude first; equal magnitudes by lower index.
+ * fabsf makes -0 and +0 equal. This is a strict total order on the pairs.  */
+static int by_magnitude_then_index(const void* pa, const void* pb)
+{
+  const mag_index* a = (const mag_index*)pa;
+  const mag_index* b = (const mag_index*)pb;
+  if (a->mag > b->mag) return -1;
+  if (a->mag < b->mag) return 1;
+  if (a->i < b->i) return -1;
+  if (a->i > b->i) return 1;
+  return 0;
+}
+
+/* Top-k sparsification (§III-C, §IV "High communication cost"): the k entries
+ * of largest magnitude, ties to the lower index, returned in ascending index
+ * order with their signed values. Also the two energies of the adaptive rule
+ * of §IV: e_all = sum g_i^2 over all i, e_kept = the same sum over the kept
+ * entries, each summed in double in ascending index order.
+ * Returns 0 on success, -1 on bad arguments or allocation failure.         */
+int oracle_topk(const float* g, uint64_t n, uint64_t k, uint32_t* idx_out, float* val_out,
+                double* e_all, double* e_kept)
+{
+  if (!g || n == 0 || n > 0xFFFFFFFFull || k < 1 || k > n) return -1;
+  mag_index* order = (mag_index*)malloc(n * sizeof(mag_index));
+  unsigned char* kept = (unsigned char*)calloc(n, 1);
+  if (!order || !kept) {
+    free(order);
+    free(kept);
+    return -1;
+  }
+  for (uint64_t i = 0; i < n; ++i) {
+    order[i].mag = fabsf(g[i]);
+    order[i].i = (uint32_t)i;
+  }
+  qsort(order, n, sizeof(mag_index), by_magnitude_then_index);
+  for (uint64_t r = 0; r < k; ++r) kept[order[r].i] = 1;
+  free(order);
+
+  uint64_t out = 0;
+  double all = 0.0, kep = 0.0;
+  for (uint64_t i = 0; i < n; ++i) {
+    double x = (double)g[i];
+    all += x * x;
+    if (kept[i]) {
+      kep += x * x;
+      if (idx_out) idx_out[out] = (uint32_t)i;
+      if (val_out) val_out[out] = g[i];
+      ++out;
+    }
+  }
+  free(kept);
+  if (e_all) *e_all = all;
+  if (e_kept) *e_kept = kep;
+  return out == k ? 0 : -1;
+}
+
+/* The adaptive compression rule of §IV: send Top-k(g) when
+ * | ||g||^2 - ||Top-k(g)||^2 | / ||g||^2 <= delta, else send g. A zero
+ * gradient loses nothing (ratio 0). Returns 1 for "send Top-k", 0 for
+ * "send g"; *loss receives the ratio.                                       */
+int oracle_compress_decision(double e_all, double e_kept, double delta, double* loss)
+{
+  double rho = (e_all == 0.0) ? 0.0 : fabs(e_all - e_kept) / e_all;
+  if (loss) *loss = rho;
+  return rho <= delta ? 1 : 0;
+}
+
+/* Weighted aggregation, Eqn 4b: out[i] = sum_{j=0..K-1} w_j * v_j(i), where
+ * v_j(i) is device j's value at i if i is one of its k_j kept positions and 0
+ * otherwise. idx[j] == NULL marks a device that sent its dense gradient
+ * (k[j] must then be n and val[j] holds n values). Accumulated in double in
+ * device order, rounded to float once at the end.
+ * Returns 0, or -1 on bad arguments.                                        */
+int oracle_aggregate(uint32_t K, uint64_t n, const uint32_t* const* idx, const float* const* val,
+                     const uint64_t* k, const float* w, float* out)
+{
+  if (K == 0 || n == 0 || !val || !k || !w || !out) return -1;
+  double* acc = (double*)calloc(n, sizeof(double));
+  if (!acc) return -1;
+  for (uint32_t j = 0; j < K; ++j) {
+    double wj = (double)w[j];
+    if (idx == NULL || idx[j] == NULL) {
+      if (k[j] != n) {
+        free(acc);
+        return -1;
+      }
+      for (uint64_t i = 0; i < n; ++i) acc[i] += wj * (double)val[j][i];
+    } else {
+      for (uint64_t t = 0; t < k[j]; ++t) {
+        uint32_t i = idx[j][t];
+        if (i >= n) {
+          free(acc);
+          return -1;
+        }
+        acc[i] += wj * (double)val[j][t];
+      }
+    }
+  }
+  for (uint64_t i = 0; i < n; ++i) out[i] = (float)acc[i];
+  free(acc);
+  return 0;
+}
+
+/* SGD update, Eqn 4c: w <- w - eta_scaled * g~, in double, rounded to float. */
+void oracle_sgd(float* p, const float* g, uint64_t n, float lr)
+{
+  for (uint64_t i = 0; i < n; ++i) p[i] = (float)((double)p[i] - (double)lr * (double)g[i]);
+}
+
+/* Weights and learning-rate scale from streaming rates (§IV "Heterogeneous
+ * streams"): batch b_j = S_j bounded to [b_min, b_max]; Eqn 4a
+ * r_j = b_j / sum b (so sum r = 1); linear scaling gamma = sum b / B.
+ * Returns 0, or -1 on bad input (negative or non-finite rate, empty sum).  */
+int oracle_stream_weights(const double* rates, uint32_t K, double b_min, double b_max,
+                          double base_batch, float* w, double* gamma)
+{
+  if (!rates || K == 0 || !w || !(b_min <= b_max)) return -1;
+  double* b = (double*)malloc(K * sizeof(double));
+  if (!b) return -1;
+  double total = 0.0;
+  for (uint32_t j = 0; j < K; ++j) {
+    double s = rates[j];
+    if (!isfinite(s) || s < 0.0) {
+      free(b);
+      return -1;
+    }
+    if (s < b_min) s = b_min;
+    if (s > b_max) s = b_max;
+    b[j] = s;
+    total += s;
+  }
+  if (!(total > 0.0) || !isfinite(total)) {
+    free(b);
+    return -1;
+  }
+  for (uint32_t j = 0; j < K; ++j) w[j] = (float)(b[j] / total);
+  if (gamma) {
+    if (!(base_batch > 0.0)) {
+      free(b);
+      return -1;
+    }
+    *gamma = total / base_batch;
+  }
+  free(b);
+  return 0;
+}
