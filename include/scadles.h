@@ -185,9 +185,10 @@ scadles_status scadles_set_option(const char* name, int64_t value);
  * milliseconds of each stage to stage_ms (host[SCADLES_PROFILE_STAGES]) and
  * the number of calls recorded to *calls, and clears the record.
  * Stages: 0 bracket (sampling), 1 main select pass (one read of every
- * gradient), 2 exact threshold from candidates, 3 ordered compaction,
- * 4 exact fallback, 5 aggregation (+SGD).                                   */
-#define SCADLES_PROFILE_STAGES 6
+ * gradient), 2 exact threshold (radix passes over the candidates, or over
+ * the full data on the exact path), 3 ordered compaction and energies,
+ * 4 weighted aggregation (+SGD; empty for scadles_topk_select).              */
+#define SCADLES_PROFILE_STAGES 5
 scadles_status scadles_profile_enable(int on);
 scadles_status scadles_profile_read(double* stage_ms, uint32_t* calls);
 

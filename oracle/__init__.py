@@ -123,6 +123,13 @@ def topk_by_threshold(g: np.ndarray, k: int):
     return idx, np.float32(t), c_gt, need
 
 
+def energies(g: np.ndarray, idx: np.ndarray):
+    """The two energies of the adaptive rule (§IV) for a kept set ``idx``:
+    (sum over all i of g_i^2, sum over kept i of g_i^2), squares and sums in double."""
+    g64 = np.asarray(g, dtype=np.float32).astype(np.float64)
+    return float(np.sum(g64 * g64)), float(np.sum(g64[idx] * g64[idx]))
+
+
 def compress_decision(e_all: float, e_kept: float, delta: float):
     """Adaptive rule of §IV. Returns (send_topk: bool, energy-loss ratio)."""
     rho = ctypes.c_double()

@@ -1,0 +1,292 @@
+"""ScaDLES hot path on MI355X: Top-k sparsification, streaming-rate-weighted
+aggregation and SGD in hand-written HIP kernels for gfx950.
+
+This package is a thin ctypes binding over ``libscadles.so`` (C ABI in
+``include/scadles.h``). It only marshals arguments: every step runs in the HIP
+kernels. PyTorch supplies device memory and the stream. Importing fails
+loudly when the library has not been built (``__graft_entry__.build()``).
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libscadles.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first "
+                      "(there is no fallback implementation)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+MAX_DEVICES = 64
+PROFILE_STAGES = 5
+STAGE_NAMES = ("bracket", "main_select", "threshold", "compaction", "aggregate")
+
+_vp = ctypes.c_void_p
+_u64 = ctypes.c_uint64
+_u32 = ctypes.c_uint32
+
+
+class Sparse(ctypes.Structure):
+    _fields_ = [("idx", _vp), ("val", _vp), ("k", _u64)]
+
+
+def _sig(name, restype, *argtypes):
+    f = getattr(_lib, name)
+    f.restype = restype
+    f.argtypes = list(argtypes)
+    return f
+
+
+_topk_k = _sig("scadles_topk_k", _u64, _u64, ctypes.c_double)
+_ws_bytes = _sig("scadles_workspace_bytes", ctypes.c_size_t, _u32, _u64, ctypes.POINTER(ctypes.c_double))
+_agg_ws_bytes = _sig("scadles_aggregate_workspace_bytes", ctypes.c_size_t, _u32, _u64)
+_topk_select = _sig("scadles_topk_select", ctypes.c_int, _vp, _u64, ctypes.c_double, _vp, _vp, _vp, _vp,
+                    ctypes.c_size_t, _vp)
+_weighted_aggregate = _sig("scadles_weighted_aggregate", ctypes.c_int, ctypes.POINTER(Sparse),
+                           ctypes.POINTER(ctypes.c_float), _u32, _u64, _vp, _vp, ctypes.c_size_t, _vp)
+_apply_sgd = _sig("scadles_apply_sgd", ctypes.c_int, _vp, _vp, _u64, ctypes.c_float, _vp)
+_step_fused = _sig("scadles_step_fused", ctypes.c_int, ctypes.POINTER(_vp), _u32, _u64,
+                   ctypes.POINTER(ctypes.c_double), ctypes.c_double, ctypes.POINTER(ctypes.c_float),
+                   ctypes.POINTER(_vp), ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, ctypes.c_float, _vp,
+                   ctypes.c_size_t, _vp)
+_stream_weights = _sig("scadles_stream_weights", ctypes.c_int, ctypes.POINTER(ctypes.c_double), _u32,
+                       ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_float),
+                       ctypes.POINTER(ctypes.c_double))
+_last_error = _sig("scadles_last_error", ctypes.c_char_p)
+_set_option = _sig("scadles_set_option", ctypes.c_int, ctypes.c_char_p, ctypes.c_int64)
+_profile_enable = _sig("scadles_profile_enable", ctypes.c_int, ctypes.c_int)
+_profile_read = _sig("scadles_profile_read", ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                     ctypes.POINTER(_u32))
+
+STATUS = {0: "SCADLES_OK", 1: "SCADLES_EINVAL", 2: "SCADLES_EWORKSPACE", 3: "SCADLES_EHIP",
+          4: "SCADLES_EUNSORTED", 5: "SCADLES_EINTERNAL"}
+
+
+class ScadlesError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+def _check(code: int):
+    if code != 0:
+        raise ScadlesError(code, _last_error().decode(errors="replace"))
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_ptr(stream) -> Optional[int]:
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _dev_f32(t, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if t.dtype != torch.float32 or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous float32 tensor")
+    return t.data_ptr()
+
+
+def library_path() -> str:
+    return LIB_PATH
+
+
+# ---- host-side rules ----------------------------------------------------------------------
+
+def topk_k(n: int, ratio: float) -> int:
+    """k = clamp(floor(ratio * n), 1, n) (0 for invalid input)."""
+    return int(_topk_k(int(n), float(ratio)))
+
+
+def workspace_bytes(K: int, n: int, ratios: Sequence[float]) -> int:
+    r = (ctypes.c_double * K)(*[float(x) for x in ratios])
+    return int(_ws_bytes(K, int(n), r))
+
+
+def aggregate_workspace_bytes(K: int, n: int) -> int:
+    return int(_agg_ws_bytes(K, int(n)))
+
+
+def stream_weights(rates, b_min: float = 0.0, b_max: float = math.inf, base_batch: Optional[float] = None):
+    """Eqn 4a weights (float32[K]) and, if base_batch is given, the linear-scaling gamma."""
+    r = np.ascontiguousarray(rates, dtype=np.float64)
+    K = r.size
+    w = np.empty(K, dtype=np.float32)
+    g = ctypes.c_double()
+    _check(_stream_weights(r.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), K, float(b_min), float(b_max),
+                           float(base_batch) if base_batch is not None else 0.0,
+                           w.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                           ctypes.byref(g) if base_batch is not None else None))
+    return (w, g.value) if base_batch is not None else (w, None)
+
+
+def set_option(name: str, value: int):
+    _check(_set_option(name.encode(), int(value)))
+
+
+def profile_enable(on: bool = True):
+    _check(_profile_enable(1 if on else 0))
+
+
+def profile_read():
+    """(dict stage -> summed ms, number of calls) since the last read; syncs the events."""
+    ms = (ctypes.c_double * PROFILE_STAGES)()
+    calls = _u32()
+    _check(_profile_read(ms, ctypes.byref(calls)))
+    return dict(zip(STAGE_NAMES, list(ms))), int(calls.value)
+
+
+def _workspace(nbytes: int, device):
+    torch = _torch()
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+# ---- the three calls of the hot path -----------------------------------------------------------
+
+def topk_select(grad, ratio: float, *, workspace=None, energies: bool = False, stream=None):
+    """Top-k of one gradient. Returns (idx uint32[k], val float32[k]) or, with
+    energies=True, (idx, val, float64[2] = (sum g^2, sum kept g^2))."""
+    torch = _torch()
+    gp = _dev_f32(grad, "grad")
+    n = grad.numel()
+    k = topk_k(n, ratio)
+    if k == 0:
+        raise ScadlesError(1, f"invalid n={n} or ratio={ratio}")
+    dev = grad.device
+    idx = torch.empty(k, dtype=torch.uint32, device=dev)
+    val = torch.empty(k, dtype=torch.float32, device=dev)
+    en = torch.empty(2, dtype=torch.float64, device=dev) if energies else None
+    need = workspace_bytes(1, n, [ratio])
+    ws = workspace if workspace is not None else _workspace(need, dev)
+    _check(_topk_select(gp, n, float(ratio), idx.data_ptr(), val.data_ptr(),
+                        en.data_ptr() if en is not None else None, ws.data_ptr(), ws.numel(),
+                        _stream_ptr(stream)))
+    return (idx, val, en) if energies else (idx, val)
+
+
+def weighted_aggregate(sets, weights, n: int, *, out=None, workspace=None, stream=None):
+    """Eqn 4b. ``sets``: list of (idx uint32 tensor or None for dense, val float32 tensor)."""
+    torch = _torch()
+    K = len(sets)
+    w = np.ascontiguousarray(weights, dtype=np.float32)
+    if w.size != K:
+        raise ValueError("one weight per set")
+    arr = (Sparse * K)()
+    dev = None
+    for j, (idx, val) in enumerate(sets):
+        vp = _dev_f32(val, f"sets[{j}].val")
+        dev = val.device
+        if idx is None:
+            arr[j] = Sparse(None, vp, val.numel())
+        else:
+            if idx.dtype not in (torch.uint32, torch.int32) or not idx.is_cuda or not idx.is_contiguous():
+                raise TypeError(f"sets[{j}].idx must be a contiguous uint32 GPU tensor")
+            if idx.numel() != val.numel():
+                raise ValueError(f"sets[{j}]: idx and val differ in length")
+            arr[j] = Sparse(idx.data_ptr(), vp, idx.numel())
+    if out is None:
+        out = torch.empty(n, dtype=torch.float32, device=dev)
+    ws = workspace if workspace is not None else _workspace(aggregate_workspace_bytes(K, n), dev)
+    _check(_weighted_aggregate(arr, w.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), K, int(n),
+                               _dev_f32(out, "out"), ws.data_ptr(), ws.numel(), _stream_ptr(stream)))
+    return out
+
+
+def apply_sgd(params, grad, lr: float, *, stream=None):
+    """Eqn 4c in place on ``params``."""
+    _check(_apply_sgd(_dev_f32(params, "params"), _dev_f32(grad, "grad"), params.numel(), float(lr),
+                      _stream_ptr(stream)))
+    return params
+
+
+# ---- the fused step -----------------------------------------------------------------------------
+
+@dataclass
+class StepOutputs:
+    idx: list
+    val: list
+    dense: object
+    energies: object
+    compressed: object
+
+
+class FusedStep:
+    """One hot-path step for K devices of n elements (Top-k + energies + adaptive
+    rule + Eqn 4b aggregation + optional Eqn 4c update), with every output and
+    the workspace allocated once so that ``run`` only marshals pointers."""
+
+    def __init__(self, grads, ratios: Sequence[float], *, delta: float = math.inf, params=None):
+        torch = _torch()
+        if isinstance(grads, torch.Tensor) and grads.dim() == 2:
+            grads = [grads[j] for j in range(grads.shape[0])]
+        self.K = len(grads)
+        if not 1 <= self.K <= MAX_DEVICES:
+            raise ValueError(f"K must be in [1, {MAX_DEVICES}]")
+        self.n = grads[0].numel()
+        self.grads = list(grads)
+        for j, g in enumerate(self.grads):
+            _dev_f32(g, f"grads[{j}]")
+            if g.numel() != self.n:
+                raise ValueError("all gradients must have n elements")
+        dev = self.grads[0].device
+        self.device = dev
+        self.params = params
+        self.delta = float(delta)
+        self.set_ratios(ratios)
+        self.dense = torch.empty(self.n, dtype=torch.float32, device=dev)
+        self.energies = torch.empty(2 * self.K, dtype=torch.float64, device=dev)
+        self.compressed = torch.empty(self.K, dtype=torch.uint8, device=dev)
+        self._grad_ptrs = (_vp * self.K)(*[g.data_ptr() for g in self.grads])
+        self._w = (ctypes.c_float * self.K)()
+
+    def set_ratios(self, ratios):
+        torch = _torch()
+        ratios = [float(r) for r in ratios]
+        if len(ratios) != self.K:
+            raise ValueError("one ratio per device")
+        self.ratios = ratios
+        self.k = [topk_k(self.n, r) for r in ratios]
+        if min(self.k) == 0:
+            raise ScadlesError(1, "ratio outside (0, 1]")
+        self.idx = [torch.empty(k, dtype=torch.uint32, device=self.device) for k in self.k]
+        self.val = [torch.empty(k, dtype=torch.float32, device=self.device) for k in self.k]
+        self._ratios = (ctypes.c_double * self.K)(*ratios)
+        self._idx_ptrs = (_vp * self.K)(*[t.data_ptr() for t in self.idx])
+        self._val_ptrs = (_vp * self.K)(*[t.data_ptr() for t in self.val])
+        need = workspace_bytes(self.K, self.n, ratios)
+        if need == 0:
+            raise ScadlesError(1, "workspace query rejected the arguments")
+        if getattr(self, "ws", None) is None or self.ws.numel() < need:
+            self.ws = _workspace(need, self.device)
+
+    def run(self, weights, lr: float = 0.0, *, stream=None) -> StepOutputs:
+        w = np.ascontiguousarray(weights, dtype=np.float32)
+        for j in range(self.K):
+            self._w[j] = float(w[j])
+        pp = _dev_f32(self.params, "params") if self.params is not None else None
+        _check(_step_fused(self._grad_ptrs, self.K, self.n, self._ratios, self.delta, self._w,
+                           self._idx_ptrs, self._val_ptrs, self.dense.data_ptr(), self.energies.data_ptr(),
+                           self.compressed.data_ptr(), pp, float(lr), self.ws.data_ptr(), self.ws.numel(),
+                           _stream_ptr(stream)))
+        return StepOutputs(self.idx, self.val, self.dense, self.energies, self.compressed)
+
+
+def step_fused(grads, ratios, weights, *, delta: float = math.inf, params=None, lr: float = 0.0,
+               stream=None) -> StepOutputs:
+    """One-shot convenience wrapper around FusedStep."""
+    return FusedStep(grads, ratios, delta=delta, params=params).run(weights, lr, stream=stream)

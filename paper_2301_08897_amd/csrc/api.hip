@@ -1,0 +1,510 @@
+// api.hip -- the C ABI of libscadles (declared in include/scadles.h).
+//
+// Host side only: argument validation, the k rule, workspace layout, path
+// choice per device, and the launch sequence. Every entry point validates
+// before launching anything and never allocates device memory.
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "scadles.h"
+#include "scadles_internal.h"
+
+using namespace scadles;
+
+namespace {
+
+thread_local std::string g_err;
+std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0};
+
+scadles_status fail(scadles_status st, const char* fmt, ...)
+{
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+scadles_status hip_fail(hipError_t e, const char* where)
+{
+  return fail(SCADLES_EHIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+// ---- stage profiling ------------------------------------------------------------------------
+constexpr int kStages = SCADLES_PROFILE_STAGES;
+constexpr int kProfMax = 4096;
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+struct ProfRec {
+  hipEvent_t ev[kStages + 1];
+};
+std::vector<ProfRec> g_prof_pool;
+size_t g_prof_used = 0;
+
+// Returns kStages + 1 events to record into, or null when profiling is off or full.
+hipEvent_t* prof_slot()
+{
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_prof_on || g_prof_used >= g_prof_pool.size()) return nullptr;
+  return g_prof_pool[g_prof_used++].ev;
+}
+
+// ---- layout ---------------------------------------------------------------------------------
+constexpr uint64_t kFastMinN = 65536;
+constexpr uint64_t kCapAlign = 64;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Layout {
+  uint32_t K = 0, tpd = 0, ncb = 0, nfb = 0, nbmax = 0, ntile = 0, s_stride = 0, s_n = 0;
+  uint64_t n = 0;
+  uint32_t k[kMaxK], cap[kMaxK], mode[kMaxK], r_lo[kMaxK], r_hi[kMaxK];
+  uint32_t any_fast = 0;
+  size_t o_desc, o_st, o_hist, o_status, o_epart, o_cidx, o_cval, o_bcnt, o_bpre, o_be, o_ticket, o_aoff, o_aerr;
+  size_t total = 0;
+};
+
+uint64_t k_rule(uint64_t n, double ratio)
+{
+  if (n == 0 || n > 0xFFFFFFFFull) return 0;
+  if (!(ratio > 0.0) || !(ratio <= 1.0)) return 0;
+  const double f = std::floor(ratio * (double)n);
+  uint64_t k = (uint64_t)f;
+  if (k < 1) k = 1;
+  if (k > n) k = n;
+  return k;
+}
+
+// Sample: one chunk of kSChunk elements every `stride` elements.
+void sample_geometry(uint64_t n, uint32_t& stride, uint32_t& s_n)
+{
+  uint64_t st = 65536;
+  if (n / st < 64) {
+    st = (n / 64) / kSChunk * kSChunk;
+    if (st < (uint64_t)kSChunk) st = kSChunk;
+  }
+  const uint64_t chunks = (n + st - 1) / st;
+  uint64_t total = 0;
+  for (uint64_t c = 0; c < chunks; ++c) {
+    const uint64_t start = c * st;
+    total += (n - start < (uint64_t)kSChunk) ? n - start : (uint64_t)kSChunk;
+  }
+  stride = (uint32_t)st;
+  s_n = (uint32_t)total;
+}
+
+bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact, bool with_select, Layout& L)
+{
+  L.K = K;
+  L.n = n;
+  L.tpd = ceil_div_u64(n, kTile);
+  L.ntile = ceil_div_u64(n, kATile);
+  sample_geometry(n, L.s_stride, L.s_n);
+  uint64_t sum_cap = 0, max_cap = 0;
+  L.any_fast = 0;
+  for (uint32_t j = 0; j < K; ++j) {
+    const uint64_t k = with_select ? k_rule(n, ratios[j]) : 0;
+    if (with_select && k == 0) return false;
+    L.k[j] = (uint32_t)k;
+    L.cap[j] = 0;
+    L.mode[j] = kModeExact;
+    L.r_lo[j] = L.r_hi[j] = 0;
+    if (!with_select) continue;
+    uint64_t slack = n / 8;
+    if (slack > (1ull << 20)) slack = 1ull << 20;
+    uint64_t cap = 2 * k + slack;
+    cap = (cap + kCapAlign - 1) / kCapAlign * kCapAlign;
+    const bool fast = !force_exact && n >= kFastMinN && 2 * cap <= n && cap < (1ull << 31);
+    if (fast) {
+      L.mode[j] = kModeFast;
+      L.cap[j] = (uint32_t)cap;
+      const double kf = (double)k * (double)L.s_n / (double)n;
+      const double sd = std::sqrt(kf);
+      double rlo = std::ceil(kf + 6.0 * sd + 8.0);
+      if (rlo > (double)L.s_n) rlo = (double)L.s_n;
+      if (rlo < 1.0) rlo = 1.0;
+      double rhi = std::floor(kf - 6.0 * sd - 8.0);
+      if (rhi < 1.0) rhi = 0.0;
+      L.r_lo[j] = (uint32_t)rlo;
+      L.r_hi[j] = (uint32_t)rhi;
+      L.any_fast = 1;
+      sum_cap += cap;
+      if (cap > max_cap) max_cap = cap;
+    }
+  }
+  L.ncb = max_cap ? ceil_div_u64(max_cap, kCBlk) : 1u;
+  L.nfb = ceil_div_u64(n, kCBlk);
+  L.nbmax = L.ncb > L.nfb ? L.ncb : L.nfb;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align256(o + bytes);
+    return at;
+  };
+  if (with_select) {
+    L.o_desc = take(sizeof(DevDesc) * K);
+    L.o_st = take(sizeof(DevState) * K);
+    L.o_hist = take(sizeof(uint32_t) * (size_t)K * kSlots * kBins);
+    L.o_status = take(sizeof(uint64_t) * (size_t)K * L.tpd);
+    L.o_epart = take(sizeof(double) * (size_t)K * L.tpd);
+    L.o_cidx = take(sizeof(uint32_t) * sum_cap);
+    L.o_cval = take(sizeof(float) * sum_cap);
+    L.o_bcnt = take(sizeof(uint64_t) * (size_t)K * L.nbmax);
+    L.o_bpre = take(sizeof(uint64_t) * (size_t)K * L.nbmax);
+    L.o_be = take(sizeof(double) * (size_t)K * L.nbmax);
+    L.o_ticket = take(256);
+  }
+  L.o_aoff = take(sizeof(uint32_t) * (size_t)K * (L.ntile + 1));
+  L.o_aerr = take(256);
+  L.total = o;
+  return true;
+}
+
+Ctx make_ctx(const Layout& L, void* ws)
+{
+  char* b = static_cast<char*>(ws);
+  Ctx c;
+  memset(&c, 0, sizeof(c));
+  c.desc = reinterpret_cast<DevDesc*>(b + L.o_desc);
+  c.st = reinterpret_cast<DevState*>(b + L.o_st);
+  c.hist = reinterpret_cast<uint32_t*>(b + L.o_hist);
+  c.status = reinterpret_cast<uint64_t*>(b + L.o_status);
+  c.epart = reinterpret_cast<double*>(b + L.o_epart);
+  c.cand_idx = reinterpret_cast<uint32_t*>(b + L.o_cidx);
+  c.cand_val = reinterpret_cast<float*>(b + L.o_cval);
+  c.blk_cnt = reinterpret_cast<uint64_t*>(b + L.o_bcnt);
+  c.blk_pre = reinterpret_cast<uint64_t*>(b + L.o_bpre);
+  c.blk_e = reinterpret_cast<double*>(b + L.o_be);
+  c.ticket = reinterpret_cast<uint32_t*>(b + L.o_ticket);
+  c.n = L.n;
+  c.K = L.K;
+  c.tpd = L.tpd;
+  c.ncb = L.ncb;
+  c.nfb = L.nfb;
+  c.nbmax = L.nbmax;
+  c.s_stride = L.s_stride;
+  c.s_n = L.s_n;
+  return c;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+scadles_status check_ws(void* ws, size_t ws_bytes, size_t need)
+{
+  if (!ws) return fail(SCADLES_EWORKSPACE, "workspace is NULL (need %zu bytes)", need);
+  if (!aligned(ws, 256)) return fail(SCADLES_EWORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < need) return fail(SCADLES_EWORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  return SCADLES_OK;
+}
+
+scadles_status check_n(uint64_t n)
+{
+  if (n == 0 || n > 0xFFFFFFFFull) return fail(SCADLES_EINVAL, "n = %llu is outside [1, 2^32 - 1]", (unsigned long long)n);
+  return SCADLES_OK;
+}
+
+scadles_status check_weights(const float* w, uint32_t K)
+{
+  if (!w) return fail(SCADLES_EINVAL, "weights is NULL");
+  double sum = 0.0;
+  for (uint32_t j = 0; j < K; ++j) {
+    if (!std::isfinite(w[j]) || w[j] < 0.0f) return fail(SCADLES_EINVAL, "weight %u is negative or not finite", j);
+    sum += (double)w[j];
+  }
+  if (std::fabs(sum - 1.0) > (double)K * std::ldexp(1.0, -23))
+    return fail(SCADLES_EINVAL, "weights sum to %.17g, not 1 (Eqn 4a)", sum);
+  return SCADLES_OK;
+}
+
+scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double delta, double* energies,
+                          uint8_t* compressed, hipStream_t s, hipEvent_t* ev)
+{
+  Ctx c = make_ctx(L, ws);
+  c.delta = delta;
+  c.energies_out = energies;
+  c.compressed_out = compressed;
+  c.force_fallback = g_force_fallback.load() ? 1u : 0u;
+  SelectPlan p;
+  p.any_fast = L.any_fast;
+  p.sample_blocks = ceil_div_u64(L.s_n, kSBlk);
+  p.ncand_blocks = L.any_fast ? L.K * L.ncb : 0u;
+  const uint64_t tiles = (uint64_t)L.K * L.tpd;
+  p.full_workers = (uint32_t)(tiles < (uint64_t)kFullWorkers ? tiles : (uint64_t)kFullWorkers);
+  hipError_t e = launch_select(c, a, p, s, ev);
+  if (e != hipSuccess) return hip_fail(e, "select launch");
+  return SCADLES_OK;
+}
+
+}  // namespace
+
+// ---- ABI ----------------------------------------------------------------------------------------
+extern "C" {
+
+uint64_t scadles_topk_k(uint64_t n, double ratio) { return k_rule(n, ratio); }
+
+size_t scadles_workspace_bytes(uint32_t K, uint64_t n, const double* ratios)
+{
+  if (K == 0 || K > kMaxK || !ratios || n == 0 || n > 0xFFFFFFFFull) return 0;
+  Layout L;
+  if (!make_layout(K, n, ratios, g_force_exact.load() != 0, true, L)) return 0;
+  // The fast/exact choice may change with the force_exact option; size for the larger.
+  Layout Lf;
+  make_layout(K, n, ratios, false, true, Lf);
+  return L.total > Lf.total ? L.total : Lf.total;
+}
+
+size_t scadles_aggregate_workspace_bytes(uint32_t K, uint64_t n)
+{
+  if (K == 0 || K > kMaxK || n == 0 || n > 0xFFFFFFFFull) return 0;
+  Layout L;
+  make_layout(K, n, nullptr, false, false, L);
+  return L.total;
+}
+
+scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio, uint32_t* idx, float* val,
+                                   double* energies, void* ws, size_t ws_bytes, void* stream)
+{
+  if (scadles_status st = check_n(n)) return st;
+  if (!grad || !idx || !val) return fail(SCADLES_EINVAL, "grad, idx and val must not be NULL");
+  if (!aligned(grad, 16)) return fail(SCADLES_EINVAL, "grad must be 16-byte aligned");
+  if (!aligned(idx, 4) || !aligned(val, 4)) return fail(SCADLES_EINVAL, "idx and val must be 4-byte aligned");
+  if (energies && !aligned(energies, 8)) return fail(SCADLES_EINVAL, "energies must be 8-byte aligned");
+  if (k_rule(n, ratio) == 0) return fail(SCADLES_EINVAL, "ratio %g is not in (0, 1]", ratio);
+  Layout L;
+  make_layout(1, n, &ratio, g_force_exact.load() != 0, true, L);
+  if (scadles_status st = check_ws(ws, ws_bytes, L.total)) return st;
+  PrepArgs a;
+  memset(&a, 0, sizeof(a));
+  a.grad[0] = grad;
+  a.idx[0] = idx;
+  a.val[0] = val;
+  a.k[0] = L.k[0];
+  a.cap[0] = L.cap[0];
+  a.mode[0] = L.mode[0];
+  a.r_lo[0] = L.r_lo[0];
+  a.r_hi[0] = L.r_hi[0];
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipEvent_t* ev = prof_slot();
+  if (ev) (void)hipEventRecord(ev[0], s);
+  scadles_status st = run_select(L, a, ws, INFINITY, energies, nullptr, s, ev);
+  if (ev) (void)hipEventRecord(ev[5], s);
+  return st;
+}
+
+scadles_status scadles_weighted_aggregate(const scadles_sparse* sets, const float* weights, uint32_t K, uint64_t n,
+                                          float* dense, void* ws, size_t ws_bytes, void* stream)
+{
+  if (K == 0 || K > kMaxK) return fail(SCADLES_EINVAL, "K = %u is outside [1, %d]", K, kMaxK);
+  if (scadles_status st = check_n(n)) return st;
+  if (!sets || !dense) return fail(SCADLES_EINVAL, "sets and dense must not be NULL");
+  if (!aligned(dense, 16)) return fail(SCADLES_EINVAL, "dense must be 16-byte aligned");
+  if (scadles_status st = check_weights(weights, K)) return st;
+  AggArgs a;
+  memset(&a, 0, sizeof(a));
+  uint64_t kmax = 0;
+  for (uint32_t j = 0; j < K; ++j) {
+    const scadles_sparse& S = sets[j];
+    if (!S.val) return fail(SCADLES_EINVAL, "set %u has a NULL val", j);
+    if (!S.idx) {
+      if (S.k != n) return fail(SCADLES_EINVAL, "dense set %u must have k == n", j);
+      if (!aligned(S.val, 16)) return fail(SCADLES_EINVAL, "dense set %u must be 16-byte aligned", j);
+      a.dense[j] = S.val;
+    } else {
+      if (S.k > n) return fail(SCADLES_EINVAL, "set %u has k = %llu > n", j, (unsigned long long)S.k);
+      if (!aligned(S.idx, 4) || !aligned(S.val, 4)) return fail(SCADLES_EINVAL, "set %u is misaligned", j);
+      if (S.k > kmax) kmax = S.k;
+    }
+    a.idx[j] = S.idx;
+    a.val[j] = S.val;
+    a.k[j] = (uint32_t)S.k;
+    a.w[j] = weights[j];
+  }
+  Layout L;
+  make_layout(K, n, nullptr, false, false, L);
+  if (scadles_status st = check_ws(ws, ws_bytes, L.total)) return st;
+  char* b = static_cast<char*>(ws);
+  AggCtx c;
+  memset(&c, 0, sizeof(c));
+  c.st = nullptr;
+  c.off = reinterpret_cast<uint32_t*>(b + L.o_aoff);
+  c.err = reinterpret_cast<uint32_t*>(b + L.o_aerr);
+  c.out = dense;
+  c.K = K;
+  c.ntile = L.ntile;
+  c.kmax = (uint32_t)kmax;
+  c.n = n;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const uint32_t validate = g_validate.load() ? 1u : 0u;
+  hipError_t e = launch_aggregate(a, c, validate, s);
+  if (e != hipSuccess) return hip_fail(e, "aggregate launch");
+  if (validate) {
+    uint32_t flag = 0;
+    e = hipMemcpyAsync(&flag, c.err, sizeof(flag), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "aggregate validation");
+    if (flag) return fail(SCADLES_EUNSORTED, "a sparse set's idx is not strictly ascending or reaches n");
+  }
+  return SCADLES_OK;
+}
+
+scadles_status scadles_apply_sgd(float* params, const float* grad, uint64_t n, float lr, void* stream)
+{
+  if (scadles_status st = check_n(n)) return st;
+  if (!params || !grad) return fail(SCADLES_EINVAL, "params and grad must not be NULL");
+  if (!aligned(params, 16) || !aligned(grad, 16)) return fail(SCADLES_EINVAL, "params and grad must be 16-byte aligned");
+  if (!std::isfinite(lr)) return fail(SCADLES_EINVAL, "lr is not finite");
+  const char* pb = reinterpret_cast<const char*>(params);
+  const char* gb = reinterpret_cast<const char*>(grad);
+  if (pb < gb + n * sizeof(float) && gb < pb + n * sizeof(float))
+    return fail(SCADLES_EINVAL, "params and grad overlap");
+  hipError_t e = launch_sgd(params, grad, n, lr, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "sgd launch");
+  return SCADLES_OK;
+}
+
+scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_t n, const double* ratios,
+                                  double delta, const float* weights, uint32_t* const* idx, float* const* val,
+                                  float* dense, double* energies, uint8_t* compressed, float* params, float lr,
+                                  void* ws, size_t ws_bytes, void* stream)
+{
+  if (K == 0 || K > kMaxK) return fail(SCADLES_EINVAL, "K = %u is outside [1, %d]", K, kMaxK);
+  if (scadles_status st = check_n(n)) return st;
+  if (!grads || !ratios || !idx || !val || !dense) return fail(SCADLES_EINVAL, "NULL argument");
+  if (std::isnan(delta) || delta < 0.0) return fail(SCADLES_EINVAL, "delta must be >= 0 (or +INFINITY)");
+  if (!aligned(dense, 16)) return fail(SCADLES_EINVAL, "dense must be 16-byte aligned");
+  if (params && !aligned(params, 16)) return fail(SCADLES_EINVAL, "params must be 16-byte aligned");
+  if (params && !std::isfinite(lr)) return fail(SCADLES_EINVAL, "lr is not finite");
+  if (energies && !aligned(energies, 8)) return fail(SCADLES_EINVAL, "energies must be 8-byte aligned");
+  if (scadles_status st = check_weights(weights, K)) return st;
+  for (uint32_t j = 0; j < K; ++j) {
+    if (!grads[j] || !idx[j] || !val[j]) return fail(SCADLES_EINVAL, "device %u has a NULL pointer", j);
+    if (!aligned(grads[j], 16)) return fail(SCADLES_EINVAL, "grads[%u] must be 16-byte aligned", j);
+    if (!aligned(idx[j], 4) || !aligned(val[j], 4)) return fail(SCADLES_EINVAL, "device %u outputs misaligned", j);
+    if (k_rule(n, ratios[j]) == 0) return fail(SCADLES_EINVAL, "ratio %g of device %u is not in (0, 1]", ratios[j], j);
+  }
+  Layout L;
+  make_layout(K, n, ratios, g_force_exact.load() != 0, true, L);
+  if (scadles_status st = check_ws(ws, ws_bytes, L.total)) return st;
+  PrepArgs a;
+  memset(&a, 0, sizeof(a));
+  AggArgs g;
+  memset(&g, 0, sizeof(g));
+  uint64_t kmax = 0;
+  for (uint32_t j = 0; j < K; ++j) {
+    a.grad[j] = grads[j];
+    a.idx[j] = idx[j];
+    a.val[j] = val[j];
+    a.k[j] = L.k[j];
+    a.cap[j] = L.cap[j];
+    a.mode[j] = L.mode[j];
+    a.r_lo[j] = L.r_lo[j];
+    a.r_hi[j] = L.r_hi[j];
+    g.idx[j] = idx[j];
+    g.val[j] = val[j];
+    g.dense[j] = grads[j];
+    g.k[j] = L.k[j];
+    g.w[j] = weights[j];
+    if (L.k[j] > kmax) kmax = L.k[j];
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipEvent_t* ev = prof_slot();
+  if (ev) (void)hipEventRecord(ev[0], s);
+  if (scadles_status st = run_select(L, a, ws, delta, energies, compressed, s, ev)) return st;
+  char* b = static_cast<char*>(ws);
+  AggCtx c;
+  memset(&c, 0, sizeof(c));
+  c.st = reinterpret_cast<const DevState*>(b + L.o_st);
+  c.off = reinterpret_cast<uint32_t*>(b + L.o_aoff);
+  c.err = reinterpret_cast<uint32_t*>(b + L.o_aerr);
+  c.out = dense;
+  c.params = params;
+  c.lr = lr;
+  c.K = K;
+  c.ntile = L.ntile;
+  c.kmax = (uint32_t)kmax;
+  c.n = n;
+  hipError_t e = launch_aggregate(g, c, 0, s);
+  if (ev) (void)hipEventRecord(ev[5], s);
+  if (e != hipSuccess) return hip_fail(e, "aggregate launch");
+  return SCADLES_OK;
+}
+
+scadles_status scadles_stream_weights(const double* rates, uint32_t K, double b_min, double b_max, double base_batch,
+                                      float* weights, double* gamma)
+{
+  if (!rates || !weights || K == 0) return fail(SCADLES_EINVAL, "rates and weights must not be NULL, K >= 1");
+  if (std::isnan(b_min) || std::isnan(b_max) || !(b_min <= b_max))
+    return fail(SCADLES_EINVAL, "need b_min <= b_max");
+  double total = 0.0;
+  std::vector<double> b(K);
+  for (uint32_t j = 0; j < K; ++j) {
+    double s = rates[j];
+    if (!std::isfinite(s) || s < 0.0) return fail(SCADLES_EINVAL, "rate %u is negative or not finite", j);
+    if (s < b_min) s = b_min;
+    if (s > b_max) s = b_max;
+    b[j] = s;
+    total += s;
+  }
+  if (!(total > 0.0) || !std::isfinite(total)) return fail(SCADLES_EINVAL, "the bounded rates sum to %g", total);
+  if (gamma && !(base_batch > 0.0)) return fail(SCADLES_EINVAL, "base_batch must be > 0");
+  for (uint32_t j = 0; j < K; ++j) weights[j] = (float)(b[j] / total);
+  if (gamma) *gamma = total / base_batch;
+  return SCADLES_OK;
+}
+
+const char* scadles_last_error(void) { return g_err.c_str(); }
+
+scadles_status scadles_set_option(const char* name, int64_t value)
+{
+  if (!name) return fail(SCADLES_EINVAL, "option name is NULL");
+  if (!strcmp(name, "validate")) g_validate = value ? 1 : 0;
+  else if (!strcmp(name, "force_exact")) g_force_exact = value ? 1 : 0;
+  else if (!strcmp(name, "force_fallback")) g_force_fallback = value ? 1 : 0;
+  else return fail(SCADLES_EINVAL, "unknown option '%s'", name);
+  return SCADLES_OK;
+}
+
+scadles_status scadles_profile_enable(int on)
+{
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (on && g_prof_pool.empty()) {
+    g_prof_pool.resize(kProfMax);
+    for (auto& r : g_prof_pool)
+      for (auto& e : r.ev)
+        if (hipEventCreate(&e) != hipSuccess) {
+          g_prof_pool.clear();
+          return fail(SCADLES_EHIP, "hipEventCreate failed");
+        }
+  }
+  g_prof_on = on != 0;
+  g_prof_used = 0;
+  return SCADLES_OK;
+}
+
+scadles_status scadles_profile_read(double* stage_ms, uint32_t* calls)
+{
+  if (!stage_ms || !calls) return fail(SCADLES_EINVAL, "NULL argument");
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (int i = 0; i < kStages; ++i) stage_ms[i] = 0.0;
+  for (size_t r = 0; r < g_prof_used; ++r) {
+    hipEvent_t* ev = g_prof_pool[r].ev;
+    if (hipEventSynchronize(ev[kStages]) != hipSuccess) return fail(SCADLES_EHIP, "hipEventSynchronize failed");
+    for (int i = 0; i < kStages; ++i) {
+      float ms = 0.f;
+      if (hipEventElapsedTime(&ms, ev[i], ev[i + 1]) == hipSuccess) stage_ms[i] += ms;
+    }
+  }
+  *calls = (uint32_t)g_prof_used;
+  g_prof_used = 0;
+  return SCADLES_OK;
+}
+
+}  // extern "C"

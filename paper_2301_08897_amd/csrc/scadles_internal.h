@@ -1,0 +1,207 @@
+// scadles_internal.h -- device-side structures, constants and primitives of the
+// ScaDLES hot-path kernels for gfx950 (CDNA4, wave64). Internal to libscadles.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace scadles {
+
+// ---- launch geometry --------------------------------------------------------------------
+constexpr int kBlock = 256;            // threads per workgroup (4 wave64)
+constexpr int kWaves = kBlock / 64;
+constexpr int kRound = kBlock * 4;     // elements per "round": one float4 per thread
+constexpr int kTile = 16384;           // main select pass: elements per workgroup (64 KiB)
+constexpr int kTileRounds = kTile / kRound;
+constexpr int kCBlk = 8192;            // candidate blocks (hist/compaction over candidates)
+constexpr int kCBlkRounds = kCBlk / kRound;
+constexpr int kSBlk = 4096;            // sample elements per workgroup
+constexpr int kSChunk = 256;           // contiguous sample chunk (1 KiB)
+constexpr int kBins = 2048;            // radix digit: 11 bits
+constexpr int kDigitBits = 11;
+constexpr int kATile = 4096;           // aggregation tile (positions)
+constexpr int kAStage = 4096;          // aggregation staging entries per round
+constexpr int kMaxK = 64;              // SCADLES_MAX_DEVICES
+constexpr int kSlots = 4;              // selection slots per device
+constexpr int kSlotSampleLo = 0, kSlotSampleHi = 1, kSlotCand = 2, kSlotFull = 3;
+constexpr uint32_t kKeyInf = 0x80000000u;   // above every 31-bit key
+constexpr uint32_t kKeyMask = 0x7FFFFFFFu;
+constexpr uint64_t kSat31 = 0x7FFFFFFFull;
+constexpr int kFullWorkers = 1024;     // grid of the grid-stride exact-path kernels
+
+enum : uint32_t { kModeFast = 0, kModeExact = 1 };
+
+// ---- workspace structures ---------------------------------------------------------------
+struct DevDesc {          // per device, written once per call by the prep kernel
+  const float* grad;
+  uint32_t* idx_out;
+  float* val_out;
+  uint64_t cand_off;      // first element of the device's candidate region
+  uint32_t k;
+  uint32_t cap;           // candidate capacity (0 in exact mode)
+  uint32_t mode;
+  uint32_t r_lo;          // sample ranks that bracket the k-th largest key
+  uint32_t r_hi;          // 0: no upper bracket
+  uint32_t pad;
+};
+
+// State of one radix selection: the key of 1-based descending rank `rank` among
+// the keys in [lo, hi) of some population, decided 11 bits at a time on the
+// offset (key - lo), most significant first.
+struct Sel {
+  uint32_t active;        // a histogram pass is pending
+  uint32_t found;         // finished: result holds the key
+  uint32_t lo, hi;        // band [lo, hi)
+  uint32_t bits;          // low bits of (key - lo) still undecided
+  uint32_t prefix;        // decided high bits of (key - lo)
+  uint32_t result;
+  uint32_t pad;
+  uint64_t rank;          // rank still sought among keys matching the prefix
+  uint64_t above;         // band keys above the prefix range seen so far
+};
+
+struct DevState {
+  Sel sel[kSlots];
+  uint64_t cand, sure;    // main pass totals: keys >= t_lo, keys >= t_hi
+  uint32_t t_lo, t_hi;    // bracket used by the main pass
+  uint32_t fallback;      // 1: the exact full-data path produces this device's output
+  uint32_t band_low;      // candidate select ran on [t_lo, t_hi): add `sure` above it
+  uint32_t thr;           // final threshold key (k-th largest)
+  uint32_t err;           // internal error bits (look-back timeout, select miss)
+  uint64_t c_gt, need;    // keys above thr; keys equal to thr that are kept
+  double e_all, e_kept;
+  uint32_t sparse;        // 1: the device sends Top-k (adaptive rule), 0: dense
+  uint32_t pad2;
+};
+
+// Kernel context: where everything lives in the workspace, plus call scalars.
+struct Ctx {
+  DevDesc* desc;
+  DevState* st;
+  uint32_t* hist;         // [K][kSlots][kBins]
+  uint64_t* status;       // [K][tpd] look-back words of the main pass
+  double* epart;          // [K][tpd] sum of squares per main tile
+  uint32_t* cand_idx;     // candidate regions
+  float* cand_val;
+  uint64_t* blk_cnt;      // [K][nbmax] packed (gt | eq << 32) per compaction block
+  uint64_t* blk_pre;      // [K][nbmax] exclusive prefix of blk_cnt
+  double* blk_e;          // [K][nbmax] kept sum of squares per compaction block
+  uint32_t* ticket;       // main pass tile ticket
+  double* energies_out;   // caller's (dev, 2K) or null
+  uint8_t* compressed_out;// caller's (dev, K) or null
+  uint64_t n;
+  uint32_t K;
+  uint32_t tpd;           // main tiles per device
+  uint32_t ncb;           // candidate blocks per device (max over devices)
+  uint32_t nfb;           // exact-path compaction blocks per device: ceil(n / kCBlk)
+  uint32_t nbmax;         // max(ncb, nfb)
+  uint32_t s_stride;      // sample chunk stride (elements)
+  uint32_t s_n;           // sample elements per device
+  uint32_t force_fallback;
+  double delta;
+};
+
+// Per-call parameters that only the prep kernel needs (passed by value).
+struct PrepArgs {
+  const float* grad[kMaxK];
+  uint32_t* idx[kMaxK];
+  float* val[kMaxK];
+  uint32_t k[kMaxK];
+  uint32_t cap[kMaxK];
+  uint32_t mode[kMaxK];
+  uint32_t r_lo[kMaxK];
+  uint32_t r_hi[kMaxK];
+};
+
+// Aggregation context.
+struct AggArgs {
+  const uint32_t* idx[kMaxK];   // sparse sets (null: dense)
+  const float* val[kMaxK];
+  const float* dense[kMaxK];    // dense gradient used when the device is dense
+  uint32_t k[kMaxK];
+  float w[kMaxK];
+};
+
+struct AggCtx {
+  const DevState* st;     // fused path: per-device sparse/dense decision; null otherwise
+  uint32_t* off;          // [K][ntile + 1] survivor offset of each tile start
+  uint32_t* err;          // validation flag
+  float* out;             // dense aggregate
+  float* params;          // null: no SGD
+  float lr;
+  uint32_t K;
+  uint32_t ntile;
+  uint32_t kmax;
+  uint64_t n;
+};
+
+// Launch plan of the selection pipeline (host side).
+struct SelectPlan {
+  uint32_t any_fast;          // some device takes the sampled single-read path
+  uint32_t sample_blocks;     // sample workgroups per device
+  uint32_t ncand_blocks;      // K * ncb candidate workgroups, or 0
+  uint32_t full_workers;      // grid-stride workgroups of the exact full-data path
+};
+
+// Launchers (select.hip, aggregate.hip). `ev`, when not null, receives events
+// at the stage boundaries 1..4 of the selection.
+hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipEvent_t* ev);
+hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate, hipStream_t s);
+hipError_t launch_sgd(float* p, const float* g, uint64_t n, float lr, hipStream_t s);
+
+// ---- sizing shared by host and device -----------------------------------------------------
+__host__ __device__ inline uint32_t bitlen32(uint32_t x) { return x ? 32u - (uint32_t)__builtin_clz(x) : 0u; }
+
+__host__ __device__ inline uint32_t ceil_div_u64(uint64_t a, uint64_t b) { return (uint32_t)((a + b - 1) / b); }
+
+// ---- device primitives ------------------------------------------------------------------
+__device__ inline uint32_t key_of(float x) { return __float_as_uint(x) & kKeyMask; }
+
+__device__ inline uint32_t lane_id() { return threadIdx.x & 63; }
+
+__device__ inline uint64_t ballot(bool p) { return __ballot(p); }
+
+// Set bits of `mask` in lanes below the calling lane.
+__device__ inline uint32_t mbcnt(uint64_t mask)
+{
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+__device__ inline uint32_t wave_incl_scan(uint32_t v)
+{
+  const uint32_t l = lane_id();
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    uint32_t t = __shfl_up(v, d, 64);
+    if (l >= (uint32_t)d) v += t;
+  }
+  return v;
+}
+
+__device__ inline uint64_t wave_sum_u64(uint64_t v)
+{
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+  return v;
+}
+
+__device__ inline double wave_sum_f64(double v)
+{
+  // Butterfly: every lane ends with the same value, summed in a fixed pattern.
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+  return v;
+}
+
+// Fixed-order block sum of one double per thread (deterministic).
+__device__ inline double block_sum_f64(double v, double* lds4)
+{
+  v = wave_sum_f64(v);
+  if (lane_id() == 0) lds4[threadIdx.x >> 6] = v;
+  __syncthreads();
+  double r = ((lds4[0] + lds4[1]) + (lds4[2] + lds4[3]));
+  __syncthreads();
+  return r;
+}
+
+}  // namespace scadles

@@ -1,0 +1,823 @@
+// select.hip -- Top-k selection kernels for gfx950.
+//
+// Top-k sparsification (§III-C, §IV "High communication cost" of ScaDLES,
+// arXiv 2301.08897) keeps, per device, the k entries of largest |g| (ties to
+// the lower index) in ascending index order. Magnitudes are ranked as the
+// 31-bit integer key bits(g) & 0x7FFFFFFF, whose order is that of |g| for
+// finite values, so every decision below is exact integer work.
+//
+// Fast path (one read of every gradient):
+//   1. bracket   : a systematic sample (256-element chunks at a fixed stride)
+//                  is radix-selected at two ranks around k * (sample/n), giving
+//                  keys t_lo <= (k-th largest key) < t_hi with high probability;
+//   2. main pass : every gradient is read once; keys >= t_lo are written as
+//                  candidates (idx, val) in index order, each tile finding its
+//                  output offset by decoupled look-back; sum g^2 is fused in;
+//   3. threshold : the exact k-th largest key is radix-selected among the
+//                  candidates in [t_lo, t_hi) (or above t_hi);
+//   4. compaction: the kept set -- keys above the threshold plus the lowest-
+//                  indexed `need` keys equal to it -- is written in index order.
+// If the bracket missed (fewer than k candidates) or the candidates overflow
+// their region, the device falls back to the exact path: a radix select over
+// all of its data, then the same ordered compaction over its data.
+#include "scadles_internal.h"
+
+namespace scadles {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
+constexpr uint32_t kSpinLimit = 1u << 20;
+constexpr uint64_t kFlagA = 1, kFlagP = 2;
+
+__device__ inline f4 ld_stream4(const float* p) { return __builtin_nontemporal_load(reinterpret_cast<const f4*>(p)); }
+__device__ inline f4 ld4(const float* p) { return *reinterpret_cast<const f4*>(p); }
+__device__ inline u4 ldu4(const uint32_t* p) { return *reinterpret_cast<const u4*>(p); }
+
+// Loads elements [e, e+4) of a row of `rem` valid elements; invalid lanes read 0.
+__device__ inline f4 load4_guarded(const float* row, uint64_t e, uint64_t rem, bool stream)
+{
+  if (e + 4 <= rem) return stream ? ld_stream4(row + e) : ld4(row + e);
+  f4 v = {0.f, 0.f, 0.f, 0.f};
+  if (e + 0 < rem) v.x = row[e + 0];
+  if (e + 1 < rem) v.y = row[e + 1];
+  if (e + 2 < rem) v.z = row[e + 2];
+  if (e + 3 < rem) v.w = row[e + 3];
+  return v;
+}
+
+__device__ inline float comp(const f4& v, int c) { return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w; }
+__device__ inline uint32_t compu(const u4& v, int c) { return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w; }
+
+__device__ inline uint64_t atomic_load_u64(const uint64_t* p)
+{
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void atomic_store_u64(uint64_t* p, uint64_t v)
+{
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---- radix-selection digit view ------------------------------------------------------------
+struct SelView {
+  uint32_t lo, hi, shift, width, prefix;
+};
+
+__device__ inline SelView view_of(const Sel& s)
+{
+  SelView v;
+  v.lo = s.lo;
+  v.hi = s.hi;
+  v.width = s.bits < (uint32_t)kDigitBits ? s.bits : (uint32_t)kDigitBits;
+  v.shift = s.bits - v.width;
+  v.prefix = s.prefix;
+  return v;
+}
+
+// Digit of `key` for the pending pass, if the key is in the band and matches the
+// digits decided so far.
+__device__ inline bool sel_digit(const SelView& v, uint32_t key, uint32_t& d)
+{
+  if (key < v.lo || key >= v.hi) return false;
+  const uint32_t o = key - v.lo;
+  if ((o >> (v.shift + v.width)) != v.prefix) return false;
+  d = (o >> v.shift) & ((1u << v.width) - 1u);
+  return true;
+}
+
+// Bracket of the main pass from the sample selections.
+__device__ inline void bracket_of(const DevDesc& d, const DevState& s, uint32_t& tlo, uint32_t& thi)
+{
+  if (d.mode != kModeFast) {
+    tlo = thi = kKeyInf;
+    return;
+  }
+  tlo = s.sel[kSlotSampleLo].found ? s.sel[kSlotSampleLo].result : 0u;
+  thi = s.sel[kSlotSampleHi].found ? s.sel[kSlotSampleHi].result + 1u : kKeyInf;
+  if (thi <= tlo) thi = kKeyInf;
+}
+
+// Threshold, count above it and ties kept, from whichever selection decided it.
+__device__ inline bool threshold_of(const DevState& s, uint32_t& thr, uint64_t& need)
+{
+  const Sel& sel = s.fallback ? s.sel[kSlotFull] : s.sel[kSlotCand];
+  if (!sel.found) {
+    thr = kKeyInf;
+    need = 0;
+    return false;
+  }
+  thr = sel.result;
+  need = sel.rank;
+  return true;
+}
+
+__device__ inline void flush_hist(const uint32_t* h, uint32_t* g, int nb)
+{
+  for (int b = threadIdx.x; b < nb; b += kBlock) {
+    uint32_t v = h[b];
+    if (v) atomicAdd(g + b, v);
+  }
+}
+
+// ---- 0. per-call preparation -----------------------------------------------------------------
+__global__ __launch_bounds__(kBlock) void k_prep(Ctx c, PrepArgs a)
+{
+  const uint32_t K = c.K;
+  if (blockIdx.x == 0 && threadIdx.x < K) {
+    const uint32_t j = threadIdx.x;
+    uint64_t off = 0;
+    for (uint32_t i = 0; i < j; ++i) off += a.cap[i];
+    DevDesc d;
+    d.grad = a.grad[j];
+    d.idx_out = a.idx[j];
+    d.val_out = a.val[j];
+    d.cand_off = off;
+    d.k = a.k[j];
+    d.cap = a.cap[j];
+    d.mode = a.mode[j];
+    d.r_lo = a.r_lo[j];
+    d.r_hi = a.r_hi[j];
+    d.pad = 0;
+    c.desc[j] = d;
+    DevState s;
+    __builtin_memset(&s, 0, sizeof(s));
+    s.t_lo = s.t_hi = kKeyInf;
+    s.thr = kKeyInf;
+    if (d.mode == kModeFast) {
+      Sel& lo = s.sel[kSlotSampleLo];
+      lo.active = 1;
+      lo.lo = 0;
+      lo.hi = kKeyInf;
+      lo.bits = 31;
+      lo.rank = d.r_lo;
+      if (d.r_hi >= 1) {
+        Sel& hi = s.sel[kSlotSampleHi];
+        hi.active = 1;
+        hi.lo = 0;
+        hi.hi = kKeyInf;
+        hi.bits = 31;
+        hi.rank = d.r_hi;
+      }
+    }
+    c.st[j] = s;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *c.ticket = 0u;
+  const uint64_t nh = (uint64_t)K * kSlots * kBins;
+  const uint64_t ns = (uint64_t)K * c.tpd;
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < nh; i += stride) c.hist[i] = 0u;
+  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < ns; i += stride) c.status[i] = 0ull;
+}
+
+// ---- 1. bracket: histogram pass over the systematic sample (two selections) ----------------
+__global__ __launch_bounds__(kBlock) void k_hist_sample(Ctx c)
+{
+  __shared__ uint32_t h[2][kBins];
+  const uint32_t j = blockIdx.y;
+  const DevDesc& d = c.desc[j];
+  if (d.mode != kModeFast) return;
+  const Sel s0 = c.st[j].sel[kSlotSampleLo];
+  const Sel s1 = c.st[j].sel[kSlotSampleHi];
+  if (!s0.active && !s1.active) return;
+  const uint64_t e0 = (uint64_t)blockIdx.x * kSBlk;
+  if (e0 >= c.s_n) return;
+  for (int b = threadIdx.x; b < 2 * kBins; b += kBlock) (&h[0][0])[b] = 0u;
+  __syncthreads();
+  const SelView v0 = view_of(s0), v1 = view_of(s1);
+  const uint64_t e1 = (e0 + kSBlk < c.s_n) ? e0 + kSBlk : c.s_n;
+  for (uint64_t e = e0 + threadIdx.x * 4; e < e1; e += kRound) {
+    const uint64_t chunk = e / kSChunk, within = e % kSChunk;
+    const float* row = d.grad + chunk * c.s_stride + within;
+    const f4 x = load4_guarded(row, 0, e1 - e, false);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (e + q >= e1) break;
+      const uint32_t key = key_of(comp(x, q));
+      uint32_t dg;
+      if (s0.active && sel_digit(v0, key, dg)) atomicAdd(&h[0][dg], 1u);
+      if (s1.active && sel_digit(v1, key, dg)) atomicAdd(&h[1][dg], 1u);
+    }
+  }
+  __syncthreads();
+  if (s0.active) flush_hist(h[0], c.hist + ((uint64_t)j * kSlots + kSlotSampleLo) * kBins, kBins);
+  if (s1.active) flush_hist(h[1], c.hist + ((uint64_t)j * kSlots + kSlotSampleHi) * kBins, kBins);
+}
+
+// ---- radix digit decision for slots [s0, s1) of one device (one wave) -----------------------
+__global__ __launch_bounds__(64) void k_find(Ctx c, int s_begin, int s_end)
+{
+  const uint32_t j = blockIdx.x, l = lane_id();
+  for (int s = s_begin; s < s_end; ++s) {
+    Sel sel = c.st[j].sel[s];
+    if (!sel.active) continue;
+    uint32_t* h = c.hist + ((uint64_t)j * kSlots + s) * kBins;
+    const uint32_t w = sel.bits < (uint32_t)kDigitBits ? sel.bits : (uint32_t)kDigitBits;
+    const int nb = 1 << w;
+    const int per = (nb + 63) / 64;
+    const int b_hi = nb - (int)l * per;           // this lane covers bins [b_lo, b_hi), top first
+    const int b_lo = b_hi - per > 0 ? b_hi - per : 0;
+    uint32_t sum = 0;
+    for (int b = b_lo; b < b_hi; ++b) sum += h[b];
+    const uint32_t incl = wave_incl_scan(sum);
+    const uint32_t excl = incl - sum;
+    const bool hit = (uint64_t)excl < sel.rank && sel.rank <= (uint64_t)incl;
+    const uint64_t m = ballot(hit);
+    uint32_t dsel = 0, cum = excl;
+    if (hit) {
+      for (int b = b_hi - 1; b >= b_lo; --b) {
+        if ((uint64_t)cum + h[b] >= sel.rank) {
+          dsel = (uint32_t)b;
+          break;
+        }
+        cum += h[b];
+      }
+    }
+    const int src = m ? __builtin_ctzll(m) : 0;
+    dsel = __shfl(dsel, src, 64);
+    cum = __shfl(cum, src, 64);
+    if (l == 0) {
+      if (!m) {
+        sel.active = 0;
+        sel.found = 0;
+        c.st[j].err |= 2u;
+      } else {
+        sel.rank -= cum;
+        sel.above += cum;
+        sel.prefix = (sel.prefix << w) | dsel;
+        sel.bits -= w;
+        if (sel.bits == 0) {
+          sel.active = 0;
+          sel.found = 1;
+          sel.result = sel.lo + sel.prefix;
+        }
+      }
+      c.st[j].sel[s] = sel;
+    }
+    for (int b = l; b < kBins; b += 64) h[b] = 0u;
+  }
+}
+
+// ---- 2. main pass: one read of every gradient ------------------------------------------------
+// Decoupled look-back over the tiles of one device (Merrill & Garland, 2016):
+// each tile publishes its own counts at once, then sums its predecessors'
+// until it meets an inclusive prefix. Status word: flag(2) | sure(31) | cand(31),
+// saturating at 2^31 - 1 (a saturated count always exceeds the capacity).
+// Tiles take their number from a ticket in start order, so every tile waited on
+// has started and never waits on a later tile; the spin is bounded anyway and a
+// timeout sends the device to the exact path.
+__device__ inline uint64_t lb_pack(uint64_t flag, uint64_t cand, uint64_t sure)
+{
+  cand = cand < kSat31 ? cand : kSat31;
+  sure = sure < kSat31 ? sure : kSat31;
+  return (flag << 62) | (sure << 31) | cand;
+}
+
+__device__ inline void lookback(uint64_t* stat, uint32_t tile, uint64_t cand, uint64_t sure, uint64_t& ex_c,
+                                uint64_t& ex_s, uint32_t* err)
+{
+  const uint32_t l = lane_id();
+  ex_c = ex_s = 0;
+  if (tile == 0) {
+    if (l == 0) atomic_store_u64(&stat[0], lb_pack(kFlagP, cand, sure));
+    return;
+  }
+  if (l == 0) atomic_store_u64(&stat[tile], lb_pack(kFlagA, cand, sure));
+  int64_t end = (int64_t)tile - 1;
+  uint32_t spins = 0;
+  while (true) {
+    const int64_t p = end - (int64_t)l;
+    const uint64_t s = (p >= 0) ? atomic_load_u64(&stat[p]) : lb_pack(kFlagP, 0, 0);
+    const uint32_t f = (uint32_t)(s >> 62);
+    const uint64_t pm = ballot(f == kFlagP), xm = ballot(f == 0);
+    const uint32_t fp = pm ? (uint32_t)__builtin_ctzll(pm) : 64u;
+    const uint64_t needed = (fp >= 63) ? ~0ull : ((2ull << fp) - 1ull);
+    if (xm & needed) {
+      if (++spins > kSpinLimit) {
+        if (l == 0) atomicOr(err, 1u);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+      continue;
+    }
+    const uint64_t vc = (l <= fp) ? (s & kSat31) : 0ull;
+    const uint64_t vs = (l <= fp) ? ((s >> 31) & kSat31) : 0ull;
+    ex_c += wave_sum_u64(vc);
+    ex_s += wave_sum_u64(vs);
+    if (fp < 64) break;
+    end -= 64;
+  }
+  if (l == 0) atomic_store_u64(&stat[tile], lb_pack(kFlagP, cand + ex_c, sure + ex_s));
+}
+
+// Element order inside a workgroup: wave w owns the contiguous chunk
+// [w*R*256, (w+1)*R*256); in round r lane l holds elements r*256 + 4l .. +3.
+// Every load is one contiguous KiB per wave, and index order is (wave, round,
+// lane, component), so a wave can keep a running output offset.
+template <int R>
+__device__ inline uint64_t elem_of(uint32_t w, int r, uint32_t l)
+{
+  return (uint64_t)w * (R * 256) + (uint64_t)r * 256 + l * 4;
+}
+
+// Exclusive per-wave prefix and block total of one packed (lo16 | hi16 << 16)
+// per-lane count; lds needs 8 words.
+__device__ inline uint32_t wave_prefix_of_block(uint32_t packed_lane, uint32_t* lds, uint32_t& total)
+{
+  const uint32_t w = threadIdx.x >> 6;
+  uint32_t t = packed_lane;
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) t += __shfl_xor(t, d, 64);
+  if (lane_id() == 0) lds[w] = t;
+  __syncthreads();
+  uint32_t ex = 0;
+  for (uint32_t i = 0; i < w; ++i) ex += lds[i];
+  total = lds[0] + lds[1] + lds[2] + lds[3];
+  __syncthreads();
+  return ex;
+}
+
+__global__ __launch_bounds__(kBlock) void k_main(Ctx c)
+{
+  __shared__ uint32_t s_ticket;
+  __shared__ uint32_t lds[8];
+  __shared__ uint64_t s_ex;
+  __shared__ double s_e[4];
+  const uint32_t tid = threadIdx.x, l = lane_id(), w = tid >> 6;
+  if (tid == 0) s_ticket = atomicAdd(c.ticket, 1u);
+  __syncthreads();
+  const uint32_t t = s_ticket;
+  const uint32_t j = t / c.tpd, tile = t - j * c.tpd;
+  const DevDesc d = c.desc[j];
+  uint32_t tlo, thi;
+  bracket_of(d, c.st[j], tlo, thi);
+  const uint64_t base = (uint64_t)tile * kTile;
+  const uint64_t rem = c.n - base;
+  const float* row = d.grad + base;
+
+  f4 v[kTileRounds];
+#pragma unroll
+  for (int r = 0; r < kTileRounds; ++r) v[r] = load4_guarded(row, elem_of<kTileRounds>(w, r, l), rem, true);
+
+  // Phase 1: sum of squares and per-lane counts of candidates / sure keys.
+  // Elements past the end load as +0 (key 0): they can only pass `key >= tlo`
+  // when tlo == 0, and then every real element passes too, so the count
+  // reaches n > cap and the device takes the exact path regardless.
+  double e2a = 0.0, e2b = 0.0;
+  uint32_t cnt = 0;
+#pragma unroll
+  for (int r = 0; r < kTileRounds; ++r) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float x = comp(v[r], q);
+      if (q & 1) e2b = __builtin_fma((double)x, (double)x, e2b);
+      else e2a = __builtin_fma((double)x, (double)x, e2a);
+      const uint32_t key = key_of(x);
+      cnt += (key >= tlo) ? 1u : 0u;
+      cnt += (key >= thi) ? 0x10000u : 0u;
+    }
+  }
+  uint32_t tot;
+  const uint32_t wex = wave_prefix_of_block(cnt, lds, tot);
+  if (w == 0) {
+    uint64_t ex_c, ex_s;
+    lookback(c.status + (uint64_t)j * c.tpd, tile, tot & 0xFFFFu, tot >> 16, ex_c, ex_s, &c.st[j].err);
+    if (l == 0) s_ex = ex_c;
+  }
+  __syncthreads();
+
+  // Phase 2: candidates in index order at the tile's offset.
+  if ((tot & 0xFFFFu) != 0u) {
+    uint64_t run = s_ex + (wex & 0xFFFFu);
+    uint32_t* cidx = c.cand_idx + d.cand_off;
+    float* cval = c.cand_val + d.cand_off;
+#pragma unroll
+    for (int r = 0; r < kTileRounds; ++r) {
+      const uint64_t e = elem_of<kTileRounds>(w, r, l);
+      bool f[4];
+      uint64_t b[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        f[q] = key_of(comp(v[r], q)) >= tlo;
+        b[q] = ballot(f[q]);
+      }
+      if ((b[0] | b[1] | b[2] | b[3]) == 0ull) continue;
+      uint64_t pos = run + mbcnt(b[0]) + mbcnt(b[1]) + mbcnt(b[2]) + mbcnt(b[3]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (f[q]) {
+          if (pos < d.cap) {
+            cidx[pos] = (uint32_t)(base + e + q);
+            cval[pos] = comp(v[r], q);
+          }
+          ++pos;
+        }
+      }
+      run += __builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) + __builtin_popcountll(b[2]) +
+             __builtin_popcountll(b[3]);
+    }
+  }
+  const double es = block_sum_f64(e2a + e2b, s_e);
+  if (tid == 0) c.epart[(uint64_t)j * c.tpd + tile] = es;
+}
+
+// ---- after the main pass: energies, candidate totals, path decision ---------------------------
+__global__ __launch_bounds__(kBlock) void k_post(Ctx c)
+{
+  __shared__ double s_e[4];
+  const uint32_t j = blockIdx.x;
+  double acc = 0.0;
+  for (uint32_t t = threadIdx.x; t < c.tpd; t += kBlock) acc += c.epart[(uint64_t)j * c.tpd + t];
+  const double e_all = block_sum_f64(acc, s_e);
+  if (threadIdx.x != 0) return;
+  DevState& s = c.st[j];
+  const DevDesc d = c.desc[j];
+  s.e_all = e_all;
+  bool fb = (d.mode != kModeFast) || c.force_fallback;
+  uint32_t tlo, thi;
+  bracket_of(d, s, tlo, thi);
+  s.t_lo = tlo;
+  s.t_hi = thi;
+  if (d.mode == kModeFast) {
+    const uint64_t wd = c.status[(uint64_t)j * c.tpd + c.tpd - 1];
+    if ((wd >> 62) != kFlagP) s.err |= 4u;
+    s.cand = wd & kSat31;
+    s.sure = (wd >> 31) & kSat31;
+    if (s.err) fb = true;
+    if (s.cand < d.k || s.cand > d.cap) fb = true;
+  }
+  Sel sel;
+  __builtin_memset(&sel, 0, sizeof(sel));
+  sel.active = 1;
+  if (fb) {
+    s.fallback = 1;
+    sel.lo = 0;
+    sel.hi = kKeyInf;
+    sel.bits = 31;
+    sel.rank = d.k;
+    s.sel[kSlotFull] = sel;
+  } else {
+    s.fallback = 0;
+    if (s.sure < d.k) {
+      sel.lo = tlo;
+      sel.hi = thi;
+      sel.rank = d.k - s.sure;
+      s.band_low = 1;
+    } else {
+      sel.lo = thi;
+      sel.hi = kKeyInf;
+      sel.rank = d.k;
+      s.band_low = 0;
+    }
+    const uint32_t b = bitlen32(sel.hi - sel.lo - 1u);
+    sel.bits = b ? b : 1u;
+    s.sel[kSlotCand] = sel;
+  }
+}
+
+// ---- 3. histogram pass over candidates (fast devices) and full data (exact devices) ----------
+__global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks)
+{
+  __shared__ uint32_t h[kBins];
+  if (blockIdx.x < ncand_blocks) {
+    const uint32_t j = blockIdx.x / c.ncb, b = blockIdx.x - j * c.ncb;
+    const DevState& s = c.st[j];
+    if (s.fallback) return;
+    const Sel sel = s.sel[kSlotCand];
+    if (!sel.active) return;
+    const uint64_t cnt = s.cand;
+    const uint64_t q0 = (uint64_t)b * kCBlk;
+    if (q0 >= cnt) return;
+    for (int i = threadIdx.x; i < kBins; i += kBlock) h[i] = 0u;
+    __syncthreads();
+    const SelView sv = view_of(sel);
+    const uint64_t rem = (cnt - q0 < (uint64_t)kCBlk) ? cnt - q0 : (uint64_t)kCBlk;
+    const float* cv = c.cand_val + c.desc[j].cand_off + q0;
+#pragma unroll 2
+    for (int r = 0; r < kCBlkRounds; ++r) {
+      const uint64_t e = (uint64_t)r * kRound + threadIdx.x * 4;
+      if (e >= rem) break;
+      const f4 x = load4_guarded(cv, e, rem, false);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t dg;
+        if (e + q < rem && sel_digit(sv, key_of(comp(x, q)), dg)) atomicAdd(&h[dg], 1u);
+      }
+    }
+    __syncthreads();
+    flush_hist(h, c.hist + ((uint64_t)j * kSlots + kSlotCand) * kBins, kBins);
+    return;
+  }
+  const uint32_t worker = blockIdx.x - ncand_blocks, G = gridDim.x - ncand_blocks;
+  for (uint32_t j = 0; j < c.K; ++j) {
+    const DevState& s = c.st[j];
+    if (!s.fallback) continue;
+    const Sel sel = s.sel[kSlotFull];
+    if (!sel.active) continue;
+    if (worker >= c.tpd) continue;
+    for (int i = threadIdx.x; i < kBins; i += kBlock) h[i] = 0u;
+    __syncthreads();
+    const SelView sv = view_of(sel);
+    const float* grad = c.desc[j].grad;
+    for (uint32_t tile = worker; tile < c.tpd; tile += G) {
+      const uint64_t base = (uint64_t)tile * kTile;
+      const uint64_t rem = c.n - base;
+#pragma unroll 4
+      for (int r = 0; r < kTileRounds; ++r) {
+        const uint64_t e = (uint64_t)r * kRound + threadIdx.x * 4;
+        const f4 x = load4_guarded(grad + base, e, rem, true);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint32_t dg;
+          if (e + q < rem && sel_digit(sv, key_of(comp(x, q)), dg)) atomicAdd(&h[dg], 1u);
+        }
+      }
+    }
+    __syncthreads();
+    flush_hist(h, c.hist + ((uint64_t)j * kSlots + kSlotFull) * kBins, kBins);
+    __syncthreads();
+  }
+}
+
+// ---- 4. ordered compaction -------------------------------------------------------------------
+// Blocks are kCBlk elements of a device's candidate list (fast path) or of its
+// gradient (exact path), in index order. Elements past the end load as +0: a
+// pad is never above the threshold, and when it equals it (threshold key 0) it
+// comes after every real element, whose equal keys already reach `need`, so
+// it is never kept and only inflates the last block's own count.
+// Per block: counts of keys above the threshold (gt) and equal to it (eq).
+template <int R>
+__device__ inline uint64_t block_gt_eq(const float* src, uint64_t rem, uint32_t thr, uint32_t* lds)
+{
+  const uint32_t w = threadIdx.x >> 6, l = lane_id();
+  uint32_t gt = 0, eq = 0;
+#pragma unroll 4
+  for (int r = 0; r < R; ++r) {
+    const uint64_t e = elem_of<R>(w, r, l);
+    if (e < rem) {
+      const f4 x = load4_guarded(src, e, rem, false);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t key = key_of(comp(x, q));
+        gt += (key > thr) ? 1u : 0u;
+        eq += (key == thr) ? 1u : 0u;
+      }
+    }
+  }
+  uint32_t tg, te;
+  wave_prefix_of_block(gt, lds, tg);
+  wave_prefix_of_block(eq, lds, te);
+  return (uint64_t)tg | ((uint64_t)te << 32);
+}
+
+__global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c, uint32_t ncand_blocks)
+{
+  __shared__ uint32_t lds[8];
+  if (blockIdx.x < ncand_blocks) {
+    const uint32_t j = blockIdx.x / c.ncb, b = blockIdx.x - j * c.ncb;
+    const DevState& s = c.st[j];
+    if (s.fallback) return;
+    const uint64_t q0 = (uint64_t)b * kCBlk;
+    if (q0 >= s.cand) return;
+    uint32_t thr;
+    uint64_t need;
+    threshold_of(s, thr, need);
+    const uint64_t rem = (s.cand - q0 < (uint64_t)kCBlk) ? s.cand - q0 : (uint64_t)kCBlk;
+    const uint64_t r = block_gt_eq<kCBlkRounds>(c.cand_val + c.desc[j].cand_off + q0, rem, thr, lds);
+    if (threadIdx.x == 0) c.blk_cnt[(uint64_t)j * c.nbmax + b] = r;
+    return;
+  }
+  const uint32_t worker = blockIdx.x - ncand_blocks, G = gridDim.x - ncand_blocks;
+  for (uint32_t j = 0; j < c.K; ++j) {
+    const DevState& s = c.st[j];
+    if (!s.fallback) continue;
+    uint32_t thr;
+    uint64_t need;
+    threshold_of(s, thr, need);
+    const float* grad = c.desc[j].grad;
+    for (uint32_t blk = worker; blk < c.nfb; blk += G) {
+      const uint64_t base = (uint64_t)blk * kCBlk;
+      const uint64_t rem = (c.n - base < (uint64_t)kCBlk) ? c.n - base : (uint64_t)kCBlk;
+      const uint64_t r = block_gt_eq<kCBlkRounds>(grad + base, rem, thr, lds);
+      if (threadIdx.x == 0) c.blk_cnt[(uint64_t)j * c.nbmax + blk] = r;
+    }
+  }
+}
+
+__device__ inline uint64_t wave_incl_scan_u64(uint64_t v)
+{
+  const uint32_t l = lane_id();
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    uint64_t t = __shfl_up(v, d, 64);
+    if (l >= (uint32_t)d) v += t;
+  }
+  return v;
+}
+
+__device__ inline uint32_t blocks_of(const Ctx& c, const DevState& s)
+{
+  return s.fallback ? c.nfb : ceil_div_u64(s.cand, kCBlk);
+}
+
+// Exclusive prefix of the packed block counts of one device.
+__global__ __launch_bounds__(kBlock) void k_scan(Ctx c)
+{
+  __shared__ uint64_t s_w[4];
+  const uint32_t j = blockIdx.x, tid = threadIdx.x;
+  const uint32_t nb = blocks_of(c, c.st[j]);
+  const uint64_t* cnt = c.blk_cnt + (uint64_t)j * c.nbmax;
+  uint64_t* pre = c.blk_pre + (uint64_t)j * c.nbmax;
+  const uint32_t per = (nb + kBlock - 1) / kBlock;
+  const uint32_t b0 = tid * per, b1 = (b0 + per < nb) ? b0 + per : nb;
+  uint64_t sum = 0;
+  for (uint32_t b = b0; b < b1; ++b) sum += cnt[b];
+  const uint64_t incl = wave_incl_scan_u64(sum);
+  if (lane_id() == 63) s_w[tid >> 6] = incl;
+  __syncthreads();
+  uint64_t base = 0;
+  for (uint32_t i = 0; i < (tid >> 6); ++i) base += s_w[i];
+  uint64_t run = base + incl - sum;
+  for (uint32_t b = b0; b < b1; ++b) {
+    pre[b] = run;
+    run += cnt[b];
+  }
+}
+
+// Writes the kept entries of one block in index order.
+//   kept: key > thr, or key == thr with fewer than `need` equal keys before it;
+//   position: (keys > thr before it) + min(equal keys before it, need).
+template <int R>
+__device__ inline double block_write(const float* src, const uint32_t* src_idx, uint64_t idx_base, uint64_t rem,
+                                     uint32_t thr, uint64_t need, uint64_t pre, uint32_t k, uint32_t* out_idx,
+                                     float* out_val, uint32_t* lds)
+{
+  const uint32_t w = threadIdx.x >> 6, l = lane_id();
+  f4 x[R];
+  uint32_t cnt = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const uint64_t e = elem_of<R>(w, r, l);
+    x[r] = (e < rem) ? load4_guarded(src, e, rem, false) : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t key = key_of(comp(x[r], q));
+      cnt += (key > thr) ? 1u : 0u;
+      cnt += (key == thr) ? 0x10000u : 0u;
+    }
+  }
+  uint32_t tot;
+  const uint32_t wex = wave_prefix_of_block(cnt, lds, tot);
+  uint64_t run_g = (pre & 0xFFFFFFFFull) + (wex & 0xFFFFu);
+  uint64_t run_e = (pre >> 32) + (wex >> 16);
+  double e2 = 0.0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const uint64_t e = elem_of<R>(w, r, l);
+    bool fg[4], fe[4];
+    uint64_t bg[4], be[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t key = key_of(comp(x[r], q));
+      fg[q] = key > thr;
+      fe[q] = key == thr;
+      bg[q] = ballot(fg[q]);
+      be[q] = ballot(fe[q]);
+    }
+    if ((bg[0] | bg[1] | bg[2] | bg[3] | be[0] | be[1] | be[2] | be[3]) == 0ull) continue;
+    uint64_t gt_b = run_g + mbcnt(bg[0]) + mbcnt(bg[1]) + mbcnt(bg[2]) + mbcnt(bg[3]);
+    uint64_t eq_b = run_e + mbcnt(be[0]) + mbcnt(be[1]) + mbcnt(be[2]) + mbcnt(be[3]);
+    u4 ix = {0u, 0u, 0u, 0u};
+    if (src_idx && e < rem) {
+      if (e + 4 <= rem) ix = ldu4(src_idx + e);
+      else
+        for (int q = 0; q < 4; ++q)
+          if (e + q < rem) ix[q] = src_idx[e + q];
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bool keep = fg[q] || (fe[q] && eq_b < need);
+      if (keep) {
+        const uint64_t pos = gt_b + (eq_b < need ? eq_b : need);
+        const float val = comp(x[r], q);
+        if (pos < k) {
+          out_idx[pos] = src_idx ? compu(ix, q) : (uint32_t)(idx_base + e + q);
+          out_val[pos] = val;
+        }
+        e2 = __builtin_fma((double)val, (double)val, e2);
+      }
+      gt_b += fg[q];
+      eq_b += fe[q];
+    }
+    run_g += __builtin_popcountll(bg[0]) + __builtin_popcountll(bg[1]) + __builtin_popcountll(bg[2]) +
+             __builtin_popcountll(bg[3]);
+    run_e += __builtin_popcountll(be[0]) + __builtin_popcountll(be[1]) + __builtin_popcountll(be[2]) +
+             __builtin_popcountll(be[3]);
+  }
+  return e2;
+}
+
+__global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c, uint32_t ncand_blocks)
+{
+  __shared__ uint32_t lds[8];
+  __shared__ double s_e[4];
+  if (blockIdx.x < ncand_blocks) {
+    const uint32_t j = blockIdx.x / c.ncb, b = blockIdx.x - j * c.ncb;
+    const DevState& s = c.st[j];
+    if (s.fallback) return;
+    const uint64_t q0 = (uint64_t)b * kCBlk;
+    if (q0 >= s.cand) return;
+    uint32_t thr;
+    uint64_t need;
+    threshold_of(s, thr, need);
+    const DevDesc d = c.desc[j];
+    const uint64_t rem = (s.cand - q0 < (uint64_t)kCBlk) ? s.cand - q0 : (uint64_t)kCBlk;
+    const double e2 = block_write<kCBlkRounds>(c.cand_val + d.cand_off + q0, c.cand_idx + d.cand_off + q0, 0, rem,
+                                               thr, need, c.blk_pre[(uint64_t)j * c.nbmax + b], d.k, d.idx_out,
+                                               d.val_out, lds);
+    const double es = block_sum_f64(e2, s_e);
+    if (threadIdx.x == 0) c.blk_e[(uint64_t)j * c.nbmax + b] = es;
+    return;
+  }
+  const uint32_t worker = blockIdx.x - ncand_blocks, G = gridDim.x - ncand_blocks;
+  for (uint32_t j = 0; j < c.K; ++j) {
+    const DevState& s = c.st[j];
+    if (!s.fallback) continue;
+    uint32_t thr;
+    uint64_t need;
+    threshold_of(s, thr, need);
+    const DevDesc d = c.desc[j];
+    for (uint32_t blk = worker; blk < c.nfb; blk += G) {
+      const uint64_t base = (uint64_t)blk * kCBlk;
+      const uint64_t rem = (c.n - base < (uint64_t)kCBlk) ? c.n - base : (uint64_t)kCBlk;
+      const double e2 = block_write<kCBlkRounds>(d.grad + base, nullptr, base, rem, thr, need,
+                                                 c.blk_pre[(uint64_t)j * c.nbmax + blk], d.k, d.idx_out, d.val_out,
+                                                 lds);
+      const double es = block_sum_f64(e2, s_e);
+      if (threadIdx.x == 0) c.blk_e[(uint64_t)j * c.nbmax + blk] = es;
+      __syncthreads();
+    }
+  }
+}
+
+// ---- 5. energies of the adaptive rule and per-device decision --------------------------------
+// §IV: send Top-k(g) when | ||g||^2 - ||Top-k(g)||^2 | / ||g||^2 <= delta.
+__global__ __launch_bounds__(kBlock) void k_final(Ctx c)
+{
+  __shared__ double s_e[4];
+  const uint32_t j = blockIdx.x;
+  DevState& s = c.st[j];
+  const uint32_t nb = blocks_of(c, s);
+  double acc = 0.0;
+  for (uint32_t b = threadIdx.x; b < nb; b += kBlock) acc += c.blk_e[(uint64_t)j * c.nbmax + b];
+  const double e_kept = block_sum_f64(acc, s_e);
+  if (threadIdx.x != 0) return;
+  uint32_t thr;
+  uint64_t need;
+  if (!threshold_of(s, thr, need)) s.err |= 8u;
+  const uint64_t tot = c.blk_pre[(uint64_t)j * c.nbmax + nb - 1] + c.blk_cnt[(uint64_t)j * c.nbmax + nb - 1];
+  s.thr = thr;
+  s.c_gt = tot & 0xFFFFFFFFull;
+  s.need = need;
+  if (s.c_gt + need != c.desc[j].k) s.err |= 16u;
+  s.e_kept = e_kept;
+  const double rho = (s.e_all == 0.0) ? 0.0 : __builtin_fabs(s.e_all - e_kept) / s.e_all;
+  s.sparse = (rho <= c.delta) ? 1u : 0u;
+  if (c.energies_out) {
+    c.energies_out[2 * j] = s.e_all;
+    c.energies_out[2 * j + 1] = e_kept;
+  }
+  if (c.compressed_out) c.compressed_out[j] = (uint8_t)s.sparse;
+}
+
+// ---- host-side launchers ---------------------------------------------------------------------
+hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipEvent_t* ev)
+{
+  const uint64_t zero_words = (uint64_t)c.K * kSlots * kBins + (uint64_t)c.K * c.tpd;
+  uint32_t gprep = (uint32_t)((zero_words + kBlock * 8 - 1) / (kBlock * 8));
+  gprep = gprep < 1 ? 1 : (gprep > 2048 ? 2048 : gprep);
+  k_prep<<<gprep, kBlock, 0, s>>>(c, a);
+  if (p.any_fast) {
+    for (int pass = 0; pass < 3; ++pass) {
+      k_hist_sample<<<dim3(p.sample_blocks, c.K), kBlock, 0, s>>>(c);
+      k_find<<<c.K, 64, 0, s>>>(c, kSlotSampleLo, kSlotSampleHi + 1);
+    }
+  }
+  if (ev) (void)hipEventRecord(ev[1], s);
+  k_main<<<c.K * c.tpd, kBlock, 0, s>>>(c);
+  if (ev) (void)hipEventRecord(ev[2], s);
+  k_post<<<c.K, kBlock, 0, s>>>(c);
+  const uint32_t g = p.ncand_blocks + p.full_workers;
+  for (int pass = 0; pass < 3; ++pass) {
+    k_hist_cf<<<g, kBlock, 0, s>>>(c, p.ncand_blocks);
+    k_find<<<c.K, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1);
+  }
+  if (ev) (void)hipEventRecord(ev[3], s);
+  k_count_cf<<<g, kBlock, 0, s>>>(c, p.ncand_blocks);
+  k_scan<<<c.K, kBlock, 0, s>>>(c);
+  k_write_cf<<<g, kBlock, 0, s>>>(c, p.ncand_blocks);
+  k_final<<<c.K, kBlock, 0, s>>>(c);
+  if (ev) (void)hipEventRecord(ev[4], s);
+  return hipGetLastError();
+}
+
+}  // namespace scadles

@@ -1,0 +1,127 @@
+"""Shared helpers of the GPU parity tests: run the HIP path through the C ABI
+and compare it with the oracle on the same seeded inputs."""
+from __future__ import annotations
+
+import math
+import sys
+
+import numpy as np
+
+import oracle
+import workloads
+
+
+def log(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return torch, torch.device("cuda:0")
+
+
+def same_bits(a: np.ndarray, b: np.ndarray) -> bool:
+    a = np.ascontiguousarray(a)
+    b = np.ascontiguousarray(b)
+    if a.shape != b.shape:
+        return False
+    return np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def within_north_star_tolerance(x: np.ndarray, ref: np.ndarray) -> bool:
+    """|x - ref| <= 1e-7 + 1e-6 |ref| elementwise (the float tolerance of the aggregate)."""
+    x = x.astype(np.float64)
+    r = ref.astype(np.float64)
+    return bool(np.all(np.abs(x - r) <= 1e-7 + 1e-6 * np.abs(r)))
+
+
+def threshold_topk(g, k):
+    """Oracle Top-k in O(n) for full-size vectors: (idx, val, e_all, e_kept)."""
+    idx, _, _, _ = oracle.topk_by_threshold(g, k)
+    e_all, e_kept = oracle.energies(g, idx)
+    return idx, g[idx], e_all, e_kept
+
+
+def oracle_topk_all(s, it, G, topk=None, threads=1):
+    """The oracle's Top-k of every device (optionally on a thread pool: the
+    oracle releases the GIL)."""
+    fn = topk or oracle.topk
+    ks = [oracle.topk_k(s.n, s.ratios[it, j]) for j in range(s.K)]
+    if threads <= 1:
+        return [fn(G[j], ks[j]) for j in range(s.K)]
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(threads) as ex:
+        return list(ex.map(lambda j: fn(G[j], ks[j]), range(s.K)))
+
+
+def check_step(sc, s, it, G, out, w, lr, params_before, params_after, delta=math.inf, topk=None,
+               label="", threads=1):
+    """Compare one fused step against the oracle. `topk(g, k)` returns the oracle's
+    (idx, val, e_all, e_kept); defaults to the full-sort oracle."""
+    n, K = s.n, s.K
+    results = oracle_topk_all(s, it, G, topk, threads)
+    w_o, gamma_o = oracle.stream_weights(s.rates[it], base_batch=s.base_batch)
+    assert same_bits(w_o, w), f"{label}: weights differ"
+    lr_o = float(np.float32(s.eta * gamma_o))
+    assert lr_o == lr
+    energies = out.energies.cpu().numpy()
+    compressed = out.compressed.cpu().numpy()
+    sets = []
+    for j in range(K):
+        k = oracle.topk_k(n, s.ratios[it, j])
+        idx, val, e_all, e_kept = results[j]
+        got_idx = out.idx[j].cpu().numpy()
+        got_val = out.val[j].cpu().numpy()
+        if not np.array_equal(got_idx, idx):
+            bad = np.flatnonzero(got_idx != idx) if got_idx.shape == idx.shape else []
+            raise AssertionError(f"{label} device {j}: Top-k indices differ (k={k}, first mismatch "
+                                 f"{bad[:5] if len(bad) else 'length'})")
+        assert same_bits(got_val, val), f"{label} device {j}: values differ"
+        assert abs(energies[2 * j] - e_all) <= 1e-12 * max(e_all, 1e-300), f"{label} device {j}: E_all"
+        assert abs(energies[2 * j + 1] - e_kept) <= 1e-12 * max(e_all, 1e-300), f"{label} device {j}: E_kept"
+        send, rho = oracle.compress_decision(e_all, e_kept, delta)
+        if abs(rho - delta) > 1e-9:
+            assert bool(compressed[j]) == send, f"{label} device {j}: adaptive decision"
+        else:
+            send = bool(compressed[j])
+        sets.append((idx, val) if send else (None, G[j]))
+    dense_o = oracle.aggregate(sets, w_o, n)
+    dense = out.dense.cpu().numpy()
+    assert within_north_star_tolerance(dense, dense_o), f"{label}: aggregate outside tolerance"
+    assert same_bits(dense, dense_o), f"{label}: aggregate not bit-identical to the oracle"
+    if params_before is not None:
+        p_o = oracle.sgd(params_before, dense_o, lr_o)
+        assert same_bits(params_after, p_o), f"{label}: SGD update differs"
+        return p_o
+    return None
+
+
+def run_config(sc, config, n=None, K=None, iterations=None, delta=math.inf, with_params=True, topk=None,
+               ratio_override=None, threads=1):
+    """Run `iterations` fused steps of a workload and check each against the oracle."""
+    torch, dev = torch_dev()
+    s = workloads.spec(config, n=n, K=K, iterations=iterations)
+    if ratio_override is not None:
+        s.ratios[:] = np.asarray(ratio_override, dtype=np.float64)
+    label = f"C{config} n={s.n} K={s.K}"
+    params = workloads.params0(s) if with_params else None
+    p_dev = torch.from_numpy(params).to(dev) if with_params else None
+    p_ref = params.copy() if with_params else None
+    for it in range(s.iterations):
+        log(f"  {label} iteration {it}: ratio {s.ratios[it, 0]}")
+        G = np.empty((s.K, s.n), dtype=np.float32)
+        for j in range(s.K):
+            workloads.gradient(s, it, j, out=G[j])
+        g_dev = torch.from_numpy(G).to(dev)
+        w, gamma = sc.stream_weights(s.rates[it], base_batch=s.base_batch)
+        lr = float(np.float32(s.eta * gamma))
+        step = sc.FusedStep(g_dev, s.ratios[it], delta=delta, params=p_dev)
+        out = step.run(w, lr)
+        torch.cuda.synchronize()
+        p_after = p_dev.cpu().numpy() if with_params else None
+        p_ref = check_step(sc, s, it, G, out, w, lr, p_ref, p_after, delta=delta, topk=topk,
+                           label=f"{label} it={it}", threads=threads)
+        del g_dev, step, out, G
+    return s

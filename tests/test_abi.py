@@ -1,0 +1,123 @@
+"""The C-ABI library: it loads, exports every declared symbol, and validates
+arguments on the host (no GPU needed for any of these)."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "scadles.h")
+
+
+@pytest.fixture(scope="module")
+def sc():
+    import paper_2301_08897_amd as sc
+    return sc
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(scadles_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_hot_path():
+    names = declared_functions()
+    for required in ("scadles_topk_select", "scadles_weighted_aggregate", "scadles_apply_sgd",
+                     "scadles_step_fused", "scadles_stream_weights", "scadles_topk_k"):
+        assert required in names
+
+
+def test_every_declared_symbol_is_exported(sc):
+    lib = ctypes.CDLL(sc.library_path())
+    for name in declared_functions():
+        assert hasattr(lib, name), f"{name} is declared in scadles.h but not exported"
+
+
+def test_k_rule_matches_oracle(sc, orc):
+    rng = np.random.default_rng(0)
+    cases = [(1_048_576, 0.01), (11_173_962, 0.01), (25_557_032, 0.1), (25_557_032, 0.001),
+             (60_192_808, 0.001), (143_667_240, 0.01), (1, 1.0), (100, 0.07),
+             (100, math.nextafter(0.07, 0)), (2**32 - 1, 0.5), (2**32, 0.5), (0, 0.5), (10, 0.0),
+             (10, float("nan")), (10, 1.0000001)]
+    cases += [(int(rng.integers(1, 10**9)), float(rng.random())) for _ in range(200)]
+    for n, r in cases:
+        assert sc.topk_k(n, r) == orc.topk_k(n, r), (n, r)
+
+
+def test_stream_weights_match_oracle_bitwise(sc, orc, wl):
+    for c in (1, 2, 3, 4, 5):
+        s = wl.spec(c)
+        for it in range(s.iterations):
+            w, g = sc.stream_weights(s.rates[it], base_batch=s.base_batch)
+            wo, go = orc.stream_weights(s.rates[it], base_batch=s.base_batch)
+            assert np.array_equal(w.view(np.uint32), wo.view(np.uint32))
+            assert g == go
+    w, g = sc.stream_weights([2.0, 8.0, 500.0, 4000.0], b_min=8, b_max=1024, base_batch=64)
+    wo, go = orc.stream_weights([2.0, 8.0, 500.0, 4000.0], b_min=8, b_max=1024, base_batch=64)
+    assert np.array_equal(w, wo) and g == go
+
+
+def test_stream_weights_rejects(sc):
+    for rates in ([0.0, 0.0], [1.0, -1.0], [1.0, float("nan")], [float("inf")]):
+        with pytest.raises(sc.ScadlesError) as e:
+            sc.stream_weights(rates)
+        assert e.value.code == 1
+    with pytest.raises(sc.ScadlesError):
+        sc.stream_weights([1.0], b_min=5, b_max=2)
+
+
+def test_host_validation_before_any_launch(sc):
+    """Invalid calls return a status and launch nothing (no GPU is touched)."""
+    E = {"inval": 1, "ws": 2}
+    assert sc._topk_select(None, 10, 0.5, 16, 16, None, None, 0, None) == E["inval"]
+    assert sc._topk_select(16, 0, 0.5, 16, 16, None, None, 0, None) == E["inval"]
+    assert sc._topk_select(16, 2**32, 0.5, 16, 16, None, None, 0, None) == E["inval"]
+    assert sc._topk_select(16, 10, 0.0, 16, 16, None, None, 0, None) == E["inval"]
+    assert sc._topk_select(18, 10, 0.5, 16, 16, None, None, 0, None) == E["inval"]   # misaligned grad
+    assert sc._topk_select(16, 10, 0.5, 16, 16, None, None, 0, None) == E["ws"]
+    assert sc._topk_select(16, 10, 0.5, 16, 16, None, 4096 + 8, 1 << 20, None) == E["ws"]  # misaligned ws
+    assert sc._topk_select(16, 10, 0.5, 16, 16, None, 4096, 16, None) == E["ws"]       # too small
+    assert sc._apply_sgd(None, 16, 10, 0.1, None) == E["inval"]
+    assert sc._apply_sgd(16, 16, 10, 0.1, None) == E["inval"]                          # aliasing
+    assert sc._apply_sgd(16, 4096, 10, float("nan"), None) == E["inval"]
+    sets = (sc.Sparse * 2)(sc.Sparse(16, 16, 3), sc.Sparse(16, 16, 3))
+    w = (ctypes.c_float * 2)(0.5, 0.5)
+    assert sc._weighted_aggregate(sets, w, 0, 10, 16, 4096, 1 << 20, None) == E["inval"]   # K = 0
+    assert sc._weighted_aggregate(sets, w, 65, 10, 16, 4096, 1 << 20, None) == E["inval"]  # K > 64
+    bad = (ctypes.c_float * 2)(0.6, 0.6)
+    assert sc._weighted_aggregate(sets, bad, 2, 10, 16, 4096, 1 << 20, None) == E["inval"]  # sum != 1
+    neg = (ctypes.c_float * 2)(1.5, -0.5)
+    assert sc._weighted_aggregate(sets, neg, 2, 10, 16, 4096, 1 << 20, None) == E["inval"]
+    dense_bad = (sc.Sparse * 2)(sc.Sparse(None, 16, 3), sc.Sparse(16, 16, 3))
+    assert sc._weighted_aggregate(dense_bad, w, 2, 10, 16, 4096, 1 << 20, None) == E["inval"]
+    over = (sc.Sparse * 2)(sc.Sparse(16, 16, 11), sc.Sparse(16, 16, 3))
+    assert sc._weighted_aggregate(over, w, 2, 10, 16, 4096, 1 << 20, None) == E["inval"]
+    assert sc._weighted_aggregate(sets, w, 2, 10, 16, 4096, 8, None) == E["ws"]
+    grads = (ctypes.c_void_p * 2)(16, 32)
+    ratios = (ctypes.c_double * 2)(0.1, 0.1)
+    outs = (ctypes.c_void_p * 2)(16, 32)
+    assert sc._step_fused(grads, 2, 1000, ratios, -1.0, w, outs, outs, 16, None, None, None, 0.0,
+                          4096, 1 << 30, None) == E["inval"]                              # delta < 0
+    assert sc._step_fused(grads, 2, 1000, ratios, float("nan"), w, outs, outs, 16, None, None, None,
+                          0.0, 4096, 1 << 30, None) == E["inval"]
+    bad_r = (ctypes.c_double * 2)(0.1, 1.5)
+    assert sc._step_fused(grads, 2, 1000, bad_r, math.inf, w, outs, outs, 16, None, None, None, 0.0,
+                          4096, 1 << 30, None) == E["inval"]
+    assert sc._step_fused(grads, 2, 1000, ratios, math.inf, w, outs, outs, 16, None, None, None, 0.0,
+                          4096, 64, None) == E["ws"]
+    assert sc._set_option(b"no_such_option", 1) == E["inval"]
+    assert b"no_such_option" in sc._last_error()
+
+
+def test_workspace_queries(sc):
+    assert sc.workspace_bytes(1, 0, [0.5]) == 0
+    assert sc.workspace_bytes(65, 100, [0.5] * 65) == 0
+    assert sc.workspace_bytes(2, 100, [0.5, 2.0]) == 0
+    big = sc.workspace_bytes(32, 143_667_240, [0.01] * 32)
+    assert 0 < big < 2 * 1024**3           # candidate regions are a few k per device, not n
+    assert sc.aggregate_workspace_bytes(0, 10) == 0
+    assert sc.aggregate_workspace_bytes(4, 1 << 20) > 0

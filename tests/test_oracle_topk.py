@@ -142,6 +142,16 @@ def test_energies(orc, wl):
     assert orc.compress_decision(4.0, 3.0, 0.2499) == (False, 0.25)
 
 
+def test_energies_helper(orc, wl):
+    s = wl.spec(2, n=40_000, K=1)
+    g = wl.gradient(s, 0, 0)
+    idx, _, e_all, e_kept = orc.topk(g, 400)
+    a, b = orc.energies(g, idx)
+    assert a == pytest.approx(math.fsum(float(x) ** 2 for x in g), rel=1e-13)
+    assert b == pytest.approx(math.fsum(float(x) ** 2 for x in g[idx]), rel=1e-13)
+    assert a == pytest.approx(e_all, rel=1e-13) and b == pytest.approx(e_kept, rel=1e-13)
+
+
 def test_pins_catch_a_wrong_tie_break(orc):
     """A planted mistake (ties to the higher index) fails the brute-force pin."""
     g = np.array([1.0, -1.0, 1.0, 0.5], dtype=np.float32)
