@@ -1,0 +1,196 @@
+#!/usr/bin/env python3
+"""Benchmark of the ScaDLES hot path on one MI355X.
+
+One step = the whole hot path over one batch of synthetic input: Eqn 4a
+weights (host), Top-k selection + energies + adaptive rule for every device,
+Eqn 4b weighted aggregation and the Eqn 4c SGD update, i.e. one
+scadles_step_fused call. Default workload: 32 devices x 143,667,240 fp32
+gradient elements (VGG-19-sized), ratio 0.01, the weights and learning rates
+of 10 consecutive iterations cycled over the steps. Inputs are resident in HBM
+before the timed region starts.
+
+Prints one JSON line (metric: gradient elements compressed+aggregated per
+second; roofline of the dominant kernel, the main select pass, against the
+8 TB/s HBM peak; the CPU oracle's rate on a bounded sample).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "gradient elements/s compressed+aggregated; % of MI355X HBM roofline"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_main_select_c5.json")
+SELECT_SRC = os.path.join(ROOT, "paper_2301_08897_amd", "csrc", "select.hip")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(s, it):
+    """Bytes the method itself must move in one step (select + compact + aggregate):
+    read every gradient once, write the (idx, val) pairs, write the dense aggregate."""
+    ks = sum(s.k(it, j) for j in range(s.K))
+    return 4 * s.K * s.n + 8 * ks + 4 * s.n
+
+
+def source_hash(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_entry():
+    """HBM bytes per launch of the main select pass measured by rocprofv3 counters,
+    if recorded for the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("select_hip_sha256_16") != source_hash(SELECT_SRC):
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(s, threads):
+    """The oracle, as it stands, on a bounded sample of the same workload: the full
+    step (Top-k by full sort, energies, Eqn 4b, Eqn 4c) for `threads` devices of
+    iteration 0, the devices' Top-k run in parallel threads."""
+    import oracle
+    import workloads
+    from concurrent.futures import ThreadPoolExecutor
+
+    S = max(1, min(s.K, threads))
+    G = np.empty((S, s.n), dtype=np.float32)
+    for j in range(S):
+        workloads.gradient(s, 0, j, out=G[j])
+    rates = s.rates[0, :S]
+    t0 = time.perf_counter()
+    w, gamma = oracle.stream_weights(rates, base_batch=s.base_batch)
+    ks = [oracle.topk_k(s.n, s.ratios[0, j]) for j in range(S)]
+    with ThreadPoolExecutor(S) as ex:
+        res = list(ex.map(lambda j: oracle.topk(G[j], ks[j]), range(S)))
+    dense = oracle.aggregate([(r[0], r[1]) for r in res], w, s.n)
+    params = np.zeros(s.n, dtype=np.float32)
+    oracle.sgd(params, dense, float(np.float32(s.eta * gamma)))
+    dt = time.perf_counter() - t0
+    return {"value": S * s.n / dt, "unit": "elements/s", "cores": S, "kind": "oracle",
+            "sample": f"{S} of the {s.K} devices (iteration 0, full n={s.n} each): full-sort Top-k "
+                      f"in {S} threads, serial double aggregation and SGD; {dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=5, help="workload 1..5 (default 5, the largest)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-threads", type=int, default=16)
+    ap.add_argument("--stages", action="store_true", help="also print per-stage milliseconds")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the hot path keeps all simulated devices in one GPU's HBM "
+              "and has no multi-GPU mode; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2301_08897_amd as sc
+    import workloads
+
+    dev = torch.device("cuda:0")
+    s = workloads.spec(args.config)
+    log(f"workload {s.name}")
+    t0 = time.perf_counter()
+    G = torch.empty((s.K, s.n), dtype=torch.float32, device=dev)
+    host = np.empty(s.n, dtype=np.float32)
+    for j in range(s.K):
+        workloads.gradient(s, 0, j, out=host)
+        G[j].copy_(torch.from_numpy(host))
+    params = torch.from_numpy(workloads.params0(s)).to(dev)
+    torch.cuda.synchronize()
+    log(f"inputs resident in HBM ({4 * s.K * s.n / 1e9:.1f} GB) after {time.perf_counter() - t0:.1f} s")
+
+    weights, lrs = [], []
+    for it in range(s.iterations):
+        w, gamma = sc.stream_weights(s.rates[it], base_batch=s.base_batch)
+        weights.append(w)
+        lrs.append(float(np.float32(s.eta * gamma)))
+    step = sc.FusedStep(G, s.ratios[0], params=params)
+    for i in range(args.warmup):
+        it = i % s.iterations
+        if any(s.ratios[it] != s.ratios[0]):
+            step.set_ratios(s.ratios[it])
+        step.run(weights[it], lrs[it])
+    torch.cuda.synchronize()
+
+    sc.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        it = i % s.iterations
+        step.run(weights[it], lrs[it])
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    stages, calls = sc.profile_read()
+    sc.profile_enable(False)
+
+    ms_per_step = dt * 1e3 / args.steps
+    value = s.K * s.n / (dt / args.steps)
+    main_ms = stages["main_select"] / max(calls, 1)
+    main_bytes = 4 * s.K * s.n
+    achieved = main_bytes / (main_ms * 1e-3) / 1e9
+    alg = np.mean([algorithmic_bytes(s, i % s.iterations) for i in range(args.steps)])
+    sel_ms = sum(stages[k] for k in ("bracket", "main_select", "threshold", "compaction", "aggregate")) / max(calls, 1)
+    traffic = traffic_entry()
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": s.name, "K": s.K, "n": s.n, "ratio": float(s.ratios[0, 0]),
+                   "delta": "inf", "iterations": s.iterations, "sgd": True},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
+                     "kernel": "k_main (main select pass: one read of every gradient)",
+                     "kernel_ms": main_ms},
+        "step_roofline": {"algorithmic_bytes": alg, "GBps": alg / (sel_ms * 1e-3) / 1e9,
+                          "frac": alg / (sel_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                          "note": "select+compact+aggregate(+SGD) stages, algorithmic bytes "
+                                  "4Kn + 8*sum(k) + 4n over their summed event time"},
+    }
+    if args.stages:
+        out["stage_ms"] = {k: v / max(calls, 1) for k, v in stages.items()}
+    if not args.no_cpu_baseline:
+        del G, step
+        torch.cuda.empty_cache()
+        log("timing the CPU oracle on a bounded sample ...")
+        out["cpu_baseline"] = cpu_baseline(s, args.cpu_threads)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

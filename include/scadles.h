@@ -63,7 +63,7 @@ typedef enum {
  * Sparse: idx (dev, k entries, strictly ascending, each < n) and val (dev, k
  * entries) hold the kept gradient entries; every other position is zero.
  * Dense: idx == NULL and k == n; val (dev, n entries) is the full gradient.
- * val must be 4-byte aligned; a dense val must be 16-byte aligned.          */
+ * idx and val must be 4-byte aligned.                                        */
 typedef struct {
   const uint32_t* idx;
   const float* val;
@@ -87,7 +87,7 @@ size_t scadles_aggregate_workspace_bytes(uint32_t K, uint64_t n);
 
 /* Top-k sparsification of one gradient (§IV "High communication cost";
  * Top-k as in §III-C), with the energies of the adaptive rule.
- *   grad      (dev, n floats, 16-byte aligned) the gradient; not modified.
+ *   grad      (dev, n floats, 4-byte aligned) the gradient; not modified.
  *   n         1 <= n <= 2^32 - 1.
  *   ratio     compression ratio in (0, 1]; k = scadles_topk_k(n, ratio).
  *   idx, val  (dev, k entries each) receive the kept positions in strictly
@@ -130,7 +130,7 @@ scadles_status scadles_apply_sgd(float* params, const float* grad, uint64_t n, f
 /* One whole hot-path step for K devices in one call (the training step of
  * §IV): Top-k + energies for every device, the adaptive decision, weighted
  * aggregation and, optionally, the SGD update.
- *   grads      (host[K] of dev pointers, n floats each, 16-byte aligned).
+ *   grads      (host[K] of dev pointers, n floats each, 4-byte aligned).
  *   ratios     (host[K]) per-device compression ratio in (0, 1].
  *   delta      compression threshold of §IV: device j sends Top-k(g_j) when
  *              |E_all - E_kept| / E_all <= delta (E_all == 0 counts as 0) and

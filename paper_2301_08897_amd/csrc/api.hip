@@ -105,7 +105,8 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
 {
   L.K = K;
   L.n = n;
-  L.tpd = ceil_div_u64(n, kTile);
+  // Tiles cover the 16-byte-aligned virtual row [0, n + shift), shift <= 3.
+  L.tpd = ceil_div_u64(n + 3, kTile);
   L.ntile = ceil_div_u64(n, kATile);
   sample_geometry(n, L.s_stride, L.s_n);
   uint64_t sum_cap = 0, max_cap = 0;
@@ -141,7 +142,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
     }
   }
   L.ncb = max_cap ? ceil_div_u64(max_cap, kCBlk) : 1u;
-  L.nfb = ceil_div_u64(n, kCBlk);
+  L.nfb = ceil_div_u64(n + 3, kCBlk);
   L.nbmax = L.ncb > L.nfb ? L.ncb : L.nfb;
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -274,7 +275,7 @@ scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio, 
 {
   if (scadles_status st = check_n(n)) return st;
   if (!grad || !idx || !val) return fail(SCADLES_EINVAL, "grad, idx and val must not be NULL");
-  if (!aligned(grad, 16)) return fail(SCADLES_EINVAL, "grad must be 16-byte aligned");
+  if (!aligned(grad, 4)) return fail(SCADLES_EINVAL, "grad must be 4-byte aligned");
   if (!aligned(idx, 4) || !aligned(val, 4)) return fail(SCADLES_EINVAL, "idx and val must be 4-byte aligned");
   if (energies && !aligned(energies, 8)) return fail(SCADLES_EINVAL, "energies must be 8-byte aligned");
   if (k_rule(n, ratio) == 0) return fail(SCADLES_EINVAL, "ratio %g is not in (0, 1]", ratio);
@@ -315,7 +316,7 @@ scadles_status scadles_weighted_aggregate(const scadles_sparse* sets, const floa
     if (!S.val) return fail(SCADLES_EINVAL, "set %u has a NULL val", j);
     if (!S.idx) {
       if (S.k != n) return fail(SCADLES_EINVAL, "dense set %u must have k == n", j);
-      if (!aligned(S.val, 16)) return fail(SCADLES_EINVAL, "dense set %u must be 16-byte aligned", j);
+      if (!aligned(S.val, 4)) return fail(SCADLES_EINVAL, "dense set %u must be 4-byte aligned", j);
       a.dense[j] = S.val;
     } else {
       if (S.k > n) return fail(SCADLES_EINVAL, "set %u has k = %llu > n", j, (unsigned long long)S.k);
@@ -386,7 +387,7 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
   if (scadles_status st = check_weights(weights, K)) return st;
   for (uint32_t j = 0; j < K; ++j) {
     if (!grads[j] || !idx[j] || !val[j]) return fail(SCADLES_EINVAL, "device %u has a NULL pointer", j);
-    if (!aligned(grads[j], 16)) return fail(SCADLES_EINVAL, "grads[%u] must be 16-byte aligned", j);
+    if (!aligned(grads[j], 4)) return fail(SCADLES_EINVAL, "grads[%u] must be 4-byte aligned", j);
     if (!aligned(idx[j], 4) || !aligned(val[j], 4)) return fail(SCADLES_EINVAL, "device %u outputs misaligned", j);
     if (k_rule(n, ratios[j]) == 0) return fail(SCADLES_EINVAL, "ratio %g of device %u is not in (0, 1]", ratios[j], j);
   }

@@ -42,7 +42,7 @@ struct DevDesc {          // per device, written once per call by the prep kerne
   uint32_t mode;
   uint32_t r_lo;          // sample ranks that bracket the k-th largest key
   uint32_t r_hi;          // 0: no upper bracket
-  uint32_t pad;
+  uint32_t shift;         // (grad address / 4) % 4: offset of element 0 in its 16-byte word
 };
 
 // State of one radix selection: the key of 1-based descending rank `rank` among
@@ -91,9 +91,9 @@ struct Ctx {
   uint8_t* compressed_out;// caller's (dev, K) or null
   uint64_t n;
   uint32_t K;
-  uint32_t tpd;           // main tiles per device
+  uint32_t tpd;           // main tiles per device: ceil((n + 3) / kTile)
   uint32_t ncb;           // candidate blocks per device (max over devices)
-  uint32_t nfb;           // exact-path compaction blocks per device: ceil(n / kCBlk)
+  uint32_t nfb;           // exact-path blocks per device: ceil((n + 3) / kCBlk)
   uint32_t nbmax;         // max(ncb, nfb)
   uint32_t s_stride;      // sample chunk stride (elements)
   uint32_t s_n;           // sample elements per device

@@ -34,20 +34,48 @@ __device__ inline f4 ld_stream4(const float* p) { return __builtin_nontemporal_l
 __device__ inline f4 ld4(const float* p) { return *reinterpret_cast<const f4*>(p); }
 __device__ inline u4 ldu4(const uint32_t* p) { return *reinterpret_cast<const u4*>(p); }
 
-// Loads elements [e, e+4) of a row of `rem` valid elements; invalid lanes read 0.
-__device__ inline f4 load4_guarded(const float* row, uint64_t e, uint64_t rem, bool stream)
+// A device's gradient seen in a 16-byte-aligned "virtual" frame: real element i
+// sits at virtual position i + shift, shift = (address / 4) % 4, so every group
+// of 4 virtual positions is one aligned 16-byte word. Positions outside the real
+// range read as the pad pattern 0xFFFFFFFF, which rank_key maps to 0.
+struct Row {
+  const float* p;      // real element 0
+  uint64_t shift;      // 0..3
+  uint64_t n;          // real elements
+};
+
+constexpr uint32_t kPadBits = 0xFFFFFFFFu;
+
+__device__ inline f4 load4(const Row& r, uint64_t v, bool stream)
 {
-  if (e + 4 <= rem) return stream ? ld_stream4(row + e) : ld4(row + e);
-  f4 v = {0.f, 0.f, 0.f, 0.f};
-  if (e + 0 < rem) v.x = row[e + 0];
-  if (e + 1 < rem) v.y = row[e + 1];
-  if (e + 2 < rem) v.z = row[e + 2];
-  if (e + 3 < rem) v.w = row[e + 3];
-  return v;
+  if (v >= r.shift && v + 4 <= r.shift + r.n) {
+    const float* a = r.p + (v - r.shift);
+    return stream ? ld_stream4(a) : ld4(a);
+  }
+  const float pad = __uint_as_float(kPadBits);
+  f4 x = {pad, pad, pad, pad};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint64_t u = v + q;
+    if (u >= r.shift && u < r.shift + r.n) x[q] = r.p[u - r.shift];
+  }
+  return x;
 }
 
-__device__ inline float comp(const f4& v, int c) { return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w; }
-__device__ inline uint32_t compu(const u4& v, int c) { return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w; }
+__device__ inline bool in_row(const Row& r, uint64_t v) { return v >= r.shift && v < r.shift + r.n; }
+
+// Ranking key offset by one: 0 for the pad pattern, key + 1 for every finite
+// value (finite keys are at most 0x7F7FFFFF, so nothing else wraps). Counting
+// on it needs no validity masks: a pad is never above or equal to key + 1 >= 1.
+__device__ inline uint32_t rank_key(float x) { return ((__float_as_uint(x) & kKeyMask) + 1u) & kKeyMask; }
+
+// Plain loads of [e, e+4) of a contiguous, aligned row of `rem` elements
+// (candidate lists); past the end reads the pad pattern.
+__device__ inline f4 load4_guarded(const float* row, uint64_t e, uint64_t rem, bool stream)
+{
+  return load4(Row{row, 0, rem}, e, stream);
+}
+
 
 __device__ inline uint64_t atomic_load_u64(const uint64_t* p)
 {
@@ -137,7 +165,7 @@ __global__ __launch_bounds__(kBlock) void k_prep(Ctx c, PrepArgs a)
     d.mode = a.mode[j];
     d.r_lo = a.r_lo[j];
     d.r_hi = a.r_hi[j];
-    d.pad = 0;
+    d.shift = (uint32_t)((reinterpret_cast<uintptr_t>(a.grad[j]) >> 2) & 3u);
     c.desc[j] = d;
     DevState s;
     __builtin_memset(&s, 0, sizeof(s));
@@ -187,12 +215,15 @@ __global__ __launch_bounds__(kBlock) void k_hist_sample(Ctx c)
   const uint64_t e1 = (e0 + kSBlk < c.s_n) ? e0 + kSBlk : c.s_n;
   for (uint64_t e = e0 + threadIdx.x * 4; e < e1; e += kRound) {
     const uint64_t chunk = e / kSChunk, within = e % kSChunk;
-    const float* row = d.grad + chunk * c.s_stride + within;
-    const f4 x = load4_guarded(row, 0, e1 - e, false);
+    const uint64_t i = chunk * c.s_stride + within;     // real position of sample element e
+    f4 x;
+    if (d.shift == 0 && e + 4 <= e1) x = ld4(d.grad + i);
+    else
+      for (int q = 0; q < 4; ++q) x[q] = (e + q < e1) ? d.grad[i + q] : 0.f;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       if (e + q >= e1) break;
-      const uint32_t key = key_of(comp(x, q));
+      const uint32_t key = key_of(x[q]);
       uint32_t dg;
       if (s0.active && sel_digit(v0, key, dg)) atomicAdd(&h[0][dg], 1u);
       if (s1.active && sel_digit(v1, key, dg)) atomicAdd(&h[1][dg], 1u);
@@ -336,6 +367,50 @@ __device__ inline uint32_t wave_prefix_of_block(uint32_t packed_lane, uint32_t* 
   return ex;
 }
 
+// One round of the main pass, phase 1: sum of squares and per-lane counts of
+// candidates (key >= tlo) and sure keys (key >= thi), on rank keys (key + 1;
+// pads are 0 and never count); fmax drops the pads' NaN from the squares.
+__device__ inline void main_count(const f4& x, uint32_t tlo1, uint32_t thi1, double& e2a, double& e2b, uint32_t& cnt)
+{
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const double sq = __builtin_fmax((double)x[q] * (double)x[q], 0.0);
+    if (q & 1) e2b += sq;
+    else e2a += sq;
+    const uint32_t key1 = rank_key(x[q]);
+    cnt += (key1 >= tlo1) ? 1u : 0u;
+    cnt += (key1 >= thi1) ? 0x10000u : 0u;
+  }
+}
+
+// One round of the main pass, phase 2: write this round's candidates of the
+// wave at the running offset `run` (index order: lane, then component).
+__device__ inline void main_write(const f4& x, uint64_t v, uint64_t shift, uint32_t tlo1, uint64_t& run, uint32_t cap,
+                                  uint32_t* cidx, float* cval)
+{
+  bool f[4];
+  uint64_t b[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    f[q] = rank_key(x[q]) >= tlo1;
+    b[q] = ballot(f[q]);
+  }
+  if ((b[0] | b[1] | b[2] | b[3]) == 0ull) return;
+  uint64_t pos = run + mbcnt(b[0]) + mbcnt(b[1]) + mbcnt(b[2]) + mbcnt(b[3]);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (f[q]) {
+      if (pos < cap) {
+        cidx[pos] = (uint32_t)(v + q - shift);
+        cval[pos] = x[q];
+      }
+      ++pos;
+    }
+  }
+  run += __builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) + __builtin_popcountll(b[2]) +
+         __builtin_popcountll(b[3]);
+}
+
 __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
 {
   __shared__ uint32_t s_ticket;
@@ -350,31 +425,25 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
   const DevDesc d = c.desc[j];
   uint32_t tlo, thi;
   bracket_of(d, c.st[j], tlo, thi);
-  const uint64_t base = (uint64_t)tile * kTile;
-  const uint64_t rem = c.n - base;
-  const float* row = d.grad + base;
+  const uint32_t tlo1 = tlo + 1u, thi1 = thi + 1u;
+  const uint64_t vbase = (uint64_t)tile * kTile;      // virtual position of the tile
+  const Row row{d.grad, d.shift, c.n};
+  // Interior tiles hold only real elements: plain aligned loads kept in
+  // registers. The (at most two) edge tiles of a device reload per round.
+  const bool full = vbase >= row.shift && vbase + kTile <= row.shift + row.n;
 
-  f4 v[kTileRounds];
-#pragma unroll
-  for (int r = 0; r < kTileRounds; ++r) v[r] = load4_guarded(row, elem_of<kTileRounds>(w, r, l), rem, true);
-
-  // Phase 1: sum of squares and per-lane counts of candidates / sure keys.
-  // Elements past the end load as +0 (key 0): they can only pass `key >= tlo`
-  // when tlo == 0, and then every real element passes too, so the count
-  // reaches n > cap and the device takes the exact path regardless.
   double e2a = 0.0, e2b = 0.0;
   uint32_t cnt = 0;
+  f4 v[kTileRounds];
+  if (full) {
+    const float* p = row.p + (vbase - row.shift);
 #pragma unroll
-  for (int r = 0; r < kTileRounds; ++r) {
+    for (int r = 0; r < kTileRounds; ++r) v[r] = ld_stream4(p + elem_of<kTileRounds>(w, r, l));
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float x = comp(v[r], q);
-      if (q & 1) e2b = __builtin_fma((double)x, (double)x, e2b);
-      else e2a = __builtin_fma((double)x, (double)x, e2a);
-      const uint32_t key = key_of(x);
-      cnt += (key >= tlo) ? 1u : 0u;
-      cnt += (key >= thi) ? 0x10000u : 0u;
-    }
+    for (int r = 0; r < kTileRounds; ++r) main_count(v[r], tlo1, thi1, e2a, e2b, cnt);
+  } else {
+    for (int r = 0; r < kTileRounds; ++r)
+      main_count(load4(row, vbase + elem_of<kTileRounds>(w, r, l), false), tlo1, thi1, e2a, e2b, cnt);
   }
   uint32_t tot;
   const uint32_t wex = wave_prefix_of_block(cnt, lds, tot);
@@ -390,30 +459,15 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
     uint64_t run = s_ex + (wex & 0xFFFFu);
     uint32_t* cidx = c.cand_idx + d.cand_off;
     float* cval = c.cand_val + d.cand_off;
+    if (full) {
 #pragma unroll
-    for (int r = 0; r < kTileRounds; ++r) {
-      const uint64_t e = elem_of<kTileRounds>(w, r, l);
-      bool f[4];
-      uint64_t b[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        f[q] = key_of(comp(v[r], q)) >= tlo;
-        b[q] = ballot(f[q]);
+      for (int r = 0; r < kTileRounds; ++r)
+        main_write(v[r], vbase + elem_of<kTileRounds>(w, r, l), row.shift, tlo1, run, d.cap, cidx, cval);
+    } else {
+      for (int r = 0; r < kTileRounds; ++r) {
+        const uint64_t vv = vbase + elem_of<kTileRounds>(w, r, l);
+        main_write(load4(row, vv, false), vv, row.shift, tlo1, run, d.cap, cidx, cval);
       }
-      if ((b[0] | b[1] | b[2] | b[3]) == 0ull) continue;
-      uint64_t pos = run + mbcnt(b[0]) + mbcnt(b[1]) + mbcnt(b[2]) + mbcnt(b[3]);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if (f[q]) {
-          if (pos < d.cap) {
-            cidx[pos] = (uint32_t)(base + e + q);
-            cval[pos] = comp(v[r], q);
-          }
-          ++pos;
-        }
-      }
-      run += __builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) + __builtin_popcountll(b[2]) +
-             __builtin_popcountll(b[3]);
     }
   }
   const double es = block_sum_f64(e2a + e2b, s_e);
@@ -491,16 +545,16 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
     __syncthreads();
     const SelView sv = view_of(sel);
     const uint64_t rem = (cnt - q0 < (uint64_t)kCBlk) ? cnt - q0 : (uint64_t)kCBlk;
-    const float* cv = c.cand_val + c.desc[j].cand_off + q0;
+    const Row row{c.cand_val + c.desc[j].cand_off + q0, 0, rem};
 #pragma unroll 2
     for (int r = 0; r < kCBlkRounds; ++r) {
       const uint64_t e = (uint64_t)r * kRound + threadIdx.x * 4;
       if (e >= rem) break;
-      const f4 x = load4_guarded(cv, e, rem, false);
+      const f4 x = load4(row, e, false);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         uint32_t dg;
-        if (e + q < rem && sel_digit(sv, key_of(comp(x, q)), dg)) atomicAdd(&h[dg], 1u);
+        if (e + q < rem && sel_digit(sv, key_of(x[q]), dg)) atomicAdd(&h[dg], 1u);
       }
     }
     __syncthreads();
@@ -513,22 +567,21 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
     if (!s.fallback) continue;
     const Sel sel = s.sel[kSlotFull];
     if (!sel.active) continue;
-    if (worker >= c.tpd) continue;
+    if (worker >= c.nfb) continue;
     for (int i = threadIdx.x; i < kBins; i += kBlock) h[i] = 0u;
     __syncthreads();
     const SelView sv = view_of(sel);
-    const float* grad = c.desc[j].grad;
-    for (uint32_t tile = worker; tile < c.tpd; tile += G) {
-      const uint64_t base = (uint64_t)tile * kTile;
-      const uint64_t rem = c.n - base;
+    const Row row{c.desc[j].grad, c.desc[j].shift, c.n};
+    for (uint32_t blk = worker; blk < c.nfb; blk += G) {
+      const uint64_t vbase = (uint64_t)blk * kCBlk;
 #pragma unroll 4
-      for (int r = 0; r < kTileRounds; ++r) {
-        const uint64_t e = (uint64_t)r * kRound + threadIdx.x * 4;
-        const f4 x = load4_guarded(grad + base, e, rem, true);
+      for (int r = 0; r < kCBlkRounds; ++r) {
+        const uint64_t v = vbase + (uint64_t)r * kRound + threadIdx.x * 4;
+        const f4 x = load4(row, v, true);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           uint32_t dg;
-          if (e + q < rem && sel_digit(sv, key_of(comp(x, q)), dg)) atomicAdd(&h[dg], 1u);
+          if (in_row(row, v + q) && sel_digit(sv, key_of(x[q]), dg)) atomicAdd(&h[dg], 1u);
         }
       }
     }
@@ -539,28 +592,24 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
 }
 
 // ---- 4. ordered compaction -------------------------------------------------------------------
-// Blocks are kCBlk elements of a device's candidate list (fast path) or of its
-// gradient (exact path), in index order. Elements past the end load as +0: a
-// pad is never above the threshold, and when it equals it (threshold key 0) it
-// comes after every real element, whose equal keys already reach `need`, so
-// it is never kept and only inflates the last block's own count.
+// Blocks are kCBlk positions of a device's candidate list (fast path) or of its
+// gradient's virtual row (exact path), in index order. Counting uses rank keys
+// (key + 1, pads 0) against thr + 1, so pads are never above or equal to it.
 // Per block: counts of keys above the threshold (gt) and equal to it (eq).
 template <int R>
-__device__ inline uint64_t block_gt_eq(const float* src, uint64_t rem, uint32_t thr, uint32_t* lds)
+__device__ inline uint64_t block_gt_eq(const Row& row, uint64_t vbase, uint32_t thr, uint32_t* lds)
 {
   const uint32_t w = threadIdx.x >> 6, l = lane_id();
+  const uint32_t thr1 = thr + 1u;
   uint32_t gt = 0, eq = 0;
 #pragma unroll 4
   for (int r = 0; r < R; ++r) {
-    const uint64_t e = elem_of<R>(w, r, l);
-    if (e < rem) {
-      const f4 x = load4_guarded(src, e, rem, false);
+    const f4 x = load4(row, vbase + elem_of<R>(w, r, l), false);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t key = key_of(comp(x, q));
-        gt += (key > thr) ? 1u : 0u;
-        eq += (key == thr) ? 1u : 0u;
-      }
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t key1 = rank_key(x[q]);
+      gt += (key1 > thr1) ? 1u : 0u;
+      eq += (key1 == thr1) ? 1u : 0u;
     }
   }
   uint32_t tg, te;
@@ -582,7 +631,7 @@ __global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c, uint32_t ncand_block
     uint64_t need;
     threshold_of(s, thr, need);
     const uint64_t rem = (s.cand - q0 < (uint64_t)kCBlk) ? s.cand - q0 : (uint64_t)kCBlk;
-    const uint64_t r = block_gt_eq<kCBlkRounds>(c.cand_val + c.desc[j].cand_off + q0, rem, thr, lds);
+    const uint64_t r = block_gt_eq<kCBlkRounds>(Row{c.cand_val + c.desc[j].cand_off + q0, 0, rem}, 0, thr, lds);
     if (threadIdx.x == 0) c.blk_cnt[(uint64_t)j * c.nbmax + b] = r;
     return;
   }
@@ -593,11 +642,9 @@ __global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c, uint32_t ncand_block
     uint32_t thr;
     uint64_t need;
     threshold_of(s, thr, need);
-    const float* grad = c.desc[j].grad;
+    const Row row{c.desc[j].grad, c.desc[j].shift, c.n};
     for (uint32_t blk = worker; blk < c.nfb; blk += G) {
-      const uint64_t base = (uint64_t)blk * kCBlk;
-      const uint64_t rem = (c.n - base < (uint64_t)kCBlk) ? c.n - base : (uint64_t)kCBlk;
-      const uint64_t r = block_gt_eq<kCBlkRounds>(grad + base, rem, thr, lds);
+      const uint64_t r = block_gt_eq<kCBlkRounds>(row, (uint64_t)blk * kCBlk, thr, lds);
       if (threadIdx.x == 0) c.blk_cnt[(uint64_t)j * c.nbmax + blk] = r;
     }
   }
@@ -646,72 +693,106 @@ __global__ __launch_bounds__(kBlock) void k_scan(Ctx c)
 // Writes the kept entries of one block in index order.
 //   kept: key > thr, or key == thr with fewer than `need` equal keys before it;
 //   position: (keys > thr before it) + min(equal keys before it, need).
-template <int R>
-__device__ inline double block_write(const float* src, const uint32_t* src_idx, uint64_t idx_base, uint64_t rem,
-                                     uint32_t thr, uint64_t need, uint64_t pre, uint32_t k, uint32_t* out_idx,
-                                     float* out_val, uint32_t* lds)
+// `src_idx` (candidate lists) gives each element's index; without it the index
+// is the virtual position minus the row's shift.
+__device__ inline uint32_t write_count(const f4& x, uint32_t thr1)
 {
-  const uint32_t w = threadIdx.x >> 6, l = lane_id();
-  f4 x[R];
   uint32_t cnt = 0;
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const uint64_t e = elem_of<R>(w, r, l);
-    x[r] = (e < rem) ? load4_guarded(src, e, rem, false) : f4{0.f, 0.f, 0.f, 0.f};
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t key1 = rank_key(x[q]);
+    cnt += (key1 > thr1) ? 1u : 0u;
+    cnt += (key1 == thr1) ? 0x10000u : 0u;
+  }
+  return cnt;
+}
+
+// One round of the ordered write: the wave's elements above the threshold, and
+// equal ones while fewer than `need` came before, at their kept positions.
+__device__ inline void write_round(const f4& x, uint64_t e, uint64_t vbase, const Row& row, const uint32_t* src_idx,
+                                   uint32_t thr1, uint64_t need, uint32_t k, uint32_t* out_idx, float* out_val,
+                                   uint64_t& run_g, uint64_t& run_e, double& e2)
+{
+  bool fg[4], fe[4];
+  uint64_t bg[4], be[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t key = key_of(comp(x[r], q));
-      cnt += (key > thr) ? 1u : 0u;
-      cnt += (key == thr) ? 0x10000u : 0u;
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t key1 = rank_key(x[q]);
+    fg[q] = key1 > thr1;
+    fe[q] = key1 == thr1;
+    bg[q] = ballot(fg[q]);
+    be[q] = ballot(fe[q]);
+  }
+  if ((bg[0] | bg[1] | bg[2] | bg[3] | be[0] | be[1] | be[2] | be[3]) == 0ull) return;
+  uint64_t gt_b = run_g + mbcnt(bg[0]) + mbcnt(bg[1]) + mbcnt(bg[2]) + mbcnt(bg[3]);
+  uint64_t eq_b = run_e + mbcnt(be[0]) + mbcnt(be[1]) + mbcnt(be[2]) + mbcnt(be[3]);
+  u4 ix = {0u, 0u, 0u, 0u};
+  if (src_idx) {
+    if (e + 4 <= row.n) ix = ldu4(src_idx + e);
+    else
+      for (int q = 0; q < 4; ++q)
+        if (e + q < row.n) ix[q] = src_idx[e + q];
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const bool keep = fg[q] || (fe[q] && eq_b < need);
+    if (keep) {
+      const uint64_t pos = gt_b + (eq_b < need ? eq_b : need);
+      const float val = x[q];
+      if (pos < k) {
+        out_idx[pos] = src_idx ? ix[q] : (uint32_t)(vbase + e + q - row.shift);
+        out_val[pos] = val;
+      }
+      e2 = __builtin_fma((double)val, (double)val, e2);
     }
+    gt_b += fg[q];
+    eq_b += fe[q];
+  }
+  run_g += __builtin_popcountll(bg[0]) + __builtin_popcountll(bg[1]) + __builtin_popcountll(bg[2]) +
+           __builtin_popcountll(bg[3]);
+  run_e += __builtin_popcountll(be[0]) + __builtin_popcountll(be[1]) + __builtin_popcountll(be[2]) +
+           __builtin_popcountll(be[3]);
+}
+
+// Writes the kept entries of one block in index order.
+//   kept: key > thr, or key == thr with fewer than `need` equal keys before it;
+//   position: (keys > thr before it) + min(equal keys before it, need).
+// `src_idx` (candidate lists) gives each element's index; without it the index
+// is the virtual position minus the row's shift.
+template <int R>
+__device__ inline double block_write(const Row& row, uint64_t vbase, const uint32_t* src_idx, uint32_t thr,
+                                     uint64_t need, uint64_t pre, uint32_t k, uint32_t* out_idx, float* out_val,
+                                     uint32_t* lds)
+{
+  const uint32_t w = threadIdx.x >> 6, l = lane_id();
+  const uint32_t thr1 = thr + 1u;
+  const bool full = vbase >= row.shift && vbase + R * kRound <= row.shift + row.n;
+  f4 x[R];
+  uint32_t cnt = 0;
+  if (full) {
+    const float* p = row.p + (vbase - row.shift);
+#pragma unroll
+    for (int r = 0; r < R; ++r) x[r] = ld4(p + elem_of<R>(w, r, l));
+#pragma unroll
+    for (int r = 0; r < R; ++r) cnt += write_count(x[r], thr1);
+  } else {
+    for (int r = 0; r < R; ++r) cnt += write_count(load4(row, vbase + elem_of<R>(w, r, l), false), thr1);
   }
   uint32_t tot;
   const uint32_t wex = wave_prefix_of_block(cnt, lds, tot);
   uint64_t run_g = (pre & 0xFFFFFFFFull) + (wex & 0xFFFFu);
   uint64_t run_e = (pre >> 32) + (wex >> 16);
   double e2 = 0.0;
+  if (full) {
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const uint64_t e = elem_of<R>(w, r, l);
-    bool fg[4], fe[4];
-    uint64_t bg[4], be[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t key = key_of(comp(x[r], q));
-      fg[q] = key > thr;
-      fe[q] = key == thr;
-      bg[q] = ballot(fg[q]);
-      be[q] = ballot(fe[q]);
+    for (int r = 0; r < R; ++r)
+      write_round(x[r], elem_of<R>(w, r, l), vbase, row, src_idx, thr1, need, k, out_idx, out_val, run_g, run_e, e2);
+  } else {
+    for (int r = 0; r < R; ++r) {
+      const uint64_t e = elem_of<R>(w, r, l);
+      write_round(load4(row, vbase + e, false), e, vbase, row, src_idx, thr1, need, k, out_idx, out_val, run_g,
+                  run_e, e2);
     }
-    if ((bg[0] | bg[1] | bg[2] | bg[3] | be[0] | be[1] | be[2] | be[3]) == 0ull) continue;
-    uint64_t gt_b = run_g + mbcnt(bg[0]) + mbcnt(bg[1]) + mbcnt(bg[2]) + mbcnt(bg[3]);
-    uint64_t eq_b = run_e + mbcnt(be[0]) + mbcnt(be[1]) + mbcnt(be[2]) + mbcnt(be[3]);
-    u4 ix = {0u, 0u, 0u, 0u};
-    if (src_idx && e < rem) {
-      if (e + 4 <= rem) ix = ldu4(src_idx + e);
-      else
-        for (int q = 0; q < 4; ++q)
-          if (e + q < rem) ix[q] = src_idx[e + q];
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const bool keep = fg[q] || (fe[q] && eq_b < need);
-      if (keep) {
-        const uint64_t pos = gt_b + (eq_b < need ? eq_b : need);
-        const float val = comp(x[r], q);
-        if (pos < k) {
-          out_idx[pos] = src_idx ? compu(ix, q) : (uint32_t)(idx_base + e + q);
-          out_val[pos] = val;
-        }
-        e2 = __builtin_fma((double)val, (double)val, e2);
-      }
-      gt_b += fg[q];
-      eq_b += fe[q];
-    }
-    run_g += __builtin_popcountll(bg[0]) + __builtin_popcountll(bg[1]) + __builtin_popcountll(bg[2]) +
-             __builtin_popcountll(bg[3]);
-    run_e += __builtin_popcountll(be[0]) + __builtin_popcountll(be[1]) + __builtin_popcountll(be[2]) +
-             __builtin_popcountll(be[3]);
   }
   return e2;
 }
@@ -731,9 +812,9 @@ __global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c, uint32_t ncand_block
     threshold_of(s, thr, need);
     const DevDesc d = c.desc[j];
     const uint64_t rem = (s.cand - q0 < (uint64_t)kCBlk) ? s.cand - q0 : (uint64_t)kCBlk;
-    const double e2 = block_write<kCBlkRounds>(c.cand_val + d.cand_off + q0, c.cand_idx + d.cand_off + q0, 0, rem,
-                                               thr, need, c.blk_pre[(uint64_t)j * c.nbmax + b], d.k, d.idx_out,
-                                               d.val_out, lds);
+    const double e2 = block_write<kCBlkRounds>(Row{c.cand_val + d.cand_off + q0, 0, rem}, 0,
+                                               c.cand_idx + d.cand_off + q0, thr, need,
+                                               c.blk_pre[(uint64_t)j * c.nbmax + b], d.k, d.idx_out, d.val_out, lds);
     const double es = block_sum_f64(e2, s_e);
     if (threadIdx.x == 0) c.blk_e[(uint64_t)j * c.nbmax + b] = es;
     return;
@@ -746,12 +827,11 @@ __global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c, uint32_t ncand_block
     uint64_t need;
     threshold_of(s, thr, need);
     const DevDesc d = c.desc[j];
+    const Row row{d.grad, d.shift, c.n};
     for (uint32_t blk = worker; blk < c.nfb; blk += G) {
-      const uint64_t base = (uint64_t)blk * kCBlk;
-      const uint64_t rem = (c.n - base < (uint64_t)kCBlk) ? c.n - base : (uint64_t)kCBlk;
-      const double e2 = block_write<kCBlkRounds>(d.grad + base, nullptr, base, rem, thr, need,
-                                                 c.blk_pre[(uint64_t)j * c.nbmax + blk], d.k, d.idx_out, d.val_out,
-                                                 lds);
+      const double e2 = block_write<kCBlkRounds>(row, (uint64_t)blk * kCBlk, nullptr, thr, need,
+                                                 c.blk_pre[(uint64_t)j * c.nbmax + blk], d.k, d.idx_out,
+                                                 d.val_out, lds);
       const double es = block_sum_f64(e2, s_e);
       if (threadIdx.x == 0) c.blk_e[(uint64_t)j * c.nbmax + blk] = es;
       __syncthreads();
