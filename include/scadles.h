@@ -63,6 +63,7 @@ typedef enum {
  * Sparse: idx (dev, k entries, strictly ascending, each < n) and val (dev, k
  * entries) hold the kept gradient entries; every other position is zero.
  * Dense: idx == NULL and k == n; val (dev, n entries) is the full gradient.
+ * Empty: k == 0 (idx and val are ignored and may be NULL); contributes nothing.
  * idx and val must be 4-byte aligned.                                        */
 typedef struct {
   const uint32_t* idx;

@@ -23,6 +23,11 @@ if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first "
                       "(there is no fallback implementation)")
 
+# torch bundles its own HIP runtime under the same soname as the system one.
+# Loading torch first makes libscadles bind to that runtime, so the process has
+# exactly one HIP/HSA runtime (two would each try to own the GPU).
+import torch as _torch_for_runtime  # noqa: E402,F401
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 MAX_DEVICES = 64

@@ -194,7 +194,7 @@ hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate
 {
   if (validate) k_zero_u32<<<1, 1, 0, s>>>(c.err);
   const uint32_t bx = c.kmax ? (uint32_t)((c.kmax + kRound - 1) / kRound) : 1u;
-  k_offsets<<<dim3(bx, c.K), kBlock, 0, s>>>(a, c, validate);
+  if (c.K) k_offsets<<<dim3(bx, c.K), kBlock, 0, s>>>(a, c, validate);
   k_aggregate<<<c.ntile, kBlock, 0, s>>>(a, c);
   return hipGetLastError();
 }

@@ -308,25 +308,29 @@ scadles_status scadles_weighted_aggregate(const scadles_sparse* sets, const floa
   if (!sets || !dense) return fail(SCADLES_EINVAL, "sets and dense must not be NULL");
   if (!aligned(dense, 16)) return fail(SCADLES_EINVAL, "dense must be 16-byte aligned");
   if (scadles_status st = check_weights(weights, K)) return st;
+  // Empty sets contribute nothing and are dropped; the others keep their order.
   AggArgs a;
   memset(&a, 0, sizeof(a));
   uint64_t kmax = 0;
+  uint32_t Kc = 0;
   for (uint32_t j = 0; j < K; ++j) {
     const scadles_sparse& S = sets[j];
+    if (S.k == 0) continue;
     if (!S.val) return fail(SCADLES_EINVAL, "set %u has a NULL val", j);
     if (!S.idx) {
       if (S.k != n) return fail(SCADLES_EINVAL, "dense set %u must have k == n", j);
       if (!aligned(S.val, 4)) return fail(SCADLES_EINVAL, "dense set %u must be 4-byte aligned", j);
-      a.dense[j] = S.val;
+      a.dense[Kc] = S.val;
     } else {
       if (S.k > n) return fail(SCADLES_EINVAL, "set %u has k = %llu > n", j, (unsigned long long)S.k);
       if (!aligned(S.idx, 4) || !aligned(S.val, 4)) return fail(SCADLES_EINVAL, "set %u is misaligned", j);
       if (S.k > kmax) kmax = S.k;
     }
-    a.idx[j] = S.idx;
-    a.val[j] = S.val;
-    a.k[j] = (uint32_t)S.k;
-    a.w[j] = weights[j];
+    a.idx[Kc] = S.idx;
+    a.val[Kc] = S.val;
+    a.k[Kc] = (uint32_t)S.k;
+    a.w[Kc] = weights[j];
+    ++Kc;
   }
   Layout L;
   make_layout(K, n, nullptr, false, false, L);
@@ -338,7 +342,7 @@ scadles_status scadles_weighted_aggregate(const scadles_sparse* sets, const floa
   c.off = reinterpret_cast<uint32_t*>(b + L.o_aoff);
   c.err = reinterpret_cast<uint32_t*>(b + L.o_aerr);
   c.out = dense;
-  c.K = K;
+  c.K = Kc;
   c.ntile = L.ntile;
   c.kmax = (uint32_t)kmax;
   c.n = n;

@@ -30,6 +30,14 @@ def same_bits(a: np.ndarray, b: np.ndarray) -> bool:
     return np.array_equal(a.view(np.uint32), b.view(np.uint32))
 
 
+def energy_tol(n: int) -> float:
+    """Relative tolerance between two double sums of n non-negative terms: the
+    oracle sums in index order, whose relative error is at most (n - 1) * 2^-53;
+    the kernels sum per lane, per tile and over tiles, a smaller bound. Twice the
+    serial bound covers both."""
+    return 2.0 * (n + 64) * 2.0**-53
+
+
 def within_north_star_tolerance(x: np.ndarray, ref: np.ndarray) -> bool:
     """|x - ref| <= 1e-7 + 1e-6 |ref| elementwise (the float tolerance of the aggregate)."""
     x = x.astype(np.float64)
@@ -79,8 +87,9 @@ def check_step(sc, s, it, G, out, w, lr, params_before, params_after, delta=math
             raise AssertionError(f"{label} device {j}: Top-k indices differ (k={k}, first mismatch "
                                  f"{bad[:5] if len(bad) else 'length'})")
         assert same_bits(got_val, val), f"{label} device {j}: values differ"
-        assert abs(energies[2 * j] - e_all) <= 1e-12 * max(e_all, 1e-300), f"{label} device {j}: E_all"
-        assert abs(energies[2 * j + 1] - e_kept) <= 1e-12 * max(e_all, 1e-300), f"{label} device {j}: E_kept"
+        tol = energy_tol(n) * max(e_all, 1e-300)
+        assert abs(energies[2 * j] - e_all) <= tol, f"{label} device {j}: E_all"
+        assert abs(energies[2 * j + 1] - e_kept) <= tol, f"{label} device {j}: E_kept"
         send, rho = oracle.compress_decision(e_all, e_kept, delta)
         if abs(rho - delta) > 1e-9:
             assert bool(compressed[j]) == send, f"{label} device {j}: adaptive decision"

@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 import oracle
-from _gpu_common import log, same_bits, torch_dev
+from _gpu_common import energy_tol, log, same_bits, torch_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -37,7 +37,8 @@ def topk_vs_oracle(sc, g: np.ndarray, ratio: float, label: str):
         assert np.array_equal(idx.cpu().numpy(), idx_o), f"{label} [{mode}]: indices"
         assert same_bits(val.cpu().numpy(), val_o), f"{label} [{mode}]: values"
         e = en.cpu().numpy()
-        assert abs(e[0] - ea) <= 1e-12 * max(ea, 1e-300) and abs(e[1] - ek) <= 1e-12 * max(ea, 1e-300), label
+        tol = energy_tol(g.size) * max(ea, 1e-300)
+        assert abs(e[0] - ea) <= tol and abs(e[1] - ek) <= tol, label
 
 
 SIZES = [1, 2, 3, 4, 5, 255, 1023, 1024, 1025, 16383, 16384, 16385, 65535, 65536, 65537, 131072 + 77,
@@ -138,7 +139,8 @@ def test_k1_device_and_64_devices(sc):
     for K, n in ((1, 100_003), (64, 70_000)):
         G = (rng.standard_normal((K, n)) * 10.0 ** rng.uniform(-5, -1, (K, 1))).astype(np.float32)
         rates = rng.uniform(1, 100, K)
-        rates[0] = 0.0                 # a device that streamed nothing: weight 0
+        if K > 1:
+            rates[0] = 0.0             # a device that streamed nothing: weight 0
         w, _ = sc.stream_weights(rates)
         params = (rng.standard_normal(n) * 0.05).astype(np.float32)
         p_dev = torch.from_numpy(params).to(dev)
