@@ -64,7 +64,7 @@ constexpr uint64_t kCapAlign = 64;
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-  uint32_t K = 0, tpd = 0, ncb = 0, nfb = 0, nbmax = 0, ntile = 0, s_stride = 0, s_n = 0;
+  uint32_t K = 0, tpd = 0, ncb = 0, nfb = 0, nbmax = 0, ntile = 0, nrange = 0, s_stride = 0, s_n = 0;
   uint64_t n = 0;
   uint32_t k[kMaxK], cap[kMaxK], mode[kMaxK], r_lo[kMaxK], r_hi[kMaxK];
   uint32_t any_fast = 0;
@@ -108,6 +108,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
   // Tiles cover the 16-byte-aligned virtual row [0, n + shift), shift <= 3.
   L.tpd = ceil_div_u64(n + 3, kTile);
   L.ntile = ceil_div_u64(n, kATile);
+  L.nrange = ceil_div_u64(L.ntile, kARange);
   sample_geometry(n, L.s_stride, L.s_n);
   uint64_t sum_cap = 0, max_cap = 0;
   L.any_fast = 0;
@@ -161,9 +162,9 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
     L.o_bcnt = take(sizeof(uint64_t) * (size_t)K * L.nbmax);
     L.o_bpre = take(sizeof(uint64_t) * (size_t)K * L.nbmax);
     L.o_be = take(sizeof(double) * (size_t)K * L.nbmax);
-    L.o_ticket = take(256);
+    L.o_ticket = take(sizeof(uint32_t) * kMaxK);
   }
-  L.o_aoff = take(sizeof(uint32_t) * (size_t)K * (L.ntile + 1));
+  L.o_aoff = take(sizeof(uint32_t) * (size_t)K * (L.nrange + 1));
   L.o_aerr = take(256);
   L.total = o;
   return true;
@@ -339,11 +340,12 @@ scadles_status scadles_weighted_aggregate(const scadles_sparse* sets, const floa
   AggCtx c;
   memset(&c, 0, sizeof(c));
   c.st = nullptr;
-  c.off = reinterpret_cast<uint32_t*>(b + L.o_aoff);
+  c.start = reinterpret_cast<uint32_t*>(b + L.o_aoff);
   c.err = reinterpret_cast<uint32_t*>(b + L.o_aerr);
   c.out = dense;
   c.K = Kc;
   c.ntile = L.ntile;
+  c.nrange = L.nrange;
   c.kmax = (uint32_t)kmax;
   c.n = n;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -427,13 +429,14 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
   AggCtx c;
   memset(&c, 0, sizeof(c));
   c.st = reinterpret_cast<const DevState*>(b + L.o_st);
-  c.off = reinterpret_cast<uint32_t*>(b + L.o_aoff);
+  c.start = reinterpret_cast<uint32_t*>(b + L.o_aoff);
   c.err = reinterpret_cast<uint32_t*>(b + L.o_aerr);
   c.out = dense;
   c.params = params;
   c.lr = lr;
   c.K = K;
   c.ntile = L.ntile;
+  c.nrange = L.nrange;
   c.kmax = (uint32_t)kmax;
   c.n = n;
   hipError_t e = launch_aggregate(g, c, 0, s);

@@ -19,8 +19,9 @@ constexpr int kSBlk = 4096;            // sample elements per workgroup
 constexpr int kSChunk = 256;           // contiguous sample chunk (1 KiB)
 constexpr int kBins = 2048;            // radix digit: 11 bits
 constexpr int kDigitBits = 11;
-constexpr int kATile = 4096;           // aggregation tile (positions)
-constexpr int kAStage = 4096;          // aggregation staging entries per round
+constexpr int kATile = 1024;           // aggregation: positions per wave tile (8 KiB of doubles in LDS)
+constexpr int kARange = 4;             // aggregation: tiles per wave
+constexpr int kABatch = 16;            // aggregation: devices whose entries are loaded together
 constexpr int kMaxK = 64;              // SCADLES_MAX_DEVICES
 constexpr int kSlots = 4;              // selection slots per device
 constexpr int kSlotSampleLo = 0, kSlotSampleHi = 1, kSlotCand = 2, kSlotFull = 3;
@@ -86,7 +87,7 @@ struct Ctx {
   uint64_t* blk_cnt;      // [K][nbmax] packed (gt | eq << 32) per compaction block
   uint64_t* blk_pre;      // [K][nbmax] exclusive prefix of blk_cnt
   double* blk_e;          // [K][nbmax] kept sum of squares per compaction block
-  uint32_t* ticket;       // main pass tile ticket
+  uint32_t* ticket;       // [K] main pass tile tickets
   double* energies_out;   // caller's (dev, 2K) or null
   uint8_t* compressed_out;// caller's (dev, K) or null
   uint64_t n;
@@ -124,13 +125,14 @@ struct AggArgs {
 
 struct AggCtx {
   const DevState* st;     // fused path: per-device sparse/dense decision; null otherwise
-  uint32_t* off;          // [K][ntile + 1] survivor offset of each tile start
+  uint32_t* start;        // [K][nrange + 1] first survivor of each wave's range
   uint32_t* err;          // validation flag
   float* out;             // dense aggregate
   float* params;          // null: no SGD
   float lr;
   uint32_t K;
-  uint32_t ntile;
+  uint32_t ntile;         // ceil(n / kATile)
+  uint32_t nrange;        // ceil(ntile / kARange): waves of the aggregation kernel
   uint32_t kmax;
   uint64_t n;
 };

@@ -189,7 +189,7 @@ __global__ __launch_bounds__(kBlock) void k_prep(Ctx c, PrepArgs a)
     }
     c.st[j] = s;
   }
-  if (blockIdx.x == 0 && threadIdx.x == 0) *c.ticket = 0u;
+  if (blockIdx.x == 0 && threadIdx.x < K) c.ticket[threadIdx.x] = 0u;
   const uint64_t nh = (uint64_t)K * kSlots * kBins;
   const uint64_t ns = (uint64_t)K * c.tpd;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
@@ -244,23 +244,31 @@ __global__ __launch_bounds__(64) void k_find(Ctx c, int s_begin, int s_end)
     uint32_t* h = c.hist + ((uint64_t)j * kSlots + s) * kBins;
     const uint32_t w = sel.bits < (uint32_t)kDigitBits ? sel.bits : (uint32_t)kDigitBits;
     const int nb = 1 << w;
-    const int per = (nb + 63) / 64;
+    const int per = (nb + 63) / 64;                // bins per lane, at most 32
     const int b_hi = nb - (int)l * per;           // this lane covers bins [b_lo, b_hi), top first
     const int b_lo = b_hi - per > 0 ? b_hi - per : 0;
+    uint32_t hv[32];
     uint32_t sum = 0;
-    for (int b = b_lo; b < b_hi; ++b) sum += h[b];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      const int b = b_hi - 1 - i;
+      hv[i] = (i < per && b >= b_lo) ? h[b] : 0u;
+      sum += hv[i];
+    }
     const uint32_t incl = wave_incl_scan(sum);
     const uint32_t excl = incl - sum;
     const bool hit = (uint64_t)excl < sel.rank && sel.rank <= (uint64_t)incl;
     const uint64_t m = ballot(hit);
     uint32_t dsel = 0, cum = excl;
     if (hit) {
-      for (int b = b_hi - 1; b >= b_lo; --b) {
-        if ((uint64_t)cum + h[b] >= sel.rank) {
-          dsel = (uint32_t)b;
-          break;
+      bool done = false;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) {
+        if (!done && (uint64_t)cum + hv[i] >= sel.rank) {
+          dsel = (uint32_t)(b_hi - 1 - i);
+          done = true;
         }
-        cum += h[b];
+        if (!done) cum += hv[i];
       }
     }
     const int src = m ? __builtin_ctzll(m) : 0;
@@ -293,9 +301,9 @@ __global__ __launch_bounds__(64) void k_find(Ctx c, int s_begin, int s_end)
 // each tile publishes its own counts at once, then sums its predecessors'
 // until it meets an inclusive prefix. Status word: flag(2) | sure(31) | cand(31),
 // saturating at 2^31 - 1 (a saturated count always exceeds the capacity).
-// Tiles take their number from a ticket in start order, so every tile waited on
-// has started and never waits on a later tile; the spin is bounded anyway and a
-// timeout sends the device to the exact path.
+// Tiles take their number from their device's ticket in start order, so every
+// tile waited on has started and never waits on a later tile; the spin is
+// bounded anyway and a timeout sends the device to the exact path.
 __device__ inline uint64_t lb_pack(uint64_t flag, uint64_t cand, uint64_t sure)
 {
   cand = cand < kSat31 ? cand : kSat31;
@@ -367,32 +375,61 @@ __device__ inline uint32_t wave_prefix_of_block(uint32_t packed_lane, uint32_t* 
   return ex;
 }
 
-// One round of the main pass, phase 1: sum of squares and per-lane counts of
-// candidates (key >= tlo) and sure keys (key >= thi), on rank keys (key + 1;
-// pads are 0 and never count); fmax drops the pads' NaN from the squares.
-__device__ inline void main_count(const f4& x, uint32_t tlo1, uint32_t thi1, double& e2a, double& e2b, uint32_t& cnt)
+// Candidates a wave stages in LDS before its output offset is known.
+constexpr int kWaveCap = 512;
+
+// One round of phase 1 for one wave: sum of squares, counts of candidates
+// (key >= tlo) and sure keys (key >= thi), and the round's candidates staged in
+// LDS in index order (lane, then component) after the `wc` already staged.
+// kEdge: the round may hold pads (pattern 0xFFFFFFFF), so keys are compared as
+// rank keys (key + 1, pads 0) and fmax drops the pads' NaN from the squares.
+// Counts are wave totals from ballots (scalar popcounts).
+template <bool kEdge>
+__device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32_t thi, double (&e2)[4], uint32_t& wc,
+                                  uint32_t& ws, uint32_t* s_ci, float* s_cv)
 {
+  uint64_t b[4];
+  bool f[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const double sq = __builtin_fmax((double)x[q] * (double)x[q], 0.0);
-    if (q & 1) e2b += sq;
-    else e2a += sq;
-    const uint32_t key1 = rank_key(x[q]);
-    cnt += (key1 >= tlo1) ? 1u : 0u;
-    cnt += (key1 >= thi1) ? 0x10000u : 0u;
+    const double xd = (double)x[q];
+    if (kEdge) e2[q] += __builtin_fmax(xd * xd, 0.0);
+    else e2[q] = __builtin_fma(xd, xd, e2[q]);
+    const uint32_t key = kEdge ? rank_key(x[q]) : key_of(x[q]);
+    const uint32_t lo = kEdge ? tlo + 1u : tlo, hi = kEdge ? thi + 1u : thi;
+    f[q] = key >= lo;
+    b[q] = ballot(f[q]);
+    ws += (uint32_t)__builtin_popcountll(ballot(key >= hi));
   }
+  const uint64_t any = b[0] | b[1] | b[2] | b[3];
+  if (any == 0ull) return;
+  uint32_t pos = wc + mbcnt(b[0]) + mbcnt(b[1]) + mbcnt(b[2]) + mbcnt(b[3]);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (f[q]) {
+      if (pos < (uint32_t)kWaveCap) {
+        s_ci[pos] = i0 + q;
+        s_cv[pos] = x[q];
+      }
+      ++pos;
+    }
+  }
+  wc += (uint32_t)(__builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) + __builtin_popcountll(b[2]) +
+                   __builtin_popcountll(b[3]));
 }
 
-// One round of the main pass, phase 2: write this round's candidates of the
-// wave at the running offset `run` (index order: lane, then component).
-__device__ inline void main_write(const f4& x, uint64_t v, uint64_t shift, uint32_t tlo1, uint64_t& run, uint32_t cap,
-                                  uint32_t* cidx, float* cval)
+// Phase 2 for a wave whose candidates overflowed its LDS stage: recompute the
+// round's flags (on rank keys, so pads never count) and write the candidates
+// straight to their global positions.
+template <bool kEdge>
+__device__ inline void main_write(const f4& x, uint32_t i0, uint32_t tlo, uint64_t& run, uint32_t cap, uint32_t* cidx,
+                                  float* cval)
 {
   bool f[4];
   uint64_t b[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    f[q] = rank_key(x[q]) >= tlo1;
+    f[q] = (kEdge ? rank_key(x[q]) : key_of(x[q])) >= (kEdge ? tlo + 1u : tlo);
     b[q] = ballot(f[q]);
   }
   if ((b[0] | b[1] | b[2] | b[3]) == 0ull) return;
@@ -401,7 +438,7 @@ __device__ inline void main_write(const f4& x, uint64_t v, uint64_t shift, uint3
   for (int q = 0; q < 4; ++q) {
     if (f[q]) {
       if (pos < cap) {
-        cidx[pos] = (uint32_t)(v + q - shift);
+        cidx[pos] = i0 + q;
         cval[pos] = x[q];
       }
       ++pos;
@@ -411,66 +448,92 @@ __device__ inline void main_write(const f4& x, uint64_t v, uint64_t shift, uint3
          __builtin_popcountll(b[3]);
 }
 
+// Each workgroup reads one tile of kTile gradient elements. Workgroup b serves
+// device b % K and takes the device's next tile number from the device's own
+// ticket, so the K tickets (and the look-back chains) are interleaved across
+// the grid. Wave w owns elements [w*4096, (w+1)*4096) of the tile.
 __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
 {
   __shared__ uint32_t s_ticket;
-  __shared__ uint32_t lds[8];
+  __shared__ uint32_t s_wc[kWaves], s_ws[kWaves];
   __shared__ uint64_t s_ex;
   __shared__ double s_e[4];
+  __shared__ uint32_t s_ci[kWaves][kWaveCap];
+  __shared__ float s_cv[kWaves][kWaveCap];
   const uint32_t tid = threadIdx.x, l = lane_id(), w = tid >> 6;
-  if (tid == 0) s_ticket = atomicAdd(c.ticket, 1u);
+  const uint32_t j = blockIdx.x % c.K;
+  if (tid == 0) s_ticket = atomicAdd(c.ticket + j, 1u);
   __syncthreads();
-  const uint32_t t = s_ticket;
-  const uint32_t j = t / c.tpd, tile = t - j * c.tpd;
+  const uint32_t tile = s_ticket;
   const DevDesc d = c.desc[j];
   uint32_t tlo, thi;
   bracket_of(d, c.st[j], tlo, thi);
-  const uint32_t tlo1 = tlo + 1u, thi1 = thi + 1u;
   const uint64_t vbase = (uint64_t)tile * kTile;      // virtual position of the tile
   const Row row{d.grad, d.shift, c.n};
   // Interior tiles hold only real elements: plain aligned loads kept in
   // registers. The (at most two) edge tiles of a device reload per round.
   const bool full = vbase >= row.shift && vbase + kTile <= row.shift + row.n;
+  const uint32_t wv0 = (uint32_t)(w * (kTileRounds * 256) + l * 4);   // this lane's first element in the tile
+  // real index of virtual position vbase + wv0 (may wrap for leading pads; never written)
+  const uint32_t i_base = (uint32_t)(vbase + wv0 - row.shift);
 
-  double e2a = 0.0, e2b = 0.0;
-  uint32_t cnt = 0;
+  double e2[4] = {0.0, 0.0, 0.0, 0.0};
+  uint32_t wc = 0, ws = 0;
   f4 v[kTileRounds];
   if (full) {
-    const float* p = row.p + (vbase - row.shift);
+    const float* p = row.p + (vbase - row.shift) + wv0;
 #pragma unroll
-    for (int r = 0; r < kTileRounds; ++r) v[r] = ld_stream4(p + elem_of<kTileRounds>(w, r, l));
+    for (int r = 0; r < kTileRounds; ++r) v[r] = ld_stream4(p + r * 256);
 #pragma unroll
-    for (int r = 0; r < kTileRounds; ++r) main_count(v[r], tlo1, thi1, e2a, e2b, cnt);
+    for (int r = 0; r < kTileRounds; ++r) {
+      main_stage<false>(v[r], i_base + r * 256, tlo, thi, e2, wc, ws, s_ci[w], s_cv[w]);
+      __builtin_amdgcn_sched_barrier(0);    // keep rounds apart: bounds the live ballot masks
+    }
   } else {
     for (int r = 0; r < kTileRounds; ++r)
-      main_count(load4(row, vbase + elem_of<kTileRounds>(w, r, l), false), tlo1, thi1, e2a, e2b, cnt);
+      main_stage<true>(load4(row, vbase + wv0 + r * 256, false), i_base + r * 256, tlo, thi, e2, wc, ws, s_ci[w],
+                       s_cv[w]);
   }
-  uint32_t tot;
-  const uint32_t wex = wave_prefix_of_block(cnt, lds, tot);
+  if (l == 0) {
+    s_wc[w] = wc;
+    s_ws[w] = ws;
+  }
+  __syncthreads();
+  uint32_t wex = 0, tot_c = 0, tot_s = 0;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) {
+    wex += (i < (int)w) ? s_wc[i] : 0u;
+    tot_c += s_wc[i];
+    tot_s += s_ws[i];
+  }
   if (w == 0) {
     uint64_t ex_c, ex_s;
-    lookback(c.status + (uint64_t)j * c.tpd, tile, tot & 0xFFFFu, tot >> 16, ex_c, ex_s, &c.st[j].err);
+    lookback(c.status + (uint64_t)j * c.tpd, tile, tot_c, tot_s, ex_c, ex_s, &c.st[j].err);
     if (l == 0) s_ex = ex_c;
   }
   __syncthreads();
 
-  // Phase 2: candidates in index order at the tile's offset.
-  if ((tot & 0xFFFFu) != 0u) {
-    uint64_t run = s_ex + (wex & 0xFFFFu);
+  // Phase 2: the wave's candidates, in index order, at the tile's offset.
+  if (wc != 0u) {
+    const uint64_t base = s_ex + wex;
     uint32_t* cidx = c.cand_idx + d.cand_off;
     float* cval = c.cand_val + d.cand_off;
-    if (full) {
-#pragma unroll
-      for (int r = 0; r < kTileRounds; ++r)
-        main_write(v[r], vbase + elem_of<kTileRounds>(w, r, l), row.shift, tlo1, run, d.cap, cidx, cval);
-    } else {
-      for (int r = 0; r < kTileRounds; ++r) {
-        const uint64_t vv = vbase + elem_of<kTileRounds>(w, r, l);
-        main_write(load4(row, vv, false), vv, row.shift, tlo1, run, d.cap, cidx, cval);
+    if (wc <= (uint32_t)kWaveCap) {
+      for (uint32_t i = l; i < wc; i += 64) {
+        const uint64_t pos = base + i;
+        if (pos < d.cap) {
+          cidx[pos] = s_ci[w][i];
+          cval[pos] = s_cv[w][i];
+        }
       }
+    } else {
+      // Rare (dense-candidate regions): reload the wave's rounds and write directly.
+      uint64_t run = base;
+      for (int r = 0; r < kTileRounds; ++r)
+        main_write<true>(load4(row, vbase + wv0 + r * 256, false), i_base + r * 256, tlo, run, d.cap, cidx, cval);
     }
   }
-  const double es = block_sum_f64(e2a + e2b, s_e);
+  const double es = block_sum_f64((e2[0] + e2[1]) + (e2[2] + e2[3]), s_e);
   if (tid == 0) c.epart[(uint64_t)j * c.tpd + tile] = es;
 }
 
