@@ -64,11 +64,12 @@ constexpr uint64_t kCapAlign = 64;
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-  uint32_t K = 0, tpd = 0, ncb = 0, nfb = 0, nbmax = 0, ntile = 0, nrange = 0, s_stride = 0, s_n = 0;
+  uint32_t K = 0, tpd = 0, nslot = 0, ncb = 0, nfb = 0, nbmax = 0, ntile = 0, nrange = 0, s_stride = 0, s_n = 0;
   uint64_t n = 0;
   uint32_t k[kMaxK], cap[kMaxK], mode[kMaxK], r_lo[kMaxK], r_hi[kMaxK];
   uint32_t any_fast = 0;
-  size_t o_desc, o_st, o_hist, o_status, o_epart, o_cidx, o_cval, o_bcnt, o_bpre, o_be, o_ticket, o_aoff, o_aerr;
+  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_sidx, o_sval, o_epart, o_cidx, o_cval, o_bcnt, o_bpre, o_be, o_aoff,
+      o_aerr;
   size_t total = 0;
 };
 
@@ -107,6 +108,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
   L.n = n;
   // Tiles cover the 16-byte-aligned virtual row [0, n + shift), shift <= 3.
   L.tpd = ceil_div_u64(n + 3, kTile);
+  L.nslot = L.tpd * kWaves;
   L.ntile = ceil_div_u64(n, kATile);
   L.nrange = ceil_div_u64(L.ntile, kARange);
   sample_geometry(n, L.s_stride, L.s_n);
@@ -155,14 +157,18 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
     L.o_desc = take(sizeof(DevDesc) * K);
     L.o_st = take(sizeof(DevState) * K);
     L.o_hist = take(sizeof(uint32_t) * (size_t)K * kSlots * kBins);
-    L.o_status = take(sizeof(uint64_t) * (size_t)K * L.tpd);
+    // Slots are needed only by fast-path devices; sized for all K for simplicity.
+    const size_t nslots = L.any_fast ? (size_t)K * L.nslot : 0;
+    L.o_scnt = take(sizeof(uint32_t) * (size_t)K * L.nslot);
+    L.o_soff = take(sizeof(uint32_t) * (size_t)K * L.nslot);
+    L.o_sidx = take(sizeof(uint32_t) * nslots * kWaveCap);
+    L.o_sval = take(sizeof(float) * nslots * kWaveCap);
     L.o_epart = take(sizeof(double) * (size_t)K * L.tpd);
     L.o_cidx = take(sizeof(uint32_t) * sum_cap);
     L.o_cval = take(sizeof(float) * sum_cap);
     L.o_bcnt = take(sizeof(uint64_t) * (size_t)K * L.nbmax);
     L.o_bpre = take(sizeof(uint64_t) * (size_t)K * L.nbmax);
     L.o_be = take(sizeof(double) * (size_t)K * L.nbmax);
-    L.o_ticket = take(sizeof(uint32_t) * kMaxK);
   }
   L.o_aoff = take(sizeof(uint32_t) * (size_t)K * (L.nrange + 1));
   L.o_aerr = take(256);
@@ -178,17 +184,20 @@ Ctx make_ctx(const Layout& L, void* ws)
   c.desc = reinterpret_cast<DevDesc*>(b + L.o_desc);
   c.st = reinterpret_cast<DevState*>(b + L.o_st);
   c.hist = reinterpret_cast<uint32_t*>(b + L.o_hist);
-  c.status = reinterpret_cast<uint64_t*>(b + L.o_status);
+  c.slot_cnt = reinterpret_cast<uint32_t*>(b + L.o_scnt);
+  c.slot_off = reinterpret_cast<uint32_t*>(b + L.o_soff);
+  c.slot_idx = reinterpret_cast<uint32_t*>(b + L.o_sidx);
+  c.slot_val = reinterpret_cast<float*>(b + L.o_sval);
   c.epart = reinterpret_cast<double*>(b + L.o_epart);
   c.cand_idx = reinterpret_cast<uint32_t*>(b + L.o_cidx);
   c.cand_val = reinterpret_cast<float*>(b + L.o_cval);
   c.blk_cnt = reinterpret_cast<uint64_t*>(b + L.o_bcnt);
   c.blk_pre = reinterpret_cast<uint64_t*>(b + L.o_bpre);
   c.blk_e = reinterpret_cast<double*>(b + L.o_be);
-  c.ticket = reinterpret_cast<uint32_t*>(b + L.o_ticket);
   c.n = L.n;
   c.K = L.K;
   c.tpd = L.tpd;
+  c.nslot = L.nslot;
   c.ncb = L.ncb;
   c.nfb = L.nfb;
   c.nbmax = L.nbmax;

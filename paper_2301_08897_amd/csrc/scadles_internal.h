@@ -29,6 +29,7 @@ constexpr uint32_t kKeyInf = 0x80000000u;   // above every 31-bit key
 constexpr uint32_t kKeyMask = 0x7FFFFFFFu;
 constexpr uint64_t kSat31 = 0x7FFFFFFFull;
 constexpr int kFullWorkers = 1024;     // grid of the grid-stride exact-path kernels
+constexpr int kWaveCap = 512;          // main pass: candidates one wave chunk (4096 elements) can stage
 
 enum : uint32_t { kModeFast = 0, kModeExact = 1 };
 
@@ -80,19 +81,22 @@ struct Ctx {
   DevDesc* desc;
   DevState* st;
   uint32_t* hist;         // [K][kSlots][kBins]
-  uint64_t* status;       // [K][tpd] look-back words of the main pass
+  uint32_t* slot_cnt;     // [K][nslot] per-wave candidate | sure << 16 counts of the main pass
+  uint32_t* slot_off;     // [K][nslot] offset of each slot in the candidate list
+  uint32_t* slot_idx;     // [K][nslot][kWaveCap] staged candidates per wave chunk
+  float* slot_val;
   double* epart;          // [K][tpd] sum of squares per main tile
   uint32_t* cand_idx;     // candidate regions
   float* cand_val;
   uint64_t* blk_cnt;      // [K][nbmax] packed (gt | eq << 32) per compaction block
   uint64_t* blk_pre;      // [K][nbmax] exclusive prefix of blk_cnt
   double* blk_e;          // [K][nbmax] kept sum of squares per compaction block
-  uint32_t* ticket;       // [K] main pass tile tickets
   double* energies_out;   // caller's (dev, 2K) or null
   uint8_t* compressed_out;// caller's (dev, K) or null
   uint64_t n;
   uint32_t K;
   uint32_t tpd;           // main tiles per device: ceil((n + 3) / kTile)
+  uint32_t nslot;         // main-pass wave chunks per device: tpd * kWaves
   uint32_t ncb;           // candidate blocks per device (max over devices)
   uint32_t nfb;           // exact-path blocks per device: ceil((n + 3) / kCBlk)
   uint32_t nbmax;         // max(ncb, nfb)

@@ -27,8 +27,6 @@ namespace scadles {
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
-constexpr uint32_t kSpinLimit = 1u << 20;
-constexpr uint64_t kFlagA = 1, kFlagP = 2;
 
 __device__ inline f4 ld_stream4(const float* p) { return __builtin_nontemporal_load(reinterpret_cast<const f4*>(p)); }
 __device__ inline f4 ld4(const float* p) { return *reinterpret_cast<const f4*>(p); }
@@ -76,15 +74,6 @@ __device__ inline f4 load4_guarded(const float* row, uint64_t e, uint64_t rem, b
   return load4(Row{row, 0, rem}, e, stream);
 }
 
-
-__device__ inline uint64_t atomic_load_u64(const uint64_t* p)
-{
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline void atomic_store_u64(uint64_t* p, uint64_t v)
-{
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 // ---- radix-selection digit view ------------------------------------------------------------
 struct SelView {
@@ -189,12 +178,9 @@ __global__ __launch_bounds__(kBlock) void k_prep(Ctx c, PrepArgs a)
     }
     c.st[j] = s;
   }
-  if (blockIdx.x == 0 && threadIdx.x < K) c.ticket[threadIdx.x] = 0u;
   const uint64_t nh = (uint64_t)K * kSlots * kBins;
-  const uint64_t ns = (uint64_t)K * c.tpd;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
   for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < nh; i += stride) c.hist[i] = 0u;
-  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < ns; i += stride) c.status[i] = 0ull;
 }
 
 // ---- 1. bracket: histogram pass over the systematic sample (two selections) ----------------
@@ -297,61 +283,10 @@ __global__ __launch_bounds__(64) void k_find(Ctx c, int s_begin, int s_end)
 }
 
 // ---- 2. main pass: one read of every gradient ------------------------------------------------
-// Decoupled look-back over the tiles of one device (Merrill & Garland, 2016):
-// each tile publishes its own counts at once, then sums its predecessors'
-// until it meets an inclusive prefix. Status word: flag(2) | sure(31) | cand(31),
-// saturating at 2^31 - 1 (a saturated count always exceeds the capacity).
-// Tiles take their number from their device's ticket in start order, so every
-// tile waited on has started and never waits on a later tile; the spin is
-// bounded anyway and a timeout sends the device to the exact path.
-__device__ inline uint64_t lb_pack(uint64_t flag, uint64_t cand, uint64_t sure)
-{
-  cand = cand < kSat31 ? cand : kSat31;
-  sure = sure < kSat31 ? sure : kSat31;
-  return (flag << 62) | (sure << 31) | cand;
-}
-
-__device__ inline void lookback(uint64_t* stat, uint32_t tile, uint64_t cand, uint64_t sure, uint64_t& ex_c,
-                                uint64_t& ex_s, uint32_t* err)
-{
-  const uint32_t l = lane_id();
-  ex_c = ex_s = 0;
-  if (tile == 0) {
-    if (l == 0) atomic_store_u64(&stat[0], lb_pack(kFlagP, cand, sure));
-    return;
-  }
-  if (l == 0) atomic_store_u64(&stat[tile], lb_pack(kFlagA, cand, sure));
-  int64_t end = (int64_t)tile - 1;
-  uint32_t spins = 0;
-  while (true) {
-    const int64_t p = end - (int64_t)l;
-    const uint64_t s = (p >= 0) ? atomic_load_u64(&stat[p]) : lb_pack(kFlagP, 0, 0);
-    const uint32_t f = (uint32_t)(s >> 62);
-    const uint64_t pm = ballot(f == kFlagP), xm = ballot(f == 0);
-    const uint32_t fp = pm ? (uint32_t)__builtin_ctzll(pm) : 64u;
-    const uint64_t needed = (fp >= 63) ? ~0ull : ((2ull << fp) - 1ull);
-    if (xm & needed) {
-      if (++spins > kSpinLimit) {
-        if (l == 0) atomicOr(err, 1u);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-      continue;
-    }
-    const uint64_t vc = (l <= fp) ? (s & kSat31) : 0ull;
-    const uint64_t vs = (l <= fp) ? ((s >> 31) & kSat31) : 0ull;
-    ex_c += wave_sum_u64(vc);
-    ex_s += wave_sum_u64(vs);
-    if (fp < 64) break;
-    end -= 64;
-  }
-  if (l == 0) atomic_store_u64(&stat[tile], lb_pack(kFlagP, cand + ex_c, sure + ex_s));
-}
-
-// Element order inside a workgroup: wave w owns the contiguous chunk
-// [w*R*256, (w+1)*R*256); in round r lane l holds elements r*256 + 4l .. +3.
-// Every load is one contiguous KiB per wave, and index order is (wave, round,
-// lane, component), so a wave can keep a running output offset.
+// No workgroup waits on another: wave w of tile t of device j stages its
+// candidates (keys >= t_lo) in index order and writes them to its own slot
+// (kWaveCap entries) with a count; a per-device scan of the slot counts then
+// gives every slot its offset in the device's candidate list.
 template <int R>
 __device__ inline uint64_t elem_of(uint32_t w, int r, uint32_t l)
 {
@@ -374,9 +309,6 @@ __device__ inline uint32_t wave_prefix_of_block(uint32_t packed_lane, uint32_t* 
   __syncthreads();
   return ex;
 }
-
-// Candidates a wave stages in LDS before its output offset is known.
-constexpr int kWaveCap = 512;
 
 // One round of phase 1 for one wave: sum of squares, counts of candidates
 // (key >= tlo) and sure keys (key >= thi), and the round's candidates staged in
@@ -418,53 +350,17 @@ __device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32
                    __builtin_popcountll(b[3]));
 }
 
-// Phase 2 for a wave whose candidates overflowed its LDS stage: recompute the
-// round's flags (on rank keys, so pads never count) and write the candidates
-// straight to their global positions.
-template <bool kEdge>
-__device__ inline void main_write(const f4& x, uint32_t i0, uint32_t tlo, uint64_t& run, uint32_t cap, uint32_t* cidx,
-                                  float* cval)
-{
-  bool f[4];
-  uint64_t b[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    f[q] = (kEdge ? rank_key(x[q]) : key_of(x[q])) >= (kEdge ? tlo + 1u : tlo);
-    b[q] = ballot(f[q]);
-  }
-  if ((b[0] | b[1] | b[2] | b[3]) == 0ull) return;
-  uint64_t pos = run + mbcnt(b[0]) + mbcnt(b[1]) + mbcnt(b[2]) + mbcnt(b[3]);
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    if (f[q]) {
-      if (pos < cap) {
-        cidx[pos] = i0 + q;
-        cval[pos] = x[q];
-      }
-      ++pos;
-    }
-  }
-  run += __builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) + __builtin_popcountll(b[2]) +
-         __builtin_popcountll(b[3]);
-}
-
-// Each workgroup reads one tile of kTile gradient elements. Workgroup b serves
-// device b % K and takes the device's next tile number from the device's own
-// ticket, so the K tickets (and the look-back chains) are interleaved across
-// the grid. Wave w owns elements [w*4096, (w+1)*4096) of the tile.
+// Each workgroup reads one tile of kTile gradient elements (workgroup b: device
+// b / tpd, tile b % tpd). Wave w owns elements [w*4096, (w+1)*4096) of the tile
+// and slot tile*kWaves + w of its device. A slot whose wave found more than
+// kWaveCap candidates stays empty; the gather re-scans that chunk instead.
 __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
 {
-  __shared__ uint32_t s_ticket;
-  __shared__ uint32_t s_wc[kWaves], s_ws[kWaves];
-  __shared__ uint64_t s_ex;
   __shared__ double s_e[4];
   __shared__ uint32_t s_ci[kWaves][kWaveCap];
   __shared__ float s_cv[kWaves][kWaveCap];
   const uint32_t tid = threadIdx.x, l = lane_id(), w = tid >> 6;
-  const uint32_t j = blockIdx.x % c.K;
-  if (tid == 0) s_ticket = atomicAdd(c.ticket + j, 1u);
-  __syncthreads();
-  const uint32_t tile = s_ticket;
+  const uint32_t j = blockIdx.x / c.tpd, tile = blockIdx.x - j * c.tpd;
   const DevDesc d = c.desc[j];
   uint32_t tlo, thi;
   bracket_of(d, c.st[j], tlo, thi);
@@ -479,9 +375,9 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
 
   double e2[4] = {0.0, 0.0, 0.0, 0.0};
   uint32_t wc = 0, ws = 0;
-  f4 v[kTileRounds];
   if (full) {
     const float* p = row.p + (vbase - row.shift) + wv0;
+    f4 v[kTileRounds];
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r) v[r] = ld_stream4(p + r * 256);
 #pragma unroll
@@ -494,60 +390,72 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
       main_stage<true>(load4(row, vbase + wv0 + r * 256, false), i_base + r * 256, tlo, thi, e2, wc, ws, s_ci[w],
                        s_cv[w]);
   }
-  if (l == 0) {
-    s_wc[w] = wc;
-    s_ws[w] = ws;
-  }
-  __syncthreads();
-  uint32_t wex = 0, tot_c = 0, tot_s = 0;
-#pragma unroll
-  for (int i = 0; i < kWaves; ++i) {
-    wex += (i < (int)w) ? s_wc[i] : 0u;
-    tot_c += s_wc[i];
-    tot_s += s_ws[i];
-  }
-  if (w == 0) {
-    uint64_t ex_c, ex_s;
-    lookback(c.status + (uint64_t)j * c.tpd, tile, tot_c, tot_s, ex_c, ex_s, &c.st[j].err);
-    if (l == 0) s_ex = ex_c;
-  }
-  __syncthreads();
-
-  // Phase 2: the wave's candidates, in index order, at the tile's offset.
-  if (wc != 0u) {
-    const uint64_t base = s_ex + wex;
-    uint32_t* cidx = c.cand_idx + d.cand_off;
-    float* cval = c.cand_val + d.cand_off;
-    if (wc <= (uint32_t)kWaveCap) {
-      for (uint32_t i = l; i < wc; i += 64) {
-        const uint64_t pos = base + i;
-        if (pos < d.cap) {
-          cidx[pos] = s_ci[w][i];
-          cval[pos] = s_cv[w][i];
-        }
-      }
-    } else {
-      // Rare (dense-candidate regions): reload the wave's rounds and write directly.
-      uint64_t run = base;
-      for (int r = 0; r < kTileRounds; ++r)
-        main_write<true>(load4(row, vbase + wv0 + r * 256, false), i_base + r * 256, tlo, run, d.cap, cidx, cval);
+  // The wave's slot (its own LDS region, written by itself: no barrier needed).
+  const uint64_t slot = (uint64_t)j * c.nslot + (uint64_t)tile * kWaves + w;
+  if (l == 0) c.slot_cnt[slot] = wc | (ws << 16);
+  if (wc <= (uint32_t)kWaveCap) {
+    uint32_t* si = c.slot_idx + slot * kWaveCap;
+    float* sv = c.slot_val + slot * kWaveCap;
+    for (uint32_t i = l; i < wc; i += 64) {
+      si[i] = s_ci[w][i];
+      sv[i] = s_cv[w][i];
     }
   }
   const double es = block_sum_f64((e2[0] + e2[1]) + (e2[2] + e2[3]), s_e);
   if (tid == 0) c.epart[(uint64_t)j * c.tpd + tile] = es;
 }
 
-// ---- after the main pass: energies, candidate totals, path decision ---------------------------
+// ---- after the main pass: energies, slot offsets, candidate totals, path decision ----------
+__device__ inline uint64_t wave_incl_scan_u64(uint64_t v)
+{
+  const uint32_t l = lane_id();
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    uint64_t t = __shfl_up(v, d, 64);
+    if (l >= (uint32_t)d) v += t;
+  }
+  return v;
+}
+
 __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
 {
   __shared__ double s_e[4];
-  const uint32_t j = blockIdx.x;
+  __shared__ uint64_t s_w[4];
+  const uint32_t j = blockIdx.x, tid = threadIdx.x;
   double acc = 0.0;
-  for (uint32_t t = threadIdx.x; t < c.tpd; t += kBlock) acc += c.epart[(uint64_t)j * c.tpd + t];
+  for (uint32_t t = tid; t < c.tpd; t += kBlock) acc += c.epart[(uint64_t)j * c.tpd + t];
   const double e_all = block_sum_f64(acc, s_e);
-  if (threadIdx.x != 0) return;
-  DevState& s = c.st[j];
   const DevDesc d = c.desc[j];
+  uint64_t cand = 0, sure = 0;
+  if (d.mode == kModeFast) {
+    // Slot counts (cand | sure << 16) -> slot offsets in the candidate list; totals.
+    const uint32_t* cnt = c.slot_cnt + (uint64_t)j * c.nslot;
+    uint32_t* off = c.slot_off + (uint64_t)j * c.nslot;
+    const uint32_t per = (c.nslot + kBlock - 1) / kBlock;
+    const uint32_t b0 = tid * per < c.nslot ? tid * per : c.nslot;
+    const uint32_t b1 = (b0 + per < c.nslot) ? b0 + per : c.nslot;
+    uint64_t sc = 0, ss = 0;
+    for (uint32_t b = b0; b < b1; ++b) {
+      sc += cnt[b] & 0xFFFFu;
+      ss += cnt[b] >> 16;
+    }
+    const uint64_t packed = sc | (ss << 32);
+    const uint64_t incl = wave_incl_scan_u64(packed);
+    if (lane_id() == 63) s_w[tid >> 6] = incl;
+    __syncthreads();
+    uint64_t run = incl - packed;
+    for (uint32_t i = 0; i < (tid >> 6); ++i) run += s_w[i];
+    const uint64_t tot = s_w[0] + s_w[1] + s_w[2] + s_w[3];
+    cand = tot & 0xFFFFFFFFull;
+    sure = tot >> 32;
+    uint64_t oc = run & 0xFFFFFFFFull;
+    for (uint32_t b = b0; b < b1; ++b) {
+      off[b] = (uint32_t)oc;
+      oc += cnt[b] & 0xFFFFu;
+    }
+  }
+  if (tid != 0) return;
+  DevState& s = c.st[j];
   s.e_all = e_all;
   bool fb = (d.mode != kModeFast) || c.force_fallback;
   uint32_t tlo, thi;
@@ -555,12 +463,10 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
   s.t_lo = tlo;
   s.t_hi = thi;
   if (d.mode == kModeFast) {
-    const uint64_t wd = c.status[(uint64_t)j * c.tpd + c.tpd - 1];
-    if ((wd >> 62) != kFlagP) s.err |= 4u;
-    s.cand = wd & kSat31;
-    s.sure = (wd >> 31) & kSat31;
+    s.cand = cand;
+    s.sure = sure;
     if (s.err) fb = true;
-    if (s.cand < d.k || s.cand > d.cap) fb = true;
+    if (cand < d.k || cand > d.cap) fb = true;
   }
   Sel sel;
   __builtin_memset(&sel, 0, sizeof(sel));
@@ -588,6 +494,70 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
     const uint32_t b = bitlen32(sel.hi - sel.lo - 1u);
     sel.bits = b ? b : 1u;
     s.sel[kSlotCand] = sel;
+  }
+}
+
+// Packs every slot into the device's candidate list at its offset (index
+// order is kept: slots are in index order and each slot is). A slot whose wave
+// overflowed is rebuilt by re-scanning its 4096-element chunk of the gradient.
+// Workgroup: kGatherSlots consecutive slots of one device, one wave per slot.
+constexpr int kGatherSlots = 16;
+
+__global__ __launch_bounds__(kBlock) void k_gather(Ctx c)
+{
+  const uint32_t groups = (c.nslot + kGatherSlots - 1) / kGatherSlots;
+  const uint32_t j = blockIdx.x / groups, g = blockIdx.x - j * groups;
+  const DevState& st = c.st[j];
+  if (st.fallback) return;
+  const DevDesc d = c.desc[j];
+  const uint32_t l = lane_id(), w = threadIdx.x >> 6;
+  uint32_t* cidx = c.cand_idx + d.cand_off;
+  float* cval = c.cand_val + d.cand_off;
+  for (uint32_t s = g * kGatherSlots + w; s < (g + 1) * kGatherSlots && s < c.nslot; s += kWaves) {
+    const uint64_t slot = (uint64_t)j * c.nslot + s;
+    const uint32_t cnt = c.slot_cnt[slot] & 0xFFFFu;
+    const uint32_t off = c.slot_off[slot];
+    if (cnt == 0) continue;
+    if (cnt <= (uint32_t)kWaveCap) {
+      const uint32_t* si = c.slot_idx + slot * kWaveCap;
+      const float* sv = c.slot_val + slot * kWaveCap;
+      for (uint32_t i = l; i < cnt; i += 64) {
+        if ((uint64_t)off + i < d.cap) {
+          cidx[off + i] = si[i];
+          cval[off + i] = sv[i];
+        }
+      }
+      continue;
+    }
+    // Overflowed slot: its chunk is tile s / kWaves, wave s % kWaves.
+    const Row row{d.grad, d.shift, c.n};
+    const uint64_t v0 = (uint64_t)(s / kWaves) * kTile + (uint64_t)(s % kWaves) * (kTileRounds * 256) + l * 4;
+    const uint32_t tlo1 = st.t_lo + 1u;
+    uint64_t run = off;
+    for (int r = 0; r < kTileRounds; ++r) {
+      const uint64_t v = v0 + (uint64_t)r * 256;
+      const f4 x = load4(row, v, false);
+      bool f[4];
+      uint64_t b[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        f[q] = rank_key(x[q]) >= tlo1;
+        b[q] = ballot(f[q]);
+      }
+      uint64_t pos = run + mbcnt(b[0]) + mbcnt(b[1]) + mbcnt(b[2]) + mbcnt(b[3]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (f[q]) {
+          if (pos < d.cap) {
+            cidx[pos] = (uint32_t)(v + q - row.shift);
+            cval[pos] = x[q];
+          }
+          ++pos;
+        }
+      }
+      run += __builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) + __builtin_popcountll(b[2]) +
+             __builtin_popcountll(b[3]);
+    }
   }
 }
 
@@ -711,17 +681,6 @@ __global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c, uint32_t ncand_block
       if (threadIdx.x == 0) c.blk_cnt[(uint64_t)j * c.nbmax + blk] = r;
     }
   }
-}
-
-__device__ inline uint64_t wave_incl_scan_u64(uint64_t v)
-{
-  const uint32_t l = lane_id();
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    uint64_t t = __shfl_up(v, d, 64);
-    if (l >= (uint32_t)d) v += t;
-  }
-  return v;
 }
 
 __device__ inline uint32_t blocks_of(const Ctx& c, const DevState& s)
@@ -935,7 +894,7 @@ __global__ __launch_bounds__(kBlock) void k_final(Ctx c)
 // ---- host-side launchers ---------------------------------------------------------------------
 hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipEvent_t* ev)
 {
-  const uint64_t zero_words = (uint64_t)c.K * kSlots * kBins + (uint64_t)c.K * c.tpd;
+  const uint64_t zero_words = (uint64_t)c.K * kSlots * kBins;
   uint32_t gprep = (uint32_t)((zero_words + kBlock * 8 - 1) / (kBlock * 8));
   gprep = gprep < 1 ? 1 : (gprep > 2048 ? 2048 : gprep);
   k_prep<<<gprep, kBlock, 0, s>>>(c, a);
@@ -949,6 +908,7 @@ hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, h
   k_main<<<c.K * c.tpd, kBlock, 0, s>>>(c);
   if (ev) (void)hipEventRecord(ev[2], s);
   k_post<<<c.K, kBlock, 0, s>>>(c);
+  if (p.any_fast) k_gather<<<c.K * ((c.nslot + kGatherSlots - 1) / kGatherSlots), kBlock, 0, s>>>(c);
   const uint32_t g = p.ncand_blocks + p.full_workers;
   for (int pass = 0; pass < 3; ++pass) {
     k_hist_cf<<<g, kBlock, 0, s>>>(c, p.ncand_blocks);
