@@ -30,6 +30,9 @@ constexpr uint32_t kKeyMask = 0x7FFFFFFFu;
 constexpr uint64_t kSat31 = 0x7FFFFFFFull;
 constexpr int kFullWorkers = 1024;     // grid of the grid-stride exact-path kernels
 constexpr int kWaveCap = 512;          // main pass: candidates one wave chunk (4096 elements) can stage
+constexpr int kScanChunk = 4096;       // slots per workgroup of the slot-offset scan
+constexpr int kMaxChunks = 256;        // >= ceil(nslot / kScanChunk) for n < 2^32
+constexpr int kGatherSlots = 8;        // slots per wave in the candidate gather
 
 enum : uint32_t { kModeFast = 0, kModeExact = 1 };
 
@@ -82,7 +85,9 @@ struct Ctx {
   DevState* st;
   uint32_t* hist;         // [K][kSlots][kBins]
   uint32_t* slot_cnt;     // [K][nslot] per-wave candidate | sure << 16 counts of the main pass
-  uint32_t* slot_off;     // [K][nslot] offset of each slot in the candidate list
+  uint32_t* slot_off;     // [K][nslot] offset of each slot within its scan chunk
+  uint64_t* chunk_tot;    // [K][kMaxChunks] candidate | sure << 32 totals of each scan chunk
+  uint32_t* chunk_off;    // [K][kMaxChunks] offset of each scan chunk in the candidate list
   uint32_t* slot_idx;     // [K][nslot][kWaveCap] staged candidates per wave chunk
   float* slot_val;
   double* epart;          // [K][tpd] sum of squares per main tile

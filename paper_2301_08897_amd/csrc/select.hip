@@ -417,6 +417,52 @@ __device__ inline uint64_t wave_incl_scan_u64(uint64_t v)
   return v;
 }
 
+// Slot offsets, level 1: one workgroup per kScanChunk slots of a fast device;
+// each thread takes 16 consecutive slots. Writes every slot's candidate offset
+// within its chunk and the chunk's totals (cand | sure << 32).
+__global__ __launch_bounds__(kBlock) void k_slot_scan(Ctx c)
+{
+  __shared__ uint64_t s_w[4];
+  const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
+  const uint32_t j = blockIdx.x / nchunk, ch = blockIdx.x - j * nchunk;
+  if (c.desc[j].mode != kModeFast) return;
+  const uint32_t tid = threadIdx.x;
+  const uint32_t s0 = ch * kScanChunk + tid * 16;
+  const uint32_t* cnt = c.slot_cnt + (uint64_t)j * c.nslot;
+  uint32_t v[16];
+  if (s0 + 16 <= c.nslot) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const u4 x = ldu4(cnt + s0 + 4 * i);
+      v[4 * i] = x.x;
+      v[4 * i + 1] = x.y;
+      v[4 * i + 2] = x.z;
+      v[4 * i + 3] = x.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = (s0 + i < c.nslot) ? cnt[s0 + i] : 0u;
+  }
+  uint64_t sum = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) sum += (uint64_t)(v[i] & 0xFFFFu) | ((uint64_t)(v[i] >> 16) << 32);
+  const uint64_t incl = wave_incl_scan_u64(sum);
+  if (lane_id() == 63) s_w[tid >> 6] = incl;
+  __syncthreads();
+  uint64_t run = incl - sum;
+  for (uint32_t i = 0; i < (tid >> 6); ++i) run += s_w[i];
+  uint32_t* off = c.slot_off + (uint64_t)j * c.nslot;
+  uint32_t oc = (uint32_t)(run & 0xFFFFFFFFull);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    if (s0 + i < c.nslot) off[s0 + i] = oc;
+    oc += v[i] & 0xFFFFu;
+  }
+  if (tid == kBlock - 1) c.chunk_tot[(uint64_t)j * kMaxChunks + ch] = run + sum;
+}
+
+// Slot offsets, level 2, and the per-device decision: chunk prefixes, candidate
+// totals, energies, then the exact path (fallback) or the candidate selection.
 __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
 {
   __shared__ double s_e[4];
@@ -428,31 +474,17 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
   const DevDesc d = c.desc[j];
   uint64_t cand = 0, sure = 0;
   if (d.mode == kModeFast) {
-    // Slot counts (cand | sure << 16) -> slot offsets in the candidate list; totals.
-    const uint32_t* cnt = c.slot_cnt + (uint64_t)j * c.nslot;
-    uint32_t* off = c.slot_off + (uint64_t)j * c.nslot;
-    const uint32_t per = (c.nslot + kBlock - 1) / kBlock;
-    const uint32_t b0 = tid * per < c.nslot ? tid * per : c.nslot;
-    const uint32_t b1 = (b0 + per < c.nslot) ? b0 + per : c.nslot;
-    uint64_t sc = 0, ss = 0;
-    for (uint32_t b = b0; b < b1; ++b) {
-      sc += cnt[b] & 0xFFFFu;
-      ss += cnt[b] >> 16;
-    }
-    const uint64_t packed = sc | (ss << 32);
-    const uint64_t incl = wave_incl_scan_u64(packed);
+    const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;    // <= kMaxChunks = kBlock
+    const uint64_t v = tid < nchunk ? c.chunk_tot[(uint64_t)j * kMaxChunks + tid] : 0ull;
+    const uint64_t incl = wave_incl_scan_u64(v);
     if (lane_id() == 63) s_w[tid >> 6] = incl;
     __syncthreads();
-    uint64_t run = incl - packed;
+    uint64_t run = incl - v;
     for (uint32_t i = 0; i < (tid >> 6); ++i) run += s_w[i];
+    if (tid < nchunk) c.chunk_off[(uint64_t)j * kMaxChunks + tid] = (uint32_t)(run & 0xFFFFFFFFull);
     const uint64_t tot = s_w[0] + s_w[1] + s_w[2] + s_w[3];
     cand = tot & 0xFFFFFFFFull;
     sure = tot >> 32;
-    uint64_t oc = run & 0xFFFFFFFFull;
-    for (uint32_t b = b0; b < b1; ++b) {
-      off[b] = (uint32_t)oc;
-      oc += cnt[b] & 0xFFFFu;
-    }
   }
   if (tid != 0) return;
   DevState& s = c.st[j];
@@ -500,64 +532,97 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
 // Packs every slot into the device's candidate list at its offset (index
 // order is kept: slots are in index order and each slot is). A slot whose wave
 // overflowed is rebuilt by re-scanning its 4096-element chunk of the gradient.
-// Workgroup: kGatherSlots consecutive slots of one device, one wave per slot.
-constexpr int kGatherSlots = 16;
+__device__ inline void gather_rescan(const Ctx& c, const DevDesc& d, uint32_t tlo, uint32_t s, uint64_t off,
+                                     uint32_t* cidx, float* cval)
+{
+  const uint32_t l = lane_id();
+  const Row row{d.grad, d.shift, c.n};
+  const uint64_t v0 = (uint64_t)(s / kWaves) * kTile + (uint64_t)(s % kWaves) * (kTileRounds * 256) + l * 4;
+  const uint32_t tlo1 = tlo + 1u;
+  uint64_t run = off;
+  for (int r = 0; r < kTileRounds; ++r) {
+    const uint64_t v = v0 + (uint64_t)r * 256;
+    const f4 x = load4(row, v, false);
+    bool f[4];
+    uint64_t b[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      f[q] = rank_key(x[q]) >= tlo1;
+      b[q] = ballot(f[q]);
+    }
+    uint64_t pos = run + mbcnt(b[0]) + mbcnt(b[1]) + mbcnt(b[2]) + mbcnt(b[3]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (f[q]) {
+        if (pos < d.cap) {
+          cidx[pos] = (uint32_t)(v + q - row.shift);
+          cval[pos] = x[q];
+        }
+        ++pos;
+      }
+    }
+    run += __builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) + __builtin_popcountll(b[2]) +
+           __builtin_popcountll(b[3]);
+  }
+}
 
+// Each wave takes kGatherSlots consecutive slots and first issues the loads of
+// all of them (metadata, then the first 64 entries of each), then stores.
 __global__ __launch_bounds__(kBlock) void k_gather(Ctx c)
 {
-  const uint32_t groups = (c.nslot + kGatherSlots - 1) / kGatherSlots;
+  constexpr uint32_t kPerBlock = kGatherSlots * kWaves;
+  const uint32_t groups = (c.nslot + kPerBlock - 1) / kPerBlock;
   const uint32_t j = blockIdx.x / groups, g = blockIdx.x - j * groups;
   const DevState& st = c.st[j];
   if (st.fallback) return;
   const DevDesc d = c.desc[j];
   const uint32_t l = lane_id(), w = threadIdx.x >> 6;
+  const uint32_t s0 = g * kPerBlock + w * kGatherSlots;
+  if (s0 >= c.nslot) return;
   uint32_t* cidx = c.cand_idx + d.cand_off;
   float* cval = c.cand_val + d.cand_off;
-  for (uint32_t s = g * kGatherSlots + w; s < (g + 1) * kGatherSlots && s < c.nslot; s += kWaves) {
-    const uint64_t slot = (uint64_t)j * c.nslot + s;
-    const uint32_t cnt = c.slot_cnt[slot] & 0xFFFFu;
-    const uint32_t off = c.slot_off[slot];
-    if (cnt == 0) continue;
-    if (cnt <= (uint32_t)kWaveCap) {
-      const uint32_t* si = c.slot_idx + slot * kWaveCap;
-      const float* sv = c.slot_val + slot * kWaveCap;
-      for (uint32_t i = l; i < cnt; i += 64) {
-        if ((uint64_t)off + i < d.cap) {
-          cidx[off + i] = si[i];
-          cval[off + i] = sv[i];
-        }
-      }
-      continue;
-    }
-    // Overflowed slot: its chunk is tile s / kWaves, wave s % kWaves.
-    const Row row{d.grad, d.shift, c.n};
-    const uint64_t v0 = (uint64_t)(s / kWaves) * kTile + (uint64_t)(s % kWaves) * (kTileRounds * 256) + l * 4;
-    const uint32_t tlo1 = st.t_lo + 1u;
-    uint64_t run = off;
-    for (int r = 0; r < kTileRounds; ++r) {
-      const uint64_t v = v0 + (uint64_t)r * 256;
-      const f4 x = load4(row, v, false);
-      bool f[4];
-      uint64_t b[4];
+  // lane i < kGatherSlots: metadata of slot s0 + i
+  uint32_t m_cnt = 0, m_off = 0;
+  if (l < (uint32_t)kGatherSlots && s0 + l < c.nslot) {
+    const uint64_t slot = (uint64_t)j * c.nslot + s0 + l;
+    m_cnt = c.slot_cnt[slot] & 0xFFFFu;
+    m_off = c.chunk_off[(uint64_t)j * kMaxChunks + (s0 + l) / kScanChunk] + c.slot_off[slot];
+  }
+  uint32_t ri[kGatherSlots];
+  float rv[kGatherSlots];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        f[q] = rank_key(x[q]) >= tlo1;
-        b[q] = ballot(f[q]);
-      }
-      uint64_t pos = run + mbcnt(b[0]) + mbcnt(b[1]) + mbcnt(b[2]) + mbcnt(b[3]);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if (f[q]) {
-          if (pos < d.cap) {
-            cidx[pos] = (uint32_t)(v + q - row.shift);
-            cval[pos] = x[q];
-          }
-          ++pos;
-        }
-      }
-      run += __builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) + __builtin_popcountll(b[2]) +
-             __builtin_popcountll(b[3]);
+  for (int i = 0; i < kGatherSlots; ++i) {
+    const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
+    ri[i] = 0u;
+    rv[i] = 0.f;
+    if (cn <= (uint32_t)kWaveCap && l < cn) {
+      const uint64_t slot = (uint64_t)j * c.nslot + s0 + i;
+      ri[i] = c.slot_idx[slot * kWaveCap + l];
+      rv[i] = c.slot_val[slot * kWaveCap + l];
     }
+  }
+#pragma unroll
+  for (int i = 0; i < kGatherSlots; ++i) {
+    const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
+    const uint32_t off = __builtin_amdgcn_readlane(m_off, i);
+    if (cn == 0u || cn > (uint32_t)kWaveCap) continue;
+    if (l < cn && (uint64_t)off + l < d.cap) {
+      cidx[off + l] = ri[i];
+      cval[off + l] = rv[i];
+    }
+    const uint64_t slot = (uint64_t)j * c.nslot + s0 + i;
+    for (uint32_t e = 64 + l; e < cn; e += 64) {
+      if ((uint64_t)off + e < d.cap) {
+        cidx[off + e] = c.slot_idx[slot * kWaveCap + e];
+        cval[off + e] = c.slot_val[slot * kWaveCap + e];
+      }
+    }
+  }
+  // Overflowed slots (rare): rebuild from the gradient chunk.
+#pragma unroll 1
+  for (int i = 0; i < kGatherSlots; ++i) {
+    const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
+    if (cn > (uint32_t)kWaveCap) gather_rescan(c, d, st.t_lo, s0 + i, __builtin_amdgcn_readlane(m_off, i), cidx, cval);
   }
 }
 
@@ -907,8 +972,12 @@ hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, h
   if (ev) (void)hipEventRecord(ev[1], s);
   k_main<<<c.K * c.tpd, kBlock, 0, s>>>(c);
   if (ev) (void)hipEventRecord(ev[2], s);
+  if (p.any_fast) k_slot_scan<<<c.K * ((c.nslot + kScanChunk - 1) / kScanChunk), kBlock, 0, s>>>(c);
   k_post<<<c.K, kBlock, 0, s>>>(c);
-  if (p.any_fast) k_gather<<<c.K * ((c.nslot + kGatherSlots - 1) / kGatherSlots), kBlock, 0, s>>>(c);
+  if (p.any_fast) {
+    constexpr uint32_t kPerBlock = kGatherSlots * kWaves;
+    k_gather<<<c.K * ((c.nslot + kPerBlock - 1) / kPerBlock), kBlock, 0, s>>>(c);
+  }
   const uint32_t g = p.ncand_blocks + p.full_workers;
   for (int pass = 0; pass < 3; ++pass) {
     k_hist_cf<<<g, kBlock, 0, s>>>(c, p.ncand_blocks);

@@ -117,7 +117,10 @@ def test_workspace_queries(sc):
     assert sc.workspace_bytes(1, 0, [0.5]) == 0
     assert sc.workspace_bytes(65, 100, [0.5] * 65) == 0
     assert sc.workspace_bytes(2, 100, [0.5, 2.0]) == 0
-    big = sc.workspace_bytes(32, 143_667_240, [0.01] * 32)
-    assert 0 < big < 2 * 1024**3           # candidate regions are a few k per device, not n
+    K, n = 32, 143_667_240
+    big = sc.workspace_bytes(K, n, [0.01] * K)
+    # per-wave candidate slots take one byte per gradient element; the candidate
+    # lists and the rest are a few k per device
+    assert 0 < big < K * n + 2 * 1024**3
     assert sc.aggregate_workspace_bytes(0, 10) == 0
     assert sc.aggregate_workspace_bytes(4, 1 << 20) > 0
