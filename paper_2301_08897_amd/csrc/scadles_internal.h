@@ -76,7 +76,7 @@ struct DevState {
   uint64_t c_gt, need;    // keys above thr; keys equal to thr that are kept
   double e_all, e_kept;
   uint32_t sparse;        // 1: the device sends Top-k (adaptive rule), 0: dense
-  uint32_t pad2;
+  uint32_t ovf_used;      // entries taken in the device's overflow region
 };
 
 // Kernel context: where everything lives in the workspace, plus call scalars.
@@ -90,6 +90,9 @@ struct Ctx {
   uint32_t* chunk_off;    // [K][kMaxChunks] offset of each scan chunk in the candidate list
   uint32_t* slot_idx;     // [K][nslot][kWaveCap] staged candidates per wave chunk
   float* slot_val;
+  uint32_t* slot_ovf;     // [K][nslot] start in the overflow region of a slot with > kWaveCap candidates
+  uint32_t* ovf_idx;      // per-device overflow regions (cap entries each, at cand_off)
+  float* ovf_val;
   double* epart;          // [K][tpd] sum of squares per main tile
   uint32_t* cand_idx;     // candidate regions
   float* cand_val;

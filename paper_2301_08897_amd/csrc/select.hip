@@ -28,16 +28,31 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
 
-__device__ inline f4 ld_stream4(const float* p) { return __builtin_nontemporal_load(reinterpret_cast<const f4*>(p)); }
-__device__ inline f4 ld4(const float* p) { return *reinterpret_cast<const f4*>(p); }
-__device__ inline u4 ldu4(const uint32_t* p) { return *reinterpret_cast<const u4*>(p); }
+// Pointers read from the device descriptors are generic; marking them global
+// lets the compiler emit global_* instead of flat_* memory instructions.
+// (The host compilation pass of this file sees plain pointers.)
+#if defined(__HIP_DEVICE_COMPILE__)
+#define GLOBAL __attribute__((address_space(1)))
+#else
+#define GLOBAL
+#endif
+template <class T>
+__device__ inline const GLOBAL T* gptr(const T* p) { return (const GLOBAL T*)p; }
+template <class T>
+__device__ inline GLOBAL T* gptr(T* p) { return (GLOBAL T*)p; }
+
+__device__ inline f4 ld_stream4(const GLOBAL float* p) { return __builtin_nontemporal_load((const GLOBAL f4*)p); }
+__device__ inline f4 ld4(const GLOBAL float* p) { return *(const GLOBAL f4*)p; }
+__device__ inline f4 ld_stream4(const float* p) { return ld_stream4(gptr(p)); }
+__device__ inline f4 ld4(const float* p) { return ld4(gptr(p)); }
+__device__ inline u4 ldu4(const uint32_t* p) { return *(const GLOBAL u4*)gptr(p); }
 
 // A device's gradient seen in a 16-byte-aligned "virtual" frame: real element i
 // sits at virtual position i + shift, shift = (address / 4) % 4, so every group
 // of 4 virtual positions is one aligned 16-byte word. Positions outside the real
 // range read as the pad pattern 0xFFFFFFFF, which rank_key maps to 0.
 struct Row {
-  const float* p;      // real element 0
+  const GLOBAL float* p;   // real element 0
   uint64_t shift;      // 0..3
   uint64_t n;          // real elements
 };
@@ -47,7 +62,7 @@ constexpr uint32_t kPadBits = 0xFFFFFFFFu;
 __device__ inline f4 load4(const Row& r, uint64_t v, bool stream)
 {
   if (v >= r.shift && v + 4 <= r.shift + r.n) {
-    const float* a = r.p + (v - r.shift);
+    const GLOBAL float* a = r.p + (v - r.shift);
     return stream ? ld_stream4(a) : ld4(a);
   }
   const float pad = __uint_as_float(kPadBits);
@@ -71,7 +86,7 @@ __device__ inline uint32_t rank_key(float x) { return ((__float_as_uint(x) & kKe
 // (candidate lists); past the end reads the pad pattern.
 __device__ inline f4 load4_guarded(const float* row, uint64_t e, uint64_t rem, bool stream)
 {
-  return load4(Row{row, 0, rem}, e, stream);
+  return load4(Row{gptr(row), 0, rem}, e, stream);
 }
 
 
@@ -205,7 +220,7 @@ __global__ __launch_bounds__(kBlock) void k_hist_sample(Ctx c)
     f4 x;
     if (d.shift == 0 && e + 4 <= e1) x = ld4(d.grad + i);
     else
-      for (int q = 0; q < 4; ++q) x[q] = (e + q < e1) ? d.grad[i + q] : 0.f;
+      for (int q = 0; q < 4; ++q) x[q] = (e + q < e1) ? gptr(d.grad)[i + q] : 0.f;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       if (e + q >= e1) break;
@@ -317,7 +332,7 @@ __device__ inline uint32_t wave_prefix_of_block(uint32_t packed_lane, uint32_t* 
 // rank keys (key + 1, pads 0) and fmax drops the pads' NaN from the squares.
 // Counts are wave totals from ballots (scalar popcounts).
 template <bool kEdge>
-__device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32_t thi, double (&e2)[4], uint32_t& wc,
+__device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32_t thi, double (&e2)[2], uint32_t& wc,
                                   uint32_t& ws, uint32_t* s_ci, float* s_cv)
 {
   uint64_t b[4];
@@ -325,8 +340,8 @@ __device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const double xd = (double)x[q];
-    if (kEdge) e2[q] += __builtin_fmax(xd * xd, 0.0);
-    else e2[q] = __builtin_fma(xd, xd, e2[q]);
+    if (kEdge) e2[q & 1] += __builtin_fmax(xd * xd, 0.0);
+    else e2[q & 1] = __builtin_fma(xd, xd, e2[q & 1]);
     const uint32_t key = kEdge ? rank_key(x[q]) : key_of(x[q]);
     const uint32_t lo = kEdge ? tlo + 1u : tlo, hi = kEdge ? thi + 1u : thi;
     f[q] = key >= lo;
@@ -350,6 +365,40 @@ __device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32
                    __builtin_popcountll(b[3]));
 }
 
+// Writes a wave chunk's candidates (rank key >= tlo + 1) in index order at
+// out[pos0...], reloading its kTileRounds rounds (just read: mostly L2 hits),
+// one round ahead of the processing.
+__device__ inline void main_append(const Row& row, uint64_t v0, uint32_t i0, uint32_t tlo, uint64_t pos0,
+                                   GLOBAL uint32_t* out_idx, GLOBAL float* out_val)
+{
+  const uint32_t tlo1 = tlo + 1u;
+  uint64_t run = pos0;
+  f4 x = load4(row, v0, false);
+#pragma unroll 1
+  for (int r = 0; r < kTileRounds; ++r) {
+    const f4 xn = (r + 1 < kTileRounds) ? load4(row, v0 + (uint64_t)(r + 1) * 256, false) : x;
+    bool f[4];
+    uint64_t b[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      f[q] = rank_key(x[q]) >= tlo1;
+      b[q] = ballot(f[q]);
+    }
+    uint64_t pos = run + mbcnt(b[0]) + mbcnt(b[1]) + mbcnt(b[2]) + mbcnt(b[3]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (f[q]) {
+        out_idx[pos] = i0 + (uint32_t)r * 256 + q;
+        out_val[pos] = x[q];
+        ++pos;
+      }
+    }
+    run += __builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) + __builtin_popcountll(b[2]) +
+           __builtin_popcountll(b[3]);
+    x = xn;
+  }
+}
+
 // Each workgroup reads one tile of kTile gradient elements (workgroup b: device
 // b / tpd, tile b % tpd). Wave w owns elements [w*4096, (w+1)*4096) of the tile
 // and slot tile*kWaves + w of its device. A slot whose wave found more than
@@ -365,7 +414,7 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
   uint32_t tlo, thi;
   bracket_of(d, c.st[j], tlo, thi);
   const uint64_t vbase = (uint64_t)tile * kTile;      // virtual position of the tile
-  const Row row{d.grad, d.shift, c.n};
+  const Row row{gptr(d.grad), d.shift, c.n};
   // Interior tiles hold only real elements: plain aligned loads kept in
   // registers. The (at most two) edge tiles of a device reload per round.
   const bool full = vbase >= row.shift && vbase + kTile <= row.shift + row.n;
@@ -373,10 +422,10 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
   // real index of virtual position vbase + wv0 (may wrap for leading pads; never written)
   const uint32_t i_base = (uint32_t)(vbase + wv0 - row.shift);
 
-  double e2[4] = {0.0, 0.0, 0.0, 0.0};
+  double e2[2] = {0.0, 0.0};
   uint32_t wc = 0, ws = 0;
   if (full) {
-    const float* p = row.p + (vbase - row.shift) + wv0;
+    const GLOBAL float* p = row.p + (vbase - row.shift) + wv0;
     f4 v[kTileRounds];
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r) v[r] = ld_stream4(p + r * 256);
@@ -400,8 +449,21 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
       si[i] = s_ci[w][i];
       sv[i] = s_cv[w][i];
     }
+  } else {
+    // Dense-candidate chunk (rare): append all its candidates, in index order, to
+    // the device's overflow region; one atomic per such wave. A region that
+    // would overflow sends the device to the exact path.
+    uint32_t ob = 0;
+    if (l == 0) ob = atomicAdd(&c.st[j].ovf_used, wc);
+    ob = __builtin_amdgcn_readfirstlane(ob);
+    if (l == 0) c.slot_ovf[slot] = ob;
+    if ((uint64_t)ob + wc <= d.cap) {
+      main_append(row, vbase + wv0, i_base, tlo, ob, gptr(c.ovf_idx + d.cand_off), gptr(c.ovf_val + d.cand_off));
+    } else if (l == 0) {
+      atomicOr(&c.st[j].err, 32u);
+    }
   }
-  const double es = block_sum_f64((e2[0] + e2[1]) + (e2[2] + e2[3]), s_e);
+  const double es = block_sum_f64(e2[0] + e2[1], s_e);
   if (tid == 0) c.epart[(uint64_t)j * c.tpd + tile] = es;
 }
 
@@ -531,41 +593,7 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
 
 // Packs every slot into the device's candidate list at its offset (index
 // order is kept: slots are in index order and each slot is). A slot whose wave
-// overflowed is rebuilt by re-scanning its 4096-element chunk of the gradient.
-__device__ inline void gather_rescan(const Ctx& c, const DevDesc& d, uint32_t tlo, uint32_t s, uint64_t off,
-                                     uint32_t* cidx, float* cval)
-{
-  const uint32_t l = lane_id();
-  const Row row{d.grad, d.shift, c.n};
-  const uint64_t v0 = (uint64_t)(s / kWaves) * kTile + (uint64_t)(s % kWaves) * (kTileRounds * 256) + l * 4;
-  const uint32_t tlo1 = tlo + 1u;
-  uint64_t run = off;
-  for (int r = 0; r < kTileRounds; ++r) {
-    const uint64_t v = v0 + (uint64_t)r * 256;
-    const f4 x = load4(row, v, false);
-    bool f[4];
-    uint64_t b[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      f[q] = rank_key(x[q]) >= tlo1;
-      b[q] = ballot(f[q]);
-    }
-    uint64_t pos = run + mbcnt(b[0]) + mbcnt(b[1]) + mbcnt(b[2]) + mbcnt(b[3]);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (f[q]) {
-        if (pos < d.cap) {
-          cidx[pos] = (uint32_t)(v + q - row.shift);
-          cval[pos] = x[q];
-        }
-        ++pos;
-      }
-    }
-    run += __builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) + __builtin_popcountll(b[2]) +
-           __builtin_popcountll(b[3]);
-  }
-}
-
+// overflowed is copied from the device's overflow region.
 // Each wave takes kGatherSlots consecutive slots and first issues the loads of
 // all of them (metadata, then the first 64 entries of each), then stores.
 __global__ __launch_bounds__(kBlock) void k_gather(Ctx c)
@@ -618,11 +646,23 @@ __global__ __launch_bounds__(kBlock) void k_gather(Ctx c)
       }
     }
   }
-  // Overflowed slots (rare): rebuild from the gradient chunk.
+  // Overflowed slots (rare): copy from the overflow region.
 #pragma unroll 1
   for (int i = 0; i < kGatherSlots; ++i) {
     const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
-    if (cn > (uint32_t)kWaveCap) gather_rescan(c, d, st.t_lo, s0 + i, __builtin_amdgcn_readlane(m_off, i), cidx, cval);
+    if (cn <= (uint32_t)kWaveCap) continue;
+    const uint32_t off = __builtin_amdgcn_readlane(m_off, i);
+    const uint64_t slot = (uint64_t)j * c.nslot + s0 + i;
+    const uint64_t src = c.slot_ovf[slot];
+    if (src + cn > d.cap) continue;       // the device took the exact path
+    const uint32_t* oi = c.ovf_idx + d.cand_off + src;
+    const float* ov = c.ovf_val + d.cand_off + src;
+    for (uint32_t e = l; e < cn; e += 64) {
+      if ((uint64_t)off + e < d.cap) {
+        cidx[off + e] = oi[e];
+        cval[off + e] = ov[e];
+      }
+    }
   }
 }
 
@@ -643,7 +683,7 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
     __syncthreads();
     const SelView sv = view_of(sel);
     const uint64_t rem = (cnt - q0 < (uint64_t)kCBlk) ? cnt - q0 : (uint64_t)kCBlk;
-    const Row row{c.cand_val + c.desc[j].cand_off + q0, 0, rem};
+    const Row row{gptr(c.cand_val + c.desc[j].cand_off + q0), 0, rem};
 #pragma unroll 2
     for (int r = 0; r < kCBlkRounds; ++r) {
       const uint64_t e = (uint64_t)r * kRound + threadIdx.x * 4;
@@ -669,7 +709,7 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
     for (int i = threadIdx.x; i < kBins; i += kBlock) h[i] = 0u;
     __syncthreads();
     const SelView sv = view_of(sel);
-    const Row row{c.desc[j].grad, c.desc[j].shift, c.n};
+    const Row row{gptr(c.desc[j].grad), c.desc[j].shift, c.n};
     for (uint32_t blk = worker; blk < c.nfb; blk += G) {
       const uint64_t vbase = (uint64_t)blk * kCBlk;
 #pragma unroll 4
@@ -729,7 +769,7 @@ __global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c, uint32_t ncand_block
     uint64_t need;
     threshold_of(s, thr, need);
     const uint64_t rem = (s.cand - q0 < (uint64_t)kCBlk) ? s.cand - q0 : (uint64_t)kCBlk;
-    const uint64_t r = block_gt_eq<kCBlkRounds>(Row{c.cand_val + c.desc[j].cand_off + q0, 0, rem}, 0, thr, lds);
+    const uint64_t r = block_gt_eq<kCBlkRounds>(Row{gptr(c.cand_val + c.desc[j].cand_off + q0), 0, rem}, 0, thr, lds);
     if (threadIdx.x == 0) c.blk_cnt[(uint64_t)j * c.nbmax + b] = r;
     return;
   }
@@ -740,7 +780,7 @@ __global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c, uint32_t ncand_block
     uint32_t thr;
     uint64_t need;
     threshold_of(s, thr, need);
-    const Row row{c.desc[j].grad, c.desc[j].shift, c.n};
+    const Row row{gptr(c.desc[j].grad), c.desc[j].shift, c.n};
     for (uint32_t blk = worker; blk < c.nfb; blk += G) {
       const uint64_t r = block_gt_eq<kCBlkRounds>(row, (uint64_t)blk * kCBlk, thr, lds);
       if (threadIdx.x == 0) c.blk_cnt[(uint64_t)j * c.nbmax + blk] = r;
@@ -797,7 +837,7 @@ __device__ inline uint32_t write_count(const f4& x, uint32_t thr1)
 // One round of the ordered write: the wave's elements above the threshold, and
 // equal ones while fewer than `need` came before, at their kept positions.
 __device__ inline void write_round(const f4& x, uint64_t e, uint64_t vbase, const Row& row, const uint32_t* src_idx,
-                                   uint32_t thr1, uint64_t need, uint32_t k, uint32_t* out_idx, float* out_val,
+                                   uint32_t thr1, uint64_t need, uint32_t k, GLOBAL uint32_t* out_idx, GLOBAL float* out_val,
                                    uint64_t& run_g, uint64_t& run_e, double& e2)
 {
   bool fg[4], fe[4];
@@ -848,7 +888,7 @@ __device__ inline void write_round(const f4& x, uint64_t e, uint64_t vbase, cons
 // is the virtual position minus the row's shift.
 template <int R>
 __device__ inline double block_write(const Row& row, uint64_t vbase, const uint32_t* src_idx, uint32_t thr,
-                                     uint64_t need, uint64_t pre, uint32_t k, uint32_t* out_idx, float* out_val,
+                                     uint64_t need, uint64_t pre, uint32_t k, GLOBAL uint32_t* out_idx, GLOBAL float* out_val,
                                      uint32_t* lds)
 {
   const uint32_t w = threadIdx.x >> 6, l = lane_id();
@@ -857,7 +897,7 @@ __device__ inline double block_write(const Row& row, uint64_t vbase, const uint3
   f4 x[R];
   uint32_t cnt = 0;
   if (full) {
-    const float* p = row.p + (vbase - row.shift);
+    const GLOBAL float* p = row.p + (vbase - row.shift);
 #pragma unroll
     for (int r = 0; r < R; ++r) x[r] = ld4(p + elem_of<R>(w, r, l));
 #pragma unroll
@@ -899,9 +939,9 @@ __global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c, uint32_t ncand_block
     threshold_of(s, thr, need);
     const DevDesc d = c.desc[j];
     const uint64_t rem = (s.cand - q0 < (uint64_t)kCBlk) ? s.cand - q0 : (uint64_t)kCBlk;
-    const double e2 = block_write<kCBlkRounds>(Row{c.cand_val + d.cand_off + q0, 0, rem}, 0,
+    const double e2 = block_write<kCBlkRounds>(Row{gptr(c.cand_val + d.cand_off + q0), 0, rem}, 0,
                                                c.cand_idx + d.cand_off + q0, thr, need,
-                                               c.blk_pre[(uint64_t)j * c.nbmax + b], d.k, d.idx_out, d.val_out, lds);
+                                               c.blk_pre[(uint64_t)j * c.nbmax + b], d.k, gptr(d.idx_out), gptr(d.val_out), lds);
     const double es = block_sum_f64(e2, s_e);
     if (threadIdx.x == 0) c.blk_e[(uint64_t)j * c.nbmax + b] = es;
     return;
@@ -914,11 +954,11 @@ __global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c, uint32_t ncand_block
     uint64_t need;
     threshold_of(s, thr, need);
     const DevDesc d = c.desc[j];
-    const Row row{d.grad, d.shift, c.n};
+    const Row row{gptr(d.grad), d.shift, c.n};
     for (uint32_t blk = worker; blk < c.nfb; blk += G) {
       const double e2 = block_write<kCBlkRounds>(row, (uint64_t)blk * kCBlk, nullptr, thr, need,
-                                                 c.blk_pre[(uint64_t)j * c.nbmax + blk], d.k, d.idx_out,
-                                                 d.val_out, lds);
+                                                 c.blk_pre[(uint64_t)j * c.nbmax + blk], d.k, gptr(d.idx_out),
+                                                 gptr(d.val_out), lds);
       const double es = block_sum_f64(e2, s_e);
       if (threadIdx.x == 0) c.blk_e[(uint64_t)j * c.nbmax + blk] = es;
       __syncthreads();
