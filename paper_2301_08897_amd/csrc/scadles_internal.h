@@ -33,6 +33,7 @@ constexpr int kWaveCap = 512;          // main pass: candidates one wave chunk (
 constexpr int kScanChunk = 4096;       // slots per workgroup of the slot-offset scan
 constexpr int kMaxChunks = 256;        // >= ceil(nslot / kScanChunk) for n < 2^32
 constexpr int kGatherSlots = 8;        // slots per wave in the candidate gather
+constexpr int kOverflowBlocks = 32;    // workgroups per device re-scanning overflowed slots
 
 enum : uint32_t { kModeFast = 0, kModeExact = 1 };
 
@@ -76,7 +77,7 @@ struct DevState {
   uint64_t c_gt, need;    // keys above thr; keys equal to thr that are kept
   double e_all, e_kept;
   uint32_t sparse;        // 1: the device sends Top-k (adaptive rule), 0: dense
-  uint32_t ovf_used;      // entries taken in the device's overflow region
+  uint32_t ovf_n;         // entries in the device's ovf_list
 };
 
 // Kernel context: where everything lives in the workspace, plus call scalars.
@@ -90,9 +91,7 @@ struct Ctx {
   uint32_t* chunk_off;    // [K][kMaxChunks] offset of each scan chunk in the candidate list
   uint32_t* slot_idx;     // [K][nslot][kWaveCap] staged candidates per wave chunk
   float* slot_val;
-  uint32_t* slot_ovf;     // [K][nslot] start in the overflow region of a slot with > kWaveCap candidates
-  uint32_t* ovf_idx;      // per-device overflow regions (cap entries each, at cand_off)
-  float* ovf_val;
+  uint32_t* ovf_list;     // [K][nslot] slots whose wave found more than kWaveCap candidates
   double* epart;          // [K][tpd] sum of squares per main tile
   uint32_t* cand_idx;     // candidate regions
   float* cand_val;

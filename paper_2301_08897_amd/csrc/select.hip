@@ -43,8 +43,10 @@ __device__ inline GLOBAL T* gptr(T* p) { return (GLOBAL T*)p; }
 
 __device__ inline f4 ld_stream4(const GLOBAL float* p) { return __builtin_nontemporal_load((const GLOBAL f4*)p); }
 __device__ inline f4 ld4(const GLOBAL float* p) { return *(const GLOBAL f4*)p; }
+#if defined(__HIP_DEVICE_COMPILE__)
 __device__ inline f4 ld_stream4(const float* p) { return ld_stream4(gptr(p)); }
 __device__ inline f4 ld4(const float* p) { return ld4(gptr(p)); }
+#endif
 __device__ inline u4 ldu4(const uint32_t* p) { return *(const GLOBAL u4*)gptr(p); }
 
 // A device's gradient seen in a 16-byte-aligned "virtual" frame: real element i
@@ -365,40 +367,6 @@ __device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32
                    __builtin_popcountll(b[3]));
 }
 
-// Writes a wave chunk's candidates (rank key >= tlo + 1) in index order at
-// out[pos0...], reloading its kTileRounds rounds (just read: mostly L2 hits),
-// one round ahead of the processing.
-__device__ inline void main_append(const Row& row, uint64_t v0, uint32_t i0, uint32_t tlo, uint64_t pos0,
-                                   GLOBAL uint32_t* out_idx, GLOBAL float* out_val)
-{
-  const uint32_t tlo1 = tlo + 1u;
-  uint64_t run = pos0;
-  f4 x = load4(row, v0, false);
-#pragma unroll 1
-  for (int r = 0; r < kTileRounds; ++r) {
-    const f4 xn = (r + 1 < kTileRounds) ? load4(row, v0 + (uint64_t)(r + 1) * 256, false) : x;
-    bool f[4];
-    uint64_t b[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      f[q] = rank_key(x[q]) >= tlo1;
-      b[q] = ballot(f[q]);
-    }
-    uint64_t pos = run + mbcnt(b[0]) + mbcnt(b[1]) + mbcnt(b[2]) + mbcnt(b[3]);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (f[q]) {
-        out_idx[pos] = i0 + (uint32_t)r * 256 + q;
-        out_val[pos] = x[q];
-        ++pos;
-      }
-    }
-    run += __builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) + __builtin_popcountll(b[2]) +
-           __builtin_popcountll(b[3]);
-    x = xn;
-  }
-}
-
 // Each workgroup reads one tile of kTile gradient elements (workgroup b: device
 // b / tpd, tile b % tpd). Wave w owns elements [w*4096, (w+1)*4096) of the tile
 // and slot tile*kWaves + w of its device. A slot whose wave found more than
@@ -449,19 +417,11 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
       si[i] = s_ci[w][i];
       sv[i] = s_cv[w][i];
     }
-  } else {
-    // Dense-candidate chunk (rare): append all its candidates, in index order, to
-    // the device's overflow region; one atomic per such wave. A region that
-    // would overflow sends the device to the exact path.
-    uint32_t ob = 0;
-    if (l == 0) ob = atomicAdd(&c.st[j].ovf_used, wc);
-    ob = __builtin_amdgcn_readfirstlane(ob);
-    if (l == 0) c.slot_ovf[slot] = ob;
-    if ((uint64_t)ob + wc <= d.cap) {
-      main_append(row, vbase + wv0, i_base, tlo, ob, gptr(c.ovf_idx + d.cand_off), gptr(c.ovf_val + d.cand_off));
-    } else if (l == 0) {
-      atomicOr(&c.st[j].err, 32u);
-    }
+  } else if (l == 0) {
+    // Dense-candidate chunk (rare): record it; k_overflow re-scans it once the
+    // slot offsets are known. One atomic per such wave.
+    const uint32_t i = atomicAdd(&c.st[j].ovf_n, 1u);
+    c.ovf_list[(uint64_t)j * c.nslot + i] = tile * kWaves + w;
   }
   const double es = block_sum_f64(e2[0] + e2[1], s_e);
   if (tid == 0) c.epart[(uint64_t)j * c.tpd + tile] = es;
@@ -592,8 +552,38 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
 }
 
 // Packs every slot into the device's candidate list at its offset (index
-// order is kept: slots are in index order and each slot is). A slot whose wave
-// overflowed is copied from the device's overflow region.
+// order is kept: slots are in index order and each slot is). Slots whose wave
+// overflowed are written by k_overflow.
+// Copies entries [from, cn) of a slot (si, sv) to (di, dv) + off, eight loads
+// per lane in flight before the stores.
+__device__ inline void gather_copy(const uint32_t* si, const float* sv, uint32_t from, uint32_t cn, uint64_t off,
+                                   uint64_t cap, uint32_t* di, float* dv)
+{
+  const uint32_t l = lane_id();
+  for (uint32_t b0 = from; b0 < cn; b0 += 8 * 64) {
+    uint32_t ti[8];
+    float tv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t e = b0 + u * 64 + l;
+      ti[u] = 0u;
+      tv[u] = 0.f;
+      if (e < cn) {
+        ti[u] = si[e];
+        tv[u] = sv[e];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t e = b0 + u * 64 + l;
+      if (e < cn && off + e < cap) {
+        di[off + e] = ti[u];
+        dv[off + e] = tv[u];
+      }
+    }
+  }
+}
+
 // Each wave takes kGatherSlots consecutive slots and first issues the loads of
 // all of them (metadata, then the first 64 entries of each), then stores.
 __global__ __launch_bounds__(kBlock) void k_gather(Ctx c)
@@ -638,30 +628,60 @@ __global__ __launch_bounds__(kBlock) void k_gather(Ctx c)
       cidx[off + l] = ri[i];
       cval[off + l] = rv[i];
     }
-    const uint64_t slot = (uint64_t)j * c.nslot + s0 + i;
-    for (uint32_t e = 64 + l; e < cn; e += 64) {
-      if ((uint64_t)off + e < d.cap) {
-        cidx[off + e] = c.slot_idx[slot * kWaveCap + e];
-        cval[off + e] = c.slot_val[slot * kWaveCap + e];
-      }
+    if (cn > 64u) {
+      const uint64_t slot = (uint64_t)j * c.nslot + s0 + i;
+      gather_copy(c.slot_idx + slot * kWaveCap, c.slot_val + slot * kWaveCap, 64, cn, off, d.cap, cidx, cval);
     }
   }
-  // Overflowed slots (rare): copy from the overflow region.
-#pragma unroll 1
-  for (int i = 0; i < kGatherSlots; ++i) {
-    const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
-    if (cn <= (uint32_t)kWaveCap) continue;
-    const uint32_t off = __builtin_amdgcn_readlane(m_off, i);
-    const uint64_t slot = (uint64_t)j * c.nslot + s0 + i;
-    const uint64_t src = c.slot_ovf[slot];
-    if (src + cn > d.cap) continue;       // the device took the exact path
-    const uint32_t* oi = c.ovf_idx + d.cand_off + src;
-    const float* ov = c.ovf_val + d.cand_off + src;
-    for (uint32_t e = l; e < cn; e += 64) {
-      if ((uint64_t)off + e < d.cap) {
-        cidx[off + e] = oi[e];
-        cval[off + e] = ov[e];
+}
+
+// Slots whose wave overflowed: re-scan the 4096-element chunk (every round
+// loaded up front) and write its candidates, in index order, at the slot's
+// offset. Each wave takes list entries i = wave, wave + waves, ... of a device.
+__global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_dev)
+{
+  const uint32_t j = blockIdx.x / blocks_per_dev, b = blockIdx.x - j * blocks_per_dev;
+  const DevState& st = c.st[j];
+  if (st.fallback) return;
+  const uint32_t n_ovf = st.ovf_n;
+  const DevDesc d = c.desc[j];
+  const uint32_t l = lane_id();
+  const uint32_t tlo1 = st.t_lo + 1u;
+  const Row row{gptr(d.grad), d.shift, c.n};
+  GLOBAL uint32_t* cidx = gptr(c.cand_idx + d.cand_off);
+  GLOBAL float* cval = gptr(c.cand_val + d.cand_off);
+  const uint32_t waves = blocks_per_dev * kWaves;
+  for (uint32_t i = b * kWaves + (threadIdx.x >> 6); i < n_ovf; i += waves) {
+    const uint32_t s = c.ovf_list[(uint64_t)j * c.nslot + i];
+    const uint64_t off = (uint64_t)c.chunk_off[(uint64_t)j * kMaxChunks + s / kScanChunk] +
+                         c.slot_off[(uint64_t)j * c.nslot + s];
+    const uint64_t v0 = (uint64_t)(s / kWaves) * kTile + (uint64_t)(s % kWaves) * (kTileRounds * 256) + l * 4;
+    f4 x[kTileRounds];
+#pragma unroll
+    for (int r = 0; r < kTileRounds; ++r) x[r] = load4(row, v0 + (uint64_t)r * 256, false);
+    uint64_t run = off;
+#pragma unroll
+    for (int r = 0; r < kTileRounds; ++r) {
+      bool f[4];
+      uint64_t bm[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        f[q] = rank_key(x[r][q]) >= tlo1;
+        bm[q] = ballot(f[q]);
       }
+      uint64_t pos = run + mbcnt(bm[0]) + mbcnt(bm[1]) + mbcnt(bm[2]) + mbcnt(bm[3]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (f[q]) {
+          if (pos < d.cap) {
+            cidx[pos] = (uint32_t)(v0 + (uint64_t)r * 256 + q - row.shift);
+            cval[pos] = x[r][q];
+          }
+          ++pos;
+        }
+      }
+      run += __builtin_popcountll(bm[0]) + __builtin_popcountll(bm[1]) + __builtin_popcountll(bm[2]) +
+             __builtin_popcountll(bm[3]);
     }
   }
 }
@@ -1017,6 +1037,7 @@ hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, h
   if (p.any_fast) {
     constexpr uint32_t kPerBlock = kGatherSlots * kWaves;
     k_gather<<<c.K * ((c.nslot + kPerBlock - 1) / kPerBlock), kBlock, 0, s>>>(c);
+    k_overflow<<<c.K * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
   }
   const uint32_t g = p.ncand_blocks + p.full_workers;
   for (int pass = 0; pass < 3; ++pass) {

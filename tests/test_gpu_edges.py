@@ -113,6 +113,20 @@ def test_adversarial_sample(sc):
     topk_vs_oracle(sc, h, 0.001, "top values outside the sample, ties below")
 
 
+def test_dense_candidate_chunks(sc):
+    """A narrow high-variance band holds about half of its elements as
+    candidates, far more than a 4096-element chunk can stage (512): those
+    chunks take the overflow path of the single-read pass."""
+    log("edge dense candidate chunks")
+    rng = np.random.default_rng(11)
+    n = 2_000_003
+    g = (rng.standard_normal(n) * 1e-4).astype(np.float32)
+    g[300_001:500_001] = (rng.standard_normal(200_000) * 1.0).astype(np.float32)
+    topk_vs_oracle(sc, g, 0.05, "dense band, ratio 0.05")
+    g[1_000_000:1_004_096] = 7.0           # one fully dense chunk of ties
+    topk_vs_oracle(sc, g, 0.05, "dense band + tied chunk")
+
+
 def test_k1_and_kn_in_fused_step(sc):
     log("edge fused k=1/k=n")
     torch, dev = torch_dev()
