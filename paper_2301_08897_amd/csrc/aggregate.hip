@@ -3,11 +3,11 @@
 // g~[i] = sum_{j=0..K-1} r_j * v_j(i) over the devices' sparse (or dense)
 // contributions. One wave owns a tile of kATile positions at a time and
 // accumulates it in LDS in double, device by device in ascending order, one
-// fused multiply-add per term (r_j * v is exact in double, so every term is
-// rounded once, exactly as a serial double sum in device order rounds it). The
-// order needs no barrier: a wave's LDS operations execute in program order.
-// No atomics, so the result is bit-reproducible and independent of the launch
-// shape. Nothing here is a dense contraction, so there is no MFMA: the bound is
+// rounding per term (r_j * v is exact in double, so every term is rounded
+// once, exactly as a serial double sum in device order rounds it). The order
+// needs no barrier: a wave's LDS operations (plain and atomic) execute in
+// program order. No global atomics and no cross-wave races, so the result is
+// bit-reproducible and independent of the launch shape. Nothing here is a dense contraction, so there is no MFMA: the bound is
 // HBM traffic (sparse pairs in, dense aggregate out, parameters in and out).
 #include "scadles_internal.h"
 
@@ -55,6 +55,15 @@ __global__ __launch_bounds__(kBlock) void k_validate(AggArgs a, AggCtx c)
   if (cur >= c.n || (p > 0 && idx[p - 1] >= cur)) atomicOr(c.err, 1u);
 }
 
+// acc += p as one LDS read-modify-write. The LDS executes a wave's operations
+// in program order, so device j's additions to a position precede device
+// j+1's; p = r_j * v is exact in double, so acc + p rounds once, exactly like
+// fma(r_j, v, acc).
+__device__ inline void lds_add(double* a, double p)
+{
+  __hip_atomic_fetch_add(a, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
 // One wave per range of kARange tiles. Lane j < K keeps device j's survivor
 // pointer; for each tile the wave loads the next 64 entries of kABatch devices
 // at once (all loads in flight), then applies them device by device: the
@@ -79,6 +88,13 @@ __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
     const uint64_t base = (uint64_t)t * kATile;
     const uint64_t tend = base + kATile;
     const uint32_t len = (uint32_t)((c.n - base < (uint64_t)kATile) ? c.n - base : (uint64_t)kATile);
+    // Parameters of a full tile are fetched now, used after the accumulation.
+    f4 pp[kATile / 256];
+    const bool pre = c.params && len == (uint32_t)kATile;
+    if (pre) {
+#pragma unroll
+      for (int m = 0; m < kATile / 256; ++m) pp[m] = *reinterpret_cast<const f4*>(c.params + base + m * 256 + l * 4);
+    }
 #pragma unroll
     for (int m = 0; m < kATile / 64; ++m) acc[m * 64 + l] = 0.0;
 
@@ -113,7 +129,7 @@ __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
 #pragma unroll 4
           for (int m = 0; m < kATile / 64; ++m) {
             const uint32_t e = m * 64 + l;
-            if (e < len) acc[e] = __builtin_fma(w, (double)g[e], acc[e]);
+            if (e < len) lds_add(&acc[e], w * (double)g[e]);
           }
           continue;
         }
@@ -123,7 +139,7 @@ __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
         while (true) {
           if (take && (uint64_t)i >= base) {
             const uint32_t pos = (uint32_t)(i - base);
-            if (pos < len) acc[pos] = __builtin_fma(w, (double)v, acc[pos]);
+            if (pos < len) lds_add(&acc[pos], w * (double)v);
           }
           const uint32_t cnt = (uint32_t)__builtin_popcountll(ballot(take));
           if (l == j) ptr += cnt;
@@ -140,6 +156,22 @@ __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
     }
 
     // Round once to float; optionally the SGD update of Eqn 4c on the float aggregate.
+    if (pre) {
+      const double nlr = -(double)c.lr;
+#pragma unroll
+      for (int m = 0; m < kATile / 256; ++m) {
+        const uint32_t e = m * 256 + l * 4;
+        const f4 g = {(float)acc[e], (float)acc[e + 1], (float)acc[e + 2], (float)acc[e + 3]};
+        *reinterpret_cast<f4*>(c.out + base + e) = g;
+        f4 p = pp[m];
+        p.x = (float)__builtin_fma(nlr, (double)g.x, (double)p.x);
+        p.y = (float)__builtin_fma(nlr, (double)g.y, (double)p.y);
+        p.z = (float)__builtin_fma(nlr, (double)g.z, (double)p.z);
+        p.w = (float)__builtin_fma(nlr, (double)g.w, (double)p.w);
+        *reinterpret_cast<f4*>(c.params + base + e) = p;
+      }
+      continue;
+    }
     for (uint32_t e = l * 4; e < len; e += 256) {
       if (e + 4 <= len) {
         const f4 g = {(float)acc[e], (float)acc[e + 1], (float)acc[e + 2], (float)acc[e + 3]};

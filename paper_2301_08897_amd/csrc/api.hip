@@ -166,7 +166,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
     L.o_olist = take(sizeof(uint32_t) * (size_t)K * L.nslot);
     L.o_sidx = take(sizeof(uint32_t) * nslots * kWaveCap);
     L.o_sval = take(sizeof(float) * nslots * kWaveCap);
-    L.o_epart = take(sizeof(double) * (size_t)K * L.tpd);
+    L.o_epart = take(sizeof(double) * (size_t)K * L.nslot);
     L.o_cidx = take(sizeof(uint32_t) * sum_cap);
     L.o_cval = take(sizeof(float) * sum_cap);
     L.o_bcnt = take(sizeof(uint64_t) * (size_t)K * L.nbmax);

@@ -92,7 +92,7 @@ struct Ctx {
   uint32_t* slot_idx;     // [K][nslot][kWaveCap] staged candidates per wave chunk
   float* slot_val;
   uint32_t* ovf_list;     // [K][nslot] slots whose wave found more than kWaveCap candidates
-  double* epart;          // [K][tpd] sum of squares per main tile
+  double* epart;          // [K][nslot] sum of squares per main-pass wave chunk
   uint32_t* cand_idx;     // candidate regions
   float* cand_val;
   uint64_t* blk_cnt;      // [K][nbmax] packed (gt | eq << 32) per compaction block
@@ -123,6 +123,11 @@ struct PrepArgs {
   uint32_t mode[kMaxK];
   uint32_t r_lo[kMaxK];
   uint32_t r_hi[kMaxK];
+};
+
+// Gradient pointers of the main pass, passed as kernel arguments.
+struct GradArgs {
+  const float* grad[kMaxK];
 };
 
 // Aggregation context.

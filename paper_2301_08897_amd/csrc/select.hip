@@ -369,20 +369,20 @@ __device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32
 
 // Each workgroup reads one tile of kTile gradient elements (workgroup b: device
 // b / tpd, tile b % tpd). Wave w owns elements [w*4096, (w+1)*4096) of the tile
-// and slot tile*kWaves + w of its device. A slot whose wave found more than
-// kWaveCap candidates stays empty; the gather re-scans that chunk instead.
-__global__ __launch_bounds__(kBlock) void k_main(Ctx c)
+// and slot tile*kWaves + w of its device. A wave that finds more than kWaveCap
+// candidates leaves its slot empty and records the slot for k_overflow. The
+// gradient pointers come as kernel arguments so that the tile's loads issue
+// before anything is read from the workspace; waves never wait on each other.
+__global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
 {
-  __shared__ double s_e[4];
   __shared__ uint32_t s_ci[kWaves][kWaveCap];
   __shared__ float s_cv[kWaves][kWaveCap];
-  const uint32_t tid = threadIdx.x, l = lane_id(), w = tid >> 6;
+  const uint32_t l = lane_id(), w = threadIdx.x >> 6;
   const uint32_t j = blockIdx.x / c.tpd, tile = blockIdx.x - j * c.tpd;
-  const DevDesc d = c.desc[j];
-  uint32_t tlo, thi;
-  bracket_of(d, c.st[j], tlo, thi);
+  const float* grad = ga.grad[j];
+  const uint64_t shift = (reinterpret_cast<uintptr_t>(grad) >> 2) & 3u;
   const uint64_t vbase = (uint64_t)tile * kTile;      // virtual position of the tile
-  const Row row{gptr(d.grad), d.shift, c.n};
+  const Row row{gptr(grad), shift, c.n};
   // Interior tiles hold only real elements: plain aligned loads kept in
   // registers. The (at most two) edge tiles of a device reload per round.
   const bool full = vbase >= row.shift && vbase + kTile <= row.shift + row.n;
@@ -397,19 +397,27 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
     f4 v[kTileRounds];
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r) v[r] = ld_stream4(p + r * 256);
+    uint32_t tlo, thi;
+    bracket_of(c.desc[j], c.st[j], tlo, thi);
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r) {
       main_stage<false>(v[r], i_base + r * 256, tlo, thi, e2, wc, ws, s_ci[w], s_cv[w]);
       __builtin_amdgcn_sched_barrier(0);    // keep rounds apart: bounds the live ballot masks
     }
   } else {
+    uint32_t tlo, thi;
+    bracket_of(c.desc[j], c.st[j], tlo, thi);
     for (int r = 0; r < kTileRounds; ++r)
       main_stage<true>(load4(row, vbase + wv0 + r * 256, false), i_base + r * 256, tlo, thi, e2, wc, ws, s_ci[w],
                        s_cv[w]);
   }
   // The wave's slot (its own LDS region, written by itself: no barrier needed).
   const uint64_t slot = (uint64_t)j * c.nslot + (uint64_t)tile * kWaves + w;
-  if (l == 0) c.slot_cnt[slot] = wc | (ws << 16);
+  const double es = wave_sum_f64(e2[0] + e2[1]);
+  if (l == 0) {
+    c.slot_cnt[slot] = wc | (ws << 16);
+    c.epart[slot] = es;
+  }
   if (wc <= (uint32_t)kWaveCap) {
     uint32_t* si = c.slot_idx + slot * kWaveCap;
     float* sv = c.slot_val + slot * kWaveCap;
@@ -423,8 +431,6 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c)
     const uint32_t i = atomicAdd(&c.st[j].ovf_n, 1u);
     c.ovf_list[(uint64_t)j * c.nslot + i] = tile * kWaves + w;
   }
-  const double es = block_sum_f64(e2[0] + e2[1], s_e);
-  if (tid == 0) c.epart[(uint64_t)j * c.tpd + tile] = es;
 }
 
 // ---- after the main pass: energies, slot offsets, candidate totals, path decision ----------
@@ -491,7 +497,7 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
   __shared__ uint64_t s_w[4];
   const uint32_t j = blockIdx.x, tid = threadIdx.x;
   double acc = 0.0;
-  for (uint32_t t = tid; t < c.tpd; t += kBlock) acc += c.epart[(uint64_t)j * c.tpd + t];
+  for (uint32_t t = tid; t < c.nslot; t += kBlock) acc += c.epart[(uint64_t)j * c.nslot + t];
   const double e_all = block_sum_f64(acc, s_e);
   const DevDesc d = c.desc[j];
   uint64_t cand = 0, sure = 0;
@@ -1030,7 +1036,9 @@ hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, h
     }
   }
   if (ev) (void)hipEventRecord(ev[1], s);
-  k_main<<<c.K * c.tpd, kBlock, 0, s>>>(c);
+  GradArgs ga;
+  for (uint32_t j = 0; j < c.K; ++j) ga.grad[j] = a.grad[j];
+  k_main<<<c.K * c.tpd, kBlock, 0, s>>>(c, ga);
   if (ev) (void)hipEventRecord(ev[2], s);
   if (p.any_fast) k_slot_scan<<<c.K * ((c.nslot + kScanChunk - 1) / kScanChunk), kBlock, 0, s>>>(c);
   k_post<<<c.K, kBlock, 0, s>>>(c);
