@@ -100,6 +100,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=16)
     ap.add_argument("--stages", action="store_true", help="also print per-stage milliseconds")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="first run one 1 GiB device-to-device copy (a plain copy kernel of known size "
+                         "for scaling HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -124,6 +127,16 @@ def main():
     params = torch.from_numpy(workloads.params0(s)).to(dev)
     torch.cuda.synchronize()
     log(f"inputs resident in HBM ({4 * s.K * s.n / 1e9:.1f} GB) after {time.perf_counter() - t0:.1f} s")
+
+    if args.calibrate:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1.0)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
 
     weights, lrs = [], []
     for it in range(s.iterations):

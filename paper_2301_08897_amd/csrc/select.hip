@@ -489,6 +489,22 @@ __global__ __launch_bounds__(kBlock) void k_slot_scan(Ctx c)
   if (tid == kBlock - 1) c.chunk_tot[(uint64_t)j * kMaxChunks + ch] = run + sum;
 }
 
+// Sum of squares of every kScanChunk wave chunks of a device (fixed order), for
+// any device mode.
+__global__ __launch_bounds__(kBlock) void k_energy_chunks(Ctx c)
+{
+  __shared__ double s_e[4];
+  const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
+  const uint32_t j = blockIdx.x / nchunk, ch = blockIdx.x - j * nchunk;
+  const uint32_t s0 = ch * kScanChunk + threadIdx.x * 16;
+  const double* ep = c.epart + (uint64_t)j * c.nslot;
+  double a = 0.0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) a += (s0 + i < c.nslot) ? ep[s0 + i] : 0.0;
+  const double t = block_sum_f64(a, s_e);
+  if (threadIdx.x == 0) c.chunk_e[(uint64_t)j * kMaxChunks + ch] = t;
+}
+
 // Slot offsets, level 2, and the per-device decision: chunk prefixes, candidate
 // totals, energies, then the exact path (fallback) or the candidate selection.
 __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
@@ -496,9 +512,8 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
   __shared__ double s_e[4];
   __shared__ uint64_t s_w[4];
   const uint32_t j = blockIdx.x, tid = threadIdx.x;
-  double acc = 0.0;
-  for (uint32_t t = tid; t < c.nslot; t += kBlock) acc += c.epart[(uint64_t)j * c.nslot + t];
-  const double e_all = block_sum_f64(acc, s_e);
+  const uint32_t nch = (c.nslot + kScanChunk - 1) / kScanChunk;    // <= kMaxChunks = kBlock
+  const double e_all = block_sum_f64(tid < nch ? c.chunk_e[(uint64_t)j * kMaxChunks + tid] : 0.0, s_e);
   const DevDesc d = c.desc[j];
   uint64_t cand = 0, sure = 0;
   if (d.mode == kModeFast) {
@@ -1040,7 +1055,9 @@ hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, h
   for (uint32_t j = 0; j < c.K; ++j) ga.grad[j] = a.grad[j];
   k_main<<<c.K * c.tpd, kBlock, 0, s>>>(c, ga);
   if (ev) (void)hipEventRecord(ev[2], s);
-  if (p.any_fast) k_slot_scan<<<c.K * ((c.nslot + kScanChunk - 1) / kScanChunk), kBlock, 0, s>>>(c);
+  const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
+  k_energy_chunks<<<c.K * nchunk, kBlock, 0, s>>>(c);
+  if (p.any_fast) k_slot_scan<<<c.K * nchunk, kBlock, 0, s>>>(c);
   k_post<<<c.K, kBlock, 0, s>>>(c);
   if (p.any_fast) {
     constexpr uint32_t kPerBlock = kGatherSlots * kWaves;
