@@ -68,7 +68,7 @@ struct Layout {
   uint64_t n = 0;
   uint32_t k[kMaxK], cap[kMaxK], mode[kMaxK], r_lo[kMaxK], r_hi[kMaxK];
   uint32_t any_fast = 0;
-  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_ctot, o_coff, o_ce, o_olist, o_sidx, o_sval, o_epart, o_cidx, o_cval, o_bcnt, o_bpre, o_be, o_aoff,
+  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_ctot, o_coff, o_ce, o_olist, o_slot, o_epart, o_cidx, o_cval, o_bcnt, o_bpre, o_be, o_aoff,
       o_aerr;
   size_t total = 0;
 };
@@ -165,8 +165,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
     L.o_coff = take(sizeof(uint32_t) * (size_t)K * kMaxChunks);
     L.o_ce = take(sizeof(double) * (size_t)K * kMaxChunks);
     L.o_olist = take(sizeof(uint32_t) * (size_t)K * L.nslot);
-    L.o_sidx = take(sizeof(uint32_t) * nslots * kWaveCap);
-    L.o_sval = take(sizeof(float) * nslots * kWaveCap);
+    L.o_slot = take(sizeof(uint64_t) * nslots * kWaveCap);
     L.o_epart = take(sizeof(double) * (size_t)K * L.nslot);
     L.o_cidx = take(sizeof(uint32_t) * sum_cap);
     L.o_cval = take(sizeof(float) * sum_cap);
@@ -194,8 +193,7 @@ Ctx make_ctx(const Layout& L, void* ws)
   c.chunk_off = reinterpret_cast<uint32_t*>(b + L.o_coff);
   c.chunk_e = reinterpret_cast<double*>(b + L.o_ce);
   c.ovf_list = reinterpret_cast<uint32_t*>(b + L.o_olist);
-  c.slot_idx = reinterpret_cast<uint32_t*>(b + L.o_sidx);
-  c.slot_val = reinterpret_cast<float*>(b + L.o_sval);
+  c.slot = reinterpret_cast<uint64_t*>(b + L.o_slot);
   c.epart = reinterpret_cast<double*>(b + L.o_epart);
   c.cand_idx = reinterpret_cast<uint32_t*>(b + L.o_cidx);
   c.cand_val = reinterpret_cast<float*>(b + L.o_cval);

@@ -90,8 +90,7 @@ struct Ctx {
   uint64_t* chunk_tot;    // [K][kMaxChunks] candidate | sure << 32 totals of each scan chunk
   uint32_t* chunk_off;    // [K][kMaxChunks] offset of each scan chunk in the candidate list
   double* chunk_e;        // [K][kMaxChunks] sum of squares of each scan chunk
-  uint32_t* slot_idx;     // [K][nslot][kWaveCap] staged candidates per wave chunk
-  float* slot_val;
+  uint64_t* slot;         // [K][nslot][kWaveCap] staged candidates per wave chunk: index | value bits << 32
   uint32_t* ovf_list;     // [K][nslot] slots whose wave found more than kWaveCap candidates
   double* epart;          // [K][nslot] sum of squares per main-pass wave chunk
   uint32_t* cand_idx;     // candidate regions

@@ -333,9 +333,12 @@ __device__ inline uint32_t wave_prefix_of_block(uint32_t packed_lane, uint32_t* 
 // kEdge: the round may hold pads (pattern 0xFFFFFFFF), so keys are compared as
 // rank keys (key + 1, pads 0) and fmax drops the pads' NaN from the squares.
 // Counts are wave totals from ballots (scalar popcounts).
+// A staged candidate: its index in the low word, its value's bits in the high word.
+__device__ inline uint64_t pack_cand(uint32_t i, float v) { return (uint64_t)i | ((uint64_t)__float_as_uint(v) << 32); }
+
 template <bool kEdge>
 __device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32_t thi, double (&e2)[2], uint32_t& wc,
-                                  uint32_t& ws, uint32_t* s_ci, float* s_cv)
+                                  uint32_t& ws, uint64_t* s_c)
 {
   uint64_t b[4];
   bool f[4];
@@ -356,10 +359,7 @@ __device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     if (f[q]) {
-      if (pos < (uint32_t)kWaveCap) {
-        s_ci[pos] = i0 + q;
-        s_cv[pos] = x[q];
-      }
+      if (pos < (uint32_t)kWaveCap) s_c[pos] = pack_cand(i0 + q, x[q]);
       ++pos;
     }
   }
@@ -375,8 +375,7 @@ __device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32
 // before anything is read from the workspace; waves never wait on each other.
 __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
 {
-  __shared__ uint32_t s_ci[kWaves][kWaveCap];
-  __shared__ float s_cv[kWaves][kWaveCap];
+  __shared__ uint64_t s_c[kWaves][kWaveCap];
   const uint32_t l = lane_id(), w = threadIdx.x >> 6;
   const uint32_t j = blockIdx.x / c.tpd, tile = blockIdx.x - j * c.tpd;
   const float* grad = ga.grad[j];
@@ -401,15 +400,14 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
     bracket_of(c.desc[j], c.st[j], tlo, thi);
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r) {
-      main_stage<false>(v[r], i_base + r * 256, tlo, thi, e2, wc, ws, s_ci[w], s_cv[w]);
+      main_stage<false>(v[r], i_base + r * 256, tlo, thi, e2, wc, ws, s_c[w]);
       __builtin_amdgcn_sched_barrier(0);    // keep rounds apart: bounds the live ballot masks
     }
   } else {
     uint32_t tlo, thi;
     bracket_of(c.desc[j], c.st[j], tlo, thi);
     for (int r = 0; r < kTileRounds; ++r)
-      main_stage<true>(load4(row, vbase + wv0 + r * 256, false), i_base + r * 256, tlo, thi, e2, wc, ws, s_ci[w],
-                       s_cv[w]);
+      main_stage<true>(load4(row, vbase + wv0 + r * 256, false), i_base + r * 256, tlo, thi, e2, wc, ws, s_c[w]);
   }
   // The wave's slot (its own LDS region, written by itself: no barrier needed).
   const uint64_t slot = (uint64_t)j * c.nslot + (uint64_t)tile * kWaves + w;
@@ -419,12 +417,9 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
     c.epart[slot] = es;
   }
   if (wc <= (uint32_t)kWaveCap) {
-    uint32_t* si = c.slot_idx + slot * kWaveCap;
-    float* sv = c.slot_val + slot * kWaveCap;
-    for (uint32_t i = l; i < wc; i += 64) {
-      si[i] = s_ci[w][i];
-      sv[i] = s_cv[w][i];
-    }
+    // Nontemporal: the slots are read once, by k_gather, after the whole pass.
+    GLOBAL uint64_t* sp = gptr(c.slot + slot * kWaveCap);
+    for (uint32_t i = l; i < wc; i += 64) __builtin_nontemporal_store(s_c[w][i], sp + i);
   } else if (l == 0) {
     // Dense-candidate chunk (rare): record it; k_overflow re-scans it once the
     // slot offsets are known. One atomic per such wave.
@@ -575,31 +570,25 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
 // Packs every slot into the device's candidate list at its offset (index
 // order is kept: slots are in index order and each slot is). Slots whose wave
 // overflowed are written by k_overflow.
-// Copies entries [from, cn) of a slot (si, sv) to (di, dv) + off, eight loads
-// per lane in flight before the stores.
-__device__ inline void gather_copy(const uint32_t* si, const float* sv, uint32_t from, uint32_t cn, uint64_t off,
-                                   uint64_t cap, uint32_t* di, float* dv)
+// Copies entries [from, cn) of a slot to (di, dv) + off, eight loads per lane
+// in flight before the stores.
+__device__ inline void gather_copy(const GLOBAL uint64_t* sp, uint32_t from, uint32_t cn, uint64_t off, uint64_t cap,
+                                   GLOBAL uint32_t* di, GLOBAL float* dv)
 {
   const uint32_t l = lane_id();
   for (uint32_t b0 = from; b0 < cn; b0 += 8 * 64) {
-    uint32_t ti[8];
-    float tv[8];
+    uint64_t t[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const uint32_t e = b0 + u * 64 + l;
-      ti[u] = 0u;
-      tv[u] = 0.f;
-      if (e < cn) {
-        ti[u] = si[e];
-        tv[u] = sv[e];
-      }
+      t[u] = e < cn ? sp[e] : 0ull;
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const uint32_t e = b0 + u * 64 + l;
       if (e < cn && off + e < cap) {
-        di[off + e] = ti[u];
-        dv[off + e] = tv[u];
+        di[off + e] = (uint32_t)t[u];
+        dv[off + e] = __uint_as_float((uint32_t)(t[u] >> 32));
       }
     }
   }
@@ -618,8 +607,9 @@ __global__ __launch_bounds__(kBlock) void k_gather(Ctx c)
   const uint32_t l = lane_id(), w = threadIdx.x >> 6;
   const uint32_t s0 = g * kPerBlock + w * kGatherSlots;
   if (s0 >= c.nslot) return;
-  uint32_t* cidx = c.cand_idx + d.cand_off;
-  float* cval = c.cand_val + d.cand_off;
+  GLOBAL uint32_t* cidx = gptr(c.cand_idx + d.cand_off);
+  GLOBAL float* cval = gptr(c.cand_val + d.cand_off);
+  const GLOBAL uint64_t* slots = gptr(c.slot) + (uint64_t)j * c.nslot * kWaveCap;
   // lane i < kGatherSlots: metadata of slot s0 + i
   uint32_t m_cnt = 0, m_off = 0;
   if (l < (uint32_t)kGatherSlots && s0 + l < c.nslot) {
@@ -627,18 +617,11 @@ __global__ __launch_bounds__(kBlock) void k_gather(Ctx c)
     m_cnt = c.slot_cnt[slot] & 0xFFFFu;
     m_off = c.chunk_off[(uint64_t)j * kMaxChunks + (s0 + l) / kScanChunk] + c.slot_off[slot];
   }
-  uint32_t ri[kGatherSlots];
-  float rv[kGatherSlots];
+  uint64_t r[kGatherSlots];
 #pragma unroll
   for (int i = 0; i < kGatherSlots; ++i) {
     const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
-    ri[i] = 0u;
-    rv[i] = 0.f;
-    if (cn <= (uint32_t)kWaveCap && l < cn) {
-      const uint64_t slot = (uint64_t)j * c.nslot + s0 + i;
-      ri[i] = c.slot_idx[slot * kWaveCap + l];
-      rv[i] = c.slot_val[slot * kWaveCap + l];
-    }
+    r[i] = (cn <= (uint32_t)kWaveCap && l < cn) ? slots[(uint64_t)(s0 + i) * kWaveCap + l] : 0ull;
   }
 #pragma unroll
   for (int i = 0; i < kGatherSlots; ++i) {
@@ -646,13 +629,10 @@ __global__ __launch_bounds__(kBlock) void k_gather(Ctx c)
     const uint32_t off = __builtin_amdgcn_readlane(m_off, i);
     if (cn == 0u || cn > (uint32_t)kWaveCap) continue;
     if (l < cn && (uint64_t)off + l < d.cap) {
-      cidx[off + l] = ri[i];
-      cval[off + l] = rv[i];
+      cidx[off + l] = (uint32_t)r[i];
+      cval[off + l] = __uint_as_float((uint32_t)(r[i] >> 32));
     }
-    if (cn > 64u) {
-      const uint64_t slot = (uint64_t)j * c.nslot + s0 + i;
-      gather_copy(c.slot_idx + slot * kWaveCap, c.slot_val + slot * kWaveCap, 64, cn, off, d.cap, cidx, cval);
-    }
+    if (cn > 64u) gather_copy(slots + (uint64_t)(s0 + i) * kWaveCap, 64, cn, off, d.cap, cidx, cval);
   }
 }
 
