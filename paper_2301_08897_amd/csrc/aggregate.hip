@@ -1,14 +1,16 @@
 // aggregate.hip -- weighted aggregation (Eqn 4b) and SGD update (Eqn 4c) for gfx950.
 //
 // g~[i] = sum_{j=0..K-1} r_j * v_j(i) over the devices' sparse (or dense)
-// contributions. One wave owns a tile of kATile positions at a time and
-// accumulates it in LDS in double, device by device in ascending order, one
-// rounding per term (r_j * v is exact in double, so every term is rounded
-// once, exactly as a serial double sum in device order rounds it). The order
-// needs no barrier: a wave's LDS operations (plain and atomic) execute in
-// program order. No global atomics and no cross-wave races, so the result is
-// bit-reproducible and independent of the launch shape. Nothing here is a dense contraction, so there is no MFMA: the bound is
-// HBM traffic (sparse pairs in, dense aggregate out, parameters in and out).
+// contributions. One wave owns a range of kARange positions and accumulates it
+// in LDS in double, device by device in ascending order, one rounding per term
+// (r_j * v is exact in double, so every term is rounded once, exactly as a
+// serial double sum in device order rounds it). The order needs no barrier: a
+// wave's LDS operations (plain and atomic) execute in program order, and one
+// device never has two entries at one position. No global atomics and no
+// cross-wave races, so the result is bit-reproducible and independent of the
+// launch shape. Nothing here is a dense contraction, so there is no MFMA: the
+// bound is HBM traffic (sparse pairs in, dense aggregate out, parameters in
+// and out).
 #include "scadles_internal.h"
 
 namespace scadles {
@@ -21,26 +23,56 @@ __device__ inline bool dense_device(const AggArgs& a, const AggCtx& c, uint32_t 
   return a.idx[j] == nullptr;
 }
 
-// start[j][r] = first position p of device j's ascending idx with
-// idx[p] >= r * kARange * kATile (binary search; any input gives a value in [0, k_j]).
-__global__ __launch_bounds__(kBlock) void k_starts(AggArgs a, AggCtx c)
+__global__ __launch_bounds__(kBlock) void k_fill_u32(uint32_t* p, uint64_t count, uint32_t v)
 {
-  const uint32_t per = c.nrange + 1;
-  const uint64_t gid = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (gid >= (uint64_t)c.K * per) return;
-  const uint32_t j = (uint32_t)(gid / per), r = (uint32_t)(gid - (uint64_t)j * per);
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < count; i += stride) p[i] = v;
+}
+
+// Range markers: the first entry of device j in range r (positions
+// [r * kARange, (r + 1) * kARange)) stores its position in rbeg[j][r], the last
+// one stores its position + 1 in rend[j][r]; ranges without entries keep
+// kNoEntry in rbeg. For ascending idx a range's entries are [rbeg, rend).
+// Entries with idx >= n are skipped (only validation mode reports them).
+// Each wave takes 1024 consecutive entries (16 per lane, all loads in flight);
+// an entry's neighbours come from the adjacent lanes.
+__global__ __launch_bounds__(kBlock) void k_mark(AggArgs a, AggCtx c)
+{
+  constexpr int kPer = 16;
+  const uint32_t j = blockIdx.y;
   const uint32_t* idx = a.idx[j];
-  uint32_t lo = 0;
-  if (idx) {
-    const uint64_t target = (uint64_t)r * kARange * kATile;
-    uint32_t hi = a.k[j];
-    while (lo < hi) {
-      const uint32_t mid = lo + (hi - lo) / 2;
-      if ((uint64_t)idx[mid] < target) lo = mid + 1;
-      else hi = mid;
+  if (!idx || dense_device(a, c, j)) return;
+  const uint64_t k = a.k[j];
+  uint32_t* rb = c.rbeg + (uint64_t)j * c.nrange;
+  uint32_t* re = c.rend + (uint64_t)j * c.nrange;
+  const uint32_t l = lane_id();
+  const uint64_t nwave = (uint64_t)gridDim.x * kWaves;
+  for (uint64_t b0 = ((uint64_t)blockIdx.x * kWaves + (threadIdx.x >> 6)) * (64 * kPer); b0 < k;
+       b0 += nwave * (64 * kPer)) {
+    uint32_t x[kPer];
+#pragma unroll
+    for (int m = 0; m < kPer; ++m) {
+      const uint64_t e = b0 + m * 64 + l;
+      x[m] = e < k ? idx[e] : 0u;
+    }
+    const uint32_t before = b0 > 0 ? idx[b0 - 1] : 0u;
+    const uint32_t after = b0 + 64 * kPer < k ? idx[b0 + 64 * kPer] : 0u;
+#pragma unroll
+    for (int m = 0; m < kPer; ++m) {
+      const uint64_t e = b0 + m * 64 + l;
+      uint32_t prev = __shfl_up(x[m], 1, 64);
+      uint32_t next = __shfl_down(x[m], 1, 64);
+      const uint32_t last_prev = m > 0 ? __builtin_amdgcn_readlane(x[m > 0 ? m - 1 : 0], 63) : before;
+      const uint32_t first_next = m + 1 < kPer ? __builtin_amdgcn_readlane(x[m + 1 < kPer ? m + 1 : 0], 0) : after;
+      if (l == 0) prev = last_prev;
+      if (l == 63) next = first_next;
+      const uint32_t i = x[m];
+      if (e >= k || (uint64_t)i >= c.n) continue;
+      const uint32_t r = i / (uint32_t)kARange;
+      if (e == 0 || prev / (uint32_t)kARange != r) rb[r] = (uint32_t)e;
+      if (e + 1 == k || next / (uint32_t)kARange != r) re[r] = (uint32_t)(e + 1);
     }
   }
-  c.start[gid] = lo;
 }
 
 // Flags a set whose idx is not strictly ascending or reaches n (validation mode).
@@ -64,134 +96,167 @@ __device__ inline void lds_add(double* a, double p)
   __hip_atomic_fetch_add(a, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-// One wave per range of kARange tiles. Lane j < K keeps device j's survivor
-// pointer; for each tile the wave loads the next 64 entries of kABatch devices
-// at once (all loads in flight), then applies them device by device: the
-// entries below the tile's end are consumed (for ascending idx they are a
-// prefix of the lanes), the pointer advances by their count, and a device with
-// 64 or more entries in the tile loops on. Dense devices add the whole tile.
+// Adds one sparse entry (position i, value v) of weight w to the range at base.
+__device__ inline void add_entry(double* acc, uint32_t i, float v, uint64_t base, double w)
+{
+  const uint64_t pos = (uint64_t)i - base;     // wraps for i < base: rejected below
+  if (pos < (uint64_t)kARange) lds_add(&acc[pos], w * (double)v);
+}
+
+// First 64 entries of devices jb .. jb + kABatch - 1 in the range.
+__device__ inline void load_batch(const AggArgs& a, uint32_t jb, uint32_t K, uint32_t eb, uint32_t em,
+                                  uint32_t (&ri)[kABatch], float (&rv)[kABatch])
+{
+  const uint32_t l = lane_id();
+#pragma unroll
+  for (int jj = 0; jj < kABatch; ++jj) {
+    const uint32_t j = jb + jj;
+    ri[jj] = 0u;
+    rv[jj] = 0.f;
+    if (j < K) {
+      const uint32_t b = __builtin_amdgcn_readlane(eb, j);
+      const uint32_t m = __builtin_amdgcn_readlane(em, j);
+      if (l < m) {
+        ri[jj] = a.idx[j][b + l];
+        rv[jj] = a.val[j][b + l];
+      }
+    }
+  }
+}
+
+// Adds devices jb .. jb + kABatch - 1 in ascending order: the loaded first 64
+// entries, then any further entries in rounds of four 64-entry windows, or the
+// whole range of a dense device.
+__device__ inline void add_batch(const AggArgs& a, double* acc, uint32_t jb, uint32_t K, uint32_t eb, uint32_t em,
+                                 uint64_t dmask, uint64_t base, uint32_t len, const uint32_t (&ri)[kABatch],
+                                 const float (&rv)[kABatch])
+{
+  const uint32_t l = lane_id();
+#pragma unroll
+  for (int jj = 0; jj < kABatch; ++jj) {
+    const uint32_t j = jb + jj;
+    if (j >= K) break;
+    const double w = (double)a.w[j];
+    if ((dmask >> j) & 1ull) {
+      const float* g = a.dense[j] + base;
+#pragma unroll 8
+      for (int m = 0; m < kARange / 64; ++m) {
+        const uint32_t e = m * 64 + l;
+        if (e < len) lds_add(&acc[e], w * (double)g[e]);
+      }
+      continue;
+    }
+    const uint32_t b = __builtin_amdgcn_readlane(eb, j);
+    const uint32_t m = __builtin_amdgcn_readlane(em, j);
+    if (l < m) add_entry(acc, ri[jj], rv[jj], base, w);
+    // Entries of one device hit distinct positions, so their order is free.
+    for (uint32_t o = 64; o < m; o += 256) {
+      uint32_t xi[4];
+      float xv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t q = o + u * 64 + l;
+        xi[u] = 0u;
+        xv[u] = 0.f;
+        if (q < m) {
+          xi[u] = a.idx[j][b + q];
+          xv[u] = a.val[j][b + q];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (o + u * 64 + l < m) add_entry(acc, xi[u], xv[u], base, w);
+    }
+  }
+}
+
+// One wave per range. Lane j < K holds device j's entry interval [eb, eb + em)
+// in the range (from the range markers). Devices are added in ascending order,
+// kABatch at a time (see load_batch / add_batch). Dense devices add the whole
+// range from their gradient.
 __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
 {
-  __shared__ double acc[kATile];
+  __shared__ double acc[kARange];
   const uint32_t l = threadIdx.x;
   const uint32_t K = c.K;
-  const uint32_t rg = blockIdx.x;
-  uint32_t ptr = 0, kj = 0, dn = 0;
+  const uint32_t r = blockIdx.x;
+  const uint64_t base = (uint64_t)r * kARange;
+  const uint32_t len = (uint32_t)((c.n - base < (uint64_t)kARange) ? c.n - base : (uint64_t)kARange);
+  uint32_t eb = 0, em = 0;
+  bool dn = false;
   if (l < K) {
-    kj = a.k[l];
-    dn = dense_device(a, c, l) ? 1u : 0u;
-    ptr = dn ? 0u : c.start[(uint64_t)l * (c.nrange + 1) + rg];
+    // both markers in one round trip; rend is meaningful only where rbeg is set
+    const uint64_t at = (uint64_t)l * c.nrange + r;
+    const uint32_t b0 = c.rbeg[at];
+    uint32_t e0 = c.rend[at];
+    const uint32_t kk = a.k[l];
+    dn = dense_device(a, c, l);
+    if (e0 > kk) e0 = kk;       // keeps any input in bounds; ascending input never needs it
+    if (!dn && b0 != kNoEntry && b0 < e0) {
+      eb = b0;
+      em = e0 - b0;
+    }
   }
-  const uint32_t t0 = rg * kARange;
-  const uint32_t t1 = (t0 + kARange < c.ntile) ? t0 + kARange : c.ntile;
-  for (uint32_t t = t0; t < t1; ++t) {
-    const uint64_t base = (uint64_t)t * kATile;
-    const uint64_t tend = base + kATile;
-    const uint32_t len = (uint32_t)((c.n - base < (uint64_t)kATile) ? c.n - base : (uint64_t)kATile);
-    // Parameters of a full tile are fetched now, used after the accumulation.
-    f4 pp[kATile / 256];
-    const bool pre = c.params && len == (uint32_t)kATile;
-    if (pre) {
+  const uint64_t dmask = ballot(dn);
+  // Parameters of a full range are fetched now, used after the accumulation.
+  f4 pp[kARange / 256];
+  const bool pre = c.params && len == (uint32_t)kARange;
+  if (pre) {
 #pragma unroll
-      for (int m = 0; m < kATile / 256; ++m) pp[m] = *reinterpret_cast<const f4*>(c.params + base + m * 256 + l * 4);
-    }
+    for (int m = 0; m < kARange / 256; ++m) pp[m] = *reinterpret_cast<const f4*>(c.params + base + m * 256 + l * 4);
+  }
 #pragma unroll
-    for (int m = 0; m < kATile / 64; ++m) acc[m * 64 + l] = 0.0;
+  for (int m = 0; m < kARange / 64; ++m) acc[m * 64 + l] = 0.0;
 
-    for (uint32_t jb = 0; jb < K; jb += kABatch) {
-      uint32_t ri[kABatch];
-      float rv[kABatch];
-      bool ok[kABatch];
-#pragma unroll
-      for (int jj = 0; jj < kABatch; ++jj) {
-        const uint32_t j = jb + jj;
-        ok[jj] = false;
-        ri[jj] = 0u;
-        rv[jj] = 0.f;
-        if (j < K) {
-          const uint32_t pj = __builtin_amdgcn_readlane(ptr, j);
-          const uint32_t kk = __builtin_amdgcn_readlane(kj, j);
-          const uint32_t dj = __builtin_amdgcn_readlane(dn, j);
-          if (!dj && (uint64_t)pj + l < kk) {
-            ok[jj] = true;
-            ri[jj] = a.idx[j][pj + l];
-            rv[jj] = a.val[j][pj + l];
-          }
-        }
-      }
-#pragma unroll
-      for (int jj = 0; jj < kABatch; ++jj) {
-        const uint32_t j = jb + jj;
-        if (j >= K) break;
-        const double w = (double)a.w[j];
-        if (__builtin_amdgcn_readlane(dn, j)) {
-          const float* g = a.dense[j] + base;
-#pragma unroll 4
-          for (int m = 0; m < kATile / 64; ++m) {
-            const uint32_t e = m * 64 + l;
-            if (e < len) lds_add(&acc[e], w * (double)g[e]);
-          }
-          continue;
-        }
-        bool take = ok[jj] && (uint64_t)ri[jj] < tend;
-        uint32_t i = ri[jj];
-        float v = rv[jj];
-        while (true) {
-          if (take && (uint64_t)i >= base) {
-            const uint32_t pos = (uint32_t)(i - base);
-            if (pos < len) lds_add(&acc[pos], w * (double)v);
-          }
-          const uint32_t cnt = (uint32_t)__builtin_popcountll(ballot(take));
-          if (l == j) ptr += cnt;
-          if (cnt < 64u) break;
-          // 64 entries of this device fell in the tile: fetch the next 64.
-          const uint32_t pj = __builtin_amdgcn_readlane(ptr, j);
-          const uint32_t kk = __builtin_amdgcn_readlane(kj, j);
-          const bool okn = (uint64_t)pj + l < kk;
-          i = okn ? a.idx[j][pj + l] : 0u;
-          v = okn ? a.val[j][pj + l] : 0.f;
-          take = okn && (uint64_t)i < tend;
-        }
-      }
-    }
+  // Batches of kABatch devices, double-buffered: the next batch's loads are in
+  // flight while the current batch is added.
+  uint32_t ia[kABatch], ib[kABatch];
+  float va[kABatch], vb[kABatch];
+  load_batch(a, 0, K, eb, em, ia, va);
+  for (uint32_t jb = 0; jb < K; jb += 2 * kABatch) {
+    if (jb + kABatch < K) load_batch(a, jb + kABatch, K, eb, em, ib, vb);
+    add_batch(a, acc, jb, K, eb, em, dmask, base, len, ia, va);
+    if (jb + kABatch >= K) break;
+    if (jb + 2 * kABatch < K) load_batch(a, jb + 2 * kABatch, K, eb, em, ia, va);
+    add_batch(a, acc, jb + kABatch, K, eb, em, dmask, base, len, ib, vb);
+  }
 
-    // Round once to float; optionally the SGD update of Eqn 4c on the float aggregate.
-    if (pre) {
-      const double nlr = -(double)c.lr;
+  // Round once to float; optionally the SGD update of Eqn 4c on the float aggregate.
+  if (pre) {
+    const double nlr = -(double)c.lr;
 #pragma unroll
-      for (int m = 0; m < kATile / 256; ++m) {
-        const uint32_t e = m * 256 + l * 4;
-        const f4 g = {(float)acc[e], (float)acc[e + 1], (float)acc[e + 2], (float)acc[e + 3]};
-        *reinterpret_cast<f4*>(c.out + base + e) = g;
-        f4 p = pp[m];
+    for (int m = 0; m < kARange / 256; ++m) {
+      const uint32_t e = m * 256 + l * 4;
+      const f4 g = {(float)acc[e], (float)acc[e + 1], (float)acc[e + 2], (float)acc[e + 3]};
+      *reinterpret_cast<f4*>(c.out + base + e) = g;
+      f4 p = pp[m];
+      p.x = (float)__builtin_fma(nlr, (double)g.x, (double)p.x);
+      p.y = (float)__builtin_fma(nlr, (double)g.y, (double)p.y);
+      p.z = (float)__builtin_fma(nlr, (double)g.z, (double)p.z);
+      p.w = (float)__builtin_fma(nlr, (double)g.w, (double)p.w);
+      *reinterpret_cast<f4*>(c.params + base + e) = p;
+    }
+    return;
+  }
+  for (uint32_t e = l * 4; e < len; e += 256) {
+    if (e + 4 <= len) {
+      const f4 g = {(float)acc[e], (float)acc[e + 1], (float)acc[e + 2], (float)acc[e + 3]};
+      *reinterpret_cast<f4*>(c.out + base + e) = g;
+      if (c.params) {
+        f4 p = *reinterpret_cast<const f4*>(c.params + base + e);
+        const double nlr = -(double)c.lr;
         p.x = (float)__builtin_fma(nlr, (double)g.x, (double)p.x);
         p.y = (float)__builtin_fma(nlr, (double)g.y, (double)p.y);
         p.z = (float)__builtin_fma(nlr, (double)g.z, (double)p.z);
         p.w = (float)__builtin_fma(nlr, (double)g.w, (double)p.w);
         *reinterpret_cast<f4*>(c.params + base + e) = p;
       }
-      continue;
-    }
-    for (uint32_t e = l * 4; e < len; e += 256) {
-      if (e + 4 <= len) {
-        const f4 g = {(float)acc[e], (float)acc[e + 1], (float)acc[e + 2], (float)acc[e + 3]};
-        *reinterpret_cast<f4*>(c.out + base + e) = g;
-        if (c.params) {
-          f4 p = *reinterpret_cast<const f4*>(c.params + base + e);
-          const double nlr = -(double)c.lr;
-          p.x = (float)__builtin_fma(nlr, (double)g.x, (double)p.x);
-          p.y = (float)__builtin_fma(nlr, (double)g.y, (double)p.y);
-          p.z = (float)__builtin_fma(nlr, (double)g.z, (double)p.z);
-          p.w = (float)__builtin_fma(nlr, (double)g.w, (double)p.w);
-          *reinterpret_cast<f4*>(c.params + base + e) = p;
-        }
-      } else {
-        for (uint32_t q = e; q < len; ++q) {
-          const float g = (float)acc[q];
-          c.out[base + q] = g;
-          if (c.params)
-            c.params[base + q] = (float)__builtin_fma(-(double)c.lr, (double)g, (double)c.params[base + q]);
-        }
+    } else {
+      for (uint32_t q = e; q < len; ++q) {
+        const float g = (float)acc[q];
+        c.out[base + q] = g;
+        if (c.params)
+          c.params[base + q] = (float)__builtin_fma(-(double)c.lr, (double)g, (double)c.params[base + q]);
       }
     }
   }
@@ -228,8 +293,15 @@ hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate
       const uint32_t bx = c.kmax ? (uint32_t)((c.kmax + kBlock - 1) / kBlock) : 1u;
       k_validate<<<dim3(bx, c.K), kBlock, 0, s>>>(a, c);
     }
-    const uint64_t ns = (uint64_t)c.K * (c.nrange + 1);
-    k_starts<<<(uint32_t)((ns + kBlock - 1) / kBlock), kBlock, 0, s>>>(a, c);
+    if (c.kmax) {
+      const uint64_t nm = (uint64_t)c.K * c.nrange;
+      uint64_t fb = (nm + kBlock - 1) / kBlock;
+      if (fb > 2048) fb = 2048;
+      k_fill_u32<<<(uint32_t)fb, kBlock, 0, s>>>(c.rbeg, nm, kNoEntry);
+      uint64_t mb = (c.kmax + kBlock * 16 - 1) / (kBlock * 16);
+      if (mb > 4096) mb = 4096;
+      k_mark<<<dim3((uint32_t)mb, c.K), kBlock, 0, s>>>(a, c);
+    }
   }
   k_aggregate<<<c.nrange, 64, 0, s>>>(a, c);
   return hipGetLastError();

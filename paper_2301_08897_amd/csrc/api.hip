@@ -64,12 +64,12 @@ constexpr uint64_t kCapAlign = 64;
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-  uint32_t K = 0, tpd = 0, nslot = 0, ncb = 0, nfb = 0, nbmax = 0, ntile = 0, nrange = 0, s_stride = 0, s_n = 0;
+  uint32_t K = 0, tpd = 0, nslot = 0, ncb = 0, nfb = 0, nbmax = 0, nrange = 0, s_stride = 0, s_n = 0;
   uint64_t n = 0;
   uint32_t k[kMaxK], cap[kMaxK], mode[kMaxK], r_lo[kMaxK], r_hi[kMaxK];
   uint32_t any_fast = 0;
-  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_ctot, o_coff, o_ce, o_olist, o_slot, o_epart, o_cidx, o_cval, o_bcnt, o_bpre, o_be, o_aoff,
-      o_aerr;
+  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_ctot, o_coff, o_ce, o_olist, o_slot, o_epart, o_cidx, o_cval, o_bcnt, o_bpre, o_be, o_rbeg,
+      o_rend, o_aerr;
   size_t total = 0;
 };
 
@@ -109,8 +109,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
   // Tiles cover the 16-byte-aligned virtual row [0, n + shift), shift <= 3.
   L.tpd = ceil_div_u64(n + 3, kTile);
   L.nslot = L.tpd * kWaves;
-  L.ntile = ceil_div_u64(n, kATile);
-  L.nrange = ceil_div_u64(L.ntile, kARange);
+  L.nrange = ceil_div_u64(n, kARange);
   sample_geometry(n, L.s_stride, L.s_n);
   uint64_t sum_cap = 0, max_cap = 0;
   L.any_fast = 0;
@@ -173,7 +172,8 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
     L.o_bpre = take(sizeof(uint64_t) * (size_t)K * L.nbmax);
     L.o_be = take(sizeof(double) * (size_t)K * L.nbmax);
   }
-  L.o_aoff = take(sizeof(uint32_t) * (size_t)K * (L.nrange + 1));
+  L.o_rbeg = take(sizeof(uint32_t) * (size_t)K * L.nrange);
+  L.o_rend = take(sizeof(uint32_t) * (size_t)K * L.nrange);
   L.o_aerr = take(256);
   L.total = o;
   return true;
@@ -355,11 +355,11 @@ scadles_status scadles_weighted_aggregate(const scadles_sparse* sets, const floa
   AggCtx c;
   memset(&c, 0, sizeof(c));
   c.st = nullptr;
-  c.start = reinterpret_cast<uint32_t*>(b + L.o_aoff);
+  c.rbeg = reinterpret_cast<uint32_t*>(b + L.o_rbeg);
+  c.rend = reinterpret_cast<uint32_t*>(b + L.o_rend);
   c.err = reinterpret_cast<uint32_t*>(b + L.o_aerr);
   c.out = dense;
   c.K = Kc;
-  c.ntile = L.ntile;
   c.nrange = L.nrange;
   c.kmax = (uint32_t)kmax;
   c.n = n;
@@ -444,13 +444,13 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
   AggCtx c;
   memset(&c, 0, sizeof(c));
   c.st = reinterpret_cast<const DevState*>(b + L.o_st);
-  c.start = reinterpret_cast<uint32_t*>(b + L.o_aoff);
+  c.rbeg = reinterpret_cast<uint32_t*>(b + L.o_rbeg);
+  c.rend = reinterpret_cast<uint32_t*>(b + L.o_rend);
   c.err = reinterpret_cast<uint32_t*>(b + L.o_aerr);
   c.out = dense;
   c.params = params;
   c.lr = lr;
   c.K = K;
-  c.ntile = L.ntile;
   c.nrange = L.nrange;
   c.kmax = (uint32_t)kmax;
   c.n = n;

@@ -19,9 +19,9 @@ constexpr int kSBlk = 4096;            // sample elements per workgroup
 constexpr int kSChunk = 256;           // contiguous sample chunk (1 KiB)
 constexpr int kBins = 2048;            // radix digit: 11 bits
 constexpr int kDigitBits = 11;
-constexpr int kATile = 1024;           // aggregation: positions per wave tile (8 KiB of doubles in LDS)
-constexpr int kARange = 4;             // aggregation: tiles per wave
-constexpr int kABatch = 16;            // aggregation: devices whose entries are loaded together
+constexpr int kARange = 2048;          // aggregation: positions per wave (16 KiB of doubles in LDS)
+constexpr int kABatch = 8;             // aggregation: devices whose entries are loaded together
+constexpr uint32_t kNoEntry = 0xFFFFFFFFu;   // range marker: the device has no entry in the range
 constexpr int kMaxK = 64;              // SCADLES_MAX_DEVICES
 constexpr int kSlots = 4;              // selection slots per device
 constexpr int kSlotSampleLo = 0, kSlotSampleHi = 1, kSlotCand = 2, kSlotFull = 3;
@@ -141,14 +141,14 @@ struct AggArgs {
 
 struct AggCtx {
   const DevState* st;     // fused path: per-device sparse/dense decision; null otherwise
-  uint32_t* start;        // [K][nrange + 1] first survivor of each wave's range
+  uint32_t* rbeg;         // [K][nrange] first entry of each device in each range (kNoEntry: none)
+  uint32_t* rend;         // [K][nrange] one past its last entry (read only where rbeg is set)
   uint32_t* err;          // validation flag
   float* out;             // dense aggregate
   float* params;          // null: no SGD
   float lr;
   uint32_t K;
-  uint32_t ntile;         // ceil(n / kATile)
-  uint32_t nrange;        // ceil(ntile / kARange): waves of the aggregation kernel
+  uint32_t nrange;        // ceil(n / kARange): waves of the aggregation kernel
   uint32_t kmax;
   uint64_t n;
 };
