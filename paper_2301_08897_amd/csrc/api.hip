@@ -64,11 +64,11 @@ constexpr uint64_t kCapAlign = 64;
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-  uint32_t K = 0, tpd = 0, nslot = 0, ncb = 0, nfb = 0, nbmax = 0, nrange = 0, s_stride = 0, s_n = 0;
+  uint32_t K = 0, tpd = 0, nslot = 0, ngrp = 0, ncb = 0, nfb = 0, nbmax = 0, nrange = 0, s_stride = 0, s_n = 0;
   uint64_t n = 0;
   uint32_t k[kMaxK], cap[kMaxK], mode[kMaxK], r_lo[kMaxK], r_hi[kMaxK];
   uint32_t any_fast = 0;
-  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_ctot, o_coff, o_ce, o_olist, o_slot, o_epart, o_cidx, o_cval, o_bcnt, o_bpre, o_be, o_rbeg,
+  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_ctot, o_coff, o_ce, o_olist, o_slot, o_epart, o_cidx, o_cval, o_band, o_gcnt, o_gpre, o_bcnt, o_bpre, o_be, o_rbeg,
       o_rend, o_aerr;
   size_t total = 0;
 };
@@ -109,6 +109,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
   // Tiles cover the 16-byte-aligned virtual row [0, n + shift), shift <= 3.
   L.tpd = ceil_div_u64(n + 3, kTile);
   L.nslot = L.tpd * kWaves;
+  L.ngrp = ceil_div_u64(L.nslot, kGatherSlots);
   L.nrange = ceil_div_u64(n, kARange);
   sample_geometry(n, L.s_stride, L.s_n);
   uint64_t sum_cap = 0, max_cap = 0;
@@ -159,15 +160,18 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
     // Slots are needed only by fast-path devices; sized for all K for simplicity.
     const size_t nslots = L.any_fast ? (size_t)K * L.nslot : 0;
     L.o_scnt = take(sizeof(uint32_t) * (size_t)K * L.nslot);
-    L.o_soff = take(sizeof(uint32_t) * (size_t)K * L.nslot);
+    L.o_soff = take(sizeof(uint64_t) * (size_t)K * L.nslot);
     L.o_ctot = take(sizeof(uint64_t) * (size_t)K * kMaxChunks);
-    L.o_coff = take(sizeof(uint32_t) * (size_t)K * kMaxChunks);
+    L.o_coff = take(sizeof(uint64_t) * (size_t)K * kMaxChunks);
     L.o_ce = take(sizeof(double) * (size_t)K * kMaxChunks);
     L.o_olist = take(sizeof(uint32_t) * (size_t)K * L.nslot);
     L.o_slot = take(sizeof(uint64_t) * nslots * kWaveCap);
     L.o_epart = take(sizeof(double) * (size_t)K * L.nslot);
     L.o_cidx = take(sizeof(uint32_t) * sum_cap);
     L.o_cval = take(sizeof(float) * sum_cap);
+    L.o_band = take(sizeof(uint32_t) * sum_cap);
+    L.o_gcnt = take(sizeof(uint64_t) * (size_t)K * L.ngrp);
+    L.o_gpre = take(sizeof(uint64_t) * (size_t)K * L.ngrp);
     L.o_bcnt = take(sizeof(uint64_t) * (size_t)K * L.nbmax);
     L.o_bpre = take(sizeof(uint64_t) * (size_t)K * L.nbmax);
     L.o_be = take(sizeof(double) * (size_t)K * L.nbmax);
@@ -188,15 +192,18 @@ Ctx make_ctx(const Layout& L, void* ws)
   c.st = reinterpret_cast<DevState*>(b + L.o_st);
   c.hist = reinterpret_cast<uint32_t*>(b + L.o_hist);
   c.slot_cnt = reinterpret_cast<uint32_t*>(b + L.o_scnt);
-  c.slot_off = reinterpret_cast<uint32_t*>(b + L.o_soff);
+  c.slot_off = reinterpret_cast<uint64_t*>(b + L.o_soff);
   c.chunk_tot = reinterpret_cast<uint64_t*>(b + L.o_ctot);
-  c.chunk_off = reinterpret_cast<uint32_t*>(b + L.o_coff);
+  c.chunk_off = reinterpret_cast<uint64_t*>(b + L.o_coff);
   c.chunk_e = reinterpret_cast<double*>(b + L.o_ce);
   c.ovf_list = reinterpret_cast<uint32_t*>(b + L.o_olist);
   c.slot = reinterpret_cast<uint64_t*>(b + L.o_slot);
   c.epart = reinterpret_cast<double*>(b + L.o_epart);
   c.cand_idx = reinterpret_cast<uint32_t*>(b + L.o_cidx);
   c.cand_val = reinterpret_cast<float*>(b + L.o_cval);
+  c.band = reinterpret_cast<uint32_t*>(b + L.o_band);
+  c.grp_cnt = reinterpret_cast<uint64_t*>(b + L.o_gcnt);
+  c.grp_pre = reinterpret_cast<uint64_t*>(b + L.o_gpre);
   c.blk_cnt = reinterpret_cast<uint64_t*>(b + L.o_bcnt);
   c.blk_pre = reinterpret_cast<uint64_t*>(b + L.o_bpre);
   c.blk_e = reinterpret_cast<double*>(b + L.o_be);
@@ -204,6 +211,7 @@ Ctx make_ctx(const Layout& L, void* ws)
   c.K = L.K;
   c.tpd = L.tpd;
   c.nslot = L.nslot;
+  c.ngrp = L.ngrp;
   c.ncb = L.ncb;
   c.nfb = L.nfb;
   c.nbmax = L.nbmax;

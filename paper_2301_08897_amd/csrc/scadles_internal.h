@@ -32,7 +32,7 @@ constexpr int kFullWorkers = 1024;     // grid of the grid-stride exact-path ker
 constexpr int kWaveCap = 512;          // main pass: candidates one wave chunk (4096 elements) can stage
 constexpr int kScanChunk = 4096;       // slots per workgroup of the slot-offset scan
 constexpr int kMaxChunks = 256;        // >= ceil(nslot / kScanChunk) for n < 2^32
-constexpr int kGatherSlots = 8;        // slots per wave in the candidate gather
+constexpr int kGatherSlots = 8;        // slots per wave in the selection-list and output passes
 constexpr int kOverflowBlocks = 32;    // workgroups per device re-scanning overflowed slots
 
 enum : uint32_t { kModeFast = 0, kModeExact = 1 };
@@ -69,11 +69,12 @@ struct Sel {
 struct DevState {
   Sel sel[kSlots];
   uint64_t cand, sure;    // main pass totals: keys >= t_lo, keys >= t_hi
+  uint64_t sel_n;         // entries of the selection list
   uint32_t t_lo, t_hi;    // bracket used by the main pass
   uint32_t fallback;      // 1: the exact full-data path produces this device's output
   uint32_t band_low;      // candidate select ran on [t_lo, t_hi): add `sure` above it
   uint32_t thr;           // final threshold key (k-th largest)
-  uint32_t err;           // internal error bits (look-back timeout, select miss)
+  uint32_t err;           // internal error bits (select miss, count mismatch)
   uint64_t c_gt, need;    // keys above thr; keys equal to thr that are kept
   double e_all, e_kept;
   uint32_t sparse;        // 1: the device sends Top-k (adaptive rule), 0: dense
@@ -86,15 +87,18 @@ struct Ctx {
   DevState* st;
   uint32_t* hist;         // [K][kSlots][kBins]
   uint32_t* slot_cnt;     // [K][nslot] per-wave candidate | sure << 16 counts of the main pass
-  uint32_t* slot_off;     // [K][nslot] offset of each slot within its scan chunk
+  uint64_t* slot_off;     // [K][nslot] candidate | sure << 32 counts before each slot within its scan chunk
   uint64_t* chunk_tot;    // [K][kMaxChunks] candidate | sure << 32 totals of each scan chunk
-  uint32_t* chunk_off;    // [K][kMaxChunks] offset of each scan chunk in the candidate list
+  uint64_t* chunk_off;    // [K][kMaxChunks] candidate | sure << 32 counts before each scan chunk
   double* chunk_e;        // [K][kMaxChunks] sum of squares of each scan chunk
   uint64_t* slot;         // [K][nslot][kWaveCap] staged candidates per wave chunk: index | value bits << 32
   uint32_t* ovf_list;     // [K][nslot] slots whose wave found more than kWaveCap candidates
   double* epart;          // [K][nslot] sum of squares per main-pass wave chunk
-  uint32_t* cand_idx;     // candidate regions
+  uint32_t* cand_idx;     // candidate regions (entries of overflowed slots only)
   float* cand_val;
+  uint32_t* band;         // selection lists: keys in the selection interval, per device at cand_off
+  uint64_t* grp_cnt;      // [K][ngrp] kept-above | equal << 32 counts per write group of slots
+  uint64_t* grp_pre;      // [K][ngrp] exclusive prefix of grp_cnt
   uint64_t* blk_cnt;      // [K][nbmax] packed (gt | eq << 32) per compaction block
   uint64_t* blk_pre;      // [K][nbmax] exclusive prefix of blk_cnt
   double* blk_e;          // [K][nbmax] kept sum of squares per compaction block
@@ -104,6 +108,7 @@ struct Ctx {
   uint32_t K;
   uint32_t tpd;           // main tiles per device: ceil((n + 3) / kTile)
   uint32_t nslot;         // main-pass wave chunks per device: tpd * kWaves
+  uint32_t ngrp;          // write groups per device: ceil(nslot / kGatherSlots)
   uint32_t ncb;           // candidate blocks per device (max over devices)
   uint32_t nfb;           // exact-path blocks per device: ceil((n + 3) / kCBlk)
   uint32_t nbmax;         // max(ncb, nfb)

@@ -10,16 +10,19 @@
 //   1. bracket   : a systematic sample (256-element chunks at a fixed stride)
 //                  is radix-selected at two ranks around k * (sample/n), giving
 //                  keys t_lo <= (k-th largest key) < t_hi with high probability;
-//   2. main pass : every gradient is read once; keys >= t_lo are written as
-//                  candidates (idx, val) in index order, each tile finding its
-//                  output offset by decoupled look-back; sum g^2 is fused in;
-//   3. threshold : the exact k-th largest key is radix-selected among the
-//                  candidates in [t_lo, t_hi) (or above t_hi);
-//   4. compaction: the kept set -- keys above the threshold plus the lowest-
-//                  indexed `need` keys equal to it -- is written in index order.
+//   2. main pass : every gradient is read once; each wave stages the keys >= t_lo
+//                  of its 4096-element chunk ("slot": index, value pairs in
+//                  index order) with counts of keys >= t_lo and >= t_hi; sum g^2
+//                  is fused in; a scan of the counts gives every slot's offsets;
+//   3. threshold : the keys of the selection interval ([t_lo, t_hi), or above
+//                  t_hi when that already holds k keys) are copied to a short
+//                  list, and the exact k-th largest key is radix-selected on it;
+//   4. output    : per group of slots, the kept entries -- keys above the
+//                  threshold plus the lowest-indexed `need` keys equal to it --
+//                  are counted, scanned and written in index order.
 // If the bracket missed (fewer than k candidates) or the candidates overflow
 // their region, the device falls back to the exact path: a radix select over
-// all of its data, then the same ordered compaction over its data.
+// all of its data, then an ordered compaction over its data.
 #include "scadles_internal.h"
 
 namespace scadles {
@@ -334,6 +337,12 @@ __device__ inline uint32_t wave_prefix_of_block(uint32_t packed_lane, uint32_t* 
 // rank keys (key + 1, pads 0) and fmax drops the pads' NaN from the squares.
 // Counts are wave totals from ballots (scalar popcounts).
 // A staged candidate: its index in the low word, its value's bits in the high word.
+// Entry e of slot s lives at ((rot(s) + e) mod kWaveCap) of the slot's region:
+// the rotation spreads the (short) written part of the regions over all
+// address bits below the region size, so the writes use every memory channel.
+static_assert((kWaveCap & (kWaveCap - 1)) == 0, "slot rotation needs a power-of-two region");
+__device__ inline uint32_t slot_rot(uint64_t slot) { return (uint32_t)(slot * 53u) & (kWaveCap - 1u); }
+
 __device__ inline uint64_t pack_cand(uint32_t i, float v) { return (uint64_t)i | ((uint64_t)__float_as_uint(v) << 32); }
 
 template <bool kEdge>
@@ -417,9 +426,10 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
     c.epart[slot] = es;
   }
   if (wc <= (uint32_t)kWaveCap) {
-    // Nontemporal: the slots are read once, by k_gather, after the whole pass.
+    // Nontemporal: the slots are read only after the whole pass (selection list, output).
     GLOBAL uint64_t* sp = gptr(c.slot + slot * kWaveCap);
-    for (uint32_t i = l; i < wc; i += 64) __builtin_nontemporal_store(s_c[w][i], sp + i);
+    const uint32_t rot = slot_rot(slot);
+    for (uint32_t i = l; i < wc; i += 64) __builtin_nontemporal_store(s_c[w][i], sp + ((rot + i) & (kWaveCap - 1u)));
   } else if (l == 0) {
     // Dense-candidate chunk (rare): record it; k_overflow re-scans it once the
     // slot offsets are known. One atomic per such wave.
@@ -474,12 +484,12 @@ __global__ __launch_bounds__(kBlock) void k_slot_scan(Ctx c)
   __syncthreads();
   uint64_t run = incl - sum;
   for (uint32_t i = 0; i < (tid >> 6); ++i) run += s_w[i];
-  uint32_t* off = c.slot_off + (uint64_t)j * c.nslot;
-  uint32_t oc = (uint32_t)(run & 0xFFFFFFFFull);
+  uint64_t* off = c.slot_off + (uint64_t)j * c.nslot;
+  uint64_t oc = run;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     if (s0 + i < c.nslot) off[s0 + i] = oc;
-    oc += v[i] & 0xFFFFu;
+    oc += (uint64_t)(v[i] & 0xFFFFu) | ((uint64_t)(v[i] >> 16) << 32);
   }
   if (tid == kBlock - 1) c.chunk_tot[(uint64_t)j * kMaxChunks + ch] = run + sum;
 }
@@ -519,7 +529,7 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
     __syncthreads();
     uint64_t run = incl - v;
     for (uint32_t i = 0; i < (tid >> 6); ++i) run += s_w[i];
-    if (tid < nchunk) c.chunk_off[(uint64_t)j * kMaxChunks + tid] = (uint32_t)(run & 0xFFFFFFFFull);
+    if (tid < nchunk) c.chunk_off[(uint64_t)j * kMaxChunks + tid] = run;
     const uint64_t tot = s_w[0] + s_w[1] + s_w[2] + s_w[3];
     cand = tot & 0xFFFFFFFFull;
     sure = tot >> 32;
@@ -541,6 +551,7 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
   Sel sel;
   __builtin_memset(&sel, 0, sizeof(sel));
   sel.active = 1;
+  s.sel_n = 0;
   if (fb) {
     s.fallback = 1;
     sel.lo = 0;
@@ -555,11 +566,13 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
       sel.hi = thi;
       sel.rank = d.k - s.sure;
       s.band_low = 1;
+      s.sel_n = s.cand - s.sure;
     } else {
       sel.lo = thi;
       sel.hi = kKeyInf;
       sel.rank = d.k;
       s.band_low = 0;
+      s.sel_n = s.sure;
     }
     const uint32_t b = bitlen32(sel.hi - sel.lo - 1u);
     sel.bits = b ? b : 1u;
@@ -567,72 +580,110 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
   }
 }
 
-// Packs every slot into the device's candidate list at its offset (index
-// order is kept: slots are in index order and each slot is). Slots whose wave
-// overflowed are written by k_overflow.
-// Copies entries [from, cn) of a slot to (di, dv) + off, eight loads per lane
-// in flight before the stores.
-__device__ inline void gather_copy(const GLOBAL uint64_t* sp, uint32_t from, uint32_t cn, uint64_t off, uint64_t cap,
-                                   GLOBAL uint32_t* di, GLOBAL float* dv)
+// Candidate counts before slot s of device j: candidates | sure << 32.
+__device__ inline uint64_t slot_pre(const Ctx& c, uint32_t j, uint32_t s)
 {
-  const uint32_t l = lane_id();
-  for (uint32_t b0 = from; b0 < cn; b0 += 8 * 64) {
-    uint64_t t[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const uint32_t e = b0 + u * 64 + l;
-      t[u] = e < cn ? sp[e] : 0ull;
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const uint32_t e = b0 + u * 64 + l;
-      if (e < cn && off + e < cap) {
-        di[off + e] = (uint32_t)t[u];
-        dv[off + e] = __uint_as_float((uint32_t)(t[u] >> 32));
-      }
-    }
-  }
+  if (s >= c.nslot) return c.st[j].cand | (c.st[j].sure << 32);
+  return c.chunk_off[(uint64_t)j * kMaxChunks + s / kScanChunk] + c.slot_off[(uint64_t)j * c.nslot + s];
 }
 
-// Each wave takes kGatherSlots consecutive slots and first issues the loads of
-// all of them (metadata, then the first 64 entries of each), then stores.
-__global__ __launch_bounds__(kBlock) void k_gather(Ctx c)
+// Offset in the selection list of the entries of slots >= s: the interval
+// [t_lo, t_hi) has candidates - sure entries before, [t_hi, inf) has sure.
+__device__ inline uint32_t sel_pre(uint64_t pre, uint32_t band_low)
+{
+  const uint32_t cand = (uint32_t)pre, sure = (uint32_t)(pre >> 32);
+  return band_low ? cand - sure : sure;
+}
+
+// Entry e of a slot: from its staged pairs, or (overflowed slot) from the
+// candidate list where k_overflow wrote it.
+struct SlotSrc {
+  const GLOBAL uint64_t* pairs;   // null: overflowed
+  uint32_t rot;
+  const GLOBAL uint32_t* ci;
+  const GLOBAL float* cv;
+};
+
+__device__ inline SlotSrc slot_src(const Ctx& c, uint32_t j, uint32_t s, uint32_t cn, uint32_t cand_at)
+{
+  SlotSrc r;
+  if (cn <= (uint32_t)kWaveCap) {
+    const uint64_t slot = (uint64_t)j * c.nslot + s;
+    r.pairs = gptr(c.slot) + slot * kWaveCap;
+    r.rot = slot_rot(slot);
+    r.ci = nullptr;
+    r.cv = nullptr;
+  } else {
+    const uint64_t o = c.desc[j].cand_off + cand_at;
+    r.pairs = nullptr;
+    r.rot = 0;
+    r.ci = gptr(c.cand_idx) + o;
+    r.cv = gptr(c.cand_val) + o;
+  }
+  return r;
+}
+
+__device__ inline uint64_t slot_entry(const SlotSrc& r, uint32_t e)
+{
+  if (r.pairs) return r.pairs[(r.rot + e) & (kWaveCap - 1u)];
+  return (uint64_t)r.ci[e] | ((uint64_t)__float_as_uint(r.cv[e]) << 32);
+}
+
+__device__ inline uint32_t entry_key(uint64_t p) { return (uint32_t)(p >> 32) & kKeyMask; }
+
+// ---- 3. selection list ----------------------------------------------------------------------
+// Each wave takes kGatherSlots consecutive slots and writes the keys of their
+// entries in the selection interval [sel.lo, sel.hi) to the device's selection
+// list, slot after slot (the slot counts give every slot's offset). The
+// threshold is then radix-selected over this short list only.
+// Occupancy 8 (at most 64 VGPRs): these passes are bound by memory latency.
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_band(Ctx c)
 {
   constexpr uint32_t kPerBlock = kGatherSlots * kWaves;
   const uint32_t groups = (c.nslot + kPerBlock - 1) / kPerBlock;
   const uint32_t j = blockIdx.x / groups, g = blockIdx.x - j * groups;
   const DevState& st = c.st[j];
   if (st.fallback) return;
-  const DevDesc d = c.desc[j];
   const uint32_t l = lane_id(), w = threadIdx.x >> 6;
   const uint32_t s0 = g * kPerBlock + w * kGatherSlots;
   if (s0 >= c.nslot) return;
-  GLOBAL uint32_t* cidx = gptr(c.cand_idx + d.cand_off);
-  GLOBAL float* cval = gptr(c.cand_val + d.cand_off);
-  const GLOBAL uint64_t* slots = gptr(c.slot) + (uint64_t)j * c.nslot * kWaveCap;
-  // lane i < kGatherSlots: metadata of slot s0 + i
-  uint32_t m_cnt = 0, m_off = 0;
+  const uint32_t lo = st.sel[kSlotCand].lo, hi = st.sel[kSlotCand].hi, band_low = st.band_low;
+  const uint64_t cap = c.desc[j].cap;
+  GLOBAL uint32_t* band = gptr(c.band + c.desc[j].cand_off);
+  // lane i < kGatherSlots: count and candidate offsets of slot s0 + i
+  uint32_t m_cnt = 0;
+  uint64_t m_pre = 0;
   if (l < (uint32_t)kGatherSlots && s0 + l < c.nslot) {
-    const uint64_t slot = (uint64_t)j * c.nslot + s0 + l;
-    m_cnt = c.slot_cnt[slot] & 0xFFFFu;
-    m_off = c.chunk_off[(uint64_t)j * kMaxChunks + (s0 + l) / kScanChunk] + c.slot_off[slot];
+    m_cnt = c.slot_cnt[(uint64_t)j * c.nslot + s0 + l] & 0xFFFFu;
+    m_pre = slot_pre(c, j, s0 + l);
   }
+  // first 64 entries of every slot in flight before any store
   uint64_t r[kGatherSlots];
 #pragma unroll
   for (int i = 0; i < kGatherSlots; ++i) {
     const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
-    r[i] = (cn <= (uint32_t)kWaveCap && l < cn) ? slots[(uint64_t)(s0 + i) * kWaveCap + l] : 0ull;
+    const uint64_t pre = ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(m_pre >> 32), i) << 32) |
+                         __builtin_amdgcn_readlane((uint32_t)m_pre, i);
+    r[i] = 0ull;
+    if (l < cn) r[i] = slot_entry(slot_src(c, j, s0 + i, cn, (uint32_t)pre), l);
   }
 #pragma unroll
   for (int i = 0; i < kGatherSlots; ++i) {
     const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
-    const uint32_t off = __builtin_amdgcn_readlane(m_off, i);
-    if (cn == 0u || cn > (uint32_t)kWaveCap) continue;
-    if (l < cn && (uint64_t)off + l < d.cap) {
-      cidx[off + l] = (uint32_t)r[i];
-      cval[off + l] = __uint_as_float((uint32_t)(r[i] >> 32));
+    if (cn == 0u) continue;
+    const uint64_t pre = ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(m_pre >> 32), i) << 32) |
+                         __builtin_amdgcn_readlane((uint32_t)m_pre, i);
+    const SlotSrc src = slot_src(c, j, s0 + i, cn, (uint32_t)pre);
+    uint64_t run = sel_pre(pre, band_low);
+    for (uint32_t e0 = 0; e0 < cn; e0 += 64) {
+      const uint64_t p = e0 == 0 ? r[i] : (e0 + l < cn ? slot_entry(src, e0 + l) : 0ull);
+      const uint32_t key = entry_key(p);
+      const bool f = e0 + l < cn && key >= lo && key < hi;
+      const uint64_t b = ballot(f);
+      const uint64_t pos = run + mbcnt(b);
+      if (f && pos < cap) band[pos] = key;
+      run += __builtin_popcountll(b);
     }
-    if (cn > 64u) gather_copy(slots + (uint64_t)(s0 + i) * kWaveCap, 64, cn, off, d.cap, cidx, cval);
   }
 }
 
@@ -654,8 +705,8 @@ __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_
   const uint32_t waves = blocks_per_dev * kWaves;
   for (uint32_t i = b * kWaves + (threadIdx.x >> 6); i < n_ovf; i += waves) {
     const uint32_t s = c.ovf_list[(uint64_t)j * c.nslot + i];
-    const uint64_t off = (uint64_t)c.chunk_off[(uint64_t)j * kMaxChunks + s / kScanChunk] +
-                         c.slot_off[(uint64_t)j * c.nslot + s];
+    const uint64_t off = (uint32_t)(c.chunk_off[(uint64_t)j * kMaxChunks + s / kScanChunk] +
+                                    c.slot_off[(uint64_t)j * c.nslot + s]);
     const uint64_t v0 = (uint64_t)(s / kWaves) * kTile + (uint64_t)(s % kWaves) * (kTileRounds * 256) + l * 4;
     f4 x[kTileRounds];
 #pragma unroll
@@ -687,7 +738,7 @@ __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_
   }
 }
 
-// ---- 3. histogram pass over candidates (fast devices) and full data (exact devices) ----------
+// ---- 4. histogram pass over selection lists (fast devices) and full data (exact devices) -----
 __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks)
 {
   __shared__ uint32_t h[kBins];
@@ -697,23 +748,27 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
     if (s.fallback) return;
     const Sel sel = s.sel[kSlotCand];
     if (!sel.active) return;
-    const uint64_t cnt = s.cand;
+    const uint64_t cnt = s.sel_n;
     const uint64_t q0 = (uint64_t)b * kCBlk;
     if (q0 >= cnt) return;
     for (int i = threadIdx.x; i < kBins; i += kBlock) h[i] = 0u;
     __syncthreads();
     const SelView sv = view_of(sel);
     const uint64_t rem = (cnt - q0 < (uint64_t)kCBlk) ? cnt - q0 : (uint64_t)kCBlk;
-    const Row row{gptr(c.cand_val + c.desc[j].cand_off + q0), 0, rem};
+    const GLOBAL uint32_t* keys = gptr(c.band + c.desc[j].cand_off + q0);
 #pragma unroll 2
     for (int r = 0; r < kCBlkRounds; ++r) {
       const uint64_t e = (uint64_t)r * kRound + threadIdx.x * 4;
       if (e >= rem) break;
-      const f4 x = load4(row, e, false);
+      u4 x = {kKeyInf, kKeyInf, kKeyInf, kKeyInf};
+      if (e + 4 <= rem) x = *(const GLOBAL u4*)(keys + e);
+      else
+        for (int q = 0; q < 4; ++q)
+          if (e + q < rem) x[q] = keys[e + q];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         uint32_t dg;
-        if (e + q < rem && sel_digit(sv, key_of(x[q]), dg)) atomicAdd(&h[dg], 1u);
+        if (e + q < rem && sel_digit(sv, x[q], dg)) atomicAdd(&h[dg], 1u);
       }
     }
     __syncthreads();
@@ -750,7 +805,131 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
   }
 }
 
-// ---- 4. ordered compaction -------------------------------------------------------------------
+// ---- 5. ordered output of the fast path ----------------------------------------------------
+// Output groups are kGatherSlots consecutive slots. Kept: key > thr, or
+// key == thr while fewer than `need` equal keys came before (index order);
+// a kept entry goes to (keys above thr before it) + min(equal keys before it, need).
+
+// Per group: keys above the threshold | keys equal to it << 32, counted on the
+// selection list; with the threshold in [t_lo, t_hi) the group's keys >= t_hi
+// (all above it) are added from the slot counts. One wave per group.
+__global__ __launch_bounds__(kBlock) void k_grp_count(Ctx c)
+{
+  const uint32_t bpd = (c.ngrp + kWaves - 1) / kWaves;
+  const uint32_t j = blockIdx.x / bpd;
+  const uint32_t g = (blockIdx.x - j * bpd) * kWaves + (threadIdx.x >> 6);
+  const DevState& st = c.st[j];
+  if (st.fallback || g >= c.ngrp) return;
+  uint32_t thr;
+  uint64_t need;
+  threshold_of(st, thr, need);
+  const uint32_t s0 = g * kGatherSlots;
+  const uint32_t s1 = (s0 + kGatherSlots < c.nslot) ? s0 + kGatherSlots : c.nslot;
+  const uint64_t p0 = slot_pre(c, j, s0), p1 = slot_pre(c, j, s1);
+  const uint32_t q0 = sel_pre(p0, st.band_low), q1 = sel_pre(p1, st.band_low);
+  const GLOBAL uint32_t* keys = gptr(c.band + c.desc[j].cand_off);
+  uint64_t gt = 0, eq = 0;
+  for (uint32_t q = q0 + lane_id(); q < q1; q += 64) {
+    const uint32_t key = keys[q];
+    gt += key > thr ? 1u : 0u;
+    eq += key == thr ? 1u : 0u;
+  }
+  gt = wave_sum_u64(gt);
+  eq = wave_sum_u64(eq);
+  if (st.band_low) gt += (p1 >> 32) - (p0 >> 32);
+  if (lane_id() == 0) c.grp_cnt[(uint64_t)j * c.ngrp + g] = gt | (eq << 32);
+}
+
+// Exclusive prefix of nb packed counts, one workgroup.
+__device__ inline void block_excl_scan_u64(const uint64_t* cnt, uint64_t* pre, uint32_t nb, uint64_t* s_w)
+{
+  const uint32_t tid = threadIdx.x;
+  const uint32_t per = (nb + kBlock - 1) / kBlock;
+  const uint32_t b0 = tid * per, b1 = (b0 + per < nb) ? b0 + per : nb;
+  uint64_t sum = 0;
+  for (uint32_t b = b0; b < b1; ++b) sum += cnt[b];
+  const uint64_t incl = wave_incl_scan_u64(sum);
+  if (lane_id() == 63) s_w[tid >> 6] = incl;
+  __syncthreads();
+  uint64_t base = 0;
+  for (uint32_t i = 0; i < (tid >> 6); ++i) base += s_w[i];
+  uint64_t run = base + incl - sum;
+  for (uint32_t b = b0; b < b1; ++b) {
+    pre[b] = run;
+    run += cnt[b];
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_grp_scan(Ctx c)
+{
+  __shared__ uint64_t s_w[4];
+  const uint32_t j = blockIdx.x;
+  if (c.st[j].fallback) return;
+  block_excl_scan_u64(c.grp_cnt + (uint64_t)j * c.ngrp, c.grp_pre + (uint64_t)j * c.ngrp, c.ngrp, s_w);
+}
+
+// One wave per group: its slots' candidates in index order, kept ones written
+// to the device's outputs; the kept sum of squares goes to epart[j][group].
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_write_fast(Ctx c)
+{
+  const uint32_t bpd = (c.ngrp + kWaves - 1) / kWaves;
+  const uint32_t j = blockIdx.x / bpd;
+  const uint32_t g = (blockIdx.x - j * bpd) * kWaves + (threadIdx.x >> 6);
+  const DevState& st = c.st[j];
+  if (st.fallback || g >= c.ngrp) return;
+  uint32_t thr;
+  uint64_t need;
+  threshold_of(st, thr, need);
+  const DevDesc d = c.desc[j];
+  GLOBAL uint32_t* oi = gptr(d.idx_out);
+  GLOBAL float* ov = gptr(d.val_out);
+  const uint32_t l = lane_id();
+  const uint32_t s0 = g * kGatherSlots;
+  const uint64_t pre = c.grp_pre[(uint64_t)j * c.ngrp + g];
+  uint64_t run_g = pre & 0xFFFFFFFFull, run_e = pre >> 32;
+  uint32_t m_cnt = 0, m_at = 0;
+  if (l < (uint32_t)kGatherSlots && s0 + l < c.nslot) {
+    m_cnt = c.slot_cnt[(uint64_t)j * c.nslot + s0 + l] & 0xFFFFu;
+    m_at = (uint32_t)slot_pre(c, j, s0 + l);
+  }
+  uint64_t r[kGatherSlots];
+#pragma unroll
+  for (int i = 0; i < kGatherSlots; ++i) {
+    const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
+    r[i] = 0ull;
+    if (l < cn) r[i] = slot_entry(slot_src(c, j, s0 + i, cn, __builtin_amdgcn_readlane(m_at, i)), l);
+  }
+  double e2 = 0.0;
+#pragma unroll
+  for (int i = 0; i < kGatherSlots; ++i) {
+    const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
+    if (cn == 0u) continue;
+    const SlotSrc src = slot_src(c, j, s0 + i, cn, __builtin_amdgcn_readlane(m_at, i));
+    for (uint32_t e0 = 0; e0 < cn; e0 += 64) {
+      const bool valid = e0 + l < cn;
+      const uint64_t p = e0 == 0 ? r[i] : (valid ? slot_entry(src, e0 + l) : 0ull);
+      const uint32_t key = entry_key(p);
+      const bool fg = valid && key > thr, fe = valid && key == thr;
+      const uint64_t bg = ballot(fg), be = ballot(fe);
+      const uint64_t gt_b = run_g + mbcnt(bg), eq_b = run_e + mbcnt(be);
+      if (fg || (fe && eq_b < need)) {
+        const uint64_t pos = gt_b + (eq_b < need ? eq_b : need);
+        const float v = __uint_as_float((uint32_t)(p >> 32));
+        if (pos < d.k) {
+          oi[pos] = (uint32_t)p;
+          ov[pos] = v;
+        }
+        e2 = __builtin_fma((double)v, (double)v, e2);
+      }
+      run_g += __builtin_popcountll(bg);
+      run_e += __builtin_popcountll(be);
+    }
+  }
+  const double es = wave_sum_f64(e2);
+  if (l == 0) c.epart[(uint64_t)j * c.nslot + g] = es;
+}
+
+// ---- 6. ordered compaction of the exact path ------------------------------------------------
 // Blocks are kCBlk positions of a device's candidate list (fast path) or of its
 // gradient's virtual row (exact path), in index order. Counting uses rank keys
 // (key + 1, pads 0) against thr + 1, so pads are never above or equal to it.
@@ -777,24 +956,9 @@ __device__ inline uint64_t block_gt_eq(const Row& row, uint64_t vbase, uint32_t 
   return (uint64_t)tg | ((uint64_t)te << 32);
 }
 
-__global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c, uint32_t ncand_blocks)
+__global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c)
 {
   __shared__ uint32_t lds[8];
-  if (blockIdx.x < ncand_blocks) {
-    const uint32_t j = blockIdx.x / c.ncb, b = blockIdx.x - j * c.ncb;
-    const DevState& s = c.st[j];
-    if (s.fallback) return;
-    const uint64_t q0 = (uint64_t)b * kCBlk;
-    if (q0 >= s.cand) return;
-    uint32_t thr;
-    uint64_t need;
-    threshold_of(s, thr, need);
-    const uint64_t rem = (s.cand - q0 < (uint64_t)kCBlk) ? s.cand - q0 : (uint64_t)kCBlk;
-    const uint64_t r = block_gt_eq<kCBlkRounds>(Row{gptr(c.cand_val + c.desc[j].cand_off + q0), 0, rem}, 0, thr, lds);
-    if (threadIdx.x == 0) c.blk_cnt[(uint64_t)j * c.nbmax + b] = r;
-    return;
-  }
-  const uint32_t worker = blockIdx.x - ncand_blocks, G = gridDim.x - ncand_blocks;
   for (uint32_t j = 0; j < c.K; ++j) {
     const DevState& s = c.st[j];
     if (!s.fallback) continue;
@@ -802,40 +966,20 @@ __global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c, uint32_t ncand_block
     uint64_t need;
     threshold_of(s, thr, need);
     const Row row{gptr(c.desc[j].grad), c.desc[j].shift, c.n};
-    for (uint32_t blk = worker; blk < c.nfb; blk += G) {
+    for (uint32_t blk = blockIdx.x; blk < c.nfb; blk += gridDim.x) {
       const uint64_t r = block_gt_eq<kCBlkRounds>(row, (uint64_t)blk * kCBlk, thr, lds);
       if (threadIdx.x == 0) c.blk_cnt[(uint64_t)j * c.nbmax + blk] = r;
     }
   }
 }
 
-__device__ inline uint32_t blocks_of(const Ctx& c, const DevState& s)
-{
-  return s.fallback ? c.nfb : ceil_div_u64(s.cand, kCBlk);
-}
-
-// Exclusive prefix of the packed block counts of one device.
+// Exclusive prefix of the packed block counts of one exact-path device.
 __global__ __launch_bounds__(kBlock) void k_scan(Ctx c)
 {
   __shared__ uint64_t s_w[4];
-  const uint32_t j = blockIdx.x, tid = threadIdx.x;
-  const uint32_t nb = blocks_of(c, c.st[j]);
-  const uint64_t* cnt = c.blk_cnt + (uint64_t)j * c.nbmax;
-  uint64_t* pre = c.blk_pre + (uint64_t)j * c.nbmax;
-  const uint32_t per = (nb + kBlock - 1) / kBlock;
-  const uint32_t b0 = tid * per, b1 = (b0 + per < nb) ? b0 + per : nb;
-  uint64_t sum = 0;
-  for (uint32_t b = b0; b < b1; ++b) sum += cnt[b];
-  const uint64_t incl = wave_incl_scan_u64(sum);
-  if (lane_id() == 63) s_w[tid >> 6] = incl;
-  __syncthreads();
-  uint64_t base = 0;
-  for (uint32_t i = 0; i < (tid >> 6); ++i) base += s_w[i];
-  uint64_t run = base + incl - sum;
-  for (uint32_t b = b0; b < b1; ++b) {
-    pre[b] = run;
-    run += cnt[b];
-  }
+  const uint32_t j = blockIdx.x;
+  if (!c.st[j].fallback) return;
+  block_excl_scan_u64(c.blk_cnt + (uint64_t)j * c.nbmax, c.blk_pre + (uint64_t)j * c.nbmax, c.nfb, s_w);
 }
 
 // Writes the kept entries of one block in index order.
@@ -945,29 +1089,10 @@ __device__ inline double block_write(const Row& row, uint64_t vbase, const uint3
   return e2;
 }
 
-__global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c, uint32_t ncand_blocks)
+__global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c)
 {
   __shared__ uint32_t lds[8];
   __shared__ double s_e[4];
-  if (blockIdx.x < ncand_blocks) {
-    const uint32_t j = blockIdx.x / c.ncb, b = blockIdx.x - j * c.ncb;
-    const DevState& s = c.st[j];
-    if (s.fallback) return;
-    const uint64_t q0 = (uint64_t)b * kCBlk;
-    if (q0 >= s.cand) return;
-    uint32_t thr;
-    uint64_t need;
-    threshold_of(s, thr, need);
-    const DevDesc d = c.desc[j];
-    const uint64_t rem = (s.cand - q0 < (uint64_t)kCBlk) ? s.cand - q0 : (uint64_t)kCBlk;
-    const double e2 = block_write<kCBlkRounds>(Row{gptr(c.cand_val + d.cand_off + q0), 0, rem}, 0,
-                                               c.cand_idx + d.cand_off + q0, thr, need,
-                                               c.blk_pre[(uint64_t)j * c.nbmax + b], d.k, gptr(d.idx_out), gptr(d.val_out), lds);
-    const double es = block_sum_f64(e2, s_e);
-    if (threadIdx.x == 0) c.blk_e[(uint64_t)j * c.nbmax + b] = es;
-    return;
-  }
-  const uint32_t worker = blockIdx.x - ncand_blocks, G = gridDim.x - ncand_blocks;
   for (uint32_t j = 0; j < c.K; ++j) {
     const DevState& s = c.st[j];
     if (!s.fallback) continue;
@@ -976,7 +1101,7 @@ __global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c, uint32_t ncand_block
     threshold_of(s, thr, need);
     const DevDesc d = c.desc[j];
     const Row row{gptr(d.grad), d.shift, c.n};
-    for (uint32_t blk = worker; blk < c.nfb; blk += G) {
+    for (uint32_t blk = blockIdx.x; blk < c.nfb; blk += gridDim.x) {
       const double e2 = block_write<kCBlkRounds>(row, (uint64_t)blk * kCBlk, nullptr, thr, need,
                                                  c.blk_pre[(uint64_t)j * c.nbmax + blk], d.k, gptr(d.idx_out),
                                                  gptr(d.val_out), lds);
@@ -987,22 +1112,26 @@ __global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c, uint32_t ncand_block
   }
 }
 
-// ---- 5. energies of the adaptive rule and per-device decision --------------------------------
+// ---- 7. energies of the adaptive rule and per-device decision --------------------------------
 // §IV: send Top-k(g) when | ||g||^2 - ||Top-k(g)||^2 | / ||g||^2 <= delta.
 __global__ __launch_bounds__(kBlock) void k_final(Ctx c)
 {
   __shared__ double s_e[4];
   const uint32_t j = blockIdx.x;
   DevState& s = c.st[j];
-  const uint32_t nb = blocks_of(c, s);
+  const bool fast = !s.fallback;
+  const uint32_t nb = fast ? c.ngrp : c.nfb;
+  const double* ep = fast ? c.epart + (uint64_t)j * c.nslot : c.blk_e + (uint64_t)j * c.nbmax;
+  const uint64_t* pre = fast ? c.grp_pre + (uint64_t)j * c.ngrp : c.blk_pre + (uint64_t)j * c.nbmax;
+  const uint64_t* cnt = fast ? c.grp_cnt + (uint64_t)j * c.ngrp : c.blk_cnt + (uint64_t)j * c.nbmax;
   double acc = 0.0;
-  for (uint32_t b = threadIdx.x; b < nb; b += kBlock) acc += c.blk_e[(uint64_t)j * c.nbmax + b];
+  for (uint32_t b = threadIdx.x; b < nb; b += kBlock) acc += ep[b];
   const double e_kept = block_sum_f64(acc, s_e);
   if (threadIdx.x != 0) return;
   uint32_t thr;
   uint64_t need;
   if (!threshold_of(s, thr, need)) s.err |= 8u;
-  const uint64_t tot = c.blk_pre[(uint64_t)j * c.nbmax + nb - 1] + c.blk_cnt[(uint64_t)j * c.nbmax + nb - 1];
+  const uint64_t tot = pre[nb - 1] + cnt[nb - 1];
   s.thr = thr;
   s.c_gt = tot & 0xFFFFFFFFull;
   s.need = need;
@@ -1041,8 +1170,8 @@ hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, h
   k_post<<<c.K, kBlock, 0, s>>>(c);
   if (p.any_fast) {
     constexpr uint32_t kPerBlock = kGatherSlots * kWaves;
-    k_gather<<<c.K * ((c.nslot + kPerBlock - 1) / kPerBlock), kBlock, 0, s>>>(c);
     k_overflow<<<c.K * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
+    k_band<<<c.K * ((c.nslot + kPerBlock - 1) / kPerBlock), kBlock, 0, s>>>(c);
   }
   const uint32_t g = p.ncand_blocks + p.full_workers;
   for (int pass = 0; pass < 3; ++pass) {
@@ -1050,9 +1179,17 @@ hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, h
     k_find<<<c.K, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1);
   }
   if (ev) (void)hipEventRecord(ev[3], s);
-  k_count_cf<<<g, kBlock, 0, s>>>(c, p.ncand_blocks);
-  k_scan<<<c.K, kBlock, 0, s>>>(c);
-  k_write_cf<<<g, kBlock, 0, s>>>(c, p.ncand_blocks);
+  if (p.any_fast) {
+    const uint32_t gb = c.K * ((c.ngrp + kWaves - 1) / kWaves);
+    k_grp_count<<<gb, kBlock, 0, s>>>(c);
+    k_grp_scan<<<c.K, kBlock, 0, s>>>(c);
+    k_write_fast<<<gb, kBlock, 0, s>>>(c);
+  }
+  if (p.full_workers) {
+    k_count_cf<<<p.full_workers, kBlock, 0, s>>>(c);
+    k_scan<<<c.K, kBlock, 0, s>>>(c);
+    k_write_cf<<<p.full_workers, kBlock, 0, s>>>(c);
+  }
   k_final<<<c.K, kBlock, 0, s>>>(c);
   if (ev) (void)hipEventRecord(ev[4], s);
   return hipGetLastError();
