@@ -177,7 +177,12 @@ const char* scadles_last_error(void);
  *                       runs the exact multi-pass radix select.
  *   "force_fallback" 1: the sampled path runs but its result is discarded as
  *                       if the bracket had missed, exercising the fallback.
- * Returns SCADLES_EINVAL for an unknown name.                               */
+ *   "parts"          1..4 (default 2): device groups whose selections are
+ *                       pipelined in scadles_step_fused (group i's main pass
+ *                       overlaps the end of group i-1's selection, which runs
+ *                       on a second stream the library creates per GPU, at the
+ *                       default priority). Results do not depend on it.
+ * Returns SCADLES_EINVAL for an unknown name or a value out of range.       */
 scadles_status scadles_set_option(const char* name, int64_t value);
 
 /* Stage timing. While enabled, every scadles_topk_select / scadles_step_fused
@@ -186,9 +191,10 @@ scadles_status scadles_set_option(const char* name, int64_t value);
  * milliseconds of each stage to stage_ms (host[SCADLES_PROFILE_STAGES]) and
  * the number of calls recorded to *calls, and clears the record.
  * Stages: 0 bracket (sampling), 1 main select pass (one read of every
- * gradient), 2 exact threshold (radix passes over the candidates, or over
- * the full data on the exact path), 3 ordered compaction and energies,
- * 4 weighted aggregation (+SGD; empty for scadles_topk_select).              */
+ * gradient; the sum over the device groups), 2 the rest of the selection
+ * after the last main pass (exact threshold, ordered compaction, energies;
+ * earlier groups' share overlaps the main passes), 3 weighted aggregation
+ * (+SGD; empty for scadles_topk_select), 4 the whole call.                  */
 #define SCADLES_PROFILE_STAGES 5
 scadles_status scadles_profile_enable(int on);
 scadles_status scadles_profile_read(double* stage_ms, uint32_t* calls);

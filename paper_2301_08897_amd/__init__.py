@@ -32,7 +32,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 
 MAX_DEVICES = 64
 PROFILE_STAGES = 5
-STAGE_NAMES = ("bracket", "main_select", "threshold", "compaction", "aggregate")
+STAGE_NAMES = ("bracket", "main_select", "post_select", "aggregate", "total")
 
 _vp = ctypes.c_void_p
 _u64 = ctypes.c_uint64

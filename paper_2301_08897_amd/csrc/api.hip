@@ -20,7 +20,7 @@ using namespace scadles;
 namespace {
 
 thread_local std::string g_err;
-std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0};
+std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0}, g_parts{2};
 
 scadles_status fail(scadles_status st, const char* fmt, ...)
 {
@@ -39,22 +39,55 @@ scadles_status hip_fail(hipError_t e, const char* where)
 }
 
 // ---- stage profiling ------------------------------------------------------------------------
+// Per call: 0 start, 1 bracket done, 2 + 2i / 3 + 2i around main-pass group i,
+// 2 + 2P selection done, 3 + 2P call done (P = groups of that call).
 constexpr int kStages = SCADLES_PROFILE_STAGES;
+constexpr int kProfEv = 4 + 2 * (int)kMaxParts;
 constexpr int kProfMax = 4096;
 std::mutex g_prof_mu;
 bool g_prof_on = false;
 struct ProfRec {
-  hipEvent_t ev[kStages + 1];
+  hipEvent_t ev[kProfEv];
+  uint32_t parts;
 };
 std::vector<ProfRec> g_prof_pool;
 size_t g_prof_used = 0;
 
-// Returns kStages + 1 events to record into, or null when profiling is off or full.
-hipEvent_t* prof_slot()
+// A record to fill, or null when profiling is off or full.
+ProfRec* prof_slot()
 {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   if (!g_prof_on || g_prof_used >= g_prof_pool.size()) return nullptr;
-  return g_prof_pool[g_prof_used++].ev;
+  return &g_prof_pool[g_prof_used++];
+}
+
+// ---- the second stream of the pipelined selection, per GPU ---------------------------------
+struct StreamSet {
+  bool ready = false;
+  hipStream_t s2 = nullptr;
+  hipEvent_t fork[kMaxParts] = {};
+  hipEvent_t join = nullptr;
+  std::mutex launch_mu;      // one call's launch sequence at a time (the events are shared)
+};
+constexpr int kMaxGpus = 64;
+StreamSet g_streams[kMaxGpus];
+std::mutex g_streams_mu;
+
+// The calling thread's current GPU's set, created on first use (default priority).
+StreamSet* stream_set()
+{
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxGpus) return nullptr;
+  std::lock_guard<std::mutex> lk(g_streams_mu);
+  StreamSet& ss = g_streams[dev];
+  if (!ss.ready) {
+    if (hipStreamCreateWithFlags(&ss.s2, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    for (auto& e : ss.fork)
+      if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess) return nullptr;
+    ss.ready = true;
+  }
+  return &ss;
 }
 
 // ---- layout ---------------------------------------------------------------------------------
@@ -68,7 +101,7 @@ struct Layout {
   uint64_t n = 0;
   uint32_t k[kMaxK], cap[kMaxK], mode[kMaxK], r_lo[kMaxK], r_hi[kMaxK];
   uint32_t any_fast = 0;
-  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_ctot, o_coff, o_ce, o_olist, o_slot, o_epart, o_cidx, o_cval, o_band, o_gcnt, o_gpre, o_bcnt, o_bpre, o_be, o_rbeg,
+  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_ctot, o_coff, o_ce, o_olist, o_slot, o_epart, o_cidx, o_cval, o_band, o_gcnt, o_gpre, o_bcnt, o_bpre, o_be, o_fb, o_rbeg,
       o_rend, o_aerr;
   size_t total = 0;
 };
@@ -108,7 +141,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
   L.n = n;
   // Tiles cover the 16-byte-aligned virtual row [0, n + shift), shift <= 3.
   L.tpd = ceil_div_u64(n + 3, kTile);
-  L.nslot = L.tpd * kWaves;
+  L.nslot = L.tpd;
   L.ngrp = ceil_div_u64(L.nslot, kGatherSlots);
   L.nrange = ceil_div_u64(n, kARange);
   sample_geometry(n, L.s_stride, L.s_n);
@@ -165,7 +198,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
     L.o_coff = take(sizeof(uint64_t) * (size_t)K * kMaxChunks);
     L.o_ce = take(sizeof(double) * (size_t)K * kMaxChunks);
     L.o_olist = take(sizeof(uint32_t) * (size_t)K * L.nslot);
-    L.o_slot = take(sizeof(uint64_t) * nslots * kWaveCap);
+    L.o_slot = take(sizeof(uint64_t) * nslots * kSlotCap);
     L.o_epart = take(sizeof(double) * (size_t)K * L.nslot);
     L.o_cidx = take(sizeof(uint32_t) * sum_cap);
     L.o_cval = take(sizeof(float) * sum_cap);
@@ -175,6 +208,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
     L.o_bcnt = take(sizeof(uint64_t) * (size_t)K * L.nbmax);
     L.o_bpre = take(sizeof(uint64_t) * (size_t)K * L.nbmax);
     L.o_be = take(sizeof(double) * (size_t)K * L.nbmax);
+    L.o_fb = take(sizeof(uint32_t));
   }
   L.o_rbeg = take(sizeof(uint32_t) * (size_t)K * L.nrange);
   L.o_rend = take(sizeof(uint32_t) * (size_t)K * L.nrange);
@@ -207,6 +241,7 @@ Ctx make_ctx(const Layout& L, void* ws)
   c.blk_cnt = reinterpret_cast<uint64_t*>(b + L.o_bcnt);
   c.blk_pre = reinterpret_cast<uint64_t*>(b + L.o_bpre);
   c.blk_e = reinterpret_cast<double*>(b + L.o_be);
+  c.fb_count = reinterpret_cast<uint32_t*>(b + L.o_fb);
   c.n = L.n;
   c.K = L.K;
   c.tpd = L.tpd;
@@ -249,8 +284,18 @@ scadles_status check_weights(const float* w, uint32_t K)
   return SCADLES_OK;
 }
 
+// Number of pipelined device groups for a call (option "parts", at most K).
+uint32_t parts_for(const Layout& L)
+{
+  int p = g_parts.load();
+  if (p < 1) p = 1;
+  if (p > (int)kMaxParts) p = (int)kMaxParts;
+  if ((uint32_t)p > L.K) p = (int)L.K;
+  return (uint32_t)p;
+}
+
 scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double delta, double* energies,
-                          uint8_t* compressed, hipStream_t s, hipEvent_t* ev)
+                          uint8_t* compressed, hipStream_t s, ProfRec* pr)
 {
   Ctx c = make_ctx(L, ws);
   c.delta = delta;
@@ -260,10 +305,19 @@ scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double d
   SelectPlan p;
   p.any_fast = L.any_fast;
   p.sample_blocks = ceil_div_u64(L.s_n, kSBlk);
-  p.ncand_blocks = L.any_fast ? L.K * L.ncb : 0u;
   const uint64_t tiles = (uint64_t)L.K * L.tpd;
   p.full_workers = (uint32_t)(tiles < (uint64_t)kFullWorkers ? tiles : (uint64_t)kFullWorkers);
-  hipError_t e = launch_select(c, a, p, s, ev);
+  p.parts = parts_for(L);
+  if (pr) pr->parts = p.parts;
+  StreamSet* ss = p.parts > 1 ? stream_set() : nullptr;
+  if (p.parts > 1 && !ss) return fail(SCADLES_EHIP, "could not create the pipeline stream");
+  hipError_t e;
+  if (ss) {
+    std::lock_guard<std::mutex> lk(ss->launch_mu);
+    e = launch_select(c, a, p, s, ss->s2, ss->fork, ss->join, pr ? pr->ev : nullptr);
+  } else {
+    e = launch_select(c, a, p, s, nullptr, nullptr, nullptr, pr ? pr->ev : nullptr);
+  }
   if (e != hipSuccess) return hip_fail(e, "select launch");
   return SCADLES_OK;
 }
@@ -317,10 +371,10 @@ scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio, 
   a.r_lo[0] = L.r_lo[0];
   a.r_hi[0] = L.r_hi[0];
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipEvent_t* ev = prof_slot();
-  if (ev) (void)hipEventRecord(ev[0], s);
-  scadles_status st = run_select(L, a, ws, INFINITY, energies, nullptr, s, ev);
-  if (ev) (void)hipEventRecord(ev[5], s);
+  ProfRec* pr = prof_slot();
+  if (pr) (void)hipEventRecord(pr->ev[0], s);
+  scadles_status st = run_select(L, a, ws, INFINITY, energies, nullptr, s, pr);
+  if (pr) (void)hipEventRecord(pr->ev[3 + 2 * pr->parts], s);
   return st;
 }
 
@@ -445,9 +499,9 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
     if (L.k[j] > kmax) kmax = L.k[j];
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipEvent_t* ev = prof_slot();
-  if (ev) (void)hipEventRecord(ev[0], s);
-  if (scadles_status st = run_select(L, a, ws, delta, energies, compressed, s, ev)) return st;
+  ProfRec* pr = prof_slot();
+  if (pr) (void)hipEventRecord(pr->ev[0], s);
+  if (scadles_status st = run_select(L, a, ws, delta, energies, compressed, s, pr)) return st;
   char* b = static_cast<char*>(ws);
   AggCtx c;
   memset(&c, 0, sizeof(c));
@@ -463,7 +517,7 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
   c.kmax = (uint32_t)kmax;
   c.n = n;
   hipError_t e = launch_aggregate(g, c, 0, s);
-  if (ev) (void)hipEventRecord(ev[5], s);
+  if (pr) (void)hipEventRecord(pr->ev[3 + 2 * pr->parts], s);
   if (e != hipSuccess) return hip_fail(e, "aggregate launch");
   return SCADLES_OK;
 }
@@ -499,6 +553,10 @@ scadles_status scadles_set_option(const char* name, int64_t value)
   if (!strcmp(name, "validate")) g_validate = value ? 1 : 0;
   else if (!strcmp(name, "force_exact")) g_force_exact = value ? 1 : 0;
   else if (!strcmp(name, "force_fallback")) g_force_fallback = value ? 1 : 0;
+  else if (!strcmp(name, "parts")) {
+    if (value < 1 || value > (int64_t)kMaxParts) return fail(SCADLES_EINVAL, "parts must be in [1, %u]", kMaxParts);
+    g_parts = (int)value;
+  }
   else return fail(SCADLES_EINVAL, "unknown option '%s'", name);
   return SCADLES_OK;
 }
@@ -525,13 +583,19 @@ scadles_status scadles_profile_read(double* stage_ms, uint32_t* calls)
   if (!stage_ms || !calls) return fail(SCADLES_EINVAL, "NULL argument");
   std::lock_guard<std::mutex> lk(g_prof_mu);
   for (int i = 0; i < kStages; ++i) stage_ms[i] = 0.0;
+  auto span = [](hipEvent_t a, hipEvent_t b) {
+    float ms = 0.f;
+    return hipEventElapsedTime(&ms, a, b) == hipSuccess ? (double)ms : 0.0;
+  };
   for (size_t r = 0; r < g_prof_used; ++r) {
-    hipEvent_t* ev = g_prof_pool[r].ev;
-    if (hipEventSynchronize(ev[kStages]) != hipSuccess) return fail(SCADLES_EHIP, "hipEventSynchronize failed");
-    for (int i = 0; i < kStages; ++i) {
-      float ms = 0.f;
-      if (hipEventElapsedTime(&ms, ev[i], ev[i + 1]) == hipSuccess) stage_ms[i] += ms;
-    }
+    const ProfRec& pr = g_prof_pool[r];
+    const uint32_t P = pr.parts;
+    if (hipEventSynchronize(pr.ev[3 + 2 * P]) != hipSuccess) return fail(SCADLES_EHIP, "hipEventSynchronize failed");
+    stage_ms[0] += span(pr.ev[0], pr.ev[1]);
+    for (uint32_t i = 0; i < P; ++i) stage_ms[1] += span(pr.ev[2 + 2 * i], pr.ev[3 + 2 * i]);
+    stage_ms[2] += span(pr.ev[3 + 2 * (P - 1)], pr.ev[2 + 2 * P]);
+    stage_ms[3] += span(pr.ev[2 + 2 * P], pr.ev[3 + 2 * P]);
+    stage_ms[4] += span(pr.ev[0], pr.ev[3 + 2 * P]);
   }
   *calls = (uint32_t)g_prof_used;
   g_prof_used = 0;

@@ -30,9 +30,10 @@ constexpr uint32_t kKeyMask = 0x7FFFFFFFu;
 constexpr uint64_t kSat31 = 0x7FFFFFFFull;
 constexpr int kFullWorkers = 1024;     // grid of the grid-stride exact-path kernels
 constexpr int kWaveCap = 512;          // main pass: candidates one wave chunk (4096 elements) can stage
+constexpr int kSlotCap = kWaves * kWaveCap;   // entries of one tile's slot region
 constexpr int kScanChunk = 4096;       // slots per workgroup of the slot-offset scan
 constexpr int kMaxChunks = 256;        // >= ceil(nslot / kScanChunk) for n < 2^32
-constexpr int kGatherSlots = 8;        // slots per wave in the selection-list and output passes
+constexpr int kGatherSlots = 2;        // tiles per wave in the selection-list and output passes
 constexpr int kOverflowBlocks = 32;    // workgroups per device re-scanning overflowed slots
 
 enum : uint32_t { kModeFast = 0, kModeExact = 1 };
@@ -86,14 +87,14 @@ struct Ctx {
   DevDesc* desc;
   DevState* st;
   uint32_t* hist;         // [K][kSlots][kBins]
-  uint32_t* slot_cnt;     // [K][nslot] per-wave candidate | sure << 16 counts of the main pass
+  uint32_t* slot_cnt;     // [K][nslot] per tile: candidates | overflowed << 15 | sure << 16
   uint64_t* slot_off;     // [K][nslot] candidate | sure << 32 counts before each slot within its scan chunk
   uint64_t* chunk_tot;    // [K][kMaxChunks] candidate | sure << 32 totals of each scan chunk
   uint64_t* chunk_off;    // [K][kMaxChunks] candidate | sure << 32 counts before each scan chunk
   double* chunk_e;        // [K][kMaxChunks] sum of squares of each scan chunk
-  uint64_t* slot;         // [K][nslot][kWaveCap] staged candidates per wave chunk: index | value bits << 32
-  uint32_t* ovf_list;     // [K][nslot] slots whose wave found more than kWaveCap candidates
-  double* epart;          // [K][nslot] sum of squares per main-pass wave chunk
+  uint64_t* slot;         // [K][nslot][kSlotCap] staged candidates per tile: index | value bits << 32
+  uint32_t* ovf_list;     // [K][nslot] tiles with a wave chunk of more than kWaveCap candidates
+  double* epart;          // [K][nslot] sum of squares per tile, later kept sum of squares per write group
   uint32_t* cand_idx;     // candidate regions (entries of overflowed slots only)
   float* cand_val;
   uint32_t* band;         // selection lists: keys in the selection interval, per device at cand_off
@@ -107,7 +108,7 @@ struct Ctx {
   uint64_t n;
   uint32_t K;
   uint32_t tpd;           // main tiles per device: ceil((n + 3) / kTile)
-  uint32_t nslot;         // main-pass wave chunks per device: tpd * kWaves
+  uint32_t nslot;         // slots (main-pass tiles) per device: tpd
   uint32_t ngrp;          // write groups per device: ceil(nslot / kGatherSlots)
   uint32_t ncb;           // candidate blocks per device (max over devices)
   uint32_t nfb;           // exact-path blocks per device: ceil((n + 3) / kCBlk)
@@ -115,6 +116,8 @@ struct Ctx {
   uint32_t s_stride;      // sample chunk stride (elements)
   uint32_t s_n;           // sample elements per device
   uint32_t force_fallback;
+  uint32_t j0, jn;        // devices [j0, j0 + jn) of this launch (the per-device kernels)
+  uint32_t* fb_count;     // devices on the exact path (the exact-path kernels exit early at 0)
   double delta;
 };
 
@@ -159,16 +162,19 @@ struct AggCtx {
 };
 
 // Launch plan of the selection pipeline (host side).
+constexpr uint32_t kMaxParts = 4;      // device groups whose main passes are pipelined
 struct SelectPlan {
   uint32_t any_fast;          // some device takes the sampled single-read path
   uint32_t sample_blocks;     // sample workgroups per device
-  uint32_t ncand_blocks;      // K * ncb candidate workgroups, or 0
   uint32_t full_workers;      // grid-stride workgroups of the exact full-data path
+  uint32_t parts;             // device groups, 1 .. kMaxParts
 };
 
-// Launchers (select.hip, aggregate.hip). `ev`, when not null, receives events
-// at the stage boundaries 1..4 of the selection.
-hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipEvent_t* ev);
+// Launchers (select.hip, aggregate.hip). fork[parts - 1] and join are events of
+// the caller's second stream s2; `ev`, when not null, receives the profiling
+// events described at launch_select.
+hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipStream_t s2,
+                         hipEvent_t* fork, hipEvent_t join, hipEvent_t* ev);
 hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate, hipStream_t s);
 hipError_t launch_sgd(float* p, const float* g, uint64_t n, float lr, hipStream_t s);
 

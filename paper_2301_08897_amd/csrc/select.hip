@@ -198,6 +198,7 @@ __global__ __launch_bounds__(kBlock) void k_prep(Ctx c, PrepArgs a)
     }
     c.st[j] = s;
   }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *c.fb_count = 0u;
   const uint64_t nh = (uint64_t)K * kSlots * kBins;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
   for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < nh; i += stride) c.hist[i] = 0u;
@@ -243,7 +244,7 @@ __global__ __launch_bounds__(kBlock) void k_hist_sample(Ctx c)
 // ---- radix digit decision for slots [s0, s1) of one device (one wave) -----------------------
 __global__ __launch_bounds__(64) void k_find(Ctx c, int s_begin, int s_end)
 {
-  const uint32_t j = blockIdx.x, l = lane_id();
+  const uint32_t j = c.j0 + blockIdx.x, l = lane_id();
   for (int s = s_begin; s < s_end; ++s) {
     Sel sel = c.st[j].sel[s];
     if (!sel.active) continue;
@@ -337,11 +338,11 @@ __device__ inline uint32_t wave_prefix_of_block(uint32_t packed_lane, uint32_t* 
 // rank keys (key + 1, pads 0) and fmax drops the pads' NaN from the squares.
 // Counts are wave totals from ballots (scalar popcounts).
 // A staged candidate: its index in the low word, its value's bits in the high word.
-// Entry e of slot s lives at ((rot(s) + e) mod kWaveCap) of the slot's region:
+// Entry e of slot s lives at ((rot(s) + e) mod kSlotCap) of the slot's region:
 // the rotation spreads the (short) written part of the regions over all
 // address bits below the region size, so the writes use every memory channel.
-static_assert((kWaveCap & (kWaveCap - 1)) == 0, "slot rotation needs a power-of-two region");
-__device__ inline uint32_t slot_rot(uint64_t slot) { return (uint32_t)(slot * 53u) & (kWaveCap - 1u); }
+static_assert((kSlotCap & (kSlotCap - 1)) == 0, "slot rotation needs a power-of-two region");
+__device__ inline uint32_t slot_rot(uint64_t slot) { return (uint32_t)(slot * 211u) & (kSlotCap - 1u); }
 
 __device__ inline uint64_t pack_cand(uint32_t i, float v) { return (uint64_t)i | ((uint64_t)__float_as_uint(v) << 32); }
 
@@ -378,15 +379,15 @@ __device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32
 
 // Each workgroup reads one tile of kTile gradient elements (workgroup b: device
 // b / tpd, tile b % tpd). Wave w owns elements [w*4096, (w+1)*4096) of the tile
-// and slot tile*kWaves + w of its device. A wave that finds more than kWaveCap
-// candidates leaves its slot empty and records the slot for k_overflow. The
-// gradient pointers come as kernel arguments so that the tile's loads issue
-// before anything is read from the workspace; waves never wait on each other.
+// and stages its candidates in LDS; the tile's slot is written at the end (the
+// only barrier). The gradient pointers come as kernel arguments so that the
+// tile's loads issue before anything is read from the workspace.
 __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
 {
   __shared__ uint64_t s_c[kWaves][kWaveCap];
   const uint32_t l = lane_id(), w = threadIdx.x >> 6;
-  const uint32_t j = blockIdx.x / c.tpd, tile = blockIdx.x - j * c.tpd;
+  const uint32_t jr = blockIdx.x / c.tpd, tile = blockIdx.x - jr * c.tpd;
+  const uint32_t j = c.j0 + jr;
   const float* grad = ga.grad[j];
   const uint64_t shift = (reinterpret_cast<uintptr_t>(grad) >> 2) & 3u;
   const uint64_t vbase = (uint64_t)tile * kTile;      // virtual position of the tile
@@ -418,23 +419,42 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
     for (int r = 0; r < kTileRounds; ++r)
       main_stage<true>(load4(row, vbase + wv0 + r * 256, false), i_base + r * 256, tlo, thi, e2, wc, ws, s_c[w]);
   }
-  // The wave's slot (its own LDS region, written by itself: no barrier needed).
-  const uint64_t slot = (uint64_t)j * c.nslot + (uint64_t)tile * kWaves + w;
+  // The tile's slot: the waves' staged candidates one after the other (index
+  // order), one contiguous rotated run; its counts and sum of squares. A tile
+  // with a wave chunk over kWaveCap candidates stages nothing and is recorded
+  // for k_overflow, which re-scans it once the slot offsets are known.
+  __shared__ uint32_t s_cnt[kWaves];
+  __shared__ double s_e[kWaves];
   const double es = wave_sum_f64(e2[0] + e2[1]);
   if (l == 0) {
-    c.slot_cnt[slot] = wc | (ws << 16);
-    c.epart[slot] = es;
+    s_cnt[w] = wc | (ws << 16);
+    s_e[w] = es;
   }
-  if (wc <= (uint32_t)kWaveCap) {
+  __syncthreads();
+  uint32_t cand = 0, sure = 0, before = 0;
+  bool ovf = false;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) {
+    const uint32_t v = s_cnt[i];
+    if ((uint32_t)i < w) before += v & 0xFFFFu;
+    cand += v & 0xFFFFu;
+    sure += v >> 16;
+    ovf |= (v & 0xFFFFu) > (uint32_t)kWaveCap;
+  }
+  const uint64_t slot = (uint64_t)j * c.nslot + tile;
+  if (threadIdx.x == 0) {
+    c.slot_cnt[slot] = cand | (ovf ? 0x8000u : 0u) | (sure << 16);
+    c.epart[slot] = (s_e[0] + s_e[1]) + (s_e[2] + s_e[3]);
+    if (ovf) {
+      const uint32_t i = atomicAdd(&c.st[j].ovf_n, 1u);
+      c.ovf_list[(uint64_t)j * c.nslot + i] = tile;
+    }
+  }
+  if (!ovf) {
     // Nontemporal: the slots are read only after the whole pass (selection list, output).
-    GLOBAL uint64_t* sp = gptr(c.slot + slot * kWaveCap);
-    const uint32_t rot = slot_rot(slot);
-    for (uint32_t i = l; i < wc; i += 64) __builtin_nontemporal_store(s_c[w][i], sp + ((rot + i) & (kWaveCap - 1u)));
-  } else if (l == 0) {
-    // Dense-candidate chunk (rare): record it; k_overflow re-scans it once the
-    // slot offsets are known. One atomic per such wave.
-    const uint32_t i = atomicAdd(&c.st[j].ovf_n, 1u);
-    c.ovf_list[(uint64_t)j * c.nslot + i] = tile * kWaves + w;
+    GLOBAL uint64_t* sp = gptr(c.slot + slot * kSlotCap);
+    const uint32_t rot = slot_rot(slot) + before;
+    for (uint32_t i = l; i < wc; i += 64) __builtin_nontemporal_store(s_c[w][i], sp + ((rot + i) & (kSlotCap - 1u)));
   }
 }
 
@@ -457,7 +477,8 @@ __global__ __launch_bounds__(kBlock) void k_slot_scan(Ctx c)
 {
   __shared__ uint64_t s_w[4];
   const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
-  const uint32_t j = blockIdx.x / nchunk, ch = blockIdx.x - j * nchunk;
+  const uint32_t jr = blockIdx.x / nchunk, ch = blockIdx.x - jr * nchunk;
+  const uint32_t j = c.j0 + jr;
   if (c.desc[j].mode != kModeFast) return;
   const uint32_t tid = threadIdx.x;
   const uint32_t s0 = ch * kScanChunk + tid * 16;
@@ -478,7 +499,7 @@ __global__ __launch_bounds__(kBlock) void k_slot_scan(Ctx c)
   }
   uint64_t sum = 0;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) sum += (uint64_t)(v[i] & 0xFFFFu) | ((uint64_t)(v[i] >> 16) << 32);
+  for (int i = 0; i < 16; ++i) sum += (uint64_t)(v[i] & 0x7FFFu) | ((uint64_t)(v[i] >> 16) << 32);
   const uint64_t incl = wave_incl_scan_u64(sum);
   if (lane_id() == 63) s_w[tid >> 6] = incl;
   __syncthreads();
@@ -489,7 +510,7 @@ __global__ __launch_bounds__(kBlock) void k_slot_scan(Ctx c)
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     if (s0 + i < c.nslot) off[s0 + i] = oc;
-    oc += (uint64_t)(v[i] & 0xFFFFu) | ((uint64_t)(v[i] >> 16) << 32);
+    oc += (uint64_t)(v[i] & 0x7FFFu) | ((uint64_t)(v[i] >> 16) << 32);
   }
   if (tid == kBlock - 1) c.chunk_tot[(uint64_t)j * kMaxChunks + ch] = run + sum;
 }
@@ -500,7 +521,8 @@ __global__ __launch_bounds__(kBlock) void k_energy_chunks(Ctx c)
 {
   __shared__ double s_e[4];
   const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
-  const uint32_t j = blockIdx.x / nchunk, ch = blockIdx.x - j * nchunk;
+  const uint32_t jr = blockIdx.x / nchunk, ch = blockIdx.x - jr * nchunk;
+  const uint32_t j = c.j0 + jr;
   const uint32_t s0 = ch * kScanChunk + threadIdx.x * 16;
   const double* ep = c.epart + (uint64_t)j * c.nslot;
   double a = 0.0;
@@ -516,7 +538,7 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
 {
   __shared__ double s_e[4];
   __shared__ uint64_t s_w[4];
-  const uint32_t j = blockIdx.x, tid = threadIdx.x;
+  const uint32_t j = c.j0 + blockIdx.x, tid = threadIdx.x;
   const uint32_t nch = (c.nslot + kScanChunk - 1) / kScanChunk;    // <= kMaxChunks = kBlock
   const double e_all = block_sum_f64(tid < nch ? c.chunk_e[(uint64_t)j * kMaxChunks + tid] : 0.0, s_e);
   const DevDesc d = c.desc[j];
@@ -554,6 +576,7 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
   s.sel_n = 0;
   if (fb) {
     s.fallback = 1;
+    atomicAdd(c.fb_count, 1u);
     sel.lo = 0;
     sel.hi = kKeyInf;
     sel.bits = 31;
@@ -604,12 +627,12 @@ struct SlotSrc {
   const GLOBAL float* cv;
 };
 
-__device__ inline SlotSrc slot_src(const Ctx& c, uint32_t j, uint32_t s, uint32_t cn, uint32_t cand_at)
+__device__ inline SlotSrc slot_src(const Ctx& c, uint32_t j, uint32_t s, uint32_t ovf, uint32_t cand_at)
 {
   SlotSrc r;
-  if (cn <= (uint32_t)kWaveCap) {
+  if (!ovf) {
     const uint64_t slot = (uint64_t)j * c.nslot + s;
-    r.pairs = gptr(c.slot) + slot * kWaveCap;
+    r.pairs = gptr(c.slot) + slot * kSlotCap;
     r.rot = slot_rot(slot);
     r.ci = nullptr;
     r.cv = nullptr;
@@ -625,93 +648,135 @@ __device__ inline SlotSrc slot_src(const Ctx& c, uint32_t j, uint32_t s, uint32_
 
 __device__ inline uint64_t slot_entry(const SlotSrc& r, uint32_t e)
 {
-  if (r.pairs) return r.pairs[(r.rot + e) & (kWaveCap - 1u)];
+  if (r.pairs) return r.pairs[(r.rot + e) & (kSlotCap - 1u)];
   return (uint64_t)r.ci[e] | ((uint64_t)__float_as_uint(r.cv[e]) << 32);
 }
 
 __device__ inline uint32_t entry_key(uint64_t p) { return (uint32_t)(p >> 32) & kKeyMask; }
 
+// Walks the entries of tiles s0 .. s0 + kGatherSlots - 1 of device j in index
+// order, 64 at a time: begin(i, pre) opens tile s0 + i (pre: its candidate |
+// sure << 32 offsets), visit(p, valid) takes one 64-entry window. The tiles'
+// counts and the first kPre windows of every tile are loaded at once, without
+// conditions (a slot region always holds kSlotCap entries and tile indices are
+// clamped, so every load is in bounds; entries past a tile's count are
+// ignored). Overflowed tiles, whose entries are in the candidate list, reload
+// them once their offset is known.
+constexpr int kPre = 4;
+
+template <class Begin, class Visit>
+__device__ inline void walk_tiles(const Ctx& c, uint32_t j, uint32_t s0, Begin begin, Visit visit)
+{
+  const uint32_t l = lane_id();
+  const uint32_t last = c.nslot - 1;
+  const uint32_t sl0 = s0 + (l < (uint32_t)kGatherSlots ? l : (uint32_t)kGatherSlots - 1u);
+  const uint32_t sl = sl0 < last ? sl0 : last;
+  const uint32_t m_v = c.slot_cnt[(uint64_t)j * c.nslot + sl];
+  const uint64_t m_pre = c.chunk_off[(uint64_t)j * kMaxChunks + sl / kScanChunk] + c.slot_off[(uint64_t)j * c.nslot + sl];
+  uint64_t r[kGatherSlots][kPre];
+#pragma unroll
+  for (int i = 0; i < kGatherSlots; ++i) {
+    const uint64_t slot = (uint64_t)j * c.nslot + (s0 + i < last ? s0 + i : last);
+    const GLOBAL uint64_t* base = gptr(c.slot) + slot * kSlotCap;
+    const uint32_t rot = slot_rot(slot);
+#pragma unroll
+    for (int m = 0; m < kPre; ++m) r[i][m] = base[(rot + m * 64 + l) & (kSlotCap - 1u)];
+  }
+#pragma unroll
+  for (int i = 0; i < kGatherSlots; ++i) {
+    const uint32_t v = __builtin_amdgcn_readlane(m_v, i);
+    const uint32_t cn = s0 + i < c.nslot ? v & 0x7FFFu : 0u;
+    const uint32_t ovf = (v >> 15) & 1u;
+    const uint64_t pre = ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(m_pre >> 32), i) << 32) |
+                         __builtin_amdgcn_readlane((uint32_t)m_pre, i);
+    if (cn && ovf) {
+      const SlotSrc src = slot_src(c, j, s0 + i, 1u, (uint32_t)pre);
+#pragma unroll
+      for (int m = 0; m < kPre; ++m) r[i][m] = m * 64 + l < cn ? slot_entry(src, m * 64 + l) : 0ull;
+    }
+    begin(i, pre);
+#pragma unroll
+    for (int m = 0; m < kPre; ++m) {
+      if ((uint32_t)m * 64 >= cn) break;
+      visit(r[i][m], m * 64 + l < cn);
+    }
+    if (cn > (uint32_t)(kPre * 64)) {
+      const SlotSrc src = slot_src(c, j, s0 + i, ovf, (uint32_t)pre);
+      for (uint32_t e0 = kPre * 64; e0 < cn; e0 += 64) {
+        const bool valid = e0 + l < cn;
+        visit(valid ? slot_entry(src, e0 + l) : 0ull, valid);
+      }
+    }
+  }
+}
+
 // ---- 3. selection list ----------------------------------------------------------------------
-// Each wave takes kGatherSlots consecutive slots and writes the keys of their
+// Each wave takes kGatherSlots consecutive tiles and writes the keys of their
 // entries in the selection interval [sel.lo, sel.hi) to the device's selection
-// list, slot after slot (the slot counts give every slot's offset). The
+// list, tile after tile (the slot counts give every tile's offset). The
 // threshold is then radix-selected over this short list only.
 // Occupancy 8 (at most 64 VGPRs): these passes are bound by memory latency.
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_band(Ctx c)
 {
   constexpr uint32_t kPerBlock = kGatherSlots * kWaves;
   const uint32_t groups = (c.nslot + kPerBlock - 1) / kPerBlock;
-  const uint32_t j = blockIdx.x / groups, g = blockIdx.x - j * groups;
+  const uint32_t jr = blockIdx.x / groups, g = blockIdx.x - jr * groups;
+  const uint32_t j = c.j0 + jr;
   const DevState& st = c.st[j];
   if (st.fallback) return;
-  const uint32_t l = lane_id(), w = threadIdx.x >> 6;
-  const uint32_t s0 = g * kPerBlock + w * kGatherSlots;
+  const uint32_t s0 = g * kPerBlock + (threadIdx.x >> 6) * kGatherSlots;
   if (s0 >= c.nslot) return;
   const uint32_t lo = st.sel[kSlotCand].lo, hi = st.sel[kSlotCand].hi, band_low = st.band_low;
   const uint64_t cap = c.desc[j].cap;
   GLOBAL uint32_t* band = gptr(c.band + c.desc[j].cand_off);
-  // lane i < kGatherSlots: count and candidate offsets of slot s0 + i
-  uint32_t m_cnt = 0;
-  uint64_t m_pre = 0;
-  if (l < (uint32_t)kGatherSlots && s0 + l < c.nslot) {
-    m_cnt = c.slot_cnt[(uint64_t)j * c.nslot + s0 + l] & 0xFFFFu;
-    m_pre = slot_pre(c, j, s0 + l);
-  }
-  // first 64 entries of every slot in flight before any store
-  uint64_t r[kGatherSlots];
-#pragma unroll
-  for (int i = 0; i < kGatherSlots; ++i) {
-    const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
-    const uint64_t pre = ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(m_pre >> 32), i) << 32) |
-                         __builtin_amdgcn_readlane((uint32_t)m_pre, i);
-    r[i] = 0ull;
-    if (l < cn) r[i] = slot_entry(slot_src(c, j, s0 + i, cn, (uint32_t)pre), l);
-  }
-#pragma unroll
-  for (int i = 0; i < kGatherSlots; ++i) {
-    const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
-    if (cn == 0u) continue;
-    const uint64_t pre = ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(m_pre >> 32), i) << 32) |
-                         __builtin_amdgcn_readlane((uint32_t)m_pre, i);
-    const SlotSrc src = slot_src(c, j, s0 + i, cn, (uint32_t)pre);
-    uint64_t run = sel_pre(pre, band_low);
-    for (uint32_t e0 = 0; e0 < cn; e0 += 64) {
-      const uint64_t p = e0 == 0 ? r[i] : (e0 + l < cn ? slot_entry(src, e0 + l) : 0ull);
-      const uint32_t key = entry_key(p);
-      const bool f = e0 + l < cn && key >= lo && key < hi;
-      const uint64_t b = ballot(f);
-      const uint64_t pos = run + mbcnt(b);
-      if (f && pos < cap) band[pos] = key;
-      run += __builtin_popcountll(b);
-    }
-  }
+  uint64_t run = 0;
+  walk_tiles(
+      c, j, s0, [&](int, uint64_t pre) { run = sel_pre(pre, band_low); },
+      [&](uint64_t p, bool valid) {
+        const uint32_t key = entry_key(p);
+        const bool f = valid && key >= lo && key < hi;
+        const uint64_t b = ballot(f);
+        const uint64_t pos = run + mbcnt(b);
+        if (f && pos < cap) band[pos] = key;
+        run += __builtin_popcountll(b);
+      });
 }
 
-// Slots whose wave overflowed: re-scan the 4096-element chunk (every round
-// loaded up front) and write its candidates, in index order, at the slot's
-// offset. Each wave takes list entries i = wave, wave + waves, ... of a device.
+// Tiles with an overflowed wave chunk: re-scan the tile and write its
+// candidates, in index order, at the tile's offset in the candidate list. One
+// workgroup per tile at a time (tiles i = block, block + blocks, ... of the
+// device's list); wave w takes chunk w, whose offset follows from the counts
+// of the chunks before it.
 __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_dev)
 {
-  const uint32_t j = blockIdx.x / blocks_per_dev, b = blockIdx.x - j * blocks_per_dev;
+  __shared__ uint32_t s_n[kWaves];
+  const uint32_t jr = blockIdx.x / blocks_per_dev, b = blockIdx.x - jr * blocks_per_dev;
+  const uint32_t j = c.j0 + jr;
   const DevState& st = c.st[j];
   if (st.fallback) return;
   const uint32_t n_ovf = st.ovf_n;
   const DevDesc d = c.desc[j];
-  const uint32_t l = lane_id();
+  const uint32_t l = lane_id(), w = threadIdx.x >> 6;
   const uint32_t tlo1 = st.t_lo + 1u;
   const Row row{gptr(d.grad), d.shift, c.n};
   GLOBAL uint32_t* cidx = gptr(c.cand_idx + d.cand_off);
   GLOBAL float* cval = gptr(c.cand_val + d.cand_off);
-  const uint32_t waves = blocks_per_dev * kWaves;
-  for (uint32_t i = b * kWaves + (threadIdx.x >> 6); i < n_ovf; i += waves) {
+  for (uint32_t i = b; i < n_ovf; i += blocks_per_dev) {
     const uint32_t s = c.ovf_list[(uint64_t)j * c.nslot + i];
-    const uint64_t off = (uint32_t)(c.chunk_off[(uint64_t)j * kMaxChunks + s / kScanChunk] +
-                                    c.slot_off[(uint64_t)j * c.nslot + s]);
-    const uint64_t v0 = (uint64_t)(s / kWaves) * kTile + (uint64_t)(s % kWaves) * (kTileRounds * 256) + l * 4;
+    const uint64_t v0 = (uint64_t)s * kTile + (uint64_t)w * (kTileRounds * 256) + l * 4;
     f4 x[kTileRounds];
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r) x[r] = load4(row, v0 + (uint64_t)r * 256, false);
-    uint64_t run = off;
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int r = 0; r < kTileRounds; ++r)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) cnt += (uint32_t)__builtin_popcountll(ballot(rank_key(x[r][q]) >= tlo1));
+    if (l == 0) s_n[w] = cnt;
+    __syncthreads();
+    uint64_t run = (uint32_t)slot_pre(c, j, s);
+    for (uint32_t u = 0; u < w; ++u) run += s_n[u];
+    __syncthreads();
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r) {
       bool f[4];
@@ -743,7 +808,8 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
 {
   __shared__ uint32_t h[kBins];
   if (blockIdx.x < ncand_blocks) {
-    const uint32_t j = blockIdx.x / c.ncb, b = blockIdx.x - j * c.ncb;
+    const uint32_t jr = blockIdx.x / c.ncb, b = blockIdx.x - jr * c.ncb;
+    const uint32_t j = c.j0 + jr;
     const DevState& s = c.st[j];
     if (s.fallback) return;
     const Sel sel = s.sel[kSlotCand];
@@ -776,7 +842,8 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
     return;
   }
   const uint32_t worker = blockIdx.x - ncand_blocks, G = gridDim.x - ncand_blocks;
-  for (uint32_t j = 0; j < c.K; ++j) {
+  if (*c.fb_count == 0u) return;
+  for (uint32_t j = c.j0; j < c.j0 + c.jn; ++j) {
     const DevState& s = c.st[j];
     if (!s.fallback) continue;
     const Sel sel = s.sel[kSlotFull];
@@ -812,32 +879,70 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
 
 // Per group: keys above the threshold | keys equal to it << 32, counted on the
 // selection list; with the threshold in [t_lo, t_hi) the group's keys >= t_hi
-// (all above it) are added from the slot counts. One wave per group.
+// (all above it) are added from the slot counts. One wave per kCountGroups
+// consecutive groups: lane i <= kCountGroups holds the offsets at group
+// boundary i; the groups' selection-list entries are one contiguous run, whose
+// first kCountPre windows are loaded at once (indices clamped into the list's
+// region, entries past the run ignored).
+constexpr int kCountGroups = 4;
+constexpr int kCountPre = 6;
+
 __global__ __launch_bounds__(kBlock) void k_grp_count(Ctx c)
 {
-  const uint32_t bpd = (c.ngrp + kWaves - 1) / kWaves;
-  const uint32_t j = blockIdx.x / bpd;
-  const uint32_t g = (blockIdx.x - j * bpd) * kWaves + (threadIdx.x >> 6);
+  const uint32_t per_dev = (c.ngrp + kCountGroups * kWaves - 1) / (kCountGroups * kWaves);
+  const uint32_t jr = blockIdx.x / per_dev;
+  const uint32_t j = c.j0 + jr;
+  const uint32_t g0 = ((blockIdx.x - jr * per_dev) * kWaves + (threadIdx.x >> 6)) * kCountGroups;
   const DevState& st = c.st[j];
-  if (st.fallback || g >= c.ngrp) return;
+  if (st.fallback || g0 >= c.ngrp) return;
   uint32_t thr;
   uint64_t need;
   threshold_of(st, thr, need);
-  const uint32_t s0 = g * kGatherSlots;
-  const uint32_t s1 = (s0 + kGatherSlots < c.nslot) ? s0 + kGatherSlots : c.nslot;
-  const uint64_t p0 = slot_pre(c, j, s0), p1 = slot_pre(c, j, s1);
-  const uint32_t q0 = sel_pre(p0, st.band_low), q1 = sel_pre(p1, st.band_low);
+  const uint32_t l = lane_id();
+  const uint32_t ng = (g0 + kCountGroups <= c.ngrp) ? kCountGroups : c.ngrp - g0;
+  const uint32_t lb = l < ng ? l : ng;
+  const uint32_t sb = (g0 + lb) * kGatherSlots;
+  const uint32_t sc = sb < c.nslot ? sb : c.nslot - 1;
+  uint64_t pb = c.chunk_off[(uint64_t)j * kMaxChunks + sc / kScanChunk] + c.slot_off[(uint64_t)j * c.nslot + sc];
+  if (sb >= c.nslot) pb = st.cand | (st.sure << 32);
+  const uint32_t qb = sel_pre(pb, st.band_low);
+  const uint32_t q0 = __builtin_amdgcn_readlane(qb, 0), q1 = __builtin_amdgcn_readlane(qb, ng);
+  const uint32_t capm = c.desc[j].cap - 1u;
   const GLOBAL uint32_t* keys = gptr(c.band + c.desc[j].cand_off);
-  uint64_t gt = 0, eq = 0;
-  for (uint32_t q = q0 + lane_id(); q < q1; q += 64) {
-    const uint32_t key = keys[q];
-    gt += key > thr ? 1u : 0u;
-    eq += key == thr ? 1u : 0u;
+  uint32_t kw[kCountPre];
+#pragma unroll
+  for (int m = 0; m < kCountPre; ++m) {
+    const uint32_t q = q0 + m * 64 + l;
+    kw[m] = keys[q < capm ? q : capm];
   }
-  gt = wave_sum_u64(gt);
-  eq = wave_sum_u64(eq);
-  if (st.band_low) gt += (p1 >> 32) - (p0 >> 32);
-  if (lane_id() == 0) c.grp_cnt[(uint64_t)j * c.ngrp + g] = gt | (eq << 32);
+  uint32_t gt[kCountGroups], eq[kCountGroups];
+#pragma unroll
+  for (int i = 0; i < kCountGroups; ++i) gt[i] = eq[i] = 0u;
+  auto count = [&](uint32_t q, uint32_t key) {
+    const bool valid = q < q1;
+    const bool fg = valid && key > thr, fe = valid && key == thr;
+#pragma unroll
+    for (int i = 0; i < kCountGroups; ++i) {
+      const uint32_t a = __builtin_amdgcn_readlane(qb, i), z = __builtin_amdgcn_readlane(qb, i + 1);
+      const bool in = q >= a && q < z;
+      gt[i] += (uint32_t)__builtin_popcountll(ballot(in && fg));
+      eq[i] += (uint32_t)__builtin_popcountll(ballot(in && fe));
+    }
+  };
+#pragma unroll
+  for (int m = 0; m < kCountPre; ++m) {
+    if (q0 + (uint32_t)m * 64 >= q1) break;
+    count(q0 + m * 64 + l, kw[m]);
+  }
+  for (uint32_t q = q0 + kCountPre * 64; q < q1; q += 64) count(q + l, q + l < q1 ? keys[q + l] : 0u);
+  const uint32_t sure_b = (uint32_t)(pb >> 32);
+#pragma unroll
+  for (int i = 0; i < kCountGroups; ++i) {
+    if ((uint32_t)i >= ng) break;
+    uint64_t g = gt[i];
+    if (st.band_low) g += __builtin_amdgcn_readlane(sure_b, i + 1) - __builtin_amdgcn_readlane(sure_b, i);
+    if (l == 0) c.grp_cnt[(uint64_t)j * c.ngrp + g0 + i] = g | ((uint64_t)eq[i] << 32);
+  }
 }
 
 // Exclusive prefix of nb packed counts, one workgroup.
@@ -863,18 +968,19 @@ __device__ inline void block_excl_scan_u64(const uint64_t* cnt, uint64_t* pre, u
 __global__ __launch_bounds__(kBlock) void k_grp_scan(Ctx c)
 {
   __shared__ uint64_t s_w[4];
-  const uint32_t j = blockIdx.x;
+  const uint32_t j = c.j0 + blockIdx.x;
   if (c.st[j].fallback) return;
   block_excl_scan_u64(c.grp_cnt + (uint64_t)j * c.ngrp, c.grp_pre + (uint64_t)j * c.ngrp, c.ngrp, s_w);
 }
 
-// One wave per group: its slots' candidates in index order, kept ones written
+// One wave per group: its tiles' candidates in index order, kept ones written
 // to the device's outputs; the kept sum of squares goes to epart[j][group].
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_write_fast(Ctx c)
 {
   const uint32_t bpd = (c.ngrp + kWaves - 1) / kWaves;
-  const uint32_t j = blockIdx.x / bpd;
-  const uint32_t g = (blockIdx.x - j * bpd) * kWaves + (threadIdx.x >> 6);
+  const uint32_t jr = blockIdx.x / bpd;
+  const uint32_t j = c.j0 + jr;
+  const uint32_t g = (blockIdx.x - jr * bpd) * kWaves + (threadIdx.x >> 6);
   const DevState& st = c.st[j];
   if (st.fallback || g >= c.ngrp) return;
   uint32_t thr;
@@ -883,50 +989,30 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) 
   const DevDesc d = c.desc[j];
   GLOBAL uint32_t* oi = gptr(d.idx_out);
   GLOBAL float* ov = gptr(d.val_out);
-  const uint32_t l = lane_id();
-  const uint32_t s0 = g * kGatherSlots;
   const uint64_t pre = c.grp_pre[(uint64_t)j * c.ngrp + g];
   uint64_t run_g = pre & 0xFFFFFFFFull, run_e = pre >> 32;
-  uint32_t m_cnt = 0, m_at = 0;
-  if (l < (uint32_t)kGatherSlots && s0 + l < c.nslot) {
-    m_cnt = c.slot_cnt[(uint64_t)j * c.nslot + s0 + l] & 0xFFFFu;
-    m_at = (uint32_t)slot_pre(c, j, s0 + l);
-  }
-  uint64_t r[kGatherSlots];
-#pragma unroll
-  for (int i = 0; i < kGatherSlots; ++i) {
-    const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
-    r[i] = 0ull;
-    if (l < cn) r[i] = slot_entry(slot_src(c, j, s0 + i, cn, __builtin_amdgcn_readlane(m_at, i)), l);
-  }
   double e2 = 0.0;
-#pragma unroll
-  for (int i = 0; i < kGatherSlots; ++i) {
-    const uint32_t cn = __builtin_amdgcn_readlane(m_cnt, i);
-    if (cn == 0u) continue;
-    const SlotSrc src = slot_src(c, j, s0 + i, cn, __builtin_amdgcn_readlane(m_at, i));
-    for (uint32_t e0 = 0; e0 < cn; e0 += 64) {
-      const bool valid = e0 + l < cn;
-      const uint64_t p = e0 == 0 ? r[i] : (valid ? slot_entry(src, e0 + l) : 0ull);
-      const uint32_t key = entry_key(p);
-      const bool fg = valid && key > thr, fe = valid && key == thr;
-      const uint64_t bg = ballot(fg), be = ballot(fe);
-      const uint64_t gt_b = run_g + mbcnt(bg), eq_b = run_e + mbcnt(be);
-      if (fg || (fe && eq_b < need)) {
-        const uint64_t pos = gt_b + (eq_b < need ? eq_b : need);
-        const float v = __uint_as_float((uint32_t)(p >> 32));
-        if (pos < d.k) {
-          oi[pos] = (uint32_t)p;
-          ov[pos] = v;
+  walk_tiles(
+      c, j, g * kGatherSlots, [](int, uint64_t) {},
+      [&](uint64_t p, bool valid) {
+        const uint32_t key = entry_key(p);
+        const bool fg = valid && key > thr, fe = valid && key == thr;
+        const uint64_t bg = ballot(fg), be = ballot(fe);
+        const uint64_t gt_b = run_g + mbcnt(bg), eq_b = run_e + mbcnt(be);
+        if (fg || (fe && eq_b < need)) {
+          const uint64_t pos = gt_b + (eq_b < need ? eq_b : need);
+          const float v = __uint_as_float((uint32_t)(p >> 32));
+          if (pos < d.k) {
+            oi[pos] = (uint32_t)p;
+            ov[pos] = v;
+          }
+          e2 = __builtin_fma((double)v, (double)v, e2);
         }
-        e2 = __builtin_fma((double)v, (double)v, e2);
-      }
-      run_g += __builtin_popcountll(bg);
-      run_e += __builtin_popcountll(be);
-    }
-  }
+        run_g += __builtin_popcountll(bg);
+        run_e += __builtin_popcountll(be);
+      });
   const double es = wave_sum_f64(e2);
-  if (l == 0) c.epart[(uint64_t)j * c.nslot + g] = es;
+  if (lane_id() == 0) c.epart[(uint64_t)j * c.nslot + g] = es;
 }
 
 // ---- 6. ordered compaction of the exact path ------------------------------------------------
@@ -959,7 +1045,8 @@ __device__ inline uint64_t block_gt_eq(const Row& row, uint64_t vbase, uint32_t 
 __global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c)
 {
   __shared__ uint32_t lds[8];
-  for (uint32_t j = 0; j < c.K; ++j) {
+  if (*c.fb_count == 0u) return;
+  for (uint32_t j = c.j0; j < c.j0 + c.jn; ++j) {
     const DevState& s = c.st[j];
     if (!s.fallback) continue;
     uint32_t thr;
@@ -977,7 +1064,7 @@ __global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c)
 __global__ __launch_bounds__(kBlock) void k_scan(Ctx c)
 {
   __shared__ uint64_t s_w[4];
-  const uint32_t j = blockIdx.x;
+  const uint32_t j = c.j0 + blockIdx.x;
   if (!c.st[j].fallback) return;
   block_excl_scan_u64(c.blk_cnt + (uint64_t)j * c.nbmax, c.blk_pre + (uint64_t)j * c.nbmax, c.nfb, s_w);
 }
@@ -1093,7 +1180,8 @@ __global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c)
 {
   __shared__ uint32_t lds[8];
   __shared__ double s_e[4];
-  for (uint32_t j = 0; j < c.K; ++j) {
+  if (*c.fb_count == 0u) return;
+  for (uint32_t j = c.j0; j < c.j0 + c.jn; ++j) {
     const DevState& s = c.st[j];
     if (!s.fallback) continue;
     uint32_t thr;
@@ -1117,7 +1205,7 @@ __global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c)
 __global__ __launch_bounds__(kBlock) void k_final(Ctx c)
 {
   __shared__ double s_e[4];
-  const uint32_t j = blockIdx.x;
+  const uint32_t j = c.j0 + blockIdx.x;
   DevState& s = c.st[j];
   const bool fast = !s.fallback;
   const uint32_t nb = fast ? c.ngrp : c.nfb;
@@ -1147,8 +1235,48 @@ __global__ __launch_bounds__(kBlock) void k_final(Ctx c)
 }
 
 // ---- host-side launchers ---------------------------------------------------------------------
-hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipEvent_t* ev)
+// Everything after the main pass for devices [c.j0, c.j0 + c.jn), on stream s.
+static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s)
 {
+  const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
+  k_energy_chunks<<<c.jn * nchunk, kBlock, 0, s>>>(c);
+  if (p.any_fast) k_slot_scan<<<c.jn * nchunk, kBlock, 0, s>>>(c);
+  k_post<<<c.jn, kBlock, 0, s>>>(c);
+  const uint32_t ncand = p.any_fast ? c.jn * c.ncb : 0u;
+  if (p.any_fast) {
+    constexpr uint32_t kPerBlock = kGatherSlots * kWaves;
+    k_overflow<<<c.jn * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
+    k_band<<<c.jn * ((c.nslot + kPerBlock - 1) / kPerBlock), kBlock, 0, s>>>(c);
+  }
+  for (int pass = 0; pass < 3; ++pass) {
+    k_hist_cf<<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand);
+    k_find<<<c.jn, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1);
+  }
+  if (p.any_fast) {
+    const uint32_t gb = c.jn * ((c.ngrp + kWaves - 1) / kWaves);
+    k_grp_count<<<c.jn * ((c.ngrp + kCountGroups * kWaves - 1) / (kCountGroups * kWaves)), kBlock, 0, s>>>(c);
+    k_grp_scan<<<c.jn, kBlock, 0, s>>>(c);
+    k_write_fast<<<gb, kBlock, 0, s>>>(c);
+  }
+  k_count_cf<<<p.full_workers, kBlock, 0, s>>>(c);
+  k_scan<<<c.jn, kBlock, 0, s>>>(c);
+  k_write_cf<<<p.full_workers, kBlock, 0, s>>>(c);
+  k_final<<<c.jn, kBlock, 0, s>>>(c);
+}
+
+// The whole selection. The devices are split into p.parts groups: the main
+// pass of group i runs on s; once it is done, the rest of group i's selection
+// runs on s2 while the main pass of group i + 1 runs on s (the last group's
+// rest runs on s), and s waits for s2 at the end. A main pass is bound by HBM
+// bandwidth and the later kernels mostly by latency, so they overlap well.
+// Profiling events (ev, optional): 0 start, 1 bracket done, 2 + 2i / 3 + 2i
+// around the main pass of group i, 2 + 2 * parts all done.
+hipError_t launch_select(const Ctx& c0, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipStream_t s2,
+                         hipEvent_t* fork, hipEvent_t join, hipEvent_t* ev)
+{
+  Ctx c = c0;
+  c.j0 = 0;
+  c.jn = c.K;
   const uint64_t zero_words = (uint64_t)c.K * kSlots * kBins;
   uint32_t gprep = (uint32_t)((zero_words + kBlock * 8 - 1) / (kBlock * 8));
   gprep = gprep < 1 ? 1 : (gprep > 2048 ? 2048 : gprep);
@@ -1162,36 +1290,29 @@ hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, h
   if (ev) (void)hipEventRecord(ev[1], s);
   GradArgs ga;
   for (uint32_t j = 0; j < c.K; ++j) ga.grad[j] = a.grad[j];
-  k_main<<<c.K * c.tpd, kBlock, 0, s>>>(c, ga);
-  if (ev) (void)hipEventRecord(ev[2], s);
-  const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
-  k_energy_chunks<<<c.K * nchunk, kBlock, 0, s>>>(c);
-  if (p.any_fast) k_slot_scan<<<c.K * nchunk, kBlock, 0, s>>>(c);
-  k_post<<<c.K, kBlock, 0, s>>>(c);
-  if (p.any_fast) {
-    constexpr uint32_t kPerBlock = kGatherSlots * kWaves;
-    k_overflow<<<c.K * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
-    k_band<<<c.K * ((c.nslot + kPerBlock - 1) / kPerBlock), kBlock, 0, s>>>(c);
+  const uint32_t parts = p.parts;
+  for (uint32_t i = 0; i < parts; ++i) {
+    Ctx ci = c;
+    ci.j0 = c.K * i / parts;
+    ci.jn = c.K * (i + 1) / parts - ci.j0;
+    if (ev) (void)hipEventRecord(ev[2 + 2 * i], s);
+    k_main<<<ci.jn * c.tpd, kBlock, 0, s>>>(ci, ga);
+    if (ev) (void)hipEventRecord(ev[3 + 2 * i], s);
+    if (i + 1 < parts) {
+      hipError_t e = hipEventRecord(fork[i], s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(s2, fork[i], 0);
+      if (e != hipSuccess) return e;
+      launch_post(ci, p, s2);
+    } else {
+      launch_post(ci, p, s);
+    }
   }
-  const uint32_t g = p.ncand_blocks + p.full_workers;
-  for (int pass = 0; pass < 3; ++pass) {
-    k_hist_cf<<<g, kBlock, 0, s>>>(c, p.ncand_blocks);
-    k_find<<<c.K, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1);
+  if (parts > 1) {
+    hipError_t e = hipEventRecord(join, s2);
+    if (e == hipSuccess) e = hipStreamWaitEvent(s, join, 0);
+    if (e != hipSuccess) return e;
   }
-  if (ev) (void)hipEventRecord(ev[3], s);
-  if (p.any_fast) {
-    const uint32_t gb = c.K * ((c.ngrp + kWaves - 1) / kWaves);
-    k_grp_count<<<gb, kBlock, 0, s>>>(c);
-    k_grp_scan<<<c.K, kBlock, 0, s>>>(c);
-    k_write_fast<<<gb, kBlock, 0, s>>>(c);
-  }
-  if (p.full_workers) {
-    k_count_cf<<<p.full_workers, kBlock, 0, s>>>(c);
-    k_scan<<<c.K, kBlock, 0, s>>>(c);
-    k_write_cf<<<p.full_workers, kBlock, 0, s>>>(c);
-  }
-  k_final<<<c.K, kBlock, 0, s>>>(c);
-  if (ev) (void)hipEventRecord(ev[4], s);
+  if (ev) (void)hipEventRecord(ev[2 + 2 * parts], s);
   return hipGetLastError();
 }
 
