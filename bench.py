@@ -51,15 +51,15 @@ def source_hash(path):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def traffic_entry():
+def traffic_entry(parts):
     """HBM bytes per launch of the main select pass measured by rocprofv3 counters,
-    if recorded for the current kernel source."""
+    if recorded for the current kernel source and the same number of launches."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("select_hip_sha256_16") != source_hash(SELECT_SRC):
+    if t.get("select_hip_sha256_16") != source_hash(SELECT_SRC) or t.get("parts") != parts:
         return None
     return t.get("hbm_bytes_per_launch")
 
@@ -100,6 +100,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=16)
     ap.add_argument("--stages", action="store_true", help="also print per-stage milliseconds")
+    ap.add_argument("--parts", type=int, default=2,
+                    help="device groups whose selections are pipelined (library option 'parts')")
     ap.add_argument("--calibrate", action="store_true",
                     help="first run one 1 GiB device-to-device copy (a plain copy kernel of known size "
                          "for scaling HBM byte counters)")
@@ -143,6 +145,8 @@ def main():
         w, gamma = sc.stream_weights(s.rates[it], base_batch=s.base_batch)
         weights.append(w)
         lrs.append(float(np.float32(s.eta * gamma)))
+    sc.set_option("parts", args.parts)
+    parts = min(args.parts, s.K)
     step = sc.FusedStep(G, s.ratios[0], params=params)
     for i in range(args.warmup):
         it = i % s.iterations
@@ -164,12 +168,14 @@ def main():
 
     ms_per_step = dt * 1e3 / args.steps
     value = s.K * s.n / (dt / args.steps)
-    main_ms = stages["main_select"] / max(calls, 1)
-    main_bytes = 4 * s.K * s.n
-    achieved = main_bytes / (main_ms * 1e-3) / 1e9
+    # The main pass runs as `parts` launches (devices split evenly), each reading
+    # its devices' gradients once: per launch 4 * (K / parts) * n bytes.
+    launch_ms = stages["main_select"] / max(calls, 1) / parts
+    launch_bytes = 4 * s.K * s.n / parts
+    achieved = launch_bytes / (launch_ms * 1e-3) / 1e9
     alg = np.mean([algorithmic_bytes(s, i % s.iterations) for i in range(args.steps)])
     sel_ms = stages["total"] / max(calls, 1)
-    traffic = traffic_entry()
+    traffic = traffic_entry(parts)
 
     out = {
         "metric": METRIC,
@@ -189,7 +195,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
                      "kernel": "k_main (main select pass: one read of every gradient)",
-                     "kernel_ms": main_ms},
+                     "launch_ms": launch_ms, "launch_bytes": launch_bytes, "launches_per_step": parts},
         "step_roofline": {"algorithmic_bytes": alg, "GBps": alg / (sel_ms * 1e-3) / 1e9,
                           "frac": alg / (sel_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
                           "note": "select+compact+aggregate(+SGD) stages, algorithmic bytes "
