@@ -122,15 +122,30 @@ __device__ inline bool sel_digit(const SelView& v, uint32_t key, uint32_t& d)
   return true;
 }
 
-// Bracket of the main pass from the sample selections.
+// Bracket of the main pass from the sample selections. The bracket only has to
+// be conservative (t_lo at or below the sample key of rank r_lo, t_hi above the
+// one of rank r_hi), so the selections stop after kBracketPasses digits: the
+// rank's bin [B, B + 2^bits) gives t_lo = B and t_hi = B + 2^bits. A selection
+// that missed gives t_lo = 0 (every key a candidate) or no upper bracket.
+constexpr int kBracketPasses = 2;
+
 __device__ inline void bracket_of(const DevDesc& d, const DevState& s, uint32_t& tlo, uint32_t& thi)
 {
   if (d.mode != kModeFast) {
     tlo = thi = kKeyInf;
     return;
   }
-  tlo = s.sel[kSlotSampleLo].found ? s.sel[kSlotSampleLo].result : 0u;
-  thi = s.sel[kSlotSampleHi].found ? s.sel[kSlotSampleHi].result + 1u : kKeyInf;
+  const Sel& a = s.sel[kSlotSampleLo];
+  const Sel& b = s.sel[kSlotSampleHi];
+  tlo = a.found ? a.result : (a.active ? a.lo + (a.prefix << a.bits) : 0u);
+  if (b.found) {
+    thi = b.result + 1u;
+  } else if (b.active) {
+    const uint64_t top = (uint64_t)b.lo + ((uint64_t)(b.prefix + 1u) << b.bits);
+    thi = top < (uint64_t)kKeyInf ? (uint32_t)top : kKeyInf;
+  } else {
+    thi = kKeyInf;
+  }
   if (thi <= tlo) thi = kKeyInf;
 }
 
@@ -242,7 +257,9 @@ __global__ __launch_bounds__(kBlock) void k_hist_sample(Ctx c)
 }
 
 // ---- radix digit decision for slots [s0, s1) of one device (one wave) -----------------------
-__global__ __launch_bounds__(64) void k_find(Ctx c, int s_begin, int s_end)
+// With `bracket` set (the last pass of the sampling stage), the device's
+// bracket [t_lo, t_hi) is then stored in its state for the main pass.
+__global__ __launch_bounds__(64) void k_find(Ctx c, int s_begin, int s_end, int bracket)
 {
   const uint32_t j = c.j0 + blockIdx.x, l = lane_id();
   for (int s = s_begin; s < s_end; ++s) {
@@ -300,6 +317,12 @@ __global__ __launch_bounds__(64) void k_find(Ctx c, int s_begin, int s_end)
       c.st[j].sel[s] = sel;
     }
     for (int b = l; b < kBins; b += 64) h[b] = 0u;
+  }
+  if (bracket && l == 0) {
+    uint32_t tlo, thi;
+    bracket_of(c.desc[j], c.st[j], tlo, thi);
+    c.st[j].t_lo = tlo;
+    c.st[j].t_hi = thi;
   }
 }
 
@@ -406,16 +429,14 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
     f4 v[kTileRounds];
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r) v[r] = ld_stream4(p + r * 256);
-    uint32_t tlo, thi;
-    bracket_of(c.desc[j], c.st[j], tlo, thi);
+    const uint32_t tlo = c.st[j].t_lo, thi = c.st[j].t_hi;
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r) {
       main_stage<false>(v[r], i_base + r * 256, tlo, thi, e2, wc, ws, s_c[w]);
       __builtin_amdgcn_sched_barrier(0);    // keep rounds apart: bounds the live ballot masks
     }
   } else {
-    uint32_t tlo, thi;
-    bracket_of(c.desc[j], c.st[j], tlo, thi);
+    const uint32_t tlo = c.st[j].t_lo, thi = c.st[j].t_hi;
     for (int r = 0; r < kTileRounds; ++r)
       main_stage<true>(load4(row, vbase + wv0 + r * 256, false), i_base + r * 256, tlo, thi, e2, wc, ws, s_c[w]);
   }
@@ -470,18 +491,26 @@ __device__ inline uint64_t wave_incl_scan_u64(uint64_t v)
   return v;
 }
 
-// Slot offsets, level 1: one workgroup per kScanChunk slots of a fast device;
-// each thread takes 16 consecutive slots. Writes every slot's candidate offset
-// within its chunk and the chunk's totals (cand | sure << 32).
-__global__ __launch_bounds__(kBlock) void k_slot_scan(Ctx c)
+// Per device and scan chunk (kScanChunk tiles; each thread takes 16
+// consecutive tiles): the chunk's sum of squares (fixed order), and for a fast
+// device the tiles' candidate | sure << 32 offsets within the chunk and the
+// chunk's totals.
+__global__ __launch_bounds__(kBlock) void k_tile_scan(Ctx c)
 {
   __shared__ uint64_t s_w[4];
+  __shared__ double s_e[4];
   const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
   const uint32_t jr = blockIdx.x / nchunk, ch = blockIdx.x - jr * nchunk;
   const uint32_t j = c.j0 + jr;
-  if (c.desc[j].mode != kModeFast) return;
   const uint32_t tid = threadIdx.x;
   const uint32_t s0 = ch * kScanChunk + tid * 16;
+  const double* ep = c.epart + (uint64_t)j * c.nslot;
+  double a = 0.0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) a += (s0 + i < c.nslot) ? ep[s0 + i] : 0.0;
+  const double t = block_sum_f64(a, s_e);
+  if (tid == 0) c.chunk_e[(uint64_t)j * kMaxChunks + ch] = t;
+  if (c.desc[j].mode != kModeFast) return;
   const uint32_t* cnt = c.slot_cnt + (uint64_t)j * c.nslot;
   uint32_t v[16];
   if (s0 + 16 <= c.nslot) {
@@ -515,23 +544,6 @@ __global__ __launch_bounds__(kBlock) void k_slot_scan(Ctx c)
   if (tid == kBlock - 1) c.chunk_tot[(uint64_t)j * kMaxChunks + ch] = run + sum;
 }
 
-// Sum of squares of every kScanChunk wave chunks of a device (fixed order), for
-// any device mode.
-__global__ __launch_bounds__(kBlock) void k_energy_chunks(Ctx c)
-{
-  __shared__ double s_e[4];
-  const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
-  const uint32_t jr = blockIdx.x / nchunk, ch = blockIdx.x - jr * nchunk;
-  const uint32_t j = c.j0 + jr;
-  const uint32_t s0 = ch * kScanChunk + threadIdx.x * 16;
-  const double* ep = c.epart + (uint64_t)j * c.nslot;
-  double a = 0.0;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) a += (s0 + i < c.nslot) ? ep[s0 + i] : 0.0;
-  const double t = block_sum_f64(a, s_e);
-  if (threadIdx.x == 0) c.chunk_e[(uint64_t)j * kMaxChunks + ch] = t;
-}
-
 // Slot offsets, level 2, and the per-device decision: chunk prefixes, candidate
 // totals, energies, then the exact path (fallback) or the candidate selection.
 __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
@@ -560,10 +572,7 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
   DevState& s = c.st[j];
   s.e_all = e_all;
   bool fb = (d.mode != kModeFast) || c.force_fallback;
-  uint32_t tlo, thi;
-  bracket_of(d, s, tlo, thi);
-  s.t_lo = tlo;
-  s.t_hi = thi;
+  const uint32_t tlo = s.t_lo, thi = s.t_hi;
   if (d.mode == kModeFast) {
     s.cand = cand;
     s.sure = sure;
@@ -662,7 +671,7 @@ __device__ inline uint32_t entry_key(uint64_t p) { return (uint32_t)(p >> 32) & 
 // clamped, so every load is in bounds; entries past a tile's count are
 // ignored). Overflowed tiles, whose entries are in the candidate list, reload
 // them once their offset is known.
-constexpr int kPre = 4;
+constexpr int kPre = 1;
 
 template <class Begin, class Visit>
 __device__ inline void walk_tiles(const Ctx& c, uint32_t j, uint32_t s0, Begin begin, Visit visit)
@@ -1239,8 +1248,7 @@ __global__ __launch_bounds__(kBlock) void k_final(Ctx c)
 static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s)
 {
   const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
-  k_energy_chunks<<<c.jn * nchunk, kBlock, 0, s>>>(c);
-  if (p.any_fast) k_slot_scan<<<c.jn * nchunk, kBlock, 0, s>>>(c);
+  k_tile_scan<<<c.jn * nchunk, kBlock, 0, s>>>(c);
   k_post<<<c.jn, kBlock, 0, s>>>(c);
   const uint32_t ncand = p.any_fast ? c.jn * c.ncb : 0u;
   if (p.any_fast) {
@@ -1250,7 +1258,7 @@ static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s)
   }
   for (int pass = 0; pass < 3; ++pass) {
     k_hist_cf<<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand);
-    k_find<<<c.jn, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1);
+    k_find<<<c.jn, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1, 0);
   }
   if (p.any_fast) {
     const uint32_t gb = c.jn * ((c.ngrp + kWaves - 1) / kWaves);
@@ -1282,9 +1290,9 @@ hipError_t launch_select(const Ctx& c0, const PrepArgs& a, const SelectPlan& p, 
   gprep = gprep < 1 ? 1 : (gprep > 2048 ? 2048 : gprep);
   k_prep<<<gprep, kBlock, 0, s>>>(c, a);
   if (p.any_fast) {
-    for (int pass = 0; pass < 3; ++pass) {
+    for (int pass = 0; pass < kBracketPasses; ++pass) {
       k_hist_sample<<<dim3(p.sample_blocks, c.K), kBlock, 0, s>>>(c);
-      k_find<<<c.K, 64, 0, s>>>(c, kSlotSampleLo, kSlotSampleHi + 1);
+      k_find<<<c.K, 64, 0, s>>>(c, kSlotSampleLo, kSlotSampleHi + 1, pass + 1 == kBracketPasses);
     }
   }
   if (ev) (void)hipEventRecord(ev[1], s);
