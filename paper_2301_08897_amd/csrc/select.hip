@@ -710,10 +710,15 @@ __device__ inline void walk_tiles(const Ctx& c, uint32_t j, uint32_t s0, Begin b
       visit(r[i][m], m * 64 + l < cn);
     }
     if (cn > (uint32_t)(kPre * 64)) {
+      // one window ahead: the next window's load is in flight while this one is used
       const SlotSrc src = slot_src(c, j, s0 + i, ovf, (uint32_t)pre);
-      for (uint32_t e0 = kPre * 64; e0 < cn; e0 += 64) {
-        const bool valid = e0 + l < cn;
-        visit(valid ? slot_entry(src, e0 + l) : 0ull, valid);
+      uint32_t e0 = kPre * 64;
+      uint64_t cur = e0 + l < cn ? slot_entry(src, e0 + l) : 0ull;
+      for (; e0 < cn; e0 += 64) {
+        const uint32_t e1 = e0 + 64;
+        const uint64_t nxt = (e1 < cn && e1 + l < cn) ? slot_entry(src, e1 + l) : 0ull;
+        visit(cur, e0 + l < cn);
+        cur = nxt;
       }
     }
   }
@@ -738,16 +743,18 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) 
   const uint32_t lo = st.sel[kSlotCand].lo, hi = st.sel[kSlotCand].hi, band_low = st.band_low;
   const uint64_t cap = c.desc[j].cap;
   GLOBAL uint32_t* band = gptr(c.band + c.desc[j].cand_off);
-  uint64_t run = 0;
+  // 32-bit positions: a device's lists hold fewer than 2^31 entries
+  const uint32_t cap32 = (uint32_t)cap, width = hi - lo;
+  uint32_t run = 0;
   walk_tiles(
       c, j, s0, [&](int, uint64_t pre) { run = sel_pre(pre, band_low); },
       [&](uint64_t p, bool valid) {
         const uint32_t key = entry_key(p);
-        const bool f = valid && key >= lo && key < hi;
+        const bool f = valid && key - lo < width;     // key in [lo, hi)
         const uint64_t b = ballot(f);
-        const uint64_t pos = run + mbcnt(b);
-        if (f && pos < cap) band[pos] = key;
-        run += __builtin_popcountll(b);
+        const uint32_t pos = run + mbcnt(b);
+        if (f && pos < cap32) band[pos] = key;
+        run += (uint32_t)__builtin_popcountll(b);
       });
 }
 
@@ -998,8 +1005,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) 
   const DevDesc d = c.desc[j];
   GLOBAL uint32_t* oi = gptr(d.idx_out);
   GLOBAL float* ov = gptr(d.val_out);
+  // 32-bit counts and positions: k < 2^32
   const uint64_t pre = c.grp_pre[(uint64_t)j * c.ngrp + g];
-  uint64_t run_g = pre & 0xFFFFFFFFull, run_e = pre >> 32;
+  uint32_t run_g = (uint32_t)pre, run_e = (uint32_t)(pre >> 32);
+  const uint32_t need32 = (uint32_t)need, k32 = d.k;
   double e2 = 0.0;
   walk_tiles(
       c, j, g * kGatherSlots, [](int, uint64_t) {},
@@ -1007,18 +1016,18 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) 
         const uint32_t key = entry_key(p);
         const bool fg = valid && key > thr, fe = valid && key == thr;
         const uint64_t bg = ballot(fg), be = ballot(fe);
-        const uint64_t gt_b = run_g + mbcnt(bg), eq_b = run_e + mbcnt(be);
-        if (fg || (fe && eq_b < need)) {
-          const uint64_t pos = gt_b + (eq_b < need ? eq_b : need);
+        const uint32_t gt_b = run_g + mbcnt(bg), eq_b = run_e + mbcnt(be);
+        if (fg || (fe && eq_b < need32)) {
+          const uint32_t pos = gt_b + (eq_b < need32 ? eq_b : need32);
           const float v = __uint_as_float((uint32_t)(p >> 32));
-          if (pos < d.k) {
+          if (pos < k32) {
             oi[pos] = (uint32_t)p;
             ov[pos] = v;
           }
           e2 = __builtin_fma((double)v, (double)v, e2);
         }
-        run_g += __builtin_popcountll(bg);
-        run_e += __builtin_popcountll(be);
+        run_g += (uint32_t)__builtin_popcountll(bg);
+        run_e += (uint32_t)__builtin_popcountll(be);
       });
   const double es = wave_sum_f64(e2);
   if (lane_id() == 0) c.epart[(uint64_t)j * c.nslot + g] = es;
