@@ -97,7 +97,7 @@ constexpr uint64_t kCapAlign = 64;
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-  uint32_t K = 0, tpd = 0, nslot = 0, ngrp = 0, ncb = 0, nfb = 0, nbmax = 0, nrange = 0, s_stride = 0, s_n = 0;
+  uint32_t K = 0, tpd = 0, nslot = 0, ngrp = 0, nfb = 0, nbmax = 0, nrange = 0, s_stride = 0, s_n = 0;
   uint64_t n = 0;
   uint32_t k[kMaxK], cap[kMaxK], mode[kMaxK], r_lo[kMaxK], r_hi[kMaxK];
   uint32_t any_fast = 0;
@@ -145,7 +145,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
   L.ngrp = ceil_div_u64(L.nslot, kGatherSlots);
   L.nrange = ceil_div_u64(n, kARange);
   sample_geometry(n, L.s_stride, L.s_n);
-  uint64_t sum_cap = 0, max_cap = 0;
+  uint64_t sum_cap = 0;
   L.any_fast = 0;
   for (uint32_t j = 0; j < K; ++j) {
     const uint64_t k = with_select ? k_rule(n, ratios[j]) : 0;
@@ -174,12 +174,10 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
       L.r_hi[j] = (uint32_t)rhi;
       L.any_fast = 1;
       sum_cap += cap;
-      if (cap > max_cap) max_cap = cap;
     }
   }
-  L.ncb = max_cap ? ceil_div_u64(max_cap, kCBlk) : 1u;
   L.nfb = ceil_div_u64(n + 3, kCBlk);
-  L.nbmax = L.ncb > L.nfb ? L.ncb : L.nfb;
+  L.nbmax = L.nfb;
   size_t o = 0;
   auto take = [&](size_t bytes) {
     size_t at = o;
@@ -247,7 +245,6 @@ Ctx make_ctx(const Layout& L, void* ws)
   c.tpd = L.tpd;
   c.nslot = L.nslot;
   c.ngrp = L.ngrp;
-  c.ncb = L.ncb;
   c.nfb = L.nfb;
   c.nbmax = L.nbmax;
   c.s_stride = L.s_stride;

@@ -70,10 +70,8 @@ struct Sel {
 struct DevState {
   Sel sel[kSlots];
   uint64_t cand, sure;    // main pass totals: keys >= t_lo, keys >= t_hi
-  uint64_t sel_n;         // entries of the selection list
   uint32_t t_lo, t_hi;    // bracket used by the main pass
   uint32_t fallback;      // 1: the exact full-data path produces this device's output
-  uint32_t band_low;      // candidate select ran on [t_lo, t_hi): add `sure` above it
   uint32_t thr;           // final threshold key (k-th largest)
   uint32_t err;           // internal error bits (select miss, count mismatch)
   uint64_t c_gt, need;    // keys above thr; keys equal to thr that are kept
@@ -92,12 +90,13 @@ struct Ctx {
   uint64_t* chunk_tot;    // [K][kMaxChunks] candidate | sure << 32 totals of each scan chunk
   uint64_t* chunk_off;    // [K][kMaxChunks] candidate | sure << 32 counts before each scan chunk
   double* chunk_e;        // [K][kMaxChunks] sum of squares of each scan chunk
-  uint64_t* slot;         // [K][nslot][kSlotCap] staged candidates per tile: index | value bits << 32
+  uint64_t* slot;         // [K][nslot][kSlotCap] per tile: staged candidates (index | value bits << 32),
+                          // then the keys of those below t_hi, two per entry; one rotated run
   uint32_t* ovf_list;     // [K][nslot] tiles with a wave chunk of more than kWaveCap candidates
   double* epart;          // [K][nslot] sum of squares per tile, later kept sum of squares per write group
   uint32_t* cand_idx;     // candidate regions (entries of overflowed slots only)
   float* cand_val;
-  uint32_t* band;         // selection lists: keys in the selection interval, per device at cand_off
+  uint32_t* band;         // band lists: keys below t_hi of overflowed tiles, per device at cand_off
   uint64_t* grp_cnt;      // [K][ngrp] kept-above | equal << 32 counts per write group of slots
   uint64_t* grp_pre;      // [K][ngrp] exclusive prefix of grp_cnt
   uint64_t* blk_cnt;      // [K][nbmax] packed (gt | eq << 32) per compaction block
@@ -110,9 +109,8 @@ struct Ctx {
   uint32_t tpd;           // main tiles per device: ceil((n + 3) / kTile)
   uint32_t nslot;         // slots (main-pass tiles) per device: tpd
   uint32_t ngrp;          // write groups per device: ceil(nslot / kGatherSlots)
-  uint32_t ncb;           // candidate blocks per device (max over devices)
   uint32_t nfb;           // exact-path blocks per device: ceil((n + 3) / kCBlk)
-  uint32_t nbmax;         // max(ncb, nfb)
+  uint32_t nbmax;         // exact-path blocks allocated per device (nfb)
   uint32_t s_stride;      // sample chunk stride (elements)
   uint32_t s_n;           // sample elements per device
   uint32_t force_fallback;

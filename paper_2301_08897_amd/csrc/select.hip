@@ -441,9 +441,11 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
       main_stage<true>(load4(row, vbase + wv0 + r * 256, false), i_base + r * 256, tlo, thi, e2, wc, ws, s_c[w]);
   }
   // The tile's slot: the waves' staged candidates one after the other (index
-  // order), one contiguous rotated run; its counts and sum of squares. A tile
-  // with a wave chunk over kWaveCap candidates stages nothing and is recorded
-  // for k_overflow, which re-scans it once the slot offsets are known.
+  // order), then the keys of the candidates below t_hi (the selection
+  // interval [t_lo, t_hi)), two per entry, as one contiguous rotated run; its
+  // counts and sum of squares. A tile with a wave chunk over kWaveCap
+  // candidates, or whose run would not fit the region, stages nothing and is
+  // recorded for k_overflow, which re-scans it once the slot offsets are known.
   __shared__ uint32_t s_cnt[kWaves];
   __shared__ double s_e[kWaves];
   const double es = wave_sum_f64(e2[0] + e2[1]);
@@ -452,16 +454,20 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
     s_e[w] = es;
   }
   __syncthreads();
-  uint32_t cand = 0, sure = 0, before = 0;
+  uint32_t cand = 0, sure = 0, before = 0, bbefore = 0;
   bool ovf = false;
 #pragma unroll
   for (int i = 0; i < kWaves; ++i) {
     const uint32_t v = s_cnt[i];
-    if ((uint32_t)i < w) before += v & 0xFFFFu;
+    if ((uint32_t)i < w) {
+      before += v & 0xFFFFu;
+      bbefore += (v & 0xFFFFu) - (v >> 16);
+    }
     cand += v & 0xFFFFu;
     sure += v >> 16;
     ovf |= (v & 0xFFFFu) > (uint32_t)kWaveCap;
   }
+  ovf |= cand + (cand - sure + 1u) / 2u > (uint32_t)kSlotCap;
   const uint64_t slot = (uint64_t)j * c.nslot + tile;
   if (threadIdx.x == 0) {
     c.slot_cnt[slot] = cand | (ovf ? 0x8000u : 0u) | (sure << 16);
@@ -472,10 +478,24 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
     }
   }
   if (!ovf) {
-    // Nontemporal: the slots are read only after the whole pass (selection list, output).
+    // Nontemporal: the slots are read only after the whole pass.
     GLOBAL uint64_t* sp = gptr(c.slot + slot * kSlotCap);
-    const uint32_t rot = slot_rot(slot) + before;
-    for (uint32_t i = l; i < wc; i += 64) __builtin_nontemporal_store(s_c[w][i], sp + ((rot + i) & (kSlotCap - 1u)));
+    GLOBAL uint32_t* sk = reinterpret_cast<GLOBAL uint32_t*>(sp);
+    const uint32_t rot = slot_rot(slot);
+    const uint32_t kbase = 2u * (rot + cand) + bbefore;      // u32 index of this wave's first key
+    const uint32_t thi = c.st[j].t_hi;
+    uint32_t brun = 0;
+    for (uint32_t i0 = 0; i0 < wc; i0 += 64) {
+      const uint32_t i = i0 + l;
+      const bool valid = i < wc;
+      const uint64_t pe = valid ? s_c[w][i] : 0ull;
+      if (valid) __builtin_nontemporal_store(pe, sp + ((rot + before + i) & (kSlotCap - 1u)));
+      const uint32_t key = (uint32_t)(pe >> 32) & kKeyMask;
+      const bool band = valid && key < thi;
+      const uint64_t bb = ballot(band);
+      if (band) __builtin_nontemporal_store(key, sk + ((kbase + brun + mbcnt(bb)) & (2u * kSlotCap - 1u)));
+      brun += (uint32_t)__builtin_popcountll(bb);
+    }
   }
 }
 
@@ -577,12 +597,12 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
     s.cand = cand;
     s.sure = sure;
     if (s.err) fb = true;
-    if (cand < d.k || cand > d.cap) fb = true;
+    // the selection interval must hold the k-th largest key: fewer than k sure keys
+    if (cand < d.k || cand > d.cap || sure >= d.k) fb = true;
   }
   Sel sel;
   __builtin_memset(&sel, 0, sizeof(sel));
   sel.active = 1;
-  s.sel_n = 0;
   if (fb) {
     s.fallback = 1;
     atomicAdd(c.fb_count, 1u);
@@ -593,19 +613,9 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
     s.sel[kSlotFull] = sel;
   } else {
     s.fallback = 0;
-    if (s.sure < d.k) {
-      sel.lo = tlo;
-      sel.hi = thi;
-      sel.rank = d.k - s.sure;
-      s.band_low = 1;
-      s.sel_n = s.cand - s.sure;
-    } else {
-      sel.lo = thi;
-      sel.hi = kKeyInf;
-      sel.rank = d.k;
-      s.band_low = 0;
-      s.sel_n = s.sure;
-    }
+    sel.lo = tlo;
+    sel.hi = thi;
+    sel.rank = d.k - s.sure;
     const uint32_t b = bitlen32(sel.hi - sel.lo - 1u);
     sel.bits = b ? b : 1u;
     s.sel[kSlotCand] = sel;
@@ -617,14 +627,6 @@ __device__ inline uint64_t slot_pre(const Ctx& c, uint32_t j, uint32_t s)
 {
   if (s >= c.nslot) return c.st[j].cand | (c.st[j].sure << 32);
   return c.chunk_off[(uint64_t)j * kMaxChunks + s / kScanChunk] + c.slot_off[(uint64_t)j * c.nslot + s];
-}
-
-// Offset in the selection list of the entries of slots >= s: the interval
-// [t_lo, t_hi) has candidates - sure entries before, [t_hi, inf) has sure.
-__device__ inline uint32_t sel_pre(uint64_t pre, uint32_t band_low)
-{
-  const uint32_t cand = (uint32_t)pre, sure = (uint32_t)(pre >> 32);
-  return band_low ? cand - sure : sure;
 }
 
 // Entry e of a slot: from its staged pairs, or (overflowed slot) from the
@@ -724,48 +726,89 @@ __device__ inline void walk_tiles(const Ctx& c, uint32_t j, uint32_t s0, Begin b
   }
 }
 
-// ---- 3. selection list ----------------------------------------------------------------------
-// Each wave takes kGatherSlots consecutive tiles and writes the keys of their
-// entries in the selection interval [sel.lo, sel.hi) to the device's selection
-// list, tile after tile (the slot counts give every tile's offset). The
-// threshold is then radix-selected over this short list only.
-// Occupancy 8 (at most 64 VGPRs): these passes are bound by memory latency.
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_band(Ctx c)
+// ---- 3. selection-interval keys per tile ---------------------------------------------------
+// The keys of a tile's candidates below t_hi (the selection interval [t_lo,
+// t_hi)) follow its candidates in the slot region, two per entry; k_overflow
+// writes those of an overflowed tile to the device's band list at the tile's
+// band offset (candidates - sure keys before it). band_tiles walks them for
+// tiles t0 .. t0 + kBandTiles - 1 of device j, tile after tile, in index order
+// within a tile, 64 at a time: visit(key, valid) takes one window, done(i,
+// sure) closes tile t0 + i (sure: its keys >= t_hi). Lane l holds tile t0 +
+// l's counts. The first window of kBandBatch tiles is loaded at once, and
+// longer runs four windows at once, without conditions: tile indices are
+// clamped, region positions wrap inside the region (2 * kSlotCap keys) and
+// band-list positions are clamped into the tile's run, so every load is in
+// bounds; keys past a tile's count are ignored.
+constexpr int kBandTiles = 32;
+constexpr int kBandBatch = 8;
+
+template <class Visit, class Done>
+__device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit visit, Done done)
 {
-  constexpr uint32_t kPerBlock = kGatherSlots * kWaves;
-  const uint32_t groups = (c.nslot + kPerBlock - 1) / kPerBlock;
-  const uint32_t jr = blockIdx.x / groups, g = blockIdx.x - jr * groups;
-  const uint32_t j = c.j0 + jr;
-  const DevState& st = c.st[j];
-  if (st.fallback) return;
-  const uint32_t s0 = g * kPerBlock + (threadIdx.x >> 6) * kGatherSlots;
-  if (s0 >= c.nslot) return;
-  const uint32_t lo = st.sel[kSlotCand].lo, hi = st.sel[kSlotCand].hi, band_low = st.band_low;
-  const uint64_t cap = c.desc[j].cap;
-  GLOBAL uint32_t* band = gptr(c.band + c.desc[j].cand_off);
-  // 32-bit positions: a device's lists hold fewer than 2^31 entries
-  const uint32_t cap32 = (uint32_t)cap, width = hi - lo;
-  uint32_t run = 0;
-  walk_tiles(
-      c, j, s0, [&](int, uint64_t pre) { run = sel_pre(pre, band_low); },
-      [&](uint64_t p, bool valid) {
-        const uint32_t key = entry_key(p);
-        const bool f = valid && key - lo < width;     // key in [lo, hi)
-        const uint64_t b = ballot(f);
-        const uint32_t pos = run + mbcnt(b);
-        if (f && pos < cap32) band[pos] = key;
-        run += (uint32_t)__builtin_popcountll(b);
-      });
+  constexpr uint32_t kMask = 2u * kSlotCap - 1u;
+  const uint32_t l = lane_id();
+  const uint32_t last = c.nslot - 1;
+  const uint64_t row = (uint64_t)j * c.nslot;
+  const uint32_t tl = t0 + l < last ? t0 + l : last;
+  const uint32_t v = t0 + l < c.nslot ? c.slot_cnt[row + tl] : 0u;
+  const uint32_t cand = v & 0x7FFFu, sure = v >> 16, nb = cand - sure;
+  const uint32_t ovf = (v >> 15) & 1u;
+  uint32_t kb = 2u * (slot_rot(row + tl) + cand);       // first key: 32-bit word of the region ...
+  if (ovf) {
+    const uint64_t pre = slot_pre(c, j, tl);
+    kb = (uint32_t)pre - (uint32_t)(pre >> 32);         // ... or position in the band list
+  }
+  const uint32_t nt = c.nslot - t0 < (uint32_t)kBandTiles ? c.nslot - t0 : (uint32_t)kBandTiles;
+  const GLOBAL uint32_t* reg = reinterpret_cast<const GLOBAL uint32_t*>(gptr(c.slot));
+  const GLOBAL uint32_t* blist = gptr(c.band) + c.desc[j].cand_off;
+  // windows e0 .. of a run of nbi keys, four at a time; key_at(e) is in bounds for every e
+  auto run = [&](uint32_t e0, uint32_t nbi, auto key_at) {
+    for (uint32_t e = e0; e < nbi; e += 256) {
+      uint32_t w4[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) w4[m] = key_at(e + m * 64 + l);
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+        if (e + m * 64 < nbi) visit(w4[m], e + m * 64 + l < nbi);
+    }
+  };
+  for (uint32_t i0 = 0; i0 < nt; i0 += kBandBatch) {
+    uint32_t kv[kBandBatch];
+#pragma unroll
+    for (int q = 0; q < kBandBatch; ++q) {
+      const uint32_t i = i0 + q;     // < kBandTiles
+      const uint32_t ti = t0 + i < last ? t0 + i : last;
+      kv[q] = reg[(row + ti) * (2u * kSlotCap) + ((__builtin_amdgcn_readlane(kb, i) + l) & kMask)];
+    }
+#pragma unroll
+    for (int q = 0; q < kBandBatch; ++q) {
+      const uint32_t i = i0 + q;
+      if (i >= nt) break;
+      const uint32_t nbi = __builtin_amdgcn_readlane(nb, i), kbi = __builtin_amdgcn_readlane(kb, i);
+      if (!__builtin_amdgcn_readlane(ovf, i)) {
+        visit(kv[q], l < nbi);
+        const GLOBAL uint32_t* base = reg + (row + t0 + i) * (2u * kSlotCap);
+        if (nbi > 64u) run(64u, nbi, [&](uint32_t e) { return base[(kbi + e) & kMask]; });
+      } else if (nbi) {
+        const GLOBAL uint32_t* p = blist + kbi;
+        run(0u, nbi, [&](uint32_t e) { return p[e < nbi ? e : nbi - 1u]; });
+      }
+      done(i, __builtin_amdgcn_readlane(sure, i));
+    }
+  }
 }
 
-// Tiles with an overflowed wave chunk: re-scan the tile and write its
-// candidates, in index order, at the tile's offset in the candidate list. One
+// Overflowed tiles (a wave chunk of more than kWaveCap candidates, or more
+// candidates and selection-interval keys than the slot region holds): re-scan
+// the tile and write its candidates, in index order, at the tile's offset in
+// the candidate list, and the keys of those below t_hi at its offset in the
+// band list. One
 // workgroup per tile at a time (tiles i = block, block + blocks, ... of the
 // device's list); wave w takes chunk w, whose offset follows from the counts
 // of the chunks before it.
 __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_dev)
 {
-  __shared__ uint32_t s_n[kWaves];
+  __shared__ uint32_t s_n[kWaves], s_b[kWaves];
   const uint32_t jr = blockIdx.x / blocks_per_dev, b = blockIdx.x - jr * blocks_per_dev;
   const uint32_t j = c.j0 + jr;
   const DevState& st = c.st[j];
@@ -773,36 +816,53 @@ __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_
   const uint32_t n_ovf = st.ovf_n;
   const DevDesc d = c.desc[j];
   const uint32_t l = lane_id(), w = threadIdx.x >> 6;
-  const uint32_t tlo1 = st.t_lo + 1u;
+  const uint32_t tlo1 = st.t_lo + 1u, thi1 = st.t_hi + 1u;   // rank keys: key + 1
   const Row row{gptr(d.grad), d.shift, c.n};
   GLOBAL uint32_t* cidx = gptr(c.cand_idx + d.cand_off);
   GLOBAL float* cval = gptr(c.cand_val + d.cand_off);
+  GLOBAL uint32_t* band = gptr(c.band + d.cand_off);
   for (uint32_t i = b; i < n_ovf; i += blocks_per_dev) {
     const uint32_t s = c.ovf_list[(uint64_t)j * c.nslot + i];
     const uint64_t v0 = (uint64_t)s * kTile + (uint64_t)w * (kTileRounds * 256) + l * 4;
     f4 x[kTileRounds];
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r) x[r] = load4(row, v0 + (uint64_t)r * 256, false);
-    uint32_t cnt = 0;
+    uint32_t cnt = 0, bcnt = 0;
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) cnt += (uint32_t)__builtin_popcountll(ballot(rank_key(x[r][q]) >= tlo1));
-    if (l == 0) s_n[w] = cnt;
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t rk = rank_key(x[r][q]);
+        cnt += (uint32_t)__builtin_popcountll(ballot(rk >= tlo1));
+        bcnt += (uint32_t)__builtin_popcountll(ballot(rk >= tlo1 && rk < thi1));
+      }
+    if (l == 0) {
+      s_n[w] = cnt;
+      s_b[w] = bcnt;
+    }
     __syncthreads();
-    uint64_t run = (uint32_t)slot_pre(c, j, s);
-    for (uint32_t u = 0; u < w; ++u) run += s_n[u];
+    const uint64_t pre = slot_pre(c, j, s);
+    uint64_t run = (uint32_t)pre;
+    uint64_t brun = (uint32_t)pre - (uint32_t)(pre >> 32);
+    for (uint32_t u = 0; u < w; ++u) {
+      run += s_n[u];
+      brun += s_b[u];
+    }
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r) {
-      bool f[4];
-      uint64_t bm[4];
+      bool f[4], fb[4];
+      uint64_t bm[4], bb[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        f[q] = rank_key(x[r][q]) >= tlo1;
+        const uint32_t rk = rank_key(x[r][q]);
+        f[q] = rk >= tlo1;
+        fb[q] = f[q] && rk < thi1;
         bm[q] = ballot(f[q]);
+        bb[q] = ballot(fb[q]);
       }
       uint64_t pos = run + mbcnt(bm[0]) + mbcnt(bm[1]) + mbcnt(bm[2]) + mbcnt(bm[3]);
+      uint64_t bpos = brun + mbcnt(bb[0]) + mbcnt(bb[1]) + mbcnt(bb[2]) + mbcnt(bb[3]);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         if (f[q]) {
@@ -812,47 +872,44 @@ __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_
           }
           ++pos;
         }
+        if (fb[q]) {
+          if (bpos < d.cap) band[bpos] = rank_key(x[r][q]) - 1u;
+          ++bpos;
+        }
       }
       run += __builtin_popcountll(bm[0]) + __builtin_popcountll(bm[1]) + __builtin_popcountll(bm[2]) +
              __builtin_popcountll(bm[3]);
+      brun += __builtin_popcountll(bb[0]) + __builtin_popcountll(bb[1]) + __builtin_popcountll(bb[2]) +
+              __builtin_popcountll(bb[3]);
     }
   }
 }
 
-// ---- 4. histogram pass over selection lists (fast devices) and full data (exact devices) -----
+// ---- 4. histogram pass over selection-interval keys (fast devices) and full data (exact devices)
+// Fast devices: workgroup b of device j takes tiles [b, b + 1) * kBandTiles * kWaves.
 __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks)
 {
   __shared__ uint32_t h[kBins];
   if (blockIdx.x < ncand_blocks) {
-    const uint32_t jr = blockIdx.x / c.ncb, b = blockIdx.x - jr * c.ncb;
+    const uint32_t per_dev = (c.nslot + kBandTiles * kWaves - 1) / (kBandTiles * kWaves);
+    const uint32_t jr = blockIdx.x / per_dev, b = blockIdx.x - jr * per_dev;
     const uint32_t j = c.j0 + jr;
     const DevState& s = c.st[j];
     if (s.fallback) return;
     const Sel sel = s.sel[kSlotCand];
     if (!sel.active) return;
-    const uint64_t cnt = s.sel_n;
-    const uint64_t q0 = (uint64_t)b * kCBlk;
-    if (q0 >= cnt) return;
     for (int i = threadIdx.x; i < kBins; i += kBlock) h[i] = 0u;
     __syncthreads();
     const SelView sv = view_of(sel);
-    const uint64_t rem = (cnt - q0 < (uint64_t)kCBlk) ? cnt - q0 : (uint64_t)kCBlk;
-    const GLOBAL uint32_t* keys = gptr(c.band + c.desc[j].cand_off + q0);
-#pragma unroll 2
-    for (int r = 0; r < kCBlkRounds; ++r) {
-      const uint64_t e = (uint64_t)r * kRound + threadIdx.x * 4;
-      if (e >= rem) break;
-      u4 x = {kKeyInf, kKeyInf, kKeyInf, kKeyInf};
-      if (e + 4 <= rem) x = *(const GLOBAL u4*)(keys + e);
-      else
-        for (int q = 0; q < 4; ++q)
-          if (e + q < rem) x[q] = keys[e + q];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        uint32_t dg;
-        if (e + q < rem && sel_digit(sv, x[q], dg)) atomicAdd(&h[dg], 1u);
-      }
-    }
+    const uint32_t t0 = (b * kWaves + (threadIdx.x >> 6)) * kBandTiles;
+    if (t0 < c.nslot)
+      band_tiles(
+          c, j, t0,
+          [&](uint32_t key, bool valid) {
+            uint32_t dg;
+            if (valid && sel_digit(sv, key, dg)) atomicAdd(&h[dg], 1u);
+          },
+          [](uint32_t, uint32_t) {});
     __syncthreads();
     flush_hist(h, c.hist + ((uint64_t)j * kSlots + kSlotCand) * kBins, kBins);
     return;
@@ -893,72 +950,40 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
 // key == thr while fewer than `need` equal keys came before (index order);
 // a kept entry goes to (keys above thr before it) + min(equal keys before it, need).
 
-// Per group: keys above the threshold | keys equal to it << 32, counted on the
-// selection list; with the threshold in [t_lo, t_hi) the group's keys >= t_hi
-// (all above it) are added from the slot counts. One wave per kCountGroups
-// consecutive groups: lane i <= kCountGroups holds the offsets at group
-// boundary i; the groups' selection-list entries are one contiguous run, whose
-// first kCountPre windows are loaded at once (indices clamped into the list's
-// region, entries past the run ignored).
-constexpr int kCountGroups = 4;
-constexpr int kCountPre = 6;
-
+// Per group: keys above the threshold | keys equal to it << 32. The threshold
+// lies in [t_lo, t_hi): equal keys and the keys above it below t_hi are
+// counted on the tiles' selection-interval keys, the keys >= t_hi come from
+// the slot counts. One wave per kBandTiles tiles (kBandTiles / 2 groups).
 __global__ __launch_bounds__(kBlock) void k_grp_count(Ctx c)
 {
-  const uint32_t per_dev = (c.ngrp + kCountGroups * kWaves - 1) / (kCountGroups * kWaves);
+  const uint32_t per_dev = (c.nslot + kBandTiles * kWaves - 1) / (kBandTiles * kWaves);
   const uint32_t jr = blockIdx.x / per_dev;
   const uint32_t j = c.j0 + jr;
-  const uint32_t g0 = ((blockIdx.x - jr * per_dev) * kWaves + (threadIdx.x >> 6)) * kCountGroups;
+  const uint32_t t0 = ((blockIdx.x - jr * per_dev) * kWaves + (threadIdx.x >> 6)) * kBandTiles;
   const DevState& st = c.st[j];
-  if (st.fallback || g0 >= c.ngrp) return;
+  if (st.fallback || t0 >= c.nslot) return;
+  static_assert(kGatherSlots == 2 && kBandTiles % 2 == 0, "groups are tile pairs");
   uint32_t thr;
   uint64_t need;
   threshold_of(st, thr, need);
   const uint32_t l = lane_id();
-  const uint32_t ng = (g0 + kCountGroups <= c.ngrp) ? kCountGroups : c.ngrp - g0;
-  const uint32_t lb = l < ng ? l : ng;
-  const uint32_t sb = (g0 + lb) * kGatherSlots;
-  const uint32_t sc = sb < c.nslot ? sb : c.nslot - 1;
-  uint64_t pb = c.chunk_off[(uint64_t)j * kMaxChunks + sc / kScanChunk] + c.slot_off[(uint64_t)j * c.nslot + sc];
-  if (sb >= c.nslot) pb = st.cand | (st.sure << 32);
-  const uint32_t qb = sel_pre(pb, st.band_low);
-  const uint32_t q0 = __builtin_amdgcn_readlane(qb, 0), q1 = __builtin_amdgcn_readlane(qb, ng);
-  const uint32_t capm = c.desc[j].cap - 1u;
-  const GLOBAL uint32_t* keys = gptr(c.band + c.desc[j].cand_off);
-  uint32_t kw[kCountPre];
-#pragma unroll
-  for (int m = 0; m < kCountPre; ++m) {
-    const uint32_t q = q0 + m * 64 + l;
-    kw[m] = keys[q < capm ? q : capm];
-  }
-  uint32_t gt[kCountGroups], eq[kCountGroups];
-#pragma unroll
-  for (int i = 0; i < kCountGroups; ++i) gt[i] = eq[i] = 0u;
-  auto count = [&](uint32_t q, uint32_t key) {
-    const bool valid = q < q1;
-    const bool fg = valid && key > thr, fe = valid && key == thr;
-#pragma unroll
-    for (int i = 0; i < kCountGroups; ++i) {
-      const uint32_t a = __builtin_amdgcn_readlane(qb, i), z = __builtin_amdgcn_readlane(qb, i + 1);
-      const bool in = q >= a && q < z;
-      gt[i] += (uint32_t)__builtin_popcountll(ballot(in && fg));
-      eq[i] += (uint32_t)__builtin_popcountll(ballot(in && fe));
-    }
-  };
-#pragma unroll
-  for (int m = 0; m < kCountPre; ++m) {
-    if (q0 + (uint32_t)m * 64 >= q1) break;
-    count(q0 + m * 64 + l, kw[m]);
-  }
-  for (uint32_t q = q0 + kCountPre * 64; q < q1; q += 64) count(q + l, q + l < q1 ? keys[q + l] : 0u);
-  const uint32_t sure_b = (uint32_t)(pb >> 32);
-#pragma unroll
-  for (int i = 0; i < kCountGroups; ++i) {
-    if ((uint32_t)i >= ng) break;
-    uint64_t g = gt[i];
-    if (st.band_low) g += __builtin_amdgcn_readlane(sure_b, i + 1) - __builtin_amdgcn_readlane(sure_b, i);
-    if (l == 0) c.grp_cnt[(uint64_t)j * c.ngrp + g0 + i] = g | ((uint64_t)eq[i] << 32);
-  }
+  uint32_t gt = 0, eq = 0;
+  uint64_t mine = 0;
+  band_tiles(
+      c, j, t0,
+      [&](uint32_t key, bool valid) {
+        gt += (uint32_t)__builtin_popcountll(ballot(valid && key > thr));
+        eq += (uint32_t)__builtin_popcountll(ballot(valid && key == thr));
+      },
+      [&](uint32_t i, uint32_t sure) {
+        gt += sure;
+        if ((i & 1u) || t0 + i + 1 == c.nslot) {
+          if (l == i / 2) mine = (uint64_t)gt | ((uint64_t)eq << 32);
+          gt = eq = 0;
+        }
+      });
+  const uint32_t g = t0 / 2 + l;
+  if (l < (uint32_t)kBandTiles / 2 && g < c.ngrp) c.grp_cnt[(uint64_t)j * c.ngrp + g] = mine;
 }
 
 // Exclusive prefix of nb packed counts, one workgroup.
@@ -1259,19 +1284,16 @@ static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s)
   const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
   k_tile_scan<<<c.jn * nchunk, kBlock, 0, s>>>(c);
   k_post<<<c.jn, kBlock, 0, s>>>(c);
-  const uint32_t ncand = p.any_fast ? c.jn * c.ncb : 0u;
-  if (p.any_fast) {
-    constexpr uint32_t kPerBlock = kGatherSlots * kWaves;
-    k_overflow<<<c.jn * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
-    k_band<<<c.jn * ((c.nslot + kPerBlock - 1) / kPerBlock), kBlock, 0, s>>>(c);
-  }
+  const uint32_t band_blocks = c.jn * ((c.nslot + kBandTiles * kWaves - 1) / (kBandTiles * kWaves));
+  const uint32_t ncand = p.any_fast ? band_blocks : 0u;
+  if (p.any_fast) k_overflow<<<c.jn * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
   for (int pass = 0; pass < 3; ++pass) {
     k_hist_cf<<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand);
     k_find<<<c.jn, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1, 0);
   }
   if (p.any_fast) {
     const uint32_t gb = c.jn * ((c.ngrp + kWaves - 1) / kWaves);
-    k_grp_count<<<c.jn * ((c.ngrp + kCountGroups * kWaves - 1) / (kCountGroups * kWaves)), kBlock, 0, s>>>(c);
+    k_grp_count<<<band_blocks, kBlock, 0, s>>>(c);
     k_grp_scan<<<c.jn, kBlock, 0, s>>>(c);
     k_write_fast<<<gb, kBlock, 0, s>>>(c);
   }
