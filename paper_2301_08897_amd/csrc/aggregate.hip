@@ -36,10 +36,10 @@ __global__ __launch_bounds__(kBlock) void k_fill_u32(uint32_t* p, uint64_t count
 // Entries with idx >= n are skipped (only validation mode reports them).
 // Each wave takes 1024 consecutive entries (16 per lane, all loads in flight);
 // an entry's neighbours come from the adjacent lanes.
-__global__ __launch_bounds__(kBlock) void k_mark(AggArgs a, AggCtx c)
+__global__ __launch_bounds__(kBlock) void k_mark(AggArgs a, AggCtx c, uint32_t j0)
 {
   constexpr int kPer = 16;
-  const uint32_t j = blockIdx.y;
+  const uint32_t j = j0 + blockIdx.y;
   const uint32_t* idx = a.idx[j];
   if (!idx || dense_device(a, c, j)) return;
   const uint64_t k = a.k[j];
@@ -285,7 +285,22 @@ __global__ __launch_bounds__(kBlock) void k_sgd(float* p, const float* g, uint64
 
 __global__ void k_zero_u32(uint32_t* p) { *p = 0u; }
 
-hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate, hipStream_t s)
+// Range markers of devices [j0, j0 + jn).
+hipError_t launch_mark(const AggArgs& a, const AggCtx& c, uint32_t j0, uint32_t jn, hipStream_t s)
+{
+  if (!c.kmax || !jn) return hipSuccess;
+  const uint64_t nm = (uint64_t)jn * c.nrange;
+  uint64_t fb = (nm + kBlock - 1) / kBlock;
+  if (fb > 2048) fb = 2048;
+  k_fill_u32<<<(uint32_t)fb, kBlock, 0, s>>>(c.rbeg + (uint64_t)j0 * c.nrange, nm, kNoEntry);
+  uint64_t mb = (c.kmax + kBlock * 16 - 1) / (kBlock * 16);
+  if (mb > 4096) mb = 4096;
+  k_mark<<<dim3((uint32_t)mb, jn), kBlock, 0, s>>>(a, c, j0);
+  return hipGetLastError();
+}
+
+// marks_done: launch_mark already ran for every device on this stream's past.
+hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate, bool marks_done, hipStream_t s)
 {
   if (c.K) {
     if (validate) {
@@ -293,14 +308,9 @@ hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate
       const uint32_t bx = c.kmax ? (uint32_t)((c.kmax + kBlock - 1) / kBlock) : 1u;
       k_validate<<<dim3(bx, c.K), kBlock, 0, s>>>(a, c);
     }
-    if (c.kmax) {
-      const uint64_t nm = (uint64_t)c.K * c.nrange;
-      uint64_t fb = (nm + kBlock - 1) / kBlock;
-      if (fb > 2048) fb = 2048;
-      k_fill_u32<<<(uint32_t)fb, kBlock, 0, s>>>(c.rbeg, nm, kNoEntry);
-      uint64_t mb = (c.kmax + kBlock * 16 - 1) / (kBlock * 16);
-      if (mb > 4096) mb = 4096;
-      k_mark<<<dim3((uint32_t)mb, c.K), kBlock, 0, s>>>(a, c);
+    if (!marks_done) {
+      const hipError_t e = launch_mark(a, c, 0, c.K, s);
+      if (e != hipSuccess) return e;
     }
   }
   k_aggregate<<<c.nrange, 64, 0, s>>>(a, c);

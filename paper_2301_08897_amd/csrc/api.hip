@@ -65,7 +65,7 @@ ProfRec* prof_slot()
 struct StreamSet {
   bool ready = false;
   hipStream_t s2 = nullptr;
-  hipEvent_t fork[kMaxParts] = {};
+  hipEvent_t done[kMaxParts] = {};   // end of each main pass
   hipEvent_t join = nullptr;
   std::mutex launch_mu;      // one call's launch sequence at a time (the events are shared)
 };
@@ -82,7 +82,7 @@ StreamSet* stream_set()
   StreamSet& ss = g_streams[dev];
   if (!ss.ready) {
     if (hipStreamCreateWithFlags(&ss.s2, hipStreamNonBlocking) != hipSuccess) return nullptr;
-    for (auto& e : ss.fork)
+    for (auto& e : ss.done)
       if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
     if (hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess) return nullptr;
     ss.ready = true;
@@ -292,7 +292,8 @@ uint32_t parts_for(const Layout& L)
 }
 
 scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double delta, double* energies,
-                          uint8_t* compressed, hipStream_t s, ProfRec* pr)
+                          uint8_t* compressed, hipStream_t s, ProfRec* pr, const AggArgs* mark_a = nullptr,
+                          const AggCtx* mark_c = nullptr)
 {
   Ctx c = make_ctx(L, ws);
   c.delta = delta;
@@ -305,13 +306,15 @@ scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double d
   const uint64_t tiles = (uint64_t)L.K * L.tpd;
   p.full_workers = (uint32_t)(tiles < (uint64_t)kFullWorkers ? tiles : (uint64_t)kFullWorkers);
   p.parts = parts_for(L);
+  p.mark_a = mark_a;
+  p.mark_c = mark_c;
   if (pr) pr->parts = p.parts;
   StreamSet* ss = p.parts > 1 ? stream_set() : nullptr;
   if (p.parts > 1 && !ss) return fail(SCADLES_EHIP, "could not create the pipeline stream");
   hipError_t e;
   if (ss) {
     std::lock_guard<std::mutex> lk(ss->launch_mu);
-    e = launch_select(c, a, p, s, ss->s2, ss->fork, ss->join, pr ? pr->ev : nullptr);
+    e = launch_select(c, a, p, s, ss->s2, ss->done, ss->join, pr ? pr->ev : nullptr);
   } else {
     e = launch_select(c, a, p, s, nullptr, nullptr, nullptr, pr ? pr->ev : nullptr);
   }
@@ -424,7 +427,7 @@ scadles_status scadles_weighted_aggregate(const scadles_sparse* sets, const floa
   c.n = n;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const uint32_t validate = g_validate.load() ? 1u : 0u;
-  hipError_t e = launch_aggregate(a, c, validate, s);
+  hipError_t e = launch_aggregate(a, c, validate, false, s);
   if (e != hipSuccess) return hip_fail(e, "aggregate launch");
   if (validate) {
     uint32_t flag = 0;
@@ -497,8 +500,6 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
   ProfRec* pr = prof_slot();
-  if (pr) (void)hipEventRecord(pr->ev[0], s);
-  if (scadles_status st = run_select(L, a, ws, delta, energies, compressed, s, pr)) return st;
   char* b = static_cast<char*>(ws);
   AggCtx c;
   memset(&c, 0, sizeof(c));
@@ -513,7 +514,10 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
   c.nrange = L.nrange;
   c.kmax = (uint32_t)kmax;
   c.n = n;
-  hipError_t e = launch_aggregate(g, c, 0, s);
+  // each device group's range markers are built right after its selection
+  if (pr) (void)hipEventRecord(pr->ev[0], s);
+  if (scadles_status st = run_select(L, a, ws, delta, energies, compressed, s, pr, &g, &c)) return st;
+  hipError_t e = launch_aggregate(g, c, 0, true, s);
   if (pr) (void)hipEventRecord(pr->ev[3 + 2 * pr->parts], s);
   if (e != hipSuccess) return hip_fail(e, "aggregate launch");
   return SCADLES_OK;

@@ -34,7 +34,7 @@ constexpr int kSlotCap = kWaves * kWaveCap;   // entries of one tile's slot regi
 constexpr int kScanChunk = 4096;       // slots per workgroup of the slot-offset scan
 constexpr int kMaxChunks = 256;        // >= ceil(nslot / kScanChunk) for n < 2^32
 constexpr int kGatherSlots = 2;        // tiles per wave in the selection-list and output passes
-constexpr int kOverflowBlocks = 32;    // workgroups per device re-scanning overflowed slots
+constexpr int kOverflowBlocks = 128;   // workgroups per device re-scanning overflowed tiles
 
 enum : uint32_t { kModeFast = 0, kModeExact = 1 };
 
@@ -166,14 +166,17 @@ struct SelectPlan {
   uint32_t sample_blocks;     // sample workgroups per device
   uint32_t full_workers;      // grid-stride workgroups of the exact full-data path
   uint32_t parts;             // device groups, 1 .. kMaxParts
+  const AggArgs* mark_a;      // not null: each group's aggregation range markers are
+  const AggCtx* mark_c;       // built right after its selection (launch_mark)
 };
 
-// Launchers (select.hip, aggregate.hip). fork[parts - 1] and join are events of
+// Launchers (select.hip, aggregate.hip). done[parts] and join are events of
 // the caller's second stream s2; `ev`, when not null, receives the profiling
 // events described at launch_select.
 hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipStream_t s2,
-                         hipEvent_t* fork, hipEvent_t join, hipEvent_t* ev);
-hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate, hipStream_t s);
+                         hipEvent_t* done, hipEvent_t join, hipEvent_t* ev);
+hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate, bool marks_done, hipStream_t s);
+hipError_t launch_mark(const AggArgs& a, const AggCtx& c, uint32_t j0, uint32_t jn, hipStream_t s);
 hipError_t launch_sgd(float* p, const float* g, uint64_t n, float lr, hipStream_t s);
 
 // ---- sizing shared by host and device -----------------------------------------------------

@@ -356,7 +356,8 @@ __device__ inline uint32_t wave_prefix_of_block(uint32_t packed_lane, uint32_t* 
 
 // One round of phase 1 for one wave: sum of squares, counts of candidates
 // (key >= tlo) and sure keys (key >= thi), and the round's candidates staged in
-// LDS in index order (lane, then component) after the `wc` already staged.
+// LDS in index order (lane, then component) after the `wc` already staged, the
+// keys of those below thi (the selection interval) likewise in s_b.
 // kEdge: the round may hold pads (pattern 0xFFFFFFFF), so keys are compared as
 // rank keys (key + 1, pads 0) and fmax drops the pads' NaN from the squares.
 // Counts are wave totals from ballots (scalar popcounts).
@@ -364,17 +365,18 @@ __device__ inline uint32_t wave_prefix_of_block(uint32_t packed_lane, uint32_t* 
 // Entry e of slot s lives at ((rot(s) + e) mod kSlotCap) of the slot's region:
 // the rotation spreads the (short) written part of the regions over all
 // address bits below the region size, so the writes use every memory channel.
+// It is even, so a run starts on a 16-byte boundary.
 static_assert((kSlotCap & (kSlotCap - 1)) == 0, "slot rotation needs a power-of-two region");
-__device__ inline uint32_t slot_rot(uint64_t slot) { return (uint32_t)(slot * 211u) & (kSlotCap - 1u); }
+__device__ inline uint32_t slot_rot(uint64_t slot) { return (uint32_t)(slot * 422u) & (kSlotCap - 2u); }
 
 __device__ inline uint64_t pack_cand(uint32_t i, float v) { return (uint64_t)i | ((uint64_t)__float_as_uint(v) << 32); }
 
 template <bool kEdge>
 __device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32_t thi, double (&e2)[2], uint32_t& wc,
-                                  uint32_t& ws, uint64_t* s_c)
+                                  uint32_t& ws, uint64_t* s_c, uint32_t* s_b)
 {
-  uint64_t b[4];
-  bool f[4];
+  uint64_t b[4], bb[4];
+  bool f[4], fb[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const double xd = (double)x[q];
@@ -383,21 +385,32 @@ __device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32
     const uint32_t key = kEdge ? rank_key(x[q]) : key_of(x[q]);
     const uint32_t lo = kEdge ? tlo + 1u : tlo, hi = kEdge ? thi + 1u : thi;
     f[q] = key >= lo;
+    fb[q] = f[q] && key < hi;
     b[q] = ballot(f[q]);
-    ws += (uint32_t)__builtin_popcountll(ballot(key >= hi));
+    bb[q] = ballot(fb[q]);
   }
   const uint64_t any = b[0] | b[1] | b[2] | b[3];
   if (any == 0ull) return;
+  const uint32_t nb = (uint32_t)(__builtin_popcountll(bb[0]) + __builtin_popcountll(bb[1]) +
+                                 __builtin_popcountll(bb[2]) + __builtin_popcountll(bb[3]));
+  const uint32_t nc = (uint32_t)(__builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) +
+                                 __builtin_popcountll(b[2]) + __builtin_popcountll(b[3]));
+  // wb, the wave's staged selection keys so far, is wc - ws
   uint32_t pos = wc + mbcnt(b[0]) + mbcnt(b[1]) + mbcnt(b[2]) + mbcnt(b[3]);
+  uint32_t bpos = (wc - ws) + mbcnt(bb[0]) + mbcnt(bb[1]) + mbcnt(bb[2]) + mbcnt(bb[3]);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     if (f[q]) {
       if (pos < (uint32_t)kWaveCap) s_c[pos] = pack_cand(i0 + q, x[q]);
       ++pos;
     }
+    if (fb[q]) {
+      if (bpos < (uint32_t)kWaveCap) s_b[bpos] = key_of(x[q]);
+      ++bpos;
+    }
   }
-  wc += (uint32_t)(__builtin_popcountll(b[0]) + __builtin_popcountll(b[1]) + __builtin_popcountll(b[2]) +
-                   __builtin_popcountll(b[3]));
+  wc += nc;
+  ws += nc - nb;
 }
 
 // Each workgroup reads one tile of kTile gradient elements (workgroup b: device
@@ -408,6 +421,7 @@ __device__ inline void main_stage(const f4& x, uint32_t i0, uint32_t tlo, uint32
 __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
 {
   __shared__ uint64_t s_c[kWaves][kWaveCap];
+  __shared__ uint32_t s_b[kWaves][kWaveCap];
   const uint32_t l = lane_id(), w = threadIdx.x >> 6;
   const uint32_t jr = blockIdx.x / c.tpd, tile = blockIdx.x - jr * c.tpd;
   const uint32_t j = c.j0 + jr;
@@ -432,20 +446,22 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
     const uint32_t tlo = c.st[j].t_lo, thi = c.st[j].t_hi;
 #pragma unroll
     for (int r = 0; r < kTileRounds; ++r) {
-      main_stage<false>(v[r], i_base + r * 256, tlo, thi, e2, wc, ws, s_c[w]);
+      main_stage<false>(v[r], i_base + r * 256, tlo, thi, e2, wc, ws, s_c[w], s_b[w]);
       __builtin_amdgcn_sched_barrier(0);    // keep rounds apart: bounds the live ballot masks
     }
   } else {
     const uint32_t tlo = c.st[j].t_lo, thi = c.st[j].t_hi;
     for (int r = 0; r < kTileRounds; ++r)
-      main_stage<true>(load4(row, vbase + wv0 + r * 256, false), i_base + r * 256, tlo, thi, e2, wc, ws, s_c[w]);
+      main_stage<true>(load4(row, vbase + wv0 + r * 256, false), i_base + r * 256, tlo, thi, e2, wc, ws, s_c[w],
+                     s_b[w]);
   }
   // The tile's slot: the waves' staged candidates one after the other (index
   // order), then the keys of the candidates below t_hi (the selection
   // interval [t_lo, t_hi)), two per entry, as one contiguous rotated run; its
   // counts and sum of squares. A tile with a wave chunk over kWaveCap
   // candidates, or whose run would not fit the region, stages nothing and is
-  // recorded for k_overflow, which re-scans it once the slot offsets are known.
+  // recorded for k_overflow, which re-scans it once the slot offsets are known;
+  // its region then holds the per-chunk counts.
   __shared__ uint32_t s_cnt[kWaves];
   __shared__ double s_e[kWaves];
   const double es = wave_sum_f64(e2[0] + e2[1]);
@@ -454,20 +470,20 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
     s_e[w] = es;
   }
   __syncthreads();
-  uint32_t cand = 0, sure = 0, before = 0, bbefore = 0;
+  // cb[i] / kb[i]: candidates / selection keys of the waves before wave i
+  uint32_t cb[kWaves + 1], kb[kWaves + 1];
   bool ovf = false;
+  cb[0] = kb[0] = 0;
 #pragma unroll
   for (int i = 0; i < kWaves; ++i) {
-    const uint32_t v = s_cnt[i];
-    if ((uint32_t)i < w) {
-      before += v & 0xFFFFu;
-      bbefore += (v & 0xFFFFu) - (v >> 16);
-    }
-    cand += v & 0xFFFFu;
-    sure += v >> 16;
-    ovf |= (v & 0xFFFFu) > (uint32_t)kWaveCap;
+    const uint32_t v = s_cnt[i], wci = v & 0xFFFFu;
+    cb[i + 1] = cb[i] + wci;
+    kb[i + 1] = kb[i] + wci - (v >> 16);
+    ovf |= wci > (uint32_t)kWaveCap;
   }
-  ovf |= cand + (cand - sure + 1u) / 2u > (uint32_t)kSlotCap;
+  const uint32_t cand = cb[kWaves], band = kb[kWaves], sure = cand - band;
+  const uint32_t words = 2u * cand + band;     // the run, in 32-bit words
+  ovf |= ((words + 3u) & ~3u) > 2u * (uint32_t)kSlotCap;
   const uint64_t slot = (uint64_t)j * c.nslot + tile;
   if (threadIdx.x == 0) {
     c.slot_cnt[slot] = cand | (ovf ? 0x8000u : 0u) | (sure << 16);
@@ -477,25 +493,37 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
       c.ovf_list[(uint64_t)j * c.nslot + i] = tile;
     }
   }
-  if (!ovf) {
-    // Nontemporal: the slots are read only after the whole pass.
-    GLOBAL uint64_t* sp = gptr(c.slot + slot * kSlotCap);
-    GLOBAL uint32_t* sk = reinterpret_cast<GLOBAL uint32_t*>(sp);
-    const uint32_t rot = slot_rot(slot);
-    const uint32_t kbase = 2u * (rot + cand) + bbefore;      // u32 index of this wave's first key
-    const uint32_t thi = c.st[j].t_hi;
-    uint32_t brun = 0;
-    for (uint32_t i0 = 0; i0 < wc; i0 += 64) {
-      const uint32_t i = i0 + l;
-      const bool valid = i < wc;
-      const uint64_t pe = valid ? s_c[w][i] : 0ull;
-      if (valid) __builtin_nontemporal_store(pe, sp + ((rot + before + i) & (kSlotCap - 1u)));
-      const uint32_t key = (uint32_t)(pe >> 32) & kKeyMask;
-      const bool band = valid && key < thi;
-      const uint64_t bb = ballot(band);
-      if (band) __builtin_nontemporal_store(key, sk + ((kbase + brun + mbcnt(bb)) & (2u * kSlotCap - 1u)));
-      brun += (uint32_t)__builtin_popcountll(bb);
+  GLOBAL uint32_t* sk = reinterpret_cast<GLOBAL uint32_t*>(gptr(c.slot + slot * kSlotCap));
+  if (ovf) {
+    // per-chunk candidate and selection-key counts for k_overflow
+    if (threadIdx.x < 2 * kWaves) {
+      const uint32_t v = s_cnt[threadIdx.x & (kWaves - 1)];
+      sk[threadIdx.x] = threadIdx.x < kWaves ? (v & 0xFFFFu) : (v & 0xFFFFu) - (v >> 16);
     }
+    return;
+  }
+  // The whole workgroup writes the run, 16 bytes per thread, consecutive
+  // threads to consecutive words (nontemporal: the slots are read only after
+  // the whole pass). Words past the run land in the unused part of the region.
+  const uint32_t* c32 = reinterpret_cast<const uint32_t*>(&s_c[0][0]);
+  const uint32_t* b32 = &s_b[0][0];
+  auto word = [&](uint32_t q) -> uint32_t {
+    if (q < 2u * cand) {
+      const uint32_t e = q >> 1;
+      const uint32_t wi = (uint32_t)(e >= cb[1]) + (uint32_t)(e >= cb[2]) + (uint32_t)(e >= cb[3]);
+      const uint32_t base = wi == 0 ? cb[0] : (wi == 1 ? cb[1] : (wi == 2 ? cb[2] : cb[3]));
+      return c32[wi * (2 * kWaveCap) + 2u * (e - base) + (q & 1u)];
+    }
+    const uint32_t i = q - 2u * cand;
+    if (i >= band) return 0u;
+    const uint32_t wi = (uint32_t)(i >= kb[1]) + (uint32_t)(i >= kb[2]) + (uint32_t)(i >= kb[3]);
+    const uint32_t base = wi == 0 ? kb[0] : (wi == 1 ? kb[1] : (wi == 2 ? kb[2] : kb[3]));
+    return b32[wi * kWaveCap + (i - base)];
+  };
+  const uint32_t w0 = 2u * slot_rot(slot);     // first word of the run, a multiple of 4
+  for (uint32_t q = 4u * threadIdx.x; q < words; q += 4u * kBlock) {
+    const u4 v = {word(q), word(q + 1), word(q + 2), word(q + 3)};
+    __builtin_nontemporal_store(v, reinterpret_cast<GLOBAL u4*>(sk + ((w0 + q) & (2u * kSlotCap - 1u))));
   }
 }
 
@@ -802,10 +830,15 @@ __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit v
 // candidates and selection-interval keys than the slot region holds): re-scan
 // the tile and write its candidates, in index order, at the tile's offset in
 // the candidate list, and the keys of those below t_hi at its offset in the
-// band list. One
-// workgroup per tile at a time (tiles i = block, block + blocks, ... of the
-// device's list); wave w takes chunk w, whose offset follows from the counts
-// of the chunks before it.
+// band list. The work items are (tile, chunk) pairs, chunk c being the 4096
+// elements the main pass's wave c read; the main pass left each chunk's
+// candidate and selection-key counts in the tile's (otherwise unused) slot
+// region, so an item's offsets are known without the rest of the tile.
+// Workgroup b of a device takes items b, b + blocks_per_dev, ...; its wave w
+// takes 1024 elements of the chunk. Keys are compared as in the main pass:
+// plain keys in interior tiles, rank keys (key + 1, pads 0) in edge tiles.
+constexpr int kChunkRounds = kTileRounds / kWaves;    // rounds of one wave in one chunk
+
 __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_dev)
 {
   __shared__ uint32_t s_n[kWaves], s_b[kWaves];
@@ -813,28 +846,38 @@ __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_
   const uint32_t j = c.j0 + jr;
   const DevState& st = c.st[j];
   if (st.fallback) return;
-  const uint32_t n_ovf = st.ovf_n;
+  const uint32_t items = st.ovf_n * kWaves;
   const DevDesc d = c.desc[j];
   const uint32_t l = lane_id(), w = threadIdx.x >> 6;
-  const uint32_t tlo1 = st.t_lo + 1u, thi1 = st.t_hi + 1u;   // rank keys: key + 1
   const Row row{gptr(d.grad), d.shift, c.n};
   GLOBAL uint32_t* cidx = gptr(c.cand_idx + d.cand_off);
   GLOBAL float* cval = gptr(c.cand_val + d.cand_off);
   GLOBAL uint32_t* band = gptr(c.band + d.cand_off);
-  for (uint32_t i = b; i < n_ovf; i += blocks_per_dev) {
-    const uint32_t s = c.ovf_list[(uint64_t)j * c.nslot + i];
-    const uint64_t v0 = (uint64_t)s * kTile + (uint64_t)w * (kTileRounds * 256) + l * 4;
-    f4 x[kTileRounds];
+  for (uint32_t it = b; it < items; it += blocks_per_dev) {
+    const uint32_t s = c.ovf_list[(uint64_t)j * c.nslot + it / kWaves], ch = it % kWaves;
+    const uint64_t slot = (uint64_t)j * c.nslot + s;
+    const GLOBAL uint32_t* ccnt = reinterpret_cast<const GLOBAL uint32_t*>(gptr(c.slot) + slot * kSlotCap);
+    const uint64_t vbase = (uint64_t)s * kTile;
+    const bool full = vbase >= row.shift && vbase + kTile <= row.shift + row.n;
+    const uint32_t lo = full ? st.t_lo : st.t_lo + 1u, hi = full ? st.t_hi : st.t_hi + 1u;
+    const uint64_t v0 = vbase + (uint64_t)ch * (kTileRounds * 256) + (uint64_t)w * (kChunkRounds * 256) + l * 4;
+    f4 x[kChunkRounds];
 #pragma unroll
-    for (int r = 0; r < kTileRounds; ++r) x[r] = load4(row, v0 + (uint64_t)r * 256, false);
+    for (int r = 0; r < kChunkRounds; ++r) x[r] = load4(row, v0 + (uint64_t)r * 256, false);
+    uint32_t cb = 0, bb0 = 0;       // candidates and selection keys of the chunks before
+    for (uint32_t u = 0; u < ch; ++u) {
+      cb += ccnt[u];
+      bb0 += ccnt[kWaves + u];
+    }
+    auto key = [&](float v) { return full ? key_of(v) : rank_key(v); };
     uint32_t cnt = 0, bcnt = 0;
 #pragma unroll
-    for (int r = 0; r < kTileRounds; ++r)
+    for (int r = 0; r < kChunkRounds; ++r)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const uint32_t rk = rank_key(x[r][q]);
-        cnt += (uint32_t)__builtin_popcountll(ballot(rk >= tlo1));
-        bcnt += (uint32_t)__builtin_popcountll(ballot(rk >= tlo1 && rk < thi1));
+        const uint32_t kq = key(x[r][q]);
+        cnt += (uint32_t)__builtin_popcountll(ballot(kq >= lo));
+        bcnt += (uint32_t)__builtin_popcountll(ballot(kq >= lo && kq < hi));
       }
     if (l == 0) {
       s_n[w] = cnt;
@@ -842,27 +885,27 @@ __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_
     }
     __syncthreads();
     const uint64_t pre = slot_pre(c, j, s);
-    uint64_t run = (uint32_t)pre;
-    uint64_t brun = (uint32_t)pre - (uint32_t)(pre >> 32);
+    uint64_t run = (uint32_t)pre + cb;
+    uint64_t brun = (uint32_t)pre - (uint32_t)(pre >> 32) + bb0;
     for (uint32_t u = 0; u < w; ++u) {
       run += s_n[u];
       brun += s_b[u];
     }
     __syncthreads();
 #pragma unroll
-    for (int r = 0; r < kTileRounds; ++r) {
+    for (int r = 0; r < kChunkRounds; ++r) {
       bool f[4], fb[4];
-      uint64_t bm[4], bb[4];
+      uint64_t bm[4], bbm[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const uint32_t rk = rank_key(x[r][q]);
-        f[q] = rk >= tlo1;
-        fb[q] = f[q] && rk < thi1;
+        const uint32_t kq = key(x[r][q]);
+        f[q] = kq >= lo;
+        fb[q] = f[q] && kq < hi;
         bm[q] = ballot(f[q]);
-        bb[q] = ballot(fb[q]);
+        bbm[q] = ballot(fb[q]);
       }
       uint64_t pos = run + mbcnt(bm[0]) + mbcnt(bm[1]) + mbcnt(bm[2]) + mbcnt(bm[3]);
-      uint64_t bpos = brun + mbcnt(bb[0]) + mbcnt(bb[1]) + mbcnt(bb[2]) + mbcnt(bb[3]);
+      uint64_t bpos = brun + mbcnt(bbm[0]) + mbcnt(bbm[1]) + mbcnt(bbm[2]) + mbcnt(bbm[3]);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         if (f[q]) {
@@ -873,14 +916,14 @@ __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_
           ++pos;
         }
         if (fb[q]) {
-          if (bpos < d.cap) band[bpos] = rank_key(x[r][q]) - 1u;
+          if (bpos < d.cap) band[bpos] = key_of(x[r][q]);
           ++bpos;
         }
       }
       run += __builtin_popcountll(bm[0]) + __builtin_popcountll(bm[1]) + __builtin_popcountll(bm[2]) +
              __builtin_popcountll(bm[3]);
-      brun += __builtin_popcountll(bb[0]) + __builtin_popcountll(bb[1]) + __builtin_popcountll(bb[2]) +
-              __builtin_popcountll(bb[3]);
+      brun += __builtin_popcountll(bbm[0]) + __builtin_popcountll(bbm[1]) + __builtin_popcountll(bbm[2]) +
+              __builtin_popcountll(bbm[3]);
     }
   }
 }
@@ -1278,40 +1321,49 @@ __global__ __launch_bounds__(kBlock) void k_final(Ctx c)
 }
 
 // ---- host-side launchers ---------------------------------------------------------------------
-// Everything after the main pass for devices [c.j0, c.j0 + c.jn), on stream s.
-static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s)
+// Everything after the main pass for devices [c.j0, c.j0 + c.jn), on stream s,
+// in two halves: 0, the threshold (scans, path decision, overflowed tiles,
+// radix passes, group counts and offsets), latency-bound and light on memory;
+// 1, the output (ordered compaction, energies and decision, range markers),
+// which moves most of the bytes.
+static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s, int half)
 {
-  const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
-  k_tile_scan<<<c.jn * nchunk, kBlock, 0, s>>>(c);
-  k_post<<<c.jn, kBlock, 0, s>>>(c);
   const uint32_t band_blocks = c.jn * ((c.nslot + kBandTiles * kWaves - 1) / (kBandTiles * kWaves));
-  const uint32_t ncand = p.any_fast ? band_blocks : 0u;
-  if (p.any_fast) k_overflow<<<c.jn * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
-  for (int pass = 0; pass < 3; ++pass) {
-    k_hist_cf<<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand);
-    k_find<<<c.jn, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1, 0);
+  if (half == 0) {
+    const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
+    k_tile_scan<<<c.jn * nchunk, kBlock, 0, s>>>(c);
+    k_post<<<c.jn, kBlock, 0, s>>>(c);
+    const uint32_t ncand = p.any_fast ? band_blocks : 0u;
+    if (p.any_fast) k_overflow<<<c.jn * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
+    for (int pass = 0; pass < 3; ++pass) {
+      k_hist_cf<<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand);
+      k_find<<<c.jn, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1, 0);
+    }
+    if (p.any_fast) {
+      k_grp_count<<<band_blocks, kBlock, 0, s>>>(c);
+      k_grp_scan<<<c.jn, kBlock, 0, s>>>(c);
+    }
+    return;
   }
-  if (p.any_fast) {
-    const uint32_t gb = c.jn * ((c.ngrp + kWaves - 1) / kWaves);
-    k_grp_count<<<band_blocks, kBlock, 0, s>>>(c);
-    k_grp_scan<<<c.jn, kBlock, 0, s>>>(c);
-    k_write_fast<<<gb, kBlock, 0, s>>>(c);
-  }
+  if (p.any_fast) k_write_fast<<<c.jn * ((c.ngrp + kWaves - 1) / kWaves), kBlock, 0, s>>>(c);
   k_count_cf<<<p.full_workers, kBlock, 0, s>>>(c);
   k_scan<<<c.jn, kBlock, 0, s>>>(c);
   k_write_cf<<<p.full_workers, kBlock, 0, s>>>(c);
   k_final<<<c.jn, kBlock, 0, s>>>(c);
+  if (p.mark_a) (void)launch_mark(*p.mark_a, *p.mark_c, c.j0, c.jn, s);
 }
 
-// The whole selection. The devices are split into p.parts groups: the main
-// pass of group i runs on s; once it is done, the rest of group i's selection
-// runs on s2 while the main pass of group i + 1 runs on s (the last group's
-// rest runs on s), and s waits for s2 at the end. A main pass is bound by HBM
-// bandwidth and the later kernels mostly by latency, so they overlap well.
-// Profiling events (ev, optional): 0 start, 1 bracket done, 2 + 2i / 3 + 2i
-// around the main pass of group i, 2 + 2 * parts all done.
+// The whole selection. The devices are split into p.parts groups whose main
+// passes run one after the other on s. A main pass is bound by HBM bandwidth,
+// the threshold half of the rest of a group's selection by latency: that half
+// of group i runs on s2 while the main pass of group i + 1 runs on s, and the
+// output half of group i, which moves more bytes, only once that main pass is
+// done (the last group's rest runs on s); s waits for s2 at the end.
+// done[i] (events of s2's owner) mark the end of main pass i. Profiling events
+// (ev, optional): 0 start, 1 bracket done, 2 + 2i / 3 + 2i around the main
+// pass of group i, 2 + 2 * parts all done.
 hipError_t launch_select(const Ctx& c0, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipStream_t s2,
-                         hipEvent_t* fork, hipEvent_t join, hipEvent_t* ev)
+                         hipEvent_t* done, hipEvent_t join, hipEvent_t* ev)
 {
   Ctx c = c0;
   c.j0 = 0;
@@ -1330,20 +1382,28 @@ hipError_t launch_select(const Ctx& c0, const PrepArgs& a, const SelectPlan& p, 
   GradArgs ga;
   for (uint32_t j = 0; j < c.K; ++j) ga.grad[j] = a.grad[j];
   const uint32_t parts = p.parts;
-  for (uint32_t i = 0; i < parts; ++i) {
+  auto group = [&](uint32_t i) {
     Ctx ci = c;
     ci.j0 = c.K * i / parts;
     ci.jn = c.K * (i + 1) / parts - ci.j0;
+    return ci;
+  };
+  for (uint32_t i = 0; i < parts; ++i) {
+    const Ctx ci = group(i);
     if (ev) (void)hipEventRecord(ev[2 + 2 * i], s);
     k_main<<<ci.jn * c.tpd, kBlock, 0, s>>>(ci, ga);
     if (ev) (void)hipEventRecord(ev[3 + 2 * i], s);
-    if (i + 1 < parts) {
-      hipError_t e = hipEventRecord(fork[i], s);
-      if (e == hipSuccess) e = hipStreamWaitEvent(s2, fork[i], 0);
+    if (parts > 1) {
+      hipError_t e = hipEventRecord(done[i], s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(s2, done[i], 0);
       if (e != hipSuccess) return e;
-      launch_post(ci, p, s2);
+    }
+    if (i > 0) launch_post(group(i - 1), p, s2, 1);
+    if (i + 1 < parts) {
+      launch_post(ci, p, s2, 0);
     } else {
-      launch_post(ci, p, s);
+      launch_post(ci, p, s, 0);
+      launch_post(ci, p, s, 1);
     }
   }
   if (parts > 1) {
