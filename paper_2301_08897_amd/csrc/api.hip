@@ -196,7 +196,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
     L.o_coff = take(sizeof(uint64_t) * (size_t)K * kMaxChunks);
     L.o_ce = take(sizeof(double) * (size_t)K * kMaxChunks);
     L.o_olist = take(sizeof(uint32_t) * (size_t)K * L.nslot);
-    L.o_slot = take(sizeof(uint64_t) * nslots * kSlotCap);
+    L.o_slot = take(sizeof(uint32_t) * nslots * kSlotWords);
     L.o_epart = take(sizeof(double) * (size_t)K * L.nslot);
     L.o_cidx = take(sizeof(uint32_t) * sum_cap);
     L.o_cval = take(sizeof(float) * sum_cap);
@@ -229,7 +229,7 @@ Ctx make_ctx(const Layout& L, void* ws)
   c.chunk_off = reinterpret_cast<uint64_t*>(b + L.o_coff);
   c.chunk_e = reinterpret_cast<double*>(b + L.o_ce);
   c.ovf_list = reinterpret_cast<uint32_t*>(b + L.o_olist);
-  c.slot = reinterpret_cast<uint64_t*>(b + L.o_slot);
+  c.slot = reinterpret_cast<uint32_t*>(b + L.o_slot);
   c.epart = reinterpret_cast<double*>(b + L.o_epart);
   c.cand_idx = reinterpret_cast<uint32_t*>(b + L.o_cidx);
   c.cand_val = reinterpret_cast<float*>(b + L.o_cval);

@@ -30,7 +30,7 @@ constexpr uint32_t kKeyMask = 0x7FFFFFFFu;
 constexpr uint64_t kSat31 = 0x7FFFFFFFull;
 constexpr int kFullWorkers = 1024;     // grid of the grid-stride exact-path kernels
 constexpr int kWaveCap = 512;          // main pass: candidates one wave chunk (4096 elements) can stage
-constexpr int kSlotCap = kWaves * kWaveCap;   // entries of one tile's slot region
+constexpr int kSlotWords = 1024;       // 32-bit words of one tile's slot region (4 KiB)
 constexpr int kScanChunk = 4096;       // slots per workgroup of the slot-offset scan
 constexpr int kMaxChunks = 256;        // >= ceil(nslot / kScanChunk) for n < 2^32
 constexpr int kGatherSlots = 2;        // tiles per wave in the selection-list and output passes
@@ -90,8 +90,8 @@ struct Ctx {
   uint64_t* chunk_tot;    // [K][kMaxChunks] candidate | sure << 32 totals of each scan chunk
   uint64_t* chunk_off;    // [K][kMaxChunks] candidate | sure << 32 counts before each scan chunk
   double* chunk_e;        // [K][kMaxChunks] sum of squares of each scan chunk
-  uint64_t* slot;         // [K][nslot][kSlotCap] per tile: staged candidates (index | value bits << 32),
-                          // then the keys of those below t_hi, two per entry; one rotated run
+  uint32_t* slot;         // [K][nslot][kSlotWords] per tile: candidates' value bits, then the keys of those
+                          // below t_hi; from the top down, the candidates' 16-bit offsets in the tile
   uint32_t* ovf_list;     // [K][nslot] tiles with a wave chunk of more than kWaveCap candidates
   double* epart;          // [K][nslot] sum of squares per tile, later kept sum of squares per write group
   uint32_t* cand_idx;     // candidate regions (entries of overflowed slots only)

@@ -362,12 +362,14 @@ __device__ inline uint32_t wave_prefix_of_block(uint32_t packed_lane, uint32_t* 
 // rank keys (key + 1, pads 0) and fmax drops the pads' NaN from the squares.
 // Counts are wave totals from ballots (scalar popcounts).
 // A staged candidate: its index in the low word, its value's bits in the high word.
-// Entry e of slot s lives at ((rot(s) + e) mod kSlotCap) of the slot's region:
-// the rotation spreads the (short) written part of the regions over all
-// address bits below the region size, so the writes use every memory channel.
-// It is even, so a run starts on a 16-byte boundary.
-static_assert((kSlotCap & (kSlotCap - 1)) == 0, "slot rotation needs a power-of-two region");
-__device__ inline uint32_t slot_rot(uint64_t slot) { return (uint32_t)(slot * 422u) & (kSlotCap - 2u); }
+// A tile's slot region (kSlotWords words, consecutive tiles back to back):
+// word e < cand holds candidate e's value bits, words cand .. cand + band - 1
+// the keys of the candidates below t_hi (the selection interval), and the
+// 16-bit word (2 * kSlotWords - 1 - e) candidate e's offset in the tile
+// (index = tile * kTile - shift + offset). Both ends are written as whole
+// 16-byte chunks; a tile whose two parts would meet overflows.
+static_assert((kSlotWords & (kSlotWords - 1)) == 0, "slot positions wrap inside a power-of-two region");
+__device__ inline uint32_t slot_off16_at(uint32_t e) { return 2u * kSlotWords - 1u - e; }
 
 __device__ inline uint64_t pack_cand(uint32_t i, float v) { return (uint64_t)i | ((uint64_t)__float_as_uint(v) << 32); }
 
@@ -482,8 +484,8 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
     ovf |= wci > (uint32_t)kWaveCap;
   }
   const uint32_t cand = cb[kWaves], band = kb[kWaves], sure = cand - band;
-  const uint32_t words = 2u * cand + band;     // the run, in 32-bit words
-  ovf |= ((words + 3u) & ~3u) > 2u * (uint32_t)kSlotCap;
+  const uint32_t na = (cand + band + 3u) / 4u, nbk = ((cand + 1u) / 2u + 3u) / 4u;   // 16-byte chunks of both ends
+  ovf |= 4u * (na + nbk) > (uint32_t)kSlotWords;
   const uint64_t slot = (uint64_t)j * c.nslot + tile;
   if (threadIdx.x == 0) {
     c.slot_cnt[slot] = cand | (ovf ? 0x8000u : 0u) | (sure << 16);
@@ -493,37 +495,50 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
       c.ovf_list[(uint64_t)j * c.nslot + i] = tile;
     }
   }
-  GLOBAL uint32_t* sk = reinterpret_cast<GLOBAL uint32_t*>(gptr(c.slot + slot * kSlotCap));
+  GLOBAL uint32_t* reg = gptr(c.slot) + slot * kSlotWords;
   if (ovf) {
     // per-chunk candidate and selection-key counts for k_overflow
     if (threadIdx.x < 2 * kWaves) {
       const uint32_t v = s_cnt[threadIdx.x & (kWaves - 1)];
-      sk[threadIdx.x] = threadIdx.x < kWaves ? (v & 0xFFFFu) : (v & 0xFFFFu) - (v >> 16);
+      reg[threadIdx.x] = threadIdx.x < kWaves ? (v & 0xFFFFu) : (v & 0xFFFFu) - (v >> 16);
     }
     return;
   }
-  // The whole workgroup writes the run, 16 bytes per thread, consecutive
-  // threads to consecutive words (nontemporal: the slots are read only after
-  // the whole pass). Words past the run land in the unused part of the region.
+  // The whole workgroup writes both ends, 16 bytes per thread (nontemporal:
+  // the slots are read only after the whole pass).
   const uint32_t* c32 = reinterpret_cast<const uint32_t*>(&s_c[0][0]);
   const uint32_t* b32 = &s_b[0][0];
-  auto word = [&](uint32_t q) -> uint32_t {
-    if (q < 2u * cand) {
-      const uint32_t e = q >> 1;
-      const uint32_t wi = (uint32_t)(e >= cb[1]) + (uint32_t)(e >= cb[2]) + (uint32_t)(e >= cb[3]);
-      const uint32_t base = wi == 0 ? cb[0] : (wi == 1 ? cb[1] : (wi == 2 ? cb[2] : cb[3]));
-      return c32[wi * (2 * kWaveCap) + 2u * (e - base) + (q & 1u)];
-    }
-    const uint32_t i = q - 2u * cand;
+  auto cand_word = [&](uint32_t e, uint32_t half) -> uint32_t {    // half 0: index, 1: value bits
+    const uint32_t wi = (uint32_t)(e >= cb[1]) + (uint32_t)(e >= cb[2]) + (uint32_t)(e >= cb[3]);
+    const uint32_t base = wi == 0 ? cb[0] : (wi == 1 ? cb[1] : (wi == 2 ? cb[2] : cb[3]));
+    return c32[wi * (2 * kWaveCap) + 2u * (e - base) + half];
+  };
+  auto low_word = [&](uint32_t q) -> uint32_t {
+    if (q < cand) return cand_word(q, 1u);
+    const uint32_t i = q - cand;
     if (i >= band) return 0u;
     const uint32_t wi = (uint32_t)(i >= kb[1]) + (uint32_t)(i >= kb[2]) + (uint32_t)(i >= kb[3]);
     const uint32_t base = wi == 0 ? kb[0] : (wi == 1 ? kb[1] : (wi == 2 ? kb[2] : kb[3]));
     return b32[wi * kWaveCap + (i - base)];
   };
-  const uint32_t w0 = 2u * slot_rot(slot);     // first word of the run, a multiple of 4
-  for (uint32_t q = 4u * threadIdx.x; q < words; q += 4u * kBlock) {
-    const u4 v = {word(q), word(q + 1), word(q + 2), word(q + 3)};
-    __builtin_nontemporal_store(v, reinterpret_cast<GLOBAL u4*>(sk + ((w0 + q) & (2u * kSlotCap - 1u))));
+  const uint32_t ibase = (uint32_t)(vbase - row.shift);   // index of tile position 0 (mod 2^32)
+  auto off16 = [&](uint32_t e) -> uint32_t { return e < cand ? (cand_word(e, 0u) - ibase) & 0xFFFFu : 0u; };
+  for (uint32_t t = threadIdx.x; t < na + nbk; t += kBlock) {
+    u4 v;
+    uint32_t p0;
+    if (t < na) {
+      p0 = 4u * t;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = low_word(p0 + i);
+    } else {
+      p0 = kSlotWords - 4u * nbk + 4u * (t - na);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t e_lo = slot_off16_at(2u * (p0 + i));     // candidate in the word's low half
+        v[i] = off16(e_lo) | (off16(e_lo - 1u) << 16);
+      }
+    }
+    __builtin_nontemporal_store(v, reinterpret_cast<GLOBAL u4*>(reg + p0));
   }
 }
 
@@ -657,106 +672,9 @@ __device__ inline uint64_t slot_pre(const Ctx& c, uint32_t j, uint32_t s)
   return c.chunk_off[(uint64_t)j * kMaxChunks + s / kScanChunk] + c.slot_off[(uint64_t)j * c.nslot + s];
 }
 
-// Entry e of a slot: from its staged pairs, or (overflowed slot) from the
-// candidate list where k_overflow wrote it.
-struct SlotSrc {
-  const GLOBAL uint64_t* pairs;   // null: overflowed
-  uint32_t rot;
-  const GLOBAL uint32_t* ci;
-  const GLOBAL float* cv;
-};
-
-__device__ inline SlotSrc slot_src(const Ctx& c, uint32_t j, uint32_t s, uint32_t ovf, uint32_t cand_at)
-{
-  SlotSrc r;
-  if (!ovf) {
-    const uint64_t slot = (uint64_t)j * c.nslot + s;
-    r.pairs = gptr(c.slot) + slot * kSlotCap;
-    r.rot = slot_rot(slot);
-    r.ci = nullptr;
-    r.cv = nullptr;
-  } else {
-    const uint64_t o = c.desc[j].cand_off + cand_at;
-    r.pairs = nullptr;
-    r.rot = 0;
-    r.ci = gptr(c.cand_idx) + o;
-    r.cv = gptr(c.cand_val) + o;
-  }
-  return r;
-}
-
-__device__ inline uint64_t slot_entry(const SlotSrc& r, uint32_t e)
-{
-  if (r.pairs) return r.pairs[(r.rot + e) & (kSlotCap - 1u)];
-  return (uint64_t)r.ci[e] | ((uint64_t)__float_as_uint(r.cv[e]) << 32);
-}
-
-__device__ inline uint32_t entry_key(uint64_t p) { return (uint32_t)(p >> 32) & kKeyMask; }
-
-// Walks the entries of tiles s0 .. s0 + kGatherSlots - 1 of device j in index
-// order, 64 at a time: begin(i, pre) opens tile s0 + i (pre: its candidate |
-// sure << 32 offsets), visit(p, valid) takes one 64-entry window. The tiles'
-// counts and the first kPre windows of every tile are loaded at once, without
-// conditions (a slot region always holds kSlotCap entries and tile indices are
-// clamped, so every load is in bounds; entries past a tile's count are
-// ignored). Overflowed tiles, whose entries are in the candidate list, reload
-// them once their offset is known.
-constexpr int kPre = 1;
-
-template <class Begin, class Visit>
-__device__ inline void walk_tiles(const Ctx& c, uint32_t j, uint32_t s0, Begin begin, Visit visit)
-{
-  const uint32_t l = lane_id();
-  const uint32_t last = c.nslot - 1;
-  const uint32_t sl0 = s0 + (l < (uint32_t)kGatherSlots ? l : (uint32_t)kGatherSlots - 1u);
-  const uint32_t sl = sl0 < last ? sl0 : last;
-  const uint32_t m_v = c.slot_cnt[(uint64_t)j * c.nslot + sl];
-  const uint64_t m_pre = c.chunk_off[(uint64_t)j * kMaxChunks + sl / kScanChunk] + c.slot_off[(uint64_t)j * c.nslot + sl];
-  uint64_t r[kGatherSlots][kPre];
-#pragma unroll
-  for (int i = 0; i < kGatherSlots; ++i) {
-    const uint64_t slot = (uint64_t)j * c.nslot + (s0 + i < last ? s0 + i : last);
-    const GLOBAL uint64_t* base = gptr(c.slot) + slot * kSlotCap;
-    const uint32_t rot = slot_rot(slot);
-#pragma unroll
-    for (int m = 0; m < kPre; ++m) r[i][m] = base[(rot + m * 64 + l) & (kSlotCap - 1u)];
-  }
-#pragma unroll
-  for (int i = 0; i < kGatherSlots; ++i) {
-    const uint32_t v = __builtin_amdgcn_readlane(m_v, i);
-    const uint32_t cn = s0 + i < c.nslot ? v & 0x7FFFu : 0u;
-    const uint32_t ovf = (v >> 15) & 1u;
-    const uint64_t pre = ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(m_pre >> 32), i) << 32) |
-                         __builtin_amdgcn_readlane((uint32_t)m_pre, i);
-    if (cn && ovf) {
-      const SlotSrc src = slot_src(c, j, s0 + i, 1u, (uint32_t)pre);
-#pragma unroll
-      for (int m = 0; m < kPre; ++m) r[i][m] = m * 64 + l < cn ? slot_entry(src, m * 64 + l) : 0ull;
-    }
-    begin(i, pre);
-#pragma unroll
-    for (int m = 0; m < kPre; ++m) {
-      if ((uint32_t)m * 64 >= cn) break;
-      visit(r[i][m], m * 64 + l < cn);
-    }
-    if (cn > (uint32_t)(kPre * 64)) {
-      // one window ahead: the next window's load is in flight while this one is used
-      const SlotSrc src = slot_src(c, j, s0 + i, ovf, (uint32_t)pre);
-      uint32_t e0 = kPre * 64;
-      uint64_t cur = e0 + l < cn ? slot_entry(src, e0 + l) : 0ull;
-      for (; e0 < cn; e0 += 64) {
-        const uint32_t e1 = e0 + 64;
-        const uint64_t nxt = (e1 < cn && e1 + l < cn) ? slot_entry(src, e1 + l) : 0ull;
-        visit(cur, e0 + l < cn);
-        cur = nxt;
-      }
-    }
-  }
-}
-
 // ---- 3. selection-interval keys per tile ---------------------------------------------------
 // The keys of a tile's candidates below t_hi (the selection interval [t_lo,
-// t_hi)) follow its candidates in the slot region, two per entry; k_overflow
+// t_hi)) follow its candidates' values in the slot region; k_overflow
 // writes those of an overflowed tile to the device's band list at the tile's
 // band offset (candidates - sure keys before it). band_tiles walks them for
 // tiles t0 .. t0 + kBandTiles - 1 of device j, tile after tile, in index order
@@ -764,7 +682,7 @@ __device__ inline void walk_tiles(const Ctx& c, uint32_t j, uint32_t s0, Begin b
 // sure) closes tile t0 + i (sure: its keys >= t_hi). Lane l holds tile t0 +
 // l's counts. The first window of kBandBatch tiles is loaded at once, and
 // longer runs four windows at once, without conditions: tile indices are
-// clamped, region positions wrap inside the region (2 * kSlotCap keys) and
+// clamped, region positions wrap inside the region and
 // band-list positions are clamped into the tile's run, so every load is in
 // bounds; keys past a tile's count are ignored.
 constexpr int kBandTiles = 32;
@@ -773,7 +691,7 @@ constexpr int kBandBatch = 8;
 template <class Visit, class Done>
 __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit visit, Done done)
 {
-  constexpr uint32_t kMask = 2u * kSlotCap - 1u;
+  constexpr uint32_t kMask = kSlotWords - 1u;
   const uint32_t l = lane_id();
   const uint32_t last = c.nslot - 1;
   const uint64_t row = (uint64_t)j * c.nslot;
@@ -781,13 +699,13 @@ __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit v
   const uint32_t v = t0 + l < c.nslot ? c.slot_cnt[row + tl] : 0u;
   const uint32_t cand = v & 0x7FFFu, sure = v >> 16, nb = cand - sure;
   const uint32_t ovf = (v >> 15) & 1u;
-  uint32_t kb = 2u * (slot_rot(row + tl) + cand);       // first key: 32-bit word of the region ...
+  uint32_t kb = cand;                                   // first key: word of the region ...
   if (ovf) {
     const uint64_t pre = slot_pre(c, j, tl);
     kb = (uint32_t)pre - (uint32_t)(pre >> 32);         // ... or position in the band list
   }
   const uint32_t nt = c.nslot - t0 < (uint32_t)kBandTiles ? c.nslot - t0 : (uint32_t)kBandTiles;
-  const GLOBAL uint32_t* reg = reinterpret_cast<const GLOBAL uint32_t*>(gptr(c.slot));
+  const GLOBAL uint32_t* reg = gptr(c.slot);
   const GLOBAL uint32_t* blist = gptr(c.band) + c.desc[j].cand_off;
   // windows e0 .. of a run of nbi keys, four at a time; key_at(e) is in bounds for every e
   auto run = [&](uint32_t e0, uint32_t nbi, auto key_at) {
@@ -806,7 +724,7 @@ __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit v
     for (int q = 0; q < kBandBatch; ++q) {
       const uint32_t i = i0 + q;     // < kBandTiles
       const uint32_t ti = t0 + i < last ? t0 + i : last;
-      kv[q] = reg[(row + ti) * (2u * kSlotCap) + ((__builtin_amdgcn_readlane(kb, i) + l) & kMask)];
+      kv[q] = reg[(row + ti) * kSlotWords + ((__builtin_amdgcn_readlane(kb, i) + l) & kMask)];
     }
 #pragma unroll
     for (int q = 0; q < kBandBatch; ++q) {
@@ -815,7 +733,7 @@ __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit v
       const uint32_t nbi = __builtin_amdgcn_readlane(nb, i), kbi = __builtin_amdgcn_readlane(kb, i);
       if (!__builtin_amdgcn_readlane(ovf, i)) {
         visit(kv[q], l < nbi);
-        const GLOBAL uint32_t* base = reg + (row + t0 + i) * (2u * kSlotCap);
+        const GLOBAL uint32_t* base = reg + (row + t0 + i) * kSlotWords;
         if (nbi > 64u) run(64u, nbi, [&](uint32_t e) { return base[(kbi + e) & kMask]; });
       } else if (nbi) {
         const GLOBAL uint32_t* p = blist + kbi;
@@ -856,7 +774,7 @@ __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_
   for (uint32_t it = b; it < items; it += blocks_per_dev) {
     const uint32_t s = c.ovf_list[(uint64_t)j * c.nslot + it / kWaves], ch = it % kWaves;
     const uint64_t slot = (uint64_t)j * c.nslot + s;
-    const GLOBAL uint32_t* ccnt = reinterpret_cast<const GLOBAL uint32_t*>(gptr(c.slot) + slot * kSlotCap);
+    const GLOBAL uint32_t* ccnt = gptr(c.slot) + slot * kSlotWords;
     const uint64_t vbase = (uint64_t)s * kTile;
     const bool full = vbase >= row.shift && vbase + kTile <= row.shift + row.n;
     const uint32_t lo = full ? st.t_lo : st.t_lo + 1u, hi = full ? st.t_hi : st.t_hi + 1u;
@@ -1057,8 +975,13 @@ __global__ __launch_bounds__(kBlock) void k_grp_scan(Ctx c)
   block_excl_scan_u64(c.grp_cnt + (uint64_t)j * c.ngrp, c.grp_pre + (uint64_t)j * c.ngrp, c.ngrp, s_w);
 }
 
-// One wave per group: its tiles' candidates in index order, kept ones written
-// to the device's outputs; the kept sum of squares goes to epart[j][group].
+// One wave per group of kGatherSlots tiles: their candidates in index order,
+// kept ones written to the device's outputs; the kept sum of squares goes to
+// epart[j][group]. A tile's values and offsets are loaded kWriteBatch windows
+// at a time (positions clamped into the tile's candidates); an overflowed
+// tile's entries come from the candidate list.
+constexpr int kWriteBatch = 8;
+
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_write_fast(Ctx c)
 {
   const uint32_t bpd = (c.ngrp + kWaves - 1) / kWaves;
@@ -1073,32 +996,75 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) 
   const DevDesc d = c.desc[j];
   GLOBAL uint32_t* oi = gptr(d.idx_out);
   GLOBAL float* ov = gptr(d.val_out);
+  const uint32_t l = lane_id();
+  const uint32_t s0 = g * kGatherSlots;
+  // lane i < kGatherSlots: tile s0 + i's counts (and list offset when it overflowed)
+  const uint32_t sl = s0 + (l < (uint32_t)kGatherSlots ? l : 0u);
+  const bool live = l < (uint32_t)kGatherSlots && sl < c.nslot;
+  const uint32_t cnt = live ? c.slot_cnt[(uint64_t)j * c.nslot + sl] : 0u;
+  const uint32_t at = ((cnt >> 15) & 1u) ? (uint32_t)slot_pre(c, j, sl) : 0u;
   // 32-bit counts and positions: k < 2^32
   const uint64_t pre = c.grp_pre[(uint64_t)j * c.ngrp + g];
   uint32_t run_g = (uint32_t)pre, run_e = (uint32_t)(pre >> 32);
   const uint32_t need32 = (uint32_t)need, k32 = d.k;
   double e2 = 0.0;
-  walk_tiles(
-      c, j, g * kGatherSlots, [](int, uint64_t) {},
-      [&](uint64_t p, bool valid) {
-        const uint32_t key = entry_key(p);
-        const bool fg = valid && key > thr, fe = valid && key == thr;
-        const uint64_t bg = ballot(fg), be = ballot(fe);
-        const uint32_t gt_b = run_g + mbcnt(bg), eq_b = run_e + mbcnt(be);
-        if (fg || (fe && eq_b < need32)) {
-          const uint32_t pos = gt_b + (eq_b < need32 ? eq_b : need32);
-          const float v = __uint_as_float((uint32_t)(p >> 32));
-          if (pos < k32) {
-            oi[pos] = (uint32_t)p;
-            ov[pos] = v;
-          }
-          e2 = __builtin_fma((double)v, (double)v, e2);
-        }
-        run_g += (uint32_t)__builtin_popcountll(bg);
-        run_e += (uint32_t)__builtin_popcountll(be);
+  auto visit = [&](uint32_t idx, uint32_t vb, bool valid) {
+    const uint32_t key = vb & kKeyMask;
+    const bool fg = valid && key > thr, fe = valid && key == thr;
+    const uint64_t bg = ballot(fg), be = ballot(fe);
+    const uint32_t gt_b = run_g + mbcnt(bg), eq_b = run_e + mbcnt(be);
+    if (fg || (fe && eq_b < need32)) {
+      const uint32_t pos = gt_b + (eq_b < need32 ? eq_b : need32);
+      const float v = __uint_as_float(vb);
+      if (pos < k32) {
+        oi[pos] = idx;
+        ov[pos] = v;
+      }
+      e2 = __builtin_fma((double)v, (double)v, e2);
+    }
+    run_g += (uint32_t)__builtin_popcountll(bg);
+    run_e += (uint32_t)__builtin_popcountll(be);
+  };
+  // windows e0 .. of a tile's cn entries: ld(e, vb, idx) loads entry e (e < cn)
+  auto walk = [&](uint32_t cn, auto ld) {
+    for (uint32_t e0 = 0; e0 < cn; e0 += kWriteBatch * 64) {
+      uint32_t vb[kWriteBatch], ix[kWriteBatch];
+#pragma unroll
+      for (int m = 0; m < kWriteBatch; ++m) {
+        vb[m] = ix[m] = 0u;
+        const uint32_t e = e0 + m * 64 + l;
+        if (e0 + m * 64 < cn) ld(e < cn ? e : cn - 1u, vb[m], ix[m]);
+      }
+#pragma unroll
+      for (int m = 0; m < kWriteBatch; ++m)
+        if (e0 + m * 64 < cn) visit(ix[m], vb[m], e0 + m * 64 + l < cn);
+    }
+  };
+  for (int i = 0; i < kGatherSlots; ++i) {
+    const uint32_t ci = __builtin_amdgcn_readlane(cnt, i);
+    const uint32_t cn = ci & 0x7FFFu;
+    if (cn == 0) continue;
+    const uint32_t s = s0 + i;
+    if (!((ci >> 15) & 1u)) {
+      const GLOBAL uint32_t* reg = gptr(c.slot) + ((uint64_t)j * c.nslot + s) * kSlotWords;
+      const GLOBAL uint16_t* r16 = reinterpret_cast<const GLOBAL uint16_t*>(reg);
+      const uint32_t ibase = (uint32_t)((uint64_t)s * kTile - d.shift);
+      walk(cn, [&](uint32_t e, uint32_t& vb, uint32_t& ix) {
+        vb = reg[e];
+        ix = ibase + r16[slot_off16_at(e)];
       });
+    } else {
+      const uint64_t o = d.cand_off + __builtin_amdgcn_readlane(at, i);
+      const GLOBAL uint32_t* cidx = gptr(c.cand_idx) + o;
+      const GLOBAL uint32_t* cval = reinterpret_cast<const GLOBAL uint32_t*>(gptr(c.cand_val) + o);
+      walk(cn, [&](uint32_t e, uint32_t& vb, uint32_t& ix) {
+        vb = cval[e];
+        ix = cidx[e];
+      });
+    }
+  }
   const double es = wave_sum_f64(e2);
-  if (lane_id() == 0) c.epart[(uint64_t)j * c.nslot + g] = es;
+  if (l == 0) c.epart[(uint64_t)j * c.nslot + g] = es;
 }
 
 // ---- 6. ordered compaction of the exact path ------------------------------------------------
