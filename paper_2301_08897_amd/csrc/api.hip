@@ -593,7 +593,7 @@ scadles_status scadles_profile_read(double* stage_ms, uint32_t* calls)
     const uint32_t P = pr.parts;
     if (hipEventSynchronize(pr.ev[3 + 2 * P]) != hipSuccess) return fail(SCADLES_EHIP, "hipEventSynchronize failed");
     stage_ms[0] += span(pr.ev[0], pr.ev[1]);
-    for (uint32_t i = 0; i < P; ++i) stage_ms[1] += span(pr.ev[2 + 2 * i], pr.ev[3 + 2 * i]);
+    for (uint32_t i = 0; i < P; ++i) stage_ms[1] += span(pr.ev[i == 0 ? 1 : 1 + 2 * i], pr.ev[3 + 2 * i]);
     stage_ms[2] += span(pr.ev[3 + 2 * (P - 1)], pr.ev[2 + 2 * P]);
     stage_ms[3] += span(pr.ev[2 + 2 * P], pr.ev[3 + 2 * P]);
     stage_ms[4] += span(pr.ev[0], pr.ev[3 + 2 * P]);

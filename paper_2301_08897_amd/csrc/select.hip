@@ -23,7 +23,7 @@
 // If the bracket missed (fewer than k candidates) or the candidates overflow
 // their region, the device falls back to the exact path: a radix select over
 // all of its data, then an ordered compaction over its data.
-#include "scadles_internal.h"
+#include "marks.h"
 
 namespace scadles {
 
@@ -558,11 +558,17 @@ __device__ inline uint64_t wave_incl_scan_u64(uint64_t v)
 // consecutive tiles): the chunk's sum of squares (fixed order), and for a fast
 // device the tiles' candidate | sure << 32 offsets within the chunk and the
 // chunk's totals.
-__global__ __launch_bounds__(kBlock) void k_tile_scan(Ctx c)
+__global__ __launch_bounds__(kBlock) void k_tile_scan(Ctx c, uint32_t* fill, uint64_t fill_n)
 {
   __shared__ uint64_t s_w[4];
   __shared__ double s_e[4];
   const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
+  if (blockIdx.x >= c.jn * nchunk) {
+    // extra blocks: clear the devices' aggregation range markers
+    const uint32_t fb = blockIdx.x - c.jn * nchunk, nfb = gridDim.x - c.jn * nchunk;
+    for (uint64_t i = (uint64_t)fb * kBlock + threadIdx.x; i < fill_n; i += (uint64_t)nfb * kBlock) fill[i] = kNoEntry;
+    return;
+  }
   const uint32_t jr = blockIdx.x / nchunk, ch = blockIdx.x - jr * nchunk;
   const uint32_t j = c.j0 + jr;
   const uint32_t tid = threadIdx.x;
@@ -915,12 +921,12 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
 // lies in [t_lo, t_hi): equal keys and the keys above it below t_hi are
 // counted on the tiles' selection-interval keys, the keys >= t_hi come from
 // the slot counts. One wave per kBandTiles tiles (kBandTiles / 2 groups).
-__global__ __launch_bounds__(kBlock) void k_grp_count(Ctx c)
+__device__ inline void grp_count_body(const Ctx& c, uint32_t b)
 {
   const uint32_t per_dev = (c.nslot + kBandTiles * kWaves - 1) / (kBandTiles * kWaves);
-  const uint32_t jr = blockIdx.x / per_dev;
+  const uint32_t jr = b / per_dev;
   const uint32_t j = c.j0 + jr;
-  const uint32_t t0 = ((blockIdx.x - jr * per_dev) * kWaves + (threadIdx.x >> 6)) * kBandTiles;
+  const uint32_t t0 = ((b - jr * per_dev) * kWaves + (threadIdx.x >> 6)) * kBandTiles;
   const DevState& st = c.st[j];
   if (st.fallback || t0 >= c.nslot) return;
   static_assert(kGatherSlots == 2 && kBandTiles % 2 == 0, "groups are tile pairs");
@@ -967,10 +973,10 @@ __device__ inline void block_excl_scan_u64(const uint64_t* cnt, uint64_t* pre, u
   }
 }
 
-__global__ __launch_bounds__(kBlock) void k_grp_scan(Ctx c)
+__device__ inline void grp_scan_body(const Ctx& c, uint32_t jr)
 {
   __shared__ uint64_t s_w[4];
-  const uint32_t j = c.j0 + blockIdx.x;
+  const uint32_t j = c.j0 + jr;
   if (c.st[j].fallback) return;
   block_excl_scan_u64(c.grp_cnt + (uint64_t)j * c.ngrp, c.grp_pre + (uint64_t)j * c.ngrp, c.ngrp, s_w);
 }
@@ -982,12 +988,12 @@ __global__ __launch_bounds__(kBlock) void k_grp_scan(Ctx c)
 // tile's entries come from the candidate list.
 constexpr int kWriteBatch = 8;
 
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_write_fast(Ctx c)
+__device__ inline void write_fast_body(const Ctx& c, uint32_t b)
 {
   const uint32_t bpd = (c.ngrp + kWaves - 1) / kWaves;
-  const uint32_t jr = blockIdx.x / bpd;
+  const uint32_t jr = b / bpd;
   const uint32_t j = c.j0 + jr;
-  const uint32_t g = (blockIdx.x - jr * bpd) * kWaves + (threadIdx.x >> 6);
+  const uint32_t g = (b - jr * bpd) * kWaves + (threadIdx.x >> 6);
   const DevState& st = c.st[j];
   if (st.fallback || g >= c.ngrp) return;
   uint32_t thr;
@@ -1094,7 +1100,7 @@ __device__ inline uint64_t block_gt_eq(const Row& row, uint64_t vbase, uint32_t 
   return (uint64_t)tg | ((uint64_t)te << 32);
 }
 
-__global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c)
+__device__ inline void count_cf_body(const Ctx& c, uint32_t worker, uint32_t workers)
 {
   __shared__ uint32_t lds[8];
   if (*c.fb_count == 0u) return;
@@ -1105,7 +1111,7 @@ __global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c)
     uint64_t need;
     threshold_of(s, thr, need);
     const Row row{gptr(c.desc[j].grad), c.desc[j].shift, c.n};
-    for (uint32_t blk = blockIdx.x; blk < c.nfb; blk += gridDim.x) {
+    for (uint32_t blk = worker; blk < c.nfb; blk += workers) {
       const uint64_t r = block_gt_eq<kCBlkRounds>(row, (uint64_t)blk * kCBlk, thr, lds);
       if (threadIdx.x == 0) c.blk_cnt[(uint64_t)j * c.nbmax + blk] = r;
     }
@@ -1113,10 +1119,10 @@ __global__ __launch_bounds__(kBlock) void k_count_cf(Ctx c)
 }
 
 // Exclusive prefix of the packed block counts of one exact-path device.
-__global__ __launch_bounds__(kBlock) void k_scan(Ctx c)
+__device__ inline void scan_cf_body(const Ctx& c, uint32_t jr)
 {
   __shared__ uint64_t s_w[4];
-  const uint32_t j = c.j0 + blockIdx.x;
+  const uint32_t j = c.j0 + jr;
   if (!c.st[j].fallback) return;
   block_excl_scan_u64(c.blk_cnt + (uint64_t)j * c.nbmax, c.blk_pre + (uint64_t)j * c.nbmax, c.nfb, s_w);
 }
@@ -1228,7 +1234,7 @@ __device__ inline double block_write(const Row& row, uint64_t vbase, const uint3
   return e2;
 }
 
-__global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c)
+__device__ inline void write_cf_body(const Ctx& c, uint32_t worker, uint32_t workers)
 {
   __shared__ uint32_t lds[8];
   __shared__ double s_e[4];
@@ -1241,7 +1247,7 @@ __global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c)
     threshold_of(s, thr, need);
     const DevDesc d = c.desc[j];
     const Row row{gptr(d.grad), d.shift, c.n};
-    for (uint32_t blk = blockIdx.x; blk < c.nfb; blk += gridDim.x) {
+    for (uint32_t blk = worker; blk < c.nfb; blk += workers) {
       const double e2 = block_write<kCBlkRounds>(row, (uint64_t)blk * kCBlk, nullptr, thr, need,
                                                  c.blk_pre[(uint64_t)j * c.nbmax + blk], d.k, gptr(d.idx_out),
                                                  gptr(d.val_out), lds);
@@ -1254,10 +1260,10 @@ __global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c)
 
 // ---- 7. energies of the adaptive rule and per-device decision --------------------------------
 // §IV: send Top-k(g) when | ||g||^2 - ||Top-k(g)||^2 | / ||g||^2 <= delta.
-__global__ __launch_bounds__(kBlock) void k_final(Ctx c)
+__device__ inline void final_body(const Ctx& c, uint32_t jr)
 {
   __shared__ double s_e[4];
-  const uint32_t j = c.j0 + blockIdx.x;
+  const uint32_t j = c.j0 + jr;
   DevState& s = c.st[j];
   const bool fast = !s.fallback;
   const uint32_t nb = fast ? c.ngrp : c.nfb;
@@ -1286,6 +1292,40 @@ __global__ __launch_bounds__(kBlock) void k_final(Ctx c)
   if (c.compressed_out) c.compressed_out[j] = (uint8_t)s.sparse;
 }
 
+// ---- merged launches ------------------------------------------------------------------------
+// Each launch of the rest of the selection serves both paths: the fast-path
+// blocks first, then the exact path's workers (which return at once when no
+// device fell back). The decision launch also builds the aggregation range
+// markers of its devices (they do not depend on the decision; a device found
+// dense ignores them).
+__global__ __launch_bounds__(kBlock) void k_count(Ctx c, uint32_t nfast)
+{
+  if (blockIdx.x < nfast) grp_count_body(c, blockIdx.x);
+  else count_cf_body(c, blockIdx.x - nfast, gridDim.x - nfast);
+}
+
+__global__ __launch_bounds__(kBlock) void k_offsets(Ctx c, uint32_t fast)
+{
+  if (fast && blockIdx.x < c.jn) grp_scan_body(c, blockIdx.x);
+  else scan_cf_body(c, blockIdx.x - (fast ? c.jn : 0u));
+}
+
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_write(Ctx c, uint32_t nfast)
+{
+  if (blockIdx.x < nfast) write_fast_body(c, blockIdx.x);
+  else write_cf_body(c, blockIdx.x - nfast, gridDim.x - nfast);
+}
+
+__global__ __launch_bounds__(kBlock) void k_final(Ctx c, AggArgs a, AggCtx ac, uint32_t mark_blocks)
+{
+  if (blockIdx.x < c.jn) {
+    final_body(c, blockIdx.x);
+    return;
+  }
+  const uint32_t b = blockIdx.x - c.jn;
+  mark_body(a, ac, c.j0 + b / mark_blocks, b % mark_blocks, mark_blocks, false);
+}
+
 // ---- host-side launchers ---------------------------------------------------------------------
 // Everything after the main pass for devices [c.j0, c.j0 + c.jn), on stream s,
 // in two halves: 0, the threshold (scans, path decision, overflowed tiles,
@@ -1297,7 +1337,16 @@ static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s, int ha
   const uint32_t band_blocks = c.jn * ((c.nslot + kBandTiles * kWaves - 1) / (kBandTiles * kWaves));
   if (half == 0) {
     const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
-    k_tile_scan<<<c.jn * nchunk, kBlock, 0, s>>>(c);
+    uint32_t* fill = nullptr;
+    uint64_t fill_n = 0;
+    uint32_t fill_blocks = 0;
+    if (p.mark_a && p.mark_c->kmax) {
+      fill = p.mark_c->rbeg + (uint64_t)c.j0 * p.mark_c->nrange;
+      fill_n = (uint64_t)c.jn * p.mark_c->nrange;
+      const uint64_t fb = (fill_n + kBlock * 4 - 1) / (kBlock * 4);
+      fill_blocks = (uint32_t)(fb < 1024 ? fb : 1024);
+    }
+    k_tile_scan<<<c.jn * nchunk + fill_blocks, kBlock, 0, s>>>(c, fill, fill_n);
     k_post<<<c.jn, kBlock, 0, s>>>(c);
     const uint32_t ncand = p.any_fast ? band_blocks : 0u;
     if (p.any_fast) k_overflow<<<c.jn * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
@@ -1305,18 +1354,22 @@ static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s, int ha
       k_hist_cf<<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand);
       k_find<<<c.jn, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1, 0);
     }
-    if (p.any_fast) {
-      k_grp_count<<<band_blocks, kBlock, 0, s>>>(c);
-      k_grp_scan<<<c.jn, kBlock, 0, s>>>(c);
-    }
+    k_count<<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand);
+    k_offsets<<<(p.any_fast ? 2 : 1) * c.jn, kBlock, 0, s>>>(c, p.any_fast);
     return;
   }
-  if (p.any_fast) k_write_fast<<<c.jn * ((c.ngrp + kWaves - 1) / kWaves), kBlock, 0, s>>>(c);
-  k_count_cf<<<p.full_workers, kBlock, 0, s>>>(c);
-  k_scan<<<c.jn, kBlock, 0, s>>>(c);
-  k_write_cf<<<p.full_workers, kBlock, 0, s>>>(c);
-  k_final<<<c.jn, kBlock, 0, s>>>(c);
-  if (p.mark_a) (void)launch_mark(*p.mark_a, *p.mark_c, c.j0, c.jn, s);
+  const uint32_t nwrite = p.any_fast ? c.jn * ((c.ngrp + kWaves - 1) / kWaves) : 0u;
+  k_write<<<nwrite + p.full_workers, kBlock, 0, s>>>(c, nwrite);
+  AggArgs ma{};
+  AggCtx mc{};
+  uint32_t mb = 0;
+  if (p.mark_a && p.mark_c->kmax) {
+    ma = *p.mark_a;
+    mc = *p.mark_c;
+    const uint64_t b = (mc.kmax + kBlock * 16 - 1) / (kBlock * 16);
+    mb = (uint32_t)(b < 4096 ? b : 4096);
+  }
+  k_final<<<c.jn * (1 + mb), kBlock, 0, s>>>(c, ma, mc, mb);
 }
 
 // The whole selection. The devices are split into p.parts groups whose main
@@ -1326,8 +1379,10 @@ static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s, int ha
 // output half of group i, which moves more bytes, only once that main pass is
 // done (the last group's rest runs on s); s waits for s2 at the end.
 // done[i] (events of s2's owner) mark the end of main pass i. Profiling events
-// (ev, optional): 0 start, 1 bracket done, 2 + 2i / 3 + 2i around the main
-// pass of group i, 2 + 2 * parts all done.
+// (ev, optional; as few as possible, each costs a few microseconds of queue
+// time): 0 start, 1 bracket done, 3 + 2i the end of main pass i (main pass i
+// starts at the end of the previous one; with profiling these also serve as
+// done[i]), 2 + 2 * parts all done.
 hipError_t launch_select(const Ctx& c0, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipStream_t s2,
                          hipEvent_t* done, hipEvent_t join, hipEvent_t* ev)
 {
@@ -1356,12 +1411,11 @@ hipError_t launch_select(const Ctx& c0, const PrepArgs& a, const SelectPlan& p, 
   };
   for (uint32_t i = 0; i < parts; ++i) {
     const Ctx ci = group(i);
-    if (ev) (void)hipEventRecord(ev[2 + 2 * i], s);
     k_main<<<ci.jn * c.tpd, kBlock, 0, s>>>(ci, ga);
-    if (ev) (void)hipEventRecord(ev[3 + 2 * i], s);
-    if (parts > 1) {
-      hipError_t e = hipEventRecord(done[i], s);
-      if (e == hipSuccess) e = hipStreamWaitEvent(s2, done[i], 0);
+    hipEvent_t de = ev ? ev[3 + 2 * i] : (parts > 1 ? done[i] : nullptr);
+    if (de) {
+      hipError_t e = hipEventRecord(de, s);
+      if (e == hipSuccess && parts > 1) e = hipStreamWaitEvent(s2, de, 0);
       if (e != hipSuccess) return e;
     }
     if (i > 0) launch_post(group(i - 1), p, s2, 1);
