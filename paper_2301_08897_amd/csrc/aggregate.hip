@@ -17,15 +17,13 @@ namespace scadles {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(kBlock) void k_fill_u32(uint32_t* p, uint64_t count, uint32_t v)
+// Range markers of every sparse device (one thread per range).
+__global__ __launch_bounds__(kBlock) void k_lb(AggArgs a, AggCtx c)
 {
-  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < count; i += stride) p[i] = v;
-}
-
-__global__ __launch_bounds__(kBlock) void k_mark(AggArgs a, AggCtx c, uint32_t j0)
-{
-  mark_body(a, c, j0 + blockIdx.y, blockIdx.x, gridDim.x, true);
+  const uint32_t j = blockIdx.y;
+  if (!a.idx[j] || dense_device(a, c, j)) return;
+  lb_ranges(a.idx[j], a.k[j], c.lb + (uint64_t)j * c.nrange, c.nrange, blockIdx.x * kBlock + threadIdx.x,
+            gridDim.x * kBlock);
 }
 
 // Flags a set whose idx is not strictly ascending or reaches n (validation mode).
@@ -138,14 +136,14 @@ __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
   uint32_t eb = 0, em = 0;
   bool dn = false;
   if (l < K) {
-    // both markers in one round trip; rend is meaningful only where rbeg is set
+    // both markers in one round trip
     const uint64_t at = (uint64_t)l * c.nrange + r;
-    const uint32_t b0 = c.rbeg[at];
-    uint32_t e0 = c.rend[at];
     const uint32_t kk = a.k[l];
+    const uint32_t b0 = c.lb[at];
+    uint32_t e0 = r + 1 < c.nrange ? c.lb[at + 1] : kk;
     dn = dense_device(a, c, l);
     if (e0 > kk) e0 = kk;       // keeps any input in bounds; ascending input never needs it
-    if (!dn && b0 != kNoEntry && b0 < e0) {
+    if (!dn && b0 < e0) {
       eb = b0;
       em = e0 - b0;
     }
@@ -238,21 +236,17 @@ __global__ __launch_bounds__(kBlock) void k_sgd(float* p, const float* g, uint64
 
 __global__ void k_zero_u32(uint32_t* p) { *p = 0u; }
 
-// Range markers of devices [j0, j0 + jn).
-hipError_t launch_mark(const AggArgs& a, const AggCtx& c, uint32_t j0, uint32_t jn, hipStream_t s)
+// Range markers of every sparse device.
+hipError_t launch_marks(const AggArgs& a, const AggCtx& c, hipStream_t s)
 {
-  if (!c.kmax || !jn) return hipSuccess;
-  const uint64_t nm = (uint64_t)jn * c.nrange;
-  uint64_t fb = (nm + kBlock - 1) / kBlock;
-  if (fb > 2048) fb = 2048;
-  k_fill_u32<<<(uint32_t)fb, kBlock, 0, s>>>(c.rbeg + (uint64_t)j0 * c.nrange, nm, kNoEntry);
-  uint64_t mb = (c.kmax + kBlock * 16 - 1) / (kBlock * 16);
-  if (mb > 4096) mb = 4096;
-  k_mark<<<dim3((uint32_t)mb, jn), kBlock, 0, s>>>(a, c, j0);
+  if (!c.K || !c.nrange) return hipSuccess;
+  uint32_t bx = (c.nrange + kBlock - 1) / kBlock;
+  if (bx > 64) bx = 64;
+  k_lb<<<dim3(bx, c.K), kBlock, 0, s>>>(a, c);
   return hipGetLastError();
 }
 
-// marks_done: launch_mark already ran for every device on this stream's past.
+// marks_done: the range markers of every device were built earlier on this stream.
 hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate, bool marks_done, hipStream_t s)
 {
   if (c.K) {
@@ -262,7 +256,7 @@ hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate
       k_validate<<<dim3(bx, c.K), kBlock, 0, s>>>(a, c);
     }
     if (!marks_done) {
-      const hipError_t e = launch_mark(a, c, 0, c.K, s);
+      const hipError_t e = launch_marks(a, c, s);
       if (e != hipSuccess) return e;
     }
   }

@@ -101,8 +101,8 @@ struct Layout {
   uint64_t n = 0;
   uint32_t k[kMaxK], cap[kMaxK], mode[kMaxK], r_lo[kMaxK], r_hi[kMaxK];
   uint32_t any_fast = 0;
-  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_ctot, o_coff, o_ce, o_olist, o_slot, o_epart, o_cidx, o_cval, o_band, o_gcnt, o_gpre, o_bcnt, o_bpre, o_be, o_fb, o_rbeg,
-      o_rend, o_aerr;
+  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_ctot, o_coff, o_ce, o_olist, o_slot, o_epart, o_cidx, o_cval, o_band, o_gcnt, o_gpre, o_bcnt, o_bpre, o_be, o_fb, o_lb,
+      o_aerr;
   size_t total = 0;
 };
 
@@ -208,8 +208,7 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
     L.o_be = take(sizeof(double) * (size_t)K * L.nbmax);
     L.o_fb = take(sizeof(uint32_t));
   }
-  L.o_rbeg = take(sizeof(uint32_t) * (size_t)K * L.nrange);
-  L.o_rend = take(sizeof(uint32_t) * (size_t)K * L.nrange);
+  L.o_lb = take(sizeof(uint32_t) * (size_t)K * L.nrange);
   L.o_aerr = take(256);
   L.total = o;
   return true;
@@ -292,8 +291,7 @@ uint32_t parts_for(const Layout& L)
 }
 
 scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double delta, double* energies,
-                          uint8_t* compressed, hipStream_t s, ProfRec* pr, const AggArgs* mark_a = nullptr,
-                          const AggCtx* mark_c = nullptr)
+                          uint8_t* compressed, hipStream_t s, ProfRec* pr, uint32_t* lb = nullptr)
 {
   Ctx c = make_ctx(L, ws);
   c.delta = delta;
@@ -306,8 +304,8 @@ scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double d
   const uint64_t tiles = (uint64_t)L.K * L.tpd;
   p.full_workers = (uint32_t)(tiles < (uint64_t)kFullWorkers ? tiles : (uint64_t)kFullWorkers);
   p.parts = parts_for(L);
-  p.mark_a = mark_a;
-  p.mark_c = mark_c;
+  c.lb = lb;
+  c.nrange = L.nrange;
   if (pr) pr->parts = p.parts;
   StreamSet* ss = p.parts > 1 ? stream_set() : nullptr;
   if (p.parts > 1 && !ss) return fail(SCADLES_EHIP, "could not create the pipeline stream");
@@ -417,8 +415,7 @@ scadles_status scadles_weighted_aggregate(const scadles_sparse* sets, const floa
   AggCtx c;
   memset(&c, 0, sizeof(c));
   c.st = nullptr;
-  c.rbeg = reinterpret_cast<uint32_t*>(b + L.o_rbeg);
-  c.rend = reinterpret_cast<uint32_t*>(b + L.o_rend);
+  c.lb = reinterpret_cast<uint32_t*>(b + L.o_lb);
   c.err = reinterpret_cast<uint32_t*>(b + L.o_aerr);
   c.out = dense;
   c.K = Kc;
@@ -504,8 +501,7 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
   AggCtx c;
   memset(&c, 0, sizeof(c));
   c.st = reinterpret_cast<const DevState*>(b + L.o_st);
-  c.rbeg = reinterpret_cast<uint32_t*>(b + L.o_rbeg);
-  c.rend = reinterpret_cast<uint32_t*>(b + L.o_rend);
+  c.lb = reinterpret_cast<uint32_t*>(b + L.o_lb);
   c.err = reinterpret_cast<uint32_t*>(b + L.o_aerr);
   c.out = dense;
   c.params = params;
@@ -516,7 +512,7 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
   c.n = n;
   // each device group's range markers are built right after its selection
   if (pr) (void)hipEventRecord(pr->ev[0], s);
-  if (scadles_status st = run_select(L, a, ws, delta, energies, compressed, s, pr, &g, &c)) return st;
+  if (scadles_status st = run_select(L, a, ws, delta, energies, compressed, s, pr, c.lb)) return st;
   hipError_t e = launch_aggregate(g, c, 0, true, s);
   if (pr) (void)hipEventRecord(pr->ev[3 + 2 * pr->parts], s);
   if (e != hipSuccess) return hip_fail(e, "aggregate launch");

@@ -12,50 +12,21 @@ __device__ inline bool dense_device(const AggArgs& a, const AggCtx& c, uint32_t 
   return a.idx[j] == nullptr;
 }
 
-// Range markers: the first entry of device j in range r (positions
-// [r * kARange, (r + 1) * kARange)) stores its position in rbeg[j][r], the last
-// one stores its position + 1 in rend[j][r]; ranges without entries keep
-// kNoEntry in rbeg. For ascending idx a range's entries are [rbeg, rend).
-// Entries with idx >= n are skipped (only validation mode reports them).
-// Each wave takes 1024 consecutive entries (16 per lane, all loads in flight);
-// an entry's neighbours come from the adjacent lanes. Block bx of nbx for
-// device j; check_dense: skip a device whose (final) decision is dense.
-__device__ inline void mark_body(const AggArgs& a, const AggCtx& c, uint32_t j, uint32_t bx, uint32_t nbx,
-                                 bool check_dense)
+// lb[r] = number of entries of an ascending set with idx < r * kARange (the
+// lower bound of the range start), for ranges r = t, t + nt, ... < nrange: a
+// binary search over the set's idx. For any input the result is in [0, k].
+__device__ inline void lb_ranges(const uint32_t* idx, uint32_t k, uint32_t* lb, uint32_t nrange, uint32_t t,
+                                 uint32_t nt)
 {
-  constexpr int kPer = 16;
-  const uint32_t* idx = a.idx[j];
-  if (!idx || (check_dense && dense_device(a, c, j))) return;
-  const uint64_t k = a.k[j];
-  uint32_t* rb = c.rbeg + (uint64_t)j * c.nrange;
-  uint32_t* re = c.rend + (uint64_t)j * c.nrange;
-  const uint32_t l = lane_id();
-  const uint64_t nwave = (uint64_t)nbx * kWaves;
-  for (uint64_t b0 = ((uint64_t)bx * kWaves + (threadIdx.x >> 6)) * (64 * kPer); b0 < k;
-       b0 += nwave * (64 * kPer)) {
-    uint32_t x[kPer];
-#pragma unroll
-    for (int m = 0; m < kPer; ++m) {
-      const uint64_t e = b0 + m * 64 + l;
-      x[m] = e < k ? idx[e] : 0u;
+  for (uint32_t r = t; r < nrange; r += nt) {
+    const uint64_t b = (uint64_t)r * kARange;
+    uint32_t lo = 0, hi = k;
+    while (lo < hi) {
+      const uint32_t mid = lo + (hi - lo) / 2u;
+      if ((uint64_t)idx[mid] < b) lo = mid + 1u;
+      else hi = mid;
     }
-    const uint32_t before = b0 > 0 ? idx[b0 - 1] : 0u;
-    const uint32_t after = b0 + 64 * kPer < k ? idx[b0 + 64 * kPer] : 0u;
-#pragma unroll
-    for (int m = 0; m < kPer; ++m) {
-      const uint64_t e = b0 + m * 64 + l;
-      uint32_t prev = __shfl_up(x[m], 1, 64);
-      uint32_t next = __shfl_down(x[m], 1, 64);
-      const uint32_t last_prev = m > 0 ? __builtin_amdgcn_readlane(x[m > 0 ? m - 1 : 0], 63) : before;
-      const uint32_t first_next = m + 1 < kPer ? __builtin_amdgcn_readlane(x[m + 1 < kPer ? m + 1 : 0], 0) : after;
-      if (l == 0) prev = last_prev;
-      if (l == 63) next = first_next;
-      const uint32_t i = x[m];
-      if (e >= k || (uint64_t)i >= c.n) continue;
-      const uint32_t r = i / (uint32_t)kARange;
-      if (e == 0 || prev / (uint32_t)kARange != r) rb[r] = (uint32_t)e;
-      if (e + 1 == k || next / (uint32_t)kARange != r) re[r] = (uint32_t)(e + 1);
-    }
+    lb[r] = lo;
   }
 }
 

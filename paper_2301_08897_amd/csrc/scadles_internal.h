@@ -21,7 +21,6 @@ constexpr int kBins = 2048;            // radix digit: 11 bits
 constexpr int kDigitBits = 11;
 constexpr int kARange = 2048;          // aggregation: positions per wave (16 KiB of doubles in LDS)
 constexpr int kABatch = 8;             // aggregation: devices whose entries are loaded together
-constexpr uint32_t kNoEntry = 0xFFFFFFFFu;   // range marker: the device has no entry in the range
 constexpr int kMaxK = 64;              // SCADLES_MAX_DEVICES
 constexpr int kSlots = 4;              // selection slots per device
 constexpr int kSlotSampleLo = 0, kSlotSampleHi = 1, kSlotCand = 2, kSlotFull = 3;
@@ -116,6 +115,8 @@ struct Ctx {
   uint32_t force_fallback;
   uint32_t j0, jn;        // devices [j0, j0 + jn) of this launch (the per-device kernels)
   uint32_t* fb_count;     // devices on the exact path (the exact-path kernels exit early at 0)
+  uint32_t* lb;           // fused step: aggregation range markers (see AggCtx), else null
+  uint32_t nrange;
   double delta;
 };
 
@@ -147,8 +148,8 @@ struct AggArgs {
 
 struct AggCtx {
   const DevState* st;     // fused path: per-device sparse/dense decision; null otherwise
-  uint32_t* rbeg;         // [K][nrange] first entry of each device in each range (kNoEntry: none)
-  uint32_t* rend;         // [K][nrange] one past its last entry (read only where rbeg is set)
+  uint32_t* lb;           // [K][nrange] entries of each device with idx below the range's start; the
+                          // entries of range r are [lb[r], lb[r + 1]) (lb[nrange] taken as k)
   uint32_t* err;          // validation flag
   float* out;             // dense aggregate
   float* params;          // null: no SGD
@@ -166,8 +167,6 @@ struct SelectPlan {
   uint32_t sample_blocks;     // sample workgroups per device
   uint32_t full_workers;      // grid-stride workgroups of the exact full-data path
   uint32_t parts;             // device groups, 1 .. kMaxParts
-  const AggArgs* mark_a;      // not null: each group's aggregation range markers are
-  const AggCtx* mark_c;       // built right after its selection (launch_mark)
 };
 
 // Launchers (select.hip, aggregate.hip). done[parts] and join are events of
@@ -176,7 +175,7 @@ struct SelectPlan {
 hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipStream_t s2,
                          hipEvent_t* done, hipEvent_t join, hipEvent_t* ev);
 hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate, bool marks_done, hipStream_t s);
-hipError_t launch_mark(const AggArgs& a, const AggCtx& c, uint32_t j0, uint32_t jn, hipStream_t s);
+hipError_t launch_marks(const AggArgs& a, const AggCtx& c, hipStream_t s);
 hipError_t launch_sgd(float* p, const float* g, uint64_t n, float lr, hipStream_t s);
 
 // ---- sizing shared by host and device -----------------------------------------------------

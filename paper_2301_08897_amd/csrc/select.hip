@@ -558,17 +558,11 @@ __device__ inline uint64_t wave_incl_scan_u64(uint64_t v)
 // consecutive tiles): the chunk's sum of squares (fixed order), and for a fast
 // device the tiles' candidate | sure << 32 offsets within the chunk and the
 // chunk's totals.
-__global__ __launch_bounds__(kBlock) void k_tile_scan(Ctx c, uint32_t* fill, uint64_t fill_n)
+__global__ __launch_bounds__(kBlock) void k_tile_scan(Ctx c)
 {
   __shared__ uint64_t s_w[4];
   __shared__ double s_e[4];
   const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
-  if (blockIdx.x >= c.jn * nchunk) {
-    // extra blocks: clear the devices' aggregation range markers
-    const uint32_t fb = blockIdx.x - c.jn * nchunk, nfb = gridDim.x - c.jn * nchunk;
-    for (uint64_t i = (uint64_t)fb * kBlock + threadIdx.x; i < fill_n; i += (uint64_t)nfb * kBlock) fill[i] = kNoEntry;
-    return;
-  }
   const uint32_t jr = blockIdx.x / nchunk, ch = blockIdx.x - jr * nchunk;
   const uint32_t j = c.j0 + jr;
   const uint32_t tid = threadIdx.x;
@@ -1014,11 +1008,32 @@ __device__ inline void write_fast_body(const Ctx& c, uint32_t b)
   uint32_t run_g = (uint32_t)pre, run_e = (uint32_t)(pre >> 32);
   const uint32_t need32 = (uint32_t)need, k32 = d.k;
   double e2 = 0.0;
+  // Fused step: the aggregation range markers of the ranges starting in the
+  // group's index span [b0, b1): lb[r] = kept entries with idx < r * kARange,
+  // i.e. the output position of the first candidate at or after the range
+  // start (or the kept total after the group). Ranges from rnext on are open.
+  GLOBAL uint32_t* lbj = c.lb ? gptr(c.lb) + (uint64_t)j * c.nrange : nullptr;
+  const uint64_t vg = (uint64_t)s0 * kTile;
+  const uint64_t b0 = vg > d.shift ? vg - d.shift : 0;
+  uint64_t b1 = vg + (uint64_t)kGatherSlots * kTile - d.shift;
+  if (b1 > c.n) b1 = c.n;
+  uint32_t rnext = (uint32_t)((b0 + kARange - 1) / kARange);
+  const uint32_t rend = (uint32_t)((b1 + kARange - 1) / kARange);
   auto visit = [&](uint32_t idx, uint32_t vb, bool valid) {
     const uint32_t key = vb & kKeyMask;
     const bool fg = valid && key > thr, fe = valid && key == thr;
     const uint64_t bg = ballot(fg), be = ballot(fe);
     const uint32_t gt_b = run_g + mbcnt(bg), eq_b = run_e + mbcnt(be);
+    if (lbj) {
+      const uint32_t ri = idx / (uint32_t)kARange;
+      const uint32_t rp = __shfl_up(ri, 1, 64);
+      const uint64_t vm = ballot(valid);
+      if (valid) {
+        const uint32_t p = gt_b + (eq_b < need32 ? eq_b : need32);
+        for (uint32_t r = (l == 0 ? rnext : rp + 1u); r <= ri; ++r) lbj[r] = p;
+      }
+      if (vm) rnext = __builtin_amdgcn_readlane(ri, 63 - __builtin_clzll(vm)) + 1u;
+    }
     if (fg || (fe && eq_b < need32)) {
       const uint32_t pos = gt_b + (eq_b < need32 ? eq_b : need32);
       const float v = __uint_as_float(vb);
@@ -1068,6 +1083,10 @@ __device__ inline void write_fast_body(const Ctx& c, uint32_t b)
         ix = cidx[e];
       });
     }
+  }
+  if (lbj) {
+    const uint32_t p = run_g + (run_e < need32 ? run_e : need32);
+    for (uint32_t r = rnext + l; r < rend; r += 64) lbj[r] = p;
   }
   const double es = wave_sum_f64(e2);
   if (l == 0) c.epart[(uint64_t)j * c.nslot + g] = es;
@@ -1295,9 +1314,9 @@ __device__ inline void final_body(const Ctx& c, uint32_t jr)
 // ---- merged launches ------------------------------------------------------------------------
 // Each launch of the rest of the selection serves both paths: the fast-path
 // blocks first, then the exact path's workers (which return at once when no
-// device fell back). The decision launch also builds the aggregation range
-// markers of its devices (they do not depend on the decision; a device found
-// dense ignores them).
+// device fell back). In the fused step the output pass of a fast device also
+// writes its aggregation range markers; the decision launch's extra blocks
+// build those of exact-path devices.
 __global__ __launch_bounds__(kBlock) void k_count(Ctx c, uint32_t nfast)
 {
   if (blockIdx.x < nfast) grp_count_body(c, blockIdx.x);
@@ -1310,43 +1329,45 @@ __global__ __launch_bounds__(kBlock) void k_offsets(Ctx c, uint32_t fast)
   else scan_cf_body(c, blockIdx.x - (fast ? c.jn : 0u));
 }
 
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_write(Ctx c, uint32_t nfast)
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_write(Ctx c)
 {
-  if (blockIdx.x < nfast) write_fast_body(c, blockIdx.x);
-  else write_cf_body(c, blockIdx.x - nfast, gridDim.x - nfast);
+  write_fast_body(c, blockIdx.x);
 }
 
-__global__ __launch_bounds__(kBlock) void k_final(Ctx c, AggArgs a, AggCtx ac, uint32_t mark_blocks)
+// The exact path's output pass has a launch of its own: it needs about twice
+// the registers of the fast one.
+__global__ __launch_bounds__(kBlock) void k_write_cf(Ctx c)
+{
+  write_cf_body(c, blockIdx.x, gridDim.x);
+}
+
+__global__ __launch_bounds__(kBlock) void k_final(Ctx c, uint32_t lb_blocks)
 {
   if (blockIdx.x < c.jn) {
     final_body(c, blockIdx.x);
     return;
   }
+  if (*c.fb_count == 0u) return;
   const uint32_t b = blockIdx.x - c.jn;
-  mark_body(a, ac, c.j0 + b / mark_blocks, b % mark_blocks, mark_blocks, false);
+  const uint32_t j = c.j0 + b / lb_blocks;
+  if (!c.st[j].fallback) return;
+  const DevDesc& d = c.desc[j];
+  lb_ranges(d.idx_out, d.k, c.lb + (uint64_t)j * c.nrange, c.nrange, (b % lb_blocks) * kBlock + threadIdx.x,
+            lb_blocks * kBlock);
 }
 
 // ---- host-side launchers ---------------------------------------------------------------------
 // Everything after the main pass for devices [c.j0, c.j0 + c.jn), on stream s,
 // in two halves: 0, the threshold (scans, path decision, overflowed tiles,
 // radix passes, group counts and offsets), latency-bound and light on memory;
-// 1, the output (ordered compaction, energies and decision, range markers),
+// 1, the output (ordered compaction with the range markers, energies and decision),
 // which moves most of the bytes.
 static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s, int half)
 {
   const uint32_t band_blocks = c.jn * ((c.nslot + kBandTiles * kWaves - 1) / (kBandTiles * kWaves));
   if (half == 0) {
     const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
-    uint32_t* fill = nullptr;
-    uint64_t fill_n = 0;
-    uint32_t fill_blocks = 0;
-    if (p.mark_a && p.mark_c->kmax) {
-      fill = p.mark_c->rbeg + (uint64_t)c.j0 * p.mark_c->nrange;
-      fill_n = (uint64_t)c.jn * p.mark_c->nrange;
-      const uint64_t fb = (fill_n + kBlock * 4 - 1) / (kBlock * 4);
-      fill_blocks = (uint32_t)(fb < 1024 ? fb : 1024);
-    }
-    k_tile_scan<<<c.jn * nchunk + fill_blocks, kBlock, 0, s>>>(c, fill, fill_n);
+    k_tile_scan<<<c.jn * nchunk, kBlock, 0, s>>>(c);
     k_post<<<c.jn, kBlock, 0, s>>>(c);
     const uint32_t ncand = p.any_fast ? band_blocks : 0u;
     if (p.any_fast) k_overflow<<<c.jn * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
@@ -1358,18 +1379,14 @@ static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s, int ha
     k_offsets<<<(p.any_fast ? 2 : 1) * c.jn, kBlock, 0, s>>>(c, p.any_fast);
     return;
   }
-  const uint32_t nwrite = p.any_fast ? c.jn * ((c.ngrp + kWaves - 1) / kWaves) : 0u;
-  k_write<<<nwrite + p.full_workers, kBlock, 0, s>>>(c, nwrite);
-  AggArgs ma{};
-  AggCtx mc{};
-  uint32_t mb = 0;
-  if (p.mark_a && p.mark_c->kmax) {
-    ma = *p.mark_a;
-    mc = *p.mark_c;
-    const uint64_t b = (mc.kmax + kBlock * 16 - 1) / (kBlock * 16);
-    mb = (uint32_t)(b < 4096 ? b : 4096);
+  if (p.any_fast) k_write<<<c.jn * ((c.ngrp + kWaves - 1) / kWaves), kBlock, 0, s>>>(c);
+  k_write_cf<<<p.full_workers, kBlock, 0, s>>>(c);
+  uint32_t lbb = 0;
+  if (c.lb) {
+    lbb = (c.nrange + kBlock - 1) / kBlock;
+    if (lbb > 64) lbb = 64;
   }
-  k_final<<<c.jn * (1 + mb), kBlock, 0, s>>>(c, ma, mc, mb);
+  k_final<<<c.jn * (1 + lbb), kBlock, 0, s>>>(c, lbb);
 }
 
 // The whole selection. The devices are split into p.parts groups whose main
