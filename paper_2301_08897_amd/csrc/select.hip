@@ -363,11 +363,12 @@ __device__ inline uint32_t wave_prefix_of_block(uint32_t packed_lane, uint32_t* 
 // Counts are wave totals from ballots (scalar popcounts).
 // A staged candidate: its index in the low word, its value's bits in the high word.
 // A tile's slot region (kSlotWords words, consecutive tiles back to back):
-// word e < cand holds candidate e's value bits, words cand .. cand + band - 1
-// the keys of the candidates below t_hi (the selection interval), and the
-// 16-bit word (2 * kSlotWords - 1 - e) candidate e's offset in the tile
-// (index = tile * kTile - shift + offset). Both ends are written as whole
-// 16-byte chunks; a tile whose two parts would meet overflows.
+// words 0 .. band - 1 hold the keys of the candidates below t_hi (the
+// selection interval), word band + e candidate e's value bits, and the 16-bit
+// word (2 * kSlotWords - 1 - e) candidate e's offset in the tile (index = tile
+// * kTile - shift + offset). The keys start at a fixed place, so their readers
+// load them before the counts arrive. Both ends are written as whole 16-byte
+// chunks; a tile whose two parts would meet overflows.
 static_assert((kSlotWords & (kSlotWords - 1)) == 0, "slot positions wrap inside a power-of-two region");
 __device__ inline uint32_t slot_off16_at(uint32_t e) { return 2u * kSlotWords - 1u - e; }
 
@@ -514,12 +515,13 @@ __global__ __launch_bounds__(kBlock) void k_main(Ctx c, GradArgs ga)
     return c32[wi * (2 * kWaveCap) + 2u * (e - base) + half];
   };
   auto low_word = [&](uint32_t q) -> uint32_t {
-    if (q < cand) return cand_word(q, 1u);
-    const uint32_t i = q - cand;
-    if (i >= band) return 0u;
-    const uint32_t wi = (uint32_t)(i >= kb[1]) + (uint32_t)(i >= kb[2]) + (uint32_t)(i >= kb[3]);
-    const uint32_t base = wi == 0 ? kb[0] : (wi == 1 ? kb[1] : (wi == 2 ? kb[2] : kb[3]));
-    return b32[wi * kWaveCap + (i - base)];
+    if (q < band) {
+      const uint32_t wi = (uint32_t)(q >= kb[1]) + (uint32_t)(q >= kb[2]) + (uint32_t)(q >= kb[3]);
+      const uint32_t base = wi == 0 ? kb[0] : (wi == 1 ? kb[1] : (wi == 2 ? kb[2] : kb[3]));
+      return b32[wi * kWaveCap + (q - base)];
+    }
+    const uint32_t e = q - band;
+    return e < cand ? cand_word(e, 1u) : 0u;
   };
   const uint32_t ibase = (uint32_t)(vbase - row.shift);   // index of tile position 0 (mod 2^32)
   auto off16 = [&](uint32_t e) -> uint32_t { return e < cand ? (cand_word(e, 0u) - ibase) & 0xFFFFu : 0u; };
@@ -674,19 +676,18 @@ __device__ inline uint64_t slot_pre(const Ctx& c, uint32_t j, uint32_t s)
 
 // ---- 3. selection-interval keys per tile ---------------------------------------------------
 // The keys of a tile's candidates below t_hi (the selection interval [t_lo,
-// t_hi)) follow its candidates' values in the slot region; k_overflow
-// writes those of an overflowed tile to the device's band list at the tile's
-// band offset (candidates - sure keys before it). band_tiles walks them for
-// tiles t0 .. t0 + kBandTiles - 1 of device j, tile after tile, in index order
-// within a tile, 64 at a time: visit(key, valid) takes one window, done(i,
-// sure) closes tile t0 + i (sure: its keys >= t_hi). Lane l holds tile t0 +
-// l's counts. The first window of kBandBatch tiles is loaded at once, and
-// longer runs four windows at once, without conditions: tile indices are
-// clamped, region positions wrap inside the region and
-// band-list positions are clamped into the tile's run, so every load is in
-// bounds; keys past a tile's count are ignored.
-constexpr int kBandTiles = 32;
-constexpr int kBandBatch = 8;
+// t_hi)) start its slot region; k_overflow writes those of an overflowed tile
+// to the device's band list at the tile's band offset (candidates - sure keys
+// before it). band_tiles walks them for tiles t0 .. t0 + kBandTiles - 1 of
+// device j, tile after tile, in index order within a tile, 64 at a time:
+// visit(key, valid) takes one window, done(i, sure) closes tile t0 + i (sure:
+// its keys >= t_hi). The first window of every tile is loaded at once, before
+// the counts arrive (lane l then holds tile t0 + l's counts), longer runs four
+// windows at once; all without conditions: tile indices are clamped, region
+// positions wrap inside the region and band-list positions are clamped into
+// the tile's run, so every load is in bounds; keys past a tile's count are
+// ignored.
+constexpr int kBandTiles = 16;
 
 template <class Visit, class Done>
 __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit visit, Done done)
@@ -695,17 +696,23 @@ __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit v
   const uint32_t l = lane_id();
   const uint32_t last = c.nslot - 1;
   const uint64_t row = (uint64_t)j * c.nslot;
+  const GLOBAL uint32_t* reg = gptr(c.slot);
+  uint32_t kv[kBandTiles];
+#pragma unroll
+  for (int i = 0; i < kBandTiles; ++i) {
+    const uint32_t ti = t0 + i < last ? t0 + i : last;
+    kv[i] = reg[(row + ti) * kSlotWords + l];
+  }
   const uint32_t tl = t0 + l < last ? t0 + l : last;
   const uint32_t v = t0 + l < c.nslot ? c.slot_cnt[row + tl] : 0u;
   const uint32_t cand = v & 0x7FFFu, sure = v >> 16, nb = cand - sure;
   const uint32_t ovf = (v >> 15) & 1u;
-  uint32_t kb = cand;                                   // first key: word of the region ...
+  uint32_t kb = 0;                                      // an overflowed tile's keys: band-list position
   if (ovf) {
     const uint64_t pre = slot_pre(c, j, tl);
-    kb = (uint32_t)pre - (uint32_t)(pre >> 32);         // ... or position in the band list
+    kb = (uint32_t)pre - (uint32_t)(pre >> 32);
   }
   const uint32_t nt = c.nslot - t0 < (uint32_t)kBandTiles ? c.nslot - t0 : (uint32_t)kBandTiles;
-  const GLOBAL uint32_t* reg = gptr(c.slot);
   const GLOBAL uint32_t* blist = gptr(c.band) + c.desc[j].cand_off;
   // windows e0 .. of a run of nbi keys, four at a time; key_at(e) is in bounds for every e
   auto run = [&](uint32_t e0, uint32_t nbi, auto key_at) {
@@ -718,29 +725,19 @@ __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit v
         if (e + m * 64 < nbi) visit(w4[m], e + m * 64 + l < nbi);
     }
   };
-  for (uint32_t i0 = 0; i0 < nt; i0 += kBandBatch) {
-    uint32_t kv[kBandBatch];
 #pragma unroll
-    for (int q = 0; q < kBandBatch; ++q) {
-      const uint32_t i = i0 + q;     // < kBandTiles
-      const uint32_t ti = t0 + i < last ? t0 + i : last;
-      kv[q] = reg[(row + ti) * kSlotWords + ((__builtin_amdgcn_readlane(kb, i) + l) & kMask)];
+  for (int i = 0; i < kBandTiles; ++i) {
+    if ((uint32_t)i >= nt) break;
+    const uint32_t nbi = __builtin_amdgcn_readlane(nb, i);
+    if (!__builtin_amdgcn_readlane(ovf, i)) {
+      visit(kv[i], l < nbi);
+      const GLOBAL uint32_t* base = reg + (row + t0 + i) * kSlotWords;
+      if (nbi > 64u) run(64u, nbi, [&](uint32_t e) { return base[e & kMask]; });
+    } else if (nbi) {
+      const GLOBAL uint32_t* p = blist + __builtin_amdgcn_readlane(kb, i);
+      run(0u, nbi, [&](uint32_t e) { return p[e < nbi ? e : nbi - 1u]; });
     }
-#pragma unroll
-    for (int q = 0; q < kBandBatch; ++q) {
-      const uint32_t i = i0 + q;
-      if (i >= nt) break;
-      const uint32_t nbi = __builtin_amdgcn_readlane(nb, i), kbi = __builtin_amdgcn_readlane(kb, i);
-      if (!__builtin_amdgcn_readlane(ovf, i)) {
-        visit(kv[q], l < nbi);
-        const GLOBAL uint32_t* base = reg + (row + t0 + i) * kSlotWords;
-        if (nbi > 64u) run(64u, nbi, [&](uint32_t e) { return base[(kbi + e) & kMask]; });
-      } else if (nbi) {
-        const GLOBAL uint32_t* p = blist + kbi;
-        run(0u, nbi, [&](uint32_t e) { return p[e < nbi ? e : nbi - 1u]; });
-      }
-      done(i, __builtin_amdgcn_readlane(sure, i));
-    }
+    done(i, __builtin_amdgcn_readlane(sure, i));
   }
 }
 
@@ -975,47 +972,57 @@ __device__ inline void grp_scan_body(const Ctx& c, uint32_t jr)
   block_excl_scan_u64(c.grp_cnt + (uint64_t)j * c.ngrp, c.grp_pre + (uint64_t)j * c.ngrp, c.ngrp, s_w);
 }
 
-// One wave per group of kGatherSlots tiles: their candidates in index order,
-// kept ones written to the device's outputs; the kept sum of squares goes to
-// epart[j][group]. A tile's values and offsets are loaded kWriteBatch windows
-// at a time (positions clamped into the tile's candidates); an overflowed
-// tile's entries come from the candidate list.
+// Output pass: one wave per kWriteGroups consecutive groups of kGatherSlots
+// tiles (their counts and group offsets are loaded together): the tiles'
+// candidates in index order, kept ones written to the device's outputs; the
+// kept sum of squares of each group goes to epart[j][group]. A tile's values
+// and offsets are loaded kWriteBatch windows at a time (positions clamped into
+// the tile's candidates); an overflowed tile's entries come from the candidate
+// list.
 constexpr int kWriteBatch = 8;
+constexpr uint32_t kWriteGroups = 1;
+constexpr uint32_t kWriteTiles = kWriteGroups * kGatherSlots;
+static_assert(kWriteTiles <= 64, "a wave holds its tiles' counts in lanes");
 
 __device__ inline void write_fast_body(const Ctx& c, uint32_t b)
 {
-  const uint32_t bpd = (c.ngrp + kWaves - 1) / kWaves;
+  constexpr uint32_t kPerBlock = kWriteGroups * kWaves;
+  const uint32_t bpd = (c.ngrp + kPerBlock - 1) / kPerBlock;
   const uint32_t jr = b / bpd;
   const uint32_t j = c.j0 + jr;
-  const uint32_t g = (b - jr * bpd) * kWaves + (threadIdx.x >> 6);
+  const uint32_t g0 = ((b - jr * bpd) * kWaves + (threadIdx.x >> 6)) * kWriteGroups;
+  if (g0 >= c.ngrp) return;
+  const uint32_t ng = c.ngrp - g0 < kWriteGroups ? c.ngrp - g0 : kWriteGroups;
+  const uint32_t l = lane_id();
+  const uint32_t s0 = g0 * kGatherSlots;
+  // lane i < kWriteTiles: tile s0 + i's counts (and list offset when it overflowed);
+  // lane q < ng: group g0 + q's kept-above | equal << 32 offsets. Loaded before
+  // the device's state is known (in bounds for any device).
+  const uint32_t sl = s0 + (l < kWriteTiles ? l : 0u);
+  const bool live = l < kWriteTiles && sl < c.nslot;
+  const uint32_t cnt = live ? c.slot_cnt[(uint64_t)j * c.nslot + sl] : 0u;
+  const uint64_t gpre = c.grp_pre[(uint64_t)j * c.ngrp + g0 + (l < ng ? l : 0u)];
   const DevState& st = c.st[j];
-  if (st.fallback || g >= c.ngrp) return;
+  if (st.fallback) return;
   uint32_t thr;
   uint64_t need;
   threshold_of(st, thr, need);
   const DevDesc d = c.desc[j];
   GLOBAL uint32_t* oi = gptr(d.idx_out);
   GLOBAL float* ov = gptr(d.val_out);
-  const uint32_t l = lane_id();
-  const uint32_t s0 = g * kGatherSlots;
-  // lane i < kGatherSlots: tile s0 + i's counts (and list offset when it overflowed)
-  const uint32_t sl = s0 + (l < (uint32_t)kGatherSlots ? l : 0u);
-  const bool live = l < (uint32_t)kGatherSlots && sl < c.nslot;
-  const uint32_t cnt = live ? c.slot_cnt[(uint64_t)j * c.nslot + sl] : 0u;
   const uint32_t at = ((cnt >> 15) & 1u) ? (uint32_t)slot_pre(c, j, sl) : 0u;
   // 32-bit counts and positions: k < 2^32
-  const uint64_t pre = c.grp_pre[(uint64_t)j * c.ngrp + g];
-  uint32_t run_g = (uint32_t)pre, run_e = (uint32_t)(pre >> 32);
+  uint32_t run_g = 0, run_e = 0;
   const uint32_t need32 = (uint32_t)need, k32 = d.k;
   double e2 = 0.0;
   // Fused step: the aggregation range markers of the ranges starting in the
-  // group's index span [b0, b1): lb[r] = kept entries with idx < r * kARange,
+  // groups' index span [b0, b1): lb[r] = kept entries with idx < r * kARange,
   // i.e. the output position of the first candidate at or after the range
-  // start (or the kept total after the group). Ranges from rnext on are open.
+  // start (or the kept total after the groups). Ranges from rnext on are open.
   GLOBAL uint32_t* lbj = c.lb ? gptr(c.lb) + (uint64_t)j * c.nrange : nullptr;
   const uint64_t vg = (uint64_t)s0 * kTile;
   const uint64_t b0 = vg > d.shift ? vg - d.shift : 0;
-  uint64_t b1 = vg + (uint64_t)kGatherSlots * kTile - d.shift;
+  uint64_t b1 = vg + (uint64_t)ng * kGatherSlots * kTile - d.shift;
   if (b1 > c.n) b1 = c.n;
   uint32_t rnext = (uint32_t)((b0 + kARange - 1) / kARange);
   const uint32_t rend = (uint32_t)((b1 + kARange - 1) / kARange);
@@ -1061,35 +1068,41 @@ __device__ inline void write_fast_body(const Ctx& c, uint32_t b)
         if (e0 + m * 64 < cn) visit(ix[m], vb[m], e0 + m * 64 + l < cn);
     }
   };
-  for (int i = 0; i < kGatherSlots; ++i) {
-    const uint32_t ci = __builtin_amdgcn_readlane(cnt, i);
-    const uint32_t cn = ci & 0x7FFFu;
-    if (cn == 0) continue;
-    const uint32_t s = s0 + i;
-    if (!((ci >> 15) & 1u)) {
-      const GLOBAL uint32_t* reg = gptr(c.slot) + ((uint64_t)j * c.nslot + s) * kSlotWords;
-      const GLOBAL uint16_t* r16 = reinterpret_cast<const GLOBAL uint16_t*>(reg);
-      const uint32_t ibase = (uint32_t)((uint64_t)s * kTile - d.shift);
-      walk(cn, [&](uint32_t e, uint32_t& vb, uint32_t& ix) {
-        vb = reg[e];
-        ix = ibase + r16[slot_off16_at(e)];
-      });
-    } else {
-      const uint64_t o = d.cand_off + __builtin_amdgcn_readlane(at, i);
-      const GLOBAL uint32_t* cidx = gptr(c.cand_idx) + o;
-      const GLOBAL uint32_t* cval = reinterpret_cast<const GLOBAL uint32_t*>(gptr(c.cand_val) + o);
-      walk(cn, [&](uint32_t e, uint32_t& vb, uint32_t& ix) {
-        vb = cval[e];
-        ix = cidx[e];
-      });
+  for (uint32_t q = 0; q < ng; ++q) {
+    run_g = __builtin_amdgcn_readlane((uint32_t)gpre, q);
+    run_e = __builtin_amdgcn_readlane((uint32_t)(gpre >> 32), q);
+    for (uint32_t i = q * kGatherSlots; i < (q + 1) * kGatherSlots; ++i) {
+      const uint32_t ci = __builtin_amdgcn_readlane(cnt, i);
+      const uint32_t cn = ci & 0x7FFFu;
+      if (cn == 0) continue;
+      const uint32_t s = s0 + i;
+      if (!((ci >> 15) & 1u)) {
+        const GLOBAL uint32_t* reg = gptr(c.slot) + ((uint64_t)j * c.nslot + s) * kSlotWords;
+        const GLOBAL uint16_t* r16 = reinterpret_cast<const GLOBAL uint16_t*>(reg);
+        const GLOBAL uint32_t* vals = reg + (cn - (ci >> 16));     // after the selection keys
+        const uint32_t ibase = (uint32_t)((uint64_t)s * kTile - d.shift);
+        walk(cn, [&](uint32_t e, uint32_t& vb, uint32_t& ix) {
+          vb = vals[e];
+          ix = ibase + r16[slot_off16_at(e)];
+        });
+      } else {
+        const uint64_t o = d.cand_off + __builtin_amdgcn_readlane(at, i);
+        const GLOBAL uint32_t* cidx = gptr(c.cand_idx) + o;
+        const GLOBAL uint32_t* cval = reinterpret_cast<const GLOBAL uint32_t*>(gptr(c.cand_val) + o);
+        walk(cn, [&](uint32_t e, uint32_t& vb, uint32_t& ix) {
+          vb = cval[e];
+          ix = cidx[e];
+        });
+      }
     }
+    const double es = wave_sum_f64(e2);
+    if (l == 0) c.epart[(uint64_t)j * c.nslot + g0 + q] = es;
+    e2 = 0.0;
   }
   if (lbj) {
     const uint32_t p = run_g + (run_e < need32 ? run_e : need32);
     for (uint32_t r = rnext + l; r < rend; r += 64) lbj[r] = p;
   }
-  const double es = wave_sum_f64(e2);
-  if (l == 0) c.epart[(uint64_t)j * c.nslot + g] = es;
 }
 
 // ---- 6. ordered compaction of the exact path ------------------------------------------------
@@ -1379,7 +1392,7 @@ static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s, int ha
     k_offsets<<<(p.any_fast ? 2 : 1) * c.jn, kBlock, 0, s>>>(c, p.any_fast);
     return;
   }
-  if (p.any_fast) k_write<<<c.jn * ((c.ngrp + kWaves - 1) / kWaves), kBlock, 0, s>>>(c);
+  if (p.any_fast) k_write<<<c.jn * ((c.ngrp + kWriteGroups * kWaves - 1) / (kWriteGroups * kWaves)), kBlock, 0, s>>>(c);
   k_write_cf<<<p.full_workers, kBlock, 0, s>>>(c);
   uint32_t lbb = 0;
   if (c.lb) {
