@@ -231,29 +231,39 @@ __global__ __launch_bounds__(kBlock) void k_hist_sample(Ctx c)
   if (!s0.active && !s1.active) return;
   const uint64_t e0 = (uint64_t)blockIdx.x * kSBlk;
   if (e0 >= c.s_n) return;
-  for (int b = threadIdx.x; b < 2 * kBins; b += kBlock) (&h[0][0])[b] = 0u;
-  __syncthreads();
   const SelView v0 = view_of(s0), v1 = view_of(s1);
+  // both selections at the same digit (always in the first pass): one histogram
+  const bool same = s0.active && s1.active && v0.lo == v1.lo && v0.hi == v1.hi && v0.shift == v1.shift &&
+                    v0.width == v1.width && v0.prefix == v1.prefix;
+  for (int b = threadIdx.x; b < 2 * kBins; b += kBlock) (&h[0][0])[b] = 0u;
+  constexpr int kR = kSBlk / kRound;
   const uint64_t e1 = (e0 + kSBlk < c.s_n) ? e0 + kSBlk : c.s_n;
-  for (uint64_t e = e0 + threadIdx.x * 4; e < e1; e += kRound) {
+  f4 x[kR];
+#pragma unroll
+  for (int r = 0; r < kR; ++r) {
+    const uint64_t e = e0 + (uint64_t)r * kRound + threadIdx.x * 4;
     const uint64_t chunk = e / kSChunk, within = e % kSChunk;
     const uint64_t i = chunk * c.s_stride + within;     // real position of sample element e
-    f4 x;
-    if (d.shift == 0 && e + 4 <= e1) x = ld4(d.grad + i);
+    if (d.shift == 0 && e + 4 <= e1) x[r] = ld4(d.grad + i);
     else
-      for (int q = 0; q < 4; ++q) x[q] = (e + q < e1) ? gptr(d.grad)[i + q] : 0.f;
+      for (int q = 0; q < 4; ++q) x[r][q] = (e + q < e1) ? gptr(d.grad)[i + q] : 0.f;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kR; ++r) {
+    const uint64_t e = e0 + (uint64_t)r * kRound + threadIdx.x * 4;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       if (e + q >= e1) break;
-      const uint32_t key = key_of(x[q]);
+      const uint32_t key = key_of(x[r][q]);
       uint32_t dg;
       if (s0.active && sel_digit(v0, key, dg)) atomicAdd(&h[0][dg], 1u);
-      if (s1.active && sel_digit(v1, key, dg)) atomicAdd(&h[1][dg], 1u);
+      if (!same && s1.active && sel_digit(v1, key, dg)) atomicAdd(&h[1][dg], 1u);
     }
   }
   __syncthreads();
   if (s0.active) flush_hist(h[0], c.hist + ((uint64_t)j * kSlots + kSlotSampleLo) * kBins, kBins);
-  if (s1.active) flush_hist(h[1], c.hist + ((uint64_t)j * kSlots + kSlotSampleHi) * kBins, kBins);
+  if (s1.active) flush_hist(same ? h[0] : h[1], c.hist + ((uint64_t)j * kSlots + kSlotSampleHi) * kBins, kBins);
 }
 
 // ---- radix digit decision for slots [s0, s1) of one device (one wave) -----------------------
