@@ -66,6 +66,9 @@ def _load():
                                          _u64p, _f32p, _f32p]
         lib.oracle_sgd.restype = None
         lib.oracle_sgd.argtypes = [_f32p, _f32p, ctypes.c_uint64, ctypes.c_float]
+        lib.oracle_momentum_sgd.restype = None
+        lib.oracle_momentum_sgd.argtypes = [_f32p, _f32p, _f32p, ctypes.c_uint64, ctypes.c_float,
+                                            ctypes.c_float, ctypes.c_float]
         lib.oracle_stream_weights.restype = ctypes.c_int
         lib.oracle_stream_weights.argtypes = [_f64p, ctypes.c_uint32, ctypes.c_double,
                                               ctypes.c_double, ctypes.c_double, _f32p, _f64p]
@@ -186,6 +189,21 @@ def sgd(params: np.ndarray, grad: np.ndarray, lr: float) -> np.ndarray:
     _load().oracle_sgd(_ptr(p, ctypes.c_float), _ptr(g, ctypes.c_float), p.size,
                        ctypes.c_float(lr))
     return p
+
+
+def momentum_sgd(params: np.ndarray, buf: np.ndarray, grad: np.ndarray, lr: float, momentum: float,
+                 weight_decay: float):
+    """Momentum SGD with weight decay (§V training setup) on copies of ``params``
+    and the momentum buffer ``buf``; returns (params, buf)."""
+    p = np.array(params, dtype=np.float32, copy=True)
+    v = np.array(buf, dtype=np.float32, copy=True)
+    g = np.ascontiguousarray(grad, dtype=np.float32)
+    if not (p.size == v.size == g.size):
+        raise ValueError("params, buf and grad must have the same size")
+    _load().oracle_momentum_sgd(_ptr(p, ctypes.c_float), _ptr(v, ctypes.c_float), _ptr(g, ctypes.c_float),
+                                p.size, ctypes.c_float(lr), ctypes.c_float(momentum),
+                                ctypes.c_float(weight_decay))
+    return p, v
 
 
 def stream_weights(rates, b_min: float = 0.0, b_max: float = float("inf"),

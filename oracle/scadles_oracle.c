@@ -146,6 +146,23 @@ void oracle_sgd(float* p, const float* g, uint64_t n, float lr)
   for (uint64_t i = 0; i < n; ++i) p[i] = (float)((double)p[i] - (double)lr * (double)g[i]);
 }
 
+/* Momentum SGD with weight decay after the aggregation: the optimizer of the
+ * paper's evaluation (§V, training setup: momentum 0.9 with weight decay
+ * 1e-4 for ResNet152 and 5e-4 for VGG19) applied to the aggregate of Eqn 4b
+ * in place of the plain step of Eqn 4c. The usual formulation without
+ * dampening or Nesterov: d = g + wd * w; v <- mu * v + d; w <- w - eta * v.
+ * Every step is evaluated in double and every stored value rounded to float
+ * once: v is stored as float and that float is the one the parameter update
+ * uses. A zero v gives v = d on the first step; mu = wd = 0 is Eqn 4c.      */
+void oracle_momentum_sgd(float* p, float* v, const float* g, uint64_t n, float lr, float mu, float wd)
+{
+  for (uint64_t i = 0; i < n; ++i) {
+    const double d = (double)g[i] + (double)wd * (double)p[i];
+    v[i] = (float)((double)mu * (double)v[i] + d);
+    p[i] = (float)((double)p[i] - (double)lr * (double)v[i]);
+  }
+}
+
 /* Weights and learning-rate scale from streaming rates (§IV "Heterogeneous
  * streams"): batch b_j = S_j bounded to [b_min, b_max]; Eqn 4a
  * r_j = b_j / sum b (so sum r = 1); linear scaling gamma = sum b / B.
