@@ -102,6 +102,9 @@ def main():
     ap.add_argument("--stages", action="store_true", help="also print per-stage milliseconds")
     ap.add_argument("--parts", type=int, default=2,
                     help="device groups whose selections are pipelined (library option 'parts')")
+    ap.add_argument("--optimizer", choices=("sgd", "momentum"), default="sgd",
+                    help="update after the aggregation: Eqn 4c (default), or momentum SGD 0.9 with weight "
+                         "decay 5e-4 (the VGG19 setup of the paper's evaluation)")
     ap.add_argument("--calibrate", action="store_true",
                     help="first run one 1 GiB device-to-device copy (a plain copy kernel of known size "
                          "for scaling HBM byte counters)")
@@ -147,7 +150,11 @@ def main():
         lrs.append(float(np.float32(s.eta * gamma)))
     sc.set_option("parts", args.parts)
     parts = min(args.parts, s.K)
-    step = sc.FusedStep(G, s.ratios[0], params=params)
+    if args.optimizer == "momentum":
+        mbuf = torch.zeros_like(params)
+        step = sc.FusedStep(G, s.ratios[0], params=params, momentum_buf=mbuf, momentum=0.9, weight_decay=5e-4)
+    else:
+        step = sc.FusedStep(G, s.ratios[0], params=params)
     for i in range(args.warmup):
         it = i % s.iterations
         if any(s.ratios[it] != s.ratios[0]):
@@ -191,7 +198,9 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": s.name, "K": s.K, "n": s.n, "ratio": float(s.ratios[0, 0]),
-                   "delta": "inf", "iterations": s.iterations, "sgd": True},
+                   "delta": "inf", "iterations": s.iterations, "sgd": True,
+                   "optimizer": ("momentum SGD 0.9, weight decay 5e-4" if args.optimizer == "momentum"
+                                 else "SGD (Eqn 4c)")},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
                      "kernel": "k_main (main select pass: one read of every gradient)",

@@ -128,6 +128,22 @@ scadles_status scadles_weighted_aggregate(const scadles_sparse* sets, const floa
 scadles_status scadles_apply_sgd(float* params, const float* grad, uint64_t n, float lr,
                                  void* stream);
 
+/* Momentum SGD with weight decay: the optimizer of the paper's evaluation
+ * (§V training setup: momentum 0.9, weight decay 1e-4 for ResNet152 and
+ * 5e-4 for VGG19), applied in place of the plain step of Eqn 4c. Per
+ * element, without dampening or Nesterov:
+ *   d         = grad[i] + weight_decay * params[i]
+ *   buf[i]    = momentum * buf[i] + d
+ *   params[i] = params[i] - lr * buf[i]     (with the buf[i] just stored)
+ * Each line is evaluated in double as one fused multiply-add (every product
+ * of two floats is exact in double) and rounded to float once. A zero-filled
+ * buf gives buf = d on the first step; momentum = weight_decay = 0 is Eqn 4c.
+ *   params, momentum_buf (dev, n floats) updated in place; grad (dev, n
+ *   floats). All 16-byte aligned, no two overlapping. lr, momentum and
+ *   weight_decay finite.                                                    */
+scadles_status scadles_apply_momentum_sgd(float* params, float* momentum_buf, const float* grad, uint64_t n,
+                                          float lr, float momentum, float weight_decay, void* stream);
+
 /* One whole hot-path step for K devices in one call (the training step of
  * §IV): Top-k + energies for every device, the adaptive decision, weighted
  * aggregation and, optionally, the SGD update.
@@ -153,6 +169,19 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
                                   double* energies, uint8_t* compressed,
                                   float* params, float lr,
                                   void* ws, size_t ws_bytes, void* stream);
+
+/* scadles_step_fused with the momentum SGD of scadles_apply_momentum_sgd in
+ * place of Eqn 4c, fused into the aggregation (computed from the float g~
+ * written to dense). params and momentum_buf (dev, n floats, 16-byte aligned,
+ * not overlapping each other or dense) are both required and updated in
+ * place; momentum and weight_decay finite. Other arguments and errors as for
+ * scadles_step_fused.                                                       */
+scadles_status scadles_step_fused_momentum(const float* const* grads, uint32_t K, uint64_t n,
+                                           const double* ratios, double delta, const float* weights,
+                                           uint32_t* const* idx, float* const* val, float* dense,
+                                           double* energies, uint8_t* compressed, float* params,
+                                           float* momentum_buf, float lr, float momentum,
+                                           float weight_decay, void* ws, size_t ws_bytes, void* stream);
 
 /* Aggregation weights and learning-rate scale from streaming rates
  * (§IV "Heterogeneous streams", Eqn 4a and the linear scaling rule):

@@ -58,10 +58,16 @@ _topk_select = _sig("scadles_topk_select", ctypes.c_int, _vp, _u64, ctypes.c_dou
 _weighted_aggregate = _sig("scadles_weighted_aggregate", ctypes.c_int, ctypes.POINTER(Sparse),
                            ctypes.POINTER(ctypes.c_float), _u32, _u64, _vp, _vp, ctypes.c_size_t, _vp)
 _apply_sgd = _sig("scadles_apply_sgd", ctypes.c_int, _vp, _vp, _u64, ctypes.c_float, _vp)
+_apply_momentum_sgd = _sig("scadles_apply_momentum_sgd", ctypes.c_int, _vp, _vp, _vp, _u64, ctypes.c_float,
+                           ctypes.c_float, ctypes.c_float, _vp)
 _step_fused = _sig("scadles_step_fused", ctypes.c_int, ctypes.POINTER(_vp), _u32, _u64,
                    ctypes.POINTER(ctypes.c_double), ctypes.c_double, ctypes.POINTER(ctypes.c_float),
                    ctypes.POINTER(_vp), ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, ctypes.c_float, _vp,
                    ctypes.c_size_t, _vp)
+_step_fused_momentum = _sig("scadles_step_fused_momentum", ctypes.c_int, ctypes.POINTER(_vp), _u32, _u64,
+                            ctypes.POINTER(ctypes.c_double), ctypes.c_double, ctypes.POINTER(ctypes.c_float),
+                            ctypes.POINTER(_vp), ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, _vp, ctypes.c_float,
+                            ctypes.c_float, ctypes.c_float, _vp, ctypes.c_size_t, _vp)
 _stream_weights = _sig("scadles_stream_weights", ctypes.c_int, ctypes.POINTER(ctypes.c_double), _u32,
                        ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_float),
                        ctypes.POINTER(ctypes.c_double))
@@ -219,6 +225,18 @@ def apply_sgd(params, grad, lr: float, *, stream=None):
     return params
 
 
+def apply_momentum_sgd(params, momentum_buf, grad, lr: float, momentum: float, weight_decay: float, *,
+                       stream=None):
+    """Momentum SGD with weight decay (§V training setup) in place on ``params``
+    and ``momentum_buf``."""
+    if not (params.numel() == momentum_buf.numel() == grad.numel()):
+        raise ValueError("params, momentum_buf and grad must have the same size")
+    _check(_apply_momentum_sgd(_dev_f32(params, "params"), _dev_f32(momentum_buf, "momentum_buf"),
+                               _dev_f32(grad, "grad"), params.numel(), float(lr), float(momentum),
+                               float(weight_decay), _stream_ptr(stream)))
+    return params, momentum_buf
+
+
 # ---- the fused step -----------------------------------------------------------------------------
 
 @dataclass
@@ -235,7 +253,8 @@ class FusedStep:
     rule + Eqn 4b aggregation + optional Eqn 4c update), with every output and
     the workspace allocated once so that ``run`` only marshals pointers."""
 
-    def __init__(self, grads, ratios: Sequence[float], *, delta: float = math.inf, params=None):
+    def __init__(self, grads, ratios: Sequence[float], *, delta: float = math.inf, params=None,
+                 momentum_buf=None, momentum: float = 0.0, weight_decay: float = 0.0):
         torch = _torch()
         if isinstance(grads, torch.Tensor) and grads.dim() == 2:
             grads = [grads[j] for j in range(grads.shape[0])]
@@ -251,6 +270,16 @@ class FusedStep:
         dev = self.grads[0].device
         self.device = dev
         self.params = params
+        # momentum SGD with weight decay in place of Eqn 4c when a buffer is given
+        self.momentum_buf = momentum_buf
+        self.momentum = float(momentum)
+        self.weight_decay = float(weight_decay)
+        if momentum_buf is not None:
+            if params is None:
+                raise ValueError("momentum_buf needs params")
+            _dev_f32(momentum_buf, "momentum_buf")
+            if momentum_buf.numel() != self.n or params.numel() != self.n:
+                raise ValueError("params and momentum_buf must have n elements")
         self.delta = float(delta)
         self.set_ratios(ratios)
         self.dense = torch.empty(self.n, dtype=torch.float32, device=dev)
@@ -284,10 +313,18 @@ class FusedStep:
         for j in range(self.K):
             self._w[j] = float(w[j])
         pp = _dev_f32(self.params, "params") if self.params is not None else None
-        _check(_step_fused(self._grad_ptrs, self.K, self.n, self._ratios, self.delta, self._w,
-                           self._idx_ptrs, self._val_ptrs, self.dense.data_ptr(), self.energies.data_ptr(),
-                           self.compressed.data_ptr(), pp, float(lr), self.ws.data_ptr(), self.ws.numel(),
-                           _stream_ptr(stream)))
+        if self.momentum_buf is not None:
+            _check(_step_fused_momentum(self._grad_ptrs, self.K, self.n, self._ratios, self.delta, self._w,
+                                        self._idx_ptrs, self._val_ptrs, self.dense.data_ptr(),
+                                        self.energies.data_ptr(), self.compressed.data_ptr(), pp,
+                                        _dev_f32(self.momentum_buf, "momentum_buf"), float(lr), self.momentum,
+                                        self.weight_decay, self.ws.data_ptr(), self.ws.numel(),
+                                        _stream_ptr(stream)))
+        else:
+            _check(_step_fused(self._grad_ptrs, self.K, self.n, self._ratios, self.delta, self._w,
+                               self._idx_ptrs, self._val_ptrs, self.dense.data_ptr(), self.energies.data_ptr(),
+                               self.compressed.data_ptr(), pp, float(lr), self.ws.data_ptr(), self.ws.numel(),
+                               _stream_ptr(stream)))
         return StepOutputs(self.idx, self.val, self.dense, self.energies, self.compressed)
 
 

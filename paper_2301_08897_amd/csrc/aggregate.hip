@@ -149,12 +149,16 @@ __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
     }
   }
   const uint64_t dmask = ballot(dn);
-  // Parameters of a full range are fetched now, used after the accumulation.
-  f4 pp[kARange / 256];
+  // Parameters (and momentum buffer) of a full range are fetched now, used after the accumulation.
+  f4 pp[kARange / 256], vv[kARange / 256];
   const bool pre = c.params && len == (uint32_t)kARange;
   if (pre) {
 #pragma unroll
     for (int m = 0; m < kARange / 256; ++m) pp[m] = *reinterpret_cast<const f4*>(c.params + base + m * 256 + l * 4);
+    if (c.mbuf) {
+#pragma unroll
+      for (int m = 0; m < kARange / 256; ++m) vv[m] = *reinterpret_cast<const f4*>(c.mbuf + base + m * 256 + l * 4);
+    }
   }
 #pragma unroll
   for (int m = 0; m < kARange / 64; ++m) acc[m * 64 + l] = 0.0;
@@ -172,19 +176,32 @@ __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
     add_batch(a, acc, jb + kABatch, K, eb, em, dmask, base, len, ib, vb);
   }
 
-  // Round once to float; optionally the SGD update of Eqn 4c on the float aggregate.
+  // Round once to float; optionally the SGD update of Eqn 4c (or momentum SGD
+  // with weight decay) on the float aggregate.
+  const double nlr = -(double)c.lr, mom = (double)c.mom, wd = (double)c.wd;
   if (pre) {
-    const double nlr = -(double)c.lr;
 #pragma unroll
     for (int m = 0; m < kARange / 256; ++m) {
       const uint32_t e = m * 256 + l * 4;
       const f4 g = {(float)acc[e], (float)acc[e + 1], (float)acc[e + 2], (float)acc[e + 3]};
       *reinterpret_cast<f4*>(c.out + base + e) = g;
       f4 p = pp[m];
-      p.x = (float)__builtin_fma(nlr, (double)g.x, (double)p.x);
-      p.y = (float)__builtin_fma(nlr, (double)g.y, (double)p.y);
-      p.z = (float)__builtin_fma(nlr, (double)g.z, (double)p.z);
-      p.w = (float)__builtin_fma(nlr, (double)g.w, (double)p.w);
+      if (c.mbuf) {
+        f4 v = vv[m];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float pq = p[q], vq = v[q];
+          momentum_step(pq, vq, g[q], nlr, mom, wd);
+          p[q] = pq;
+          v[q] = vq;
+        }
+        *reinterpret_cast<f4*>(c.mbuf + base + e) = v;
+      } else {
+        p.x = (float)__builtin_fma(nlr, (double)g.x, (double)p.x);
+        p.y = (float)__builtin_fma(nlr, (double)g.y, (double)p.y);
+        p.z = (float)__builtin_fma(nlr, (double)g.z, (double)p.z);
+        p.w = (float)__builtin_fma(nlr, (double)g.w, (double)p.w);
+      }
       *reinterpret_cast<f4*>(c.params + base + e) = p;
     }
     return;
@@ -195,19 +212,36 @@ __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
       *reinterpret_cast<f4*>(c.out + base + e) = g;
       if (c.params) {
         f4 p = *reinterpret_cast<const f4*>(c.params + base + e);
-        const double nlr = -(double)c.lr;
-        p.x = (float)__builtin_fma(nlr, (double)g.x, (double)p.x);
-        p.y = (float)__builtin_fma(nlr, (double)g.y, (double)p.y);
-        p.z = (float)__builtin_fma(nlr, (double)g.z, (double)p.z);
-        p.w = (float)__builtin_fma(nlr, (double)g.w, (double)p.w);
+        if (c.mbuf) {
+          f4 v = *reinterpret_cast<const f4*>(c.mbuf + base + e);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+          float pq = p[q], vq = v[q];
+          momentum_step(pq, vq, g[q], nlr, mom, wd);
+          p[q] = pq;
+          v[q] = vq;
+        }
+          *reinterpret_cast<f4*>(c.mbuf + base + e) = v;
+        } else {
+          p.x = (float)__builtin_fma(nlr, (double)g.x, (double)p.x);
+          p.y = (float)__builtin_fma(nlr, (double)g.y, (double)p.y);
+          p.z = (float)__builtin_fma(nlr, (double)g.z, (double)p.z);
+          p.w = (float)__builtin_fma(nlr, (double)g.w, (double)p.w);
+        }
         *reinterpret_cast<f4*>(c.params + base + e) = p;
       }
     } else {
       for (uint32_t q = e; q < len; ++q) {
         const float g = (float)acc[q];
         c.out[base + q] = g;
-        if (c.params)
-          c.params[base + q] = (float)__builtin_fma(-(double)c.lr, (double)g, (double)c.params[base + q]);
+        if (c.params && c.mbuf) {
+          float p = c.params[base + q], v = c.mbuf[base + q];
+          momentum_step(p, v, g, nlr, mom, wd);
+          c.mbuf[base + q] = v;
+          c.params[base + q] = p;
+        } else if (c.params) {
+          c.params[base + q] = (float)__builtin_fma(nlr, (double)g, (double)c.params[base + q]);
+        }
       }
     }
   }
@@ -261,6 +295,46 @@ hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate
     }
   }
   k_aggregate<<<c.nrange, 64, 0, s>>>(a, c);
+  return hipGetLastError();
+}
+
+// Momentum SGD with weight decay on its own (same arithmetic as the fused update).
+__global__ __launch_bounds__(kBlock) void k_momentum_sgd(float* p, float* v, const float* g, uint64_t n, float lr,
+                                                         float mom, float wd)
+{
+  const double nlr = -(double)lr, mu = (double)mom, dw = (double)wd;
+  const uint64_t n4 = n / 4;
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n4; i += stride) {
+    f4 pv = *reinterpret_cast<const f4*>(p + 4 * i);
+    f4 vv = *reinterpret_cast<const f4*>(v + 4 * i);
+    const f4 gv = __builtin_nontemporal_load(reinterpret_cast<const f4*>(g + 4 * i));
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float pq = pv[q], vq = vv[q];
+      momentum_step(pq, vq, gv[q], nlr, mu, dw);
+      pv[q] = pq;
+      vv[q] = vq;
+    }
+    *reinterpret_cast<f4*>(v + 4 * i) = vv;
+    *reinterpret_cast<f4*>(p + 4 * i) = pv;
+  }
+  if (blockIdx.x == 0 && threadIdx.x < (n & 3)) {
+    const uint64_t i = 4 * n4 + threadIdx.x;
+    float pi = p[i], vi = v[i];
+    momentum_step(pi, vi, g[i], nlr, mu, dw);
+    v[i] = vi;
+    p[i] = pi;
+  }
+}
+
+hipError_t launch_momentum_sgd(float* p, float* v, const float* g, uint64_t n, float lr, float mom, float wd,
+                               hipStream_t s)
+{
+  uint64_t blocks = (n / 4 + kBlock - 1) / kBlock;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 8192) blocks = 8192;
+  k_momentum_sgd<<<(uint32_t)blocks, kBlock, 0, s>>>(p, v, g, n, lr, mom, wd);
   return hipGetLastError();
 }
 

@@ -253,6 +253,14 @@ Ctx make_ctx(const Layout& L, void* ws)
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// Whether two float arrays of n elements share memory.
+bool overlap(const float* a, const float* b, uint64_t n)
+{
+  const char* x = reinterpret_cast<const char*>(a);
+  const char* y = reinterpret_cast<const char*>(b);
+  return x < y + n * sizeof(float) && y < x + n * sizeof(float);
+}
+
 scadles_status check_ws(void* ws, size_t ws_bytes, size_t need)
 {
   if (!ws) return fail(SCADLES_EWORKSPACE, "workspace is NULL (need %zu bytes)", need);
@@ -436,6 +444,23 @@ scadles_status scadles_weighted_aggregate(const scadles_sparse* sets, const floa
   return SCADLES_OK;
 }
 
+scadles_status scadles_apply_momentum_sgd(float* params, float* momentum_buf, const float* grad, uint64_t n,
+                                          float lr, float momentum, float weight_decay, void* stream)
+{
+  if (scadles_status st = check_n(n)) return st;
+  if (!params || !momentum_buf || !grad) return fail(SCADLES_EINVAL, "params, momentum_buf and grad must not be NULL");
+  if (!aligned(params, 16) || !aligned(momentum_buf, 16) || !aligned(grad, 16))
+    return fail(SCADLES_EINVAL, "params, momentum_buf and grad must be 16-byte aligned");
+  if (!std::isfinite(lr) || !std::isfinite(momentum) || !std::isfinite(weight_decay))
+    return fail(SCADLES_EINVAL, "lr, momentum and weight_decay must be finite");
+  if (overlap(params, grad, n) || overlap(momentum_buf, grad, n) || overlap(params, momentum_buf, n))
+    return fail(SCADLES_EINVAL, "params, momentum_buf and grad must not overlap");
+  hipError_t e = launch_momentum_sgd(params, momentum_buf, grad, n, lr, momentum, weight_decay,
+                                     static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "momentum sgd launch");
+  return SCADLES_OK;
+}
+
 scadles_status scadles_apply_sgd(float* params, const float* grad, uint64_t n, float lr, void* stream)
 {
   if (scadles_status st = check_n(n)) return st;
@@ -451,10 +476,12 @@ scadles_status scadles_apply_sgd(float* params, const float* grad, uint64_t n, f
   return SCADLES_OK;
 }
 
-scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_t n, const double* ratios,
-                                  double delta, const float* weights, uint32_t* const* idx, float* const* val,
-                                  float* dense, double* energies, uint8_t* compressed, float* params, float lr,
-                                  void* ws, size_t ws_bytes, void* stream)
+// Both fused entry points: mbuf == NULL applies Eqn 4c, else momentum SGD with weight decay.
+static scadles_status step_fused_impl(const float* const* grads, uint32_t K, uint64_t n, const double* ratios,
+                                      double delta, const float* weights, uint32_t* const* idx, float* const* val,
+                                      float* dense, double* energies, uint8_t* compressed, float* params,
+                                      float* mbuf, float lr, float mom, float wd, void* ws, size_t ws_bytes,
+                                      void* stream)
 {
   if (K == 0 || K > kMaxK) return fail(SCADLES_EINVAL, "K = %u is outside [1, %d]", K, kMaxK);
   if (scadles_status st = check_n(n)) return st;
@@ -463,6 +490,13 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
   if (!aligned(dense, 16)) return fail(SCADLES_EINVAL, "dense must be 16-byte aligned");
   if (params && !aligned(params, 16)) return fail(SCADLES_EINVAL, "params must be 16-byte aligned");
   if (params && !std::isfinite(lr)) return fail(SCADLES_EINVAL, "lr is not finite");
+  if (mbuf) {
+    if (!params) return fail(SCADLES_EINVAL, "the momentum update needs params");
+    if (!aligned(mbuf, 16)) return fail(SCADLES_EINVAL, "momentum_buf must be 16-byte aligned");
+    if (!std::isfinite(mom) || !std::isfinite(wd)) return fail(SCADLES_EINVAL, "momentum and weight_decay must be finite");
+    if (overlap(mbuf, params, n) || overlap(mbuf, dense, n))
+      return fail(SCADLES_EINVAL, "momentum_buf overlaps params or dense");
+  }
   if (energies && !aligned(energies, 8)) return fail(SCADLES_EINVAL, "energies must be 8-byte aligned");
   if (scadles_status st = check_weights(weights, K)) return st;
   for (uint32_t j = 0; j < K; ++j) {
@@ -505,7 +539,10 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
   c.err = reinterpret_cast<uint32_t*>(b + L.o_aerr);
   c.out = dense;
   c.params = params;
+  c.mbuf = mbuf;
   c.lr = lr;
+  c.mom = mom;
+  c.wd = wd;
   c.K = K;
   c.nrange = L.nrange;
   c.kmax = (uint32_t)kmax;
@@ -517,6 +554,26 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
   if (pr) (void)hipEventRecord(pr->ev[3 + 2 * pr->parts], s);
   if (e != hipSuccess) return hip_fail(e, "aggregate launch");
   return SCADLES_OK;
+}
+
+scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_t n, const double* ratios,
+                                  double delta, const float* weights, uint32_t* const* idx, float* const* val,
+                                  float* dense, double* energies, uint8_t* compressed, float* params, float lr,
+                                  void* ws, size_t ws_bytes, void* stream)
+{
+  return step_fused_impl(grads, K, n, ratios, delta, weights, idx, val, dense, energies, compressed, params, nullptr,
+                         lr, 0.f, 0.f, ws, ws_bytes, stream);
+}
+
+scadles_status scadles_step_fused_momentum(const float* const* grads, uint32_t K, uint64_t n, const double* ratios,
+                                           double delta, const float* weights, uint32_t* const* idx,
+                                           float* const* val, float* dense, double* energies, uint8_t* compressed,
+                                           float* params, float* momentum_buf, float lr, float momentum,
+                                           float weight_decay, void* ws, size_t ws_bytes, void* stream)
+{
+  if (!params || !momentum_buf) return fail(SCADLES_EINVAL, "params and momentum_buf must not be NULL");
+  return step_fused_impl(grads, K, n, ratios, delta, weights, idx, val, dense, energies, compressed, params,
+                         momentum_buf, lr, momentum, weight_decay, ws, ws_bytes, stream);
 }
 
 scadles_status scadles_stream_weights(const double* rates, uint32_t K, double b_min, double b_max, double base_batch,

@@ -153,7 +153,9 @@ struct AggCtx {
   uint32_t* err;          // validation flag
   float* out;             // dense aggregate
   float* params;          // null: no SGD
+  float* mbuf;            // not null: momentum SGD with weight decay (momentum buffer), else Eqn 4c
   float lr;
+  float mom, wd;
   uint32_t K;
   uint32_t nrange;        // ceil(n / kARange): waves of the aggregation kernel
   uint32_t kmax;
@@ -177,6 +179,18 @@ hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, h
 hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate, bool marks_done, hipStream_t s);
 hipError_t launch_marks(const AggArgs& a, const AggCtx& c, hipStream_t s);
 hipError_t launch_sgd(float* p, const float* g, uint64_t n, float lr, hipStream_t s);
+hipError_t launch_momentum_sgd(float* p, float* v, const float* g, uint64_t n, float lr, float mom, float wd,
+                               hipStream_t s);
+
+// Momentum SGD with weight decay on one element: every product of two floats is
+// exact in double, each step rounds once in double, and the stored buffer is
+// the value the parameter update uses.
+__device__ inline void momentum_step(float& p, float& v, float g, double nlr, double mom, double wd)
+{
+  const double d = __builtin_fma(wd, (double)p, (double)g);
+  v = (float)__builtin_fma(mom, (double)v, d);
+  p = (float)__builtin_fma(nlr, (double)v, (double)p);
+}
 
 // ---- sizing shared by host and device -----------------------------------------------------
 __host__ __device__ inline uint32_t bitlen32(uint32_t x) { return x ? 32u - (uint32_t)__builtin_clz(x) : 0u; }

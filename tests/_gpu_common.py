@@ -65,9 +65,11 @@ def oracle_topk_all(s, it, G, topk=None, threads=1):
 
 
 def check_step(sc, s, it, G, out, w, lr, params_before, params_after, delta=math.inf, topk=None,
-               label="", threads=1):
+               label="", threads=1, mom=None):
     """Compare one fused step against the oracle. `topk(g, k)` returns the oracle's
-    (idx, val, e_all, e_kept); defaults to the full-sort oracle."""
+    (idx, val, e_all, e_kept); defaults to the full-sort oracle. With `mom` =
+    (momentum, weight_decay, buf_before, buf_after) the update is momentum SGD
+    and (params, buf) of the oracle are returned."""
     n, K = s.n, s.K
     results = oracle_topk_all(s, it, G, topk, threads)
     w_o, gamma_o = oracle.stream_weights(s.rates[it], base_batch=s.base_batch)
@@ -100,6 +102,12 @@ def check_step(sc, s, it, G, out, w, lr, params_before, params_after, delta=math
     dense = out.dense.cpu().numpy()
     assert within_north_star_tolerance(dense, dense_o), f"{label}: aggregate outside tolerance"
     assert same_bits(dense, dense_o), f"{label}: aggregate not bit-identical to the oracle"
+    if params_before is not None and mom is not None:
+        mu, wd, v_before, v_after = mom
+        p_o, v_o = oracle.momentum_sgd(params_before, v_before, dense_o, lr_o, mu, wd)
+        assert same_bits(v_after, v_o), f"{label}: momentum buffer differs"
+        assert same_bits(params_after, p_o), f"{label}: momentum SGD update differs"
+        return p_o, v_o
     if params_before is not None:
         p_o = oracle.sgd(params_before, dense_o, lr_o)
         assert same_bits(params_after, p_o), f"{label}: SGD update differs"
@@ -108,8 +116,10 @@ def check_step(sc, s, it, G, out, w, lr, params_before, params_after, delta=math
 
 
 def run_config(sc, config, n=None, K=None, iterations=None, delta=math.inf, with_params=True, topk=None,
-               ratio_override=None, threads=1):
-    """Run `iterations` fused steps of a workload and check each against the oracle."""
+               ratio_override=None, threads=1, momentum=None):
+    """Run `iterations` fused steps of a workload and check each against the oracle.
+    `momentum` = (momentum, weight_decay) runs the momentum-SGD fused step from a
+    zero buffer."""
     torch, dev = torch_dev()
     s = workloads.spec(config, n=n, K=K, iterations=iterations)
     if ratio_override is not None:
@@ -118,6 +128,9 @@ def run_config(sc, config, n=None, K=None, iterations=None, delta=math.inf, with
     params = workloads.params0(s) if with_params else None
     p_dev = torch.from_numpy(params).to(dev) if with_params else None
     p_ref = params.copy() if with_params else None
+    if momentum is not None:
+        v_ref = np.zeros(s.n, dtype=np.float32)
+        v_dev = torch.zeros(s.n, dtype=torch.float32, device=dev)
     for it in range(s.iterations):
         log(f"  {label} iteration {it}: ratio {s.ratios[it, 0]}")
         G = np.empty((s.K, s.n), dtype=np.float32)
@@ -126,11 +139,20 @@ def run_config(sc, config, n=None, K=None, iterations=None, delta=math.inf, with
         g_dev = torch.from_numpy(G).to(dev)
         w, gamma = sc.stream_weights(s.rates[it], base_batch=s.base_batch)
         lr = float(np.float32(s.eta * gamma))
-        step = sc.FusedStep(g_dev, s.ratios[it], delta=delta, params=p_dev)
+        if momentum is not None:
+            step = sc.FusedStep(g_dev, s.ratios[it], delta=delta, params=p_dev, momentum_buf=v_dev,
+                                momentum=momentum[0], weight_decay=momentum[1])
+        else:
+            step = sc.FusedStep(g_dev, s.ratios[it], delta=delta, params=p_dev)
         out = step.run(w, lr)
         torch.cuda.synchronize()
         p_after = p_dev.cpu().numpy() if with_params else None
-        p_ref = check_step(sc, s, it, G, out, w, lr, p_ref, p_after, delta=delta, topk=topk,
-                           label=f"{label} it={it}", threads=threads)
+        if momentum is not None:
+            p_ref, v_ref = check_step(sc, s, it, G, out, w, lr, p_ref, p_after, delta=delta, topk=topk,
+                                      label=f"{label} it={it}", threads=threads,
+                                      mom=(momentum[0], momentum[1], v_ref, v_dev.cpu().numpy()))
+        else:
+            p_ref = check_step(sc, s, it, G, out, w, lr, p_ref, p_after, delta=delta, topk=topk,
+                               label=f"{label} it={it}", threads=threads)
         del g_dev, step, out, G
     return s

@@ -113,6 +113,35 @@ def test_host_validation_before_any_launch(sc):
     assert b"no_such_option" in sc._last_error()
 
 
+def test_momentum_validation_before_any_launch(sc):
+    """Invalid momentum-SGD calls return EINVAL and launch nothing."""
+    inval = 1
+    f = sc._apply_momentum_sgd
+    assert f(None, 4096, 8192, 10, 0.1, 0.9, 0.0, None) == inval                 # NULL params
+    assert f(16, None, 8192, 10, 0.1, 0.9, 0.0, None) == inval                   # NULL buffer
+    assert f(16, 4096, 8192, 0, 0.1, 0.9, 0.0, None) == inval                    # n = 0
+    assert f(20, 4096, 8192, 10, 0.1, 0.9, 0.0, None) == inval                   # misaligned
+    assert f(16, 16, 8192, 10, 0.1, 0.9, 0.0, None) == inval                     # params is the buffer
+    assert f(16, 4096, 16, 10, 0.1, 0.9, 0.0, None) == inval                     # grad aliases params
+    assert f(16, 4096, 8192, 10, 0.1, float("inf"), 0.0, None) == inval          # momentum not finite
+    assert f(16, 4096, 8192, 10, 0.1, 0.9, float("nan"), None) == inval          # decay not finite
+    grads = (ctypes.c_void_p * 2)(16, 32)
+    ratios = (ctypes.c_double * 2)(0.1, 0.1)
+    outs = (ctypes.c_void_p * 2)(16, 32)
+    w = (ctypes.c_float * 2)(0.5, 0.5)
+    g = sc._step_fused_momentum
+    assert g(grads, 2, 1000, ratios, math.inf, w, outs, outs, 16, None, None, None, 4096, 0.1, 0.9, 0.0,
+             4096, 1 << 30, None) == inval                                          # no params
+    assert g(grads, 2, 1000, ratios, math.inf, w, outs, outs, 16, None, None, 8192, None, 0.1, 0.9, 0.0,
+             4096, 1 << 30, None) == inval                                          # no buffer
+    assert g(grads, 2, 1000, ratios, math.inf, w, outs, outs, 16, None, None, 8192, 8192, 0.1, 0.9, 0.0,
+             4096, 1 << 30, None) == inval                                          # buffer is params
+    assert g(grads, 2, 1000, ratios, math.inf, w, outs, outs, 16, None, None, 8192, 16, 0.1, 0.9, 0.0,
+             4096, 1 << 30, None) == inval                                          # buffer is dense
+    assert g(grads, 2, 1000, ratios, math.inf, w, outs, outs, 16, None, None, 8192, 65536, 0.1,
+             float("nan"), 0.0, 4096, 1 << 30, None) == inval                       # momentum not finite
+
+
 def test_workspace_queries(sc):
     assert sc.workspace_bytes(1, 0, [0.5]) == 0
     assert sc.workspace_bytes(65, 100, [0.5] * 65) == 0
