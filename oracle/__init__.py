@@ -66,6 +66,10 @@ def _load():
                                          _u64p, _f32p, _f32p]
         lib.oracle_sgd.restype = None
         lib.oracle_sgd.argtypes = [_f32p, _f32p, ctypes.c_uint64, ctypes.c_float]
+        lib.oracle_adaptive_step.restype = ctypes.c_int
+        lib.oracle_adaptive_step.argtypes = [_f64p, ctypes.POINTER(ctypes.c_uint64), ctypes.c_double,
+                                             ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                             ctypes.c_uint64, ctypes.c_uint64]
         lib.oracle_momentum_sgd.restype = None
         lib.oracle_momentum_sgd.argtypes = [_f32p, _f32p, _f32p, ctypes.c_uint64, ctypes.c_float,
                                             ctypes.c_float, ctypes.c_float]
@@ -139,6 +143,27 @@ def compress_decision(e_all: float, e_kept: float, delta: float):
     r = _load().oracle_compress_decision(float(e_all), float(e_kept), float(delta),
                                          ctypes.byref(rho))
     return bool(r), rho.value
+
+
+def adaptive_step(state: np.ndarray, counters, e_all: float, e_kept: float, beta: float, delta: float,
+                  k: int, n: int) -> bool:
+    """Adaptive rule of §IV on the moving average of the energies, with the
+    accounting of §V-G. ``state`` (float64[2]) and ``counters`` (uint64[3] or
+    None) of one device are updated in place. Returns whether Top-k is sent."""
+    if state.dtype != np.float64 or state.size != 2 or not state.flags.c_contiguous:
+        raise ValueError("state must be a contiguous float64[2]")
+    cp = None
+    if counters is not None:
+        if counters.dtype != np.uint64 or counters.size != 3 or not counters.flags.c_contiguous:
+            raise ValueError("counters must be a contiguous uint64[3]")
+        cp = counters.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64))
+    return bool(_load().oracle_adaptive_step(_ptr(state, ctypes.c_double), cp, float(e_all), float(e_kept),
+                                             float(beta), float(delta), int(k), int(n)))
+
+
+def cnc_ratio(counters) -> float:
+    """CNC ratio of §V-G: iterations that sent Top-k over all iterations."""
+    return float(counters[0]) / float(counters[1]) if counters[1] else 0.0
 
 
 def aggregate(sets, weights, n: int) -> np.ndarray:

@@ -104,6 +104,36 @@ int oracle_compress_decision(double e_all, double e_kept, double delta, double* 
   return rho <= delta ? 1 : 0;
 }
 
+/* Adaptive compression with the moving average of §IV (the energies of the
+ * compressed and uncompressed gradients tracked as an exponentially weighted
+ * moving average) and the accounting of §V-G (CNC ratio, floats sent). The
+ * paper gives no smoothing factor, so beta is a parameter; beta = 0 is the
+ * instantaneous rule. state[0..1] are one device's smoothed E_all and E_kept;
+ * both zero means no history, and that iteration takes its energies as they
+ * are. Otherwise each is replaced by beta * state + (1 - beta) * E, evaluated
+ * in double. The rule of §IV is then applied to the smoothed pair.
+ * counters (or NULL): [0] iterations that sent Top-k, [1] iterations, [2]
+ * floats sent (k when compressed, n otherwise: the update's values, which is
+ * what §V-G counts). Returns 1 to send Top-k, 0 to send the dense gradient.  */
+int oracle_adaptive_step(double* state, uint64_t* counters, double e_all, double e_kept, double beta,
+                         double delta, uint64_t k, uint64_t n)
+{
+  if (state[0] == 0.0 && state[1] == 0.0) {
+    state[0] = e_all;
+    state[1] = e_kept;
+  } else {
+    state[0] = beta * state[0] + (1.0 - beta) * e_all;
+    state[1] = beta * state[1] + (1.0 - beta) * e_kept;
+  }
+  const int send = oracle_compress_decision(state[0], state[1], delta, NULL);
+  if (counters) {
+    counters[0] += (uint64_t)send;
+    counters[1] += 1;
+    counters[2] += send ? k : n;
+  }
+  return send;
+}
+
 /* Weighted aggregation, Eqn 4b: out[i] = sum_{j=0..K-1} w_j * v_j(i), where
  * v_j(i) is device j's value at i if i is one of its k_j kept positions and 0
  * otherwise. idx[j] == NULL marks a device that sent its dense gradient
