@@ -170,18 +170,47 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
                                   float* params, float lr,
                                   void* ws, size_t ws_bytes, void* stream);
 
-/* scadles_step_fused with the momentum SGD of scadles_apply_momentum_sgd in
- * place of Eqn 4c, fused into the aggregation (computed from the float g~
- * written to dense). params and momentum_buf (dev, n floats, 16-byte aligned,
- * not overlapping each other or dense) are both required and updated in
- * place; momentum and weight_decay finite. Other arguments and errors as for
- * scadles_step_fused.                                                       */
-scadles_status scadles_step_fused_momentum(const float* const* grads, uint32_t K, uint64_t n,
-                                           const double* ratios, double delta, const float* weights,
-                                           uint32_t* const* idx, float* const* val, float* dense,
-                                           double* energies, uint8_t* compressed, float* params,
-                                           float* momentum_buf, float lr, float momentum,
-                                           float weight_decay, void* ws, size_t ws_bytes, void* stream);
+/* Options of scadles_step_fused_ex; an all-zero struct gives exactly
+ * scadles_step_fused.
+ *   momentum_buf  (dev, n floats, 16-byte aligned, not overlapping params or
+ *                 dense) or NULL. When set, the update after the aggregation
+ *                 is the momentum SGD of scadles_apply_momentum_sgd with
+ *                 `momentum` and `weight_decay` (finite) in place of Eqn 4c,
+ *                 computed from the float g~ written to dense; params is
+ *                 then required.
+ *   ewma          (dev, 2K doubles, 8-byte aligned) or NULL. When set, the
+ *                 adaptive rule of §IV is applied to moving averages of each
+ *                 device's energies kept here (the paper tracks them as an
+ *                 exponentially weighted moving average but prints no
+ *                 factor): ewma[2j], ewma[2j+1] <- ewma_beta * ewma + (1 -
+ *                 ewma_beta) * (E_all, E_kept), in double; a device whose
+ *                 pair is (0, 0) has no history and takes its energies as they
+ *                 are. Zero-fill before the first step. ewma_beta in [0, 1);
+ *                 0 is the instantaneous rule.
+ *   counters      (dev, 3K uint64, 8-byte aligned) or NULL. When set, each
+ *                 call adds per device j: counters[3j] += 1 if it sent Top-k,
+ *                 counters[3j+1] += 1, counters[3j+2] += k_j if it sent
+ *                 Top-k else n (floats sent; values only, as §V-G counts
+ *                 them). The CNC ratio of §V-G is counters[3j] /
+ *                 counters[3j+1].                                           */
+typedef struct scadles_step_options {
+  float* momentum_buf;
+  float momentum;
+  float weight_decay;
+  double* ewma;
+  double ewma_beta;
+  uint64_t* counters;
+} scadles_step_options;
+
+/* scadles_step_fused with the options above (momentum SGD, moving-average
+ * adaptive rule, CNC and floats-sent accounting). options must not be NULL.
+ * Other arguments and errors as for scadles_step_fused.                    */
+scadles_status scadles_step_fused_ex(const float* const* grads, uint32_t K, uint64_t n,
+                                     const double* ratios, double delta, const float* weights,
+                                     uint32_t* const* idx, float* const* val, float* dense,
+                                     double* energies, uint8_t* compressed, float* params, float lr,
+                                     const scadles_step_options* options, void* ws, size_t ws_bytes,
+                                     void* stream);
 
 /* Aggregation weights and learning-rate scale from streaming rates
  * (§IV "Heterogeneous streams", Eqn 4a and the linear scaling rule):

@@ -43,6 +43,12 @@ class Sparse(ctypes.Structure):
     _fields_ = [("idx", _vp), ("val", _vp), ("k", _u64)]
 
 
+class StepOptions(ctypes.Structure):
+    """scadles_step_options (momentum SGD, moving-average adaptive rule, accounting)."""
+    _fields_ = [("momentum_buf", _vp), ("momentum", ctypes.c_float), ("weight_decay", ctypes.c_float),
+                ("ewma", _vp), ("ewma_beta", ctypes.c_double), ("counters", _vp)]
+
+
 def _sig(name, restype, *argtypes):
     f = getattr(_lib, name)
     f.restype = restype
@@ -64,10 +70,10 @@ _step_fused = _sig("scadles_step_fused", ctypes.c_int, ctypes.POINTER(_vp), _u32
                    ctypes.POINTER(ctypes.c_double), ctypes.c_double, ctypes.POINTER(ctypes.c_float),
                    ctypes.POINTER(_vp), ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, ctypes.c_float, _vp,
                    ctypes.c_size_t, _vp)
-_step_fused_momentum = _sig("scadles_step_fused_momentum", ctypes.c_int, ctypes.POINTER(_vp), _u32, _u64,
-                            ctypes.POINTER(ctypes.c_double), ctypes.c_double, ctypes.POINTER(ctypes.c_float),
-                            ctypes.POINTER(_vp), ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, _vp, ctypes.c_float,
-                            ctypes.c_float, ctypes.c_float, _vp, ctypes.c_size_t, _vp)
+_step_fused_ex = _sig("scadles_step_fused_ex", ctypes.c_int, ctypes.POINTER(_vp), _u32, _u64,
+                      ctypes.POINTER(ctypes.c_double), ctypes.c_double, ctypes.POINTER(ctypes.c_float),
+                      ctypes.POINTER(_vp), ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, ctypes.c_float,
+                      ctypes.POINTER(StepOptions), _vp, ctypes.c_size_t, _vp)
 _stream_weights = _sig("scadles_stream_weights", ctypes.c_int, ctypes.POINTER(ctypes.c_double), _u32,
                        ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_float),
                        ctypes.POINTER(ctypes.c_double))
@@ -254,7 +260,8 @@ class FusedStep:
     the workspace allocated once so that ``run`` only marshals pointers."""
 
     def __init__(self, grads, ratios: Sequence[float], *, delta: float = math.inf, params=None,
-                 momentum_buf=None, momentum: float = 0.0, weight_decay: float = 0.0):
+                 momentum_buf=None, momentum: float = 0.0, weight_decay: float = 0.0,
+                 ewma_beta: Optional[float] = None, track: bool = False):
         torch = _torch()
         if isinstance(grads, torch.Tensor) and grads.dim() == 2:
             grads = [grads[j] for j in range(grads.shape[0])]
@@ -282,6 +289,17 @@ class FusedStep:
                 raise ValueError("params and momentum_buf must have n elements")
         self.delta = float(delta)
         self.set_ratios(ratios)
+        # §IV moving average of the energies (state zero-filled: no history) and
+        # §V-G accounting, both kept on the device across run() calls
+        self.ewma_beta = None if ewma_beta is None else float(ewma_beta)
+        self.ewma = (torch.zeros(2 * self.K, dtype=torch.float64, device=dev)
+                     if ewma_beta is not None else None)
+        self.counters = torch.zeros(3 * self.K, dtype=torch.int64, device=dev) if track else None
+        self._opts = StepOptions(
+            momentum_buf.data_ptr() if momentum_buf is not None else None, self.momentum, self.weight_decay,
+            self.ewma.data_ptr() if self.ewma is not None else None,
+            self.ewma_beta if self.ewma_beta is not None else 0.0,
+            self.counters.data_ptr() if self.counters is not None else None)
         self.dense = torch.empty(self.n, dtype=torch.float32, device=dev)
         self.energies = torch.empty(2 * self.K, dtype=torch.float64, device=dev)
         self.compressed = torch.empty(self.K, dtype=torch.uint8, device=dev)
@@ -313,19 +331,27 @@ class FusedStep:
         for j in range(self.K):
             self._w[j] = float(w[j])
         pp = _dev_f32(self.params, "params") if self.params is not None else None
-        if self.momentum_buf is not None:
-            _check(_step_fused_momentum(self._grad_ptrs, self.K, self.n, self._ratios, self.delta, self._w,
-                                        self._idx_ptrs, self._val_ptrs, self.dense.data_ptr(),
-                                        self.energies.data_ptr(), self.compressed.data_ptr(), pp,
-                                        _dev_f32(self.momentum_buf, "momentum_buf"), float(lr), self.momentum,
-                                        self.weight_decay, self.ws.data_ptr(), self.ws.numel(),
-                                        _stream_ptr(stream)))
+        if self.momentum_buf is not None or self.ewma is not None or self.counters is not None:
+            _check(_step_fused_ex(self._grad_ptrs, self.K, self.n, self._ratios, self.delta, self._w,
+                                  self._idx_ptrs, self._val_ptrs, self.dense.data_ptr(), self.energies.data_ptr(),
+                                  self.compressed.data_ptr(), pp, float(lr), ctypes.byref(self._opts),
+                                  self.ws.data_ptr(), self.ws.numel(), _stream_ptr(stream)))
         else:
             _check(_step_fused(self._grad_ptrs, self.K, self.n, self._ratios, self.delta, self._w,
                                self._idx_ptrs, self._val_ptrs, self.dense.data_ptr(), self.energies.data_ptr(),
                                self.compressed.data_ptr(), pp, float(lr), self.ws.data_ptr(), self.ws.numel(),
                                _stream_ptr(stream)))
         return StepOutputs(self.idx, self.val, self.dense, self.energies, self.compressed)
+
+
+    def accounting(self):
+        """Per device (iterations that sent Top-k, iterations, floats sent) and the
+        CNC ratio of §V-G, from the counters (``track=True``)."""
+        if self.counters is None:
+            raise ValueError("construct with track=True")
+        c = self.counters.cpu().numpy().reshape(self.K, 3)
+        cnc = [float(r[0]) / float(r[1]) if r[1] else 0.0 for r in c]
+        return c, cnc
 
 
 def step_fused(grads, ratios, weights, *, delta: float = math.inf, params=None, lr: float = 0.0,

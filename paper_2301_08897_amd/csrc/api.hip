@@ -299,7 +299,8 @@ uint32_t parts_for(const Layout& L)
 }
 
 scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double delta, double* energies,
-                          uint8_t* compressed, hipStream_t s, ProfRec* pr, uint32_t* lb = nullptr)
+                          uint8_t* compressed, hipStream_t s, ProfRec* pr, uint32_t* lb = nullptr,
+                          const scadles_step_options* opt = nullptr)
 {
   Ctx c = make_ctx(L, ws);
   c.delta = delta;
@@ -314,6 +315,11 @@ scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double d
   p.parts = parts_for(L);
   c.lb = lb;
   c.nrange = L.nrange;
+  if (opt) {
+    c.ewma = opt->ewma;
+    c.ewma_beta = opt->ewma_beta;
+    c.counters = opt->counters;
+  }
   if (pr) pr->parts = p.parts;
   StreamSet* ss = p.parts > 1 ? stream_set() : nullptr;
   if (p.parts > 1 && !ss) return fail(SCADLES_EHIP, "could not create the pipeline stream");
@@ -476,13 +482,15 @@ scadles_status scadles_apply_sgd(float* params, const float* grad, uint64_t n, f
   return SCADLES_OK;
 }
 
-// Both fused entry points: mbuf == NULL applies Eqn 4c, else momentum SGD with weight decay.
+// Both fused entry points (opt all zero: scadles_step_fused).
 static scadles_status step_fused_impl(const float* const* grads, uint32_t K, uint64_t n, const double* ratios,
                                       double delta, const float* weights, uint32_t* const* idx, float* const* val,
                                       float* dense, double* energies, uint8_t* compressed, float* params,
-                                      float* mbuf, float lr, float mom, float wd, void* ws, size_t ws_bytes,
+                                      float lr, const scadles_step_options& opt, void* ws, size_t ws_bytes,
                                       void* stream)
 {
+  float* mbuf = opt.momentum_buf;
+  const float mom = opt.momentum, wd = opt.weight_decay;
   if (K == 0 || K > kMaxK) return fail(SCADLES_EINVAL, "K = %u is outside [1, %d]", K, kMaxK);
   if (scadles_status st = check_n(n)) return st;
   if (!grads || !ratios || !idx || !val || !dense) return fail(SCADLES_EINVAL, "NULL argument");
@@ -497,6 +505,11 @@ static scadles_status step_fused_impl(const float* const* grads, uint32_t K, uin
     if (overlap(mbuf, params, n) || overlap(mbuf, dense, n))
       return fail(SCADLES_EINVAL, "momentum_buf overlaps params or dense");
   }
+  if (opt.ewma) {
+    if (!aligned(opt.ewma, 8)) return fail(SCADLES_EINVAL, "ewma must be 8-byte aligned");
+    if (!(opt.ewma_beta >= 0.0 && opt.ewma_beta < 1.0)) return fail(SCADLES_EINVAL, "ewma_beta must be in [0, 1)");
+  }
+  if (opt.counters && !aligned(opt.counters, 8)) return fail(SCADLES_EINVAL, "counters must be 8-byte aligned");
   if (energies && !aligned(energies, 8)) return fail(SCADLES_EINVAL, "energies must be 8-byte aligned");
   if (scadles_status st = check_weights(weights, K)) return st;
   for (uint32_t j = 0; j < K; ++j) {
@@ -549,7 +562,7 @@ static scadles_status step_fused_impl(const float* const* grads, uint32_t K, uin
   c.n = n;
   // each device group's range markers are built right after its selection
   if (pr) (void)hipEventRecord(pr->ev[0], s);
-  if (scadles_status st = run_select(L, a, ws, delta, energies, compressed, s, pr, c.lb)) return st;
+  if (scadles_status st = run_select(L, a, ws, delta, energies, compressed, s, pr, c.lb, &opt)) return st;
   hipError_t e = launch_aggregate(g, c, 0, true, s);
   if (pr) (void)hipEventRecord(pr->ev[3 + 2 * pr->parts], s);
   if (e != hipSuccess) return hip_fail(e, "aggregate launch");
@@ -561,19 +574,20 @@ scadles_status scadles_step_fused(const float* const* grads, uint32_t K, uint64_
                                   float* dense, double* energies, uint8_t* compressed, float* params, float lr,
                                   void* ws, size_t ws_bytes, void* stream)
 {
-  return step_fused_impl(grads, K, n, ratios, delta, weights, idx, val, dense, energies, compressed, params, nullptr,
-                         lr, 0.f, 0.f, ws, ws_bytes, stream);
+  scadles_step_options none;
+  memset(&none, 0, sizeof(none));
+  return step_fused_impl(grads, K, n, ratios, delta, weights, idx, val, dense, energies, compressed, params, lr,
+                         none, ws, ws_bytes, stream);
 }
 
-scadles_status scadles_step_fused_momentum(const float* const* grads, uint32_t K, uint64_t n, const double* ratios,
-                                           double delta, const float* weights, uint32_t* const* idx,
-                                           float* const* val, float* dense, double* energies, uint8_t* compressed,
-                                           float* params, float* momentum_buf, float lr, float momentum,
-                                           float weight_decay, void* ws, size_t ws_bytes, void* stream)
+scadles_status scadles_step_fused_ex(const float* const* grads, uint32_t K, uint64_t n, const double* ratios,
+                                     double delta, const float* weights, uint32_t* const* idx, float* const* val,
+                                     float* dense, double* energies, uint8_t* compressed, float* params, float lr,
+                                     const scadles_step_options* options, void* ws, size_t ws_bytes, void* stream)
 {
-  if (!params || !momentum_buf) return fail(SCADLES_EINVAL, "params and momentum_buf must not be NULL");
-  return step_fused_impl(grads, K, n, ratios, delta, weights, idx, val, dense, energies, compressed, params,
-                         momentum_buf, lr, momentum, weight_decay, ws, ws_bytes, stream);
+  if (!options) return fail(SCADLES_EINVAL, "options must not be NULL");
+  return step_fused_impl(grads, K, n, ratios, delta, weights, idx, val, dense, energies, compressed, params, lr,
+                         *options, ws, ws_bytes, stream);
 }
 
 scadles_status scadles_stream_weights(const double* rates, uint32_t K, double b_min, double b_max, double base_batch,

@@ -117,6 +117,9 @@ struct Ctx {
   uint32_t* fb_count;     // devices on the exact path (the exact-path kernels exit early at 0)
   uint32_t* lb;           // fused step: aggregation range markers (see AggCtx), else null
   uint32_t nrange;
+  double* ewma;           // [K][2] moving averages of E_all, E_kept (adaptive rule), or null
+  double ewma_beta;
+  uint64_t* counters;     // [K][3] iterations compressed, iterations, floats sent; or null
   double delta;
 };
 

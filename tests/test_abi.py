@@ -129,17 +129,21 @@ def test_momentum_validation_before_any_launch(sc):
     ratios = (ctypes.c_double * 2)(0.1, 0.1)
     outs = (ctypes.c_void_p * 2)(16, 32)
     w = (ctypes.c_float * 2)(0.5, 0.5)
-    g = sc._step_fused_momentum
-    assert g(grads, 2, 1000, ratios, math.inf, w, outs, outs, 16, None, None, None, 4096, 0.1, 0.9, 0.0,
-             4096, 1 << 30, None) == inval                                          # no params
-    assert g(grads, 2, 1000, ratios, math.inf, w, outs, outs, 16, None, None, 8192, None, 0.1, 0.9, 0.0,
-             4096, 1 << 30, None) == inval                                          # no buffer
-    assert g(grads, 2, 1000, ratios, math.inf, w, outs, outs, 16, None, None, 8192, 8192, 0.1, 0.9, 0.0,
-             4096, 1 << 30, None) == inval                                          # buffer is params
-    assert g(grads, 2, 1000, ratios, math.inf, w, outs, outs, 16, None, None, 8192, 16, 0.1, 0.9, 0.0,
-             4096, 1 << 30, None) == inval                                          # buffer is dense
-    assert g(grads, 2, 1000, ratios, math.inf, w, outs, outs, 16, None, None, 8192, 65536, 0.1,
-             float("nan"), 0.0, 4096, 1 << 30, None) == inval                       # momentum not finite
+
+    def ex(params, opts):
+        return sc._step_fused_ex(grads, 2, 1000, ratios, math.inf, w, outs, outs, 16, None, None, params, 0.1,
+                                 ctypes.byref(opts) if opts is not None else None, 4096, 1 << 30, None)
+
+    O = sc.StepOptions
+    assert ex(8192, None) == inval                                            # no options
+    assert ex(None, O(4096, 0.9, 0.0, None, 0.0, None)) == inval              # momentum without params
+    assert ex(8192, O(8192, 0.9, 0.0, None, 0.0, None)) == inval              # buffer is params
+    assert ex(8192, O(16, 0.9, 0.0, None, 0.0, None)) == inval                # buffer is dense
+    assert ex(8192, O(65536, float("nan"), 0.0, None, 0.0, None)) == inval    # momentum not finite
+    assert ex(8192, O(None, 0.0, 0.0, 65536, 1.0, None)) == inval             # beta outside [0, 1)
+    assert ex(8192, O(None, 0.0, 0.0, 65536, -0.5, None)) == inval
+    assert ex(8192, O(None, 0.0, 0.0, 65537, 0.5, None)) == inval             # misaligned ewma
+    assert ex(8192, O(None, 0.0, 0.0, None, 0.0, 65539)) == inval             # misaligned counters
 
 
 def test_workspace_queries(sc):
