@@ -57,6 +57,9 @@ def _load():
         lib.oracle_topk.restype = ctypes.c_int
         lib.oracle_topk.argtypes = [_f32p, ctypes.c_uint64, ctypes.c_uint64, _u32p, _f32p,
                                     _f64p, _f64p]
+        lib.oracle_topk_layers.restype = ctypes.c_int
+        lib.oracle_topk_layers.argtypes = [_f32p, _u64p, ctypes.c_uint32, ctypes.c_double, _u32p, _f32p,
+                                           _f64p, _f64p, _u64p]
         lib.oracle_compress_decision.restype = ctypes.c_int
         lib.oracle_compress_decision.argtypes = [ctypes.c_double, ctypes.c_double,
                                                  ctypes.c_double, _f64p]
@@ -128,6 +131,52 @@ def topk_by_threshold(g: np.ndarray, k: int):
     keep[ties] = True
     idx = np.flatnonzero(keep).astype(np.uint32)
     return idx, np.float32(t), c_gt, need
+
+
+def layers_k(seg_off, ratio: float) -> int:
+    """Entries kept by the per-layer Top-k: the sum over layers of topk_k(layer size, ratio)."""
+    off = np.asarray(seg_off, dtype=np.uint64)
+    return sum(topk_k(int(off[l + 1] - off[l]), ratio) for l in range(off.size - 1))
+
+
+def topk_layers(g: np.ndarray, seg_off, ratio: float):
+    """Per-layer Top-k (each layer keeps its own top fraction; the per-layer
+    reading of §IV) by a full sort of every layer. ``seg_off`` = [0, ..., n],
+    layer l being g[seg_off[l]:seg_off[l+1]]. Returns (idx uint32 ascending,
+    val float32, e_all, e_kept) of the whole gradient."""
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    off = np.ascontiguousarray(seg_off, dtype=np.uint64)
+    L = off.size - 1
+    if L < 1 or int(off[-1]) != g.size:
+        raise ValueError("seg_off must run from 0 to g.size")
+    k = layers_k(off, ratio)
+    idx = np.empty(max(k, 1), dtype=np.uint32)
+    val = np.empty(max(k, 1), dtype=np.float32)
+    e_all = ctypes.c_double()
+    e_kept = ctypes.c_double()
+    k_out = ctypes.c_uint64()
+    rc = _load().oracle_topk_layers(_ptr(g, ctypes.c_float), _ptr(off, ctypes.c_uint64), L, float(ratio),
+                                    _ptr(idx, ctypes.c_uint32), _ptr(val, ctypes.c_float), ctypes.byref(e_all),
+                                    ctypes.byref(e_kept), ctypes.byref(k_out))
+    if rc != 0 or int(k_out.value) != k:
+        raise ValueError(f"oracle_topk_layers rejected L={L} ratio={ratio}")
+    return idx[:k], val[:k], e_all.value, e_kept.value
+
+
+def topk_layers_by_threshold(g: np.ndarray, seg_off, ratio: float):
+    """Per-layer Top-k in O(n) for full-size vectors: ``topk_by_threshold`` on
+    every layer, indices shifted by the layer's start. Returns (idx, val,
+    e_all, e_kept) like ``topk_layers``."""
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    off = np.asarray(seg_off, dtype=np.uint64)
+    parts = []
+    for l in range(off.size - 1):
+        a, b = int(off[l]), int(off[l + 1])
+        i, _, _, _ = topk_by_threshold(g[a:b], topk_k(b - a, ratio))
+        parts.append(i.astype(np.uint64) + a)
+    idx = np.concatenate(parts).astype(np.uint32)
+    e_all, e_kept = energies(g, idx)
+    return idx, g[idx], e_all, e_kept
 
 
 def energies(g: np.ndarray, idx: np.ndarray):

@@ -93,6 +93,42 @@ int oracle_topk(const float* g, uint64_t n, uint64_t k, uint32_t* idx_out, float
   return out == k ? 0 : -1;
 }
 
+/* Per-layer Top-k: the reading of the Top-k of §IV in which every layer of the
+ * model keeps its own top fraction. The gradient is cut into L layers, layer l
+ * being positions [seg_off[l], seg_off[l+1]); each layer keeps its
+ * oracle_topk_k(layer size, ratio) entries of largest magnitude (ties to the
+ * lower index) among its own entries only. The kept set is the union over the
+ * layers, written in ascending index order; e_all and e_kept are the energies
+ * of the whole gradient, summed in ascending index order as in oracle_topk.
+ * *k_out receives the total kept. Returns 0, or -1 on bad arguments.        */
+int oracle_topk_layers(const float* g, const uint64_t* seg_off, uint32_t L, double ratio,
+                       uint32_t* idx_out, float* val_out, double* e_all, double* e_kept, uint64_t* k_out)
+{
+  if (!g || !seg_off || L == 0 || seg_off[0] != 0 || seg_off[L] > 0xFFFFFFFFull) return -1;
+  uint64_t at = 0;
+  for (uint32_t l = 0; l < L; ++l) {
+    if (seg_off[l + 1] <= seg_off[l]) return -1;
+    uint64_t n_l = seg_off[l + 1] - seg_off[l];
+    uint64_t k_l = oracle_topk_k(n_l, ratio);
+    if (k_l == 0) return -1;
+    /* the layer on its own: positions relative to its start */
+    if (oracle_topk(g + seg_off[l], n_l, k_l, idx_out ? idx_out + at : NULL, val_out ? val_out + at : NULL,
+                    NULL, NULL) != 0)
+      return -1;
+    if (idx_out)
+      for (uint64_t r = 0; r < k_l; ++r) idx_out[at + r] += (uint32_t)seg_off[l];
+    at += k_l;
+  }
+  if (k_out) *k_out = at;
+  double all = 0.0, kep = 0.0;
+  for (uint64_t i = 0; i < seg_off[L]; ++i) all += (double)g[i] * (double)g[i];
+  if (val_out)
+    for (uint64_t r = 0; r < at; ++r) kep += (double)val_out[r] * (double)val_out[r];
+  if (e_all) *e_all = all;
+  if (e_kept) *e_kept = kep;
+  return 0;
+}
+
 /* The adaptive compression rule of §IV: send Top-k(g) when
  * | ||g||^2 - ||Top-k(g)||^2 | / ||g||^2 <= delta, else send g. A zero
  * gradient loses nothing (ratio 0). Returns 1 for "send Top-k", 0 for
