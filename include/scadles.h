@@ -103,6 +103,30 @@ scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio,
                                    uint32_t* idx, float* val, double* energies,
                                    void* ws, size_t ws_bytes, void* stream);
 
+/* Per-layer Top-k: the per-layer reading of the Top-k sparsification of §IV
+ * (each layer of the model keeps its own top fraction) for K devices whose
+ * flat gradients share one layer layout. Layer l is positions
+ * [seg_off[l], seg_off[l+1]) of every gradient and keeps k_l =
+ * scadles_topk_k(seg_off[l+1] - seg_off[l], ratio_j) entries of device j,
+ * chosen as scadles_topk_select chooses them within the layer. Device j's
+ * kept set is the union over its layers, written in ascending index order
+ * (layer after layer, indices relative to the whole gradient) to idx[j] /
+ * val[j]: scadles_layers_k(seg_off, L, ratio_j) entries.
+ *   grads     (host[K] of dev pointers, seg_off[L] floats each, 4-byte aligned).
+ *   seg_off   (host[L+1]) 0 = seg_off[0] < seg_off[1] < ... < seg_off[L] <= 2^32 - 1; L >= 1.
+ *   ratios    (host[K]) in (0, 1].
+ *   idx, val  (host[K] of dev pointers, 4-byte aligned).
+ *   energies  (dev, 2K doubles) or NULL: E_all and E_kept of each whole gradient.
+ *   ws        scadles_layers_workspace_bytes(K, seg_off, L, ratios) bytes.
+ * The layers are selected one after the other; feed the sets to
+ * scadles_weighted_aggregate for Eqn 4b. Same error convention as above.    */
+uint64_t scadles_layers_k(const uint64_t* seg_off, uint32_t L, double ratio);
+size_t scadles_layers_workspace_bytes(uint32_t K, const uint64_t* seg_off, uint32_t L, const double* ratios);
+scadles_status scadles_topk_select_layers(const float* const* grads, uint32_t K, const uint64_t* seg_off,
+                                          uint32_t L, const double* ratios, uint32_t* const* idx,
+                                          float* const* val, double* energies, void* ws, size_t ws_bytes,
+                                          void* stream);
+
 /* Weighted aggregation of K devices' contributions (Eqn 4b):
  *   dense[i] = sum over j = 0..K-1, in that order, of w_j * v_j(i)
  * where v_j(i) is device j's value at i (zero when i is not in a sparse set).

@@ -61,6 +61,12 @@ _ws_bytes = _sig("scadles_workspace_bytes", ctypes.c_size_t, _u32, _u64, ctypes.
 _agg_ws_bytes = _sig("scadles_aggregate_workspace_bytes", ctypes.c_size_t, _u32, _u64)
 _topk_select = _sig("scadles_topk_select", ctypes.c_int, _vp, _u64, ctypes.c_double, _vp, _vp, _vp, _vp,
                     ctypes.c_size_t, _vp)
+_layers_k = _sig("scadles_layers_k", _u64, ctypes.POINTER(_u64), _u32, ctypes.c_double)
+_layers_ws_bytes = _sig("scadles_layers_workspace_bytes", ctypes.c_size_t, _u32, ctypes.POINTER(_u64), _u32,
+                        ctypes.POINTER(ctypes.c_double))
+_topk_select_layers = _sig("scadles_topk_select_layers", ctypes.c_int, ctypes.POINTER(_vp), _u32,
+                           ctypes.POINTER(_u64), _u32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_vp),
+                           ctypes.POINTER(_vp), _vp, _vp, ctypes.c_size_t, _vp)
 _weighted_aggregate = _sig("scadles_weighted_aggregate", ctypes.c_int, ctypes.POINTER(Sparse),
                            ctypes.POINTER(ctypes.c_float), _u32, _u64, _vp, _vp, ctypes.c_size_t, _vp)
 _apply_sgd = _sig("scadles_apply_sgd", ctypes.c_int, _vp, _vp, _u64, ctypes.c_float, _vp)
@@ -133,6 +139,24 @@ def topk_k(n: int, ratio: float) -> int:
 def workspace_bytes(K: int, n: int, ratios: Sequence[float]) -> int:
     r = (ctypes.c_double * K)(*[float(x) for x in ratios])
     return int(_ws_bytes(K, int(n), r))
+
+
+def _seg_array(seg_off):
+    off = [int(x) for x in seg_off]
+    return (_u64 * len(off))(*off), len(off) - 1
+
+
+def layers_k(seg_off: Sequence[int], ratio: float) -> int:
+    """Entries kept by the per-layer Top-k over layers [seg_off[l], seg_off[l+1])
+    (0 for invalid input)."""
+    arr, L = _seg_array(seg_off)
+    return int(_layers_k(arr, max(L, 0), float(ratio))) if L >= 1 else 0
+
+
+def layers_workspace_bytes(K: int, seg_off: Sequence[int], ratios: Sequence[float]) -> int:
+    arr, L = _seg_array(seg_off)
+    r = (ctypes.c_double * K)(*[float(x) for x in ratios])
+    return int(_layers_ws_bytes(K, arr, L, r)) if L >= 1 else 0
 
 
 def aggregate_workspace_bytes(K: int, n: int) -> int:
@@ -241,6 +265,50 @@ def apply_momentum_sgd(params, momentum_buf, grad, lr: float, momentum: float, w
                                _dev_f32(grad, "grad"), params.numel(), float(lr), float(momentum),
                                float(weight_decay), _stream_ptr(stream)))
     return params, momentum_buf
+
+
+class LayerSelect:
+    """Per-layer Top-k of K gradients that share one layer layout (every layer
+    keeps its own top fraction): outputs and workspace allocated once, ``run``
+    only marshals pointers. ``seg_off`` = [0, ..., n] are the layer bounds."""
+
+    def __init__(self, grads, seg_off: Sequence[int], ratios: Sequence[float]):
+        torch = _torch()
+        if isinstance(grads, torch.Tensor) and grads.dim() == 2:
+            grads = [grads[j] for j in range(grads.shape[0])]
+        self.grads = list(grads)
+        self.K = len(self.grads)
+        if not 1 <= self.K <= MAX_DEVICES:
+            raise ValueError(f"K must be in [1, {MAX_DEVICES}]")
+        self.seg_off = [int(x) for x in seg_off]
+        self.n = self.seg_off[-1] if self.seg_off else 0
+        for j, g in enumerate(self.grads):
+            _dev_f32(g, f"grads[{j}]")
+            if g.numel() != self.n:
+                raise ValueError("every gradient must have seg_off[-1] elements")
+        self.ratios = [float(r) for r in ratios]
+        if len(self.ratios) != self.K:
+            raise ValueError("one ratio per device")
+        self.k = [layers_k(self.seg_off, r) for r in self.ratios]
+        if min(self.k) == 0:
+            raise ScadlesError(1, "invalid layer bounds or ratio")
+        dev = self.grads[0].device
+        self.idx = [torch.empty(k, dtype=torch.uint32, device=dev) for k in self.k]
+        self.val = [torch.empty(k, dtype=torch.float32, device=dev) for k in self.k]
+        self.energies = torch.empty(2 * self.K, dtype=torch.float64, device=dev)
+        self.ws = _workspace(layers_workspace_bytes(self.K, self.seg_off, self.ratios), dev)
+        self._seg, self._L = _seg_array(self.seg_off)
+        self._ratios = (ctypes.c_double * self.K)(*self.ratios)
+        self._grad_ptrs = (_vp * self.K)(*[g.data_ptr() for g in self.grads])
+        self._idx_ptrs = (_vp * self.K)(*[t.data_ptr() for t in self.idx])
+        self._val_ptrs = (_vp * self.K)(*[t.data_ptr() for t in self.val])
+
+    def run(self, *, stream=None):
+        """Select every device's kept set; returns (idx list, val list, energies float64[2K])."""
+        _check(_topk_select_layers(self._grad_ptrs, self.K, self._seg, self._L, self._ratios, self._idx_ptrs,
+                                   self._val_ptrs, self.energies.data_ptr(), self.ws.data_ptr(), self.ws.numel(),
+                                   _stream_ptr(stream)))
+        return self.idx, self.val, self.energies
 
 
 # ---- the fused step -----------------------------------------------------------------------------

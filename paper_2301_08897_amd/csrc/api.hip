@@ -300,7 +300,8 @@ uint32_t parts_for(const Layout& L)
 
 scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double delta, double* energies,
                           uint8_t* compressed, hipStream_t s, ProfRec* pr, uint32_t* lb = nullptr,
-                          const scadles_step_options* opt = nullptr)
+                          const scadles_step_options* opt = nullptr, uint32_t idx_base = 0,
+                          bool energies_add = false)
 {
   Ctx c = make_ctx(L, ws);
   c.delta = delta;
@@ -315,6 +316,8 @@ scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double d
   p.parts = parts_for(L);
   c.lb = lb;
   c.nrange = L.nrange;
+  c.idx_base = idx_base;
+  c.energies_add = energies_add ? 1u : 0u;
   if (opt) {
     c.ewma = opt->ewma;
     c.ewma_beta = opt->ewma_beta;
@@ -388,6 +391,88 @@ scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio, 
   scadles_status st = run_select(L, a, ws, INFINITY, energies, nullptr, s, pr);
   if (pr) (void)hipEventRecord(pr->ev[3 + 2 * pr->parts], s);
   return st;
+}
+
+// Layers of a per-layer selection: checks seg_off (0 = off[0] < ... < off[L]
+// <= 2^32 - 1) and returns the kept entries of one device.
+static scadles_status check_layers(const uint64_t* seg_off, uint32_t L)
+{
+  if (!seg_off || L == 0) return fail(SCADLES_EINVAL, "seg_off must not be NULL and L >= 1");
+  if (seg_off[0] != 0) return fail(SCADLES_EINVAL, "seg_off[0] must be 0");
+  for (uint32_t l = 0; l < L; ++l)
+    if (!(seg_off[l] < seg_off[l + 1])) return fail(SCADLES_EINVAL, "layer %u is empty or out of order", l);
+  if (seg_off[L] > 0xFFFFFFFFull) return fail(SCADLES_EINVAL, "n = %llu exceeds 2^32 - 1", (unsigned long long)seg_off[L]);
+  return SCADLES_OK;
+}
+
+uint64_t scadles_layers_k(const uint64_t* seg_off, uint32_t L, double ratio)
+{
+  if (!seg_off || L == 0 || seg_off[0] != 0) return 0;
+  uint64_t k = 0;
+  for (uint32_t l = 0; l < L; ++l) {
+    if (!(seg_off[l] < seg_off[l + 1]) || seg_off[L] > 0xFFFFFFFFull) return 0;
+    const uint64_t kl = k_rule(seg_off[l + 1] - seg_off[l], ratio);
+    if (kl == 0) return 0;
+    k += kl;
+  }
+  return k;
+}
+
+size_t scadles_layers_workspace_bytes(uint32_t K, const uint64_t* seg_off, uint32_t L, const double* ratios)
+{
+  if (K == 0 || K > kMaxK || !ratios || scadles_layers_k(seg_off, L, 0.5) == 0) return 0;
+  size_t most = 0;
+  for (uint32_t l = 0; l < L; ++l) {
+    const size_t b = scadles_workspace_bytes(K, seg_off[l + 1] - seg_off[l], ratios);
+    if (b == 0) return 0;
+    if (b > most) most = b;
+  }
+  return most;
+}
+
+scadles_status scadles_topk_select_layers(const float* const* grads, uint32_t K, const uint64_t* seg_off, uint32_t L,
+                                          const double* ratios, uint32_t* const* idx, float* const* val,
+                                          double* energies, void* ws, size_t ws_bytes, void* stream)
+{
+  if (K == 0 || K > kMaxK) return fail(SCADLES_EINVAL, "K = %u is outside [1, %d]", K, kMaxK);
+  if (scadles_status st = check_layers(seg_off, L)) return st;
+  if (!grads || !ratios || !idx || !val) return fail(SCADLES_EINVAL, "NULL argument");
+  if (energies && !aligned(energies, 8)) return fail(SCADLES_EINVAL, "energies must be 8-byte aligned");
+  for (uint32_t j = 0; j < K; ++j) {
+    if (!grads[j] || !idx[j] || !val[j]) return fail(SCADLES_EINVAL, "device %u has a NULL pointer", j);
+    if (!aligned(grads[j], 4)) return fail(SCADLES_EINVAL, "grads[%u] must be 4-byte aligned", j);
+    if (!aligned(idx[j], 4) || !aligned(val[j], 4)) return fail(SCADLES_EINVAL, "device %u outputs misaligned", j);
+    if (scadles_layers_k(seg_off, L, ratios[j]) == 0)
+      return fail(SCADLES_EINVAL, "ratio %g of device %u is not in (0, 1]", ratios[j], j);
+  }
+  const size_t need = scadles_layers_workspace_bytes(K, seg_off, L, ratios);
+  if (scadles_status st = check_ws(ws, ws_bytes, need)) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint64_t at[kMaxK] = {};          // entries written so far per device
+  for (uint32_t l = 0; l < L; ++l) {
+    const uint64_t off = seg_off[l], nl = seg_off[l + 1] - off;
+    Layout Ll;
+    make_layout(K, nl, ratios, g_force_exact.load() != 0, true, Ll);
+    PrepArgs a;
+    memset(&a, 0, sizeof(a));
+    for (uint32_t j = 0; j < K; ++j) {
+      a.grad[j] = grads[j] + off;
+      a.idx[j] = idx[j] + at[j];
+      a.val[j] = val[j] + at[j];
+      a.k[j] = Ll.k[j];
+      a.cap[j] = Ll.cap[j];
+      a.mode[j] = Ll.mode[j];
+      a.r_lo[j] = Ll.r_lo[j];
+      a.r_hi[j] = Ll.r_hi[j];
+      at[j] += Ll.k[j];
+    }
+    // each layer on its own, its indices offset by the layer's start; the
+    // energies of later layers are added to the first's
+    if (scadles_status st = run_select(Ll, a, ws, INFINITY, energies, nullptr, s, nullptr, nullptr, nullptr,
+                                       (uint32_t)off, l > 0))
+      return st;
+  }
+  return SCADLES_OK;
 }
 
 scadles_status scadles_weighted_aggregate(const scadles_sparse* sets, const float* weights, uint32_t K, uint64_t n,

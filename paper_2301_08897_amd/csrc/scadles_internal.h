@@ -120,6 +120,8 @@ struct Ctx {
   double* ewma;           // [K][2] moving averages of E_all, E_kept (adaptive rule), or null
   double ewma_beta;
   uint64_t* counters;     // [K][3] iterations compressed, iterations, floats sent; or null
+  uint32_t idx_base;      // added to every output index (a layer's offset in the gradient)
+  uint32_t energies_add;  // 1: add the energies to energies_out (a layer after the first)
   double delta;
 };
 

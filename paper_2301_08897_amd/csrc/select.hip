@@ -1055,7 +1055,7 @@ __device__ inline void write_fast_body(const Ctx& c, uint32_t b)
       const uint32_t pos = gt_b + (eq_b < need32 ? eq_b : need32);
       const float v = __uint_as_float(vb);
       if (pos < k32) {
-        oi[pos] = idx;
+        oi[pos] = idx + c.idx_base;
         ov[pos] = v;
       }
       e2 = __builtin_fma((double)v, (double)v, e2);
@@ -1172,8 +1172,8 @@ __device__ inline void scan_cf_body(const Ctx& c, uint32_t jr)
 // Writes the kept entries of one block in index order.
 //   kept: key > thr, or key == thr with fewer than `need` equal keys before it;
 //   position: (keys > thr before it) + min(equal keys before it, need).
-// `src_idx` (candidate lists) gives each element's index; without it the index
-// is the virtual position minus the row's shift.
+// An element's index is its virtual position minus the row's shift, plus
+// `base` (the offset of a layer selected on its own).
 __device__ inline uint32_t write_count(const f4& x, uint32_t thr1)
 {
   uint32_t cnt = 0;
@@ -1188,7 +1188,7 @@ __device__ inline uint32_t write_count(const f4& x, uint32_t thr1)
 
 // One round of the ordered write: the wave's elements above the threshold, and
 // equal ones while fewer than `need` came before, at their kept positions.
-__device__ inline void write_round(const f4& x, uint64_t e, uint64_t vbase, const Row& row, const uint32_t* src_idx,
+__device__ inline void write_round(const f4& x, uint64_t e, uint64_t vbase, const Row& row, uint32_t base,
                                    uint32_t thr1, uint64_t need, uint32_t k, GLOBAL uint32_t* out_idx, GLOBAL float* out_val,
                                    uint64_t& run_g, uint64_t& run_e, double& e2)
 {
@@ -1205,13 +1205,6 @@ __device__ inline void write_round(const f4& x, uint64_t e, uint64_t vbase, cons
   if ((bg[0] | bg[1] | bg[2] | bg[3] | be[0] | be[1] | be[2] | be[3]) == 0ull) return;
   uint64_t gt_b = run_g + mbcnt(bg[0]) + mbcnt(bg[1]) + mbcnt(bg[2]) + mbcnt(bg[3]);
   uint64_t eq_b = run_e + mbcnt(be[0]) + mbcnt(be[1]) + mbcnt(be[2]) + mbcnt(be[3]);
-  u4 ix = {0u, 0u, 0u, 0u};
-  if (src_idx) {
-    if (e + 4 <= row.n) ix = ldu4(src_idx + e);
-    else
-      for (int q = 0; q < 4; ++q)
-        if (e + q < row.n) ix[q] = src_idx[e + q];
-  }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const bool keep = fg[q] || (fe[q] && eq_b < need);
@@ -1219,7 +1212,7 @@ __device__ inline void write_round(const f4& x, uint64_t e, uint64_t vbase, cons
       const uint64_t pos = gt_b + (eq_b < need ? eq_b : need);
       const float val = x[q];
       if (pos < k) {
-        out_idx[pos] = src_idx ? ix[q] : (uint32_t)(vbase + e + q - row.shift);
+        out_idx[pos] = (uint32_t)(vbase + e + q - row.shift) + base;
         out_val[pos] = val;
       }
       e2 = __builtin_fma((double)val, (double)val, e2);
@@ -1236,10 +1229,10 @@ __device__ inline void write_round(const f4& x, uint64_t e, uint64_t vbase, cons
 // Writes the kept entries of one block in index order.
 //   kept: key > thr, or key == thr with fewer than `need` equal keys before it;
 //   position: (keys > thr before it) + min(equal keys before it, need).
-// `src_idx` (candidate lists) gives each element's index; without it the index
-// is the virtual position minus the row's shift.
+// An element's index is its virtual position minus the row's shift, plus
+// `base` (the offset of a layer selected on its own).
 template <int R>
-__device__ inline double block_write(const Row& row, uint64_t vbase, const uint32_t* src_idx, uint32_t thr,
+__device__ inline double block_write(const Row& row, uint64_t vbase, uint32_t base, uint32_t thr,
                                      uint64_t need, uint64_t pre, uint32_t k, GLOBAL uint32_t* out_idx, GLOBAL float* out_val,
                                      uint32_t* lds)
 {
@@ -1265,11 +1258,11 @@ __device__ inline double block_write(const Row& row, uint64_t vbase, const uint3
   if (full) {
 #pragma unroll
     for (int r = 0; r < R; ++r)
-      write_round(x[r], elem_of<R>(w, r, l), vbase, row, src_idx, thr1, need, k, out_idx, out_val, run_g, run_e, e2);
+      write_round(x[r], elem_of<R>(w, r, l), vbase, row, base, thr1, need, k, out_idx, out_val, run_g, run_e, e2);
   } else {
     for (int r = 0; r < R; ++r) {
       const uint64_t e = elem_of<R>(w, r, l);
-      write_round(load4(row, vbase + e, false), e, vbase, row, src_idx, thr1, need, k, out_idx, out_val, run_g,
+      write_round(load4(row, vbase + e, false), e, vbase, row, base, thr1, need, k, out_idx, out_val, run_g,
                   run_e, e2);
     }
   }
@@ -1290,7 +1283,7 @@ __device__ inline void write_cf_body(const Ctx& c, uint32_t worker, uint32_t wor
     const DevDesc d = c.desc[j];
     const Row row{gptr(d.grad), d.shift, c.n};
     for (uint32_t blk = worker; blk < c.nfb; blk += workers) {
-      const double e2 = block_write<kCBlkRounds>(row, (uint64_t)blk * kCBlk, nullptr, thr, need,
+      const double e2 = block_write<kCBlkRounds>(row, (uint64_t)blk * kCBlk, c.idx_base, thr, need,
                                                  c.blk_pre[(uint64_t)j * c.nbmax + blk], d.k, gptr(d.idx_out),
                                                  gptr(d.val_out), lds);
       const double es = block_sum_f64(e2, s_e);
@@ -1350,8 +1343,13 @@ __device__ inline void final_body(const Ctx& c, uint32_t jr)
     q[2] += s.sparse ? (uint64_t)c.desc[j].k : c.n;
   }
   if (c.energies_out) {
-    c.energies_out[2 * j] = s.e_all;
-    c.energies_out[2 * j + 1] = e_kept;
+    if (c.energies_add) {
+      c.energies_out[2 * j] += s.e_all;
+      c.energies_out[2 * j + 1] += e_kept;
+    } else {
+      c.energies_out[2 * j] = s.e_all;
+      c.energies_out[2 * j + 1] = e_kept;
+    }
   }
   if (c.compressed_out) c.compressed_out[j] = (uint8_t)s.sparse;
 }

@@ -157,3 +157,40 @@ def test_workspace_queries(sc):
     assert 0 < big < K * n + 2 * 1024**3
     assert sc.aggregate_workspace_bytes(0, 10) == 0
     assert sc.aggregate_workspace_bytes(4, 1 << 20) > 0
+
+
+def test_layers_validation_before_any_launch(sc):
+    """Invalid per-layer selections return a status and launch nothing."""
+    inval, ws = 1, 2
+    grads = (ctypes.c_void_p * 2)(16, 32)
+    idx = (ctypes.c_void_p * 2)(4096, 8192)
+    val = (ctypes.c_void_p * 2)(12288, 16384)
+    ratios = (ctypes.c_double * 2)(0.1, 0.1)
+
+    def call(off, r=ratios, K=2, g=grads, ws_bytes=1 << 30):
+        arr = (ctypes.c_uint64 * len(off))(*off)
+        return sc._topk_select_layers(g, K, arr, len(off) - 1, r, idx, val, None, 65536, ws_bytes, None)
+
+    assert call([1, 10]) == inval                                   # does not start at 0
+    assert call([0, 5, 5, 10]) == inval                             # empty layer
+    assert call([0, 6, 5, 10]) == inval                             # out of order
+    assert call([0, 2**32]) == inval                                # n too large
+    assert call([0]) == inval                                       # no layer
+    assert call([0, 10], r=(ctypes.c_double * 2)(0.1, 0.0)) == inval
+    assert call([0, 10], K=0) == inval
+    assert call([0, 10], g=(ctypes.c_void_p * 2)(18, 32)) == inval  # misaligned gradient
+    assert call([0, 5, 10], ws_bytes=64) == ws
+    assert sc._topk_select_layers(grads, 2, None, 1, ratios, idx, val, None, 65536, 1 << 30, None) == inval
+
+
+def test_layers_queries(sc, orc):
+    for off, r in (([0, 4, 10], 0.3), ([0, 64, 1064, 1101, 5101, 5102], 0.01), ([0, 10], 1.0),
+                   ([0, 1, 2, 3], 0.5), ([0, 100, 10**6, 143_667_240], 0.01)):
+        assert sc.layers_k(off, r) == orc.layers_k(off, r)
+    assert sc.layers_k([0, 5, 5, 10], 0.5) == 0
+    assert sc.layers_k([1, 10], 0.5) == 0
+    assert sc.layers_k([0, 10], 0.0) == 0
+    off = [0, 1000, 2_000_000, 2_000_100]
+    need = sc.layers_workspace_bytes(3, off, [0.01] * 3)
+    assert need >= sc.workspace_bytes(3, 1_999_000, [0.01] * 3) > 0
+    assert sc.layers_workspace_bytes(3, [0, 5, 5], [0.01] * 3) == 0

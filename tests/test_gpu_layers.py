@@ -1,0 +1,179 @@
+"""Per-layer Top-k on the HIP path against the oracle (every layer keeps its
+own top fraction, the per-layer reading of the Top-k of §IV): the workloads'
+own layer layouts, tiny and ragged layers, ties across layer bounds, every
+selection path, and the layered sets fed to the Eqn 4b aggregation. Indices
+and values bit for bit; energies within the bound of two double sums."""
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from _gpu_common import energy_tol, log, same_bits, torch_dev
+
+pytestmark = pytest.mark.gpu
+
+MODES = ("default", "force_exact", "force_fallback")
+
+
+@pytest.fixture(scope="module")
+def sc():
+    import paper_2301_08897_amd as sc
+    sc.set_option("force_exact", 0)
+    sc.set_option("force_fallback", 0)
+    return sc
+
+
+def layers_vs_oracle(sc, G: np.ndarray, seg_off, ratios, label, modes=("default",), topk=None,
+                     check_aggregate=False):
+    """Run the per-layer selection of every device of G (K x n) and compare it
+    with the oracle; returns the oracle's per-device results."""
+    torch, dev = torch_dev()
+    K = G.shape[0]
+    fn = topk or oracle.topk_layers
+    ref = [fn(G[j], seg_off, ratios[j]) for j in range(K)]
+    g_dev = torch.from_numpy(G).to(dev)
+    for mode in modes:
+        if mode != "default":
+            sc.set_option(mode, 1)
+        try:
+            sel = sc.LayerSelect(g_dev, seg_off, ratios)
+            idx, val, en = sel.run()
+            torch.cuda.synchronize()
+        finally:
+            if mode != "default":
+                sc.set_option(mode, 0)
+        e = en.cpu().numpy()
+        for j in range(K):
+            idx_o, val_o, ea, ek = ref[j]
+            got = idx[j].cpu().numpy()
+            if not np.array_equal(got, idx_o):
+                bad = np.flatnonzero(got != idx_o) if got.shape == idx_o.shape else "length"
+                raise AssertionError(f"{label} [{mode}] device {j}: indices (first mismatch {bad[:5]})")
+            assert same_bits(val[j].cpu().numpy(), val_o), f"{label} [{mode}] device {j}: values"
+            tol = energy_tol(G.shape[1]) * max(ea, 1e-300)
+            assert abs(e[2 * j] - ea) <= tol, f"{label} [{mode}] device {j}: E_all"
+            assert abs(e[2 * j + 1] - ek) <= tol, f"{label} [{mode}] device {j}: E_kept"
+        if check_aggregate:
+            w, _ = sc.stream_weights(np.arange(1.0, K + 1.0))
+            dense = sc.weighted_aggregate(list(zip(idx, val)), w, G.shape[1])
+            torch.cuda.synchronize()
+            dense_o = oracle.aggregate([(r[0], r[1]) for r in ref], w, G.shape[1])
+            assert same_bits(dense.cpu().numpy(), dense_o), f"{label} [{mode}]: aggregate of the layered sets"
+        del sel
+    return ref
+
+
+@pytest.mark.parametrize("config,n,K", [(1, None, None), (2, 700_001, 3), (3, 400_000, 4), (4, 900_000, 2),
+                                        (5, 1_200_000, 3)])
+def test_workload_layers(sc, config, n, K):
+    s = workloads.spec(config, n=n, K=K, iterations=1)
+    seg_off = [0] + [int(x) for x in s.seg_end]
+    log(f"layers C{config} n={s.n} K={s.K} L={len(seg_off) - 1}")
+    G = np.empty((s.K, s.n), dtype=np.float32)
+    for j in range(s.K):
+        workloads.gradient(s, 0, j, out=G[j])
+    layers_vs_oracle(sc, G, seg_off, list(s.ratios[0]), f"C{config} layers", modes=MODES,
+                     check_aggregate=True)
+
+
+def test_tiny_and_ragged_layers(sc):
+    rng = np.random.default_rng(11)
+    sizes = [1, 2, 3, 4, 5, 63, 64, 65, 255, 1023, 1024, 1025, 16385, 65537, 131072 + 77, 7]
+    seg_off = np.concatenate([[0], np.cumsum(sizes)]).tolist()
+    n = seg_off[-1]
+    K = 3
+    G = (rng.standard_normal((K, n)) * 10.0 ** rng.uniform(-4, 0, (K, n))).astype(np.float32)
+    for ratios in ([1e-9, 0.01, 0.3], [1.0, 0.5, 0.001]):
+        log(f"layers tiny/ragged ratios={ratios}")
+        layers_vs_oracle(sc, G, seg_off, ratios, f"ragged {ratios}", modes=MODES)
+
+
+def test_ties_across_layer_bounds(sc):
+    # few magnitude levels, signed zeros: every layer's threshold is tied, and
+    # equal values sit on both sides of each layer bound
+    rng = np.random.default_rng(12)
+    n = 300_000
+    seg_off = [0, 1000, 1001, 70_000, 70_001, 150_000, n]
+    G = (rng.integers(-3, 4, size=(2, n)) * 0.5).astype(np.float32)
+    G[rng.random((2, n)) < 0.2] = -0.0
+    for ratios in ([0.01, 0.1], [0.5, 0.9]):
+        log(f"layers ties ratios={ratios}")
+        layers_vs_oracle(sc, G, seg_off, ratios, f"ties {ratios}", modes=MODES)
+
+
+def test_one_layer_matches_whole_vector(sc):
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(13)
+    n = 500_000
+    g = rng.standard_normal(n).astype(np.float32)
+    log("layers L=1 vs the whole-vector selection")
+    idx, val, en = sc.LayerSelect(torch.from_numpy(g[None, :]).to(dev), [0, n], [0.01]).run()
+    idx1, val1, en1 = sc.topk_select(torch.from_numpy(g).to(dev), 0.01, energies=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(idx[0].cpu().numpy(), idx1.cpu().numpy())
+    assert same_bits(val[0].cpu().numpy(), val1.cpu().numpy())
+    assert np.array_equal(en.cpu().numpy(), en1.cpu().numpy())
+
+
+def test_repeated_runs_reuse_workspace(sc):
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(14)
+    n = 250_000
+    seg_off = [0, 100, 60_000, 60_100, n]
+    G = rng.standard_normal((2, n)).astype(np.float32)
+    ref = [oracle.topk_layers(G[j], seg_off, 0.02) for j in range(2)]
+    g_dev = torch.from_numpy(G).to(dev)
+    sel = sc.LayerSelect(g_dev, seg_off, [0.02, 0.02])
+    log("layers repeated runs")
+    for _ in range(3):
+        idx, val, en = sel.run()
+        torch.cuda.synchronize()
+        for j in range(2):
+            assert np.array_equal(idx[j].cpu().numpy(), ref[j][0])
+            assert same_bits(val[j].cpu().numpy(), ref[j][1])
+
+
+def test_layers_validation(sc):
+    torch, dev = torch_dev()
+    g = torch.zeros(10, dtype=torch.float32, device=dev)
+    with pytest.raises(sc.ScadlesError):
+        sc.LayerSelect([g], [0, 5, 5, 10], [0.5])
+    with pytest.raises(ValueError):
+        sc.LayerSelect([g], [0, 5, 11], [0.5])
+    with pytest.raises(sc.ScadlesError):
+        sc.LayerSelect([g], [0, 5, 10], [0.0])
+
+
+@pytest.mark.slow
+def test_full_size_vgg19_layers(sc):
+    """The largest workload (32 devices x 143,667,240, its 38 layers) at ratio
+    0.01, against the O(n) oracle on sampled devices (every device's kept
+    count and order checked)."""
+    torch, dev = torch_dev()
+    s = workloads.spec(5, iterations=1)
+    seg_off = [0] + [int(x) for x in s.seg_end]
+    log(f"full-size layers C5 n={s.n} K={s.K} L={len(seg_off) - 1}")
+    G = torch.empty((s.K, s.n), dtype=torch.float32, device=dev)
+    host = np.empty(s.n, dtype=np.float32)
+    sampled = {0: None, 13: None, 31: None}
+    for j in range(s.K):
+        workloads.gradient(s, 0, j, out=host)
+        G[j].copy_(torch.from_numpy(host))
+        if j in sampled:
+            sampled[j] = host.copy()
+    sel = sc.LayerSelect(G, seg_off, list(s.ratios[0]))
+    idx, val, en = sel.run()
+    torch.cuda.synchronize()
+    k = oracle.layers_k(seg_off, s.ratios[0, 0])
+    for j in range(s.K):
+        got = idx[j].cpu().numpy()
+        assert got.size == k and np.all(np.diff(got.astype(np.int64)) > 0), f"device {j}: order"
+    e = en.cpu().numpy()
+    for j, g in sampled.items():
+        log(f"  oracle device {j}")
+        idx_o, val_o, ea, ek = oracle.topk_layers_by_threshold(g, seg_off, s.ratios[0, j])
+        assert np.array_equal(idx[j].cpu().numpy(), idx_o), f"device {j}: indices"
+        assert same_bits(val[j].cpu().numpy(), val_o), f"device {j}: values"
+        tol = energy_tol(s.n) * ea
+        assert abs(e[2 * j] - ea) <= tol and abs(e[2 * j + 1] - ek) <= tol, f"device {j}: energies"
