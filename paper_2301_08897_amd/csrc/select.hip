@@ -95,6 +95,8 @@ __device__ inline f4 load4_guarded(const float* row, uint64_t e, uint64_t rem, b
 }
 
 
+constexpr uint32_t kNoDevice = 0xFFFFFFFFu;
+
 // ---- radix-selection digit view ------------------------------------------------------------
 struct SelView {
   uint32_t lo, hi, shift, width, prefix;
@@ -884,32 +886,47 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
   }
   const uint32_t worker = blockIdx.x - ncand_blocks, G = gridDim.x - ncand_blocks;
   if (*c.fb_count == 0u) return;
-  for (uint32_t j = c.j0; j < c.j0 + c.jn; ++j) {
-    const DevState& s = c.st[j];
-    if (!s.fallback) continue;
-    const Sel sel = s.sel[kSlotFull];
-    if (!sel.active) continue;
-    if (worker >= c.nfb) continue;
-    for (int i = threadIdx.x; i < kBins; i += kBlock) h[i] = 0u;
-    __syncthreads();
-    const SelView sv = view_of(sel);
-    const Row row{gptr(c.desc[j].grad), c.desc[j].shift, c.n};
-    for (uint32_t blk = worker; blk < c.nfb; blk += G) {
-      const uint64_t vbase = (uint64_t)blk * kCBlk;
+  // Work items are the (device, block) pairs of the group, device-major, taken
+  // grid-stride: every worker has a share of every exact-path device. A
+  // worker's items of one device share its histogram, flushed when the device
+  // changes (all conditions below are uniform over the workgroup).
+  const uint64_t items = (uint64_t)c.jn * c.nfb;
+  uint32_t cur = kNoDevice;
+  SelView sv{};
+  Row row{};
+  for (uint64_t it = worker; it < items; it += G) {
+    const uint32_t jr = (uint32_t)(it / c.nfb), blk = (uint32_t)(it - (uint64_t)jr * c.nfb);
+    const uint32_t j = c.j0 + jr;
+    if (j != cur) {
+      if (cur != kNoDevice) {
+        __syncthreads();
+        flush_hist(h, c.hist + ((uint64_t)cur * kSlots + kSlotFull) * kBins, kBins);
+        cur = kNoDevice;
+      }
+      const DevState& s = c.st[j];
+      if (!s.fallback || !s.sel[kSlotFull].active) continue;
+      __syncthreads();
+      for (int i = threadIdx.x; i < kBins; i += kBlock) h[i] = 0u;
+      __syncthreads();
+      cur = j;
+      sv = view_of(s.sel[kSlotFull]);
+      row = Row{gptr(c.desc[j].grad), c.desc[j].shift, c.n};
+    }
+    const uint64_t vbase = (uint64_t)blk * kCBlk;
 #pragma unroll 4
-      for (int r = 0; r < kCBlkRounds; ++r) {
-        const uint64_t v = vbase + (uint64_t)r * kRound + threadIdx.x * 4;
-        const f4 x = load4(row, v, true);
+    for (int r = 0; r < kCBlkRounds; ++r) {
+      const uint64_t v = vbase + (uint64_t)r * kRound + threadIdx.x * 4;
+      const f4 x = load4(row, v, true);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          uint32_t dg;
-          if (in_row(row, v + q) && sel_digit(sv, key_of(x[q]), dg)) atomicAdd(&h[dg], 1u);
-        }
+      for (int q = 0; q < 4; ++q) {
+        uint32_t dg;
+        if (in_row(row, v + q) && sel_digit(sv, key_of(x[q]), dg)) atomicAdd(&h[dg], 1u);
       }
     }
+  }
+  if (cur != kNoDevice) {
     __syncthreads();
-    flush_hist(h, c.hist + ((uint64_t)j * kSlots + kSlotFull) * kBins, kBins);
-    __syncthreads();
+    flush_hist(h, c.hist + ((uint64_t)cur * kSlots + kSlotFull) * kBins, kBins);
   }
 }
 
@@ -1146,17 +1163,19 @@ __device__ inline void count_cf_body(const Ctx& c, uint32_t worker, uint32_t wor
 {
   __shared__ uint32_t lds[8];
   if (*c.fb_count == 0u) return;
-  for (uint32_t j = c.j0; j < c.j0 + c.jn; ++j) {
+  // (device, block) items of the group, grid-stride (see k_hist_cf)
+  const uint64_t items = (uint64_t)c.jn * c.nfb;
+  for (uint64_t it = worker; it < items; it += workers) {
+    const uint32_t jr = (uint32_t)(it / c.nfb), blk = (uint32_t)(it - (uint64_t)jr * c.nfb);
+    const uint32_t j = c.j0 + jr;
     const DevState& s = c.st[j];
     if (!s.fallback) continue;
     uint32_t thr;
     uint64_t need;
     threshold_of(s, thr, need);
     const Row row{gptr(c.desc[j].grad), c.desc[j].shift, c.n};
-    for (uint32_t blk = worker; blk < c.nfb; blk += workers) {
-      const uint64_t r = block_gt_eq<kCBlkRounds>(row, (uint64_t)blk * kCBlk, thr, lds);
-      if (threadIdx.x == 0) c.blk_cnt[(uint64_t)j * c.nbmax + blk] = r;
-    }
+    const uint64_t r = block_gt_eq<kCBlkRounds>(row, (uint64_t)blk * kCBlk, thr, lds);
+    if (threadIdx.x == 0) c.blk_cnt[(uint64_t)j * c.nbmax + blk] = r;
   }
 }
 
@@ -1274,7 +1293,11 @@ __device__ inline void write_cf_body(const Ctx& c, uint32_t worker, uint32_t wor
   __shared__ uint32_t lds[8];
   __shared__ double s_e[4];
   if (*c.fb_count == 0u) return;
-  for (uint32_t j = c.j0; j < c.j0 + c.jn; ++j) {
+  // (device, block) items of the group, grid-stride (see k_hist_cf)
+  const uint64_t items = (uint64_t)c.jn * c.nfb;
+  for (uint64_t it = worker; it < items; it += workers) {
+    const uint32_t jr = (uint32_t)(it / c.nfb), blk = (uint32_t)(it - (uint64_t)jr * c.nfb);
+    const uint32_t j = c.j0 + jr;
     const DevState& s = c.st[j];
     if (!s.fallback) continue;
     uint32_t thr;
@@ -1282,14 +1305,12 @@ __device__ inline void write_cf_body(const Ctx& c, uint32_t worker, uint32_t wor
     threshold_of(s, thr, need);
     const DevDesc d = c.desc[j];
     const Row row{gptr(d.grad), d.shift, c.n};
-    for (uint32_t blk = worker; blk < c.nfb; blk += workers) {
-      const double e2 = block_write<kCBlkRounds>(row, (uint64_t)blk * kCBlk, c.idx_base, thr, need,
-                                                 c.blk_pre[(uint64_t)j * c.nbmax + blk], d.k, gptr(d.idx_out),
-                                                 gptr(d.val_out), lds);
-      const double es = block_sum_f64(e2, s_e);
-      if (threadIdx.x == 0) c.blk_e[(uint64_t)j * c.nbmax + blk] = es;
-      __syncthreads();
-    }
+    const double e2 = block_write<kCBlkRounds>(row, (uint64_t)blk * kCBlk, c.idx_base, thr, need,
+                                               c.blk_pre[(uint64_t)j * c.nbmax + blk], d.k, gptr(d.idx_out),
+                                               gptr(d.val_out), lds);
+    const double es = block_sum_f64(e2, s_e);
+    if (threadIdx.x == 0) c.blk_e[(uint64_t)j * c.nbmax + blk] = es;
+    __syncthreads();
   }
 }
 
