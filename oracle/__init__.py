@@ -60,6 +60,9 @@ def _load():
         lib.oracle_topk_layers.restype = ctypes.c_int
         lib.oracle_topk_layers.argtypes = [_f32p, _u64p, ctypes.c_uint32, ctypes.c_double, _u32p, _f32p,
                                            _f64p, _f64p, _u64p]
+        lib.oracle_stream_run.restype = ctypes.c_int
+        lib.oracle_stream_run.argtypes = [ctypes.c_uint32, _u64p, _u64p, ctypes.c_uint64, ctypes.c_uint64,
+                                          ctypes.c_int, ctypes.c_uint64, _u64p, _u64p, _u64p]
         lib.oracle_compress_decision.restype = ctypes.c_int
         lib.oracle_compress_decision.argtypes = [ctypes.c_double, ctypes.c_double,
                                                  ctypes.c_double, _f64p]
@@ -293,3 +296,27 @@ def stream_weights(rates, b_min: float = 0.0, b_max: float = float("inf"),
     if rc != 0:
         raise ValueError("oracle_stream_weights rejected its input")
     return w, gamma.value
+
+
+PERSISTENCE, TRUNCATION = 0, 1
+
+
+def stream_run(rates, iter_us, b_min: int, b_max: int, policy: int, T: int):
+    """Streaming buffers of K devices over T iterations (§III-A Eqn 2, §IV buffer
+    policies and batch rule). ``rates``: samples/s per device, ``iter_us``:
+    iteration time per device in microseconds (integers). Returns (queued
+    uint64[T+1, K], batch uint64[T, K], dropped uint64[K])."""
+    r = np.ascontiguousarray(rates, dtype=np.uint64)
+    t = np.ascontiguousarray(iter_us, dtype=np.uint64)
+    K = r.size
+    if t.size != K:
+        raise ValueError("one iteration time per device")
+    queued = np.empty((T + 1, K), dtype=np.uint64)
+    batch = np.empty((max(T, 1), K), dtype=np.uint64)
+    dropped = np.empty(K, dtype=np.uint64)
+    rc = _load().oracle_stream_run(K, _ptr(r, ctypes.c_uint64), _ptr(t, ctypes.c_uint64), int(b_min), int(b_max),
+                                   int(policy), int(T), _ptr(queued, ctypes.c_uint64), _ptr(batch, ctypes.c_uint64),
+                                   _ptr(dropped, ctypes.c_uint64))
+    if rc != 0:
+        raise ValueError("oracle_stream_run rejected its input")
+    return queued, batch[:T], dropped

@@ -266,3 +266,53 @@ int oracle_stream_weights(const double* rates, uint32_t K, double b_min, double 
   free(b);
   return 0;
 }
+
+/* Streaming buffers of K devices over T training iterations (§III-A, Eqn 2;
+ * §IV "Limited memory and storage": the persistence and truncation policies;
+ * §IV "Heterogeneous streams": the batch rule b = S bounded to [b_min, b_max]).
+ * Device j streams rate[j] samples per second; one iteration lasts iter_us[j]
+ * microseconds. Iteration 0 starts with one second of arrivals in the buffer
+ * (rate[j] samples; Eqn 2 at T = 0). Every iteration, in this order:
+ *   1. the device trains on min(b_j, queued) samples, the oldest ones;
+ *   2. the samples that arrived during the iteration are added: the count of
+ *      arrivals up to the end of iteration T is floor(rate * iter_us * T / 10^6)
+ *      (a continuous stream), the difference of two such counts per iteration;
+ *   3. persistence keeps every sample; truncation discards the residual of
+ *      step 1 and keeps at most rate[j] of the new arrivals (the newest ones).
+ * queued[(T'+1) x K]: buffer occupancy before iteration T' (row 0) and after
+ * the last one (row T); batch[T x K]: samples trained on; dropped[K]: samples
+ * discarded by truncation over the run. Any output may be NULL.
+ * policy 0 = persistence, 1 = truncation. Returns 0, or -1 on bad input.  */
+int oracle_stream_run(uint32_t K, const uint64_t* rate, const uint64_t* iter_us, uint64_t b_min, uint64_t b_max,
+                      int policy, uint64_t T, uint64_t* queued, uint64_t* batch, uint64_t* dropped)
+{
+  if (K == 0 || !rate || !iter_us || b_min > b_max || (policy != 0 && policy != 1)) return -1;
+  for (uint32_t j = 0; j < K; ++j) {
+    if (rate[j] > 0xFFFFFFFFull || iter_us[j] > 0xFFFFFFFFull) return -1;
+    uint64_t b = rate[j];
+    if (b < b_min) b = b_min;
+    if (b > b_max) b = b_max;
+    uint64_t q = rate[j];
+    uint64_t lost = 0;
+    if (queued) queued[j] = q;
+    for (uint64_t t = 0; t < T; ++t) {
+      uint64_t used = b < q ? b : q;
+      q -= used;
+      if (batch) batch[t * K + j] = used;
+      /* arrivals during iteration t, from the cumulative count of a continuous stream */
+      unsigned __int128 before = (unsigned __int128)rate[j] * iter_us[j] * t / 1000000u;
+      unsigned __int128 after = (unsigned __int128)rate[j] * iter_us[j] * (t + 1) / 1000000u;
+      uint64_t arrived = (uint64_t)(after - before);
+      if (policy == 0) {
+        q += arrived;
+      } else {
+        lost += q;
+        q = arrived < rate[j] ? arrived : rate[j];
+        lost += arrived - q;
+      }
+      if (queued) queued[(t + 1) * K + j] = q;
+    }
+    if (dropped) dropped[j] = lost;
+  }
+  return 0;
+}
