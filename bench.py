@@ -150,6 +150,12 @@ def main():
                     help="Top-k over each flat gradient (default), or per layer of the workload's layer "
                          "layout (each layer keeps its own top fraction; three library calls per step: "
                          "per-layer selection, Eqn 4b aggregation, Eqn 4c SGD)")
+    ap.add_argument("--stream", choices=("none", "persistence", "truncation"), default="none",
+                    help="take every step's weights and learning rate from the devices' stream buffers "
+                         "under this policy (host, inside the timed step): the workload's rates as samples/s, "
+                         "iterations of --iter-s seconds, batches bounded to [8, 1024]")
+    ap.add_argument("--iter-s", type=float, default=1.6,
+                    help="simulated iteration time of --stream (default 1.6 s, the paper's VGG19 iteration)")
     ap.add_argument("--calibrate", action="store_true",
                     help="first run one 1 GiB device-to-device copy (a plain copy kernel of known size "
                          "for scaling HBM byte counters)")
@@ -209,12 +215,25 @@ def main():
         step.run(weights[it], lrs[it])
     torch.cuda.synchronize()
 
+    buffers, host_s = None, 0.0
+    if args.stream != "none":
+        buffers = sc.StreamBuffers(np.rint(s.rates[0]).astype(np.uint64), b_min=8, b_max=1024, policy=args.stream,
+                                   base_batch=s.base_batch)
+        iter_us = int(round(args.iter_s * 1e6))
+
     sc.profile_enable(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         it = i % s.iterations
-        step.run(weights[it], lrs[it])
+        if buffers is not None:
+            h0 = time.perf_counter()
+            _, w, gamma = buffers.iteration(iter_us)
+            lr = float(np.float32(s.eta * gamma))
+            host_s += time.perf_counter() - h0
+            step.run(w, lr)
+        else:
+            step.run(weights[it], lrs[it])
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     stages, calls = sc.profile_read()
@@ -257,6 +276,17 @@ def main():
                           "note": "select+compact+aggregate(+SGD) stages, algorithmic bytes "
                                   "4Kn + 8*sum(k) + 4n over their summed event time"},
     }
+    if buffers is not None:
+        out["config"]["stream"] = {"policy": args.stream, "iteration_s": args.iter_s, "b_min": 8, "b_max": 1024}
+        out["stream"] = {"host_us_per_iteration": host_s * 1e6 / args.steps,
+                         "queued_samples_after": int(buffers.field("queued").sum()),
+                         "dropped_samples": int(buffers.field("dropped").sum())}
+        # the buffer simulation alone: all devices over 10^5 iterations (after one untimed run)
+        sim = (np.rint(s.rates[0]).astype(np.uint64), [iter_us] * s.K, 8, 1024, args.stream, 100_000)
+        sc.stream_simulate(*sim)
+        h0 = time.perf_counter()
+        sc.stream_simulate(*sim)
+        out["stream"]["simulate_ns_per_device_iteration"] = (time.perf_counter() - h0) * 1e9 / (s.K * 100_000)
     if args.stages:
         out["stage_ms"] = {k: v / max(calls, 1) for k, v in stages.items()}
     if not args.no_cpu_baseline:

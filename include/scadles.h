@@ -250,6 +250,59 @@ scadles_status scadles_stream_weights(const double* rates, uint32_t K, double b_
                                       double b_max, double base_batch, float* weights,
                                       double* gamma);
 
+/* ---- streaming buffers, batch sizes, weights and learning-rate scale --------
+ * The step before the aggregation (§III-A, Eqns 2 and 3; §IV "Heterogeneous
+ * streams" and "Limited memory and storage"): device j receives a continuous
+ * stream of S_j samples per second into its buffer and trains one iteration
+ * of t_j seconds on a batch of b_j = clamp(S_j, b_min, b_max) samples, or on
+ * all it holds when that is fewer. After an iteration the samples that
+ * arrived meanwhile join the buffer. Stream persistence keeps every sample;
+ * stream truncation discards the residual the iteration left and keeps at
+ * most S_j of the new arrivals (the newest), so its buffer stays O(S_j)
+ * while persistence grows as (t_j S_j - b_j) T + S_j after T iterations
+ * (Eqn 2). A continuous stream has delivered floor(S_j * us / 10^6) samples
+ * after `us` microseconds; a buffer starts with one second of it (S_j).
+ * Host-only: none of these calls touches GPU state.                         */
+#define SCADLES_PERSISTENCE 0
+#define SCADLES_TRUNCATION 1
+
+/* One device's stream buffer. */
+typedef struct scadles_stream {
+  uint64_t rate;        /* S_j, samples per second, < 2^32                      */
+  uint64_t elapsed_us;  /* stream time covered by the iterations so far         */
+  uint64_t queued;      /* samples in the buffer                                */
+  uint64_t trained;     /* samples trained on so far                            */
+  uint64_t dropped;     /* samples discarded by truncation so far               */
+} scadles_stream;
+
+/* Sets st[j] to a fresh buffer of stream rate rate[j] (queued = rate[j]).
+ *   rate (host[K]) < 2^32; st (host[K]).                                    */
+scadles_status scadles_stream_init(uint32_t K, const uint64_t* rate, scadles_stream* st);
+
+/* One training iteration of K devices: every device takes its batch from its
+ * buffer (batch[j] = min(clamp(S_j, b_min, b_max), queued)), the weights and
+ * learning-rate scale of that iteration follow from the batches as in
+ * scadles_stream_weights (r_j = batch_j / sum batch, Eqn 4a; gamma = sum
+ * batch / base_batch), then the arrivals of iter_us[j] microseconds join the
+ * buffer under `policy`.
+ *   st       (host[K], in/out) from scadles_stream_init.
+ *   iter_us  (host[K]) this iteration's duration per device, < 2^32.
+ *   b_min <= b_max (UINT64_MAX: no upper bound). policy: SCADLES_PERSISTENCE
+ *   or SCADLES_TRUNCATION. base_batch > 0 when gamma is not NULL.
+ *   batch (host[K]) or NULL; weights (host[K]) or NULL; gamma or NULL.
+ * When no device holds a sample, weights are all 0 and gamma is 0 (there is
+ * nothing to aggregate). Errors leave st unchanged.                        */
+scadles_status scadles_stream_iteration(uint32_t K, scadles_stream* st, const uint64_t* iter_us, uint64_t b_min,
+                                        uint64_t b_max, int policy, double base_batch, uint64_t* batch,
+                                        float* weights, double* gamma);
+
+/* T iterations of constant duration iter_us[j] from fresh buffers.
+ *   queued (host[(T+1) x K]) or NULL: row t = buffer before iteration t, row T
+ *   after the last; batch (host[T x K]) or NULL; dropped (host[K]) or NULL.   */
+scadles_status scadles_stream_simulate(uint32_t K, const uint64_t* rate, const uint64_t* iter_us, uint64_t b_min,
+                                       uint64_t b_max, int policy, uint64_t T, uint64_t* queued, uint64_t* batch,
+                                       uint64_t* dropped);
+
 /* Message for the last non-OK status returned on the calling thread.        */
 const char* scadles_last_error(void);
 

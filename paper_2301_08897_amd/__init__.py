@@ -49,6 +49,11 @@ class StepOptions(ctypes.Structure):
                 ("ewma", _vp), ("ewma_beta", ctypes.c_double), ("counters", _vp)]
 
 
+class Stream(ctypes.Structure):
+    """scadles_stream: one device's stream buffer."""
+    _fields_ = [("rate", _u64), ("elapsed_us", _u64), ("queued", _u64), ("trained", _u64), ("dropped", _u64)]
+
+
 def _sig(name, restype, *argtypes):
     f = getattr(_lib, name)
     f.restype = restype
@@ -83,6 +88,12 @@ _step_fused_ex = _sig("scadles_step_fused_ex", ctypes.c_int, ctypes.POINTER(_vp)
 _stream_weights = _sig("scadles_stream_weights", ctypes.c_int, ctypes.POINTER(ctypes.c_double), _u32,
                        ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_float),
                        ctypes.POINTER(ctypes.c_double))
+_stream_init = _sig("scadles_stream_init", ctypes.c_int, _u32, ctypes.POINTER(_u64), ctypes.POINTER(Stream))
+_stream_iteration = _sig("scadles_stream_iteration", ctypes.c_int, _u32, ctypes.POINTER(Stream), ctypes.POINTER(_u64),
+                         _u64, _u64, ctypes.c_int, ctypes.c_double, ctypes.POINTER(_u64),
+                         ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double))
+_stream_simulate = _sig("scadles_stream_simulate", ctypes.c_int, _u32, ctypes.POINTER(_u64), ctypes.POINTER(_u64), _u64,
+                        _u64, ctypes.c_int, _u64, ctypes.POINTER(_u64), ctypes.POINTER(_u64), ctypes.POINTER(_u64))
 _last_error = _sig("scadles_last_error", ctypes.c_char_p)
 _set_option = _sig("scadles_set_option", ctypes.c_int, ctypes.c_char_p, ctypes.c_int64)
 _profile_enable = _sig("scadles_profile_enable", ctypes.c_int, ctypes.c_int)
@@ -174,6 +185,68 @@ def stream_weights(rates, b_min: float = 0.0, b_max: float = math.inf, base_batc
                            w.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
                            ctypes.byref(g) if base_batch is not None else None))
     return (w, g.value) if base_batch is not None else (w, None)
+
+
+PERSISTENCE, TRUNCATION = 0, 1
+NO_BOUND = 2**64 - 1
+_POLICIES = {"persistence": PERSISTENCE, "truncation": TRUNCATION, PERSISTENCE: PERSISTENCE,
+             TRUNCATION: TRUNCATION}
+
+
+def _u64_array(x, n=None):
+    a = np.ascontiguousarray(x, dtype=np.uint64)
+    if n is not None and a.size != n:
+        raise ValueError(f"expected {n} values")
+    return a
+
+
+def _p64(a):
+    return a.ctypes.data_as(ctypes.POINTER(_u64))
+
+
+class StreamBuffers:
+    """The stream buffers of K devices (persistence or truncation) and, per
+    training iteration, the batch each device trains on with the Eqn 4a
+    weights and learning-rate scale that follow from them. Host only."""
+
+    def __init__(self, rates, *, b_min: int = 0, b_max: int = NO_BOUND, policy="persistence",
+                 base_batch: Optional[float] = None):
+        r = _u64_array(rates)
+        self.K = r.size
+        self.b_min, self.b_max = int(b_min), int(b_max)
+        self.policy = _POLICIES[policy]
+        self.base_batch = base_batch
+        self.state = (Stream * self.K)()
+        _check(_stream_init(self.K, _p64(r), self.state))
+
+    def iteration(self, iter_us):
+        """One iteration of iter_us microseconds per device (scalar or per device).
+        Returns (batch uint64[K], weights float32[K], gamma or None)."""
+        t = _u64_array(np.broadcast_to(np.asarray(iter_us, dtype=np.uint64), (self.K,)), self.K)
+        batch = np.empty(self.K, dtype=np.uint64)
+        w = np.empty(self.K, dtype=np.float32)
+        g = ctypes.c_double()
+        _check(_stream_iteration(self.K, self.state, _p64(t), self.b_min, self.b_max, self.policy,
+                                 float(self.base_batch) if self.base_batch is not None else 0.0, _p64(batch),
+                                 w.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                                 ctypes.byref(g) if self.base_batch is not None else None))
+        return batch, w, (g.value if self.base_batch is not None else None)
+
+    def field(self, name: str) -> np.ndarray:
+        return np.array([getattr(s, name) for s in self.state], dtype=np.uint64)
+
+
+def stream_simulate(rates, iter_us, b_min: int, b_max: int, policy, T: int):
+    """T iterations from fresh buffers: (queued uint64[T+1, K], batch uint64[T, K], dropped uint64[K])."""
+    r = _u64_array(rates)
+    K = r.size
+    t = _u64_array(iter_us, K)
+    queued = np.empty((T + 1, K), dtype=np.uint64)
+    batch = np.empty((max(T, 1), K), dtype=np.uint64)
+    dropped = np.empty(K, dtype=np.uint64)
+    _check(_stream_simulate(K, _p64(r), _p64(t), int(b_min), int(b_max), _POLICIES[policy], int(T), _p64(queued),
+                            _p64(batch), _p64(dropped)))
+    return queued, batch[:T], dropped
 
 
 def set_option(name: str, value: int):

@@ -17,10 +17,9 @@
 
 using namespace scadles;
 
-namespace {
+namespace scadles {
 
 thread_local std::string g_err;
-std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0}, g_parts{2};
 
 scadles_status fail(scadles_status st, const char* fmt, ...)
 {
@@ -32,6 +31,12 @@ scadles_status fail(scadles_status st, const char* fmt, ...)
   g_err = buf;
   return st;
 }
+
+}  // namespace scadles
+
+namespace {
+
+std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0}, g_parts{2};
 
 scadles_status hip_fail(hipError_t e, const char* where)
 {

@@ -1,0 +1,108 @@
+"""The library's streaming buffers, batch sizes, weights and learning-rate
+scale (§III-A Eqns 2-3, §IV) against the oracle: host-only code, so these run
+without a GPU. Integers bit for bit; weights bit for bit against the oracle's
+Eqn 4a on the same batches."""
+import math
+
+import numpy as np
+import pytest
+
+
+@pytest.fixture(scope="module")
+def sc():
+    import paper_2301_08897_amd as sc
+    return sc
+
+
+@pytest.mark.parametrize("seed", range(20))
+@pytest.mark.parametrize("policy", [0, 1])
+def test_simulate_matches_oracle(sc, orc, seed, policy):
+    rng = np.random.default_rng(100 + seed)
+    K = int(rng.integers(1, 65))
+    rates = rng.integers(0, 5000, K)
+    iter_us = rng.integers(0, 5_000_000, K)
+    b_min, b_max = sorted(int(x) for x in rng.integers(0, 2000, 2))
+    T = int(rng.integers(0, 300))
+    got = sc.stream_simulate(rates, iter_us, b_min, b_max, policy, T)
+    want = orc.stream_run(rates, iter_us, b_min, b_max, policy, T)
+    for g, w in zip(got, want):
+        assert np.array_equal(g, w)
+
+
+def test_paper_sized_runs(sc, orc):
+    # the iteration times and rates of Table II, 10^5 iterations, both policies
+    rates = [100, 600, 100, 600]
+    iter_us = [1_200_000, 1_200_000, 1_600_000, 1_600_000]
+    for policy in (0, 1):
+        got = sc.stream_simulate(rates, iter_us, 8, 1024, policy, 100_000)
+        want = orc.stream_run(rates, iter_us, 8, 1024, policy, 100_000)
+        for g, w in zip(got, want):
+            assert np.array_equal(g, w)
+
+
+@pytest.mark.parametrize("policy", ["persistence", "truncation"])
+def test_iterations_match_simulation_and_weights(sc, orc, policy):
+    rng = np.random.default_rng(7)
+    K, T = 32, 200
+    rates = rng.integers(1, 3000, K)
+    iter_us = rng.integers(100_000, 3_000_000, K)
+    q_o, b_o, d_o = orc.stream_run(rates, iter_us, 8, 1024, 0 if policy == "persistence" else 1, T)
+    buf = sc.StreamBuffers(rates, b_min=8, b_max=1024, policy=policy, base_batch=64.0 * K)
+    for t in range(T):
+        assert np.array_equal(buf.field("queued"), q_o[t])
+        batch, w, gamma = buf.iteration(iter_us)
+        assert np.array_equal(batch, b_o[t])
+        w_o, g_o = orc.stream_weights(b_o[t].astype(np.float64), base_batch=64.0 * K)
+        assert np.array_equal(w.view(np.uint32), w_o.view(np.uint32))
+        assert gamma == g_o
+    assert np.array_equal(buf.field("queued"), q_o[T])
+    assert np.array_equal(buf.field("dropped"), d_o)
+    assert np.array_equal(buf.field("trained"), b_o.sum(axis=0))
+
+
+def test_varying_iteration_times(sc):
+    # iteration times that change every iteration: the arrivals are those of a
+    # continuous stream over the summed time, whatever the split
+    rng = np.random.default_rng(8)
+    K, T = 5, 400
+    rates = rng.integers(1, 2000, K)
+    buf = sc.StreamBuffers(rates, b_min=8, b_max=1024, policy="persistence")
+    elapsed = np.zeros(K, dtype=np.int64)
+    q = rates.astype(np.int64).copy()
+    for _ in range(T):
+        t = rng.integers(0, 4_000_000, K)
+        batch, _, _ = buf.iteration(t)
+        b = np.minimum(np.clip(rates, 8, 1024), q)
+        assert np.array_equal(batch, b.astype(np.uint64))
+        q = q - b + (rates * (elapsed + t)) // 1_000_000 - (rates * elapsed) // 1_000_000
+        elapsed += t
+        assert np.array_equal(buf.field("queued"), q.astype(np.uint64))
+    assert np.array_equal(buf.field("elapsed_us"), elapsed.astype(np.uint64))
+
+
+def test_no_samples_gives_zero_weights(sc):
+    buf = sc.StreamBuffers([0, 0, 0], policy="truncation", base_batch=10.0)
+    batch, w, gamma = buf.iteration(1_000_000)
+    assert batch.tolist() == [0, 0, 0] and w.tolist() == [0.0, 0.0, 0.0] and gamma == 0.0
+
+
+def test_validation(sc):
+    with pytest.raises(sc.ScadlesError):
+        sc.stream_simulate([10], [10], 5, 4, 0, 3)
+    with pytest.raises(sc.ScadlesError):
+        sc.stream_simulate([2**32], [10], 0, 4, 0, 3)
+    with pytest.raises(sc.ScadlesError):
+        sc.stream_simulate([10], [2**32], 0, 4, 0, 3)
+    with pytest.raises(KeyError):
+        sc.StreamBuffers([10], policy="keep-half")
+    buf = sc.StreamBuffers([10, 20], base_batch=-1.0)
+    before = buf.field("queued").copy()
+    with pytest.raises(sc.ScadlesError):
+        buf.iteration(1000)
+    assert np.array_equal(buf.field("queued"), before)      # errors leave the buffers unchanged
+    buf = sc.StreamBuffers([10, 20])
+    with pytest.raises(sc.ScadlesError):
+        buf.iteration([1000, 2**32])
+    assert buf.field("queued").tolist() == [10, 20]
+    assert sc._stream_init(0, None, None) == 1
+    assert math.isclose(sc.StreamBuffers([5], base_batch=5.0).iteration(0)[2], 1.0)
