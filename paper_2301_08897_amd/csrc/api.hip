@@ -3,6 +3,7 @@
 // Host side only: argument validation, the k rule, workspace layout, path
 // choice per device, and the launch sequence. Every entry point validates
 // before launching anything and never allocates device memory.
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <cstdarg>
@@ -37,6 +38,8 @@ scadles_status fail(scadles_status st, const char* fmt, ...)
 namespace {
 
 std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0}, g_parts{2};
+// per-layer selection: layers of at most this many elements go to the row kernels
+std::atomic<int64_t> g_row_max{1 << 21};
 
 scadles_status hip_fail(hipError_t e, const char* where)
 {
@@ -423,16 +426,36 @@ uint64_t scadles_layers_k(const uint64_t* seg_off, uint32_t L, double ratio)
   return k;
 }
 
-size_t scadles_layers_workspace_bytes(uint32_t K, const uint64_t* seg_off, uint32_t L, const double* ratios)
+// Workspace of a per-layer selection: the selection region (the largest
+// layer's, for layers selected by the multi-launch path) and after it the
+// row region (layer table, row descriptors, per-row energies).
+struct LayersWs {
+  size_t sel = 0, table = 0, rows = 0, row_e = 0, total = 0;
+};
+
+static LayersWs layers_ws(uint32_t K, const uint64_t* seg_off, uint32_t L, const double* ratios)
 {
-  if (K == 0 || K > kMaxK || !ratios || scadles_layers_k(seg_off, L, 0.5) == 0) return 0;
+  LayersWs w;
   size_t most = 0;
   for (uint32_t l = 0; l < L; ++l) {
     const size_t b = scadles_workspace_bytes(K, seg_off[l + 1] - seg_off[l], ratios);
-    if (b == 0) return 0;
+    if (b == 0) return LayersWs{};
     if (b > most) most = b;
   }
-  return most;
+  w.sel = align256(most);
+  w.table = w.sel;
+  w.rows = align256(w.table + sizeof(uint64_t) * (2ull * L + 1));
+  w.row_e = align256(w.rows + sizeof(RowDesc) * (size_t)K * L);
+  w.total = align256(w.row_e + sizeof(double) * 2ull * K * L);
+  return w;
+}
+
+size_t scadles_layers_workspace_bytes(uint32_t K, const uint64_t* seg_off, uint32_t L, const double* ratios)
+{
+  if (K == 0 || K > kMaxK || !ratios || scadles_layers_k(seg_off, L, 0.5) == 0) return 0;
+  for (uint32_t j = 0; j < K; ++j)
+    if (scadles_layers_k(seg_off, L, ratios[j]) == 0) return 0;
+  return layers_ws(K, seg_off, L, ratios).total;
 }
 
 scadles_status scadles_topk_select_layers(const float* const* grads, uint32_t K, const uint64_t* seg_off, uint32_t L,
@@ -450,12 +473,54 @@ scadles_status scadles_topk_select_layers(const float* const* grads, uint32_t K,
     if (scadles_layers_k(seg_off, L, ratios[j]) == 0)
       return fail(SCADLES_EINVAL, "ratio %g of device %u is not in (0, 1]", ratios[j], j);
   }
-  const size_t need = scadles_layers_workspace_bytes(K, seg_off, L, ratios);
-  if (scadles_status st = check_ws(ws, ws_bytes, need)) return st;
+  const LayersWs lw = layers_ws(K, seg_off, L, ratios);
+  if (scadles_status st = check_ws(ws, ws_bytes, lw.total)) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  uint64_t at[kMaxK] = {};          // entries written so far per device
+  uint8_t* base = static_cast<uint8_t*>(ws);
+
+  // Short layers (at most row_max elements), longest first, go to the row
+  // kernels: one workgroup per (layer, device) row, all in one launch.
+  const uint64_t row_max = (uint64_t)g_row_max.load();
+  std::vector<uint32_t> shorts;
+  for (uint32_t l = 0; l < L; ++l)
+    if (seg_off[l + 1] - seg_off[l] <= row_max) shorts.push_back(l);
+  std::stable_sort(shorts.begin(), shorts.end(), [&](uint32_t a, uint32_t b) {
+    return seg_off[a + 1] - seg_off[a] > seg_off[b + 1] - seg_off[b];
+  });
+  std::vector<uint64_t> table(2ull * L + 1, ~0ull);
+  for (uint32_t l = 0; l <= L; ++l) table[l] = seg_off[l];
+  for (size_t q = 0; q < shorts.size(); ++q) table[L + 1 + shorts[q]] = q;
+  hipError_t e = launch_put_table(table.data(), table.size(), reinterpret_cast<uint64_t*>(base + lw.table), s);
+  if (e != hipSuccess) return hip_fail(e, "layer table");
+  RowsCtx rc;
+  rc.table = reinterpret_cast<const uint64_t*>(base + lw.table);
+  rc.rows = reinterpret_cast<RowDesc*>(base + lw.rows);
+  rc.row_e = reinterpret_cast<double*>(base + lw.row_e);
+  rc.K = K;
+  rc.L = L;
+  rc.Ls = (uint32_t)shorts.size();
+  RowsPrep rp;
+  memset(&rp, 0, sizeof(rp));
+  for (uint32_t j = 0; j < K; ++j) {
+    rp.grad[j] = grads[j];
+    rp.idx[j] = idx[j];
+    rp.val[j] = val[j];
+    rp.ratio[j] = ratios[j];
+  }
+  e = launch_rows(rc, rp, energies, s);
+  if (e != hipSuccess) return hip_fail(e, "row selection");
+
+  // Longer layers: the multi-launch selection, one layer after the other, its
+  // indices offset by the layer's start and its energies added to those of the
+  // layers before.
+  uint64_t at[kMaxK] = {};          // where layer l's entries start in device j's output
+  bool first = rc.Ls == 0;
   for (uint32_t l = 0; l < L; ++l) {
     const uint64_t off = seg_off[l], nl = seg_off[l + 1] - off;
+    if (nl <= row_max) {
+      for (uint32_t j = 0; j < K; ++j) at[j] += k_rule(nl, ratios[j]);
+      continue;
+    }
     Layout Ll;
     make_layout(K, nl, ratios, g_force_exact.load() != 0, true, Ll);
     PrepArgs a;
@@ -471,11 +536,10 @@ scadles_status scadles_topk_select_layers(const float* const* grads, uint32_t K,
       a.r_hi[j] = Ll.r_hi[j];
       at[j] += Ll.k[j];
     }
-    // each layer on its own, its indices offset by the layer's start; the
-    // energies of later layers are added to the first's
     if (scadles_status st = run_select(Ll, a, ws, INFINITY, energies, nullptr, s, nullptr, nullptr, nullptr,
-                                       (uint32_t)off, l > 0))
+                                       (uint32_t)off, !first))
       return st;
+    first = false;
   }
   return SCADLES_OK;
 }
@@ -711,6 +775,10 @@ scadles_status scadles_set_option(const char* name, int64_t value)
   if (!strcmp(name, "validate")) g_validate = value ? 1 : 0;
   else if (!strcmp(name, "force_exact")) g_force_exact = value ? 1 : 0;
   else if (!strcmp(name, "force_fallback")) g_force_fallback = value ? 1 : 0;
+  else if (!strcmp(name, "row_max")) {
+    if (value < 0 || value > 0xFFFFFFFFll) return fail(SCADLES_EINVAL, "row_max must be in [0, 2^32 - 1]");
+    g_row_max = value;
+  }
   else if (!strcmp(name, "parts")) {
     if (value < 1 || value > (int64_t)kMaxParts) return fail(SCADLES_EINVAL, "parts must be in [1, %u]", kMaxParts);
     g_parts = (int)value;

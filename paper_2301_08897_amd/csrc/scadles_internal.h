@@ -197,6 +197,51 @@ __device__ inline void momentum_step(float& p, float& v, float g, double nlr, do
   p = (float)__builtin_fma(nlr, (double)v, (double)p);
 }
 
+// ---- per-layer selection of short layers: one workgroup per (device, layer) row ------
+// Layers of at most RowsCtx::row_max elements are selected by k_rows, one
+// workgroup of kRowBlock threads per row, instead of running the multi-launch
+// selection once per layer.
+constexpr int kRowBlock = 1024;
+constexpr int kRowCand = 14336;        // keys of the threshold bin held in LDS
+constexpr int kPutWords = 240;         // table words per k_put launch (kernel-argument copy)
+
+struct RowDesc {
+  const float* grad;     // the layer's first element
+  uint32_t* idx_out;     // the row's first output
+  float* val_out;
+  uint32_t n, k;
+  uint32_t base;         // index of the layer's first element in the whole gradient
+  uint32_t eslot;        // j * L + l: where the row's energies go
+};
+
+struct RowsPrep {
+  const float* grad[kMaxK];
+  uint32_t* idx[kMaxK];
+  float* val[kMaxK];
+  double ratio[kMaxK];
+};
+
+struct RowsCtx {
+  const uint64_t* table;  // seg_off[0..L], then per layer its position among the short layers (or ~0)
+  RowDesc* rows;          // [Ls x K]: row q * K + j is device j's q-th short layer (longest first)
+  double* row_e;          // [K x L x 2]: E_all, E_kept of device j's layer l (short layers)
+  uint32_t K, L, Ls;
+};
+
+hipError_t launch_put_table(const uint64_t* src, uint64_t count, uint64_t* dst, hipStream_t s);
+hipError_t launch_rows(const RowsCtx& rc, const RowsPrep& rp, double* energies, hipStream_t s);
+
+// k = clamp(floor(ratio * n), 1, n), the same double arithmetic on host and device.
+__host__ __device__ inline uint64_t k_of(uint64_t n, double ratio)
+{
+  if (n == 0) return 0;
+  const double f = __builtin_floor(ratio * (double)n);
+  uint64_t k = (uint64_t)f;
+  if (k < 1) k = 1;
+  if (k > n) k = n;
+  return k;
+}
+
 // ---- sizing shared by host and device -----------------------------------------------------
 __host__ __device__ inline uint32_t bitlen32(uint32_t x) { return x ? 32u - (uint32_t)__builtin_clz(x) : 0u; }
 

@@ -14,6 +14,11 @@ from _gpu_common import energy_tol, log, same_bits, torch_dev
 pytestmark = pytest.mark.gpu
 
 MODES = ("default", "force_exact", "force_fallback")
+# Layers of at most row_max elements are selected by one workgroup per
+# (device, layer) row; longer ones by the multi-launch selection. 0 sends every
+# layer to the multi-launch selection, 2^32 - 1 every layer to the rows.
+ROW_MAX_DEFAULT = 1 << 21
+ROW_MAXES = (ROW_MAX_DEFAULT, 0, 2**32 - 1)
 
 
 @pytest.fixture(scope="module")
@@ -25,7 +30,7 @@ def sc():
 
 
 def layers_vs_oracle(sc, G: np.ndarray, seg_off, ratios, label, modes=("default",), topk=None,
-                     check_aggregate=False):
+                     check_aggregate=False, row_maxes=ROW_MAXES):
     """Run the per-layer selection of every device of G (K x n) and compare it
     with the oracle; returns the oracle's per-device results."""
     torch, dev = torch_dev()
@@ -33,9 +38,11 @@ def layers_vs_oracle(sc, G: np.ndarray, seg_off, ratios, label, modes=("default"
     fn = topk or oracle.topk_layers
     ref = [fn(G[j], seg_off, ratios[j]) for j in range(K)]
     g_dev = torch.from_numpy(G).to(dev)
-    for mode in modes:
+    runs = [(m, ROW_MAX_DEFAULT) for m in modes] + [("default", r) for r in row_maxes if r != ROW_MAX_DEFAULT]
+    for mode, row_max in runs:
         if mode != "default":
             sc.set_option(mode, 1)
+        sc.set_option("row_max", row_max)
         try:
             sel = sc.LayerSelect(g_dev, seg_off, ratios)
             idx, val, en = sel.run()
@@ -43,6 +50,8 @@ def layers_vs_oracle(sc, G: np.ndarray, seg_off, ratios, label, modes=("default"
         finally:
             if mode != "default":
                 sc.set_option(mode, 0)
+            sc.set_option("row_max", ROW_MAX_DEFAULT)
+        mode = f"{mode}, row_max {row_max}"
         e = en.cpu().numpy()
         for j in range(K):
             idx_o, val_o, ea, ek = ref[j]
@@ -102,6 +111,32 @@ def test_ties_across_layer_bounds(sc):
         layers_vs_oracle(sc, G, seg_off, ratios, f"ties {ratios}", modes=MODES)
 
 
+def test_layers_at_the_row_limit(sc):
+    # one layer just at the row limit (selected by a workgroup, its threshold
+    # bin too large for LDS), one just above it (multi-launch selection), and
+    # a short tail
+    rng = np.random.default_rng(15)
+    sizes = [ROW_MAX_DEFAULT, ROW_MAX_DEFAULT + 1, 3]
+    seg_off = np.concatenate([[0], np.cumsum(sizes)]).tolist()
+    G = rng.standard_normal((2, seg_off[-1])).astype(np.float32)
+    log("layers at the row limit")
+    layers_vs_oracle(sc, G, seg_off, [0.01, 0.3], "row limit", topk=oracle.topk_layers_by_threshold,
+                     row_maxes=(ROW_MAX_DEFAULT,))
+
+
+def test_rows_with_equal_keys(sc):
+    # whole layers of one magnitude (every key tied), of zeros and signed
+    # zeros, and a layer whose keys differ only in the lowest bits
+    n_l = 40_000
+    parts = [np.full(n_l, -1.25, dtype=np.float32), np.zeros(n_l, dtype=np.float32),
+             np.where(np.arange(n_l) % 2 == 0, 0.0, -0.0).astype(np.float32),
+             (np.float32(1.0) + np.arange(n_l, dtype=np.float32) % 7 * np.float32(2.0**-23)).astype(np.float32)]
+    g = np.concatenate(parts)
+    seg_off = [0, n_l, 2 * n_l, 3 * n_l, 4 * n_l]
+    log("layers with equal keys")
+    layers_vs_oracle(sc, np.stack([g, -g]), seg_off, [0.01, 0.5], "equal keys")
+
+
 def test_one_layer_matches_whole_vector(sc):
     torch, dev = torch_dev()
     rng = np.random.default_rng(13)
@@ -113,7 +148,8 @@ def test_one_layer_matches_whole_vector(sc):
     torch.cuda.synchronize()
     assert np.array_equal(idx[0].cpu().numpy(), idx1.cpu().numpy())
     assert same_bits(val[0].cpu().numpy(), val1.cpu().numpy())
-    assert np.array_equal(en.cpu().numpy(), en1.cpu().numpy())
+    e, e1 = en.cpu().numpy(), en1.cpu().numpy()
+    assert np.all(np.abs(e - e1) <= energy_tol(n) * e1[0])
 
 
 def test_repeated_runs_reuse_workspace(sc):
