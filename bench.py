@@ -92,30 +92,26 @@ def cpu_baseline(s, threads):
 
 
 def bench_layers(args, s, sc, torch, G, params, weights, lrs):
-    """The hot path with the per-layer Top-k: per-layer selection of every device
-    (the workload's layer layout), Eqn 4b over the layered sets, Eqn 4c. Timed
-    as whole steps; the roofline entry is the step's algorithmic bytes over its
-    time (no per-kernel events on this path)."""
+    """The hot path with the per-layer Top-k (the workload's layer layout):
+    per-layer selection of every device, Eqn 4b over the layered sets and
+    Eqn 4c, in one library call per step. Timed as whole steps; the roofline
+    entry is the step's algorithmic bytes over its time."""
     seg_off = [0] + [int(x) for x in s.seg_end]
-    sel = sc.LayerSelect(G, seg_off, list(s.ratios[0]))
-    dense = torch.empty(s.n, dtype=torch.float32, device=G.device)
-    agg_ws = torch.empty(max(sc.aggregate_workspace_bytes(s.K, s.n), 256), dtype=torch.uint8, device=G.device)
-
-    def one(it):
-        idx, val, _ = sel.run()
-        sc.weighted_aggregate(list(zip(idx, val)), weights[it], s.n, out=dense, workspace=agg_ws)
-        sc.apply_sgd(params, dense, lrs[it])
-
+    if args.row_max is not None:
+        sc.set_option("row_max", args.row_max)
+    step = sc.FusedStep(G, s.ratios[0], params=params, seg_off=seg_off)
     for i in range(args.warmup):
-        one(i % s.iterations)
+        it = i % s.iterations
+        step.run(weights[it], lrs[it])
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        one(i % s.iterations)
+        it = i % s.iterations
+        step.run(weights[it], lrs[it])
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     ms = dt * 1e3 / args.steps
-    ks = sum(sel.k)
+    ks = sum(step.k)
     alg = 4 * s.K * s.n + 8 * ks + 4 * s.n
     gbps = alg / (ms * 1e-3) / 1e9
     out = {
@@ -156,6 +152,9 @@ def main():
                          "iterations of --iter-s seconds, batches bounded to [8, 1024]")
     ap.add_argument("--iter-s", type=float, default=1.6,
                     help="simulated iteration time of --stream (default 1.6 s, the paper's VGG19 iteration)")
+    ap.add_argument("--row-max", type=int, default=None,
+                    help="with --topk layers: layers of at most this many elements are selected one workgroup "
+                         "per (device, layer) (library option 'row_max')")
     ap.add_argument("--calibrate", action="store_true",
                     help="first run one 1 GiB device-to-device copy (a plain copy kernel of known size "
                          "for scaling HBM byte counters)")

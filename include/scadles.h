@@ -236,6 +236,24 @@ scadles_status scadles_step_fused_ex(const float* const* grads, uint32_t K, uint
                                      const scadles_step_options* options, void* ws, size_t ws_bytes,
                                      void* stream);
 
+/* The fused step with the per-layer Top-k: scadles_topk_select_layers for
+ * every device, the adaptive rule of §IV on each device's whole-gradient
+ * energies (with the moving average and accounting of `options`, which may
+ * be NULL), then Eqn 4b over the layered sets (or the dense gradients of
+ * devices that send g) and the update (Eqn 4c, or momentum SGD when
+ * options->momentum_buf is set), as scadles_step_fused_ex does for the
+ * whole-vector Top-k. idx[j] / val[j] hold scadles_layers_k(seg_off, L,
+ * ratios[j]) entries; dense, params and the options as for
+ * scadles_step_fused_ex; ws is scadles_step_layers_workspace_bytes(...) bytes.
+ * Same error convention as above.                                           */
+size_t scadles_step_layers_workspace_bytes(uint32_t K, const uint64_t* seg_off, uint32_t L, const double* ratios);
+scadles_status scadles_step_fused_layers(const float* const* grads, uint32_t K, const uint64_t* seg_off, uint32_t L,
+                                         const double* ratios, double delta, const float* weights,
+                                         uint32_t* const* idx, float* const* val, float* dense, double* energies,
+                                         uint8_t* compressed, float* params, float lr,
+                                         const scadles_step_options* options, void* ws, size_t ws_bytes,
+                                         void* stream);
+
 /* Aggregation weights and learning-rate scale from streaming rates
  * (§IV "Heterogeneous streams", Eqn 4a and the linear scaling rule):
  *   b_j = clamp(S_j, b_min, b_max)   (batch bounded to [b_min, b_max]),

@@ -88,6 +88,12 @@ _step_fused_ex = _sig("scadles_step_fused_ex", ctypes.c_int, ctypes.POINTER(_vp)
 _stream_weights = _sig("scadles_stream_weights", ctypes.c_int, ctypes.POINTER(ctypes.c_double), _u32,
                        ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_float),
                        ctypes.POINTER(ctypes.c_double))
+_step_layers_ws_bytes = _sig("scadles_step_layers_workspace_bytes", ctypes.c_size_t, _u32, ctypes.POINTER(_u64),
+                             _u32, ctypes.POINTER(ctypes.c_double))
+_step_fused_layers = _sig("scadles_step_fused_layers", ctypes.c_int, ctypes.POINTER(_vp), _u32, ctypes.POINTER(_u64),
+                          _u32, ctypes.POINTER(ctypes.c_double), ctypes.c_double, ctypes.POINTER(ctypes.c_float),
+                          ctypes.POINTER(_vp), ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, ctypes.c_float,
+                          ctypes.POINTER(StepOptions), _vp, ctypes.c_size_t, _vp)
 _stream_init = _sig("scadles_stream_init", ctypes.c_int, _u32, ctypes.POINTER(_u64), ctypes.POINTER(Stream))
 _stream_iteration = _sig("scadles_stream_iteration", ctypes.c_int, _u32, ctypes.POINTER(Stream), ctypes.POINTER(_u64),
                          _u64, _u64, ctypes.c_int, ctypes.c_double, ctypes.POINTER(_u64),
@@ -402,7 +408,7 @@ class FusedStep:
 
     def __init__(self, grads, ratios: Sequence[float], *, delta: float = math.inf, params=None,
                  momentum_buf=None, momentum: float = 0.0, weight_decay: float = 0.0,
-                 ewma_beta: Optional[float] = None, track: bool = False):
+                 ewma_beta: Optional[float] = None, track: bool = False, seg_off: Optional[Sequence[int]] = None):
         torch = _torch()
         if isinstance(grads, torch.Tensor) and grads.dim() == 2:
             grads = [grads[j] for j in range(grads.shape[0])]
@@ -410,6 +416,12 @@ class FusedStep:
         if not 1 <= self.K <= MAX_DEVICES:
             raise ValueError(f"K must be in [1, {MAX_DEVICES}]")
         self.n = grads[0].numel()
+        # per-layer Top-k over layers [seg_off[l], seg_off[l+1]) when given
+        self.seg_off = None if seg_off is None else [int(x) for x in seg_off]
+        if self.seg_off is not None:
+            if len(self.seg_off) < 2 or self.seg_off[-1] != self.n:
+                raise ValueError("seg_off must run from 0 to the gradients' size")
+            self._seg, self._L = _seg_array(self.seg_off)
         self.grads = list(grads)
         for j, g in enumerate(self.grads):
             _dev_f32(g, f"grads[{j}]")
@@ -453,7 +465,10 @@ class FusedStep:
         if len(ratios) != self.K:
             raise ValueError("one ratio per device")
         self.ratios = ratios
-        self.k = [topk_k(self.n, r) for r in ratios]
+        if self.seg_off is not None:
+            self.k = [layers_k(self.seg_off, r) for r in ratios]
+        else:
+            self.k = [topk_k(self.n, r) for r in ratios]
         if min(self.k) == 0:
             raise ScadlesError(1, "ratio outside (0, 1]")
         self.idx = [torch.empty(k, dtype=torch.uint32, device=self.device) for k in self.k]
@@ -461,7 +476,10 @@ class FusedStep:
         self._ratios = (ctypes.c_double * self.K)(*ratios)
         self._idx_ptrs = (_vp * self.K)(*[t.data_ptr() for t in self.idx])
         self._val_ptrs = (_vp * self.K)(*[t.data_ptr() for t in self.val])
-        need = workspace_bytes(self.K, self.n, ratios)
+        if self.seg_off is not None:
+            need = int(_step_layers_ws_bytes(self.K, self._seg, self._L, self._ratios))
+        else:
+            need = workspace_bytes(self.K, self.n, ratios)
         if need == 0:
             raise ScadlesError(1, "workspace query rejected the arguments")
         if getattr(self, "ws", None) is None or self.ws.numel() < need:
@@ -472,7 +490,14 @@ class FusedStep:
         for j in range(self.K):
             self._w[j] = float(w[j])
         pp = _dev_f32(self.params, "params") if self.params is not None else None
-        if self.momentum_buf is not None or self.ewma is not None or self.counters is not None:
+        opts = self.momentum_buf is not None or self.ewma is not None or self.counters is not None
+        if self.seg_off is not None:
+            _check(_step_fused_layers(self._grad_ptrs, self.K, self._seg, self._L, self._ratios, self.delta, self._w,
+                                      self._idx_ptrs, self._val_ptrs, self.dense.data_ptr(),
+                                      self.energies.data_ptr(), self.compressed.data_ptr(), pp, float(lr),
+                                      ctypes.byref(self._opts) if opts else None, self.ws.data_ptr(),
+                                      self.ws.numel(), _stream_ptr(stream)))
+        elif opts:
             _check(_step_fused_ex(self._grad_ptrs, self.K, self.n, self._ratios, self.delta, self._w,
                                   self._idx_ptrs, self._val_ptrs, self.dense.data_ptr(), self.energies.data_ptr(),
                                   self.compressed.data_ptr(), pp, float(lr), ctypes.byref(self._opts),

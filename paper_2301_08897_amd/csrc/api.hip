@@ -458,24 +458,12 @@ size_t scadles_layers_workspace_bytes(uint32_t K, const uint64_t* seg_off, uint3
   return layers_ws(K, seg_off, L, ratios).total;
 }
 
-scadles_status scadles_topk_select_layers(const float* const* grads, uint32_t K, const uint64_t* seg_off, uint32_t L,
-                                          const double* ratios, uint32_t* const* idx, float* const* val,
-                                          double* energies, void* ws, size_t ws_bytes, void* stream)
+// The per-layer selection into idx / val with the whole-gradient energies
+// (arguments validated by the caller; lw laid out in ws).
+static scadles_status run_layers(const float* const* grads, uint32_t K, const uint64_t* seg_off, uint32_t L,
+                                 const double* ratios, uint32_t* const* idx, float* const* val, double* energies,
+                                 void* ws, const LayersWs& lw, hipStream_t s)
 {
-  if (K == 0 || K > kMaxK) return fail(SCADLES_EINVAL, "K = %u is outside [1, %d]", K, kMaxK);
-  if (scadles_status st = check_layers(seg_off, L)) return st;
-  if (!grads || !ratios || !idx || !val) return fail(SCADLES_EINVAL, "NULL argument");
-  if (energies && !aligned(energies, 8)) return fail(SCADLES_EINVAL, "energies must be 8-byte aligned");
-  for (uint32_t j = 0; j < K; ++j) {
-    if (!grads[j] || !idx[j] || !val[j]) return fail(SCADLES_EINVAL, "device %u has a NULL pointer", j);
-    if (!aligned(grads[j], 4)) return fail(SCADLES_EINVAL, "grads[%u] must be 4-byte aligned", j);
-    if (!aligned(idx[j], 4) || !aligned(val[j], 4)) return fail(SCADLES_EINVAL, "device %u outputs misaligned", j);
-    if (scadles_layers_k(seg_off, L, ratios[j]) == 0)
-      return fail(SCADLES_EINVAL, "ratio %g of device %u is not in (0, 1]", ratios[j], j);
-  }
-  const LayersWs lw = layers_ws(K, seg_off, L, ratios);
-  if (scadles_status st = check_ws(ws, ws_bytes, lw.total)) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
   uint8_t* base = static_cast<uint8_t*>(ws);
 
   // Short layers (at most row_max elements), longest first, go to the row
@@ -541,6 +529,147 @@ scadles_status scadles_topk_select_layers(const float* const* grads, uint32_t K,
       return st;
     first = false;
   }
+  return SCADLES_OK;
+}
+
+scadles_status scadles_topk_select_layers(const float* const* grads, uint32_t K, const uint64_t* seg_off, uint32_t L,
+                                          const double* ratios, uint32_t* const* idx, float* const* val,
+                                          double* energies, void* ws, size_t ws_bytes, void* stream)
+{
+  if (K == 0 || K > kMaxK) return fail(SCADLES_EINVAL, "K = %u is outside [1, %d]", K, kMaxK);
+  if (scadles_status st = check_layers(seg_off, L)) return st;
+  if (!grads || !ratios || !idx || !val) return fail(SCADLES_EINVAL, "NULL argument");
+  if (energies && !aligned(energies, 8)) return fail(SCADLES_EINVAL, "energies must be 8-byte aligned");
+  for (uint32_t j = 0; j < K; ++j) {
+    if (!grads[j] || !idx[j] || !val[j]) return fail(SCADLES_EINVAL, "device %u has a NULL pointer", j);
+    if (!aligned(grads[j], 4)) return fail(SCADLES_EINVAL, "grads[%u] must be 4-byte aligned", j);
+    if (!aligned(idx[j], 4) || !aligned(val[j], 4)) return fail(SCADLES_EINVAL, "device %u outputs misaligned", j);
+    if (scadles_layers_k(seg_off, L, ratios[j]) == 0)
+      return fail(SCADLES_EINVAL, "ratio %g of device %u is not in (0, 1]", ratios[j], j);
+  }
+  const LayersWs lw = layers_ws(K, seg_off, L, ratios);
+  if (scadles_status st = check_ws(ws, ws_bytes, lw.total)) return st;
+  return run_layers(grads, K, seg_off, L, ratios, idx, val, energies, ws, lw, static_cast<hipStream_t>(stream));
+}
+
+// Workspace of the per-layer fused step: the per-layer selection's, then the
+// energies, decisions, aggregation range markers and validation flag.
+struct StepLayersWs {
+  LayersWs lw;
+  size_t e = 0, st = 0, lb = 0, err = 0, total = 0;
+  uint32_t nrange = 0;
+};
+
+static StepLayersWs step_layers_ws(uint32_t K, const uint64_t* seg_off, uint32_t L, const double* ratios)
+{
+  StepLayersWs w;
+  w.lw = layers_ws(K, seg_off, L, ratios);
+  if (!w.lw.total) return StepLayersWs{};
+  w.nrange = ceil_div_u64(seg_off[L], kARange);
+  w.e = w.lw.total;
+  w.st = align256(w.e + sizeof(double) * 2 * K);
+  w.lb = align256(w.st + sizeof(DevState) * K);
+  w.err = align256(w.lb + sizeof(uint32_t) * (size_t)K * w.nrange);
+  w.total = align256(w.err + sizeof(uint32_t));
+  return w;
+}
+
+size_t scadles_step_layers_workspace_bytes(uint32_t K, const uint64_t* seg_off, uint32_t L, const double* ratios)
+{
+  if (scadles_layers_workspace_bytes(K, seg_off, L, ratios) == 0) return 0;
+  return step_layers_ws(K, seg_off, L, ratios).total;
+}
+
+scadles_status scadles_step_fused_layers(const float* const* grads, uint32_t K, const uint64_t* seg_off, uint32_t L,
+                                         const double* ratios, double delta, const float* weights,
+                                         uint32_t* const* idx, float* const* val, float* dense, double* energies,
+                                         uint8_t* compressed, float* params, float lr,
+                                         const scadles_step_options* options, void* ws, size_t ws_bytes,
+                                         void* stream)
+{
+  if (K == 0 || K > kMaxK) return fail(SCADLES_EINVAL, "K = %u is outside [1, %d]", K, kMaxK);
+  if (scadles_status st = check_layers(seg_off, L)) return st;
+  const uint64_t n = seg_off[L];
+  scadles_step_options opt;
+  memset(&opt, 0, sizeof(opt));
+  if (options) opt = *options;
+  if (!grads || !ratios || !idx || !val || !dense) return fail(SCADLES_EINVAL, "NULL argument");
+  if (std::isnan(delta) || delta < 0.0) return fail(SCADLES_EINVAL, "delta must be >= 0 (or +INFINITY)");
+  if (!aligned(dense, 16)) return fail(SCADLES_EINVAL, "dense must be 16-byte aligned");
+  if (params && !aligned(params, 16)) return fail(SCADLES_EINVAL, "params must be 16-byte aligned");
+  if (params && !std::isfinite(lr)) return fail(SCADLES_EINVAL, "lr is not finite");
+  if (opt.momentum_buf) {
+    if (!params) return fail(SCADLES_EINVAL, "the momentum update needs params");
+    if (!aligned(opt.momentum_buf, 16)) return fail(SCADLES_EINVAL, "momentum_buf must be 16-byte aligned");
+    if (!std::isfinite(opt.momentum) || !std::isfinite(opt.weight_decay))
+      return fail(SCADLES_EINVAL, "momentum and weight_decay must be finite");
+    if (overlap(opt.momentum_buf, params, n) || overlap(opt.momentum_buf, dense, n))
+      return fail(SCADLES_EINVAL, "momentum_buf overlaps params or dense");
+  }
+  if (opt.ewma) {
+    if (!aligned(opt.ewma, 8)) return fail(SCADLES_EINVAL, "ewma must be 8-byte aligned");
+    if (!(opt.ewma_beta >= 0.0 && opt.ewma_beta < 1.0)) return fail(SCADLES_EINVAL, "ewma_beta must be in [0, 1)");
+  }
+  if (opt.counters && !aligned(opt.counters, 8)) return fail(SCADLES_EINVAL, "counters must be 8-byte aligned");
+  if (energies && !aligned(energies, 8)) return fail(SCADLES_EINVAL, "energies must be 8-byte aligned");
+  if (scadles_status st = check_weights(weights, K)) return st;
+  uint64_t kk[kMaxK];
+  for (uint32_t j = 0; j < K; ++j) {
+    if (!grads[j] || !idx[j] || !val[j]) return fail(SCADLES_EINVAL, "device %u has a NULL pointer", j);
+    if (!aligned(grads[j], 4)) return fail(SCADLES_EINVAL, "grads[%u] must be 4-byte aligned", j);
+    if (!aligned(idx[j], 4) || !aligned(val[j], 4)) return fail(SCADLES_EINVAL, "device %u outputs misaligned", j);
+    kk[j] = scadles_layers_k(seg_off, L, ratios[j]);
+    if (kk[j] == 0) return fail(SCADLES_EINVAL, "ratio %g of device %u is not in (0, 1]", ratios[j], j);
+  }
+  const StepLayersWs w = step_layers_ws(K, seg_off, L, ratios);
+  if (scadles_status st = check_ws(ws, ws_bytes, w.total)) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* b = static_cast<char*>(ws);
+  double* e_ws = reinterpret_cast<double*>(b + w.e);
+  if (scadles_status st = run_layers(grads, K, seg_off, L, ratios, idx, val, e_ws, ws, w.lw, s)) return st;
+  DecideArgs da;
+  memset(&da, 0, sizeof(da));
+  da.e = e_ws;
+  da.st = reinterpret_cast<DevState*>(b + w.st);
+  da.ewma = opt.ewma;
+  da.beta = opt.ewma_beta;
+  da.delta = delta;
+  da.counters = opt.counters;
+  da.energies_out = energies;
+  da.compressed_out = compressed;
+  da.n = n;
+  da.K = K;
+  AggArgs g;
+  memset(&g, 0, sizeof(g));
+  uint64_t kmax = 0;
+  for (uint32_t j = 0; j < K; ++j) {
+    da.k[j] = (uint32_t)kk[j];
+    g.idx[j] = idx[j];
+    g.val[j] = val[j];
+    g.dense[j] = grads[j];
+    g.k[j] = (uint32_t)kk[j];
+    g.w[j] = weights[j];
+    if (kk[j] > kmax) kmax = kk[j];
+  }
+  hipError_t e = launch_layers_decide(da, s);
+  if (e != hipSuccess) return hip_fail(e, "decision launch");
+  AggCtx c;
+  memset(&c, 0, sizeof(c));
+  c.st = da.st;
+  c.lb = reinterpret_cast<uint32_t*>(b + w.lb);
+  c.err = reinterpret_cast<uint32_t*>(b + w.err);
+  c.out = dense;
+  c.params = params;
+  c.mbuf = opt.momentum_buf;
+  c.lr = lr;
+  c.mom = opt.momentum;
+  c.wd = opt.weight_decay;
+  c.K = K;
+  c.nrange = w.nrange;
+  c.kmax = (uint32_t)kmax;
+  c.n = n;
+  e = launch_aggregate(g, c, 0, false, s);
+  if (e != hipSuccess) return hip_fail(e, "aggregate launch");
   return SCADLES_OK;
 }
 

@@ -24,6 +24,14 @@ constexpr int kRowLevels = 3;
 __device__ inline uint32_t level_shift(int level) { return level == 0 ? 19u : (level == 1 ? 9u : 0u); }
 __device__ inline uint32_t level_width(int level) { return level == 0 ? 12u : (level == 1 ? 10u : 9u); }
 constexpr uint32_t kRowBins = 1u << 12;
+constexpr int kRowSampleBits = 13;           // digit of the sample histogram
+constexpr uint32_t kRowSampleStride = 4096;  // one 256-element sample chunk per this many elements
+constexpr uint32_t kRowWholeMax = 65536;     // rows up to this long are their own sample
+// The full reads take kRowR rounds of 256 contiguous elements per wave at once
+// (every lane loads its 4 elements of each round before any is used): wave w
+// of a workgroup round covers [w, w + 1) * 256 * kRowR of it.
+constexpr int kRowR = 8;
+constexpr uint64_t kRowRound = (uint64_t)kRowBlock * 4 * kRowR;
 constexpr uint64_t kNotShort = ~0ull;
 
 // Inclusive scan of one value per thread in thread order over the workgroup;
@@ -148,52 +156,123 @@ __global__ __launch_bounds__(256) void k_rows_prep(RowsCtx rc, RowsPrep rp)
   }
 }
 
-// The selection of one row (see the top of this file).
-__global__ __launch_bounds__(kRowBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_rows(RowsCtx rc)
+// First virtual position of lane l's 4 elements in round r of wave w.
+__device__ inline uint64_t row_pos(uint64_t v0, uint32_t w, int r, uint32_t l)
 {
-  __shared__ uint32_t hist[kRowBins];
-  __shared__ uint32_t cand[kRowCand];
-  __shared__ uint32_t s_w[kRowWaves];
-  __shared__ uint32_t s_res[4];
-  __shared__ double s_d[kRowWaves];
-  const RowDesc d = rc.rows[blockIdx.x];
-  const uint32_t tid = threadIdx.x;
-  const Row row{gptr(d.grad), ((uint64_t)d.grad >> 2) & 3u, d.n};
-  const uint64_t vend = (uint64_t)d.n + row.shift;
-  constexpr uint64_t kStep = (uint64_t)kRowBlock * 4;
+  return v0 + (uint64_t)w * (256u * kRowR) + (uint64_t)r * 256u + 4u * l;
+}
 
-  // top digit over the row, and sum g^2
-  for (uint32_t i = tid; i < kRowBins; i += kRowBlock) hist[i] = 0u;
-  __syncthreads();
-  double e_all = 0.0;
-  for (uint64_t v = (uint64_t)tid * 4; v < vend; v += kStep) {
-    const f4 x = load4(row, v, false);
+// One round of the ordered output in a wave: its kept entries (keys above the
+// threshold, and keys equal to it while fewer than `need` came before) at
+// their positions; run_g / run_e count the wave's keys above / equal so far.
+__device__ inline void row_write_round(const f4& x, uint64_t v, uint64_t vend, const Row& row, uint32_t base,
+                                       uint32_t thr, uint32_t need, uint32_t k, GLOBAL uint32_t* oi,
+                                       GLOBAL float* ov, uint32_t& run_g, uint32_t& run_e, double& e2)
+{
+  bool fg[4], fe[4];
+  uint64_t bg[4], be[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (in_row(row, v + q)) {
-        atomicAdd(&hist[key_of(x[q]) >> level_shift(0)], 1u);
-        e_all = __builtin_fma((double)x[q], (double)x[q], e_all);
+  for (int q = 0; q < 4; ++q) {
+    const bool valid = v < vend && in_row(row, v + q);
+    const uint32_t key = key_of(x[q]);
+    fg[q] = valid && key > thr;
+    fe[q] = valid && key == thr;
+    bg[q] = ballot(fg[q]);
+    be[q] = ballot(fe[q]);
+  }
+  if ((bg[0] | bg[1] | bg[2] | bg[3] | be[0] | be[1] | be[2] | be[3]) == 0ull) return;
+  uint32_t gt_b = run_g + mbcnt(bg[0]) + mbcnt(bg[1]) + mbcnt(bg[2]) + mbcnt(bg[3]);
+  uint32_t eq_b = run_e + mbcnt(be[0]) + mbcnt(be[1]) + mbcnt(be[2]) + mbcnt(be[3]);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (fg[q] || (fe[q] && eq_b < need)) {
+      const uint32_t pos = gt_b + (eq_b < need ? eq_b : need);
+      if (pos < k) {
+        oi[pos] = (uint32_t)(v + q - row.shift) + base;
+        ov[pos] = x[q];
+      }
+      e2 = __builtin_fma((double)x[q], (double)x[q], e2);
+    }
+    gt_b += fg[q] ? 1u : 0u;
+    eq_b += fe[q] ? 1u : 0u;
+  }
+  run_g += (uint32_t)(__builtin_popcountll(bg[0]) + __builtin_popcountll(bg[1]) + __builtin_popcountll(bg[2]) +
+                      __builtin_popcountll(bg[3]));
+  run_e += (uint32_t)(__builtin_popcountll(be[0]) + __builtin_popcountll(be[1]) + __builtin_popcountll(be[2]) +
+                      __builtin_popcountll(be[3]));
+}
+
+// Radix selection, digit by digit, of the rank-th largest key among the keys
+// with prefix `prefix` of `pbits` bits, starting at digit level `level`, over
+// the m keys in cand (LDS). Returns the key; `rank` ends as the number of keys
+// equal to it that are kept (the rank within the equal keys).
+__device__ inline uint32_t row_select_lds(const uint32_t* cand, uint32_t m, uint32_t& rank, uint32_t* hist,
+                                          uint32_t* s_w, uint32_t* s_res)
+{
+  const uint32_t tid = threadIdx.x;
+  uint32_t prefix = 0, pbits = 0;
+  for (int level = 0; level < kRowLevels; ++level) {
+    const uint32_t sh = level_shift(level), mask = (1u << level_width(level)) - 1u;
+    const uint32_t pshift = 31u - pbits;
+    for (uint32_t i = tid; i < kRowBins; i += kRowBlock) hist[i] = 0u;
+    if (tid == 0) s_res[0] = s_res[1] = s_res[2] = 0u;
+    __syncthreads();
+    for (uint32_t i = tid; i < m; i += kRowBlock) {
+      const uint32_t key = cand[i];
+      if (pbits == 0 || (key >> pshift) == prefix) atomicAdd(&hist[(key >> sh) & mask], 1u);
+    }
+    __syncthreads();
+    row_select_bin(hist, level_width(level), rank, s_w, s_res);
+    rank -= s_res[1];
+    prefix = (prefix << level_width(level)) | s_res[0];
+    pbits += level_width(level);
+    __syncthreads();
+  }
+  return prefix;
+}
+
+// The same over the whole row in global memory, for rows whose sampled
+// bracket missed: a histogram read per digit until the keys sharing the
+// decided digits fit in LDS, then the rest in LDS.
+__device__ inline uint32_t row_select_global(const Row& row, uint64_t vend, uint32_t& rank, uint32_t* hist,
+                                             uint32_t* cand, uint32_t* s_w, uint32_t* s_res)
+{
+  const uint32_t tid = threadIdx.x;
+  constexpr uint64_t kStep = (uint64_t)kRowBlock * 4;
+  uint32_t prefix = 0, pbits = 0, m = 0;
+  bool in_lds = false;
+  for (int level = 0; level < kRowLevels; ++level) {
+    const uint32_t sh = level_shift(level), mask = (1u << level_width(level)) - 1u;
+    const uint32_t pshift = 31u - pbits;
+    for (uint32_t i = tid; i < kRowBins; i += kRowBlock) hist[i] = 0u;
+    if (tid == 0) s_res[0] = s_res[1] = s_res[2] = 0u;
+    __syncthreads();
+    if (in_lds) {
+      for (uint32_t i = tid; i < m; i += kRowBlock) {
+        const uint32_t key = cand[i];
+        if ((key >> pshift) == prefix) atomicAdd(&hist[(key >> sh) & mask], 1u);
+      }
+    } else {
+      for (uint64_t v = (uint64_t)tid * 4; v < vend; v += kStep) {
+        const f4 x = load4(row, v, false);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t key = key_of(x[q]);
+          if (in_row(row, v + q) && (pbits == 0 || (key >> pshift) == prefix))
+            atomicAdd(&hist[(key >> sh) & mask], 1u);
+        }
       }
     }
-  }
-  {
-    const double ea = row_sum_f64(e_all, s_d);  // (its barriers also complete the histogram)
-    if (tid == 0) rc.row_e[2ull * d.eslot] = ea;
-  }
-
-  uint32_t rank = d.k, prefix = 0, pbits = 0, m = 0;
-  bool in_lds = false;
-  for (int level = 0;; ++level) {
-    if (tid == 0) s_res[0] = s_res[1] = s_res[2] = 0u;
+    __syncthreads();
     row_select_bin(hist, level_width(level), rank, s_w, s_res);
-    const uint32_t b = s_res[0], above = s_res[1], h = s_res[2];
-    rank -= above;
-    prefix = (prefix << level_width(level)) | b;
+    const uint32_t h = s_res[2];
+    rank -= s_res[1];
+    prefix = (prefix << level_width(level)) | s_res[0];
     pbits += level_width(level);
-    if (level + 1 == kRowLevels) break;
-    const uint32_t pshift = 31u - pbits;
-    if (!in_lds && h <= (uint32_t)kRowCand) {
+    __syncthreads();
+    if (level + 1 < kRowLevels && !in_lds && h <= (uint32_t)kRowCand) {
       // the keys sharing the decided digits fit in LDS: collect them
+      const uint32_t ps = 31u - pbits;
       if (tid == 0) s_res[3] = 0u;
       __syncthreads();
       for (uint64_t v = (uint64_t)tid * 4; v < vend; v += kStep) {
@@ -201,7 +280,7 @@ __global__ __launch_bounds__(kRowBlock) __attribute__((amdgpu_waves_per_eu(8, 8)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const uint32_t key = key_of(x[q]);
-          if (in_row(row, v + q) && (key >> pshift) == prefix) {
+          if (in_row(row, v + q) && (key >> ps) == prefix) {
             const uint32_t at = atomicAdd(&s_res[3], 1u);
             if (at < (uint32_t)kRowCand) cand[at] = key;
           }
@@ -210,68 +289,172 @@ __global__ __launch_bounds__(kRowBlock) __attribute__((amdgpu_waves_per_eu(8, 8)
       __syncthreads();
       m = s_res[3] < (uint32_t)kRowCand ? s_res[3] : (uint32_t)kRowCand;
       in_lds = true;
+      __syncthreads();
     }
-    // histogram of the next digit over the keys sharing the decided digits
-    const uint32_t nshift = level_shift(level + 1), nmask = (1u << level_width(level + 1)) - 1u;
-    __syncthreads();
-    for (uint32_t i = tid; i < kRowBins; i += kRowBlock) hist[i] = 0u;
-    __syncthreads();
-    if (in_lds) {
-      for (uint32_t i = tid; i < m; i += kRowBlock) {
-        const uint32_t key = cand[i];
-        if ((key >> pshift) == prefix) atomicAdd(&hist[(key >> nshift) & nmask], 1u);
-      }
-    } else {
-      for (uint64_t v = (uint64_t)tid * 4; v < vend; v += kStep) {
-        const f4 x = load4(row, v, false);
+  }
+  return prefix;
+}
+
+// The selection of one row. A systematic sample (256-element chunks every
+// kRowSampleStride elements; the whole row when it is short) gives a bracket
+// [t_lo, t_hi) that holds the k-th largest key with high probability: the
+// bins of its 13-bit histogram around k's expected sample rank, six standard
+// deviations and 8 ranks either side. One read of the row then counts the keys
+// at or above t_hi, gathers the keys inside the bracket into LDS and sums g^2;
+// the k-th largest key is selected among the gathered ones. If the bracket
+// missed or overflowed LDS, the digits are decided over the whole row instead.
+// A last read writes the kept entries in index order.
+__global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
+{
+  __shared__ uint32_t hist[kRowBins];
+  __shared__ uint32_t cand[kRowCand];
+  __shared__ uint32_t s_w[kRowWaves];
+  __shared__ uint32_t s_res[4];
+  __shared__ double s_d[kRowWaves];
+  const RowDesc d = rc.rows[blockIdx.x];
+  const uint32_t tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
+  const Row row{gptr(d.grad), ((uint64_t)d.grad >> 2) & 3u, d.n};
+  const uint64_t vend = (uint64_t)d.n + row.shift;
+  constexpr uint64_t kStep = (uint64_t)kRowBlock * 4;
+
+  // 1. sample histogram (13-bit digit, in the candidate array's memory)
+  uint32_t* shist = cand;
+  static_assert((1 << kRowSampleBits) <= kRowCand, "the sample histogram lives in the candidate array");
+  const bool whole = d.n <= (uint32_t)kRowWholeMax;
+  const uint64_t stride = whole ? 256u : (uint64_t)kRowSampleStride;
+  for (uint32_t i = tid; i < (1u << kRowSampleBits); i += kRowBlock) shist[i] = 0u;
+  __syncthreads();
+  uint32_t s_cnt = 0;
+  for (uint64_t c = w; c * stride < vend; c += kRowWaves) {
+    const uint64_t v = c * stride + 4u * lane;
+    if (v < vend) {
+      const f4 x = load4(row, v, false);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t key = key_of(x[q]);
-          if (in_row(row, v + q) && (key >> pshift) == prefix) atomicAdd(&hist[(key >> nshift) & nmask], 1u);
+      for (int q = 0; q < 4; ++q) {
+        if (in_row(row, v + q)) {
+          atomicAdd(&shist[key_of(x[q]) >> (31 - kRowSampleBits)], 1u);
+          ++s_cnt;
         }
       }
     }
+  }
+  uint32_t s_n;
+  row_scan(s_cnt, s_w, s_n);
+  // sample ranks bracketing the k-th largest key
+  uint32_t r_lo, r_hi;
+  if (whole) {
+    r_lo = r_hi = d.k;
+  } else {
+    const double kf = (double)d.k * (double)s_n / (double)d.n, sd = __builtin_sqrt(kf);
+    double lo = __builtin_ceil(kf + 6.0 * sd + 8.0), hi = __builtin_floor(kf - 6.0 * sd - 8.0);
+    lo = lo > (double)s_n ? (double)s_n : (lo < 1.0 ? 1.0 : lo);
+    r_lo = (uint32_t)lo;
+    r_hi = hi < 1.0 ? 0u : (uint32_t)hi;
+  }
+  if (tid == 0) s_res[0] = s_res[1] = s_res[2] = 0u;
+  row_select_bin(shist, kRowSampleBits, r_lo, s_w, s_res);
+  const uint32_t t_lo = s_res[0] << (31 - kRowSampleBits);
+  __syncthreads();
+  uint32_t t_hi = kKeyInf;
+  if (r_hi >= 1) {
+    if (tid == 0) s_res[0] = s_res[1] = s_res[2] = 0u;
+    row_select_bin(shist, kRowSampleBits, r_hi, s_w, s_res);
+    t_hi = (s_res[0] + 1u) << (31 - kRowSampleBits);
     __syncthreads();
   }
-  const uint32_t thr = prefix, need = rank;
 
-  // ordered output: 4096 positions per round, kept positions by a workgroup scan
+  // 2. one read: keys >= t_hi counted, keys in [t_lo, t_hi) gathered, sum g^2
+  if (tid == 0) s_res[3] = 0u;
+  __syncthreads();
+  double e_all = 0.0;
+  uint32_t sure = 0;
+  for (uint64_t v0 = 0; v0 < vend; v0 += kRowRound) {
+    f4 x[kRowR];
+#pragma unroll
+    for (int r = 0; r < kRowR; ++r) {
+      const uint64_t v = row_pos(v0, w, r, lane);
+      x[r] = v < vend ? load4(row, v, false) : f4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int r = 0; r < kRowR; ++r) {
+      const uint64_t v = row_pos(v0, w, r, lane);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const bool valid = v < vend && in_row(row, v + q);
+        const uint32_t key = key_of(x[r][q]);
+        sure += (valid && key >= t_hi) ? 1u : 0u;
+        const bool band = valid && key >= t_lo && key < t_hi;
+        const uint64_t bal = ballot(band);
+        if (bal) {
+          uint32_t at = 0;
+          if (lane == (uint32_t)__builtin_ctzll(bal)) at = atomicAdd(&s_res[3], (uint32_t)__builtin_popcountll(bal));
+          at = __shfl(at, __builtin_ctzll(bal), 64) + mbcnt(bal);
+          if (band && at < (uint32_t)kRowCand) cand[at] = key;
+        }
+        if (valid) e_all = __builtin_fma((double)x[r][q], (double)x[r][q], e_all);
+      }
+    }
+  }
+  uint32_t sure_all;
+  row_scan(sure, s_w, sure_all);
+  const uint32_t nband = s_res[3];
+  {
+    const double ea = row_sum_f64(e_all, s_d);
+    if (tid == 0) rc.row_e[2ull * d.eslot] = ea;
+  }
+
+  // 3. the threshold key and the number of keys equal to it that are kept
+  uint32_t thr, need;
+  if (sure_all < d.k && d.k - sure_all <= nband && nband <= (uint32_t)kRowCand) {
+    need = d.k - sure_all;
+    thr = row_select_lds(cand, nband, need, hist, s_w, s_res);
+  } else {
+    need = d.k;
+    thr = row_select_global(row, vend, need, hist, cand, s_w, s_res);
+  }
+
+  // 4. ordered output: per workgroup round, the waves' counts of keys above
+  // and equal to the threshold give each wave's starting position
   uint32_t run_g = 0, run_e = 0;
   double e_kept = 0.0;
   GLOBAL uint32_t* oi = gptr(d.idx_out);
   GLOBAL float* ov = gptr(d.val_out);
 #pragma unroll 1
-  for (uint64_t v0 = 0; v0 < vend; v0 += kStep) {
-    const uint64_t v = v0 + (uint64_t)tid * 4;
-    const f4 x = v < vend ? load4(row, v, false) : f4{0.f, 0.f, 0.f, 0.f};
-    bool g[4], e[4];
-    uint32_t cg = 0, ce = 0;
+  for (uint64_t v0 = 0; v0 < vend; v0 += kRowRound) {
+    f4 x[kRowR];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const bool valid = v < vend && in_row(row, v + q);
-      const uint32_t key = key_of(x[q]);
-      g[q] = valid && key > thr;
-      e[q] = valid && key == thr;
-      cg += g[q] ? 1u : 0u;
-      ce += e[q] ? 1u : 0u;
+    for (int r = 0; r < kRowR; ++r) {
+      const uint64_t v = row_pos(v0, w, r, lane);
+      x[r] = v < vend ? load4(row, v, false) : f4{0.f, 0.f, 0.f, 0.f};
     }
-    const uint32_t mine = cg | (ce << 16);
-    uint32_t tot;
-    const uint32_t ex = row_scan(mine, s_w, tot) - mine;
-    uint32_t gb = run_g + (ex & 0xFFFFu), eb = run_e + (ex >> 16);
+    uint32_t cnt = 0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (g[q] || (e[q] && eb < need)) {
-        const uint32_t pos = gb + (eb < need ? eb : need);
-        if (pos < d.k) {
-          oi[pos] = (uint32_t)(v + q - row.shift) + d.base;
-          ov[pos] = x[q];
-        }
-        e_kept = __builtin_fma((double)x[q], (double)x[q], e_kept);
+    for (int r = 0; r < kRowR; ++r) {
+      const uint64_t v = row_pos(v0, w, r, lane);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const bool valid = v < vend && in_row(row, v + q);
+        const uint32_t key = key_of(x[r][q]);
+        cnt += (valid && key > thr) ? 1u : 0u;
+        cnt += (valid && key == thr) ? 0x10000u : 0u;
       }
-      gb += g[q] ? 1u : 0u;
-      eb += e[q] ? 1u : 0u;
     }
+    uint32_t wt = cnt;
+#pragma unroll
+    for (int dd = 32; dd >= 1; dd >>= 1) wt += __shfl_xor(wt, dd, 64);
+    if (lane == 0) s_w[w] = wt;
+    __syncthreads();
+    uint32_t wex = 0, tot = 0;
+    for (uint32_t i = 0; i < (uint32_t)kRowWaves; ++i) {
+      const uint32_t y = s_w[i];
+      wex += i < w ? y : 0u;
+      tot += y;
+    }
+    __syncthreads();
+    uint32_t rg = run_g + (wex & 0xFFFFu), re = run_e + (wex >> 16);
+#pragma unroll
+    for (int r = 0; r < kRowR; ++r)
+      row_write_round(x[r], row_pos(v0, w, r, lane), vend, row, d.base, thr, need, d.k, oi, ov, rg, re, e_kept);
     run_g += tot & 0xFFFFu;
     run_e += tot >> 16;
   }
@@ -294,7 +477,30 @@ __global__ __launch_bounds__(64) void k_rows_energy(RowsCtx rc, double* energies
   energies[2 * j + 1] = ek;
 }
 
+// The adaptive rule of §IV per device on its whole-gradient energies after a
+// per-layer selection (and the moving average and accounting options).
+__global__ __launch_bounds__(64) void k_layers_decide(DecideArgs a)
+{
+  const uint32_t j = blockIdx.x * 64 + threadIdx.x;
+  if (j >= a.K) return;
+  const double ea = a.e[2 * j], ek = a.e[2 * j + 1];
+  const uint32_t sp = adaptive_rule(ea, ek, a.ewma ? a.ewma + 2 * (uint64_t)j : nullptr, a.beta, a.delta);
+  a.st[j].sparse = sp;
+  if (a.counters) account(a.counters + 3 * (uint64_t)j, sp, a.k[j], a.n);
+  if (a.energies_out) {
+    a.energies_out[2 * j] = ea;
+    a.energies_out[2 * j + 1] = ek;
+  }
+  if (a.compressed_out) a.compressed_out[j] = (uint8_t)sp;
+}
+
 }  // namespace
+
+hipError_t launch_layers_decide(const DecideArgs& a, hipStream_t s)
+{
+  k_layers_decide<<<(a.K + 63) / 64, 64, 0, s>>>(a);
+  return hipGetLastError();
+}
 
 hipError_t launch_put_table(const uint64_t* src, uint64_t count, uint64_t* dst, hipStream_t s)
 {

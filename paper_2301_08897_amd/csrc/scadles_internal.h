@@ -229,6 +229,21 @@ struct RowsCtx {
 };
 
 hipError_t launch_put_table(const uint64_t* src, uint64_t count, uint64_t* dst, hipStream_t s);
+
+// Decision of the per-layer fused step.
+struct DecideArgs {
+  const double* e;          // [K x 2] whole-gradient energies
+  DevState* st;             // .sparse receives the decision
+  double* ewma;             // moving-average states or null
+  double beta, delta;
+  uint64_t* counters;       // accounting or null
+  double* energies_out;     // copy of e, or null
+  uint8_t* compressed_out;  // or null
+  uint64_t n;
+  uint32_t K;
+  uint32_t k[kMaxK];        // entries kept per device
+};
+hipError_t launch_layers_decide(const DecideArgs& a, hipStream_t s);
 hipError_t launch_rows(const RowsCtx& rc, const RowsPrep& rp, double* energies, hipStream_t s);
 
 // k = clamp(floor(ratio * n), 1, n), the same double arithmetic on host and device.
@@ -240,6 +255,36 @@ __host__ __device__ inline uint64_t k_of(uint64_t n, double ratio)
   if (k < 1) k = 1;
   if (k > n) k = n;
   return k;
+}
+
+// The adaptive compression rule of §IV on a device's energies E_all, E_kept:
+// with a moving-average state m (2 doubles; both 0 means no history, and the
+// energies are taken as they are) the rule sees m <- beta m + (1 - beta) E.
+// Returns 1 to send Top-k (relative energy loss at most delta), else 0.
+__device__ inline uint32_t adaptive_rule(double ea, double ek, double* m, double beta, double delta)
+{
+  if (m) {
+    if (m[0] == 0.0 && m[1] == 0.0) {
+      m[0] = ea;
+      m[1] = ek;
+    } else {
+      m[0] = beta * m[0] + (1.0 - beta) * ea;
+      m[1] = beta * m[1] + (1.0 - beta) * ek;
+    }
+    ea = m[0];
+    ek = m[1];
+  }
+  const double rho = (ea == 0.0) ? 0.0 : __builtin_fabs(ea - ek) / ea;
+  return (rho <= delta) ? 1u : 0u;
+}
+
+// §V-G accounting of one iteration: [0] iterations that sent Top-k, [1]
+// iterations, [2] floats sent (k when compressed, n otherwise).
+__device__ inline void account(uint64_t* q, uint32_t sparse, uint64_t k, uint64_t n)
+{
+  q[0] += sparse;
+  q[1] += 1u;
+  q[2] += sparse ? k : n;
 }
 
 // ---- sizing shared by host and device -----------------------------------------------------

@@ -1273,29 +1273,8 @@ __device__ inline void final_body(const Ctx& c, uint32_t jr)
   if (s.c_gt + need != c.desc[j].k) s.err |= 16u;
   s.e_kept = e_kept;
   // §IV: the rule compares the energies, optionally their moving averages
-  // (no history yet: the first iteration takes its energies as they are)
-  double ea = s.e_all, ek = e_kept;
-  if (c.ewma) {
-    double* m = c.ewma + 2 * (uint64_t)j;
-    if (m[0] == 0.0 && m[1] == 0.0) {
-      m[0] = ea;
-      m[1] = ek;
-    } else {
-      m[0] = c.ewma_beta * m[0] + (1.0 - c.ewma_beta) * ea;
-      m[1] = c.ewma_beta * m[1] + (1.0 - c.ewma_beta) * ek;
-    }
-    ea = m[0];
-    ek = m[1];
-  }
-  const double rho = (ea == 0.0) ? 0.0 : __builtin_fabs(ea - ek) / ea;
-  s.sparse = (rho <= c.delta) ? 1u : 0u;
-  if (c.counters) {
-    // §V-G accounting: iterations that sent Top-k, iterations, floats sent
-    uint64_t* q = c.counters + 3 * (uint64_t)j;
-    q[0] += s.sparse;
-    q[1] += 1u;
-    q[2] += s.sparse ? (uint64_t)c.desc[j].k : c.n;
-  }
+  s.sparse = adaptive_rule(s.e_all, e_kept, c.ewma ? c.ewma + 2 * (uint64_t)j : nullptr, c.ewma_beta, c.delta);
+  if (c.counters) account(c.counters + 3 * (uint64_t)j, s.sparse, c.desc[j].k, c.n);
   if (c.energies_out) {
     if (c.energies_add) {
       c.energies_out[2 * j] += s.e_all;

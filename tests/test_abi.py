@@ -194,3 +194,31 @@ def test_layers_queries(sc, orc):
     need = sc.layers_workspace_bytes(3, off, [0.01] * 3)
     assert need >= sc.workspace_bytes(3, 1_999_000, [0.01] * 3) > 0
     assert sc.layers_workspace_bytes(3, [0, 5, 5], [0.01] * 3) == 0
+
+
+def test_fused_layers_validation_before_any_launch(sc):
+    """Invalid per-layer fused steps return EINVAL / EWORKSPACE and launch nothing."""
+    inval, ws = 1, 2
+    grads = (ctypes.c_void_p * 2)(16, 32)
+    outs = (ctypes.c_void_p * 2)(4096, 8192)
+    ratios = (ctypes.c_double * 2)(0.1, 0.1)
+    w = (ctypes.c_float * 2)(0.5, 0.5)
+
+    def call(off, delta=math.inf, weights=w, dense=1 << 20, ws_bytes=1 << 30, params=None):
+        arr = (ctypes.c_uint64 * len(off))(*off)
+        return sc._step_fused_layers(grads, 2, arr, len(off) - 1, ratios, delta, weights, outs, outs, dense, None,
+                                     None, params, 0.1, None, 65536, ws_bytes, None)
+
+    assert call([0, 5, 5, 10]) == inval                                   # empty layer
+    assert call([0, 10], delta=-1.0) == inval
+    assert call([0, 10], weights=(ctypes.c_float * 2)(0.7, 0.7)) == inval  # weights do not sum to 1
+    assert call([0, 10], dense=(1 << 20) + 4) == inval                    # misaligned dense
+    assert call([0, 10], params=(1 << 21) + 8) == inval                   # misaligned params
+    assert call([0, 4, 10], ws_bytes=64) == ws
+    O = sc.StepOptions
+    arr = (ctypes.c_uint64 * 2)(0, 10)
+    bad = O(None, 0.0, 0.0, 65536, 1.5, None)                             # beta outside [0, 1)
+    assert sc._step_fused_layers(grads, 2, arr, 1, ratios, math.inf, w, outs, outs, 1 << 20, None, None, None,
+                                 0.1, ctypes.byref(bad), 65536, 1 << 30, None) == inval
+    need = sc._step_layers_ws_bytes(2, arr, 1, ratios)
+    assert need >= sc.layers_workspace_bytes(2, [0, 10], [0.1, 0.1]) > 0

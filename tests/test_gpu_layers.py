@@ -213,3 +213,73 @@ def test_full_size_vgg19_layers(sc):
         assert same_bits(val[j].cpu().numpy(), val_o), f"device {j}: values"
         tol = energy_tol(s.n) * ea
         assert abs(e[2 * j] - ea) <= tol and abs(e[2 * j + 1] - ek) <= tol, f"device {j}: energies"
+
+
+@pytest.mark.parametrize("config,n,K,iters,beta,optimizer", [(5, 1_500_001, 6, 3, 0.5, "sgd"),
+                                                              (2, 700_001, 8, 2, None, "momentum"),
+                                                              (4, 900_000, 4, 2, 0.9, "momentum")])
+def test_fused_layers_step(sc, config, n, K, iters, beta, optimizer):
+    """Per-layer selection, the adaptive rule on the whole-gradient energies
+    (moving average when beta is set), Eqn 4b and the update in one call,
+    over several iterations with fresh gradients, against the oracle."""
+    torch, dev = torch_dev()
+    s = workloads.spec(config, n=n, K=K, iterations=iters)
+    seg_off = [0] + [int(x) for x in s.seg_end]
+    log(f"fused layers C{config} n={s.n} K={s.K} L={len(seg_off) - 1} beta={beta} {optimizer}")
+    G = np.empty((s.K, s.n), dtype=np.float32)
+    for j in range(s.K):
+        workloads.gradient(s, 0, j, out=G[j])
+    sets0 = [oracle.topk_layers(G[j], seg_off, s.ratios[0, j]) for j in range(s.K)]
+    rho = sorted(oracle.compress_decision(r[2], r[3], 0.0)[1] for r in sets0)
+    delta = 0.5 * (rho[len(rho) // 2 - 1] + rho[len(rho) // 2])
+    g_dev = torch.from_numpy(G).to(dev)
+    params = workloads.params0(s)
+    p_dev = torch.from_numpy(params).to(dev)
+    mom = (0.9, 5e-4) if optimizer == "momentum" else None
+    v_dev = torch.zeros(s.n, dtype=torch.float32, device=dev) if mom else None
+    step = sc.FusedStep(g_dev, s.ratios[0], delta=delta, params=p_dev, seg_off=seg_off, ewma_beta=beta, track=True,
+                        momentum_buf=v_dev, momentum=mom[0] if mom else 0.0, weight_decay=mom[1] if mom else 0.0)
+    p_ref = params.copy()
+    v_ref = np.zeros(s.n, dtype=np.float32)
+    state = np.zeros((s.K, 2))
+    counters = np.zeros((s.K, 3), dtype=np.uint64)
+    tol = energy_tol(s.n)
+    for it in range(s.iterations):
+        if it:
+            for j in range(s.K):
+                workloads.gradient(s, it, j, out=G[j])
+            g_dev.copy_(torch.from_numpy(G))
+        res = sets0 if it == 0 else [oracle.topk_layers(G[j], seg_off, s.ratios[it, j]) for j in range(s.K)]
+        w, gamma = sc.stream_weights(s.rates[it], base_batch=s.base_batch)
+        lr = float(np.float32(s.eta * gamma))
+        out = step.run(w, lr)
+        torch.cuda.synchronize()
+        got = out.compressed.cpu().numpy()
+        e = out.energies.cpu().numpy()
+        sets = []
+        for j, (idx, val, e_all, e_kept) in enumerate(res):
+            assert np.array_equal(out.idx[j].cpu().numpy(), idx), f"iteration {it} device {j}: indices"
+            assert same_bits(out.val[j].cpu().numpy(), val), f"iteration {it} device {j}: values"
+            assert abs(e[2 * j] - e_all) <= tol * e_all and abs(e[2 * j + 1] - e_kept) <= tol * e_all
+            if beta is None:
+                send, r = oracle.compress_decision(e_all, e_kept, delta)
+            else:
+                send = oracle.adaptive_step(state[j], counters[j], e_all, e_kept, beta, delta,
+                                            oracle.layers_k(seg_off, s.ratios[it, j]), s.n)
+                r = oracle.compress_decision(state[j][0], state[j][1], 0.0)[1]
+            if abs(r - delta) <= 8 * (it + 1) * tol:
+                send = bool(got[j])               # at the boundary either answer is correct
+            assert bool(got[j]) == send, f"iteration {it} device {j}: decision"
+            sets.append((idx, val) if send else (None, G[j]))
+        dense_o = oracle.aggregate(sets, w, s.n)
+        assert same_bits(out.dense.cpu().numpy(), dense_o), f"iteration {it}: aggregate"
+        if mom:
+            p_ref, v_ref = oracle.momentum_sgd(p_ref, v_ref, dense_o, lr, mom[0], mom[1])
+            assert same_bits(v_dev.cpu().numpy(), v_ref), f"iteration {it}: momentum buffer"
+        else:
+            p_ref = oracle.sgd(p_ref, dense_o, lr)
+        assert same_bits(p_dev.cpu().numpy(), p_ref), f"iteration {it}: update"
+    acc, _ = step.accounting()
+    assert np.all(acc[:, 1] == s.iterations)
+    sent = acc[:, 0]
+    assert np.all(acc[:, 2] == sent * np.array(step.k) + (s.iterations - sent) * s.n)
