@@ -32,6 +32,8 @@ constexpr uint32_t kRowWholeMax = 65536;     // rows up to this long are their o
 // of a workgroup round covers [w, w + 1) * 256 * kRowR of it.
 constexpr int kRowR = 8;
 constexpr uint64_t kRowRound = (uint64_t)kRowBlock * 4 * kRowR;
+// Per-wave chunks of a row whose tallies fit in LDS (rows up to 2^21 + 32768 elements)
+constexpr uint32_t kRowChunks = 65 * kRowWaves;
 constexpr uint64_t kNotShort = ~0ull;
 
 // Inclusive scan of one value per thread in thread order over the workgroup;
@@ -311,6 +313,7 @@ __global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
   __shared__ uint32_t s_w[kRowWaves];
   __shared__ uint32_t s_res[4];
   __shared__ double s_d[kRowWaves];
+  __shared__ uint32_t s_chunk[2 * kRowChunks];
   const RowDesc d = rc.rows[blockIdx.x];
   const uint32_t tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
   const Row row{gptr(d.grad), ((uint64_t)d.grad >> 2) & 3u, d.n};
@@ -325,14 +328,20 @@ __global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
   for (uint32_t i = tid; i < (1u << kRowSampleBits); i += kRowBlock) shist[i] = 0u;
   __syncthreads();
   uint32_t s_cnt = 0;
-  for (uint64_t c = w; c * stride < vend; c += kRowWaves) {
-    const uint64_t v = c * stride + 4u * lane;
-    if (v < vend) {
-      const f4 x = load4(row, v, false);
+  for (uint64_t c0 = w; c0 * stride < vend; c0 += 4 * kRowWaves) {
+    f4 x[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const uint64_t v = (c0 + r * kRowWaves) * stride + 4u * lane;
+      x[r] = v < vend ? load4(row, v, false) : f4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const uint64_t v = (c0 + r * kRowWaves) * stride + 4u * lane;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        if (in_row(row, v + q)) {
-          atomicAdd(&shist[key_of(x[q]) >> (31 - kRowSampleBits)], 1u);
+        if (v < vend && in_row(row, v + q)) {
+          atomicAdd(&shist[key_of(x[r][q]) >> (31 - kRowSampleBits)], 1u);
           ++s_cnt;
         }
       }
@@ -368,6 +377,8 @@ __global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
   __syncthreads();
   double e_all = 0.0;
   uint32_t sure = 0;
+  const uint64_t nchunk = (vend + kRowRound - 1) / kRowRound * kRowWaves;
+  const bool tally = nchunk <= (uint64_t)kRowChunks;
   for (uint64_t v0 = 0; v0 < vend; v0 += kRowRound) {
     f4 x[kRowR];
 #pragma unroll
@@ -375,6 +386,9 @@ __global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
       const uint64_t v = row_pos(v0, w, r, lane);
       x[r] = v < vend ? load4(row, v, false) : f4{0.f, 0.f, 0.f, 0.f};
     }
+    // count this lane's keys in the bracket, then one wave-wide slot
+    // reservation for all of them (one LDS atomic per wave and round)
+    uint32_t nb = 0, sure_w = 0;
 #pragma unroll
     for (int r = 0; r < kRowR; ++r) {
       const uint64_t v = row_pos(v0, w, r, lane);
@@ -382,16 +396,45 @@ __global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
       for (int q = 0; q < 4; ++q) {
         const bool valid = v < vend && in_row(row, v + q);
         const uint32_t key = key_of(x[r][q]);
-        sure += (valid && key >= t_hi) ? 1u : 0u;
-        const bool band = valid && key >= t_lo && key < t_hi;
-        const uint64_t bal = ballot(band);
-        if (bal) {
-          uint32_t at = 0;
-          if (lane == (uint32_t)__builtin_ctzll(bal)) at = atomicAdd(&s_res[3], (uint32_t)__builtin_popcountll(bal));
-          at = __shfl(at, __builtin_ctzll(bal), 64) + mbcnt(bal);
-          if (band && at < (uint32_t)kRowCand) cand[at] = key;
-        }
+        const bool above = valid && key >= t_hi;
+        sure += above ? 1u : 0u;
+        sure_w += (uint32_t)__builtin_popcountll(ballot(above));
+        nb += (valid && key >= t_lo && key < t_hi) ? 1u : 0u;
         if (valid) e_all = __builtin_fma((double)x[r][q], (double)x[r][q], e_all);
+      }
+    }
+    // this wave's chunk of the round: keys at or above t_hi, and where its
+    // bracket keys start in cand and how many there are
+    const uint64_t chunk = v0 / kRowRound * kRowWaves + w;
+    if (!ballot(nb != 0u)) {
+      if (tally && lane == 0) {
+        s_chunk[2 * chunk] = sure_w;
+        s_chunk[2 * chunk + 1] = 0u;
+      }
+    } else {
+      const uint32_t incl = wave_incl_scan(nb);
+      const uint32_t total = __shfl(incl, 63, 64);
+      uint32_t at = 0;
+      if (lane == 0) {
+        at = atomicAdd(&s_res[3], total);
+        if (tally) {
+          s_chunk[2 * chunk] = sure_w | (total << 16);
+          s_chunk[2 * chunk + 1] = at;
+        }
+      }
+      at = __shfl(at, 0, 64) + incl - nb;
+#pragma unroll
+      for (int r = 0; r < kRowR; ++r) {
+        const uint64_t v = row_pos(v0, w, r, lane);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const bool valid = v < vend && in_row(row, v + q);
+          const uint32_t key = key_of(x[r][q]);
+          if (valid && key >= t_lo && key < t_hi) {
+            if (at < (uint32_t)kRowCand) cand[at] = key;
+            ++at;
+          }
+        }
       }
     }
   }
@@ -405,7 +448,8 @@ __global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
 
   // 3. the threshold key and the number of keys equal to it that are kept
   uint32_t thr, need;
-  if (sure_all < d.k && d.k - sure_all <= nband && nband <= (uint32_t)kRowCand) {
+  const bool in_band = sure_all < d.k && d.k - sure_all <= nband && nband <= (uint32_t)kRowCand;
+  if (in_band) {
     need = d.k - sure_all;
     thr = row_select_lds(cand, nband, need, hist, s_w, s_res);
   } else {
@@ -413,50 +457,100 @@ __global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
     thr = row_select_global(row, vend, need, hist, cand, s_w, s_res);
   }
 
-  // 4. ordered output: per workgroup round, the waves' counts of keys above
-  // and equal to the threshold give each wave's starting position
-  uint32_t run_g = 0, run_e = 0;
+  // 4. ordered output
   double e_kept = 0.0;
   GLOBAL uint32_t* oi = gptr(d.idx_out);
   GLOBAL float* ov = gptr(d.val_out);
-#pragma unroll 1
-  for (uint64_t v0 = 0; v0 < vend; v0 += kRowRound) {
-    f4 x[kRowR];
-#pragma unroll
-    for (int r = 0; r < kRowR; ++r) {
-      const uint64_t v = row_pos(v0, w, r, lane);
-      x[r] = v < vend ? load4(row, v, false) : f4{0.f, 0.f, 0.f, 0.f};
+  if (tally && in_band) {
+    // every chunk's keys above / equal to the threshold from its tallies and
+    // bracket keys, their exclusive prefix in index order, then each wave
+    // writes its chunks on its own
+    const uint32_t per = (uint32_t)((nchunk + kRowBlock - 1) / kRowBlock);
+    const uint32_t c0 = tid * per, c1 = c0 + per < (uint32_t)nchunk ? c0 + per : (uint32_t)nchunk;
+    uint32_t gsum = 0, esum = 0;
+    for (uint32_t c = c0; c < c1; ++c) {
+      const uint32_t tl = s_chunk[2 * c], st = s_chunk[2 * c + 1], nbc = tl >> 16;
+      uint32_t g = tl & 0xFFFFu, e = 0;
+      for (uint32_t i = 0; i < nbc; ++i) {
+        const uint32_t key = cand[st + i];
+        g += key > thr ? 1u : 0u;
+        e += key == thr ? 1u : 0u;
+      }
+      s_chunk[2 * c] = g;
+      s_chunk[2 * c + 1] = e;
+      gsum += g;
+      esum += e;
     }
-    uint32_t cnt = 0;
-#pragma unroll
-    for (int r = 0; r < kRowR; ++r) {
-      const uint64_t v = row_pos(v0, w, r, lane);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const bool valid = v < vend && in_row(row, v + q);
-        const uint32_t key = key_of(x[r][q]);
-        cnt += (valid && key > thr) ? 1u : 0u;
-        cnt += (valid && key == thr) ? 0x10000u : 0u;
+    uint32_t tg, te;
+    const uint32_t gex = row_scan(gsum, s_w, tg) - gsum;
+    const uint32_t eex = row_scan(esum, s_w, te) - esum;
+    {
+      uint32_t rg = gex, re = eex;
+      for (uint32_t c = c0; c < c1; ++c) {
+        const uint32_t g = s_chunk[2 * c], e = s_chunk[2 * c + 1];
+        s_chunk[2 * c] = rg;
+        s_chunk[2 * c + 1] = re;
+        rg += g;
+        re += e;
       }
     }
-    uint32_t wt = cnt;
-#pragma unroll
-    for (int dd = 32; dd >= 1; dd >>= 1) wt += __shfl_xor(wt, dd, 64);
-    if (lane == 0) s_w[w] = wt;
     __syncthreads();
-    uint32_t wex = 0, tot = 0;
-    for (uint32_t i = 0; i < (uint32_t)kRowWaves; ++i) {
-      const uint32_t y = s_w[i];
-      wex += i < w ? y : 0u;
-      tot += y;
+#pragma unroll 1
+    for (uint64_t v0 = 0; v0 < vend; v0 += kRowRound) {
+      const uint64_t chunk = v0 / kRowRound * kRowWaves + w;
+      f4 x[kRowR];
+#pragma unroll
+      for (int r = 0; r < kRowR; ++r) {
+        const uint64_t v = row_pos(v0, w, r, lane);
+        x[r] = v < vend ? load4(row, v, false) : f4{0.f, 0.f, 0.f, 0.f};
+      }
+      uint32_t rg = s_chunk[2 * chunk], re = s_chunk[2 * chunk + 1];
+#pragma unroll
+      for (int r = 0; r < kRowR; ++r)
+        row_write_round(x[r], row_pos(v0, w, r, lane), vend, row, d.base, thr, need, d.k, oi, ov, rg, re, e_kept);
     }
-    __syncthreads();
-    uint32_t rg = run_g + (wex & 0xFFFFu), re = run_e + (wex >> 16);
+  } else {
+    // per workgroup round, the waves' counts give each wave's starting position
+    uint32_t run_g = 0, run_e = 0;
+#pragma unroll 1
+    for (uint64_t v0 = 0; v0 < vend; v0 += kRowRound) {
+      f4 x[kRowR];
 #pragma unroll
-    for (int r = 0; r < kRowR; ++r)
-      row_write_round(x[r], row_pos(v0, w, r, lane), vend, row, d.base, thr, need, d.k, oi, ov, rg, re, e_kept);
-    run_g += tot & 0xFFFFu;
-    run_e += tot >> 16;
+      for (int r = 0; r < kRowR; ++r) {
+        const uint64_t v = row_pos(v0, w, r, lane);
+        x[r] = v < vend ? load4(row, v, false) : f4{0.f, 0.f, 0.f, 0.f};
+      }
+      uint32_t cnt = 0;
+#pragma unroll
+      for (int r = 0; r < kRowR; ++r) {
+        const uint64_t v = row_pos(v0, w, r, lane);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const bool valid = v < vend && in_row(row, v + q);
+          const uint32_t key = key_of(x[r][q]);
+          cnt += (valid && key > thr) ? 1u : 0u;
+          cnt += (valid && key == thr) ? 0x10000u : 0u;
+        }
+      }
+      uint32_t wt = cnt;
+#pragma unroll
+      for (int dd = 32; dd >= 1; dd >>= 1) wt += __shfl_xor(wt, dd, 64);
+      if (lane == 0) s_w[w] = wt;
+      __syncthreads();
+      uint32_t wex = 0, tot = 0;
+      for (uint32_t i = 0; i < (uint32_t)kRowWaves; ++i) {
+        const uint32_t y = s_w[i];
+        wex += i < w ? y : 0u;
+        tot += y;
+      }
+      __syncthreads();
+      uint32_t rg = run_g + (wex & 0xFFFFu), re = run_e + (wex >> 16);
+#pragma unroll
+      for (int r = 0; r < kRowR; ++r)
+        row_write_round(x[r], row_pos(v0, w, r, lane), vend, row, d.base, thr, need, d.k, oi, ov, rg, re, e_kept);
+      run_g += tot & 0xFFFFu;
+      run_e += tot >> 16;
+    }
   }
   const double ek = row_sum_f64(e_kept, s_d);
   if (tid == 0) rc.row_e[2ull * d.eslot + 1] = ek;
