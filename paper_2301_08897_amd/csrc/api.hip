@@ -128,9 +128,11 @@ uint64_t k_rule(uint64_t n, double ratio)
 // Sample: one chunk of kSChunk elements every `stride` elements.
 void sample_geometry(uint64_t n, uint32_t& stride, uint32_t& s_n)
 {
+  // at most one chunk per 65536 elements, at least 1024 chunks while n allows:
+  // a smaller sample widens the bracket and overflows the tiles' regions
   uint64_t st = 65536;
-  if (n / st < 64) {
-    st = (n / 64) / kSChunk * kSChunk;
+  if (n / st < 1024) {
+    st = (n / 1024) / kSChunk * kSChunk;
     if (st < (uint64_t)kSChunk) st = kSChunk;
   }
   const uint64_t chunks = (n + st - 1) / st;
