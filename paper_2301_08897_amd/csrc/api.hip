@@ -76,6 +76,10 @@ struct StreamSet {
   hipEvent_t done[kMaxParts] = {};   // end of each main pass
   hipEvent_t join = nullptr;
   std::mutex launch_mu;      // one call's launch sequence at a time (the events are shared)
+  // per-layer selection: the short layers' rows run on s3 beside the long layers
+  hipStream_t s3 = nullptr;
+  hipEvent_t fork = nullptr, rows_done = nullptr;
+  std::mutex rows_mu;
 };
 constexpr int kMaxGpus = 64;
 StreamSet g_streams[kMaxGpus];
@@ -93,6 +97,9 @@ StreamSet* stream_set()
     for (auto& e : ss.done)
       if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
     if (hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess) return nullptr;
+    if (hipStreamCreateWithFlags(&ss.s3, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&ss.rows_done, hipEventDisableTiming) != hipSuccess) return nullptr;
     ss.ready = true;
   }
   return &ss;
@@ -432,7 +439,7 @@ uint64_t scadles_layers_k(const uint64_t* seg_off, uint32_t L, double ratio)
 // layer's, for layers selected by the multi-launch path) and after it the
 // row region (layer table, row descriptors, per-row energies).
 struct LayersWs {
-  size_t sel = 0, table = 0, rows = 0, row_e = 0, total = 0;
+  size_t sel = 0, table = 0, rows = 0, row_e = 0, e_long = 0, total = 0;
 };
 
 static LayersWs layers_ws(uint32_t K, const uint64_t* seg_off, uint32_t L, const double* ratios)
@@ -448,7 +455,8 @@ static LayersWs layers_ws(uint32_t K, const uint64_t* seg_off, uint32_t L, const
   w.table = w.sel;
   w.rows = align256(w.table + sizeof(uint64_t) * (2ull * L + 1));
   w.row_e = align256(w.rows + sizeof(RowDesc) * (size_t)K * L);
-  w.total = align256(w.row_e + sizeof(double) * 2ull * K * L);
+  w.e_long = align256(w.row_e + sizeof(double) * 2ull * K * L);
+  w.total = align256(w.e_long + sizeof(double) * 2ull * K);
   return w;
 }
 
@@ -480,8 +488,6 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
   std::vector<uint64_t> table(2ull * L + 1, ~0ull);
   for (uint32_t l = 0; l <= L; ++l) table[l] = seg_off[l];
   for (size_t q = 0; q < shorts.size(); ++q) table[L + 1 + shorts[q]] = q;
-  hipError_t e = launch_put_table(table.data(), table.size(), reinterpret_cast<uint64_t*>(base + lw.table), s);
-  if (e != hipSuccess) return hip_fail(e, "layer table");
   RowsCtx rc;
   rc.table = reinterpret_cast<const uint64_t*>(base + lw.table);
   rc.rows = reinterpret_cast<RowDesc*>(base + lw.rows);
@@ -497,14 +503,36 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
     rp.val[j] = val[j];
     rp.ratio[j] = ratios[j];
   }
-  e = launch_rows(rc, rp, energies, s);
+  const bool any_long = rc.Ls < L;
+  // With both kinds of layer, the rows run on the library's third stream
+  // while the long layers' selections run on s (their outputs and workspace
+  // regions are disjoint); the long layers' energies then go to their own
+  // accumulator, and both are summed once s has waited for the rows.
+  StreamSet* ss = (rc.Ls > 0 && any_long) ? stream_set() : nullptr;
+  std::unique_lock<std::mutex> lk;
+  if (ss) lk = std::unique_lock<std::mutex>(ss->rows_mu);
+  hipStream_t sr = ss ? ss->s3 : s;
+  hipError_t e = hipSuccess;
+  if (ss) {
+    e = hipEventRecord(ss->fork, s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(sr, ss->fork, 0);
+    if (e != hipSuccess) return hip_fail(e, "row stream fork");
+  }
+  e = launch_put_table(table.data(), table.size(), reinterpret_cast<uint64_t*>(base + lw.table), sr);
+  if (e != hipSuccess) return hip_fail(e, "layer table");
+  e = launch_rows(rc, rp, ss ? nullptr : energies, sr);
   if (e != hipSuccess) return hip_fail(e, "row selection");
+  if (ss) {
+    e = hipEventRecord(ss->rows_done, sr);
+    if (e != hipSuccess) return hip_fail(e, "row stream join");
+  }
 
   // Longer layers: the multi-launch selection, one layer after the other, its
   // indices offset by the layer's start and its energies added to those of the
   // layers before.
+  double* e_long = ss ? reinterpret_cast<double*>(base + lw.e_long) : energies;
   uint64_t at[kMaxK] = {};          // where layer l's entries start in device j's output
-  bool first = rc.Ls == 0;
+  bool first = ss ? true : rc.Ls == 0;
   for (uint32_t l = 0; l < L; ++l) {
     const uint64_t off = seg_off[l], nl = seg_off[l + 1] - off;
     if (nl <= row_max) {
@@ -526,10 +554,15 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
       a.r_hi[j] = Ll.r_hi[j];
       at[j] += Ll.k[j];
     }
-    if (scadles_status st = run_select(Ll, a, ws, INFINITY, energies, nullptr, s, nullptr, nullptr, nullptr,
+    if (scadles_status st = run_select(Ll, a, ws, INFINITY, e_long, nullptr, s, nullptr, nullptr, nullptr,
                                        (uint32_t)off, !first))
       return st;
     first = false;
+  }
+  if (ss) {
+    e = hipStreamWaitEvent(s, ss->rows_done, 0);
+    if (e == hipSuccess && energies) e = launch_rows_energy(rc, energies, e_long, s);
+    if (e != hipSuccess) return hip_fail(e, "row stream join");
   }
   return SCADLES_OK;
 }

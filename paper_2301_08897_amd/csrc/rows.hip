@@ -556,8 +556,9 @@ __global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
   if (tid == 0) rc.row_e[2ull * d.eslot + 1] = ek;
 }
 
-// Per device: the energies of its short layers summed in layer order.
-__global__ __launch_bounds__(64) void k_rows_energy(RowsCtx rc, double* energies)
+// Per device: the energies of its short layers summed in layer order, plus
+// those of the long layers (`add`, when not null).
+__global__ __launch_bounds__(64) void k_rows_energy(RowsCtx rc, double* energies, const double* add)
 {
   if (threadIdx.x != 0) return;
   const uint32_t j = blockIdx.x;
@@ -566,6 +567,10 @@ __global__ __launch_bounds__(64) void k_rows_energy(RowsCtx rc, double* energies
     if (rc.table[rc.L + 1 + l] == kNotShort) continue;
     ea += rc.row_e[2ull * ((uint64_t)j * rc.L + l)];
     ek += rc.row_e[2ull * ((uint64_t)j * rc.L + l) + 1];
+  }
+  if (add) {
+    ea += add[2 * j];
+    ek += add[2 * j + 1];
   }
   energies[2 * j] = ea;
   energies[2 * j + 1] = ek;
@@ -613,8 +618,14 @@ hipError_t launch_rows(const RowsCtx& rc, const RowsPrep& rp, double* energies, 
   k_rows_prep<<<rc.K, 256, 0, s>>>(rc, rp);
   if (rc.Ls > 0) {
     k_rows<<<rc.Ls * rc.K, kRowBlock, 0, s>>>(rc);
-    if (energies) k_rows_energy<<<rc.K, 64, 0, s>>>(rc, energies);
+    if (energies) k_rows_energy<<<rc.K, 64, 0, s>>>(rc, energies, nullptr);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_rows_energy(const RowsCtx& rc, double* energies, const double* add, hipStream_t s)
+{
+  k_rows_energy<<<rc.K, 64, 0, s>>>(rc, energies, add);
   return hipGetLastError();
 }
 

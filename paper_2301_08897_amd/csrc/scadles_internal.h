@@ -245,6 +245,8 @@ struct DecideArgs {
 };
 hipError_t launch_layers_decide(const DecideArgs& a, hipStream_t s);
 hipError_t launch_rows(const RowsCtx& rc, const RowsPrep& rp, double* energies, hipStream_t s);
+// energies = the short layers' energies (layer order) + add (the long layers', or null)
+hipError_t launch_rows_energy(const RowsCtx& rc, double* energies, const double* add, hipStream_t s);
 
 // k = clamp(floor(ratio * n), 1, n), the same double arithmetic on host and device.
 __host__ __device__ inline uint64_t k_of(uint64_t n, double ratio)
