@@ -79,6 +79,9 @@ struct StreamSet {
   // per-layer selection: the short layers' rows run on s3 beside the long layers
   hipStream_t s3 = nullptr;
   hipEvent_t fork = nullptr, rows_done = nullptr;
+  // long layers: end of a layer's main pass; end of the rest of the last layer
+  // that used each of the two workspace regions
+  hipEvent_t layer_main = nullptr, post_done[2] = {};
   std::mutex rows_mu;
 };
 constexpr int kMaxGpus = 64;
@@ -100,6 +103,9 @@ StreamSet* stream_set()
     if (hipStreamCreateWithFlags(&ss.s3, hipStreamNonBlocking) != hipSuccess) return nullptr;
     if (hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess) return nullptr;
     if (hipEventCreateWithFlags(&ss.rows_done, hipEventDisableTiming) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&ss.layer_main, hipEventDisableTiming) != hipSuccess) return nullptr;
+    for (auto& e : ss.post_done)
+      if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
     ss.ready = true;
   }
   return &ss;
@@ -318,7 +324,8 @@ uint32_t parts_for(const Layout& L)
 scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double delta, double* energies,
                           uint8_t* compressed, hipStream_t s, ProfRec* pr, uint32_t* lb = nullptr,
                           const scadles_step_options* opt = nullptr, uint32_t idx_base = 0,
-                          bool energies_add = false)
+                          bool energies_add = false, hipStream_t s2_detached = nullptr,
+                          hipEvent_t main_done = nullptr)
 {
   Ctx c = make_ctx(L, ws);
   c.delta = delta;
@@ -339,6 +346,13 @@ scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double d
     c.ewma = opt->ewma;
     c.ewma_beta = opt->ewma_beta;
     c.counters = opt->counters;
+  }
+  if (s2_detached) {
+    // one group; the rest after the main pass on s2_detached, not joined
+    p.parts = 1;
+    const hipError_t e = launch_select_detached(c, a, p, s, s2_detached, main_done);
+    if (e != hipSuccess) return hip_fail(e, "select launch");
+    return SCADLES_OK;
   }
   if (pr) pr->parts = p.parts;
   StreamSet* ss = p.parts > 1 ? stream_set() : nullptr;
@@ -451,8 +465,9 @@ static LayersWs layers_ws(uint32_t K, const uint64_t* seg_off, uint32_t L, const
     if (b == 0) return LayersWs{};
     if (b > most) most = b;
   }
+  // two selection regions: consecutive long layers alternate between them
   w.sel = align256(most);
-  w.table = w.sel;
+  w.table = 2 * w.sel;
   w.rows = align256(w.table + sizeof(uint64_t) * (2ull * L + 1));
   w.row_e = align256(w.rows + sizeof(RowDesc) * (size_t)K * L);
   w.e_long = align256(w.row_e + sizeof(double) * 2ull * K * L);
@@ -504,25 +519,28 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
     rp.ratio[j] = ratios[j];
   }
   const bool any_long = rc.Ls < L;
-  // With both kinds of layer, the rows run on the library's third stream
-  // while the long layers' selections run on s (their outputs and workspace
-  // regions are disjoint); the long layers' energies then go to their own
-  // accumulator, and both are summed once s has waited for the rows.
-  StreamSet* ss = (rc.Ls > 0 && any_long) ? stream_set() : nullptr;
+  // With long layers, consecutive long layers pipeline: each one's main pass
+  // runs on s and the rest of its selection on the library's second stream,
+  // the layers alternating between two workspace regions (a region is reused
+  // once the layer before last has finished with it). The rows of the short
+  // layers run on the third stream beside them; the long layers' energies go
+  // to their own accumulator and both are summed once s has waited for all.
+  StreamSet* ss = any_long ? stream_set() : nullptr;
   std::unique_lock<std::mutex> lk;
   if (ss) lk = std::unique_lock<std::mutex>(ss->rows_mu);
-  hipStream_t sr = ss ? ss->s3 : s;
+  const bool rows_beside = ss && rc.Ls > 0;
+  hipStream_t sr = rows_beside ? ss->s3 : s;
   hipError_t e = hipSuccess;
-  if (ss) {
+  if (rows_beside) {
     e = hipEventRecord(ss->fork, s);
     if (e == hipSuccess) e = hipStreamWaitEvent(sr, ss->fork, 0);
     if (e != hipSuccess) return hip_fail(e, "row stream fork");
   }
   e = launch_put_table(table.data(), table.size(), reinterpret_cast<uint64_t*>(base + lw.table), sr);
   if (e != hipSuccess) return hip_fail(e, "layer table");
-  e = launch_rows(rc, rp, ss ? nullptr : energies, sr);
+  e = launch_rows(rc, rp, rows_beside ? nullptr : energies, sr);
   if (e != hipSuccess) return hip_fail(e, "row selection");
-  if (ss) {
+  if (rows_beside) {
     e = hipEventRecord(ss->rows_done, sr);
     if (e != hipSuccess) return hip_fail(e, "row stream join");
   }
@@ -530,9 +548,10 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
   // Longer layers: the multi-launch selection, one layer after the other, its
   // indices offset by the layer's start and its energies added to those of the
   // layers before.
-  double* e_long = ss ? reinterpret_cast<double*>(base + lw.e_long) : energies;
+  double* e_long = rows_beside ? reinterpret_cast<double*>(base + lw.e_long) : energies;
   uint64_t at[kMaxK] = {};          // where layer l's entries start in device j's output
   bool first = ss ? true : rc.Ls == 0;
+  uint32_t li = 0;                  // long layers so far
   for (uint32_t l = 0; l < L; ++l) {
     const uint64_t off = seg_off[l], nl = seg_off[l + 1] - off;
     if (nl <= row_max) {
@@ -554,12 +573,28 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
       a.r_hi[j] = Ll.r_hi[j];
       at[j] += Ll.k[j];
     }
-    if (scadles_status st = run_select(Ll, a, ws, INFINITY, e_long, nullptr, s, nullptr, nullptr, nullptr,
-                                       (uint32_t)off, !first))
+    const uint32_t region = li & 1u;
+    void* wsr = ss ? static_cast<void*>(base + region * lw.sel) : ws;
+    if (ss && li >= 2) {
+      e = hipStreamWaitEvent(s, ss->post_done[region], 0);
+      if (e != hipSuccess) return hip_fail(e, "layer pipeline");
+    }
+    if (scadles_status st = run_select(Ll, a, wsr, INFINITY, e_long, nullptr, s, nullptr, nullptr, nullptr,
+                                       (uint32_t)off, !first, ss ? ss->s2 : nullptr, ss ? ss->layer_main : nullptr))
       return st;
+    if (ss) {
+      e = hipEventRecord(ss->post_done[region], ss->s2);
+      if (e != hipSuccess) return hip_fail(e, "layer pipeline");
+    }
     first = false;
+    ++li;
   }
-  if (ss) {
+  if (ss && li > 0) {
+    // the second stream runs the layers' rests in order: the last one's end is all of them
+    e = hipStreamWaitEvent(s, ss->post_done[(li - 1) & 1u], 0);
+    if (e != hipSuccess) return hip_fail(e, "layer pipeline join");
+  }
+  if (rows_beside) {
     e = hipStreamWaitEvent(s, ss->rows_done, 0);
     if (e == hipSuccess && energies) e = launch_rows_energy(rc, energies, e_long, s);
     if (e != hipSuccess) return hip_fail(e, "row stream join");

@@ -181,6 +181,9 @@ struct SelectPlan {
 // events described at launch_select.
 hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipStream_t s2,
                          hipEvent_t* done, hipEvent_t join, hipEvent_t* ev);
+// All devices in one group; the rest after the main pass on s2, not joined.
+hipError_t launch_select_detached(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s,
+                                  hipStream_t s2, hipEvent_t main_done);
 hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate, bool marks_done, hipStream_t s);
 hipError_t launch_marks(const AggArgs& a, const AggCtx& c, hipStream_t s);
 hipError_t launch_sgd(float* p, const float* g, uint64_t n, float lr, hipStream_t s);

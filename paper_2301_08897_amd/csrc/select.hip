@@ -1428,4 +1428,36 @@ hipError_t launch_select(const Ctx& c0, const PrepArgs& a, const SelectPlan& p, 
   return hipGetLastError();
 }
 
+// The whole selection of all devices with the rest after the main pass on s2
+// and no join: s carries the preparation, bracket and main pass, then records
+// main_done; s2 waits for it and runs the rest. Consecutive calls on
+// alternating workspaces thus overlap a selection's rest with the next one's
+// main pass; the caller orders workspace reuse and the final join.
+hipError_t launch_select_detached(const Ctx& c0, const PrepArgs& a, const SelectPlan& p, hipStream_t s,
+                                  hipStream_t s2, hipEvent_t main_done)
+{
+  Ctx c = c0;
+  c.j0 = 0;
+  c.jn = c.K;
+  const uint64_t zero_words = (uint64_t)c.K * kSlots * kBins;
+  uint32_t gprep = (uint32_t)((zero_words + kBlock * 8 - 1) / (kBlock * 8));
+  gprep = gprep < 1 ? 1 : (gprep > 2048 ? 2048 : gprep);
+  k_prep<<<gprep, kBlock, 0, s>>>(c, a);
+  if (p.any_fast) {
+    for (int pass = 0; pass < kBracketPasses; ++pass) {
+      k_hist_sample<<<dim3(p.sample_blocks, c.K), kBlock, 0, s>>>(c);
+      k_find<<<c.K, 64, 0, s>>>(c, kSlotSampleLo, kSlotSampleHi + 1, pass + 1 == kBracketPasses);
+    }
+  }
+  GradArgs ga;
+  for (uint32_t j = 0; j < c.K; ++j) ga.grad[j] = a.grad[j];
+  k_main<<<c.K * c.tpd, kBlock, 0, s>>>(c, ga);
+  hipError_t e = hipEventRecord(main_done, s);
+  if (e == hipSuccess) e = hipStreamWaitEvent(s2, main_done, 0);
+  if (e != hipSuccess) return e;
+  launch_post(c, p, s2, 0);
+  launch_post(c, p, s2, 1);
+  return hipGetLastError();
+}
+
 }  // namespace scadles
