@@ -137,7 +137,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=16)
     ap.add_argument("--stages", action="store_true", help="also print per-stage milliseconds")
-    ap.add_argument("--parts", type=int, default=2,
+    ap.add_argument("--parts", type=int, default=1,
                     help="device groups whose selections are pipelined (library option 'parts')")
     ap.add_argument("--optimizer", choices=("sgd", "momentum"), default="sgd",
                     help="update after the aggregation: Eqn 4c (default), or momentum SGD 0.9 with weight "

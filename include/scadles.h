@@ -330,11 +330,17 @@ const char* scadles_last_error(void);
  *                       runs the exact multi-pass radix select.
  *   "force_fallback" 1: the sampled path runs but its result is discarded as
  *                       if the bracket had missed, exercising the fallback.
- *   "parts"          1..4 (default 2): device groups whose selections are
+ *   "parts"          1..4 (default 1): device groups whose selections are
  *                       pipelined in scadles_step_fused (group i's main pass
  *                       overlaps the end of group i-1's selection, which runs
  *                       on a second stream the library creates per GPU, at the
  *                       default priority). Results do not depend on it.
+ *   "row_max"        0..2^32-1 (default 2^21): in the per-layer selection,
+ *                       layers of at most this many elements are selected by
+ *                       one workgroup per (device, layer); longer ones by the
+ *                       multi-launch selection, consecutive ones pipelined on
+ *                       the library's second stream and the short layers' rows
+ *                       on a third. Results do not depend on it.
  * Returns SCADLES_EINVAL for an unknown name or a value out of range.       */
 scadles_status scadles_set_option(const char* name, int64_t value);
 

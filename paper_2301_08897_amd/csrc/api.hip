@@ -37,7 +37,7 @@ scadles_status fail(scadles_status st, const char* fmt, ...)
 
 namespace {
 
-std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0}, g_parts{2};
+std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0}, g_parts{1};
 // per-layer selection: layers of at most this many elements go to the row kernels
 std::atomic<int64_t> g_row_max{1 << 21};
 

@@ -63,6 +63,18 @@ def test_workload_runtime_fallback(sc, fallback_mode, config, n, K, iters):
     run_config(sc, config, n=n, K=K, iterations=iters)
 
 
+@pytest.mark.parametrize("parts", [2, 3, 4])
+@pytest.mark.parametrize("config,n,K,iters", [CASES[3], CASES[4]])
+def test_pipelined_device_groups(sc, parts, config, n, K, iters):
+    # devices split into groups whose selections overlap on two streams
+    log(f"parity with {parts} device groups C{config} n={n} K={K}")
+    sc.set_option("parts", parts)
+    try:
+        run_config(sc, config, n=n, K=K, iterations=iters)
+    finally:
+        sc.set_option("parts", 1)
+
+
 def test_per_device_ratios(sc):
     log("parity per-device ratios")
     K = 16
