@@ -4,14 +4,16 @@
 // such rows of all devices in one launch, instead of one multi-launch
 // selection per layer.
 //
-// A row's k-th largest key (31-bit magnitude key, ties to the lower index) is
-// found digit by digit, 12 + 10 + 9 bits: a histogram of the top digit over
-// the row (one read, with sum g^2); once the keys that share the decided
-// digits fit in LDS they are collected there (a second read) and the remaining
-// digits are decided in LDS; a bin too large for LDS is refined by another
-// histogram read instead. A last read writes the kept entries in index order:
-// keys above the threshold, and keys equal to it while fewer than `need` came
-// before.
+// Per row (31-bit magnitude keys, ties to the lower index): a systematic
+// sample brackets the k-th largest key; one read counts the keys above the
+// bracket, gathers the keys inside it into LDS and tallies every wave's chunk;
+// the exact key is selected among the gathered keys digit by digit (12 + 10 +
+// 9 bits) in LDS; a last read writes the kept entries in index order -- keys
+// above the threshold, and keys equal to it while fewer than `need` came
+// before -- each wave at the positions its chunk tallies give. When the
+// bracket misses or overflows LDS, the digits are decided over the whole row
+// (a histogram read per digit until the remaining keys fit in LDS) and the
+// output positions come from a workgroup scan per round.
 #include "frame.h"
 
 namespace scadles {

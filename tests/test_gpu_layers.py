@@ -38,7 +38,8 @@ def layers_vs_oracle(sc, G: np.ndarray, seg_off, ratios, label, modes=("default"
     fn = topk or oracle.topk_layers
     ref = [fn(G[j], seg_off, ratios[j]) for j in range(K)]
     g_dev = torch.from_numpy(G).to(dev)
-    runs = [(m, ROW_MAX_DEFAULT) for m in modes] + [("default", r) for r in row_maxes if r != ROW_MAX_DEFAULT]
+    runs = [(m, ROW_MAX_DEFAULT) for m in modes] + [("default", r) for r in row_maxes
+                                                     if r != ROW_MAX_DEFAULT or not modes]
     for mode, row_max in runs:
         if mode != "default":
             sc.set_option(mode, 1)
@@ -283,3 +284,34 @@ def test_fused_layers_step(sc, config, n, K, iters, beta, optimizer):
     assert np.all(acc[:, 1] == s.iterations)
     sent = acc[:, 0]
     assert np.all(acc[:, 2] == sent * np.array(step.k) + (s.iterations - sent) * s.n)
+
+
+def test_long_row_without_chunk_tallies(sc):
+    # with every layer short, a 3M-element layer is one workgroup's row, too
+    # long for the per-chunk tallies: its output takes the scanned path
+    rng = np.random.default_rng(16)
+    sizes = [3_000_000, 1000]
+    seg_off = np.concatenate([[0], np.cumsum(sizes)]).tolist()
+    G = (rng.standard_normal((2, seg_off[-1])) * rng.uniform(0.1, 2.0, (2, 1))).astype(np.float32)
+    log("layers: one long row without chunk tallies")
+    layers_vs_oracle(sc, G, seg_off, [0.01, 0.2], "long row", topk=oracle.topk_layers_by_threshold,
+                     row_maxes=(2**32 - 1,), modes=())
+
+
+def test_select_layers_without_energies(sc):
+    import ctypes
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(17)
+    seg_off = [0, 5000, 3_000_000, 3_000_100]
+    G = rng.standard_normal((2, seg_off[-1])).astype(np.float32)
+    ref = [oracle.topk_layers(G[j], seg_off, 0.01) for j in range(2)]
+    g_dev = torch.from_numpy(G).to(dev)
+    sel = sc.LayerSelect(g_dev, seg_off, [0.01, 0.01])
+    log("layers without energies")
+    rc = sc._topk_select_layers(sel._grad_ptrs, sel.K, sel._seg, sel._L, sel._ratios, sel._idx_ptrs, sel._val_ptrs,
+                                None, sel.ws.data_ptr(), sel.ws.numel(), torch.cuda.current_stream().cuda_stream)
+    assert rc == 0
+    torch.cuda.synchronize()
+    for j in range(2):
+        assert np.array_equal(sel.idx[j].cpu().numpy(), ref[j][0])
+        assert same_bits(sel.val[j].cpu().numpy(), ref[j][1])
