@@ -288,6 +288,21 @@ def main():
         out["stream"]["simulate_ns_per_device_iteration"] = (time.perf_counter() - h0) * 1e9 / (s.K * 100_000)
     if args.stages:
         out["stage_ms"] = {k: v / max(calls, 1) for k, v in stages.items()}
+    # Eqn 4c on its own (the fused step folds it into the aggregation): reads
+    # params and the aggregate, writes params, 12 n bytes per call
+    dense = step.dense
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(3):
+        sc.apply_sgd(params, dense, 0.0)
+    ev0.record()
+    for _ in range(20):
+        sc.apply_sgd(params, dense, 0.0)
+    ev1.record()
+    torch.cuda.synchronize()
+    sgd_ms = ev0.elapsed_time(ev1) / 20
+    out["sgd_alone"] = {"ms": sgd_ms, "bytes": 12 * s.n, "GBps": 12 * s.n / (sgd_ms * 1e-3) / 1e9,
+                        "frac": 12 * s.n / (sgd_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                        "note": "scadles_apply_sgd on n elements (lr 0), HIP events on the stream it runs on"}
     if not args.no_cpu_baseline:
         del G, step
         torch.cuda.empty_cache()
