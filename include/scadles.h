@@ -113,7 +113,8 @@ scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio,
  * (layer after layer, indices relative to the whole gradient) to idx[j] /
  * val[j]: scadles_layers_k(seg_off, L, ratio_j) entries.
  *   grads     (host[K] of dev pointers, seg_off[L] floats each, 4-byte aligned).
- *   seg_off   (host[L+1]) 0 = seg_off[0] < seg_off[1] < ... < seg_off[L] <= 2^32 - 1; L >= 1.
+ *   seg_off   (host[L+1]) 0 = seg_off[0] < seg_off[1] < ... < seg_off[L] <= 2^32 - 1;
+ *             1 <= L <= 2^24.
  *   ratios    (host[K]) in (0, 1].
  *   idx, val  (host[K] of dev pointers, 4-byte aligned).
  *   energies  (dev, 2K doubles) or NULL: E_all and E_kept of each whole gradient.

@@ -426,9 +426,13 @@ scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio, 
 
 // Layers of a per-layer selection: checks seg_off (0 = off[0] < ... < off[L]
 // <= 2^32 - 1) and returns the kept entries of one device.
+// At most 2^24 layers: keeps every (device, layer) index within 32 bits.
+constexpr uint32_t kMaxLayers = 1u << 24;
+
 static scadles_status check_layers(const uint64_t* seg_off, uint32_t L)
 {
   if (!seg_off || L == 0) return fail(SCADLES_EINVAL, "seg_off must not be NULL and L >= 1");
+  if (L > kMaxLayers) return fail(SCADLES_EINVAL, "L = %u exceeds 2^24 layers", L);
   if (seg_off[0] != 0) return fail(SCADLES_EINVAL, "seg_off[0] must be 0");
   for (uint32_t l = 0; l < L; ++l)
     if (!(seg_off[l] < seg_off[l + 1])) return fail(SCADLES_EINVAL, "layer %u is empty or out of order", l);
@@ -438,7 +442,7 @@ static scadles_status check_layers(const uint64_t* seg_off, uint32_t L)
 
 uint64_t scadles_layers_k(const uint64_t* seg_off, uint32_t L, double ratio)
 {
-  if (!seg_off || L == 0 || seg_off[0] != 0) return 0;
+  if (!seg_off || L == 0 || L > kMaxLayers || seg_off[0] != 0) return 0;
   uint64_t k = 0;
   for (uint32_t l = 0; l < L; ++l) {
     if (!(seg_off[l] < seg_off[l + 1]) || seg_off[L] > 0xFFFFFFFFull) return 0;

@@ -181,6 +181,10 @@ def test_layers_validation_before_any_launch(sc):
     assert call([0, 10], g=(ctypes.c_void_p * 2)(18, 32)) == inval  # misaligned gradient
     assert call([0, 5, 10], ws_bytes=64) == ws
     assert sc._topk_select_layers(grads, 2, None, 1, ratios, idx, val, None, 65536, 1 << 30, None) == inval
+    few = (ctypes.c_uint64 * 2)(0, 10)       # more than 2^24 layers is rejected before seg_off is read
+    assert sc._topk_select_layers(grads, 2, few, (1 << 24) + 1, ratios, idx, val, None, 65536, 1 << 30,
+                                  None) == inval
+    assert sc._layers_k(few, (1 << 24) + 1, 0.5) == 0
 
 
 def test_layers_queries(sc, orc):
