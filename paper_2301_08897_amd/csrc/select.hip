@@ -35,12 +35,25 @@ struct SelView {
   uint32_t lo, hi, shift, width, prefix;
 };
 
-__device__ inline SelView view_of(const Sel& s)
+// Width of the pending digit. The sample selections take 11-bit digits from
+// the top (their bracket stops after kBracketPasses digits); the exact
+// selections take the remainder bits first and 11-bit digits after, the same
+// number of passes with the smallest histogram in the first pass, which sees
+// the most keys and flushes the most bins.
+__device__ inline uint32_t digit_width(uint32_t bits, bool remainder_first)
+{
+  if (bits <= (uint32_t)kDigitBits) return bits;
+  if (!remainder_first) return (uint32_t)kDigitBits;
+  const uint32_t r = bits % (uint32_t)kDigitBits;
+  return r ? r : (uint32_t)kDigitBits;
+}
+
+__device__ inline SelView view_of(const Sel& s, bool remainder_first)
 {
   SelView v;
   v.lo = s.lo;
   v.hi = s.hi;
-  v.width = s.bits < (uint32_t)kDigitBits ? s.bits : (uint32_t)kDigitBits;
+  v.width = digit_width(s.bits, remainder_first);
   v.shift = s.bits - v.width;
   v.prefix = s.prefix;
   return v;
@@ -166,7 +179,7 @@ __global__ __launch_bounds__(kBlock) void k_hist_sample(Ctx c)
   if (!s0.active && !s1.active) return;
   const uint64_t e0 = (uint64_t)blockIdx.x * kSBlk;
   if (e0 >= c.s_n) return;
-  const SelView v0 = view_of(s0), v1 = view_of(s1);
+  const SelView v0 = view_of(s0, false), v1 = view_of(s1, false);
   // both selections at the same digit (always in the first pass): one histogram
   const bool same = s0.active && s1.active && v0.lo == v1.lo && v0.hi == v1.hi && v0.shift == v1.shift &&
                     v0.width == v1.width && v0.prefix == v1.prefix;
@@ -211,7 +224,7 @@ __global__ __launch_bounds__(64) void k_find(Ctx c, int s_begin, int s_end, int 
     Sel sel = c.st[j].sel[s];
     if (!sel.active) continue;
     uint32_t* h = c.hist + ((uint64_t)j * kSlots + s) * kBins;
-    const uint32_t w = sel.bits < (uint32_t)kDigitBits ? sel.bits : (uint32_t)kDigitBits;
+    const uint32_t w = digit_width(sel.bits, s >= kSlotCand);
     const int nb = 1 << w;
     const int per = (nb + 63) / 64;                // bins per lane, at most 32
     const int b_hi = nb - (int)l * per;           // this lane covers bins [b_lo, b_hi), top first
@@ -803,7 +816,7 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
     if (!sel.active) return;
     for (int i = threadIdx.x; i < kBins; i += kBlock) h[i] = 0u;
     __syncthreads();
-    const SelView sv = view_of(sel);
+    const SelView sv = view_of(sel, true);
     const uint32_t t0 = (b * kWaves + (threadIdx.x >> 6)) * kBandTiles;
     if (t0 < c.nslot)
       band_tiles(
@@ -842,7 +855,7 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
       for (int i = threadIdx.x; i < kBins; i += kBlock) h[i] = 0u;
       __syncthreads();
       cur = j;
-      sv = view_of(s.sel[kSlotFull]);
+      sv = view_of(s.sel[kSlotFull], true);
       row = Row{gptr(c.desc[j].grad), c.desc[j].shift, c.n};
     }
     const uint64_t vbase = (uint64_t)blk * kCBlk;
