@@ -315,3 +315,14 @@ def test_select_layers_without_energies(sc):
     for j in range(2):
         assert np.array_equal(sel.idx[j].cpu().numpy(), ref[j][0])
         assert same_bits(sel.val[j].cpu().numpy(), ref[j][1])
+
+
+@pytest.mark.parametrize("K", [1, 64])
+def test_device_count_extremes(sc, K):
+    # one device, and the most devices a call takes, over short and long layers
+    rng = np.random.default_rng(18 + K)
+    seg_off = [0, 3000, 40_000, 2_300_000] if K == 1 else [0, 700, 20_000, 90_000]
+    G = (rng.standard_normal((K, seg_off[-1])) * rng.uniform(0.01, 3.0, (K, 1))).astype(np.float32)
+    ratios = list(rng.choice([0.001, 0.01, 0.1, 0.5], size=K))
+    log(f"layers with K={K}")
+    layers_vs_oracle(sc, G, seg_off, ratios, f"K={K}", topk=oracle.topk_layers_by_threshold, check_aggregate=True)
