@@ -38,7 +38,7 @@ def energy_tol(n: int) -> float:
     return 2.0 * (n + 64) * 2.0**-53
 
 
-def within_north_star_tolerance(x: np.ndarray, ref: np.ndarray) -> bool:
+def within_aggregate_tolerance(x: np.ndarray, ref: np.ndarray) -> bool:
     """|x - ref| <= 1e-7 + 1e-6 |ref| elementwise (the float tolerance of the aggregate)."""
     x = x.astype(np.float64)
     r = ref.astype(np.float64)
@@ -100,7 +100,7 @@ def check_step(sc, s, it, G, out, w, lr, params_before, params_after, delta=math
         sets.append((idx, val) if send else (None, G[j]))
     dense_o = oracle.aggregate(sets, w_o, n)
     dense = out.dense.cpu().numpy()
-    assert within_north_star_tolerance(dense, dense_o), f"{label}: aggregate outside tolerance"
+    assert within_aggregate_tolerance(dense, dense_o), f"{label}: aggregate outside tolerance"
     assert same_bits(dense, dense_o), f"{label}: aggregate not bit-identical to the oracle"
     if params_before is not None and mom is not None:
         mu, wd, v_before, v_after = mom
