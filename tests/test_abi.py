@@ -226,3 +226,24 @@ def test_fused_layers_validation_before_any_launch(sc):
                                  0.1, ctypes.byref(bad), 65536, 1 << 30, None) == inval
     need = sc._step_layers_ws_bytes(2, arr, 1, ratios)
     assert need >= sc.layers_workspace_bytes(2, [0, 10], [0.1, 0.1]) > 0
+
+
+def test_layer_workspace_sizes(sc):
+    import numpy as np
+    rng = np.random.default_rng(3)
+    for _ in range(20):
+        L = int(rng.integers(1, 50))
+        sizes = rng.integers(1, 3_000_000, L)
+        off = [0] + np.cumsum(sizes).tolist()
+        K = int(rng.integers(1, 65))
+        ratios = [float(r) for r in rng.choice([0.001, 0.01, 0.1, 1.0], K)]
+        sel = sc.layers_workspace_bytes(K, off, ratios)
+        arr = (ctypes.c_uint64 * len(off))(*off)
+        rr = (ctypes.c_double * K)(*ratios)
+        step = int(sc._step_layers_ws_bytes(K, arr, L, rr))
+        assert sel > 0 and step > sel
+        # at least two selection regions of the longest layer
+        assert sel >= 2 * sc.workspace_bytes(K, int(max(sizes)), ratios)
+        # more devices never need less
+        if K < 64:
+            assert sc.layers_workspace_bytes(K + 1, off, ratios + [0.01]) >= sel
