@@ -75,6 +75,19 @@ def test_pipelined_device_groups(sc, parts, config, n, K, iters):
         sc.set_option("parts", 1)
 
 
+@pytest.mark.parametrize("mode", ["force_exact", "force_fallback"])
+def test_pipelined_groups_on_the_exact_path(sc, mode):
+    config, n, K, iters = CASES[3]
+    log(f"parity with 2 device groups, {mode}, C{config} n={n} K={K}")
+    sc.set_option("parts", 2)
+    sc.set_option(mode, 1)
+    try:
+        run_config(sc, config, n=n, K=K, iterations=iters)
+    finally:
+        sc.set_option(mode, 0)
+        sc.set_option("parts", 1)
+
+
 def test_per_device_ratios(sc):
     log("parity per-device ratios")
     K = 16
