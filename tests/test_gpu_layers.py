@@ -326,3 +326,39 @@ def test_device_count_extremes(sc, K):
     ratios = list(rng.choice([0.001, 0.01, 0.1, 0.5], size=K))
     log(f"layers with K={K}")
     layers_vs_oracle(sc, G, seg_off, ratios, f"K={K}", topk=oracle.topk_layers_by_threshold, check_aggregate=True)
+
+
+def test_concurrent_callers(sc):
+    """Two host threads, each with its own stream, buffers and workspace, run
+    per-layer selections at once: the library's shared streams and events are
+    used by one call's launch sequence at a time, so both stay exact."""
+    import threading
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(19)
+    seg_off = [0, 4000, 2_500_000, 2_600_000]
+    data = [rng.standard_normal((2, seg_off[-1])).astype(np.float32) for _ in range(2)]
+    refs = [[oracle.topk_layers(G[j], seg_off, 0.01) for j in range(2)] for G in data]
+    sels = [sc.LayerSelect(torch.from_numpy(G).to(dev), seg_off, [0.01, 0.01]) for G in data]
+    torch.cuda.synchronize()
+    errors = []
+
+    def work(t):
+        try:
+            stream = torch.cuda.Stream()
+            with torch.cuda.stream(stream):
+                for _ in range(5):
+                    idx, val, _ = sels[t].run(stream=stream)
+                stream.synchronize()
+            for j in range(2):
+                assert np.array_equal(idx[j].cpu().numpy(), refs[t][j][0]), f"thread {t} device {j}"
+                assert same_bits(val[j].cpu().numpy(), refs[t][j][1]), f"thread {t} device {j}"
+        except Exception as exc:      # reported from the main thread
+            errors.append(exc)
+
+    log("layers from two threads at once")
+    threads = [threading.Thread(target=work, args=(t,)) for t in range(2)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert not errors, errors
