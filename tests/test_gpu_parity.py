@@ -107,3 +107,45 @@ def test_full_size_c1(sc):
     """C1 at its full size with the full-sort oracle."""
     log("parity C1 full size")
     run_config(sc, 1)
+
+
+def test_concurrent_fused_steps_with_groups(sc):
+    """Two host threads run fused steps at once on their own streams with two
+    device groups each (the library's second stream is shared between them)."""
+    import threading
+    import numpy as np
+    import oracle
+    import workloads
+    from _gpu_common import same_bits, torch_dev
+    torch, dev = torch_dev()
+    s = workloads.spec(2, n=300_001, K=4, iterations=1)
+    G = np.stack([workloads.gradient(s, 0, j) for j in range(s.K)])
+    w, _ = sc.stream_weights(s.rates[0], base_batch=s.base_batch)
+    sets = [oracle.topk(G[j], oracle.topk_k(s.n, s.ratios[0, j]))[:2] for j in range(s.K)]
+    dense_o = oracle.aggregate(sets, w, s.n)
+    steps = [sc.FusedStep(torch.from_numpy(G).to(dev), s.ratios[0]) for _ in range(2)]
+    torch.cuda.synchronize()
+    errors = []
+
+    def work(t):
+        try:
+            stream = torch.cuda.Stream()
+            with torch.cuda.stream(stream):
+                for _ in range(5):
+                    out = steps[t].run(w, 0.0, stream=stream)
+                stream.synchronize()
+            assert same_bits(out.dense.cpu().numpy(), dense_o), f"thread {t}: aggregate"
+        except Exception as exc:
+            errors.append(exc)
+
+    log("fused steps from two threads, two device groups")
+    sc.set_option("parts", 2)
+    try:
+        threads = [threading.Thread(target=work, args=(t,)) for t in range(2)]
+        for th in threads:
+            th.start()
+        for th in threads:
+            th.join()
+    finally:
+        sc.set_option("parts", 1)
+    assert not errors, errors
