@@ -67,11 +67,4 @@ __device__ inline bool in_row(const Row& r, uint64_t v) { return v >= r.shift &&
 // on it needs no validity masks: a pad is never above or equal to key + 1 >= 1.
 __device__ inline uint32_t rank_key(float x) { return ((__float_as_uint(x) & kKeyMask) + 1u) & kKeyMask; }
 
-// Plain loads of [e, e+4) of a contiguous, aligned row of `rem` elements
-// (candidate lists); past the end reads the pad pattern.
-__device__ inline f4 load4_guarded(const float* row, uint64_t e, uint64_t rem, bool stream)
-{
-  return load4(Row{gptr(row), 0, rem}, e, stream);
-}
-
 }  // namespace scadles

@@ -320,7 +320,6 @@ __global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
   const uint32_t tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
   const Row row{gptr(d.grad), ((uint64_t)d.grad >> 2) & 3u, d.n};
   const uint64_t vend = (uint64_t)d.n + row.shift;
-  constexpr uint64_t kStep = (uint64_t)kRowBlock * 4;
 
   // 1. sample histogram (13-bit digit, in the candidate array's memory)
   uint32_t* shist = cand;
