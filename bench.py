@@ -155,6 +155,9 @@ def main():
     ap.add_argument("--row-max", type=int, default=None,
                     help="with --topk layers: layers of at most this many elements are selected one workgroup "
                          "per (device, layer) (library option 'row_max')")
+    ap.add_argument("--ewma", type=float, default=None, metavar="BETA",
+                    help="adaptive rule on moving averages of the energies with this factor, and the CNC / "
+                         "floats-sent accounting, inside the fused step (delta stays +inf)")
     ap.add_argument("--evict", action="store_true",
                     help="write 1 GiB of scratch before every timed step (not timed) so that no input sits in "
                          "the 256 MB last-level cache; step times then come from events around each step")
@@ -203,11 +206,13 @@ def main():
         lrs.append(float(np.float32(s.eta * gamma)))
     sc.set_option("parts", args.parts)
     parts = min(args.parts, s.K)
+    extra = {} if args.ewma is None else {"ewma_beta": args.ewma, "track": True}
     if args.optimizer == "momentum":
         mbuf = torch.zeros_like(params)
-        step = sc.FusedStep(G, s.ratios[0], params=params, momentum_buf=mbuf, momentum=0.9, weight_decay=5e-4)
+        step = sc.FusedStep(G, s.ratios[0], params=params, momentum_buf=mbuf, momentum=0.9, weight_decay=5e-4,
+                            **extra)
     else:
-        step = sc.FusedStep(G, s.ratios[0], params=params)
+        step = sc.FusedStep(G, s.ratios[0], params=params, **extra)
     if args.topk == "layers":
         return bench_layers(args, s, sc, torch, G, params, weights, lrs)
     for i in range(args.warmup):
@@ -284,6 +289,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": s.name, "K": s.K, "n": s.n, "ratio": float(s.ratios[0, 0]),
                    "delta": "inf", "iterations": s.iterations, "sgd": True, "cache_evicted": bool(args.evict),
+                   "adaptive": ("moving average, beta %g, with accounting" % args.ewma if args.ewma is not None
+                                else "instantaneous energies"),
                    "optimizer": ("momentum SGD 0.9, weight decay 5e-4" if args.optimizer == "momentum"
                                  else "SGD (Eqn 4c)")},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
