@@ -119,8 +119,14 @@ scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio,
  *   idx, val  (host[K] of dev pointers, 4-byte aligned).
  *   energies  (dev, 2K doubles) or NULL: E_all and E_kept of each whole gradient.
  *   ws        scadles_layers_workspace_bytes(K, seg_off, L, ratios) bytes.
- * The layers are selected one after the other; feed the sets to
- * scadles_weighted_aggregate for Eqn 4b. Same error convention as above.    */
+ * Layers of at most "row_max" elements (scadles_set_option) are selected one
+ * workgroup per (device, layer), all at once; longer ones by the selection of
+ * scadles_topk_select, one layer after the other, overlapped with each other
+ * on a second and third stream the library creates per GPU (default
+ * priority; the caller's stream waits for them before the call's work ends
+ * on it). Results do not depend on this split. Feed the sets to
+ * scadles_weighted_aggregate for Eqn 4b, or use scadles_step_fused_layers.
+ * Same error convention as above.                                           */
 uint64_t scadles_layers_k(const uint64_t* seg_off, uint32_t L, double ratio);
 size_t scadles_layers_workspace_bytes(uint32_t K, const uint64_t* seg_off, uint32_t L, const double* ratios);
 scadles_status scadles_topk_select_layers(const float* const* grads, uint32_t K, const uint64_t* seg_off,
