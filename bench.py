@@ -39,10 +39,10 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(s, it):
+def algorithmic_bytes(sc, s, it):
     """Bytes the method itself must move in one step (select + compact + aggregate):
     read every gradient once, write the (idx, val) pairs, write the dense aggregate."""
-    ks = sum(s.k(it, j) for j in range(s.K))
+    ks = sum(sc.topk_k(s.n, s.ratios[it, j]) for j in range(s.K))
     return 4 * s.K * s.n + 8 * ks + 4 * s.n
 
 
@@ -75,7 +75,7 @@ def cpu_baseline(s, threads):
     S = max(1, min(s.K, threads))
     G = np.empty((S, s.n), dtype=np.float32)
     for j in range(S):
-        workloads.gradient(s, 0, j, out=G[j])
+        workloads.gradient(s, 0, j, out=G[j], k=oracle.topk_k(s.n, s.ratios[0, j]))
     rates = s.rates[0, :S]
     t0 = time.perf_counter()
     w, gamma = oracle.stream_weights(rates, base_batch=s.base_batch)
@@ -183,7 +183,7 @@ def main():
     G = torch.empty((s.K, s.n), dtype=torch.float32, device=dev)
     host = np.empty(s.n, dtype=np.float32)
     for j in range(s.K):
-        workloads.gradient(s, 0, j, out=host)
+        workloads.gradient(s, 0, j, out=host, k=sc.topk_k(s.n, s.ratios[0, j]))
         G[j].copy_(torch.from_numpy(host))
     params = torch.from_numpy(workloads.params0(s)).to(dev)
     torch.cuda.synchronize()
@@ -268,7 +268,7 @@ def main():
     launch_ms = stages["main_select"] / max(calls, 1) / parts
     launch_bytes = 4 * s.K * s.n / parts
     achieved = launch_bytes / (launch_ms * 1e-3) / 1e9
-    alg = np.mean([algorithmic_bytes(s, i % s.iterations) for i in range(args.steps)])
+    alg = np.mean([algorithmic_bytes(sc, s, i % s.iterations) for i in range(args.steps)])
     sel_ms = stages["total"] / max(calls, 1)
     traffic = traffic_entry(parts)
 

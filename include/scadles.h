@@ -276,7 +276,7 @@ scadles_status scadles_stream_weights(const double* rates, uint32_t K, double b_
                                       double* gamma);
 
 /* ---- streaming buffers, batch sizes, weights and learning-rate scale --------
- * The step before the aggregation (§III-A, Eqns 2 and 3; §IV "Heterogeneous
+ * The step before the aggregation (§II-C, Eqns 2 and 3; §IV "Heterogeneous
  * streams" and "Limited memory and storage"): device j receives a continuous
  * stream of S_j samples per second into its buffer and trains one iteration
  * of t_j seconds on a batch of b_j = clamp(S_j, b_min, b_max) samples, or on

@@ -189,6 +189,18 @@ def energies(g: np.ndarray, idx: np.ndarray):
     return float(np.sum(g64 * g64)), float(np.sum(g64[idx] * g64[idx]))
 
 
+def energies_extended(g: np.ndarray, idx: np.ndarray):
+    """The same two energies (§IV) as references for comparing double sums taken
+    in other orders: every square of a float is exact in double, and both sums
+    run in numpy's long double (64-bit significand on x86-64), so a sum of m
+    terms is within (m - 1) * 2^-64 of its exact value relative to it, far below
+    the error any order of double additions may have. Returns np.longdouble."""
+    if np.finfo(np.longdouble).nmant < 63:
+        raise RuntimeError("long double has no 64-bit significand on this host")
+    sq = np.square(np.asarray(g, dtype=np.float32), dtype=np.float64)
+    return np.sum(sq, dtype=np.longdouble), np.sum(sq[np.asarray(idx, dtype=np.int64)], dtype=np.longdouble)
+
+
 def compress_decision(e_all: float, e_kept: float, delta: float):
     """Adaptive rule of §IV. Returns (send_topk: bool, energy-loss ratio)."""
     rho = ctypes.c_double()
@@ -302,7 +314,7 @@ PERSISTENCE, TRUNCATION = 0, 1
 
 
 def stream_run(rates, iter_us, b_min: int, b_max: int, policy: int, T: int):
-    """Streaming buffers of K devices over T iterations (§III-A Eqn 2, §IV buffer
+    """Streaming buffers of K devices over T iterations (§II-C Eqn 2, §IV buffer
     policies and batch rule). ``rates``: samples/s per device, ``iter_us``:
     iteration time per device in microseconds (integers). Returns (queued
     uint64[T+1, K], batch uint64[T, K], dropped uint64[K])."""

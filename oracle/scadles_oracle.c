@@ -267,7 +267,7 @@ int oracle_stream_weights(const double* rates, uint32_t K, double b_min, double 
   return 0;
 }
 
-/* Streaming buffers of K devices over T training iterations (§III-A, Eqn 2;
+/* Streaming buffers of K devices over T training iterations (§II-C, Eqn 2;
  * §IV "Limited memory and storage": the persistence and truncation policies;
  * §IV "Heterogeneous streams": the batch rule b = S bounded to [b_min, b_max]).
  * Device j streams rate[j] samples per second; one iteration lasts iter_us[j]

@@ -509,15 +509,12 @@ class FusedStep:
                                _stream_ptr(stream)))
         return StepOutputs(self.idx, self.val, self.dense, self.energies, self.compressed)
 
-
     def accounting(self):
-        """Per device (iterations that sent Top-k, iterations, floats sent) and the
-        CNC ratio of §V-G, from the counters (``track=True``)."""
+        """The counters of ``track=True`` as uint64[K, 3]: per device the iterations
+        that sent Top-k, the iterations, and the floats sent (§V-G)."""
         if self.counters is None:
             raise ValueError("construct with track=True")
-        c = self.counters.cpu().numpy().reshape(self.K, 3)
-        cnc = [float(r[0]) / float(r[1]) if r[1] else 0.0 for r in c]
-        return c, cnc
+        return self.counters.cpu().numpy().reshape(self.K, 3).astype(np.uint64)
 
 
 def step_fused(grads, ratios, weights, *, delta: float = math.inf, params=None, lr: float = 0.0,

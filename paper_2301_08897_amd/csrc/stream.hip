@@ -1,6 +1,6 @@
 // stream.hip -- the streaming buffers of the devices and what each iteration
 // takes from them: batch sizes, Eqn 4a weights and the learning-rate scale
-// (§III-A Eqns 2-3, §IV). Host only: nothing here touches GPU state.
+// (§II-C Eqns 2-3, §IV). Host only: nothing here touches GPU state.
 #include <cmath>
 #include <cstdint>
 #include <limits>

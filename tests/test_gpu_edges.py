@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 import oracle
-from _gpu_common import energy_tol, log, same_bits, torch_dev
+from _gpu_common import check_energies, log, same_bits, torch_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -25,6 +25,8 @@ def topk_vs_oracle(sc, g: np.ndarray, ratio: float, label: str):
     torch, dev = torch_dev()
     k = oracle.topk_k(g.size, ratio)
     idx_o, val_o, ea, ek = oracle.topk(g, k)
+    ref = oracle.energies_extended(g, idx_o)
+    check_energies(f"{label} (oracle)", ea, ek, ref, g.size, k)
     for mode in ("default", "force_exact", "force_fallback"):
         if mode != "default":
             sc.set_option(mode, 1)
@@ -37,8 +39,7 @@ def topk_vs_oracle(sc, g: np.ndarray, ratio: float, label: str):
         assert np.array_equal(idx.cpu().numpy(), idx_o), f"{label} [{mode}]: indices"
         assert same_bits(val.cpu().numpy(), val_o), f"{label} [{mode}]: values"
         e = en.cpu().numpy()
-        tol = energy_tol(g.size) * max(ea, 1e-300)
-        assert abs(e[0] - ea) <= tol and abs(e[1] - ek) <= tol, label
+        check_energies(f"{label} [{mode}]", e[0], e[1], ref, g.size, k)
 
 
 SIZES = [1, 2, 3, 4, 5, 255, 1023, 1024, 1025, 16383, 16384, 16385, 65535, 65536, 65537, 131072 + 77,
@@ -234,7 +235,8 @@ def test_determinism(sc):
     torch, dev = torch_dev()
     import workloads
     s = workloads.spec(4, n=2_000_003, K=16)
-    G = torch.from_numpy(np.stack([workloads.gradient(s, 0, j) for j in range(s.K)])).to(dev)
+    G = torch.from_numpy(np.stack([workloads.gradient(s, 0, j, k=oracle.topk_k(s.n, s.ratios[0, j]))
+                                   for j in range(s.K)])).to(dev)
     w, _ = sc.stream_weights(s.rates[0])
     step = sc.FusedStep(G, s.ratios[0], delta=0.5)
     ref = None

@@ -2,14 +2,15 @@
 own top fraction, the per-layer reading of the Top-k of §IV): the workloads'
 own layer layouts, tiny and ragged layers, ties across layer bounds, every
 selection path, and the layered sets fed to the Eqn 4b aggregation. Indices
-and values bit for bit; energies within the bound of two double sums."""
+and values bit for bit; energies within the bound of a double sum of their
+terms in any order, against extended-precision references."""
 
 import numpy as np
 import pytest
 
 import oracle
 import workloads
-from _gpu_common import energy_tol, log, same_bits, torch_dev
+from _gpu_common import check_energies, decision_window, log, same_bits, torch_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -37,6 +38,9 @@ def layers_vs_oracle(sc, G: np.ndarray, seg_off, ratios, label, modes=("default"
     K = G.shape[0]
     fn = topk or oracle.topk_layers
     ref = [fn(G[j], seg_off, ratios[j]) for j in range(K)]
+    refs = [oracle.energies_extended(G[j], ref[j][0]) for j in range(K)]
+    for j in range(K):
+        check_energies(f"{label} device {j} (oracle)", ref[j][2], ref[j][3], refs[j], G.shape[1], ref[j][0].size)
     g_dev = torch.from_numpy(G).to(dev)
     runs = [(m, ROW_MAX_DEFAULT) for m in modes] + [("default", r) for r in row_maxes
                                                      if r != ROW_MAX_DEFAULT or not modes]
@@ -61,9 +65,8 @@ def layers_vs_oracle(sc, G: np.ndarray, seg_off, ratios, label, modes=("default"
                 bad = np.flatnonzero(got != idx_o) if got.shape == idx_o.shape else "length"
                 raise AssertionError(f"{label} [{mode}] device {j}: indices (first mismatch {bad[:5]})")
             assert same_bits(val[j].cpu().numpy(), val_o), f"{label} [{mode}] device {j}: values"
-            tol = energy_tol(G.shape[1]) * max(ea, 1e-300)
-            assert abs(e[2 * j] - ea) <= tol, f"{label} [{mode}] device {j}: E_all"
-            assert abs(e[2 * j + 1] - ek) <= tol, f"{label} [{mode}] device {j}: E_kept"
+            check_energies(f"{label} [{mode}] device {j}", e[2 * j], e[2 * j + 1], refs[j], G.shape[1],
+                           idx_o.size)
         if check_aggregate:
             w, _ = sc.stream_weights(np.arange(1.0, K + 1.0))
             dense = sc.weighted_aggregate(list(zip(idx, val)), w, G.shape[1])
@@ -82,7 +85,7 @@ def test_workload_layers(sc, config, n, K):
     log(f"layers C{config} n={s.n} K={s.K} L={len(seg_off) - 1}")
     G = np.empty((s.K, s.n), dtype=np.float32)
     for j in range(s.K):
-        workloads.gradient(s, 0, j, out=G[j])
+        workloads.gradient(s, 0, j, out=G[j], k=oracle.topk_k(s.n, s.ratios[0, j]))
     layers_vs_oracle(sc, G, seg_off, list(s.ratios[0]), f"C{config} layers", modes=MODES,
                      check_aggregate=True)
 
@@ -150,7 +153,10 @@ def test_one_layer_matches_whole_vector(sc):
     assert np.array_equal(idx[0].cpu().numpy(), idx1.cpu().numpy())
     assert same_bits(val[0].cpu().numpy(), val1.cpu().numpy())
     e, e1 = en.cpu().numpy(), en1.cpu().numpy()
-    assert np.all(np.abs(e - e1) <= energy_tol(n) * e1[0])
+    k = idx1.numel()
+    ref = oracle.energies_extended(g, idx1.cpu().numpy())
+    check_energies("one layer", e[0], e[1], ref, n, k)
+    check_energies("whole vector", e1[0], e1[1], ref, n, k)
 
 
 def test_repeated_runs_reuse_workspace(sc):
@@ -183,37 +189,57 @@ def test_layers_validation(sc):
 
 
 @pytest.mark.slow
-def test_full_size_vgg19_layers(sc):
+@pytest.mark.timeout(900)
+def test_full_size_vgg19_layers_fused(sc):
     """The largest workload (32 devices x 143,667,240, its 38 layers) at ratio
-    0.01, against the O(n) oracle on sampled devices (every device's kept
-    count and order checked)."""
+    0.01 in the launch configuration the benchmark times: the fused per-layer
+    step (selection, the rule of §IV at delta = +inf, Eqn 4b, Eqn 4c) over two
+    consecutive iterations, every device's kept set against the O(n) oracle,
+    the aggregate and the update bit for bit."""
+    from concurrent.futures import ThreadPoolExecutor
     torch, dev = torch_dev()
-    s = workloads.spec(5, iterations=1)
+    s = workloads.spec(5, iterations=2)
     seg_off = [0] + [int(x) for x in s.seg_end]
-    log(f"full-size layers C5 n={s.n} K={s.K} L={len(seg_off) - 1}")
+    log(f"full-size fused layers C5 n={s.n} K={s.K} L={len(seg_off) - 1}")
     G = torch.empty((s.K, s.n), dtype=torch.float32, device=dev)
+    params = workloads.params0(s)
+    p_dev = torch.from_numpy(params).to(dev)
+    p_ref = params
     host = np.empty(s.n, dtype=np.float32)
-    sampled = {0: None, 13: None, 31: None}
-    for j in range(s.K):
-        workloads.gradient(s, 0, j, out=host)
-        G[j].copy_(torch.from_numpy(host))
-        if j in sampled:
-            sampled[j] = host.copy()
-    sel = sc.LayerSelect(G, seg_off, list(s.ratios[0]))
-    idx, val, en = sel.run()
-    torch.cuda.synchronize()
-    k = oracle.layers_k(seg_off, s.ratios[0, 0])
-    for j in range(s.K):
-        got = idx[j].cpu().numpy()
-        assert got.size == k and np.all(np.diff(got.astype(np.int64)) > 0), f"device {j}: order"
-    e = en.cpu().numpy()
-    for j, g in sampled.items():
-        log(f"  oracle device {j}")
-        idx_o, val_o, ea, ek = oracle.topk_layers_by_threshold(g, seg_off, s.ratios[0, j])
-        assert np.array_equal(idx[j].cpu().numpy(), idx_o), f"device {j}: indices"
-        assert same_bits(val[j].cpu().numpy(), val_o), f"device {j}: values"
-        tol = energy_tol(s.n) * ea
-        assert abs(e[2 * j] - ea) <= tol and abs(e[2 * j + 1] - ek) <= tol, f"device {j}: energies"
+    step = None
+    for it in range(s.iterations):
+        for j in range(s.K):
+            workloads.gradient(s, it, j, out=host)
+            G[j].copy_(torch.from_numpy(host))
+        if step is None:
+            step = sc.FusedStep(G, s.ratios[0], params=p_dev, seg_off=seg_off)
+        w, gam = sc.stream_weights(s.rates[it], base_batch=s.base_batch)
+        lr = float(np.float32(s.eta * gam))
+        out = step.run(w, lr)
+        torch.cuda.synchronize()
+        log(f"  iteration {it}: step done, oracle on every device")
+
+        def one(j):
+            g = workloads.gradient(s, it, j, nthreads=2)
+            idx, val, ea, ek = oracle.topk_layers_by_threshold(g, seg_off, s.ratios[it, j])
+            return idx, val, ea, ek, oracle.energies_extended(g, idx)
+
+        with ThreadPoolExecutor(8) as ex:
+            res = list(ex.map(one, range(s.K)))
+        e = out.energies.cpu().numpy()
+        assert np.all(out.compressed.cpu().numpy() == 1), "delta = +inf always sends Top-k"
+        sets = []
+        for j, (idx, val, ea, ek, ref) in enumerate(res):
+            assert np.array_equal(out.idx[j].cpu().numpy(), idx), f"iteration {it} device {j}: indices"
+            assert same_bits(out.val[j].cpu().numpy(), val), f"iteration {it} device {j}: values"
+            check_energies(f"iteration {it} device {j} (oracle)", ea, ek, ref, s.n, idx.size)
+            check_energies(f"iteration {it} device {j}", e[2 * j], e[2 * j + 1], ref, s.n, idx.size)
+            sets.append((idx, val))
+        dense_o = oracle.aggregate(sets, w, s.n)
+        assert same_bits(out.dense.cpu().numpy(), dense_o), f"iteration {it}: aggregate"
+        p_ref = oracle.sgd(p_ref, dense_o, lr)
+        assert same_bits(p_dev.cpu().numpy(), p_ref), f"iteration {it}: update"
+        del res, sets, dense_o
 
 
 @pytest.mark.parametrize("config,n,K,iters,beta,optimizer", [(5, 1_500_001, 6, 3, 0.5, "sgd"),
@@ -229,7 +255,7 @@ def test_fused_layers_step(sc, config, n, K, iters, beta, optimizer):
     log(f"fused layers C{config} n={s.n} K={s.K} L={len(seg_off) - 1} beta={beta} {optimizer}")
     G = np.empty((s.K, s.n), dtype=np.float32)
     for j in range(s.K):
-        workloads.gradient(s, 0, j, out=G[j])
+        workloads.gradient(s, 0, j, out=G[j], k=oracle.topk_k(s.n, s.ratios[0, j]))
     sets0 = [oracle.topk_layers(G[j], seg_off, s.ratios[0, j]) for j in range(s.K)]
     rho = sorted(oracle.compress_decision(r[2], r[3], 0.0)[1] for r in sets0)
     delta = 0.5 * (rho[len(rho) // 2 - 1] + rho[len(rho) // 2])
@@ -244,11 +270,10 @@ def test_fused_layers_step(sc, config, n, K, iters, beta, optimizer):
     v_ref = np.zeros(s.n, dtype=np.float32)
     state = np.zeros((s.K, 2))
     counters = np.zeros((s.K, 3), dtype=np.uint64)
-    tol = energy_tol(s.n)
     for it in range(s.iterations):
         if it:
             for j in range(s.K):
-                workloads.gradient(s, it, j, out=G[j])
+                workloads.gradient(s, it, j, out=G[j], k=oracle.topk_k(s.n, s.ratios[it, j]))
             g_dev.copy_(torch.from_numpy(G))
         res = sets0 if it == 0 else [oracle.topk_layers(G[j], seg_off, s.ratios[it, j]) for j in range(s.K)]
         w, gamma = sc.stream_weights(s.rates[it], base_batch=s.base_batch)
@@ -261,15 +286,16 @@ def test_fused_layers_step(sc, config, n, K, iters, beta, optimizer):
         for j, (idx, val, e_all, e_kept) in enumerate(res):
             assert np.array_equal(out.idx[j].cpu().numpy(), idx), f"iteration {it} device {j}: indices"
             assert same_bits(out.val[j].cpu().numpy(), val), f"iteration {it} device {j}: values"
-            assert abs(e[2 * j] - e_all) <= tol * e_all and abs(e[2 * j + 1] - e_kept) <= tol * e_all
+            check_energies(f"iteration {it} device {j}", e[2 * j], e[2 * j + 1],
+                           oracle.energies_extended(G[j], idx), s.n, idx.size)
             if beta is None:
                 send, r = oracle.compress_decision(e_all, e_kept, delta)
             else:
                 send = oracle.adaptive_step(state[j], counters[j], e_all, e_kept, beta, delta,
                                             oracle.layers_k(seg_off, s.ratios[it, j]), s.n)
                 r = oracle.compress_decision(state[j][0], state[j][1], 0.0)[1]
-            if abs(r - delta) <= 8 * (it + 1) * tol:
-                send = bool(got[j])               # at the boundary either answer is correct
+            if abs(r - delta) <= decision_window(s.n, idx.size, updates=0 if beta is None else it + 1):
+                send = bool(got[j])               # within rounding of delta either answer is correct
             assert bool(got[j]) == send, f"iteration {it} device {j}: decision"
             sets.append((idx, val) if send else (None, G[j]))
         dense_o = oracle.aggregate(sets, w, s.n)
@@ -280,7 +306,7 @@ def test_fused_layers_step(sc, config, n, K, iters, beta, optimizer):
         else:
             p_ref = oracle.sgd(p_ref, dense_o, lr)
         assert same_bits(p_dev.cpu().numpy(), p_ref), f"iteration {it}: update"
-    acc, _ = step.accounting()
+    acc = step.accounting()
     assert np.all(acc[:, 1] == s.iterations)
     sent = acc[:, 0]
     assert np.all(acc[:, 2] == sent * np.array(step.k) + (s.iterations - sent) * s.n)

@@ -202,3 +202,40 @@ def test_sgd(orc):
         exact = Fraction(float(p[i])) - Fraction(float(lr)) * Fraction(float(g[i]))
         assert abs(Fraction(float(q[i])) - exact) <= Fraction(float(np.spacing(np.float32(abs(float(exact))))))
     assert np.all(q[g > 0] < p[g > 0]) and np.all(q[g < 0] > p[g < 0])
+
+
+def test_extended_energies_against_exact_sums(orc):
+    """The long-double energy references used to bound the kernels' double sums:
+    within (m - 1) 2^-64 of the exact rational sum of the squares, including
+    denormals and signed zeros, and far inside any double summation's bound."""
+    from fractions import Fraction
+    rng = np.random.default_rng(21)
+    for n in (1, 2, 7, 300, 4097):
+        g = (rng.standard_normal(n) * 10.0 ** rng.uniform(-6, 1, n)).astype(np.float32)
+        if n > 4:
+            g[:3] = np.array([np.float32(1e-40), -0.0, np.float32(-3e-39)], dtype=np.float32)
+        idx = np.sort(rng.choice(n, size=max(1, n // 5), replace=False)).astype(np.uint32)
+        ea, ek = orc.energies_extended(g, idx)
+        exact_a = sum(Fraction(float(x)) ** 2 for x in g)
+        exact_k = sum(Fraction(float(g[i])) ** 2 for i in idx)
+        for got, exact, m in ((ea, exact_a, n), (ek, exact_k, idx.size)):
+            err = abs(Fraction(float(got)) - exact) if exact else abs(Fraction(float(got)))
+            # the long double result is rounded once more to double for the comparison
+            assert err <= (max(m - 1, 0) * 2.0**-64 + 2.0**-53) * float(exact) + 0.0, (n, m)
+        # against a correctly rounded double sum
+        sq = np.square(g.astype(np.float64))
+        assert abs(float(ea) - math.fsum(sq)) <= (n * 2.0**-64 + 2.0**-52) * math.fsum(sq)
+
+
+def test_extended_energies_catch_a_dropped_term(orc):
+    """A reference that dropped one kept square would fail the bound of the
+    comparisons at once (the bound is ~m 2^-53 relative, a term is far larger)."""
+    rng = np.random.default_rng(22)
+    g = rng.standard_normal(100_000).astype(np.float32)
+    k = orc.topk_k(g.size, 0.01)
+    idx, _, ea, ek = orc.topk(g, k)
+    ra, rk = orc.energies_extended(g, idx)
+    bound = 2 * k * 2.0**-53 * float(rk)
+    assert abs(ek - float(rk)) <= bound
+    _, rk_short = orc.energies_extended(g, idx[1:])
+    assert abs(ek - float(rk_short)) > bound

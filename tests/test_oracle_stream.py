@@ -1,4 +1,4 @@
-"""Pins of the oracle's streaming-buffer simulation (§III-A Eqns 2 and 3, the
+"""Pins of the oracle's streaming-buffer simulation (§II-C Eqns 2 and 3, the
 buffer policies and batch rule of §IV, Table II).
 
 Checked against: the closed form of Eqn 2 (exact for a continuous stream as
@@ -101,7 +101,7 @@ def test_eqn2_fractional_arrivals(orc):
 
 def test_eqn3_reproduces_table_ii(orc):
     # Eqn 3 (b negligible beside t S): Q = T t S + S; with b = 0 the
-    # simulation is exactly that, and at the sample size of Section V-C it
+    # simulation is exactly that, and at the sample size of Section V-F it
     # gives Table II in GiB
     g = json.load(open(GOLDEN))["table_ii_data_accumulated_GiB"]
     for e in g["entries"]:

@@ -1,5 +1,5 @@
 """The library's streaming buffers, batch sizes, weights and learning-rate
-scale (§III-A Eqns 2-3, §IV) against the oracle: host-only code, so these run
+scale (§II-C Eqns 2-3, §IV) against the oracle: host-only code, so these run
 without a GPU. Integers bit for bit; weights bit for bit against the oracle's
 Eqn 4a on the same batches."""
 import math

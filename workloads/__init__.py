@@ -179,9 +179,6 @@ class Spec:
     seed: int = 0
     notes: dict = field(default_factory=dict)
 
-    def k(self, it: int, j: int) -> int:
-        r = float(self.ratios[it, j])
-        return max(1, min(self.n, int(math.floor(r * self.n))))
 
 
 # Full-size shapes of the five workloads.
@@ -273,8 +270,13 @@ def spec(config: int, n: int | None = None, K: int | None = None,
 
 
 def gradient(s: Spec, it: int, j: int, out: np.ndarray | None = None,
-             nthreads: int | None = None) -> np.ndarray:
-    """Device j's gradient at iteration `it` (float32[n])."""
+             nthreads: int | None = None, k: int | None = None) -> np.ndarray:
+    """Device j's gradient at iteration `it` (float32[n]). A workload with tied
+    magnitudes (s.p_tie > 0) places them at the ceil(k/2)-th largest magnitude,
+    so that they straddle the Top-k boundary: its caller passes k, the number
+    of entries kept at this device's ratio (this module holds no k rule)."""
+    if s.p_tie > 0.0 and k is None:
+        raise ValueError(f"{s.name}: pass k (the kept count at ratio {s.ratios[it, j]}) to place the ties")
     lib = _load()
     if out is None:
         out = np.empty(s.n, dtype=np.float32)
@@ -291,8 +293,7 @@ def gradient(s: Spec, it: int, j: int, out: np.ndarray | None = None,
         if s.p_tie > 0.0:
             # Tie magnitude m*: the ceil(k/2)-th largest |g| before the ties go in,
             # so that the tied block straddles the Top-k boundary.
-            k = s.k(it, j)
-            r = (k + 1) // 2
+            r = (int(k) + 1) // 2
             mag = np.abs(out)
             m_star = float(np.partition(mag, s.n - r)[s.n - r])
             del mag
