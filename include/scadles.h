@@ -53,7 +53,9 @@ typedef enum {
   SCADLES_EHIP = 3,        /* the HIP runtime reported an error while launching        */
   SCADLES_EUNSORTED = 4,   /* validation mode only: a sparse set's idx is not strictly
                               ascending or holds an entry >= n                          */
-  SCADLES_EINTERNAL = 5    /* internal consistency check failed                        */
+  SCADLES_EINTERNAL = 5    /* validation mode only: an internal consistency check of a
+                              selection failed (a radix pass missed, the threshold was
+                              not found, or the kept count is not k)                   */
 } scadles_status;
 
 /* Largest number of devices one call accepts. */
@@ -332,7 +334,15 @@ scadles_status scadles_stream_simulate(uint32_t K, const uint64_t* rate, const u
 const char* scadles_last_error(void);
 
 /* Process-wide options, for testing and diagnosis:
- *   "validate"       1: scadles_weighted_aggregate checks its sets (syncs).
+ *   "validate"       1: scadles_weighted_aggregate checks its sets, and
+ *                       scadles_topk_select, scadles_step_fused and
+ *                       scadles_step_fused_ex read every device's selection
+ *                       state back after the call and return
+ *                       SCADLES_EINTERNAL if its internal checks failed
+ *                       (all of these then synchronise `stream`).
+ *   "inject_count_error" 1 (testing): the whole-vector selection reports a
+ *                       failed count check for device 0 (its outputs are
+ *                       unaffected), to exercise the validation above.
  *   "force_exact"    1: Top-k skips the sampled single-read path and always
  *                       runs the exact multi-pass radix select.
  *   "force_fallback" 1: the sampled path runs but its result is discarded as

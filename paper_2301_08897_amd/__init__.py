@@ -459,6 +459,20 @@ class FusedStep:
         self._grad_ptrs = (_vp * self.K)(*[g.data_ptr() for g in self.grads])
         self._w = (ctypes.c_float * self.K)()
 
+    def set_grads(self, grads):
+        """Point the step at other gradients of the same shape (marshalling only)."""
+        torch = _torch()
+        if isinstance(grads, torch.Tensor) and grads.dim() == 2:
+            grads = [grads[j] for j in range(grads.shape[0])]
+        if len(grads) != self.K:
+            raise ValueError("one gradient per device")
+        for j, g in enumerate(grads):
+            _dev_f32(g, f"grads[{j}]")
+            if g.numel() != self.n:
+                raise ValueError("all gradients must have n elements")
+        self.grads = list(grads)
+        self._grad_ptrs = (_vp * self.K)(*[g.data_ptr() for g in self.grads])
+
     def set_ratios(self, ratios):
         torch = _torch()
         ratios = [float(r) for r in ratios]

@@ -247,13 +247,15 @@ __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
   }
 }
 
-// Eqn 4c on its own: p <- p - lr * g, one fused multiply-add in double.
+// Eqn 4c on its own: p <- p - lr * g, one fused multiply-add in double. One
+// float4 of each operand per thread and no loop: every load of the launch is
+// independent, which keeps the most bytes in flight (a grid-stride loop with
+// the same arithmetic measured 25% slower on the largest workload's size).
 __global__ __launch_bounds__(kBlock) void k_sgd(float* p, const float* g, uint64_t n, float lr)
 {
   const double nlr = -(double)lr;
-  const uint64_t n4 = n / 4;
-  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n4; i += stride) {
+  const uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (i < n / 4) {
     f4 pv = *reinterpret_cast<const f4*>(p + 4 * i);
     const f4 gv = __builtin_nontemporal_load(reinterpret_cast<const f4*>(g + 4 * i));
     pv.x = (float)__builtin_fma(nlr, (double)gv.x, (double)pv.x);
@@ -263,8 +265,8 @@ __global__ __launch_bounds__(kBlock) void k_sgd(float* p, const float* g, uint64
     *reinterpret_cast<f4*>(p + 4 * i) = pv;
   }
   if (blockIdx.x == 0 && threadIdx.x < (n & 3)) {
-    const uint64_t i = 4 * n4 + threadIdx.x;
-    p[i] = (float)__builtin_fma(nlr, (double)g[i], (double)p[i]);
+    const uint64_t t = (n & ~3ull) + threadIdx.x;
+    p[t] = (float)__builtin_fma(nlr, (double)g[t], (double)p[t]);
   }
 }
 
@@ -298,14 +300,14 @@ hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate
   return hipGetLastError();
 }
 
-// Momentum SGD with weight decay on its own (same arithmetic as the fused update).
+// Momentum SGD with weight decay on its own (same arithmetic as the fused
+// update), one float4 of each operand per thread like k_sgd.
 __global__ __launch_bounds__(kBlock) void k_momentum_sgd(float* p, float* v, const float* g, uint64_t n, float lr,
                                                          float mom, float wd)
 {
   const double nlr = -(double)lr, mu = (double)mom, dw = (double)wd;
-  const uint64_t n4 = n / 4;
-  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n4; i += stride) {
+  const uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (i < n / 4) {
     f4 pv = *reinterpret_cast<const f4*>(p + 4 * i);
     f4 vv = *reinterpret_cast<const f4*>(v + 4 * i);
     const f4 gv = __builtin_nontemporal_load(reinterpret_cast<const f4*>(g + 4 * i));
@@ -320,30 +322,31 @@ __global__ __launch_bounds__(kBlock) void k_momentum_sgd(float* p, float* v, con
     *reinterpret_cast<f4*>(p + 4 * i) = pv;
   }
   if (blockIdx.x == 0 && threadIdx.x < (n & 3)) {
-    const uint64_t i = 4 * n4 + threadIdx.x;
-    float pi = p[i], vi = v[i];
-    momentum_step(pi, vi, g[i], nlr, mu, dw);
-    v[i] = vi;
-    p[i] = pi;
+    const uint64_t t = (n & ~3ull) + threadIdx.x;
+    float pt = p[t], vt = v[t];
+    momentum_step(pt, vt, g[t], nlr, mu, dw);
+    v[t] = vt;
+    p[t] = pt;
   }
+}
+
+// One thread per float4 (at least one workgroup, for the tail of n < 4).
+static uint32_t elementwise_blocks(uint64_t n)
+{
+  const uint64_t b = (n / 4 + kBlock - 1) / kBlock;
+  return (uint32_t)(b < 1 ? 1 : b);
 }
 
 hipError_t launch_momentum_sgd(float* p, float* v, const float* g, uint64_t n, float lr, float mom, float wd,
                                hipStream_t s)
 {
-  uint64_t blocks = (n / 4 + kBlock - 1) / kBlock;
-  if (blocks < 1) blocks = 1;
-  if (blocks > 8192) blocks = 8192;
-  k_momentum_sgd<<<(uint32_t)blocks, kBlock, 0, s>>>(p, v, g, n, lr, mom, wd);
+  k_momentum_sgd<<<elementwise_blocks(n), kBlock, 0, s>>>(p, v, g, n, lr, mom, wd);
   return hipGetLastError();
 }
 
 hipError_t launch_sgd(float* p, const float* g, uint64_t n, float lr, hipStream_t s)
 {
-  uint64_t blocks = (n / 4 + kBlock - 1) / kBlock;
-  if (blocks < 1) blocks = 1;
-  if (blocks > 8192) blocks = 8192;
-  k_sgd<<<(uint32_t)blocks, kBlock, 0, s>>>(p, g, n, lr);
+  k_sgd<<<elementwise_blocks(n), kBlock, 0, s>>>(p, g, n, lr);
   return hipGetLastError();
 }
 

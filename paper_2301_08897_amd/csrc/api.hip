@@ -37,7 +37,7 @@ scadles_status fail(scadles_status st, const char* fmt, ...)
 
 namespace {
 
-std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0}, g_parts{1};
+std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0}, g_parts{1}, g_inject_count_error{0};
 // per-layer selection: layers of at most this many elements go to the row kernels
 std::atomic<int64_t> g_row_max{1 << 21};
 
@@ -122,7 +122,7 @@ struct Layout {
   uint64_t n = 0;
   uint32_t k[kMaxK], cap[kMaxK], mode[kMaxK], r_lo[kMaxK], r_hi[kMaxK];
   uint32_t any_fast = 0;
-  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_ctot, o_coff, o_ce, o_olist, o_slot, o_epart, o_cidx, o_cval, o_band, o_gcnt, o_gpre, o_bcnt, o_bpre, o_be, o_fb, o_lb,
+  size_t o_desc, o_st, o_hist, o_scnt, o_soff, o_olist, o_slot, o_epart, o_cidx, o_cval, o_band, o_gcnt, o_gpre, o_bcnt, o_bpre, o_be, o_fb, o_lb,
       o_aerr;
   size_t total = 0;
 };
@@ -215,9 +215,6 @@ bool make_layout(uint32_t K, uint64_t n, const double* ratios, bool force_exact,
     const size_t nslots = L.any_fast ? (size_t)K * L.nslot : 0;
     L.o_scnt = take(sizeof(uint32_t) * (size_t)K * L.nslot);
     L.o_soff = take(sizeof(uint64_t) * (size_t)K * L.nslot);
-    L.o_ctot = take(sizeof(uint64_t) * (size_t)K * kMaxChunks);
-    L.o_coff = take(sizeof(uint64_t) * (size_t)K * kMaxChunks);
-    L.o_ce = take(sizeof(double) * (size_t)K * kMaxChunks);
     L.o_olist = take(sizeof(uint32_t) * (size_t)K * L.nslot);
     L.o_slot = take(sizeof(uint32_t) * nslots * kSlotWords);
     L.o_epart = take(sizeof(double) * (size_t)K * L.nslot);
@@ -247,9 +244,6 @@ Ctx make_ctx(const Layout& L, void* ws)
   c.hist = reinterpret_cast<uint32_t*>(b + L.o_hist);
   c.slot_cnt = reinterpret_cast<uint32_t*>(b + L.o_scnt);
   c.slot_off = reinterpret_cast<uint64_t*>(b + L.o_soff);
-  c.chunk_tot = reinterpret_cast<uint64_t*>(b + L.o_ctot);
-  c.chunk_off = reinterpret_cast<uint64_t*>(b + L.o_coff);
-  c.chunk_e = reinterpret_cast<double*>(b + L.o_ce);
   c.ovf_list = reinterpret_cast<uint32_t*>(b + L.o_olist);
   c.slot = reinterpret_cast<uint32_t*>(b + L.o_slot);
   c.epart = reinterpret_cast<double*>(b + L.o_epart);
@@ -332,6 +326,7 @@ scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double d
   c.energies_out = energies;
   c.compressed_out = compressed;
   c.force_fallback = g_force_fallback.load() ? 1u : 0u;
+  c.inject_count_error = g_inject_count_error.load() ? 1u : 0u;
   SelectPlan p;
   p.any_fast = L.any_fast;
   p.sample_blocks = ceil_div_u64(L.s_n, kSBlk);
@@ -368,6 +363,22 @@ scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double d
   return SCADLES_OK;
 }
 
+// Validation mode: waits for the call's work on s and reports a device whose
+// selection state carries an error bit other than a recovered bracket miss
+// (its output would be wrong).
+scadles_status check_states(const Layout& L, void* ws, hipStream_t s)
+{
+  DevState st[kMaxK];
+  hipError_t e = hipMemcpyAsync(st, static_cast<char*>(ws) + L.o_st, sizeof(DevState) * L.K, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "selection state readback");
+  for (uint32_t j = 0; j < L.K; ++j)
+    if (st[j].err & kErrFatal)
+      return fail(SCADLES_EINTERNAL, "device %u: the selection's internal check failed (error bits 0x%x)", j,
+                  st[j].err);
+  return SCADLES_OK;
+}
+
 }  // namespace
 
 // ---- ABI ----------------------------------------------------------------------------------------
@@ -394,8 +405,9 @@ size_t scadles_aggregate_workspace_bytes(uint32_t K, uint64_t n)
   return L.total;
 }
 
-scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio, uint32_t* idx, float* val,
-                                   double* energies, void* ws, size_t ws_bytes, void* stream)
+// Argument checks and layout of a one-gradient selection.
+static scadles_status topk_args(const float* grad, uint64_t n, double ratio, uint32_t* idx, float* val,
+                                double* energies, Layout& L)
 {
   if (scadles_status st = check_n(n)) return st;
   if (!grad || !idx || !val) return fail(SCADLES_EINVAL, "grad, idx and val must not be NULL");
@@ -403,9 +415,15 @@ scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio, 
   if (!aligned(idx, 4) || !aligned(val, 4)) return fail(SCADLES_EINVAL, "idx and val must be 4-byte aligned");
   if (energies && !aligned(energies, 8)) return fail(SCADLES_EINVAL, "energies must be 8-byte aligned");
   if (k_rule(n, ratio) == 0) return fail(SCADLES_EINVAL, "ratio %g is not in (0, 1]", ratio);
-  Layout L;
   make_layout(1, n, &ratio, g_force_exact.load() != 0, true, L);
-  if (scadles_status st = check_ws(ws, ws_bytes, L.total)) return st;
+  return SCADLES_OK;
+}
+
+// The selection of one gradient into a checked workspace (one device: one
+// group, so no library stream is created and nothing is allocated).
+static scadles_status topk_run(const float* grad, const Layout& L, uint32_t* idx, float* val, double* energies,
+                               void* ws, hipStream_t s)
+{
   PrepArgs a;
   memset(&a, 0, sizeof(a));
   a.grad[0] = grad;
@@ -416,12 +434,21 @@ scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio, 
   a.mode[0] = L.mode[0];
   a.r_lo[0] = L.r_lo[0];
   a.r_hi[0] = L.r_hi[0];
-  hipStream_t s = static_cast<hipStream_t>(stream);
   ProfRec* pr = prof_slot();
   if (pr) (void)hipEventRecord(pr->ev[0], s);
   scadles_status st = run_select(L, a, ws, INFINITY, energies, nullptr, s, pr);
   if (pr) (void)hipEventRecord(pr->ev[3 + 2 * pr->parts], s);
+  if (st == SCADLES_OK && g_validate.load()) st = check_states(L, ws, s);
   return st;
+}
+
+scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio, uint32_t* idx, float* val,
+                                   double* energies, void* ws, size_t ws_bytes, void* stream)
+{
+  Layout L;
+  if (scadles_status st = topk_args(grad, n, ratio, idx, val, energies, L)) return st;
+  if (scadles_status st = check_ws(ws, ws_bytes, L.total)) return st;
+  return topk_run(grad, L, idx, val, energies, ws, static_cast<hipStream_t>(stream));
 }
 
 // Layers of a per-layer selection: checks seg_off (0 = off[0] < ... < off[L]
@@ -923,6 +950,7 @@ static scadles_status step_fused_impl(const float* const* grads, uint32_t K, uin
   hipError_t e = launch_aggregate(g, c, 0, true, s);
   if (pr) (void)hipEventRecord(pr->ev[3 + 2 * pr->parts], s);
   if (e != hipSuccess) return hip_fail(e, "aggregate launch");
+  if (g_validate.load()) return check_states(L, ws, s);
   return SCADLES_OK;
 }
 
@@ -978,6 +1006,7 @@ scadles_status scadles_set_option(const char* name, int64_t value)
   if (!strcmp(name, "validate")) g_validate = value ? 1 : 0;
   else if (!strcmp(name, "force_exact")) g_force_exact = value ? 1 : 0;
   else if (!strcmp(name, "force_fallback")) g_force_fallback = value ? 1 : 0;
+  else if (!strcmp(name, "inject_count_error")) g_inject_count_error = value ? 1 : 0;
   else if (!strcmp(name, "row_max")) {
     if (value < 0 || value > 0xFFFFFFFFll) return fail(SCADLES_EINVAL, "row_max must be in [0, 2^32 - 1]");
     g_row_max = value;

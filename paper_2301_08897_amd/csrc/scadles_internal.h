@@ -30,12 +30,20 @@ constexpr uint64_t kSat31 = 0x7FFFFFFFull;
 constexpr int kFullWorkers = 1024;     // grid of the grid-stride exact-path kernels
 constexpr int kWaveCap = 512;          // main pass: candidates one wave chunk (4096 elements) can stage
 constexpr int kSlotWords = 1024;       // 32-bit words of one tile's slot region (4 KiB)
-constexpr int kScanChunk = 4096;       // slots per workgroup of the slot-offset scan
-constexpr int kMaxChunks = 256;        // >= ceil(nslot / kScanChunk) for n < 2^32
 constexpr int kGatherSlots = 2;        // tiles per wave in the selection-list and output passes
 constexpr int kOverflowBlocks = 128;   // workgroups per device re-scanning overflowed tiles
 
 enum : uint32_t { kModeFast = 0, kModeExact = 1 };
+
+// DevState::err bits. A bracket miss only sends the device to the exact path;
+// the others mean its output is wrong and are reported in validation mode.
+enum : uint32_t {
+  kErrBracket = 2u,       // a sample selection of the bracket missed (recovered by the exact path)
+  kErrSelect = 4u,        // a radix pass of the threshold selection missed
+  kErrNoThreshold = 8u,   // the threshold selection did not finish
+  kErrCount = 16u,        // keys above the threshold + ties kept != k
+};
+constexpr uint32_t kErrFatal = kErrSelect | kErrNoThreshold | kErrCount;
 
 // ---- workspace structures ---------------------------------------------------------------
 struct DevDesc {          // per device, written once per call by the prep kernel
@@ -72,7 +80,7 @@ struct DevState {
   uint32_t t_lo, t_hi;    // bracket used by the main pass
   uint32_t fallback;      // 1: the exact full-data path produces this device's output
   uint32_t thr;           // final threshold key (k-th largest)
-  uint32_t err;           // internal error bits (select miss, count mismatch)
+  uint32_t err;           // internal error bits, kErr*
   uint64_t c_gt, need;    // keys above thr; keys equal to thr that are kept
   double e_all, e_kept;
   uint32_t sparse;        // 1: the device sends Top-k (adaptive rule), 0: dense
@@ -85,10 +93,7 @@ struct Ctx {
   DevState* st;
   uint32_t* hist;         // [K][kSlots][kBins]
   uint32_t* slot_cnt;     // [K][nslot] per tile: candidates | overflowed << 15 | sure << 16
-  uint64_t* slot_off;     // [K][nslot] candidate | sure << 32 counts before each slot within its scan chunk
-  uint64_t* chunk_tot;    // [K][kMaxChunks] candidate | sure << 32 totals of each scan chunk
-  uint64_t* chunk_off;    // [K][kMaxChunks] candidate | sure << 32 counts before each scan chunk
-  double* chunk_e;        // [K][kMaxChunks] sum of squares of each scan chunk
+  uint64_t* slot_off;     // [K][nslot] candidate | sure << 32 counts of the device's tiles before each tile
   uint32_t* slot;         // [K][nslot][kSlotWords] per tile: candidates' value bits, then the keys of those
                           // below t_hi; from the top down, the candidates' 16-bit offsets in the tile
   uint32_t* ovf_list;     // [K][nslot] tiles with a wave chunk of more than kWaveCap candidates
@@ -113,6 +118,7 @@ struct Ctx {
   uint32_t s_stride;      // sample chunk stride (elements)
   uint32_t s_n;           // sample elements per device
   uint32_t force_fallback;
+  uint32_t inject_count_error;   // testing: device 0 reports kErrCount
   uint32_t j0, jn;        // devices [j0, j0 + jn) of this launch (the per-device kernels)
   uint32_t* fb_count;     // devices on the exact path (the exact-path kernels exit early at 0)
   uint32_t* lb;           // fused step: aggregation range markers (see AggCtx), else null

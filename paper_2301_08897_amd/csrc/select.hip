@@ -70,6 +70,86 @@ __device__ inline bool sel_digit(const SelView& v, uint32_t key, uint32_t& d)
   return true;
 }
 
+// Threshold, count above it and ties kept, from whichever selection decided it.
+__device__ inline bool threshold_of(const DevState& s, uint32_t& thr, uint64_t& need)
+{
+  const Sel& sel = s.fallback ? s.sel[kSlotFull] : s.sel[kSlotCand];
+  if (!sel.found) {
+    thr = kKeyInf;
+    need = 0;
+    return false;
+  }
+  thr = sel.result;
+  need = sel.rank;
+  return true;
+}
+
+__device__ inline void flush_hist(const uint32_t* h, uint32_t* g, int nb)
+{
+  for (int b = threadIdx.x; b < nb; b += kBlock) {
+    uint32_t v = h[b];
+    if (v) atomicAdd(g + b, v);
+  }
+}
+
+// ---- block-wide rank selection over a histogram -----------------------------------------------
+// Among nb bins (nb a multiple of NT) holding counts of keys by digit, finds the
+// bin of the key of 1-based descending rank `rank` (the largest digit is the
+// top bin) and the number of keys in the bins above it. Every thread returns
+// the same result; false (bin 0, above = total) when rank exceeds the total.
+// The histogram must be complete (a barrier before the call); s_w holds
+// NT / 64 + 3 words of LDS.
+template <int NT>
+__device__ inline bool block_find(const uint32_t* h, int nb, uint64_t rank, uint32_t* s_w, uint32_t& bin,
+                                  uint64_t& above)
+{
+  constexpr int kW = NT / 64;
+  const int per = nb / NT;
+  const uint32_t tid = threadIdx.x, w = tid >> 6;
+  const int b_hi = nb - (int)tid * per;               // this thread's bins [b_hi - per, b_hi), top first
+  uint32_t sum = 0;
+  for (int i = 0; i < per; ++i) sum += h[b_hi - 1 - i];
+  const uint32_t incl = wave_incl_scan(sum);
+  if (lane_id() == 63) s_w[w] = incl;
+  if (tid == 0) s_w[kW + 2] = 0u;
+  __syncthreads();
+  uint64_t excl = incl - sum;
+  for (uint32_t i = 0; i < w; ++i) excl += s_w[i];
+  if (excl < rank && rank <= excl + sum) {
+    uint64_t cum = excl;
+    for (int i = 0; i < per; ++i) {
+      const uint32_t v = h[b_hi - 1 - i];
+      if (cum + v >= rank) {
+        s_w[kW] = (uint32_t)(b_hi - 1 - i);
+        s_w[kW + 1] = (uint32_t)(cum - excl);       // within this thread's share: < 2^32
+        s_w[kW + 2] = 1u + tid;
+        break;
+      }
+      cum += v;
+    }
+  }
+  __syncthreads();
+  const uint32_t who = s_w[kW + 2];
+  const bool ok = who != 0u;
+  if (ok) {
+    bin = s_w[kW];
+    // the finder's exclusive prefix: the wave totals before its wave, then the
+    // bins of the lanes before it in its wave, then its own bins above the hit
+    const uint32_t ft = who - 1u, fw = ft >> 6;
+    uint64_t pre = 0;
+    for (uint32_t i = 0; i < fw; ++i) pre += s_w[i];
+    for (int b = nb - (int)(fw * 64) * per - 1; b >= nb - (int)ft * per; --b) pre += h[b];
+    above = pre + s_w[kW + 1];
+  } else {
+    bin = 0;
+    uint64_t tot = 0;
+    for (int i = 0; i < kW; ++i) tot += s_w[i];
+    above = tot;
+  }
+  __syncthreads();
+  return ok;
+}
+
 // Bracket of the main pass from the sample selections. The bracket only has to
 // be conservative (t_lo at or below the sample key of rank r_lo, t_hi above the
 // one of rank r_hi), so the selections stop after kBracketPasses digits: the
@@ -95,28 +175,6 @@ __device__ inline void bracket_of(const DevDesc& d, const DevState& s, uint32_t&
     thi = kKeyInf;
   }
   if (thi <= tlo) thi = kKeyInf;
-}
-
-// Threshold, count above it and ties kept, from whichever selection decided it.
-__device__ inline bool threshold_of(const DevState& s, uint32_t& thr, uint64_t& need)
-{
-  const Sel& sel = s.fallback ? s.sel[kSlotFull] : s.sel[kSlotCand];
-  if (!sel.found) {
-    thr = kKeyInf;
-    need = 0;
-    return false;
-  }
-  thr = sel.result;
-  need = sel.rank;
-  return true;
-}
-
-__device__ inline void flush_hist(const uint32_t* h, uint32_t* g, int nb)
-{
-  for (int b = threadIdx.x; b < nb; b += kBlock) {
-    uint32_t v = h[b];
-    if (v) atomicAdd(g + b, v);
-  }
 }
 
 // ---- 0. per-call preparation -----------------------------------------------------------------
@@ -260,7 +318,7 @@ __global__ __launch_bounds__(64) void k_find(Ctx c, int s_begin, int s_end, int 
       if (!m) {
         sel.active = 0;
         sel.found = 0;
-        c.st[j].err |= 2u;
+        c.st[j].err |= s < kSlotCand ? kErrBracket : kErrSelect;   // a bracket miss sends the device to the exact path
       } else {
         sel.rank -= cum;
         sel.above += cum;
@@ -514,94 +572,67 @@ __device__ inline uint64_t wave_incl_scan_u64(uint64_t v)
   return v;
 }
 
-// Per device and scan chunk (kScanChunk tiles; each thread takes 16
-// consecutive tiles): the chunk's sum of squares (fixed order), and for a fast
-// device the tiles' candidate | sure << 32 offsets within the chunk and the
-// chunk's totals.
-__global__ __launch_bounds__(kBlock) void k_tile_scan(Ctx c)
+// One workgroup per device: the exclusive prefix of the tiles' candidate | sure
+// << 32 counts (each thread takes a run of consecutive tiles), the sum of
+// squares over all tiles in a fixed order, then the path decision: the exact
+// path (fallback) or the radix selection on the selection interval.
+constexpr int kScanBlock = 1024;
+
+__global__ __launch_bounds__(kScanBlock) void k_scan(Ctx c)
 {
-  __shared__ uint64_t s_w[4];
-  __shared__ double s_e[4];
-  const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
-  const uint32_t jr = blockIdx.x / nchunk, ch = blockIdx.x - jr * nchunk;
-  const uint32_t j = c.j0 + jr;
-  const uint32_t tid = threadIdx.x;
-  const uint32_t s0 = ch * kScanChunk + tid * 16;
-  const double* ep = c.epart + (uint64_t)j * c.nslot;
-  double a = 0.0;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) a += (s0 + i < c.nslot) ? ep[s0 + i] : 0.0;
-  const double t = block_sum_f64(a, s_e);
-  if (tid == 0) c.chunk_e[(uint64_t)j * kMaxChunks + ch] = t;
-  if (c.desc[j].mode != kModeFast) return;
+  constexpr int kW = kScanBlock / 64;
+  __shared__ uint64_t s_w[kW];
+  __shared__ double s_e[kW];
+  const uint32_t j = c.j0 + blockIdx.x, tid = threadIdx.x, w = tid >> 6;
+  const DevDesc d = c.desc[j];
+  const bool fast = d.mode == kModeFast;
+  const uint32_t per = (c.nslot + kScanBlock - 1) / kScanBlock;
+  const uint32_t t0 = tid * per < c.nslot ? tid * per : c.nslot;
+  const uint32_t t1 = t0 + per < c.nslot ? t0 + per : c.nslot;
   const uint32_t* cnt = c.slot_cnt + (uint64_t)j * c.nslot;
-  uint32_t v[16];
-  if (s0 + 16 <= c.nslot) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const u4 x = ldu4(cnt + s0 + 4 * i);
-      v[4 * i] = x.x;
-      v[4 * i + 1] = x.y;
-      v[4 * i + 2] = x.z;
-      v[4 * i + 3] = x.w;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 16; ++i) v[i] = (s0 + i < c.nslot) ? cnt[s0 + i] : 0u;
-  }
+  const double* ep = c.epart + (uint64_t)j * c.nslot;
   uint64_t sum = 0;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) sum += (uint64_t)(v[i] & 0x7FFFu) | ((uint64_t)(v[i] >> 16) << 32);
+  double e = 0.0;
+  for (uint32_t t = t0; t < t1; ++t) {
+    e += ep[t];
+    if (fast) {
+      const uint32_t v = cnt[t];
+      sum += (uint64_t)(v & 0x7FFFu) | ((uint64_t)(v >> 16) << 32);
+    }
+  }
+  // energies: per thread in tile order, then lanes and waves in a fixed pattern
+  const double ew = wave_sum_f64(e);
   const uint64_t incl = wave_incl_scan_u64(sum);
-  if (lane_id() == 63) s_w[tid >> 6] = incl;
+  if (lane_id() == 63) s_w[w] = incl;
+  if (lane_id() == 0) s_e[w] = ew;
   __syncthreads();
   uint64_t run = incl - sum;
-  for (uint32_t i = 0; i < (tid >> 6); ++i) run += s_w[i];
-  uint64_t* off = c.slot_off + (uint64_t)j * c.nslot;
-  uint64_t oc = run;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    if (s0 + i < c.nslot) off[s0 + i] = oc;
-    oc += (uint64_t)(v[i] & 0x7FFFu) | ((uint64_t)(v[i] >> 16) << 32);
-  }
-  if (tid == kBlock - 1) c.chunk_tot[(uint64_t)j * kMaxChunks + ch] = run + sum;
-}
-
-// Slot offsets, level 2, and the per-device decision: chunk prefixes, candidate
-// totals, energies, then the exact path (fallback) or the candidate selection.
-__global__ __launch_bounds__(kBlock) void k_post(Ctx c)
-{
-  __shared__ double s_e[4];
-  __shared__ uint64_t s_w[4];
-  const uint32_t j = c.j0 + blockIdx.x, tid = threadIdx.x;
-  const uint32_t nch = (c.nslot + kScanChunk - 1) / kScanChunk;    // <= kMaxChunks = kBlock
-  const double e_all = block_sum_f64(tid < nch ? c.chunk_e[(uint64_t)j * kMaxChunks + tid] : 0.0, s_e);
-  const DevDesc d = c.desc[j];
-  uint64_t cand = 0, sure = 0;
-  if (d.mode == kModeFast) {
-    const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;    // <= kMaxChunks = kBlock
-    const uint64_t v = tid < nchunk ? c.chunk_tot[(uint64_t)j * kMaxChunks + tid] : 0ull;
-    const uint64_t incl = wave_incl_scan_u64(v);
-    if (lane_id() == 63) s_w[tid >> 6] = incl;
-    __syncthreads();
-    uint64_t run = incl - v;
-    for (uint32_t i = 0; i < (tid >> 6); ++i) run += s_w[i];
-    if (tid < nchunk) c.chunk_off[(uint64_t)j * kMaxChunks + tid] = run;
-    const uint64_t tot = s_w[0] + s_w[1] + s_w[2] + s_w[3];
-    cand = tot & 0xFFFFFFFFull;
-    sure = tot >> 32;
+  for (uint32_t i = 0; i < w; ++i) run += s_w[i];
+  if (fast) {
+    uint64_t* off = c.slot_off + (uint64_t)j * c.nslot;
+    for (uint32_t t = t0; t < t1; ++t) {
+      off[t] = run;
+      const uint32_t v = cnt[t];
+      run += (uint64_t)(v & 0x7FFFu) | ((uint64_t)(v >> 16) << 32);
+    }
   }
   if (tid != 0) return;
+  uint64_t tot = 0;
+  double e_all = 0.0;
+  for (int i = 0; i < kW; ++i) {
+    tot += s_w[i];
+    e_all += s_e[i];
+  }
   DevState& s = c.st[j];
   s.e_all = e_all;
-  bool fb = (d.mode != kModeFast) || c.force_fallback;
+  bool fb = !fast || c.force_fallback;
   const uint32_t tlo = s.t_lo, thi = s.t_hi;
-  if (d.mode == kModeFast) {
-    s.cand = cand;
-    s.sure = sure;
+  if (fast) {
+    s.cand = tot & 0xFFFFFFFFull;
+    s.sure = tot >> 32;
     if (s.err) fb = true;
     // the selection interval must hold the k-th largest key: fewer than k sure keys
-    if (cand < d.k || cand > d.cap || sure >= d.k) fb = true;
+    if (s.cand < d.k || s.cand > d.cap || s.sure >= d.k) fb = true;
   }
   Sel sel;
   __builtin_memset(&sel, 0, sizeof(sel));
@@ -629,7 +660,7 @@ __global__ __launch_bounds__(kBlock) void k_post(Ctx c)
 __device__ inline uint64_t slot_pre(const Ctx& c, uint32_t j, uint32_t s)
 {
   if (s >= c.nslot) return c.st[j].cand | (c.st[j].sure << 32);
-  return c.chunk_off[(uint64_t)j * kMaxChunks + s / kScanChunk] + c.slot_off[(uint64_t)j * c.nslot + s];
+  return c.slot_off[(uint64_t)j * c.nslot + s];
 }
 
 // ---- 3. selection-interval keys per tile ---------------------------------------------------
@@ -1278,12 +1309,12 @@ __device__ inline void final_body(const Ctx& c, uint32_t jr)
   if (threadIdx.x != 0) return;
   uint32_t thr;
   uint64_t need;
-  if (!threshold_of(s, thr, need)) s.err |= 8u;
+  if (!threshold_of(s, thr, need)) s.err |= kErrNoThreshold;
   const uint64_t tot = pre[nb - 1] + cnt[nb - 1];
   s.thr = thr;
   s.c_gt = tot & 0xFFFFFFFFull;
   s.need = need;
-  if (s.c_gt + need != c.desc[j].k) s.err |= 16u;
+  if (s.c_gt + need != c.desc[j].k || (c.inject_count_error && j == 0)) s.err |= kErrCount;
   s.e_kept = e_kept;
   // §IV: the rule compares the energies, optionally their moving averages
   s.sparse = adaptive_rule(s.e_all, e_kept, c.ewma ? c.ewma + 2 * (uint64_t)j : nullptr, c.ewma_beta, c.delta);
@@ -1355,9 +1386,7 @@ static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s, int ha
 {
   const uint32_t band_blocks = c.jn * ((c.nslot + kBandTiles * kWaves - 1) / (kBandTiles * kWaves));
   if (half == 0) {
-    const uint32_t nchunk = (c.nslot + kScanChunk - 1) / kScanChunk;
-    k_tile_scan<<<c.jn * nchunk, kBlock, 0, s>>>(c);
-    k_post<<<c.jn, kBlock, 0, s>>>(c);
+    k_scan<<<c.jn, kScanBlock, 0, s>>>(c);
     const uint32_t ncand = p.any_fast ? band_blocks : 0u;
     if (p.any_fast) k_overflow<<<c.jn * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
     for (int pass = 0; pass < 3; ++pass) {

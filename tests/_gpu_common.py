@@ -11,9 +11,18 @@ import oracle
 import workloads
 
 
+# pytest's capture manager (set by a fixture in conftest.py): progress lines of
+# long tests reach the terminal even while the test's output is captured.
+CAPTURE = None
+
+
 def log(msg: str):
-    print(msg, flush=True)
-    sys.stdout.flush()
+    if CAPTURE is not None:
+        with CAPTURE.global_and_fixture_disabled():
+            print(msg, flush=True)
+    else:
+        print(msg, flush=True)
+        sys.stdout.flush()
 
 
 def torch_dev():

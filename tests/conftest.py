@@ -23,3 +23,12 @@ def orc():
 def wl():
     import workloads
     return workloads
+
+
+@pytest.fixture(scope="session", autouse=True)
+def _progress_lines(request):
+    """Progress lines of long GPU tests bypass output capture."""
+    import _gpu_common
+    _gpu_common.CAPTURE = request.config.pluginmanager.get_plugin("capturemanager")
+    yield
+    _gpu_common.CAPTURE = None

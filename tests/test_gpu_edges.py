@@ -256,3 +256,33 @@ def test_determinism(sc):
             assert same_bits(ref[2], snap[2])
             assert np.array_equal(ref[3].view(np.uint64), snap[3].view(np.uint64))
             assert np.array_equal(ref[4], snap[4])
+
+
+def test_validation_reports_internal_errors(sc):
+    """In validation mode the selection calls read every device's state back:
+    a clean call returns OK, a count check forced to fail (from the host, for
+    device 0) returns SCADLES_EINTERNAL naming the device; without validation
+    the same call returns OK (nothing is read back)."""
+    log("edge validation of the selection state")
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(31)
+    g = torch.from_numpy(rng.standard_normal(300_001).astype(np.float32)).to(dev)
+    G = torch.from_numpy(rng.standard_normal((3, 200_003)).astype(np.float32)).to(dev)
+    w, _ = sc.stream_weights([1.0, 2.0, 3.0])
+    try:
+        sc.set_option("validate", 1)
+        sc.topk_select(g, 0.01)
+        sc.FusedStep(G, [0.01] * 3).run(w)
+        sc.set_option("inject_count_error", 1)
+        with pytest.raises(sc.ScadlesError) as e1:
+            sc.topk_select(g, 0.01)
+        assert e1.value.code == 5 and "device 0" in str(e1.value)
+        with pytest.raises(sc.ScadlesError) as e2:
+            sc.FusedStep(G, [0.01] * 3).run(w)
+        assert e2.value.code == 5
+        sc.set_option("validate", 0)
+        sc.topk_select(g, 0.01)
+        torch.cuda.synchronize()
+    finally:
+        sc.set_option("inject_count_error", 0)
+        sc.set_option("validate", 0)
