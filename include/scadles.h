@@ -105,6 +105,27 @@ scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio,
                                    uint32_t* idx, float* val, double* energies,
                                    void* ws, size_t ws_bytes, void* stream);
 
+/* scadles_topk_select without a workspace argument and without allocating,
+ * for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation). The
+ * workspace is a static array of SCADLES_NOALLOC_SCRATCH_BYTES bytes that the
+ * library holds on every GPU it runs on until the process ends; its address is
+ * looked up once per GPU, on the first call there. The call allocates nothing
+ * and launches the same kernels as scadles_topk_select, with the same
+ * results, and clears the parts of the scratch that must start at zero.
+ * Every call on one GPU shares that GPU's scratch: calls that may overlap on
+ * one GPU (several host threads, or streams that do not order them) race and
+ * give unspecified results; order them on one stream. Arguments and errors as
+ * for scadles_topk_select; in addition SCADLES_EWORKSPACE when the selection
+ * needs more scratch than the maximum (scadles_workspace_bytes(1, n, &ratio) >
+ * SCADLES_NOALLOC_SCRATCH_BYTES; e.g. a gradient of 143,667,240 elements fits
+ * at ratio 0.01 but not at 0.1). The first call on a GPU may return
+ * SCADLES_EHIP if the scratch address cannot be looked up.               */
+#define SCADLES_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+scadles_status scadles_topk_select_noalloc(const float* grad, uint64_t n, double ratio,
+                                           uint32_t* idx, float* val, double* energies,
+                                           void* stream);
+
 /* Per-layer Top-k: the per-layer reading of the Top-k sparsification of §IV
  * (each layer of the model keeps its own top fraction) for K devices whose
  * flat gradients share one layer layout. Layer l is positions
@@ -335,7 +356,7 @@ const char* scadles_last_error(void);
 
 /* Process-wide options, for testing and diagnosis:
  *   "validate"       1: scadles_weighted_aggregate checks its sets, and
- *                       scadles_topk_select, scadles_step_fused and
+ *                       scadles_topk_select(_noalloc), scadles_step_fused and
  *                       scadles_step_fused_ex read every device's selection
  *                       state back after the call and return
  *                       SCADLES_EINTERNAL if its internal checks failed

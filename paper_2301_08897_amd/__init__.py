@@ -31,6 +31,7 @@ import torch as _torch_for_runtime  # noqa: E402,F401
 _lib = ctypes.CDLL(LIB_PATH)
 
 MAX_DEVICES = 64
+NOALLOC_SCRATCH_BYTES = 128 << 20      # SCADLES_NOALLOC_SCRATCH_BYTES
 PROFILE_STAGES = 5
 STAGE_NAMES = ("bracket", "main_select", "post_select", "aggregate", "total")
 
@@ -66,6 +67,8 @@ _ws_bytes = _sig("scadles_workspace_bytes", ctypes.c_size_t, _u32, _u64, ctypes.
 _agg_ws_bytes = _sig("scadles_aggregate_workspace_bytes", ctypes.c_size_t, _u32, _u64)
 _topk_select = _sig("scadles_topk_select", ctypes.c_int, _vp, _u64, ctypes.c_double, _vp, _vp, _vp, _vp,
                     ctypes.c_size_t, _vp)
+_topk_select_noalloc = _sig("scadles_topk_select_noalloc", ctypes.c_int, _vp, _u64, ctypes.c_double, _vp, _vp,
+                            _vp, _vp)
 _layers_k = _sig("scadles_layers_k", _u64, ctypes.POINTER(_u64), _u32, ctypes.c_double)
 _layers_ws_bytes = _sig("scadles_layers_workspace_bytes", ctypes.c_size_t, _u32, ctypes.POINTER(_u64), _u32,
                         ctypes.POINTER(ctypes.c_double))
@@ -297,6 +300,27 @@ def topk_select(grad, ratio: float, *, workspace=None, energies: bool = False, s
                         en.data_ptr() if en is not None else None, ws.data_ptr(), ws.numel(),
                         _stream_ptr(stream)))
     return (idx, val, en) if energies else (idx, val)
+
+
+def topk_select_noalloc(grad, ratio: float, idx, val, energies=None, *, stream=None):
+    """Top-k of one gradient into caller-given outputs (idx uint32[k], val
+    float32[k], energies float64[2] or None) using the library's static
+    scratch: the call allocates nothing (scadles_topk_select_noalloc)."""
+    torch = _torch()
+    gp = _dev_f32(grad, "grad")
+    n = grad.numel()
+    k = topk_k(n, ratio)
+    if k == 0:
+        raise ScadlesError(1, f"invalid n={n} or ratio={ratio}")
+    if idx.numel() < k or val.numel() < k or not idx.is_cuda or not idx.is_contiguous():
+        raise ValueError(f"idx and val must be contiguous GPU tensors of at least k={k} entries")
+    if idx.dtype not in (torch.uint32, torch.int32):
+        raise TypeError("idx must be uint32")
+    if energies is not None and (energies.dtype != torch.float64 or energies.numel() < 2 or not energies.is_cuda):
+        raise TypeError("energies must be a float64 GPU tensor of 2 entries")
+    _check(_topk_select_noalloc(gp, n, float(ratio), idx.data_ptr(), _dev_f32(val, "val"),
+                                energies.data_ptr() if energies is not None else None, _stream_ptr(stream)))
+    return idx, val, energies
 
 
 def weighted_aggregate(sets, weights, n: int, *, out=None, workspace=None, stream=None):

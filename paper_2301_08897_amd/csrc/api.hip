@@ -111,6 +111,36 @@ StreamSet* stream_set()
   return &ss;
 }
 
+// ---- static scratch of the allocation-free selection --------------------------------------
+// scadles_topk_select_noalloc keeps its workspace here instead of in a caller
+// buffer: one array per GPU, created when the code object loads on that GPU
+// and held until the process ends. In host code `scratch` names a host-side
+// stand-in, not device memory: only the address from hipGetSymbolAddress,
+// taken once per device with that device current, is passed to kernels.
+constexpr size_t kScratchBytes = SCADLES_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+void* g_scratch_ptr[kMaxGpus] = {};
+std::mutex g_scratch_mu;
+
+// The current GPU's scratch address, looked up on the first call on that GPU.
+hipError_t scratch_address(void** out)
+{
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxGpus) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
 // ---- layout ---------------------------------------------------------------------------------
 constexpr uint64_t kFastMinN = 65536;
 constexpr uint64_t kCapAlign = 64;
@@ -448,6 +478,22 @@ scadles_status scadles_topk_select(const float* grad, uint64_t n, double ratio, 
   Layout L;
   if (scadles_status st = topk_args(grad, n, ratio, idx, val, energies, L)) return st;
   if (scadles_status st = check_ws(ws, ws_bytes, L.total)) return st;
+  return topk_run(grad, L, idx, val, energies, ws, static_cast<hipStream_t>(stream));
+}
+
+scadles_status scadles_topk_select_noalloc(const float* grad, uint64_t n, double ratio, uint32_t* idx, float* val,
+                                           double* energies, void* stream)
+{
+  Layout L;
+  if (scadles_status st = topk_args(grad, n, ratio, idx, val, energies, L)) return st;
+  if (L.total > kScratchBytes)
+    return fail(SCADLES_EWORKSPACE,
+                "n = %llu at ratio %g needs %zu bytes of scratch; the library's static scratch holds %zu "
+                "(use scadles_topk_select with a workspace)",
+                (unsigned long long)n, ratio, L.total, kScratchBytes);
+  void* ws = nullptr;
+  const hipError_t e = scratch_address(&ws);
+  if (e != hipSuccess) return hip_fail(e, "scratch address");
   return topk_run(grad, L, idx, val, energies, ws, static_cast<hipStream_t>(stream));
 }
 

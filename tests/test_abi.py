@@ -247,3 +247,23 @@ def test_layer_workspace_sizes(sc):
         # more devices never need less
         if K < 64:
             assert sc.layers_workspace_bytes(K + 1, off, ratios + [0.01]) >= sel
+
+
+def test_noalloc_select_rejects_oversize_on_the_host(sc):
+    """The allocation-free selection refuses, before touching the GPU, a size
+    whose workspace exceeds the static scratch (the pointers are never used)."""
+    lib = ctypes.CDLL(sc.library_path())
+    f = lib.scadles_topk_select_noalloc
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_void_p]
+    fake = 1 << 20                                  # aligned, never dereferenced on the host
+    n = 143_667_240
+    assert sc.workspace_bytes(1, n, [0.1]) > sc.NOALLOC_SCRATCH_BYTES
+    assert f(fake, n, 0.1, fake, fake, None, None) == 2          # SCADLES_EWORKSPACE
+    err = lib.scadles_last_error
+    err.restype = ctypes.c_char_p
+    assert b"scratch" in err()
+    assert f(None, n, 0.01, fake, fake, None, None) == 1          # SCADLES_EINVAL
+    assert f(fake, n, 0.0, fake, fake, None, None) == 1
+    assert sc.workspace_bytes(1, n, [0.01]) <= sc.NOALLOC_SCRATCH_BYTES
