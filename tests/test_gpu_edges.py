@@ -286,3 +286,31 @@ def test_validation_reports_internal_errors(sc):
     finally:
         sc.set_option("inject_count_error", 0)
         sc.set_option("validate", 0)
+
+
+@pytest.mark.parametrize("offset", [0, 1, 3])
+def test_overflowed_interior_and_edge_tiles(sc, offset):
+    """Tiles whose candidates overflow the main pass's staging are re-scanned
+    after it: dense magnitudes in the first, a middle and the last tile make
+    all three overflow, at a 4-byte offset into the buffer (offset 1 and 3:
+    the first tile is an edge tile holding pads) and with a ragged end."""
+    torch, dev = torch_dev()
+    n = 9 * 16384 + 777
+    rng = np.random.default_rng(41 + offset)
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    g[:20000] = (rng.standard_normal(20000) * 10.0).astype(np.float32)
+    g[4 * 16384:5 * 16384] = (rng.standard_normal(16384) * 10.0).astype(np.float32)
+    g[-3000:] = (rng.standard_normal(3000) * 10.0).astype(np.float32)
+    buf = torch.zeros(n + 4, dtype=torch.float32, device=dev)
+    buf[offset:offset + n].copy_(torch.from_numpy(g))
+    view = buf[offset:offset + n]
+    log(f"edge overflowed tiles, offset {offset}")
+    for ratio in (0.05, 0.1):
+        k = oracle.topk_k(n, ratio)
+        idx_o, val_o, ea, ek = oracle.topk(g, k)
+        idx, val, en = sc.topk_select(view, ratio, energies=True)
+        torch.cuda.synchronize()
+        assert np.array_equal(idx.cpu().numpy(), idx_o), f"offset {offset} ratio {ratio}: indices"
+        assert same_bits(val.cpu().numpy(), val_o), f"offset {offset} ratio {ratio}: values"
+        e = en.cpu().numpy()
+        check_energies(f"offset {offset} ratio {ratio}", e[0], e[1], oracle.energies_extended(g, idx_o), n, k)
