@@ -147,6 +147,8 @@ def bench_layers(args, s, sc, torch, G, params, weights, lrs):
     seg_off = [0] + [int(x) for x in s.seg_end]
     if args.row_max is not None:
         sc.set_option("row_max", args.row_max)
+    if args.row_split is not None:
+        sc.set_option("row_split", args.row_split)
     step = sc.FusedStep(G[0], s.ratios[0], params=params, seg_off=seg_off)
     R = len(G)
     for i in range(args.warmup):
@@ -212,6 +214,9 @@ def main():
     ap.add_argument("--row-max", type=int, default=None,
                     help="with --topk layers: layers of at most this many elements are selected one workgroup "
                          "per (device, layer) (library option 'row_max')")
+    ap.add_argument("--row-split", type=int, default=None,
+                    help="--topk layers: rows of more than this many elements are split over several "
+                         "workgroups (library option 'row_split')")
     ap.add_argument("--ewma", type=float, default=None, metavar="BETA",
                     help="adaptive rule on moving averages of the energies with this factor, and the CNC / "
                          "floats-sent accounting, inside the fused step (delta stays +inf)")

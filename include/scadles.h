@@ -142,12 +142,15 @@ scadles_status scadles_topk_select_noalloc(const float* grad, uint64_t n, double
  *   idx, val  (host[K] of dev pointers, 4-byte aligned).
  *   energies  (dev, 2K doubles) or NULL: E_all and E_kept of each whole gradient.
  *   ws        scadles_layers_workspace_bytes(K, seg_off, L, ratios) bytes.
- * Layers of at most "row_max" elements (scadles_set_option) are selected one
- * workgroup per (device, layer), all at once; longer ones by the selection of
+ * Layers of at most "row_max" elements (scadles_set_option) are selected as
+ * (device, layer) rows, all at once: one workgroup per row, or, for rows of
+ * more than "row_split" elements, one workgroup per 16384-element part of the
+ * row in each of its passes. Longer layers are selected by the selection of
  * scadles_topk_select, one layer after the other, overlapped with each other
  * on a second and third stream the library creates per GPU (default
- * priority; the caller's stream waits for them before the call's work ends
- * on it). Results do not depend on this split. Feed the sets to
+ * priority; those streams start after the caller's earlier work on `stream`,
+ * and the caller's stream waits for them before the call's work ends on it).
+ * Results do not depend on these splits. Feed the sets to
  * scadles_weighted_aggregate for Eqn 4b, or use scadles_step_fused_layers.
  * Same error convention as above.                                           */
 uint64_t scadles_layers_k(const uint64_t* seg_off, uint32_t L, double ratio);
@@ -374,11 +377,18 @@ const char* scadles_last_error(void);
  *                       on a second stream the library creates per GPU, at the
  *                       default priority). Results do not depend on it.
  *   "row_max"        0..2^32-1 (default 2^21): in the per-layer selection,
- *                       layers of at most this many elements are selected by
- *                       one workgroup per (device, layer); longer ones by the
- *                       multi-launch selection, consecutive ones pipelined on
- *                       the library's second stream and the short layers' rows
- *                       on a third. Results do not depend on it.
+ *                       layers of at most this many elements are selected as
+ *                       (device, layer) rows; longer ones by the multi-launch
+ *                       selection, consecutive ones pipelined on the library's
+ *                       second stream and the rows on a third. Results do
+ *                       not depend on it.
+ *   "row_split"      0..2^32-1 (default 2^18; at least 65536 takes effect):
+ *                       rows of more than this many elements are read by one
+ *                       workgroup per 16384-element part (their candidates
+ *                       staged, so each row is read once) instead of one
+ *                       workgroup per row, unless their ratio is so high that
+ *                       a part's candidates could exceed half its elements.
+ *                       Results do not depend on it.
  * Returns SCADLES_EINVAL for an unknown name or a value out of range.       */
 scadles_status scadles_set_option(const char* name, int64_t value);
 

@@ -40,6 +40,10 @@ namespace {
 std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0}, g_parts{1}, g_inject_count_error{0};
 // per-layer selection: layers of at most this many elements go to the row kernels
 std::atomic<int64_t> g_row_max{1 << 21};
+std::atomic<int64_t> g_row_split{1 << 18};
+// Per-layer selection: the short layers' rows on a third stream beside the
+// long layers (true) or on the caller's stream before them (false).
+constexpr bool kRowsBeside = true;
 
 scadles_status hip_fail(hipError_t e, const char* where)
 {
@@ -79,9 +83,9 @@ struct StreamSet {
   // per-layer selection: the short layers' rows run on s3 beside the long layers
   hipStream_t s3 = nullptr;
   hipEvent_t fork = nullptr, rows_done = nullptr;
-  // long layers: end of a layer's main pass; end of the rest of the last layer
-  // that used each of the two workspace regions
-  hipEvent_t layer_main = nullptr, post_done[2] = {};
+  // long layers: end of a layer's main pass; end of the bracket of the layer
+  // using each of the two workspace regions; end of all the layers' rests
+  hipEvent_t layer_main = nullptr, bracket_done[2] = {}, rests_done = nullptr;
   std::mutex rows_mu;
 };
 constexpr int kMaxGpus = 64;
@@ -104,7 +108,8 @@ StreamSet* stream_set()
     if (hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess) return nullptr;
     if (hipEventCreateWithFlags(&ss.rows_done, hipEventDisableTiming) != hipSuccess) return nullptr;
     if (hipEventCreateWithFlags(&ss.layer_main, hipEventDisableTiming) != hipSuccess) return nullptr;
-    for (auto& e : ss.post_done)
+    if (hipEventCreateWithFlags(&ss.rests_done, hipEventDisableTiming) != hipSuccess) return nullptr;
+    for (auto& e : ss.bracket_done)
       if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
     ss.ready = true;
   }
@@ -345,24 +350,22 @@ uint32_t parts_for(const Layout& L)
   return (uint32_t)p;
 }
 
-scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double delta, double* energies,
-                          uint8_t* compressed, hipStream_t s, ProfRec* pr, uint32_t* lb = nullptr,
-                          const scadles_step_options* opt = nullptr, uint32_t idx_base = 0,
-                          bool energies_add = false, hipStream_t s2_detached = nullptr,
-                          hipEvent_t main_done = nullptr)
+// Kernel context and launch plan of one selection call.
+void select_setup(const Layout& L, void* ws, double delta, double* energies, uint8_t* compressed, uint32_t* lb,
+                  const scadles_step_options* opt, uint32_t idx_base, bool energies_add, Ctx& c, SelectPlan& p)
 {
-  Ctx c = make_ctx(L, ws);
+  c = make_ctx(L, ws);
   c.delta = delta;
   c.energies_out = energies;
   c.compressed_out = compressed;
   c.force_fallback = g_force_fallback.load() ? 1u : 0u;
   c.inject_count_error = g_inject_count_error.load() ? 1u : 0u;
-  SelectPlan p;
   p.any_fast = L.any_fast;
   p.sample_blocks = ceil_div_u64(L.s_n, kSBlk);
   const uint64_t tiles = (uint64_t)L.K * L.tpd;
   p.full_workers = (uint32_t)(tiles < (uint64_t)kFullWorkers ? tiles : (uint64_t)kFullWorkers);
   p.parts = parts_for(L);
+  p.beside = 0;
   c.lb = lb;
   c.nrange = L.nrange;
   c.idx_base = idx_base;
@@ -372,13 +375,15 @@ scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double d
     c.ewma_beta = opt->ewma_beta;
     c.counters = opt->counters;
   }
-  if (s2_detached) {
-    // one group; the rest after the main pass on s2_detached, not joined
-    p.parts = 1;
-    const hipError_t e = launch_select_detached(c, a, p, s, s2_detached, main_done);
-    if (e != hipSuccess) return hip_fail(e, "select launch");
-    return SCADLES_OK;
-  }
+}
+
+scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double delta, double* energies,
+                          uint8_t* compressed, hipStream_t s, ProfRec* pr, uint32_t* lb = nullptr,
+                          const scadles_step_options* opt = nullptr)
+{
+  Ctx c;
+  SelectPlan p;
+  select_setup(L, ws, delta, energies, compressed, lb, opt, 0, false, c, p);
   if (pr) pr->parts = p.parts;
   StreamSet* ss = p.parts > 1 ? stream_set() : nullptr;
   if (p.parts > 1 && !ss) return fail(SCADLES_EHIP, "could not create the pipeline stream");
@@ -530,8 +535,30 @@ uint64_t scadles_layers_k(const uint64_t* seg_off, uint32_t L, double ratio)
 // layer's, for layers selected by the multi-launch path) and after it the
 // row region (layer table, row descriptors, per-row energies).
 struct LayersWs {
-  size_t sel = 0, table = 0, rows = 0, row_e = 0, e_long = 0, total = 0;
+  size_t sel = 0, table = 0, rows = 0, row_e = 0, e_long = 0, bst = 0, chunk = 0, cand = 0, part_e = 0, total = 0;
 };
+
+// Parts of a split row of n elements (the virtual row [0, n + shift), shift <= 3).
+static uint64_t row_parts_of(uint64_t n) { return ceil_div_u64(n + 3, kRowPartLen); }
+
+// Capacity of one wave's candidate region in the split rows of a layer of n
+// elements: twice the wave's share of 2 k_max + 4096 (k_max the largest k of
+// the devices) plus 64, in multiples of 64; 0 when that exceeds half a
+// wave's elements (high ratios): such rows are not split. It falls as n grows,
+// so the split rows are the longest ones.
+static uint64_t row_wave_cap(uint64_t n, const double* ratios, uint32_t K)
+{
+  uint64_t kmax = 0;
+  for (uint32_t j = 0; j < K; ++j) kmax = std::max<uint64_t>(kmax, k_rule(n, ratios[j]));
+  const uint64_t share = (2 * (2 * kmax + 4096) * kRowWaveLen + n - 1) / n + 64;
+  return share <= kRowWaveLen / 2 ? (share + 63) / 64 * 64 : 0;
+}
+
+// Entries of a split row's candidate list (0: the row is not split).
+static uint64_t row_cand_list(uint64_t n, const double* ratios, uint32_t K)
+{
+  return row_parts_of(n) * kRowPartWaves * row_wave_cap(n, ratios, K);
+}
 
 static LayersWs layers_ws(uint32_t K, const uint64_t* seg_off, uint32_t L, const double* ratios)
 {
@@ -543,12 +570,28 @@ static LayersWs layers_ws(uint32_t K, const uint64_t* seg_off, uint32_t L, const
     if (b > most) most = b;
   }
   // two selection regions: consecutive long layers alternate between them
+  // split rows: room for every layer that could be split under any option
+  uint64_t nbig = 0, parts = 0, cands = 0;
+  for (uint32_t l = 0; l < L; ++l) {
+    const uint64_t nl = seg_off[l + 1] - seg_off[l];
+    if (nl > kRowSplitMin && row_cand_list(nl, ratios, K) > 0) {
+      ++nbig;
+      parts += row_parts_of(nl);
+      cands += row_cand_list(nl, ratios, K);
+    }
+  }
+  parts *= K;
+  cands *= K;
   w.sel = align256(most);
   w.table = 2 * w.sel;
-  w.rows = align256(w.table + sizeof(uint64_t) * (2ull * L + 1));
+  w.rows = align256(w.table + sizeof(uint64_t) * (4ull * L + 3));
   w.row_e = align256(w.rows + sizeof(RowDesc) * (size_t)K * L);
   w.e_long = align256(w.row_e + sizeof(double) * 2ull * K * L);
-  w.total = align256(w.e_long + sizeof(double) * 2ull * K);
+  w.bst = align256(w.e_long + sizeof(double) * 2ull * K);
+  w.chunk = align256(w.bst + sizeof(BigRowState) * (size_t)(nbig * K));
+  w.cand = align256(w.chunk + sizeof(uint32_t) * (size_t)kChunkWords * kRowPartChunks * parts);
+  w.part_e = align256(w.cand + sizeof(uint64_t) * cands);
+  w.total = align256(w.part_e + sizeof(double) * 2ull * kRowPartWaves * parts);
   return w;
 }
 
@@ -577,9 +620,30 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
   std::stable_sort(shorts.begin(), shorts.end(), [&](uint32_t a, uint32_t b) {
     return seg_off[a + 1] - seg_off[a] > seg_off[b + 1] - seg_off[b];
   });
+  // The longest of them, those of more than row_split elements, are split into
+  // parts, each read by a workgroup of its own.
+  const uint64_t split = std::max<uint64_t>((uint64_t)g_row_split.load(), kRowSplitMin);
+  uint32_t Lb = 0;
+  while (Lb < shorts.size()) {
+    const uint64_t nl = seg_off[shorts[Lb] + 1] - seg_off[shorts[Lb]];
+    if (nl <= split || row_cand_list(nl, ratios, K) == 0) break;
+    ++Lb;
+  }
   std::vector<uint64_t> table(2ull * L + 1, ~0ull);
   for (uint32_t l = 0; l <= L; ++l) table[l] = seg_off[l];
   for (size_t q = 0; q < shorts.size(); ++q) table[L + 1 + shorts[q]] = q;
+  uint64_t part_pre = 0;
+  for (uint32_t q = 0; q < Lb; ++q) {
+    table.push_back(part_pre);
+    part_pre += row_parts_of(seg_off[shorts[q] + 1] - seg_off[shorts[q]]);
+  }
+  table.push_back(part_pre);
+  uint64_t cand_pre = 0;
+  for (uint32_t q = 0; q < Lb; ++q) {
+    table.push_back(cand_pre);
+    cand_pre += row_cand_list(seg_off[shorts[q] + 1] - seg_off[shorts[q]], ratios, K);
+  }
+  table.push_back(cand_pre);
   RowsCtx rc;
   rc.table = reinterpret_cast<const uint64_t*>(base + lw.table);
   rc.rows = reinterpret_cast<RowDesc*>(base + lw.rows);
@@ -587,6 +651,12 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
   rc.K = K;
   rc.L = L;
   rc.Ls = (uint32_t)shorts.size();
+  rc.Lb = Lb;
+  rc.nparts = (uint32_t)(part_pre * K);
+  rc.bst = reinterpret_cast<BigRowState*>(base + lw.bst);
+  rc.chunk = reinterpret_cast<uint32_t*>(base + lw.chunk);
+  rc.cand = reinterpret_cast<uint64_t*>(base + lw.cand);
+  rc.part_e = reinterpret_cast<double*>(base + lw.part_e);
   RowsPrep rp;
   memset(&rp, 0, sizeof(rp));
   for (uint32_t j = 0; j < K; ++j) {
@@ -596,39 +666,33 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
     rp.ratio[j] = ratios[j];
   }
   const bool any_long = rc.Ls < L;
-  // With long layers, consecutive long layers pipeline: each one's main pass
-  // runs on s and the rest of its selection on the library's second stream,
-  // the layers alternating between two workspace regions (a region is reused
-  // once the layer before last has finished with it). The rows of the short
-  // layers run on the third stream beside them; the long layers' energies go
-  // to their own accumulator and both are summed once s has waited for all.
+  // Consecutive long layers pipeline over two workspace regions: each one's
+  // main pass runs on s, everything after it on the library's second stream
+  // s2, and the bracket of the next layer goes to s2 ahead of that rest (right
+  // after the rest of the layer before, the last user of its region), so it
+  // runs during the main pass. The first layer's bracket runs on s, and only
+  // then do the rows of the short layers start on the third stream beside
+  // them: their workgroups fill whole compute units and would hold the small
+  // bracket kernels back. The long layers' energies go to an accumulator of
+  // their own when rows run beside them; both are summed once s has waited
+  // for everything.
   StreamSet* ss = any_long ? stream_set() : nullptr;
+  if (any_long && !ss) return fail(SCADLES_EHIP, "could not create the layer pipeline streams");
   std::unique_lock<std::mutex> lk;
   if (ss) lk = std::unique_lock<std::mutex>(ss->rows_mu);
-  const bool rows_beside = ss && rc.Ls > 0;
-  hipStream_t sr = rows_beside ? ss->s3 : s;
-  hipError_t e = hipSuccess;
-  if (rows_beside) {
-    e = hipEventRecord(ss->fork, s);
-    if (e == hipSuccess) e = hipStreamWaitEvent(sr, ss->fork, 0);
-    if (e != hipSuccess) return hip_fail(e, "row stream fork");
-  }
-  e = launch_put_table(table.data(), table.size(), reinterpret_cast<uint64_t*>(base + lw.table), sr);
-  if (e != hipSuccess) return hip_fail(e, "layer table");
-  e = launch_rows(rc, rp, rows_beside ? nullptr : energies, sr);
-  if (e != hipSuccess) return hip_fail(e, "row selection");
-  if (rows_beside) {
-    e = hipEventRecord(ss->rows_done, sr);
-    if (e != hipSuccess) return hip_fail(e, "row stream join");
-  }
+  const bool both = ss && rc.Ls > 0;               // long and short layers: energies summed at the end
+  const bool rows_beside = both && kRowsBeside;
+  double* e_long = both ? reinterpret_cast<double*>(base + lw.e_long) : energies;
 
-  // Longer layers: the multi-launch selection, one layer after the other, its
-  // indices offset by the layer's start and its energies added to those of the
-  // layers before.
-  double* e_long = rows_beside ? reinterpret_cast<double*>(base + lw.e_long) : energies;
+  // Long layers: the multi-launch selection of each, its indices offset by the
+  // layer's start, its energies added to those of the long layers before.
+  struct LongLayer {
+    Ctx c;
+    SelectPlan p;
+    PrepArgs a;
+  };
+  std::vector<LongLayer> longs;
   uint64_t at[kMaxK] = {};          // where layer l's entries start in device j's output
-  bool first = ss ? true : rc.Ls == 0;
-  uint32_t li = 0;                  // long layers so far
   for (uint32_t l = 0; l < L; ++l) {
     const uint64_t off = seg_off[l], nl = seg_off[l + 1] - off;
     if (nl <= row_max) {
@@ -637,7 +701,9 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
     }
     Layout Ll;
     make_layout(K, nl, ratios, g_force_exact.load() != 0, true, Ll);
-    PrepArgs a;
+    longs.emplace_back();
+    LongLayer& ll = longs.back();
+    PrepArgs& a = ll.a;
     memset(&a, 0, sizeof(a));
     for (uint32_t j = 0; j < K; ++j) {
       a.grad[j] = grads[j] + off;
@@ -650,31 +716,68 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
       a.r_hi[j] = Ll.r_hi[j];
       at[j] += Ll.k[j];
     }
-    const uint32_t region = li & 1u;
-    void* wsr = ss ? static_cast<void*>(base + region * lw.sel) : ws;
-    if (ss && li >= 2) {
-      e = hipStreamWaitEvent(s, ss->post_done[region], 0);
-      if (e != hipSuccess) return hip_fail(e, "layer pipeline");
-    }
-    if (scadles_status st = run_select(Ll, a, wsr, INFINITY, e_long, nullptr, s, nullptr, nullptr, nullptr,
-                                       (uint32_t)off, !first, ss ? ss->s2 : nullptr, ss ? ss->layer_main : nullptr))
-      return st;
-    if (ss) {
-      e = hipEventRecord(ss->post_done[region], ss->s2);
-      if (e != hipSuccess) return hip_fail(e, "layer pipeline");
-    }
-    first = false;
-    ++li;
+    const size_t region = (longs.size() - 1) & 1u;
+    select_setup(Ll, base + region * lw.sel, INFINITY, e_long, nullptr, nullptr, nullptr, (uint32_t)off,
+                 longs.size() > 1, ll.c, ll.p);
+    ll.p.parts = 1;
+    ll.p.beside = 1;
   }
-  if (ss && li > 0) {
-    // the second stream runs the layers' rests in order: the last one's end is all of them
-    e = hipStreamWaitEvent(s, ss->post_done[(li - 1) & 1u], 0);
+
+  hipError_t e = hipSuccess;
+  if (ss) {
+    // the library's streams start after the caller's earlier work on s (which may write the gradients)
+    e = hipEventRecord(ss->fork, s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(ss->s2, ss->fork, 0);
+    if (e != hipSuccess) return hip_fail(e, "stream fork");
+  }
+  if (!longs.empty()) {
+    e = launch_bracket(longs[0].c, longs[0].a, longs[0].p, s);
+    if (e != hipSuccess) return hip_fail(e, "layer bracket");
+  }
+  hipStream_t sr = rows_beside ? ss->s3 : s;
+  if (rows_beside) {
+    e = hipEventRecord(ss->fork, s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(sr, ss->fork, 0);
+    if (e != hipSuccess) return hip_fail(e, "row stream fork");
+  }
+  e = launch_put_table(table.data(), table.size(), reinterpret_cast<uint64_t*>(base + lw.table), sr);
+  if (e != hipSuccess) return hip_fail(e, "layer table");
+  e = launch_rows(rc, rp, both ? nullptr : energies, sr);
+  if (e != hipSuccess) return hip_fail(e, "row selection");
+  if (rows_beside) {
+    e = hipEventRecord(ss->rows_done, sr);
+    if (e != hipSuccess) return hip_fail(e, "row stream join");
+  }
+  for (size_t li = 0; li < longs.size(); ++li) {
+    const LongLayer& ll = longs[li];
+    if (li > 0) {
+      e = hipStreamWaitEvent(s, ss->bracket_done[li & 1u], 0);
+      if (e != hipSuccess) return hip_fail(e, "layer pipeline");
+    }
+    e = launch_main(ll.c, ll.a, s);
+    if (e == hipSuccess) e = hipEventRecord(ss->layer_main, s);
+    if (e == hipSuccess && li + 1 < longs.size()) {
+      const LongLayer& nx = longs[li + 1];
+      e = launch_bracket(nx.c, nx.a, nx.p, ss->s2);
+      if (e == hipSuccess) e = hipEventRecord(ss->bracket_done[(li + 1) & 1u], ss->s2);
+    }
+    if (e == hipSuccess) e = hipStreamWaitEvent(ss->s2, ss->layer_main, 0);
+    if (e == hipSuccess) e = launch_rest(ll.c, ll.p, ss->s2);
+    if (e != hipSuccess) return hip_fail(e, "layer pipeline");
+  }
+  if (!longs.empty()) {
+    // s2 runs the layers' rests in order: its last one's end is all of them
+    e = hipEventRecord(ss->rests_done, ss->s2);
+    if (e == hipSuccess) e = hipStreamWaitEvent(s, ss->rests_done, 0);
     if (e != hipSuccess) return hip_fail(e, "layer pipeline join");
   }
   if (rows_beside) {
     e = hipStreamWaitEvent(s, ss->rows_done, 0);
-    if (e == hipSuccess && energies) e = launch_rows_energy(rc, energies, e_long, s);
     if (e != hipSuccess) return hip_fail(e, "row stream join");
+  }
+  if (both && energies) {
+    e = launch_rows_energy(rc, energies, e_long, s);
+    if (e != hipSuccess) return hip_fail(e, "layer energies");
   }
   return SCADLES_OK;
 }
@@ -1056,6 +1159,10 @@ scadles_status scadles_set_option(const char* name, int64_t value)
   else if (!strcmp(name, "row_max")) {
     if (value < 0 || value > 0xFFFFFFFFll) return fail(SCADLES_EINVAL, "row_max must be in [0, 2^32 - 1]");
     g_row_max = value;
+  }
+  else if (!strcmp(name, "row_split")) {
+    if (value < 0 || value > 0xFFFFFFFFll) return fail(SCADLES_EINVAL, "row_split must be in [0, 2^32 - 1]");
+    g_row_split = value;
   }
   else if (!strcmp(name, "parts")) {
     if (value < 1 || value > (int64_t)kMaxParts) return fail(SCADLES_EINVAL, "parts must be in [1, %u]", kMaxParts);

@@ -299,31 +299,15 @@ __device__ inline uint32_t row_select_global(const Row& row, uint64_t vend, uint
   return prefix;
 }
 
-// The selection of one row. A systematic sample (256-element chunks every
-// kRowSampleStride elements; the whole row when it is short) gives a bracket
-// [t_lo, t_hi) that holds the k-th largest key with high probability: the
-// bins of its 13-bit histogram around k's expected sample rank, six standard
-// deviations and 8 ranks either side. One read of the row then counts the keys
-// at or above t_hi, gathers the keys inside the bracket into LDS and sums g^2;
-// the k-th largest key is selected among the gathered ones. If the bracket
-// missed or overflowed LDS, the digits are decided over the whole row instead.
-// A last read writes the kept entries in index order.
-__global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
+// The bracket [t_lo, t_hi) of a row from a systematic sample (256-element
+// chunks every kRowSampleStride elements; the whole row when it is short):
+// the bins of its 13-bit histogram (in shist, kRowCand words of LDS) around
+// k's expected sample rank, six standard deviations and 8 ranks either side.
+__device__ inline void row_bracket(const RowDesc& d, const Row& row, uint64_t vend, uint32_t* shist, uint32_t* s_w,
+                                   uint32_t* s_res, uint32_t& t_lo, uint32_t& t_hi)
 {
-  __shared__ uint32_t hist[kRowBins];
-  __shared__ uint32_t cand[kRowCand];
-  __shared__ uint32_t s_w[kRowWaves];
-  __shared__ uint32_t s_res[4];
-  __shared__ double s_d[kRowWaves];
-  __shared__ uint32_t s_chunk[2 * kRowChunks];
-  const RowDesc d = rc.rows[blockIdx.x];
+  static_assert((1 << kRowSampleBits) <= kRowCand, "the sample histogram fits the candidate array");
   const uint32_t tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
-  const Row row{gptr(d.grad), ((uint64_t)d.grad >> 2) & 3u, d.n};
-  const uint64_t vend = (uint64_t)d.n + row.shift;
-
-  // 1. sample histogram (13-bit digit, in the candidate array's memory)
-  uint32_t* shist = cand;
-  static_assert((1 << kRowSampleBits) <= kRowCand, "the sample histogram lives in the candidate array");
   const bool whole = d.n <= (uint32_t)kRowWholeMax;
   const uint64_t stride = whole ? 256u : (uint64_t)kRowSampleStride;
   for (uint32_t i = tid; i < (1u << kRowSampleBits); i += kRowBlock) shist[i] = 0u;
@@ -363,15 +347,93 @@ __global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
   }
   if (tid == 0) s_res[0] = s_res[1] = s_res[2] = 0u;
   row_select_bin(shist, kRowSampleBits, r_lo, s_w, s_res);
-  const uint32_t t_lo = s_res[0] << (31 - kRowSampleBits);
+  t_lo = s_res[0] << (31 - kRowSampleBits);
   __syncthreads();
-  uint32_t t_hi = kKeyInf;
+  t_hi = kKeyInf;
   if (r_hi >= 1) {
     if (tid == 0) s_res[0] = s_res[1] = s_res[2] = 0u;
     row_select_bin(shist, kRowSampleBits, r_hi, s_w, s_res);
     t_hi = (s_res[0] + 1u) << (31 - kRowSampleBits);
     __syncthreads();
   }
+}
+
+// Ordered output of a whole row by one workgroup, without chunk tallies: per
+// workgroup round the waves' counts give each wave's starting position. Returns
+// this thread's share of the kept sum of squares.
+__device__ inline double row_write_ordered(const RowDesc& d, const Row& row, uint64_t vend, uint32_t thr,
+                                           uint32_t need, GLOBAL uint32_t* oi, GLOBAL float* ov, uint32_t* s_w)
+{
+  const uint32_t lane = lane_id(), w = threadIdx.x >> 6;
+  double e_kept = 0.0;
+  uint32_t run_g = 0, run_e = 0;
+#pragma unroll 1
+  for (uint64_t v0 = 0; v0 < vend; v0 += kRowRound) {
+    f4 x[kRowR];
+#pragma unroll
+    for (int r = 0; r < kRowR; ++r) {
+      const uint64_t v = row_pos(v0, w, r, lane);
+      x[r] = v < vend ? load4(row, v, false) : f4{0.f, 0.f, 0.f, 0.f};
+    }
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int r = 0; r < kRowR; ++r) {
+      const uint64_t v = row_pos(v0, w, r, lane);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const bool valid = v < vend && in_row(row, v + q);
+        const uint32_t key = key_of(x[r][q]);
+        cnt += (valid && key > thr) ? 1u : 0u;
+        cnt += (valid && key == thr) ? 0x10000u : 0u;
+      }
+    }
+    uint32_t wt = cnt;
+#pragma unroll
+    for (int dd = 32; dd >= 1; dd >>= 1) wt += __shfl_xor(wt, dd, 64);
+    if (lane == 0) s_w[w] = wt;
+    __syncthreads();
+    uint32_t wex = 0, tot = 0;
+    for (uint32_t i = 0; i < (uint32_t)kRowWaves; ++i) {
+      const uint32_t y = s_w[i];
+      wex += i < w ? y : 0u;
+      tot += y;
+    }
+    __syncthreads();
+    uint32_t rg = run_g + (wex & 0xFFFFu), re = run_e + (wex >> 16);
+#pragma unroll
+    for (int r = 0; r < kRowR; ++r)
+      row_write_round(x[r], row_pos(v0, w, r, lane), vend, row, d.base, thr, need, d.k, oi, ov, rg, re, e_kept);
+    run_g += tot & 0xFFFFu;
+    run_e += tot >> 16;
+  }
+  return e_kept;
+}
+
+// The selection of one row. A systematic sample (256-element chunks every
+// kRowSampleStride elements; the whole row when it is short) gives a bracket
+// [t_lo, t_hi) that holds the k-th largest key with high probability: the
+// bins of its 13-bit histogram around k's expected sample rank, six standard
+// deviations and 8 ranks either side. One read of the row then counts the keys
+// at or above t_hi, gathers the keys inside the bracket into LDS and sums g^2;
+// the k-th largest key is selected among the gathered ones. If the bracket
+// missed or overflowed LDS, the digits are decided over the whole row instead.
+// A last read writes the kept entries in index order.
+__global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
+{
+  __shared__ uint32_t hist[kRowBins];
+  __shared__ uint32_t cand[kRowCand];
+  __shared__ uint32_t s_w[kRowWaves];
+  __shared__ uint32_t s_res[4];
+  __shared__ double s_d[kRowWaves];
+  __shared__ uint32_t s_chunk[2 * kRowChunks];
+  const RowDesc d = rc.rows[rc.Lb * rc.K + blockIdx.x];
+  const uint32_t tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
+  const Row row{gptr(d.grad), ((uint64_t)d.grad >> 2) & 3u, d.n};
+  const uint64_t vend = (uint64_t)d.n + row.shift;
+
+  // 1. bracket from the sample
+  uint32_t t_lo, t_hi;
+  row_bracket(d, row, vend, cand, s_w, s_res, t_lo, t_hi);
 
   // 2. one read: keys >= t_hi counted, keys in [t_lo, t_hi) gathered, sum g^2
   if (tid == 0) s_res[3] = 0u;
@@ -511,50 +573,413 @@ __global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
         row_write_round(x[r], row_pos(v0, w, r, lane), vend, row, d.base, thr, need, d.k, oi, ov, rg, re, e_kept);
     }
   } else {
-    // per workgroup round, the waves' counts give each wave's starting position
-    uint32_t run_g = 0, run_e = 0;
-#pragma unroll 1
-    for (uint64_t v0 = 0; v0 < vend; v0 += kRowRound) {
-      f4 x[kRowR];
-#pragma unroll
-      for (int r = 0; r < kRowR; ++r) {
-        const uint64_t v = row_pos(v0, w, r, lane);
-        x[r] = v < vend ? load4(row, v, false) : f4{0.f, 0.f, 0.f, 0.f};
-      }
-      uint32_t cnt = 0;
-#pragma unroll
-      for (int r = 0; r < kRowR; ++r) {
-        const uint64_t v = row_pos(v0, w, r, lane);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const bool valid = v < vend && in_row(row, v + q);
-          const uint32_t key = key_of(x[r][q]);
-          cnt += (valid && key > thr) ? 1u : 0u;
-          cnt += (valid && key == thr) ? 0x10000u : 0u;
-        }
-      }
-      uint32_t wt = cnt;
-#pragma unroll
-      for (int dd = 32; dd >= 1; dd >>= 1) wt += __shfl_xor(wt, dd, 64);
-      if (lane == 0) s_w[w] = wt;
-      __syncthreads();
-      uint32_t wex = 0, tot = 0;
-      for (uint32_t i = 0; i < (uint32_t)kRowWaves; ++i) {
-        const uint32_t y = s_w[i];
-        wex += i < w ? y : 0u;
-        tot += y;
-      }
-      __syncthreads();
-      uint32_t rg = run_g + (wex & 0xFFFFu), re = run_e + (wex >> 16);
-#pragma unroll
-      for (int r = 0; r < kRowR; ++r)
-        row_write_round(x[r], row_pos(v0, w, r, lane), vend, row, d.base, thr, need, d.k, oi, ov, rg, re, e_kept);
-      run_g += tot & 0xFFFFu;
-      run_e += tot >> 16;
-    }
+    e_kept = row_write_ordered(d, row, vend, thr, need, oi, ov, s_w);
   }
   const double ek = row_sum_f64(e_kept, s_d);
   if (tid == 0) rc.row_e[2ull * d.eslot + 1] = ek;
+}
+
+// ---- split rows --------------------------------------------------------------------------
+// A row longer than the split threshold is read by one workgroup per part:
+//   k_big_bracket  one workgroup per row: the sampled bracket [t_lo, t_hi)
+//                  (as k_rows computes it);
+//   k_big_gather   one workgroup per part, the one read of the row: sum of
+//                  g^2 and, per chunk, the keys >= t_hi counted and the
+//                  candidates (keys >= t_lo) staged in index order in the
+//                  wave's own region of the row's candidate list;
+//   k_big_select   one workgroup per row: the selection-interval keys (the
+//                  candidates below t_hi) collected in LDS, the threshold
+//                  selected among them, then every chunk's kept entries above /
+//                  equal to it (counted on its candidates) and their exclusive
+//                  prefix in index order. A row whose bracket missed, or whose
+//                  candidates overflowed a wave's region, is selected and
+//                  written here, by this workgroup alone, as k_rows does it;
+//   k_big_write    one workgroup per part: every chunk's kept entries, from its
+//                  candidates, at the positions from its prefix;
+//   k_big_finish   the kept energy of each row from its waves' sums, in order.
+// No workgroup waits for another inside a launch, and the part kernels have
+// no barrier and no atomic but the rare overflow flag.
+constexpr int kPartWaves = (int)kRowPartWaves;
+constexpr int kPartBlock = 64 * kPartWaves;
+constexpr int kWaveChunks = kRowPartChunks / kPartWaves;    // chunks of one wave, loaded at once
+static_assert(kRowChunkLen == 256u * kRowR, "a chunk is one wave's kRowR rounds");
+static_assert(kWaveChunks * kPartWaves == (int)kRowPartChunks, "a part's chunks are split evenly over its waves");
+
+// Part workgroup g: its row (index into rc.rows), part, the row's first part
+// workgroup and number of parts.
+struct PartOf {
+  uint32_t b, p, g0, np;
+};
+
+__device__ inline PartOf part_of(const RowsCtx& rc, uint32_t g)
+{
+  const uint64_t* pre = rc.table + 2ull * rc.L + 1;
+  uint32_t lo = 0, hi = rc.Lb;     // pre[lo] * K <= g < pre[hi] * K
+  while (hi - lo > 1) {
+    const uint32_t mid = (lo + hi) / 2;
+    if (pre[mid] * rc.K <= g) lo = mid;
+    else hi = mid;
+  }
+  const uint32_t np = (uint32_t)(pre[lo + 1] - pre[lo]);
+  const uint32_t rel = g - (uint32_t)(pre[lo] * rc.K);
+  const uint32_t j = rel / np;
+  PartOf r;
+  r.b = lo * rc.K + j;
+  r.p = rel - j * np;
+  r.g0 = g - r.p;
+  r.np = np;
+  return r;
+}
+
+// Split row b's first part workgroup and number of parts.
+__device__ inline void row_parts(const RowsCtx& rc, uint32_t b, uint32_t& g0, uint32_t& np)
+{
+  const uint64_t* pre = rc.table + 2ull * rc.L + 1;
+  const uint32_t q = b / rc.K, j = b - q * rc.K;
+  np = (uint32_t)(pre[q + 1] - pre[q]);
+  g0 = (uint32_t)(pre[q] * rc.K) + j * np;
+}
+
+// Split row b's candidate list: its first entry and the capacity of one wave's region.
+__device__ inline void row_cands(const RowsCtx& rc, uint32_t b, uint64_t& off, uint32_t& wcap)
+{
+  const uint64_t* pre = rc.table + 2ull * rc.L + 1;             // part_pre, then cand_pre
+  const uint64_t* cpre = pre + rc.Lb + 1;
+  const uint32_t q = b / rc.K, j = b - q * rc.K;
+  const uint64_t per_row = cpre[q + 1] - cpre[q];
+  off = cpre[q] * rc.K + (uint64_t)j * per_row;
+  wcap = (uint32_t)(per_row / ((pre[q + 1] - pre[q]) * kPartWaves));
+}
+
+// Fixed-order sum of n doubles by one wave (lane l adds l, l + 64, ...).
+__device__ inline double wave_sum_list(const double* a, uint32_t n)
+{
+  double v = 0.0;
+  for (uint32_t i = lane_id(); i < n; i += 64) v += a[i];
+  return wave_sum_f64(v);
+}
+
+__global__ __launch_bounds__(kRowBlock) void k_big_bracket(RowsCtx rc)
+{
+  __shared__ uint32_t shist[kRowCand];
+  __shared__ uint32_t s_w[kRowWaves];
+  __shared__ uint32_t s_res[4];
+  const RowDesc d = rc.rows[blockIdx.x];
+  const Row row{gptr(d.grad), ((uint64_t)d.grad >> 2) & 3u, d.n};
+  uint32_t t_lo, t_hi;
+  row_bracket(d, row, (uint64_t)d.n + row.shift, shist, s_w, s_res, t_lo, t_hi);
+  if (threadIdx.x == 0) {
+    BigRowState st;
+    __builtin_memset(&st, 0, sizeof(st));
+    st.t_lo = t_lo;
+    st.t_hi = t_hi;
+    rc.bst[blockIdx.x] = st;
+  }
+}
+
+// Gather-pass counts of one chunk in one wave (x holds its kRowR rounds: lane
+// l has elements v0 + r * 256 + 4 l .. + 3 of round r): keys >= t_hi and
+// candidates (keys >= t_lo); e_all accumulates g^2. kFull: every element is in
+// the row.
+template <bool kFull>
+__device__ inline void gather_count(const f4 (&x)[kRowR], uint64_t v0, uint64_t vend, const Row& row, uint32_t t_lo,
+                                    uint32_t t_hi, uint32_t& nsure, uint32_t& ncand, double& e_all)
+{
+  nsure = ncand = 0;
+#pragma unroll
+  for (int r = 0; r < kRowR; ++r) {
+    const uint64_t v = v0 + r * 256u;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bool valid = kFull || (v < vend && in_row(row, v + q));
+      const uint32_t key = key_of(x[r][q]);
+      nsure += (uint32_t)__builtin_popcountll(ballot(valid && key >= t_hi));
+      ncand += (uint32_t)__builtin_popcountll(ballot(valid && key >= t_lo));
+      if (kFull) e_all = __builtin_fma((double)x[r][q], (double)x[r][q], e_all);
+      else if (valid) e_all = __builtin_fma((double)x[r][q], (double)x[r][q], e_all);
+    }
+  }
+}
+
+// Stages one chunk's candidates at cand[at ..] (index order: round, lane,
+// component), at most up to position cap.
+template <bool kFull>
+__device__ inline void gather_write(const f4 (&x)[kRowR], uint64_t v0, uint64_t vend, const Row& row, uint32_t t_lo,
+                                    uint32_t at, GLOBAL uint64_t* cand, uint32_t cap)
+{
+#pragma unroll
+  for (int r = 0; r < kRowR; ++r) {
+    const uint64_t v = v0 + r * 256u;
+    bool f[4];
+    uint64_t bc[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bool valid = kFull || (v < vend && in_row(row, v + q));
+      f[q] = valid && key_of(x[r][q]) >= t_lo;
+      bc[q] = ballot(f[q]);
+    }
+    if ((bc[0] | bc[1] | bc[2] | bc[3]) == 0ull) continue;
+    uint32_t cp = at + mbcnt(bc[0]) + mbcnt(bc[1]) + mbcnt(bc[2]) + mbcnt(bc[3]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (f[q]) {
+        if (cp < cap) cand[cp] = (uint64_t)(uint32_t)(v + q - row.shift) | ((uint64_t)__float_as_uint(x[r][q]) << 32);
+        ++cp;
+      }
+    }
+    at += (uint32_t)(__builtin_popcountll(bc[0]) + __builtin_popcountll(bc[1]) + __builtin_popcountll(bc[2]) +
+                     __builtin_popcountll(bc[3]));
+  }
+}
+
+// Each wave loads its kWaveChunks consecutive chunks at once, counts them and
+// stages their candidates in its region.
+__global__ __launch_bounds__(kPartBlock) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_big_gather(RowsCtx rc)
+{
+  const PartOf po = part_of(rc, blockIdx.x);
+  const RowDesc d = rc.rows[po.b];
+  GLOBAL BigRowState* st = gptr(rc.bst) + po.b;
+  const uint32_t lane = lane_id(), w = threadIdx.x >> 6;
+  const Row row{gptr(d.grad), ((uint64_t)d.grad >> 2) & 3u, d.n};
+  const uint64_t vend = (uint64_t)d.n + row.shift;
+  const uint32_t c0 = w * kWaveChunks;
+  const uint64_t vw = (uint64_t)po.p * kRowPartLen + (uint64_t)c0 * kRowChunkLen;   // the wave's first element
+  const bool full = vw >= row.shift && vw + (uint64_t)kWaveChunks * kRowChunkLen <= vend;
+  const uint64_t v0 = vw + 4u * lane;
+  f4 x[kWaveChunks][kRowR];
+  if (full) {
+    const GLOBAL float* p = row.p + (vw - row.shift) + 4u * lane;
+#pragma unroll
+    for (int c = 0; c < kWaveChunks; ++c)
+#pragma unroll
+      for (int r = 0; r < kRowR; ++r) x[c][r] = ld_stream4(p + c * kRowChunkLen + r * 256u);
+  } else {
+#pragma unroll
+    for (int c = 0; c < kWaveChunks; ++c)
+#pragma unroll
+      for (int r = 0; r < kRowR; ++r) {
+        const uint64_t v = v0 + (uint64_t)c * kRowChunkLen + r * 256u;
+        x[c][r] = v < vend ? load4(row, v, false) : f4{0.f, 0.f, 0.f, 0.f};
+      }
+  }
+  const uint32_t t_lo = st->t_lo, t_hi = st->t_hi;
+  uint64_t coff;
+  uint32_t wcap;
+  row_cands(rc, po.b, coff, wcap);
+  const uint32_t wbase = (po.p * kPartWaves + w) * wcap;       // the wave's region in the row's list
+  GLOBAL uint64_t* cand = gptr(rc.cand) + coff + wbase;
+  GLOBAL uint32_t* rec = gptr(rc.chunk) + ((uint64_t)blockIdx.x * kRowPartChunks + c0) * kChunkWords;
+  double e_all = 0.0;
+  uint32_t at = 0;
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const uint64_t vc = v0 + (uint64_t)c * kRowChunkLen;
+    uint32_t nsure, ncand;
+    if (full) gather_count<true>(x[c], vc, vend, row, t_lo, t_hi, nsure, ncand, e_all);
+    else gather_count<false>(x[c], vc, vend, row, t_lo, t_hi, nsure, ncand, e_all);
+    if (ncand) {
+      if (full) gather_write<true>(x[c], vc, vend, row, t_lo, at, cand, wcap);
+      else gather_write<false>(x[c], vc, vend, row, t_lo, at, cand, wcap);
+    }
+    if (lane == 0) {
+      const u4 w4 = {nsure, 0u, wbase + at, ncand};
+      *reinterpret_cast<GLOBAL u4*>(rec + c * kChunkWords) = w4;
+    }
+    at += ncand;
+  }
+  if (at > wcap && lane == 0) __hip_atomic_fetch_or(&st->ovf, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const double e = wave_sum_f64(e_all);
+  if (lane == 0) rc.part_e[(uint64_t)blockIdx.x * kPartWaves + w] = e;
+}
+
+__global__ __launch_bounds__(kRowBlock) void k_big_select(RowsCtx rc)
+{
+  __shared__ uint32_t hist[kRowBins];
+  __shared__ uint32_t cand[kRowCand];
+  __shared__ uint32_t s_w[kRowWaves];
+  __shared__ uint32_t s_res[4];
+  __shared__ double s_d[kRowWaves];
+  const uint32_t b = blockIdx.x, tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
+  const RowDesc d = rc.rows[b];
+  GLOBAL BigRowState* st = gptr(rc.bst) + b;
+  uint32_t g0, np;
+  row_parts(rc, b, g0, np);
+  uint64_t coff;
+  uint32_t wcap;
+  row_cands(rc, b, coff, wcap);
+  const GLOBAL uint64_t* list = gptr(rc.cand) + coff;
+  const uint32_t nch = np * kRowPartChunks;
+  GLOBAL uint32_t* ch = gptr(rc.chunk) + (uint64_t)g0 * kRowPartChunks * kChunkWords;
+  const Row row{gptr(d.grad), ((uint64_t)d.grad >> 2) & 3u, d.n};
+  const uint64_t vend = (uint64_t)d.n + row.shift;
+  const uint32_t t_hi = st->t_hi;
+  if (w == 0) {
+    const double ea = wave_sum_list(rc.part_e + (uint64_t)g0 * kPartWaves, np * kPartWaves);
+    if (lane == 0) rc.row_e[2ull * d.eslot] = ea;
+  }
+  // each thread a run of consecutive chunks (one chunk per thread for rows up
+  // to kRowBlock chunks); their records stay in registers for the first run
+  const uint32_t per = (nch + kRowBlock - 1) / kRowBlock;
+  const uint32_t c0 = tid * per < nch ? tid * per : nch, c1 = c0 + per < nch ? c0 + per : nch;
+  uint32_t sure = 0;
+  for (uint32_t c = c0; c < c1; ++c) sure += ch[kChunkWords * c];
+  uint32_t sure_all;
+  if (tid == 0) s_res[3] = 0u;
+  row_scan(sure, s_w, sure_all);
+  const bool ovf = st->ovf != 0u;
+  bool in_band = false;
+  uint32_t nband = 0;
+  // visit(key) for every staged candidate of the thread's chunks, eight loads in flight
+  auto each_key = [&](auto visit) {
+    for (uint32_t c = c0; c < c1; ++c) {
+      const uint32_t at = ch[kChunkWords * c + 2], n = ch[kChunkWords * c + 3];
+      for (uint32_t e0 = 0; e0 < n; e0 += 8) {
+        uint32_t kv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) kv[i] = e0 + i < n ? (uint32_t)(list[at + e0 + i] >> 32) & kKeyMask : kKeyInf;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (e0 + i < n) visit(kv[i]);
+      }
+    }
+  };
+  if (!ovf && sure_all < d.k) {
+    // the selection-interval keys: the candidates below t_hi
+    each_key([&](uint32_t key) {
+      if (key < t_hi) {
+        const uint32_t pos = atomicAdd(&s_res[3], 1u);
+        if (pos < (uint32_t)kRowCand) cand[pos] = key;
+      }
+    });
+    __syncthreads();
+    nband = s_res[3];
+    in_band = d.k - sure_all <= nband && nband <= (uint32_t)kRowCand;
+  }
+  if (in_band) {
+    uint32_t need = d.k - sure_all;
+    const uint32_t thr = row_select_lds(cand, nband, need, hist, s_w, s_res);
+    // the thread's chunks' candidates above / equal to the threshold, then
+    // their exclusive prefix in index order
+    uint32_t gsum = 0, esum = 0;
+    for (uint32_t c = c0; c < c1; ++c) {
+      const uint32_t at = ch[kChunkWords * c + 2], n = ch[kChunkWords * c + 3];
+      uint32_t g = 0, e = 0;
+      for (uint32_t e0 = 0; e0 < n; e0 += 8) {
+        uint32_t kv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) kv[i] = e0 + i < n ? (uint32_t)(list[at + e0 + i] >> 32) & kKeyMask : 0u;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          g += (e0 + i < n && kv[i] > thr) ? 1u : 0u;
+          e += (e0 + i < n && kv[i] == thr) ? 1u : 0u;
+        }
+      }
+      ch[kChunkWords * c] = g;
+      ch[kChunkWords * c + 1] = e;
+      gsum += g;
+      esum += e;
+    }
+    uint32_t tg, te;
+    uint32_t rg = row_scan(gsum, s_w, tg) - gsum;
+    uint32_t re = row_scan(esum, s_w, te) - esum;
+    for (uint32_t c = c0; c < c1; ++c) {
+      const uint32_t g = ch[kChunkWords * c], e = ch[kChunkWords * c + 1];
+      ch[kChunkWords * c] = rg;
+      ch[kChunkWords * c + 1] = re;
+      rg += g;
+      re += e;
+    }
+    if (tid == 0) {
+      st->thr = thr;
+      st->need = need;
+      st->slow = 0u;
+    }
+  } else {
+    // the bracket missed or a wave's candidates overflowed: this workgroup
+    // selects and writes the row on its own
+    uint32_t need = d.k;
+    const uint32_t thr = row_select_global(row, vend, need, hist, cand, s_w, s_res);
+    const double ek =
+        row_sum_f64(row_write_ordered(d, row, vend, thr, need, gptr(d.idx_out), gptr(d.val_out), s_w), s_d);
+    if (tid == 0) {
+      rc.row_e[2ull * d.eslot + 1] = ek;
+      st->slow = 1u;
+    }
+  }
+}
+
+// Kept entries of one chunk from its staged candidates (index order): n of
+// them at cand, run_g / run_e the kept entries above / equal to the threshold
+// before the chunk.
+__device__ inline void write_staged(const GLOBAL uint64_t* cand, uint32_t n, uint32_t base, uint32_t thr,
+                                    uint32_t need, uint32_t k, GLOBAL uint32_t* oi, GLOBAL float* ov, uint32_t run_g,
+                                    uint32_t run_e, double& e2)
+{
+  const uint32_t lane = lane_id();
+  for (uint32_t e0 = 0; e0 < n; e0 += 4 * 64) {
+    uint64_t w4[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      const uint32_t e = e0 + m * 64 + lane;
+      w4[m] = e < n ? cand[e] : 0ull;
+    }
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      if (e0 + m * 64 >= n) break;
+      const bool valid = e0 + m * 64 + lane < n;
+      const uint32_t vb = (uint32_t)(w4[m] >> 32), key = vb & kKeyMask;
+      const bool fg = valid && key > thr, fe = valid && key == thr;
+      const uint64_t bg = ballot(fg), be = ballot(fe);
+      const uint32_t gt_b = run_g + mbcnt(bg), eq_b = run_e + mbcnt(be);
+      if (fg || (fe && eq_b < need)) {
+        const uint32_t pos = gt_b + (eq_b < need ? eq_b : need);
+        const float v = __uint_as_float(vb);
+        if (pos < k) {
+          oi[pos] = (uint32_t)w4[m] + base;
+          ov[pos] = v;
+        }
+        e2 = __builtin_fma((double)v, (double)v, e2);
+      }
+      run_g += (uint32_t)__builtin_popcountll(bg);
+      run_e += (uint32_t)__builtin_popcountll(be);
+    }
+  }
+}
+
+__global__ __launch_bounds__(kPartBlock) void k_big_write(RowsCtx rc)
+{
+  const PartOf po = part_of(rc, blockIdx.x);
+  const GLOBAL BigRowState* st = gptr(rc.bst) + po.b;
+  const uint32_t lane = lane_id(), w = threadIdx.x >> 6;
+  double e_kept = 0.0;
+  if (!st->slow) {
+    const RowDesc d = rc.rows[po.b];
+    const uint32_t thr = st->thr, need = st->need;
+    uint64_t coff;
+    uint32_t wcap;
+    row_cands(rc, po.b, coff, wcap);
+    const GLOBAL uint64_t* list = gptr(rc.cand) + coff;
+    const GLOBAL uint32_t* rec = gptr(rc.chunk) + (uint64_t)blockIdx.x * kRowPartChunks * kChunkWords;
+    GLOBAL uint32_t* oi = gptr(d.idx_out);
+    GLOBAL float* ov = gptr(d.val_out);
+#pragma unroll
+    for (int c = 0; c < kWaveChunks; ++c) {
+      const u4 r4 = *reinterpret_cast<const GLOBAL u4*>(rec + (w * kWaveChunks + c) * kChunkWords);
+      if (r4[3]) write_staged(list + r4[2], r4[3], d.base, thr, need, d.k, oi, ov, r4[0], r4[1], e_kept);
+    }
+  }
+  const double e = wave_sum_f64(e_kept);
+  if (lane == 0) rc.part_e[((uint64_t)rc.nparts + blockIdx.x) * kPartWaves + w] = e;
+}
+
+__global__ __launch_bounds__(64) void k_big_finish(RowsCtx rc)
+{
+  const uint32_t b = blockIdx.x;
+  if (rc.bst[b].slow) return;
+  uint32_t g0, np;
+  row_parts(rc, b, g0, np);
+  const double ek = wave_sum_list(rc.part_e + ((uint64_t)rc.nparts + g0) * kPartWaves, np * kPartWaves);
+  if (threadIdx.x == 0) rc.row_e[2ull * rc.rows[b].eslot + 1] = ek;
 }
 
 // Per device: the energies of its short layers summed in layer order, plus
@@ -617,10 +1042,16 @@ hipError_t launch_put_table(const uint64_t* src, uint64_t count, uint64_t* dst, 
 hipError_t launch_rows(const RowsCtx& rc, const RowsPrep& rp, double* energies, hipStream_t s)
 {
   k_rows_prep<<<rc.K, 256, 0, s>>>(rc, rp);
-  if (rc.Ls > 0) {
-    k_rows<<<rc.Ls * rc.K, kRowBlock, 0, s>>>(rc);
-    if (energies) k_rows_energy<<<rc.K, 64, 0, s>>>(rc, energies, nullptr);
+  if (rc.Lb > 0) {
+    const uint32_t nb = rc.Lb * rc.K;
+    k_big_bracket<<<nb, kRowBlock, 0, s>>>(rc);
+    k_big_gather<<<rc.nparts, kPartBlock, 0, s>>>(rc);
+    k_big_select<<<nb, kRowBlock, 0, s>>>(rc);
+    k_big_write<<<rc.nparts, kPartBlock, 0, s>>>(rc);
+    k_big_finish<<<nb, 64, 0, s>>>(rc);
   }
+  if (rc.Ls > rc.Lb) k_rows<<<(rc.Ls - rc.Lb) * rc.K, kRowBlock, 0, s>>>(rc);
+  if (rc.Ls > 0 && energies) k_rows_energy<<<rc.K, 64, 0, s>>>(rc, energies, nullptr);
   return hipGetLastError();
 }
 

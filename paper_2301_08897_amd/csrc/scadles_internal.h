@@ -180,6 +180,7 @@ struct SelectPlan {
   uint32_t sample_blocks;     // sample workgroups per device
   uint32_t full_workers;      // grid-stride workgroups of the exact full-data path
   uint32_t parts;             // device groups, 1 .. kMaxParts
+  uint32_t beside;            // the rest runs beside other selections' main passes (small workgroups)
 };
 
 // Launchers (select.hip, aggregate.hip). done[parts] and join are events of
@@ -187,9 +188,11 @@ struct SelectPlan {
 // events described at launch_select.
 hipError_t launch_select(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s, hipStream_t s2,
                          hipEvent_t* done, hipEvent_t join, hipEvent_t* ev);
-// All devices in one group; the rest after the main pass on s2, not joined.
-hipError_t launch_select_detached(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s,
-                                  hipStream_t s2, hipEvent_t main_done);
+// All devices in one group, in three parts on streams of the caller's choice:
+// preparation and bracket, the main pass, the rest (see select.hip).
+hipError_t launch_bracket(const Ctx& c, const PrepArgs& a, const SelectPlan& p, hipStream_t s);
+hipError_t launch_main(const Ctx& c, const PrepArgs& a, hipStream_t s);
+hipError_t launch_rest(const Ctx& c, const SelectPlan& p, hipStream_t s);
 hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate, bool marks_done, hipStream_t s);
 hipError_t launch_marks(const AggArgs& a, const AggCtx& c, hipStream_t s);
 hipError_t launch_sgd(float* p, const float* g, uint64_t n, float lr, hipStream_t s);
@@ -230,11 +233,51 @@ struct RowsPrep {
   double ratio[kMaxK];
 };
 
+// Rows of more than the option "row_split" elements are split into parts of
+// kRowPartLen elements, each read by its own workgroup (k_big_* kernels), so
+// that one long row does not keep a single compute unit busy while the rest of
+// the GPU idles. A part is kRowPartChunks chunks of kRowChunkLen elements; a
+// chunk is what one wave reads at once.
+constexpr uint32_t kRowChunkLen = 2048;
+constexpr uint32_t kRowPartChunks = 8;
+constexpr uint64_t kRowPartLen = (uint64_t)kRowChunkLen * kRowPartChunks;
+constexpr uint32_t kRowPartWaves = 4;       // waves of a part workgroup
+constexpr uint64_t kRowWaveLen = kRowPartLen / kRowPartWaves;   // elements of one wave in a part
+constexpr uint64_t kRowSplitMin = 65536;   // smallest row that may be split
+constexpr uint32_t kChunkWords = 4;         // words of a chunk's record
+
+// Per split row: its bracket, whether some wave's candidates overflowed their
+// region, and the outcome of its threshold selection.
+struct BigRowState {
+  uint32_t t_lo, t_hi;    // bracket of the sampled selection
+  uint32_t ovf;           // nonzero: a wave had more candidates than its region holds
+  uint32_t slow;          // 1: the select kernel wrote the row on its own (bracket missed or ovf)
+  uint32_t thr;           // threshold key and the number of keys equal to it that are kept
+  uint32_t need;
+  uint32_t pad[2];
+};
+
 struct RowsCtx {
-  const uint64_t* table;  // seg_off[0..L], then per layer its position among the short layers (or ~0)
+  const uint64_t* table;  // seg_off[0..L], then per layer its position among the short layers (or ~0),
+                          // then part_pre[0..Lb], then cand_pre[0..Lb]
   RowDesc* rows;          // [Ls x K]: row q * K + j is device j's q-th short layer (longest first)
   double* row_e;          // [K x L x 2]: E_all, E_kept of device j's layer l (short layers)
   uint32_t K, L, Ls;
+  // Split rows: the first Lb short layers (the longest). Part p of device j's
+  // row of split layer q is workgroup part_pre[q] * K + j * (part_pre[q + 1] -
+  // part_pre[q]) + p of the part kernels; its chunks are kRowPartChunks
+  // records of `chunk` from that number times kRowPartChunks on. The row's
+  // candidates are staged from cand_pre[q] * K + j * (cand_pre[q + 1] -
+  // cand_pre[q]) of `cand` on, in a region of equal size per wave of its parts.
+  uint32_t Lb;
+  uint32_t nparts;        // part workgroups of all split rows
+  BigRowState* bst;       // [Lb x K]
+  uint32_t* chunk;        // [nparts x kRowPartChunks x kChunkWords]: per chunk, keys >= t_hi, 0, where
+                          // its candidates start in the row's region, their number; after the
+                          // selection the first two are the kept entries above / equal to the
+                          // threshold before the chunk
+  uint64_t* cand;         // staged candidates: index | value bits << 32, in index order per chunk
+  double* part_e;         // [2 x nparts x 4] E_all, then E_kept, partial sums per wave of each part
 };
 
 hipError_t launch_put_table(const uint64_t* src, uint64_t count, uint64_t* dst, hipStream_t s);

@@ -575,9 +575,12 @@ __device__ inline uint64_t wave_incl_scan_u64(uint64_t v)
 // One workgroup per device: the exclusive prefix of the tiles' candidate | sure
 // << 32 counts (each thread takes a run of consecutive tiles), the sum of
 // squares over all tiles in a fixed order, then the path decision: the exact
-// path (fallback) or the radix selection on the selection interval.
-constexpr int kScanBlock = 1024;
-
+// path (fallback) or the radix selection on the selection interval. NT = 1024
+// when it runs alone; 256 when it runs beside another selection's main pass,
+// whose stream of small workgroups rarely leaves 16 waves of a compute unit
+// free at once.
+constexpr int kScanBlockLarge = 1024, kScanBlockSmall = 256;
+template <int kScanBlock>
 __global__ __launch_bounds__(kScanBlock) void k_scan(Ctx c)
 {
   constexpr int kW = kScanBlock / 64;
@@ -1386,7 +1389,8 @@ static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s, int ha
 {
   const uint32_t band_blocks = c.jn * ((c.nslot + kBandTiles * kWaves - 1) / (kBandTiles * kWaves));
   if (half == 0) {
-    k_scan<<<c.jn, kScanBlock, 0, s>>>(c);
+    if (p.beside) k_scan<kScanBlockSmall><<<c.jn, kScanBlockSmall, 0, s>>>(c);
+    else k_scan<kScanBlockLarge><<<c.jn, kScanBlockLarge, 0, s>>>(c);
     const uint32_t ncand = p.any_fast ? band_blocks : 0u;
     if (p.any_fast) k_overflow<<<c.jn * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
     for (int pass = 0; pass < 3; ++pass) {
@@ -1470,13 +1474,11 @@ hipError_t launch_select(const Ctx& c0, const PrepArgs& a, const SelectPlan& p, 
   return hipGetLastError();
 }
 
-// The whole selection of all devices with the rest after the main pass on s2
-// and no join: s carries the preparation, bracket and main pass, then records
-// main_done; s2 waits for it and runs the rest. Consecutive calls on
-// alternating workspaces thus overlap a selection's rest with the next one's
-// main pass; the caller orders workspace reuse and the final join.
-hipError_t launch_select_detached(const Ctx& c0, const PrepArgs& a, const SelectPlan& p, hipStream_t s,
-                                  hipStream_t s2, hipEvent_t main_done)
+// The selection of all devices in three parts, for callers that pipeline
+// several selections on alternating workspaces (the long layers of a
+// per-layer selection): preparation and bracket; the main pass; everything
+// after it. The caller orders them and the workspace reuse with events.
+hipError_t launch_bracket(const Ctx& c0, const PrepArgs& a, const SelectPlan& p, hipStream_t s)
 {
   Ctx c = c0;
   c.j0 = 0;
@@ -1491,14 +1493,27 @@ hipError_t launch_select_detached(const Ctx& c0, const PrepArgs& a, const Select
       k_find<<<c.K, 64, 0, s>>>(c, kSlotSampleLo, kSlotSampleHi + 1, pass + 1 == kBracketPasses);
     }
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_main(const Ctx& c0, const PrepArgs& a, hipStream_t s)
+{
+  Ctx c = c0;
+  c.j0 = 0;
+  c.jn = c.K;
   GradArgs ga;
   for (uint32_t j = 0; j < c.K; ++j) ga.grad[j] = a.grad[j];
   k_main<<<c.K * c.tpd, kBlock, 0, s>>>(c, ga);
-  hipError_t e = hipEventRecord(main_done, s);
-  if (e == hipSuccess) e = hipStreamWaitEvent(s2, main_done, 0);
-  if (e != hipSuccess) return e;
-  launch_post(c, p, s2, 0);
-  launch_post(c, p, s2, 1);
+  return hipGetLastError();
+}
+
+hipError_t launch_rest(const Ctx& c0, const SelectPlan& p, hipStream_t s)
+{
+  Ctx c = c0;
+  c.j0 = 0;
+  c.jn = c.K;
+  launch_post(c, p, s, 0);
+  launch_post(c, p, s, 1);
   return hipGetLastError();
 }
 

@@ -20,6 +20,12 @@ MODES = ("default", "force_exact", "force_fallback")
 # layer to the multi-launch selection, 2^32 - 1 every layer to the rows.
 ROW_MAX_DEFAULT = 1 << 21
 ROW_MAXES = (ROW_MAX_DEFAULT, 0, 2**32 - 1)
+# Rows of more than row_split elements (at least 65536) are split into parts
+# read by workgroups of their own: 0 splits every row above 65536 elements,
+# 2^32 - 1 none. These runs take the test's largest row_max (with the default
+# list, every layer a row).
+ROW_SPLIT_DEFAULT = 1 << 18
+ROW_SPLITS = (0, 2**32 - 1)
 
 
 @pytest.fixture(scope="module")
@@ -31,7 +37,7 @@ def sc():
 
 
 def layers_vs_oracle(sc, G: np.ndarray, seg_off, ratios, label, modes=("default",), topk=None,
-                     check_aggregate=False, row_maxes=ROW_MAXES):
+                     check_aggregate=False, row_maxes=ROW_MAXES, row_splits=ROW_SPLITS):
     """Run the per-layer selection of every device of G (K x n) and compare it
     with the oracle; returns the oracle's per-device results."""
     torch, dev = torch_dev()
@@ -42,12 +48,14 @@ def layers_vs_oracle(sc, G: np.ndarray, seg_off, ratios, label, modes=("default"
     for j in range(K):
         check_energies(f"{label} device {j} (oracle)", ref[j][2], ref[j][3], refs[j], G.shape[1], ref[j][0].size)
     g_dev = torch.from_numpy(G).to(dev)
-    runs = [(m, ROW_MAX_DEFAULT) for m in modes] + [("default", r) for r in row_maxes
-                                                     if r != ROW_MAX_DEFAULT or not modes]
-    for mode, row_max in runs:
+    runs = ([(m, ROW_MAX_DEFAULT, ROW_SPLIT_DEFAULT) for m in modes]
+            + [("default", r, ROW_SPLIT_DEFAULT) for r in row_maxes if r != ROW_MAX_DEFAULT or not modes]
+            + [("default", max(row_maxes), r) for r in row_splits])
+    for mode, row_max, row_split in runs:
         if mode != "default":
             sc.set_option(mode, 1)
         sc.set_option("row_max", row_max)
+        sc.set_option("row_split", row_split)
         try:
             sel = sc.LayerSelect(g_dev, seg_off, ratios)
             idx, val, en = sel.run()
@@ -56,7 +64,8 @@ def layers_vs_oracle(sc, G: np.ndarray, seg_off, ratios, label, modes=("default"
             if mode != "default":
                 sc.set_option(mode, 0)
             sc.set_option("row_max", ROW_MAX_DEFAULT)
-        mode = f"{mode}, row_max {row_max}"
+            sc.set_option("row_split", ROW_SPLIT_DEFAULT)
+        mode = f"{mode}, row_max {row_max}, row_split {row_split}"
         e = en.cpu().numpy()
         for j in range(K):
             idx_o, val_o, ea, ek = ref[j]
@@ -139,6 +148,29 @@ def test_rows_with_equal_keys(sc):
     seg_off = [0, n_l, 2 * n_l, 3 * n_l, 4 * n_l]
     log("layers with equal keys")
     layers_vs_oracle(sc, np.stack([g, -g]), seg_off, [0.01, 0.5], "equal keys")
+
+
+def test_split_rows(sc):
+    # rows split into parts: lengths around the part size (65536) and its
+    # multiples, unaligned layer starts, a row whose keys are all equal and
+    # one with few magnitude levels (their selection intervals overflow, so
+    # the select kernel writes them on its own), dense large magnitudes in one
+    # part only
+    rng = np.random.default_rng(18)
+    sizes = [65_537, 3, 131_071, 131_073, 1, 200_000, 100_000, 90_001, 70_000]
+    seg_off = np.concatenate([[0], np.cumsum(sizes)]).tolist()
+    n = seg_off[-1]
+    G = rng.standard_normal((2, n)).astype(np.float32)
+    a, b = seg_off[6], seg_off[7]
+    G[:, a:b] = -2.5                                       # all keys equal
+    a, b = seg_off[7], seg_off[8]
+    G[:, a:b] = (rng.integers(-3, 4, size=(2, b - a)) * 0.25).astype(np.float32)
+    a = seg_off[5]
+    G[:, a + 70_000:a + 75_000] *= 1e3                     # large values in one part
+    for ratios in ([0.01, 0.2], [0.001, 0.6]):
+        log(f"layers split rows ratios={ratios}")
+        layers_vs_oracle(sc, G, seg_off, ratios, f"split rows {ratios}", row_maxes=(ROW_MAX_DEFAULT,),
+                         row_splits=(0,))
 
 
 def test_one_layer_matches_whole_vector(sc):
