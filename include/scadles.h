@@ -383,12 +383,12 @@ const char* scadles_last_error(void);
  *                       second stream and the rows on a third. Results do
  *                       not depend on it.
  *   "row_split"      0..2^32-1 (default 2^18; at least 65536 takes effect):
- *                       rows of more than this many elements are read by one
- *                       workgroup per 16384-element part (their candidates
- *                       staged, so each row is read once) instead of one
- *                       workgroup per row, unless their ratio is so high that
- *                       a part's candidates could exceed half its elements.
- *                       Results do not depend on it.
+ *                       rows of more than this many elements (and at most
+ *                       2^24) are read by one workgroup per 16384-element part
+ *                       (their candidates staged, so each row is read once)
+ *                       instead of one workgroup per row, unless their ratio
+ *                       is so high that a part's candidates could exceed half
+ *                       its elements. Results do not depend on it.
  * Returns SCADLES_EINVAL for an unknown name or a value out of range.       */
 scadles_status scadles_set_option(const char* name, int64_t value);
 

@@ -544,10 +544,12 @@ static uint64_t row_parts_of(uint64_t n) { return ceil_div_u64(n + 3, kRowPartLe
 // Capacity of one wave's candidate region in the split rows of a layer of n
 // elements: twice the wave's share of 2 k_max + 4096 (k_max the largest k of
 // the devices) plus 64, in multiples of 64; 0 when that exceeds half a
-// wave's elements (high ratios): such rows are not split. It falls as n grows,
-// so the split rows are the longest ones.
+// wave's elements (high ratios) or n exceeds kRowSplitMax: such rows are not
+// split. Up to kRowSplitMax it falls as n grows, so the split rows are the
+// longest ones.
 static uint64_t row_wave_cap(uint64_t n, const double* ratios, uint32_t K)
 {
+  if (n > kRowSplitMax) return 0;
   uint64_t kmax = 0;
   for (uint32_t j = 0; j < K; ++j) kmax = std::max<uint64_t>(kmax, k_rule(n, ratios[j]));
   const uint64_t share = (2 * (2 * kmax + 4096) * kRowWaveLen + n - 1) / n + 64;
@@ -623,6 +625,12 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
   // The longest of them, those of more than row_split elements, are split into
   // parts, each read by a workgroup of its own.
   const uint64_t split = std::max<uint64_t>((uint64_t)g_row_split.load(), kRowSplitMin);
+  // (rows above kRowSplitMax are not split; they come first in the order, so
+  // the split rows are moved to the front of the row list)
+  std::stable_partition(shorts.begin(), shorts.end(), [&](uint32_t l) {
+    const uint64_t nl = seg_off[l + 1] - seg_off[l];
+    return nl > split && row_cand_list(nl, ratios, K) > 0;
+  });
   uint32_t Lb = 0;
   while (Lb < shorts.size()) {
     const uint64_t nl = seg_off[shorts[Lb] + 1] - seg_off[shorts[Lb]];

@@ -244,6 +244,7 @@ constexpr uint64_t kRowPartLen = (uint64_t)kRowChunkLen * kRowPartChunks;
 constexpr uint32_t kRowPartWaves = 4;       // waves of a part workgroup
 constexpr uint64_t kRowWaveLen = kRowPartLen / kRowPartWaves;   // elements of one wave in a part
 constexpr uint64_t kRowSplitMin = 65536;   // smallest row that may be split
+constexpr uint64_t kRowSplitMax = 1u << 24; // longest row that may be split
 constexpr uint32_t kChunkWords = 4;         // words of a chunk's record
 
 // Per split row: its bracket, whether some wave's candidates overflowed their
