@@ -121,6 +121,8 @@ __device__ inline void add_batch(const AggArgs& a, double* acc, uint32_t jb, uin
   }
 }
 
+constexpr uint32_t kAGroup = 16;   // consecutive ranges per XCD turn
+
 // One wave per range. Lane j < K holds device j's entry interval [eb, eb + em)
 // in the range (from the range markers). Devices are added in ascending order,
 // kABatch at a time (see load_batch / add_batch). Dense devices add the whole
@@ -130,7 +132,14 @@ __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
   __shared__ double acc[kARange];
   const uint32_t l = threadIdx.x;
   const uint32_t K = c.K;
-  const uint32_t r = blockIdx.x;
+  // Workgroups are dealt to the GPU's 8 XCDs in turn; consecutive groups of
+  // kAGroup ranges go to one XCD, so the cache lines that neighbouring ranges
+  // share (the markers, the ends of every device's entry window) are fetched
+  // into one XCD's L2 rather than into several (1.14 -> 1.02 x the
+  // algorithmic bytes fetched at the largest workload, same time).
+  const uint32_t bq = blockIdx.x >> 3;
+  const uint32_t r = (bq / kAGroup) * (8 * kAGroup) + (blockIdx.x & 7u) * kAGroup + bq % kAGroup;
+  if (r >= c.nrange) return;
   const uint64_t base = (uint64_t)r * kARange;
   const uint32_t len = (uint32_t)((c.n - base < (uint64_t)kARange) ? c.n - base : (uint64_t)kARange);
   uint32_t eb = 0, em = 0;
@@ -296,7 +305,7 @@ hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate
       if (e != hipSuccess) return e;
     }
   }
-  k_aggregate<<<c.nrange, 64, 0, s>>>(a, c);
+  k_aggregate<<<(c.nrange + 8 * kAGroup - 1) / (8 * kAGroup) * (8 * kAGroup), 64, 0, s>>>(a, c);
   return hipGetLastError();
 }
 

@@ -41,6 +41,9 @@ std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0}, g_parts{1
 // per-layer selection: layers of at most this many elements go to the row kernels
 std::atomic<int64_t> g_row_max{1 << 21};
 std::atomic<int64_t> g_row_split{1 << 18};
+// Per-layer selection: workspace regions of the long layers, used in turn; the
+// brackets of the first kLayerRegions long layers are computed up front.
+constexpr uint32_t kLayerRegions = 2;
 // Per-layer selection: the short layers' rows on a third stream beside the
 // long layers (true) or on the caller's stream before them (false).
 constexpr bool kRowsBeside = true;
@@ -85,7 +88,7 @@ struct StreamSet {
   hipEvent_t fork = nullptr, rows_done = nullptr;
   // long layers: end of a layer's main pass; end of the bracket of the layer
   // using each of the two workspace regions; end of all the layers' rests
-  hipEvent_t layer_main = nullptr, bracket_done[2] = {}, rests_done = nullptr;
+  hipEvent_t layer_main = nullptr, bracket_done[kLayerRegions] = {}, rests_done = nullptr;
   std::mutex rows_mu;
 };
 constexpr int kMaxGpus = 64;
@@ -585,7 +588,7 @@ static LayersWs layers_ws(uint32_t K, const uint64_t* seg_off, uint32_t L, const
   parts *= K;
   cands *= K;
   w.sel = align256(most);
-  w.table = 2 * w.sel;
+  w.table = kLayerRegions * w.sel;
   w.rows = align256(w.table + sizeof(uint64_t) * (4ull * L + 3));
   w.row_e = align256(w.rows + sizeof(RowDesc) * (size_t)K * L);
   w.e_long = align256(w.row_e + sizeof(double) * 2ull * K * L);
@@ -724,7 +727,7 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
       a.r_hi[j] = Ll.r_hi[j];
       at[j] += Ll.k[j];
     }
-    const size_t region = (longs.size() - 1) & 1u;
+    const size_t region = (longs.size() - 1) % kLayerRegions;
     select_setup(Ll, base + region * lw.sel, INFINITY, e_long, nullptr, nullptr, nullptr, (uint32_t)off,
                  longs.size() > 1, ll.c, ll.p);
     ll.p.parts = 1;
@@ -756,18 +759,26 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
     e = hipEventRecord(ss->rows_done, sr);
     if (e != hipSuccess) return hip_fail(e, "row stream join");
   }
+  // the brackets of long layers 1 .. kLayerRegions - 1 on s2 up front; layer
+  // li + kLayerRegions - 1's bracket after layer li - 1's rest (its region's
+  // last user), ahead of layer li's rest
+  for (size_t li = 1; li < longs.size() && li < kLayerRegions; ++li) {
+    e = launch_bracket(longs[li].c, longs[li].a, longs[li].p, ss->s2);
+    if (e == hipSuccess) e = hipEventRecord(ss->bracket_done[li % kLayerRegions], ss->s2);
+    if (e != hipSuccess) return hip_fail(e, "layer bracket");
+  }
   for (size_t li = 0; li < longs.size(); ++li) {
     const LongLayer& ll = longs[li];
     if (li > 0) {
-      e = hipStreamWaitEvent(s, ss->bracket_done[li & 1u], 0);
+      e = hipStreamWaitEvent(s, ss->bracket_done[li % kLayerRegions], 0);
       if (e != hipSuccess) return hip_fail(e, "layer pipeline");
     }
     e = launch_main(ll.c, ll.a, s);
     if (e == hipSuccess) e = hipEventRecord(ss->layer_main, s);
-    if (e == hipSuccess && li + 1 < longs.size()) {
-      const LongLayer& nx = longs[li + 1];
-      e = launch_bracket(nx.c, nx.a, nx.p, ss->s2);
-      if (e == hipSuccess) e = hipEventRecord(ss->bracket_done[(li + 1) & 1u], ss->s2);
+    const size_t nx = li + kLayerRegions - 1;
+    if (e == hipSuccess && li > 0 && nx < longs.size()) {
+      e = launch_bracket(longs[nx].c, longs[nx].a, longs[nx].p, ss->s2);
+      if (e == hipSuccess) e = hipEventRecord(ss->bracket_done[nx % kLayerRegions], ss->s2);
     }
     if (e == hipSuccess) e = hipStreamWaitEvent(ss->s2, ss->layer_main, 0);
     if (e == hipSuccess) e = launch_rest(ll.c, ll.p, ss->s2);
