@@ -382,7 +382,7 @@ const char* scadles_last_error(void);
  *                       selection, consecutive ones pipelined on the library's
  *                       second stream and the rows on a third. Results do
  *                       not depend on it.
- *   "row_split"      0..2^32-1 (default 2^18; at least 65536 takes effect):
+ *   "row_split"      0..2^32-1 (default 65536, the least that takes effect):
  *                       rows of more than this many elements (and at most
  *                       2^24) are read by one workgroup per 16384-element part
  *                       (their candidates staged, so each row is read once)

@@ -40,7 +40,7 @@ namespace {
 std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0}, g_parts{1}, g_inject_count_error{0};
 // per-layer selection: layers of at most this many elements go to the row kernels
 std::atomic<int64_t> g_row_max{1 << 21};
-std::atomic<int64_t> g_row_split{1 << 18};
+std::atomic<int64_t> g_row_split{65536};
 // Per-layer selection: workspace regions of the long layers, used in turn; the
 // brackets of the first kLayerRegions long layers are computed up front.
 constexpr uint32_t kLayerRegions = 2;

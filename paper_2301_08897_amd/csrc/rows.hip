@@ -683,9 +683,9 @@ __global__ __launch_bounds__(kRowBlock) void k_big_bracket(RowsCtx rc)
 // the row.
 template <bool kFull>
 __device__ inline void gather_count(const f4 (&x)[kRowR], uint64_t v0, uint64_t vend, const Row& row, uint32_t t_lo,
-                                    uint32_t t_hi, uint32_t& nsure, uint32_t& ncand, double& e_all)
+                                    uint32_t t_hi, uint32_t& nsure, uint32_t& ncand, uint32_t& nband, double& e_all)
 {
-  nsure = ncand = 0;
+  nsure = ncand = nband = 0;
 #pragma unroll
   for (int r = 0; r < kRowR; ++r) {
     const uint64_t v = v0 + r * 256u;
@@ -695,6 +695,7 @@ __device__ inline void gather_count(const f4 (&x)[kRowR], uint64_t v0, uint64_t 
       const uint32_t key = key_of(x[r][q]);
       nsure += (uint32_t)__builtin_popcountll(ballot(valid && key >= t_hi));
       ncand += (uint32_t)__builtin_popcountll(ballot(valid && key >= t_lo));
+      nband += (uint32_t)__builtin_popcountll(ballot(valid && key >= t_lo && key < t_hi));
       if (kFull) e_all = __builtin_fma((double)x[r][q], (double)x[r][q], e_all);
       else if (valid) e_all = __builtin_fma((double)x[r][q], (double)x[r][q], e_all);
     }
@@ -774,15 +775,15 @@ __global__ __launch_bounds__(kPartBlock) __attribute__((amdgpu_waves_per_eu(4, 4
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
     const uint64_t vc = v0 + (uint64_t)c * kRowChunkLen;
-    uint32_t nsure, ncand;
-    if (full) gather_count<true>(x[c], vc, vend, row, t_lo, t_hi, nsure, ncand, e_all);
-    else gather_count<false>(x[c], vc, vend, row, t_lo, t_hi, nsure, ncand, e_all);
+    uint32_t nsure, ncand, nband;
+    if (full) gather_count<true>(x[c], vc, vend, row, t_lo, t_hi, nsure, ncand, nband, e_all);
+    else gather_count<false>(x[c], vc, vend, row, t_lo, t_hi, nsure, ncand, nband, e_all);
     if (ncand) {
       if (full) gather_write<true>(x[c], vc, vend, row, t_lo, at, cand, wcap);
       else gather_write<false>(x[c], vc, vend, row, t_lo, at, cand, wcap);
     }
     if (lane == 0) {
-      const u4 w4 = {nsure, 0u, wbase + at, ncand};
+      const u4 w4 = {nsure, nband, wbase + at, ncand};
       *reinterpret_cast<GLOBAL u4*>(rec + c * kChunkWords) = w4;
     }
     at += ncand;
@@ -821,16 +822,19 @@ __global__ __launch_bounds__(kRowBlock) void k_big_select(RowsCtx rc)
   // to kRowBlock chunks); their records stay in registers for the first run
   const uint32_t per = (nch + kRowBlock - 1) / kRowBlock;
   const uint32_t c0 = tid * per < nch ? tid * per : nch, c1 = c0 + per < nch ? c0 + per : nch;
-  uint32_t sure = 0;
-  for (uint32_t c = c0; c < c1; ++c) sure += ch[kChunkWords * c];
-  uint32_t sure_all;
-  if (tid == 0) s_res[3] = 0u;
+  uint32_t sure = 0, band = 0;
+  for (uint32_t c = c0; c < c1; ++c) {
+    sure += ch[kChunkWords * c];
+    band += ch[kChunkWords * c + 1];
+  }
+  uint32_t sure_all, nband;
   row_scan(sure, s_w, sure_all);
-  const bool ovf = st->ovf != 0u;
-  bool in_band = false;
-  uint32_t nband = 0;
-  // visit(key) for every staged candidate of the thread's chunks, eight loads in flight
-  auto each_key = [&](auto visit) {
+  const uint32_t boff = row_scan(band, s_w, nband) - band;   // the thread's chunks' keys start here in LDS
+  const bool in_band = st->ovf == 0u && sure_all < d.k && d.k - sure_all <= nband && nband <= (uint32_t)kRowCand;
+  if (in_band) {
+    // the selection-interval keys (the candidates below t_hi) into LDS, each
+    // thread's chunks in order from boff: the only read of the candidates
+    uint32_t pos = boff;
     for (uint32_t c = c0; c < c1; ++c) {
       const uint32_t at = ch[kChunkWords * c + 2], n = ch[kChunkWords * c + 3];
       for (uint32_t e0 = 0; e0 < n; e0 += 8) {
@@ -839,41 +843,28 @@ __global__ __launch_bounds__(kRowBlock) void k_big_select(RowsCtx rc)
         for (int i = 0; i < 8; ++i) kv[i] = e0 + i < n ? (uint32_t)(list[at + e0 + i] >> 32) & kKeyMask : kKeyInf;
 #pragma unroll
         for (int i = 0; i < 8; ++i)
-          if (e0 + i < n) visit(kv[i]);
+          if (kv[i] < t_hi) {
+            if (pos < (uint32_t)kRowCand) cand[pos] = kv[i];
+            ++pos;
+          }
       }
     }
-  };
-  if (!ovf && sure_all < d.k) {
-    // the selection-interval keys: the candidates below t_hi
-    each_key([&](uint32_t key) {
-      if (key < t_hi) {
-        const uint32_t pos = atomicAdd(&s_res[3], 1u);
-        if (pos < (uint32_t)kRowCand) cand[pos] = key;
-      }
-    });
     __syncthreads();
-    nband = s_res[3];
-    in_band = d.k - sure_all <= nband && nband <= (uint32_t)kRowCand;
-  }
-  if (in_band) {
     uint32_t need = d.k - sure_all;
     const uint32_t thr = row_select_lds(cand, nband, need, hist, s_w, s_res);
-    // the thread's chunks' candidates above / equal to the threshold, then
-    // their exclusive prefix in index order
+    // every chunk's kept entries above / equal to the threshold (its keys >=
+    // t_hi and its band keys in LDS), then their exclusive prefix in index order
     uint32_t gsum = 0, esum = 0;
+    pos = boff;
     for (uint32_t c = c0; c < c1; ++c) {
-      const uint32_t at = ch[kChunkWords * c + 2], n = ch[kChunkWords * c + 3];
-      uint32_t g = 0, e = 0;
-      for (uint32_t e0 = 0; e0 < n; e0 += 8) {
-        uint32_t kv[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) kv[i] = e0 + i < n ? (uint32_t)(list[at + e0 + i] >> 32) & kKeyMask : 0u;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          g += (e0 + i < n && kv[i] > thr) ? 1u : 0u;
-          e += (e0 + i < n && kv[i] == thr) ? 1u : 0u;
-        }
+      const uint32_t nb = ch[kChunkWords * c + 1];
+      uint32_t g = ch[kChunkWords * c], e = 0;
+      for (uint32_t i = 0; i < nb; ++i) {
+        const uint32_t key = cand[pos + i];
+        g += key > thr ? 1u : 0u;
+        e += key == thr ? 1u : 0u;
       }
+      pos += nb;
       ch[kChunkWords * c] = g;
       ch[kChunkWords * c + 1] = e;
       gsum += g;

@@ -21,11 +21,11 @@ MODES = ("default", "force_exact", "force_fallback")
 ROW_MAX_DEFAULT = 1 << 21
 ROW_MAXES = (ROW_MAX_DEFAULT, 0, 2**32 - 1)
 # Rows of more than row_split elements (at least 65536) are split into parts
-# read by workgroups of their own: 0 splits every row above 65536 elements,
-# 2^32 - 1 none. These runs take the test's largest row_max (with the default
-# list, every layer a row).
-ROW_SPLIT_DEFAULT = 1 << 18
-ROW_SPLITS = (0, 2**32 - 1)
+# read by workgroups of their own: the default splits every row above 65536
+# elements, 2^18 only the longer ones, 2^32 - 1 none. These runs take the
+# test's largest row_max (with the default list, every layer a row).
+ROW_SPLIT_DEFAULT = 65536
+ROW_SPLITS = (1 << 18, 2**32 - 1)
 
 
 @pytest.fixture(scope="module")
