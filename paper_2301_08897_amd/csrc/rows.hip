@@ -600,6 +600,10 @@ __global__ __launch_bounds__(kRowBlock) void k_rows(RowsCtx rc)
 // No workgroup waits for another inside a launch, and the part kernels have
 // no barrier and no atomic but the rare overflow flag.
 constexpr int kPartWaves = (int)kRowPartWaves;
+// selection-interval keys a split row's select workgroup holds in LDS (one
+// workgroup per row: it can take most of a compute unit's 160 KiB)
+constexpr int kBigCand = 32768;
+static_assert(kBigCand >= kRowCand, "the whole-row path of the select kernel uses kRowCand keys of the array");
 constexpr int kPartBlock = 64 * kPartWaves;
 constexpr int kWaveChunks = kRowPartChunks / kPartWaves;    // chunks of one wave, loaded at once
 static_assert(kRowChunkLen == 256u * kRowR, "a chunk is one wave's kRowR rounds");
@@ -661,7 +665,7 @@ __device__ inline double wave_sum_list(const double* a, uint32_t n)
 
 __global__ __launch_bounds__(kRowBlock) void k_big_bracket(RowsCtx rc)
 {
-  __shared__ uint32_t shist[kRowCand];
+  __shared__ uint32_t shist[1 << kRowSampleBits];
   __shared__ uint32_t s_w[kRowWaves];
   __shared__ uint32_t s_res[4];
   const RowDesc d = rc.rows[blockIdx.x];
@@ -796,7 +800,7 @@ __global__ __launch_bounds__(kPartBlock) __attribute__((amdgpu_waves_per_eu(4, 4
 __global__ __launch_bounds__(kRowBlock) void k_big_select(RowsCtx rc)
 {
   __shared__ uint32_t hist[kRowBins];
-  __shared__ uint32_t cand[kRowCand];
+  __shared__ uint32_t cand[kBigCand];
   __shared__ uint32_t s_w[kRowWaves];
   __shared__ uint32_t s_res[4];
   __shared__ double s_d[kRowWaves];
@@ -830,7 +834,7 @@ __global__ __launch_bounds__(kRowBlock) void k_big_select(RowsCtx rc)
   uint32_t sure_all, nband;
   row_scan(sure, s_w, sure_all);
   const uint32_t boff = row_scan(band, s_w, nband) - band;   // the thread's chunks' keys start here in LDS
-  const bool in_band = st->ovf == 0u && sure_all < d.k && d.k - sure_all <= nband && nband <= (uint32_t)kRowCand;
+  const bool in_band = st->ovf == 0u && sure_all < d.k && d.k - sure_all <= nband && nband <= (uint32_t)kBigCand;
   if (in_band) {
     // the selection-interval keys (the candidates below t_hi) into LDS, each
     // thread's chunks in order from boff: the only read of the candidates
@@ -844,7 +848,7 @@ __global__ __launch_bounds__(kRowBlock) void k_big_select(RowsCtx rc)
 #pragma unroll
         for (int i = 0; i < 8; ++i)
           if (kv[i] < t_hi) {
-            if (pos < (uint32_t)kRowCand) cand[pos] = kv[i];
+            if (pos < (uint32_t)kBigCand) cand[pos] = kv[i];
             ++pos;
           }
       }
@@ -973,18 +977,22 @@ __global__ __launch_bounds__(64) void k_big_finish(RowsCtx rc)
   if (threadIdx.x == 0) rc.row_e[2ull * rc.rows[b].eslot + 1] = ek;
 }
 
-// Per device: the energies of its short layers summed in layer order, plus
-// those of the long layers (`add`, when not null).
+// Per device: the energies of its short layers (each lane a strided subset in
+// layer order, then the lanes in a fixed tree), plus those of the long layers
+// (`add`, when not null).
 __global__ __launch_bounds__(64) void k_rows_energy(RowsCtx rc, double* energies, const double* add)
 {
-  if (threadIdx.x != 0) return;
+  // lane i adds layers i, i + 64, ... in order, then the lanes in a fixed tree
   const uint32_t j = blockIdx.x;
   double ea = 0.0, ek = 0.0;
-  for (uint32_t l = 0; l < rc.L; ++l) {
+  for (uint32_t l = threadIdx.x; l < rc.L; l += 64) {
     if (rc.table[rc.L + 1 + l] == kNotShort) continue;
     ea += rc.row_e[2ull * ((uint64_t)j * rc.L + l)];
     ek += rc.row_e[2ull * ((uint64_t)j * rc.L + l) + 1];
   }
+  ea = wave_sum_f64(ea);
+  ek = wave_sum_f64(ek);
+  if (threadIdx.x != 0) return;
   if (add) {
     ea += add[2 * j];
     ek += add[2 * j + 1];
