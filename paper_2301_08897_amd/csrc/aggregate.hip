@@ -26,6 +26,61 @@ __global__ __launch_bounds__(kBlock) void k_lb(AggArgs a, AggCtx c)
             gridDim.x * kBlock);
 }
 
+// Range markers of sets this library built (ascending by construction) in one
+// streaming pass over their idx instead of a search per range: position p
+// (0 <= p <= k) is the marker of every range start in (idx[p-1], idx[p]],
+// with idx[-1] below and idx[k] above every index, so each marker is written
+// exactly once. A lane writes an interval of up to kMarkShort ranges itself;
+// longer ones (sparse sets) are written by the whole wave. Writes stay below
+// nrange for any input; for a set that is not ascending some markers keep
+// older values, which the aggregation's clamping keeps in bounds.
+constexpr uint32_t kMarkBatch = 8;    // positions per lane per pass
+constexpr uint32_t kMarkShort = 4;
+__global__ __launch_bounds__(kBlock) void k_marks(AggArgs a, AggCtx c)
+{
+  const uint32_t j = blockIdx.y;
+  if (!a.idx[j] || dense_device(a, c, j)) return;
+  const uint32_t* idx = a.idx[j];
+  const uint32_t k = a.k[j];
+  uint32_t* lb = c.lb + (uint64_t)j * c.nrange;
+  const uint32_t l = lane_id();
+  const uint32_t rlast = c.nrange - 1u;
+  constexpr uint32_t kSpan = kMarkBatch * 64;
+  const uint64_t np = (uint64_t)k + 1u;
+  const uint64_t step = (uint64_t)gridDim.x * (kBlock / 64) * kSpan;
+  for (uint64_t w0 = ((uint64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)) * kSpan; w0 < np; w0 += step) {
+    uint32_t cur[kMarkBatch];
+#pragma unroll
+    for (int m = 0; m < (int)kMarkBatch; ++m) {
+      const uint64_t p = w0 + m * 64 + l;
+      cur[m] = p < k ? idx[p] : 0u;
+    }
+    uint32_t last = w0 > 0 ? idx[w0 - 1] : 0u;
+#pragma unroll
+    for (int m = 0; m < (int)kMarkBatch; ++m) {
+      const uint64_t p = w0 + m * 64 + l;
+      const uint32_t up = __shfl_up(cur[m], 1, 64);
+      const uint32_t prev = l ? up : last;
+      last = __builtin_amdgcn_readlane(cur[m], 63);
+      const uint32_t ra = p ? prev / kARange + 1u : 0u;
+      uint32_t rb = p < k ? cur[m] / kARange : rlast;
+      if (rb > rlast) rb = rlast;
+      const bool live = p < np && ra <= rb;
+      const uint32_t pv = (uint32_t)p;
+      if (live && rb - ra < kMarkShort)
+        for (uint32_t r = ra; r <= rb; ++r) lb[r] = pv;
+      uint64_t lm = ballot(live && rb - ra >= kMarkShort);
+      while (lm) {
+        const int q = __builtin_ctzll(lm);
+        lm &= lm - 1;
+        const uint32_t qa = __builtin_amdgcn_readlane(ra, q), qb = __builtin_amdgcn_readlane(rb, q);
+        const uint32_t qp = __builtin_amdgcn_readlane(pv, q);
+        for (uint32_t r = qa + l; r <= qb; r += 64) lb[r] = qp;
+      }
+    }
+  }
+}
+
 // Flags a set whose idx is not strictly ascending or reaches n (validation mode).
 __global__ __launch_bounds__(kBlock) void k_validate(AggArgs a, AggCtx c)
 {
@@ -288,6 +343,17 @@ hipError_t launch_marks(const AggArgs& a, const AggCtx& c, hipStream_t s)
   uint32_t bx = (c.nrange + kBlock - 1) / kBlock;
   if (bx > 64) bx = 64;
   k_lb<<<dim3(bx, c.K), kBlock, 0, s>>>(a, c);
+  return hipGetLastError();
+}
+
+// Range markers of sets this library built, by a streaming pass (k_marks).
+hipError_t launch_marks_built(const AggArgs& a, const AggCtx& c, hipStream_t s)
+{
+  if (!c.K || !c.nrange) return hipSuccess;
+  constexpr uint64_t kPerBlock = (kBlock / 64) * kMarkBatch * 64;
+  uint64_t bx = ((uint64_t)c.kmax + kPerBlock) / kPerBlock;
+  if (bx > 1024) bx = 1024;
+  k_marks<<<dim3((uint32_t)bx, c.K), kBlock, 0, s>>>(a, c);
   return hipGetLastError();
 }
 

@@ -937,7 +937,9 @@ scadles_status scadles_step_fused_layers(const float* const* grads, uint32_t K, 
   c.nrange = w.nrange;
   c.kmax = (uint32_t)kmax;
   c.n = n;
-  e = launch_aggregate(g, c, 0, false, s);
+  e = launch_marks_built(g, c, s);
+  if (e != hipSuccess) return hip_fail(e, "marker launch");
+  e = launch_aggregate(g, c, 0, true, s);
   if (e != hipSuccess) return hip_fail(e, "aggregate launch");
   return SCADLES_OK;
 }

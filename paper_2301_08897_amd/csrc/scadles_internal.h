@@ -195,6 +195,7 @@ hipError_t launch_main(const Ctx& c, const PrepArgs& a, hipStream_t s);
 hipError_t launch_rest(const Ctx& c, const SelectPlan& p, hipStream_t s);
 hipError_t launch_aggregate(const AggArgs& a, const AggCtx& c, uint32_t validate, bool marks_done, hipStream_t s);
 hipError_t launch_marks(const AggArgs& a, const AggCtx& c, hipStream_t s);
+hipError_t launch_marks_built(const AggArgs& a, const AggCtx& c, hipStream_t s);
 hipError_t launch_sgd(float* p, const float* g, uint64_t n, float lr, hipStream_t s);
 hipError_t launch_momentum_sgd(float* p, float* v, const float* g, uint64_t n, float lr, float mom, float wd,
                                hipStream_t s);

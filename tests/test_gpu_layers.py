@@ -344,6 +344,43 @@ def test_fused_layers_step(sc, config, n, K, iters, beta, optimizer):
     assert np.all(acc[:, 2] == sent * np.array(step.k) + (s.iterations - sent) * s.n)
 
 
+def test_fused_layers_sparse_sets(sc):
+    """Fused per-layer step with kept sets so sparse that consecutive kept
+    indices lie many aggregation ranges apart (down to one entry per layer),
+    beside denser devices and one that keeps everything: each range's first
+    entry is found for every device, so the aggregate and the update match the
+    oracle bit for bit."""
+    torch, dev = torch_dev()
+    ratios = [1e-6, 2e-5, 3e-4, 0.02, 1.0]
+    s = workloads.spec(5, n=3_000_001, K=len(ratios), iterations=1)
+    seg_off = [0] + [int(x) for x in s.seg_end]
+    log(f"fused layers, sparse sets n={s.n} K={s.K} L={len(seg_off) - 1} ratios={ratios}")
+    G = np.empty((s.K, s.n), dtype=np.float32)
+    for j in range(s.K):
+        workloads.gradient(s, 0, j, out=G[j], k=oracle.topk_k(s.n, ratios[j]))
+    g_dev = torch.from_numpy(G).to(dev)
+    params = workloads.params0(s)
+    p_dev = torch.from_numpy(params).to(dev)
+    step = sc.FusedStep(g_dev, ratios, params=p_dev, seg_off=seg_off)
+    w, gamma = sc.stream_weights(s.rates[0], base_batch=s.base_batch)
+    lr = float(np.float32(s.eta * gamma))
+    for rep in range(2):          # the second call reuses the first call's markers' memory
+        out = step.run(w, lr)
+        torch.cuda.synchronize()
+        sets = []
+        for j in range(s.K):
+            idx, val, _, _ = oracle.topk_layers(G[j], seg_off, ratios[j])
+            assert np.array_equal(out.idx[j].cpu().numpy(), idx), f"call {rep} device {j}: indices"
+            assert same_bits(out.val[j].cpu().numpy(), val), f"call {rep} device {j}: values"
+            sets.append((idx, val))
+        gaps = np.diff(sets[0][0].astype(np.int64)) // 2048
+        assert gaps.max() > 64, "the sparsest device spans many ranges between kept entries"
+        dense_o = oracle.aggregate(sets, w, s.n)
+        assert same_bits(out.dense.cpu().numpy(), dense_o), f"call {rep}: aggregate"
+        params = oracle.sgd(params, dense_o, lr)
+        assert same_bits(p_dev.cpu().numpy(), params), f"call {rep}: update"
+
+
 def test_long_row_without_chunk_tallies(sc):
     # with every layer short, a 3M-element layer is one workgroup's row, too
     # long for the per-chunk tallies: its output takes the scanned path
