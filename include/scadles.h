@@ -362,11 +362,16 @@ const char* scadles_last_error(void);
  *                       scadles_topk_select(_noalloc), scadles_step_fused and
  *                       scadles_step_fused_ex read every device's selection
  *                       state back after the call and return
- *                       SCADLES_EINTERNAL if its internal checks failed
- *                       (all of these then synchronise `stream`).
- *   "inject_count_error" 1 (testing): the whole-vector selection reports a
- *                       failed count check for device 0 (its outputs are
- *                       unaffected), to exercise the validation above.
+ *                       SCADLES_EINTERNAL if its internal checks failed;
+ *                       scadles_topk_select_layers and
+ *                       scadles_step_fused_layers do the same for their
+ *                       layers of more than "row_max" elements (all of these
+ *                       then synchronise `stream`).
+ *   "inject_count_error" 1 (testing): the multi-launch selection (of the
+ *                       whole vector, and of a per-layer selection's long
+ *                       layers) reports a failed count check for device 0
+ *                       (its outputs are unaffected), to exercise the
+ *                       validation above.
  *   "force_exact"    1: Top-k skips the sampled single-read path and always
  *                       runs the exact multi-pass radix select.
  *   "force_fallback" 1: the sampled path runs but its result is discarded as
@@ -389,6 +394,14 @@ const char* scadles_last_error(void);
  *                       instead of one workgroup per row, unless their ratio
  *                       is so high that a part's candidates could exceed half
  *                       its elements. Results do not depend on it.
+ *   "layer_order"    0..2 (default 1): the order in which the per-layer
+ *                       selection runs its layers of more than "row_max"
+ *                       elements: 0 index order, 1 ascending length (the
+ *                       longest last, so the end of every earlier layer's
+ *                       selection overlaps a long main pass), 2 descending
+ *                       length. Every layer writes its own part of the
+ *                       outputs and of the energy sums, so results do not
+ *                       depend on it.
  * Returns SCADLES_EINVAL for an unknown name or a value out of range.       */
 scadles_status scadles_set_option(const char* name, int64_t value);
 

@@ -41,6 +41,7 @@ std::atomic<int> g_validate{0}, g_force_exact{0}, g_force_fallback{0}, g_parts{1
 // per-layer selection: layers of at most this many elements go to the row kernels
 std::atomic<int64_t> g_row_max{1 << 21};
 std::atomic<int64_t> g_row_split{65536};
+std::atomic<int64_t> g_layer_order{1};
 // Per-layer selection: workspace regions of the long layers, used in turn; the
 // brackets of the first kLayerRegions long layers are computed up front.
 constexpr uint32_t kLayerRegions = 2;
@@ -355,7 +356,7 @@ uint32_t parts_for(const Layout& L)
 
 // Kernel context and launch plan of one selection call.
 void select_setup(const Layout& L, void* ws, double delta, double* energies, uint8_t* compressed, uint32_t* lb,
-                  const scadles_step_options* opt, uint32_t idx_base, bool energies_add, Ctx& c, SelectPlan& p)
+                  const scadles_step_options* opt, uint32_t idx_base, uint32_t e_stride, Ctx& c, SelectPlan& p)
 {
   c = make_ctx(L, ws);
   c.delta = delta;
@@ -372,7 +373,7 @@ void select_setup(const Layout& L, void* ws, double delta, double* energies, uin
   c.lb = lb;
   c.nrange = L.nrange;
   c.idx_base = idx_base;
-  c.energies_add = energies_add ? 1u : 0u;
+  c.e_stride = e_stride;
   if (opt) {
     c.ewma = opt->ewma;
     c.ewma_beta = opt->ewma_beta;
@@ -386,7 +387,7 @@ scadles_status run_select(const Layout& L, const PrepArgs& a, void* ws, double d
 {
   Ctx c;
   SelectPlan p;
-  select_setup(L, ws, delta, energies, compressed, lb, opt, 0, false, c, p);
+  select_setup(L, ws, delta, energies, compressed, lb, opt, 0, 2u, c, p);
   if (pr) pr->parts = p.parts;
   StreamSet* ss = p.parts > 1 ? stream_set() : nullptr;
   if (p.parts > 1 && !ss) return fail(SCADLES_EHIP, "could not create the pipeline stream");
@@ -538,7 +539,7 @@ uint64_t scadles_layers_k(const uint64_t* seg_off, uint32_t L, double ratio)
 // layer's, for layers selected by the multi-launch path) and after it the
 // row region (layer table, row descriptors, per-row energies).
 struct LayersWs {
-  size_t sel = 0, table = 0, rows = 0, row_e = 0, e_long = 0, bst = 0, chunk = 0, cand = 0, part_e = 0, total = 0;
+  size_t sel = 0, table = 0, rows = 0, row_e = 0, bst = 0, chunk = 0, cand = 0, part_e = 0, err = 0, total = 0;
 };
 
 // Parts of a split row of n elements (the virtual row [0, n + shift), shift <= 3).
@@ -591,12 +592,12 @@ static LayersWs layers_ws(uint32_t K, const uint64_t* seg_off, uint32_t L, const
   w.table = kLayerRegions * w.sel;
   w.rows = align256(w.table + sizeof(uint64_t) * (4ull * L + 3));
   w.row_e = align256(w.rows + sizeof(RowDesc) * (size_t)K * L);
-  w.e_long = align256(w.row_e + sizeof(double) * 2ull * K * L);
-  w.bst = align256(w.e_long + sizeof(double) * 2ull * K);
+  w.bst = align256(w.row_e + sizeof(double) * 2ull * K * L);
   w.chunk = align256(w.bst + sizeof(BigRowState) * (size_t)(nbig * K));
   w.cand = align256(w.chunk + sizeof(uint32_t) * (size_t)kChunkWords * kRowPartChunks * parts);
   w.part_e = align256(w.cand + sizeof(uint64_t) * cands);
-  w.total = align256(w.part_e + sizeof(double) * 2ull * kRowPartWaves * parts);
+  w.err = align256(w.part_e + sizeof(double) * 2ull * kRowPartWaves * parts);
+  w.total = align256(w.err + sizeof(uint32_t) * K);
   return w;
 }
 
@@ -684,16 +685,17 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
   // runs during the main pass. The first layer's bracket runs on s, and only
   // then do the rows of the short layers start on the third stream beside
   // them: their workgroups fill whole compute units and would hold the small
-  // bracket kernels back. The long layers' energies go to an accumulator of
-  // their own when rows run beside them; both are summed once s has waited
-  // for everything.
+  // bracket kernels back. Every layer's energies go to a slot of their own,
+  // summed in layer order once s has waited for everything, so the order in
+  // which the long layers run does not change them.
   StreamSet* ss = any_long ? stream_set() : nullptr;
   if (any_long && !ss) return fail(SCADLES_EHIP, "could not create the layer pipeline streams");
   std::unique_lock<std::mutex> lk;
   if (ss) lk = std::unique_lock<std::mutex>(ss->rows_mu);
-  const bool both = ss && rc.Ls > 0;               // long and short layers: energies summed at the end
+  const bool both = ss && rc.Ls > 0;               // long and short layers
   const bool rows_beside = both && kRowsBeside;
-  double* e_long = both ? reinterpret_cast<double*>(base + lw.e_long) : energies;
+  // validation mode: the long layers' fatal error bits, ORed per device
+  uint32_t* err_acc = ss && g_validate.load() ? reinterpret_cast<uint32_t*>(base + lw.err) : nullptr;
 
   // Long layers: the multi-launch selection of each, its indices offset by the
   // layer's start, its energies added to those of the long layers before.
@@ -702,39 +704,57 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
     SelectPlan p;
     PrepArgs a;
   };
-  std::vector<LongLayer> longs;
-  uint64_t at[kMaxK] = {};          // where layer l's entries start in device j's output
-  for (uint32_t l = 0; l < L; ++l) {
-    const uint64_t off = seg_off[l], nl = seg_off[l + 1] - off;
-    if (nl <= row_max) {
-      for (uint32_t j = 0; j < K; ++j) at[j] += k_rule(nl, ratios[j]);
-      continue;
+  std::vector<uint32_t> order;                   // the long layers, in the order they run
+  std::vector<uint64_t> at((size_t)L * K);       // where layer l's entries start in device j's output
+  {
+    uint64_t run[kMaxK] = {};
+    for (uint32_t l = 0; l < L; ++l) {
+      const uint64_t nl = seg_off[l + 1] - seg_off[l];
+      for (uint32_t j = 0; j < K; ++j) {
+        at[(size_t)l * K + j] = run[j];
+        run[j] += k_rule(nl, ratios[j]);
+      }
+      if (nl > row_max) order.push_back(l);
     }
+  }
+  const int64_t lorder = g_layer_order.load();
+  if (lorder == 1 || lorder == 2)
+    std::stable_sort(order.begin(), order.end(), [&](uint32_t x, uint32_t y) {
+      const uint64_t nx = seg_off[x + 1] - seg_off[x], ny = seg_off[y + 1] - seg_off[y];
+      return lorder == 1 ? nx < ny : nx > ny;
+    });
+  std::vector<LongLayer> longs(order.size());
+  for (size_t q = 0; q < order.size(); ++q) {
+    const uint32_t l = order[q];
+    const uint64_t off = seg_off[l], nl = seg_off[l + 1] - off;
     Layout Ll;
     make_layout(K, nl, ratios, g_force_exact.load() != 0, true, Ll);
-    longs.emplace_back();
-    LongLayer& ll = longs.back();
+    LongLayer& ll = longs[q];
     PrepArgs& a = ll.a;
     memset(&a, 0, sizeof(a));
     for (uint32_t j = 0; j < K; ++j) {
       a.grad[j] = grads[j] + off;
-      a.idx[j] = idx[j] + at[j];
-      a.val[j] = val[j] + at[j];
+      a.idx[j] = idx[j] + at[(size_t)l * K + j];
+      a.val[j] = val[j] + at[(size_t)l * K + j];
       a.k[j] = Ll.k[j];
       a.cap[j] = Ll.cap[j];
       a.mode[j] = Ll.mode[j];
       a.r_lo[j] = Ll.r_lo[j];
       a.r_hi[j] = Ll.r_hi[j];
-      at[j] += Ll.k[j];
     }
-    const size_t region = (longs.size() - 1) % kLayerRegions;
-    select_setup(Ll, base + region * lw.sel, INFINITY, e_long, nullptr, nullptr, nullptr, (uint32_t)off,
-                 longs.size() > 1, ll.c, ll.p);
+    // the layer's energies go to its own slot of the per-layer energies
+    select_setup(Ll, base + (q % kLayerRegions) * lw.sel, INFINITY, energies ? rc.row_e + 2ull * l : nullptr,
+                 nullptr, nullptr, nullptr, (uint32_t)off, 2u * L, ll.c, ll.p);
     ll.p.parts = 1;
     ll.p.beside = 1;
+    ll.c.err_acc = err_acc;
   }
 
   hipError_t e = hipSuccess;
+  if (err_acc) {
+    e = launch_zero_words(err_acc, K, s);
+    if (e != hipSuccess) return hip_fail(e, "error word clear");
+  }
   if (ss) {
     // the library's streams start after the caller's earlier work on s (which may write the gradients)
     e = hipEventRecord(ss->fork, s);
@@ -753,7 +773,7 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
   }
   e = launch_put_table(table.data(), table.size(), reinterpret_cast<uint64_t*>(base + lw.table), sr);
   if (e != hipSuccess) return hip_fail(e, "layer table");
-  e = launch_rows(rc, rp, both ? nullptr : energies, sr);
+  e = launch_rows(rc, rp, any_long ? nullptr : energies, sr);
   if (e != hipSuccess) return hip_fail(e, "row selection");
   if (rows_beside) {
     e = hipEventRecord(ss->rows_done, sr);
@@ -794,9 +814,18 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
     e = hipStreamWaitEvent(s, ss->rows_done, 0);
     if (e != hipSuccess) return hip_fail(e, "row stream join");
   }
-  if (both && energies) {
-    e = launch_rows_energy(rc, energies, e_long, s);
+  if (any_long && energies) {
+    e = launch_rows_energy(rc, energies, s);
     if (e != hipSuccess) return hip_fail(e, "layer energies");
+  }
+  if (err_acc) {
+    uint32_t err[kMaxK];
+    e = hipMemcpyAsync(err, err_acc, sizeof(uint32_t) * K, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "selection state readback");
+    for (uint32_t j = 0; j < K; ++j)
+      if (err[j])
+        return fail(SCADLES_EINTERNAL, "device %u: a long layer's internal check failed (error bits 0x%x)", j, err[j]);
   }
   return SCADLES_OK;
 }
@@ -1184,6 +1213,10 @@ scadles_status scadles_set_option(const char* name, int64_t value)
   else if (!strcmp(name, "row_split")) {
     if (value < 0 || value > 0xFFFFFFFFll) return fail(SCADLES_EINVAL, "row_split must be in [0, 2^32 - 1]");
     g_row_split = value;
+  }
+  else if (!strcmp(name, "layer_order")) {
+    if (value < 0 || value > 2) return fail(SCADLES_EINVAL, "layer_order must be 0, 1 or 2");
+    g_layer_order = value;
   }
   else if (!strcmp(name, "parts")) {
     if (value < 1 || value > (int64_t)kMaxParts) return fail(SCADLES_EINVAL, "parts must be in [1, %u]", kMaxParts);

@@ -980,23 +980,18 @@ __global__ __launch_bounds__(64) void k_big_finish(RowsCtx rc)
 // Per device: the energies of its short layers (each lane a strided subset in
 // layer order, then the lanes in a fixed tree), plus those of the long layers
 // (`add`, when not null).
-__global__ __launch_bounds__(64) void k_rows_energy(RowsCtx rc, double* energies, const double* add)
+__global__ __launch_bounds__(64) void k_rows_energy(RowsCtx rc, double* energies)
 {
   // lane i adds layers i, i + 64, ... in order, then the lanes in a fixed tree
   const uint32_t j = blockIdx.x;
   double ea = 0.0, ek = 0.0;
   for (uint32_t l = threadIdx.x; l < rc.L; l += 64) {
-    if (rc.table[rc.L + 1 + l] == kNotShort) continue;
     ea += rc.row_e[2ull * ((uint64_t)j * rc.L + l)];
     ek += rc.row_e[2ull * ((uint64_t)j * rc.L + l) + 1];
   }
   ea = wave_sum_f64(ea);
   ek = wave_sum_f64(ek);
   if (threadIdx.x != 0) return;
-  if (add) {
-    ea += add[2 * j];
-    ek += add[2 * j + 1];
-  }
   energies[2 * j] = ea;
   energies[2 * j + 1] = ek;
 }
@@ -1050,13 +1045,26 @@ hipError_t launch_rows(const RowsCtx& rc, const RowsPrep& rp, double* energies, 
     k_big_finish<<<nb, 64, 0, s>>>(rc);
   }
   if (rc.Ls > rc.Lb) k_rows<<<(rc.Ls - rc.Lb) * rc.K, kRowBlock, 0, s>>>(rc);
-  if (rc.Ls > 0 && energies) k_rows_energy<<<rc.K, 64, 0, s>>>(rc, energies, nullptr);
+  if (rc.Ls > 0 && energies) k_rows_energy<<<rc.K, 64, 0, s>>>(rc, energies);
   return hipGetLastError();
 }
 
-hipError_t launch_rows_energy(const RowsCtx& rc, double* energies, const double* add, hipStream_t s)
+// Clears n words (a fill kernel rather than a memset node, so that the call
+// stays safe to capture in a graph).
+__global__ __launch_bounds__(256) void k_zero_words(uint32_t* p, uint32_t n)
 {
-  k_rows_energy<<<rc.K, 64, 0, s>>>(rc, energies, add);
+  for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0u;
+}
+
+hipError_t launch_zero_words(uint32_t* p, uint32_t n, hipStream_t s)
+{
+  k_zero_words<<<1, 256, 0, s>>>(p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_rows_energy(const RowsCtx& rc, double* energies, hipStream_t s)
+{
+  k_rows_energy<<<rc.K, 64, 0, s>>>(rc, energies);
   return hipGetLastError();
 }
 

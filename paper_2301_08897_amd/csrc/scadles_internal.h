@@ -127,7 +127,8 @@ struct Ctx {
   double ewma_beta;
   uint64_t* counters;     // [K][3] iterations compressed, iterations, floats sent; or null
   uint32_t idx_base;      // added to every output index (a layer's offset in the gradient)
-  uint32_t energies_add;  // 1: add the energies to energies_out (a layer after the first)
+  uint32_t e_stride;      // doubles between devices' energy pairs in energies_out (2: packed)
+  uint32_t* err_acc;      // [K] fatal error bits of every selection of a call ORed together, or null
   double delta;
 };
 
@@ -263,7 +264,7 @@ struct RowsCtx {
   const uint64_t* table;  // seg_off[0..L], then per layer its position among the short layers (or ~0),
                           // then part_pre[0..Lb], then cand_pre[0..Lb]
   RowDesc* rows;          // [Ls x K]: row q * K + j is device j's q-th short layer (longest first)
-  double* row_e;          // [K x L x 2]: E_all, E_kept of device j's layer l (short layers)
+  double* row_e;          // [K x L x 2]: E_all, E_kept of device j's layer l
   uint32_t K, L, Ls;
   // Split rows: the first Lb short layers (the longest). Part p of device j's
   // row of split layer q is workgroup part_pre[q] * K + j * (part_pre[q + 1] -
@@ -300,7 +301,8 @@ struct DecideArgs {
 hipError_t launch_layers_decide(const DecideArgs& a, hipStream_t s);
 hipError_t launch_rows(const RowsCtx& rc, const RowsPrep& rp, double* energies, hipStream_t s);
 // energies = the short layers' energies (layer order) + add (the long layers', or null)
-hipError_t launch_rows_energy(const RowsCtx& rc, double* energies, const double* add, hipStream_t s);
+hipError_t launch_rows_energy(const RowsCtx& rc, double* energies, hipStream_t s);
+hipError_t launch_zero_words(uint32_t* p, uint32_t n, hipStream_t s);
 
 // k = clamp(floor(ratio * n), 1, n), the same double arithmetic on host and device.
 __host__ __device__ inline uint64_t k_of(uint64_t n, double ratio)

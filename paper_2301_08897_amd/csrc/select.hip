@@ -1318,18 +1318,14 @@ __device__ inline void final_body(const Ctx& c, uint32_t jr)
   s.c_gt = tot & 0xFFFFFFFFull;
   s.need = need;
   if (s.c_gt + need != c.desc[j].k || (c.inject_count_error && j == 0)) s.err |= kErrCount;
+  if (c.err_acc && (s.err & kErrFatal)) atomicOr(c.err_acc + j, s.err & kErrFatal);
   s.e_kept = e_kept;
   // §IV: the rule compares the energies, optionally their moving averages
   s.sparse = adaptive_rule(s.e_all, e_kept, c.ewma ? c.ewma + 2 * (uint64_t)j : nullptr, c.ewma_beta, c.delta);
   if (c.counters) account(c.counters + 3 * (uint64_t)j, s.sparse, c.desc[j].k, c.n);
   if (c.energies_out) {
-    if (c.energies_add) {
-      c.energies_out[2 * j] += s.e_all;
-      c.energies_out[2 * j + 1] += e_kept;
-    } else {
-      c.energies_out[2 * j] = s.e_all;
-      c.energies_out[2 * j + 1] = e_kept;
-    }
+    c.energies_out[(uint64_t)c.e_stride * j] = s.e_all;
+    c.energies_out[(uint64_t)c.e_stride * j + 1] = e_kept;
   }
   if (c.compressed_out) c.compressed_out[j] = (uint8_t)s.sparse;
 }

@@ -26,6 +26,7 @@ ROW_MAXES = (ROW_MAX_DEFAULT, 0, 2**32 - 1)
 # test's largest row_max (with the default list, every layer a row).
 ROW_SPLIT_DEFAULT = 65536
 ROW_SPLITS = (1 << 18, 2**32 - 1)
+LAYER_ORDER_DEFAULT = 1
 
 
 @pytest.fixture(scope="module")
@@ -379,6 +380,92 @@ def test_fused_layers_sparse_sets(sc):
         assert same_bits(out.dense.cpu().numpy(), dense_o), f"call {rep}: aggregate"
         params = oracle.sgd(params, dense_o, lr)
         assert same_bits(p_dev.cpu().numpy(), params), f"call {rep}: update"
+
+
+def test_layer_order(sc):
+    """The long layers run in index order, by ascending or by descending
+    length: each writes its own part of the outputs and of the per-layer
+    energies, summed in layer order, so the kept sets, the energies (bit for
+    bit) and the fused step's aggregate and update do not change, and match
+    the oracle."""
+    torch, dev = torch_dev()
+    s = workloads.spec(5, n=2_000_003, K=3, iterations=1)
+    seg_off = [0] + [int(x) for x in s.seg_end]
+    row_max = 1 << 15
+    nlong = int(np.sum(np.diff(seg_off) > row_max))
+    log(f"layer order n={s.n} K={s.K} L={len(seg_off) - 1}, {nlong} long layers")
+    assert nlong >= 4
+    ratios = [0.01, 0.003, 0.05]
+    G = np.empty((s.K, s.n), dtype=np.float32)
+    for j in range(s.K):
+        workloads.gradient(s, 0, j, out=G[j], k=oracle.topk_k(s.n, ratios[j]))
+    ref = [oracle.topk_layers(G[j], seg_off, ratios[j]) for j in range(s.K)]
+    g_dev = torch.from_numpy(G).to(dev)
+    params = workloads.params0(s)
+    w, gamma = sc.stream_weights(s.rates[0], base_batch=s.base_batch)
+    lr = float(np.float32(s.eta * gamma))
+    dense_o = oracle.aggregate([(r[0], r[1]) for r in ref], w, s.n)
+    p_ref = oracle.sgd(params, dense_o, lr)
+    energies = []
+    for order in (0, 1, 2):
+        sc.set_option("layer_order", order)
+        sc.set_option("row_max", row_max)
+        try:
+            sel = sc.LayerSelect(g_dev, seg_off, ratios)
+            idx, val, en = sel.run()
+            p_dev = torch.from_numpy(params).to(dev)
+            step = sc.FusedStep(g_dev, ratios, params=p_dev, seg_off=seg_off)
+            out = step.run(w, lr)
+            torch.cuda.synchronize()
+        finally:
+            sc.set_option("layer_order", LAYER_ORDER_DEFAULT)
+            sc.set_option("row_max", ROW_MAX_DEFAULT)
+        e = en.cpu().numpy()
+        for j in range(s.K):
+            idx_o, val_o, _, _ = ref[j]
+            assert np.array_equal(idx[j].cpu().numpy(), idx_o), f"order {order} device {j}: indices"
+            assert same_bits(val[j].cpu().numpy(), val_o), f"order {order} device {j}: values"
+            assert np.array_equal(out.idx[j].cpu().numpy(), idx_o), f"order {order} device {j}: fused indices"
+            check_energies(f"order {order} device {j}", e[2 * j], e[2 * j + 1],
+                           oracle.energies_extended(G[j], idx_o), s.n, idx_o.size)
+        assert same_bits(out.energies.cpu().numpy(), e), f"order {order}: fused step's energies"
+        assert same_bits(out.dense.cpu().numpy(), dense_o), f"order {order}: aggregate"
+        assert same_bits(p_dev.cpu().numpy(), p_ref), f"order {order}: update"
+        energies.append(e)
+        del sel, step
+    for order in (1, 2):
+        assert same_bits(energies[order], energies[0]), f"order {order}: energies differ from index order"
+
+
+def test_layers_validation_of_long_layers(sc):
+    """With the validate option the per-layer calls read the long layers'
+    selection checks back: OK on good input, SCADLES_EINTERNAL (code 5) for
+    device 0 when the count check is made to fail; without the option the
+    same calls return OK."""
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(37)
+    n = 2_600_001
+    seg_off = [0, 120_000, 120_000 + (1 << 21) + 5_000, n]       # the middle layer is long
+    G = torch.from_numpy(rng.standard_normal((3, n)).astype(np.float32)).to(dev)
+    w, _ = sc.stream_weights([1.0, 2.0, 3.0])
+    log("per-layer validation of the long layers' selection state")
+    try:
+        sc.set_option("validate", 1)
+        sc.LayerSelect(G, seg_off, [0.01] * 3).run()
+        sc.FusedStep(G, [0.01] * 3, seg_off=seg_off).run(w)
+        sc.set_option("inject_count_error", 1)
+        with pytest.raises(sc.ScadlesError) as e1:
+            sc.LayerSelect(G, seg_off, [0.01] * 3).run()
+        assert e1.value.code == 5 and "device 0" in str(e1.value)
+        with pytest.raises(sc.ScadlesError) as e2:
+            sc.FusedStep(G, [0.01] * 3, seg_off=seg_off).run(w)
+        assert e2.value.code == 5
+        sc.set_option("validate", 0)
+        sc.LayerSelect(G, seg_off, [0.01] * 3).run()
+        torch.cuda.synchronize()
+    finally:
+        sc.set_option("inject_count_error", 0)
+        sc.set_option("validate", 0)
 
 
 def test_long_row_without_chunk_tallies(sc):
