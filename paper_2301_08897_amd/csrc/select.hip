@@ -678,56 +678,82 @@ __device__ inline uint64_t slot_pre(const Ctx& c, uint32_t j, uint32_t s)
 // windows at once; all without conditions: tile indices are clamped, region
 // positions wrap inside the region and band-list positions are clamped into
 // the tile's run, so every load is in bounds; keys past a tile's count are
-// ignored.
+// ignored. Sources of the staged tiles' keys (kSrc): kBandRegions, their
+// slot regions; kBandCopy, the same, also copying the keys to the band list
+// at the tiles' band offsets, which completes the list (the overflowed tiles'
+// keys are there already): the device's selection-interval keys, contiguous
+// and in index order; kBandList, that completed list (every tile's first
+// window then loads once its offset is known).
 constexpr int kBandTiles = 16;
+constexpr int kBandRegions = 0, kBandCopy = 1, kBandList = 2;
 
-template <class Visit, class Done>
+template <int kSrc = kBandRegions, class Visit, class Done>
 __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit visit, Done done)
 {
   constexpr uint32_t kMask = kSlotWords - 1u;
+  constexpr bool kCopy = kSrc == kBandCopy;
   const uint32_t l = lane_id();
   const uint32_t last = c.nslot - 1;
   const uint64_t row = (uint64_t)j * c.nslot;
   const GLOBAL uint32_t* reg = gptr(c.slot);
   uint32_t kv[kBandTiles];
+  if (kSrc != kBandList) {
 #pragma unroll
-  for (int i = 0; i < kBandTiles; ++i) {
-    const uint32_t ti = t0 + i < last ? t0 + i : last;
-    kv[i] = reg[(row + ti) * kSlotWords + l];
+    for (int i = 0; i < kBandTiles; ++i) {
+      const uint32_t ti = t0 + i < last ? t0 + i : last;
+      kv[i] = reg[(row + ti) * kSlotWords + l];
+    }
   }
   const uint32_t tl = t0 + l < last ? t0 + l : last;
   const uint32_t v = t0 + l < c.nslot ? c.slot_cnt[row + tl] : 0u;
   const uint32_t cand = v & 0x7FFFu, sure = v >> 16, nb = cand - sure;
   const uint32_t ovf = (v >> 15) & 1u;
-  uint32_t kb = 0;                                      // an overflowed tile's keys: band-list position
-  if (ovf) {
+  uint32_t kb = 0;                                      // the tile's keys: band-list position
+  if (ovf || kSrc != kBandRegions) {
     const uint64_t pre = slot_pre(c, j, tl);
     kb = (uint32_t)pre - (uint32_t)(pre >> 32);
   }
   const uint32_t nt = c.nslot - t0 < (uint32_t)kBandTiles ? c.nslot - t0 : (uint32_t)kBandTiles;
-  const GLOBAL uint32_t* blist = gptr(c.band) + c.desc[j].cand_off;
-  // windows e0 .. of a run of nbi keys, four at a time; key_at(e) is in bounds for every e
-  auto run = [&](uint32_t e0, uint32_t nbi, auto key_at) {
+  GLOBAL uint32_t* blist = gptr(c.band) + c.desc[j].cand_off;
+  if (kSrc == kBandList) {
+    // first windows: key l of tile i (loaded only where it exists)
+#pragma unroll
+    for (int i = 0; i < kBandTiles; ++i)
+      kv[i] = l < __builtin_amdgcn_readlane(nb, i) ? blist[__builtin_amdgcn_readlane(kb, i) + l] : 0u;
+  }
+  // windows e0 .. of a run of nbi keys, four at a time; key_at(e) is in bounds
+  // for every e; key e also goes to dst[e] when dst is set
+  auto run = [&](uint32_t e0, uint32_t nbi, auto key_at, GLOBAL uint32_t* dst) {
     for (uint32_t e = e0; e < nbi; e += 256) {
       uint32_t w4[4];
 #pragma unroll
       for (int m = 0; m < 4; ++m) w4[m] = key_at(e + m * 64 + l);
 #pragma unroll
       for (int m = 0; m < 4; ++m)
-        if (e + m * 64 < nbi) visit(w4[m], e + m * 64 + l < nbi);
+        if (e + m * 64 < nbi) {
+          const bool valid = e + m * 64 + l < nbi;
+          if (dst && valid) dst[e + m * 64 + l] = w4[m];
+          visit(w4[m], valid);
+        }
     }
   };
 #pragma unroll
   for (int i = 0; i < kBandTiles; ++i) {
     if ((uint32_t)i >= nt) break;
     const uint32_t nbi = __builtin_amdgcn_readlane(nb, i);
-    if (!__builtin_amdgcn_readlane(ovf, i)) {
+    if (kSrc == kBandList) {
+      visit(kv[i], l < nbi);
+      const GLOBAL uint32_t* p = blist + __builtin_amdgcn_readlane(kb, i);
+      if (nbi > 64u) run(64u, nbi, [&](uint32_t e) { return p[e < nbi ? e : nbi - 1u]; }, nullptr);
+    } else if (!__builtin_amdgcn_readlane(ovf, i)) {
+      GLOBAL uint32_t* dst = kCopy ? blist + __builtin_amdgcn_readlane(kb, i) : nullptr;
+      if (kCopy && l < nbi) dst[l] = kv[i];
       visit(kv[i], l < nbi);
       const GLOBAL uint32_t* base = reg + (row + t0 + i) * kSlotWords;
-      if (nbi > 64u) run(64u, nbi, [&](uint32_t e) { return base[e & kMask]; });
+      if (nbi > 64u) run(64u, nbi, [&](uint32_t e) { return base[e & kMask]; }, dst);
     } else if (nbi) {
       const GLOBAL uint32_t* p = blist + __builtin_amdgcn_readlane(kb, i);
-      run(0u, nbi, [&](uint32_t e) { return p[e < nbi ? e : nbi - 1u]; });
+      run(0u, nbi, [&](uint32_t e) { return p[e < nbi ? e : nbi - 1u]; }, nullptr);
     }
     done(i, __builtin_amdgcn_readlane(sure, i));
   }
@@ -836,8 +862,13 @@ __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_
 }
 
 // ---- 4. histogram pass over selection-interval keys (fast devices) and full data (exact devices)
-// Fast devices: workgroup b of device j takes tiles [b, b + 1) * kBandTiles * kWaves.
-__global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks)
+// Fast devices, first pass: workgroup b of device j takes tiles [b, b + 1) *
+// kBandTiles * kWaves, walking the tiles' keys and copying those of the
+// staged tiles to the band list, which then holds all of the device's keys;
+// later passes: workgroup b takes keys [b, b + 1) * kBandChunk of that list
+// (and every per_dev-th chunk after it).
+constexpr uint32_t kBandChunk = 16 * kBlock;
+__global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks, uint32_t pass)
 {
   __shared__ uint32_t h[kBins];
   if (blockIdx.x < ncand_blocks) {
@@ -848,18 +879,32 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
     if (s.fallback) return;
     const Sel sel = s.sel[kSlotCand];
     if (!sel.active) return;
+    const uint32_t nband = (uint32_t)(s.cand - s.sure);       // keys in [t_lo, t_hi): at most cap < 2^31
+    if (pass > 0 && (uint64_t)b * kBandChunk >= nband) return;
     for (int i = threadIdx.x; i < kBins; i += kBlock) h[i] = 0u;
     __syncthreads();
     const SelView sv = view_of(sel, true);
-    const uint32_t t0 = (b * kWaves + (threadIdx.x >> 6)) * kBandTiles;
-    if (t0 < c.nslot)
-      band_tiles(
-          c, j, t0,
-          [&](uint32_t key, bool valid) {
-            uint32_t dg;
-            if (valid && sel_digit(sv, key, dg)) atomicAdd(&h[dg], 1u);
-          },
-          [](uint32_t, uint32_t) {});
+    auto add = [&](uint32_t key, bool valid) {
+      uint32_t dg;
+      if (valid && sel_digit(sv, key, dg)) atomicAdd(&h[dg], 1u);
+    };
+    if (pass == 0) {
+      const uint32_t t0 = (b * kWaves + (threadIdx.x >> 6)) * kBandTiles;
+      if (t0 < c.nslot) band_tiles<kBandCopy>(c, j, t0, add, [](uint32_t, uint32_t) {});
+    } else {
+      const GLOBAL uint32_t* blist = gptr(c.band) + c.desc[j].cand_off;
+      for (uint64_t o = (uint64_t)b * kBandChunk; o < nband; o += (uint64_t)per_dev * kBandChunk) {
+        uint32_t key[kBandChunk / kBlock];
+#pragma unroll
+        for (int r = 0; r < (int)(kBandChunk / kBlock); ++r) {
+          const uint64_t e = o + (uint64_t)r * kBlock + threadIdx.x;
+          key[r] = e < nband ? blist[e] : 0u;
+        }
+#pragma unroll
+        for (int r = 0; r < (int)(kBandChunk / kBlock); ++r)
+          add(key[r], o + (uint64_t)r * kBlock + threadIdx.x < nband);
+      }
+    }
     __syncthreads();
     flush_hist(h, c.hist + ((uint64_t)j * kSlots + kSlotCand) * kBins, kBins);
     return;
@@ -934,7 +979,8 @@ __device__ inline void grp_count_body(const Ctx& c, uint32_t b)
   const uint32_t l = lane_id();
   uint32_t gt = 0, eq = 0;
   uint64_t mine = 0;
-  band_tiles(
+  // the first histogram pass completed the band list
+  band_tiles<kBandList>(
       c, j, t0,
       [&](uint32_t key, bool valid) {
         gt += (uint32_t)__builtin_popcountll(ballot(valid && key > thr));
@@ -1390,7 +1436,7 @@ static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s, int ha
     const uint32_t ncand = p.any_fast ? band_blocks : 0u;
     if (p.any_fast) k_overflow<<<c.jn * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
     for (int pass = 0; pass < 3; ++pass) {
-      k_hist_cf<<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand);
+      k_hist_cf<<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand, (uint32_t)pass);
       k_find<<<c.jn, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1, 0);
     }
     k_count<<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand);
