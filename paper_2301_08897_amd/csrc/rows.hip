@@ -977,9 +977,8 @@ __global__ __launch_bounds__(64) void k_big_finish(RowsCtx rc)
   if (threadIdx.x == 0) rc.row_e[2ull * rc.rows[b].eslot + 1] = ek;
 }
 
-// Per device: the energies of its short layers (each lane a strided subset in
-// layer order, then the lanes in a fixed tree), plus those of the long layers
-// (`add`, when not null).
+// Per device: the energies of all its layers, short and long (each lane a
+// strided subset in layer order, then the lanes in a fixed tree).
 __global__ __launch_bounds__(64) void k_rows_energy(RowsCtx rc, double* energies)
 {
   // lane i adds layers i, i + 64, ... in order, then the lanes in a fixed tree
