@@ -111,6 +111,11 @@ def test_host_validation_before_any_launch(sc):
                           4096, 64, None) == E["ws"]
     assert sc._set_option(b"no_such_option", 1) == E["inval"]
     assert b"no_such_option" in sc._last_error()
+    # the per-layer order of the long layers: 0, 1 (default) or 2
+    assert sc._set_option(b"layer_order", 3) == E["inval"]
+    assert sc._set_option(b"layer_order", -1) == E["inval"]
+    for v in (0, 2, 1):
+        assert sc._set_option(b"layer_order", v) == 0
 
 
 def test_momentum_validation_before_any_launch(sc):
