@@ -698,34 +698,38 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
   uint32_t* err_acc = ss && g_validate.load() ? reinterpret_cast<uint32_t*>(base + lw.err) : nullptr;
 
   // Long layers: the multi-launch selection of each, its indices offset by the
-  // layer's start, its energies added to those of the long layers before.
+  // layer's start, its energies in the layer's own slot.
   struct LongLayer {
     Ctx c;
     SelectPlan p;
     PrepArgs a;
   };
-  std::vector<uint32_t> order;                   // the long layers, in the order they run
-  std::vector<uint64_t> at((size_t)L * K);       // where layer l's entries start in device j's output
+  // the long layers in index order (layer[i]) with where their entries start
+  // in each device's output (at[i * K + j]), then the order they run in
+  std::vector<uint32_t> layer;
+  std::vector<uint64_t> at;
   {
     uint64_t run[kMaxK] = {};
     for (uint32_t l = 0; l < L; ++l) {
       const uint64_t nl = seg_off[l + 1] - seg_off[l];
-      for (uint32_t j = 0; j < K; ++j) {
-        at[(size_t)l * K + j] = run[j];
-        run[j] += k_rule(nl, ratios[j]);
+      if (nl > row_max) {
+        layer.push_back(l);
+        at.insert(at.end(), run, run + K);
       }
-      if (nl > row_max) order.push_back(l);
+      for (uint32_t j = 0; j < K; ++j) run[j] += k_rule(nl, ratios[j]);
     }
   }
+  std::vector<uint32_t> order(layer.size());
+  for (size_t i = 0; i < order.size(); ++i) order[i] = (uint32_t)i;
   const int64_t lorder = g_layer_order.load();
   if (lorder == 1 || lorder == 2)
     std::stable_sort(order.begin(), order.end(), [&](uint32_t x, uint32_t y) {
-      const uint64_t nx = seg_off[x + 1] - seg_off[x], ny = seg_off[y + 1] - seg_off[y];
+      const uint64_t nx = seg_off[layer[x] + 1] - seg_off[layer[x]], ny = seg_off[layer[y] + 1] - seg_off[layer[y]];
       return lorder == 1 ? nx < ny : nx > ny;
     });
   std::vector<LongLayer> longs(order.size());
   for (size_t q = 0; q < order.size(); ++q) {
-    const uint32_t l = order[q];
+    const uint32_t i = order[q], l = layer[i];
     const uint64_t off = seg_off[l], nl = seg_off[l + 1] - off;
     Layout Ll;
     make_layout(K, nl, ratios, g_force_exact.load() != 0, true, Ll);
@@ -734,8 +738,8 @@ static scadles_status run_layers(const float* const* grads, uint32_t K, const ui
     memset(&a, 0, sizeof(a));
     for (uint32_t j = 0; j < K; ++j) {
       a.grad[j] = grads[j] + off;
-      a.idx[j] = idx[j] + at[(size_t)l * K + j];
-      a.val[j] = val[j] + at[(size_t)l * K + j];
+      a.idx[j] = idx[j] + at[(size_t)i * K + j];
+      a.val[j] = val[j] + at[(size_t)i * K + j];
       a.k[j] = Ll.k[j];
       a.cap[j] = Ll.cap[j];
       a.mode[j] = Ll.mode[j];
