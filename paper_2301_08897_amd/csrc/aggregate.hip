@@ -241,14 +241,17 @@ __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
   }
 
   // Round once to float; optionally the SGD update of Eqn 4c (or momentum SGD
-  // with weight decay) on the float aggregate.
+  // with weight decay) on the float aggregate. The aggregate goes out with
+  // nontemporal stores: nothing here reads it again (0.03 ms less per step at
+  // the largest workload than plain stores; the parameters' plain stores are
+  // faster than nontemporal ones).
   const double nlr = -(double)c.lr, mom = (double)c.mom, wd = (double)c.wd;
   if (pre) {
 #pragma unroll
     for (int m = 0; m < kARange / 256; ++m) {
       const uint32_t e = m * 256 + l * 4;
       const f4 g = {(float)acc[e], (float)acc[e + 1], (float)acc[e + 2], (float)acc[e + 3]};
-      *reinterpret_cast<f4*>(c.out + base + e) = g;
+      __builtin_nontemporal_store(g, reinterpret_cast<f4*>(c.out + base + e));
       f4 p = pp[m];
       if (c.mbuf) {
         f4 v = vv[m];
@@ -273,18 +276,18 @@ __global__ __launch_bounds__(64) void k_aggregate(AggArgs a, AggCtx c)
   for (uint32_t e = l * 4; e < len; e += 256) {
     if (e + 4 <= len) {
       const f4 g = {(float)acc[e], (float)acc[e + 1], (float)acc[e + 2], (float)acc[e + 3]};
-      *reinterpret_cast<f4*>(c.out + base + e) = g;
+      __builtin_nontemporal_store(g, reinterpret_cast<f4*>(c.out + base + e));
       if (c.params) {
         f4 p = *reinterpret_cast<const f4*>(c.params + base + e);
         if (c.mbuf) {
           f4 v = *reinterpret_cast<const f4*>(c.mbuf + base + e);
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-          float pq = p[q], vq = v[q];
-          momentum_step(pq, vq, g[q], nlr, mom, wd);
-          p[q] = pq;
-          v[q] = vq;
-        }
+            float pq = p[q], vq = v[q];
+            momentum_step(pq, vq, g[q], nlr, mom, wd);
+            p[q] = pq;
+            v[q] = vq;
+          }
           *reinterpret_cast<f4*>(c.mbuf + base + e) = v;
         } else {
           p.x = (float)__builtin_fma(nlr, (double)g.x, (double)p.x);
