@@ -507,7 +507,20 @@ def test_device_count_extremes(sc, K):
     G = (rng.standard_normal((K, seg_off[-1])) * rng.uniform(0.01, 3.0, (K, 1))).astype(np.float32)
     ratios = list(rng.choice([0.001, 0.01, 0.1, 0.5], size=K))
     log(f"layers with K={K}")
-    layers_vs_oracle(sc, G, seg_off, ratios, f"K={K}", topk=oracle.topk_layers_by_threshold, check_aggregate=True)
+    ref = layers_vs_oracle(sc, G, seg_off, ratios, f"K={K}", topk=oracle.topk_layers_by_threshold,
+                           check_aggregate=True)
+    # the fused per-layer step (its own range markers, Eqn 4b, Eqn 4c) at this K
+    torch, dev = torch_dev()
+    n = seg_off[-1]
+    params = rng.standard_normal(n).astype(np.float32)
+    p_dev = torch.from_numpy(params).to(dev)
+    w, _ = sc.stream_weights(np.arange(1.0, K + 1.0))
+    lr = float(np.float32(0.05))
+    out = sc.FusedStep(torch.from_numpy(G).to(dev), ratios, params=p_dev, seg_off=seg_off).run(w, lr)
+    torch.cuda.synchronize()
+    dense_o = oracle.aggregate([(r[0], r[1]) for r in ref], w, n)
+    assert same_bits(out.dense.cpu().numpy(), dense_o), f"K={K}: fused per-layer aggregate"
+    assert same_bits(p_dev.cpu().numpy(), oracle.sgd(params, dense_o, lr)), f"K={K}: fused per-layer update"
 
 
 def test_concurrent_callers(sc):
