@@ -670,7 +670,7 @@ __device__ inline uint64_t slot_pre(const Ctx& c, uint32_t j, uint32_t s)
 // The keys of a tile's candidates below t_hi (the selection interval [t_lo,
 // t_hi)) start its slot region; k_overflow writes those of an overflowed tile
 // to the device's band list at the tile's band offset (candidates - sure keys
-// before it). band_tiles walks them for tiles t0 .. t0 + kBandTiles - 1 of
+// before it). band_tiles walks them for tiles t0 .. t0 + kBT - 1 of
 // device j, tile after tile, in index order within a tile, 64 at a time:
 // visit(key, valid) takes one window, done(i, sure) closes tile t0 + i (sure:
 // its keys >= t_hi). The first window of every tile is loaded at once, before
@@ -683,11 +683,11 @@ __device__ inline uint64_t slot_pre(const Ctx& c, uint32_t j, uint32_t s)
 // at the tiles' band offsets, which completes the list (the overflowed tiles'
 // keys are there already): the device's selection-interval keys, contiguous
 // and in index order; kBandList, that completed list (every tile's first
-// window then loads once its offset is known).
-constexpr int kBandTiles = 16;
+// window then loads once its offset is known). kBT, the tiles per wave, is
+// chosen per call (band_tiles_per_wave).
 constexpr int kBandRegions = 0, kBandCopy = 1, kBandList = 2;
 
-template <int kSrc = kBandRegions, class Visit, class Done>
+template <int kBT, int kSrc = kBandRegions, class Visit, class Done>
 __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit visit, Done done)
 {
   constexpr uint32_t kMask = kSlotWords - 1u;
@@ -696,10 +696,10 @@ __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit v
   const uint32_t last = c.nslot - 1;
   const uint64_t row = (uint64_t)j * c.nslot;
   const GLOBAL uint32_t* reg = gptr(c.slot);
-  uint32_t kv[kBandTiles];
+  uint32_t kv[kBT];
   if (kSrc != kBandList) {
 #pragma unroll
-    for (int i = 0; i < kBandTiles; ++i) {
+    for (int i = 0; i < kBT; ++i) {
       const uint32_t ti = t0 + i < last ? t0 + i : last;
       kv[i] = reg[(row + ti) * kSlotWords + l];
     }
@@ -713,12 +713,12 @@ __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit v
     const uint64_t pre = slot_pre(c, j, tl);
     kb = (uint32_t)pre - (uint32_t)(pre >> 32);
   }
-  const uint32_t nt = c.nslot - t0 < (uint32_t)kBandTiles ? c.nslot - t0 : (uint32_t)kBandTiles;
+  const uint32_t nt = c.nslot - t0 < (uint32_t)kBT ? c.nslot - t0 : (uint32_t)kBT;
   GLOBAL uint32_t* blist = gptr(c.band) + c.desc[j].cand_off;
   if (kSrc == kBandList) {
     // first windows: key l of tile i (loaded only where it exists)
 #pragma unroll
-    for (int i = 0; i < kBandTiles; ++i)
+    for (int i = 0; i < kBT; ++i)
       kv[i] = l < __builtin_amdgcn_readlane(nb, i) ? blist[__builtin_amdgcn_readlane(kb, i) + l] : 0u;
   }
   // windows e0 .. of a run of nbi keys, four at a time; key_at(e) is in bounds
@@ -738,7 +738,7 @@ __device__ inline void band_tiles(const Ctx& c, uint32_t j, uint32_t t0, Visit v
     }
   };
 #pragma unroll
-  for (int i = 0; i < kBandTiles; ++i) {
+  for (int i = 0; i < kBT; ++i) {
     if ((uint32_t)i >= nt) break;
     const uint32_t nbi = __builtin_amdgcn_readlane(nb, i);
     if (kSrc == kBandList) {
@@ -863,16 +863,17 @@ __global__ __launch_bounds__(kBlock) void k_overflow(Ctx c, uint32_t blocks_per_
 
 // ---- 4. histogram pass over selection-interval keys (fast devices) and full data (exact devices)
 // Fast devices, first pass: workgroup b of device j takes tiles [b, b + 1) *
-// kBandTiles * kWaves, walking the tiles' keys and copying those of the
+// kBT * kWaves, walking the tiles' keys and copying those of the
 // staged tiles to the band list, which then holds all of the device's keys;
 // later passes: workgroup b takes keys [b, b + 1) * kBandChunk of that list
 // (and every per_dev-th chunk after it).
 constexpr uint32_t kBandChunk = 16 * kBlock;
+template <int kBT>
 __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks, uint32_t pass)
 {
   __shared__ uint32_t h[kBins];
   if (blockIdx.x < ncand_blocks) {
-    const uint32_t per_dev = (c.nslot + kBandTiles * kWaves - 1) / (kBandTiles * kWaves);
+    const uint32_t per_dev = (c.nslot + kBT * kWaves - 1) / (kBT * kWaves);
     const uint32_t jr = blockIdx.x / per_dev, b = blockIdx.x - jr * per_dev;
     const uint32_t j = c.j0 + jr;
     const DevState& s = c.st[j];
@@ -889,8 +890,8 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
       if (valid && sel_digit(sv, key, dg)) atomicAdd(&h[dg], 1u);
     };
     if (pass == 0) {
-      const uint32_t t0 = (b * kWaves + (threadIdx.x >> 6)) * kBandTiles;
-      if (t0 < c.nslot) band_tiles<kBandCopy>(c, j, t0, add, [](uint32_t, uint32_t) {});
+      const uint32_t t0 = (b * kWaves + (threadIdx.x >> 6)) * kBT;
+      if (t0 < c.nslot) band_tiles<kBT, kBandCopy>(c, j, t0, add, [](uint32_t, uint32_t) {});
     } else {
       const GLOBAL uint32_t* blist = gptr(c.band) + c.desc[j].cand_off;
       for (uint64_t o = (uint64_t)b * kBandChunk; o < nband; o += (uint64_t)per_dev * kBandChunk) {
@@ -963,16 +964,17 @@ __global__ __launch_bounds__(kBlock) void k_hist_cf(Ctx c, uint32_t ncand_blocks
 // Per group: keys above the threshold | keys equal to it << 32. The threshold
 // lies in [t_lo, t_hi): equal keys and the keys above it below t_hi are
 // counted on the tiles' selection-interval keys, the keys >= t_hi come from
-// the slot counts. One wave per kBandTiles tiles (kBandTiles / 2 groups).
+// the slot counts. One wave per kBT tiles (kBT / 2 groups).
+template <int kBT>
 __device__ inline void grp_count_body(const Ctx& c, uint32_t b)
 {
-  const uint32_t per_dev = (c.nslot + kBandTiles * kWaves - 1) / (kBandTiles * kWaves);
+  const uint32_t per_dev = (c.nslot + kBT * kWaves - 1) / (kBT * kWaves);
   const uint32_t jr = b / per_dev;
   const uint32_t j = c.j0 + jr;
-  const uint32_t t0 = ((b - jr * per_dev) * kWaves + (threadIdx.x >> 6)) * kBandTiles;
+  const uint32_t t0 = ((b - jr * per_dev) * kWaves + (threadIdx.x >> 6)) * kBT;
   const DevState& st = c.st[j];
   if (st.fallback || t0 >= c.nslot) return;
-  static_assert(kGatherSlots == 2 && kBandTiles % 2 == 0, "groups are tile pairs");
+  static_assert(kGatherSlots == 2 && kBT % 2 == 0 && kBT <= 64, "groups are tile pairs; a lane holds a tile's counts");
   uint32_t thr;
   uint64_t need;
   threshold_of(st, thr, need);
@@ -980,7 +982,7 @@ __device__ inline void grp_count_body(const Ctx& c, uint32_t b)
   uint32_t gt = 0, eq = 0;
   uint64_t mine = 0;
   // the first histogram pass completed the band list
-  band_tiles<kBandList>(
+  band_tiles<kBT, kBandList>(
       c, j, t0,
       [&](uint32_t key, bool valid) {
         gt += (uint32_t)__builtin_popcountll(ballot(valid && key > thr));
@@ -994,7 +996,7 @@ __device__ inline void grp_count_body(const Ctx& c, uint32_t b)
         }
       });
   const uint32_t g = t0 / 2 + l;
-  if (l < (uint32_t)kBandTiles / 2 && g < c.ngrp) c.grp_cnt[(uint64_t)j * c.ngrp + g] = mine;
+  if (l < (uint32_t)kBT / 2 && g < c.ngrp) c.grp_cnt[(uint64_t)j * c.ngrp + g] = mine;
 }
 
 // Exclusive prefix of nb packed counts, one workgroup.
@@ -1382,9 +1384,10 @@ __device__ inline void final_body(const Ctx& c, uint32_t jr)
 // device fell back). In the fused step the output pass of a fast device also
 // writes its aggregation range markers; the decision launch's extra blocks
 // build those of exact-path devices.
+template <int kBT>
 __global__ __launch_bounds__(kBlock) void k_count(Ctx c, uint32_t nfast)
 {
-  if (blockIdx.x < nfast) grp_count_body(c, blockIdx.x);
+  if (blockIdx.x < nfast) grp_count_body<kBT>(c, blockIdx.x);
   else count_cf_body(c, blockIdx.x - nfast, gridDim.x - nfast);
 }
 
@@ -1427,19 +1430,45 @@ __global__ __launch_bounds__(kBlock) void k_final(Ctx c, uint32_t lb_blocks)
 // radix passes, group counts and offsets), latency-bound and light on memory;
 // 1, the output (ordered compaction with the range markers, energies and decision),
 // which moves most of the bytes.
+// Tiles per wave of the walks over the tiles' selection-interval keys (the
+// first radix pass and the group counts): the most, up to 16, that still
+// give 6000 waves over the devices of the launch, else 4. Few tiles per wave
+// keep small launches wide; many keep large ones from flushing a histogram
+// per few tiles (16 / 8 / 4: 3.83 / 3.84 / 3.89 ms per step at 32 x 143.7M,
+// 0.737 / 0.707 / 0.692 at 16 x 25.6M, 0.276 / 0.263 / 0.256 at 8 x 11.2M).
+// Beside another launch's main pass (a layer of the per-layer selection)
+// always 16: fewer workgroups wait less for the slots that pass leaves.
+static int band_tiles_per_wave(const Ctx& c, const SelectPlan& p)
+{
+  if (p.beside) return 16;
+  const uint64_t tiles = (uint64_t)c.jn * c.nslot;
+  if (tiles / 16 >= 6000) return 16;
+  if (tiles / 8 >= 6000) return 8;
+  return 4;
+}
+
+template <int kBT>
+static void launch_band_passes(const Ctx& c, const SelectPlan& p, hipStream_t s)
+{
+  const uint32_t ncand = p.any_fast ? c.jn * ((c.nslot + kBT * kWaves - 1) / (kBT * kWaves)) : 0u;
+  for (int pass = 0; pass < 3; ++pass) {
+    k_hist_cf<kBT><<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand, (uint32_t)pass);
+    k_find<<<c.jn, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1, 0);
+  }
+  k_count<kBT><<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand);
+}
+
 static void launch_post(const Ctx& c, const SelectPlan& p, hipStream_t s, int half)
 {
-  const uint32_t band_blocks = c.jn * ((c.nslot + kBandTiles * kWaves - 1) / (kBandTiles * kWaves));
   if (half == 0) {
     if (p.beside) k_scan<kScanBlockSmall><<<c.jn, kScanBlockSmall, 0, s>>>(c);
     else k_scan<kScanBlockLarge><<<c.jn, kScanBlockLarge, 0, s>>>(c);
-    const uint32_t ncand = p.any_fast ? band_blocks : 0u;
     if (p.any_fast) k_overflow<<<c.jn * kOverflowBlocks, kBlock, 0, s>>>(c, kOverflowBlocks);
-    for (int pass = 0; pass < 3; ++pass) {
-      k_hist_cf<<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand, (uint32_t)pass);
-      k_find<<<c.jn, 64, 0, s>>>(c, kSlotCand, kSlotFull + 1, 0);
+    switch (band_tiles_per_wave(c, p)) {
+      case 16: launch_band_passes<16>(c, p, s); break;
+      case 8: launch_band_passes<8>(c, p, s); break;
+      default: launch_band_passes<4>(c, p, s); break;
     }
-    k_count<<<ncand + p.full_workers, kBlock, 0, s>>>(c, ncand);
     k_offsets<<<(p.any_fast ? 2 : 1) * c.jn, kBlock, 0, s>>>(c, p.any_fast);
     return;
   }
